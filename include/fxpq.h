@@ -1,0 +1,260 @@
+/*
+ * fxpq.h -- C ABI of libfxpq, the MI355X (gfx950) hot path of FxP-QNet's
+ * post-training quantizer (Shawahna et al., "FxP-QNet: A Post-Training
+ * Quantizer for the Design of Mixed Low-Precision DNNs with Dynamic Fixed-Point
+ * Representation", IEEE Access 2022).
+ *
+ * The hot path is the calibration forward under dynamic fixed-point (DFX)
+ * quantization: quantize a tensor (Eq. 10-12), search its fractional length
+ * by the data-structure error (Eq. 14), run each integer C-Block (conv/FC +
+ * bias + Scale + ReLU, Sec. "Integer-Only Inference") and requantize its
+ * output in the FxP-QLayer (Sec. "FxP-QLayer").
+ *
+ * Conventions shared by every call:
+ *  - A k-bit code X with fractional length fl stands for X * 2^-fl (Eq. 1).
+ *    Signed codes lie in [-2^(k-1), 2^(k-1)-1], unsigned in [0, 2^k-1] (Eq. 12).
+ *  - All tensor pointers are caller-owned DEVICE memory on the handle's device;
+ *    the library never frees them.  Scalars that later kernels consume (chosen
+ *    formats, value scales, min/max) also live in device memory, so a whole
+ *    calibration forward runs without a host round trip.
+ *  - Every call is asynchronous on the handle's stream.  Argument errors that
+ *    the host can see are returned at once and nothing is launched.  Conditions
+ *    only the device can see (non-finite input, a value outside the exact
+ *    range) set sticky flags that fxpq_sync_status() returns.
+ *  - A handle owns its scratch memory (allocated once in fxpq_create); calls do
+ *    not allocate.  A handle is not thread-safe: use one per host thread.
+ *  - Code dtype FXPQ_U8OFF stores an unsigned 8-bit code u as the signed byte
+ *    u - 128 (bit pattern u ^ 0x80), so that it feeds the signed int8 matrix
+ *    cores; every call that reads it adds the 128 back exactly.  FXPQ_C8 lets
+ *    the device pick I8 or U8OFF from the sign of the format it was written
+ *    with; a call reading FXPQ_C8 codes needs that format (device pointer).
+ */
+#ifndef FXPQ_H
+#define FXPQ_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FXPQ_OK = 0,
+  FXPQ_ERR_INVALID_ARG = 1, /* null pointer, bad size, bad word length, ... */
+  FXPQ_ERR_UNSUPPORTED = 2, /* a valid combination this build does not implement */
+  FXPQ_ERR_NONFINITE = 3,   /* reported through fxpq_sync_status flags */
+  FXPQ_ERR_OVERFLOW = 4,    /* int32 accumulator could overflow for this shape */
+  FXPQ_ERR_HIP = 5,         /* a HIP runtime call failed */
+  FXPQ_ERR_ALLOC = 6        /* fxpq_create could not allocate its scratch */
+} fxpq_status;
+
+typedef enum {
+  FXPQ_I8 = 0,    /* signed 8-bit codes */
+  FXPQ_U8OFF = 1, /* unsigned 8-bit codes stored as u - 128 */
+  FXPQ_I16 = 2,
+  FXPQ_I32 = 3,
+  FXPQ_I64 = 4,
+  FXPQ_F32 = 5,
+  FXPQ_C8 = 6     /* 8-bit code whose storage follows the device format: I8 when
+                     the format is signed, U8OFF when it is unsigned */
+} fxpq_dtype;
+
+#define FXPQ_SIGN_AUTO (-1) /* Eq. 6: signed iff the smallest value is negative */
+
+/* Sticky device flags returned by fxpq_sync_status. */
+#define FXPQ_FLAG_NONFINITE 0x1u /* NaN or Inf in an fp32 input */
+#define FXPQ_FLAG_RANGE 0x2u     /* a value left the exactly handled range (see fxpq_fl_search) */
+#define FXPQ_FLAG_CODE 0x4u      /* a code did not fit the requested code dtype */
+
+/*
+ * A DFX format in device memory: word length k, fractional length fl, sign
+ * strategy (0 unsigned, 1 signed).  status is 0 when the format is valid;
+ * fxpq_fl_search writes a nonzero status when it could not choose one.
+ */
+typedef struct {
+  int32_t wl;
+  int32_t fl;
+  int32_t sign;
+  int32_t status;
+} fxpq_fmt;
+
+/*
+ * Integer C-Block epilogue (Sec. "Integer-Only Inference", text under Fig.
+ * "FxP-QNet hardware").  The accumulator of a conv/FC with input codes at
+ * fractional length fl_in (read from d_fmt_in on the device) and weights at
+ * fl_w has scale s = fl_in + fl_w.  The C-Block value is, per output channel c:
+ *     v = acc                                   (scale s)
+ *     v = v + bias[c]        if bias            both aligned to max(s, fl_bias)
+ *     v = v * scale[c]       if scale           scale += fl_scale (BN->Scale, Eq. 4-5)
+ *     v = v + shift[c]       if shift           both aligned to max(., fl_shift)
+ *     v = max(v, 0)          if relu
+ * Alignment is an exact left shift of the coarser operand, so v is the exact
+ * value of the C-Block; only the following FxP-QLayer rounds.  bias, scale and
+ * shift are per-channel integer codes (device, int64) or NULL.  `channels` is
+ * the number of output channels, the innermost dimension of the accumulators.
+ */
+typedef struct {
+  int32_t channels;
+  int32_t fl_w;
+  const fxpq_fmt* d_fmt_in;
+  const int64_t* bias;
+  int32_t fl_bias;
+  int32_t relu;
+  const int64_t* scale;
+  int32_t fl_scale;
+  int32_t pad0;
+  const int64_t* shift;
+  int32_t fl_shift;
+  int32_t pad1;
+} fxpq_epilogue;
+
+/*
+ * The values an FxP-QLayer quantizes (Sec. "FxP-QLayer"), described without
+ * materializing them:
+ *   FXPQ_SRC_F32  x is float[n]; the values are x.
+ *   FXPQ_SRC_INT  x is int32[n] (dtype FXPQ_I32) or int64[n] (FXPQ_I64); the
+ *                 values are x * 2^-s with s read from d_scale (device int32).
+ *   FXPQ_SRC_ACC  x is int32[n] conv/FC accumulators laid out [rows][channels];
+ *                 the values are the C-Block epilogue `ep` applied to them.
+ *   FXPQ_SRC_ADD  Eltwise C-Block: x and x2 are code tensors (dtype / dtype2 in
+ *                 {FXPQ_I8, FXPQ_U8OFF}) in the formats d_fmt_a / d_fmt_b; the
+ *                 values are a + b, aligned to the finer fractional length,
+ *                 followed by ReLU when relu != 0.
+ * d_minmax (nullable) is a device double[2] holding the exact min and max of
+ * the values when the caller already has them (fxpq_qconv writes it); when
+ * NULL the library computes it.
+ */
+typedef enum { FXPQ_SRC_F32 = 0, FXPQ_SRC_INT = 1, FXPQ_SRC_ACC = 2, FXPQ_SRC_ADD = 3 } fxpq_src_kind;
+
+typedef struct {
+  int32_t kind;
+  int32_t dtype;
+  const void* x;
+  const void* x2;
+  int32_t dtype2;
+  int32_t relu;
+  const int32_t* d_scale;
+  const fxpq_fmt* d_fmt_a;
+  const fxpq_fmt* d_fmt_b;
+  const fxpq_epilogue* ep;
+  const double* d_minmax;
+} fxpq_src;
+
+/* Convolution shape: input NHWC codes, weights KRSC int8 codes, output NHWK. */
+typedef struct {
+  int32_t n, h, w, c; /* input batch, height, width, channels */
+  int32_t k, r, s;    /* output channels, kernel height, kernel width */
+  int32_t stride, pad;
+} fxpq_conv_desc;
+
+typedef struct fxpq_handle_s* fxpq_handle;
+
+/* ---- handle and status --------------------------------------------------- */
+
+/* Creates a handle on HIP device `device` using the default stream. */
+fxpq_status fxpq_create(fxpq_handle* h, int device);
+fxpq_status fxpq_destroy(fxpq_handle h);
+/* Sets the stream (a hipStream_t, NULL = default stream) for later calls. */
+fxpq_status fxpq_set_stream(fxpq_handle h, void* hip_stream);
+const char* fxpq_status_string(fxpq_status s);
+/* Waits for the handle's stream, returns and clears the sticky FXPQ_FLAG_* bits. */
+fxpq_status fxpq_sync_status(fxpq_handle h, uint32_t* flags);
+
+/* ---- hot path -------------------------------------------------------------- */
+
+/*
+ * Quantize (Eq. 10-12): codes[i] = clip(rne(x[i] * 2^fl), Qmin, Qmax) with the
+ * format read from d_fmt (device).  rne rounds half to even.  code_type is
+ * FXPQ_I8, FXPQ_U8OFF (unsigned 8-bit formats only), FXPQ_I16 or FXPQ_I32 and
+ * must hold the format's code range.  n >= 0; n == 0 launches nothing.
+ * Word lengths 2..32 (the 1-bit binary rule of Eq. 13 returns UNSUPPORTED).
+ */
+fxpq_status fxpq_quantize(fxpq_handle h, const float* x, int64_t n, const fxpq_fmt* d_fmt,
+                          void* codes, fxpq_dtype code_type);
+
+/*
+ * FxP-QLayer requantization (Sec. "FxP-QLayer"; Eq. 10-12 applied to the exact
+ * C-Block values): codes[i] = clip(rne(v[i] * 2^fl), Qmin, Qmax) for the values
+ * v described by src and the format in d_fmt.  Computed exactly: the result is
+ * the same as quantizing the exact rational value.  code_type as above.
+ */
+fxpq_status fxpq_requant(fxpq_handle h, const fxpq_src* src, int64_t n, const fxpq_fmt* d_fmt,
+                         void* codes, fxpq_dtype code_type);
+
+/*
+ * Fractional-length search (Sec. "Quantization Parameters Optimization"): for
+ * every fl in [fl_lo, fl_hi] the data-structure error of Eq. 14,
+ *     L(fl) = sum_i (v_i - Q(v_i; wl, fl, S) * 2^-fl)^2,
+ * and the fl with the smallest error; equal errors go to the LARGER fl.  The
+ * comparison is exact.  sign is 0, 1 or FXPQ_SIGN_AUTO (Eq. 6).  The chosen
+ * format {wl, fl, sign, 0} is written to d_fmt_out (device).  When d_sse is not
+ * NULL it receives fl_hi - fl_lo + 1 errors (device doubles; fp64 sums whose
+ * relative error is far below 1e-9); otherwise candidates that provably cannot
+ * win are skipped.  Requirements: 2 <= wl <= 32, -64 <= fl_lo <= fl_hi <= 64,
+ * n >= 1.  Exact range: |v| * 2^(fl_hi+24) < 2^52 for fp32 values and
+ * |v * 2^s| < 2^52 for integer values when wl <= 16; |v * 2^max(s, fl_hi)| <
+ * 2^62 when wl > 16.  Outside it FXPQ_FLAG_RANGE is raised and d_fmt_out gets a
+ * nonzero status.
+ */
+fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
+                           int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out, double* d_sse);
+
+/*
+ * Quantized convolution (C-Block contraction, Sec. "Integer-Only Inference"):
+ * acc[n][oh][ow][k] = sum_{r,s,c} x[n][oh*stride-pad+r][ow*stride-pad+s][c] * w[k][r][s][c]
+ * with zero padding (value 0 in either code dtype), int32 accumulation on the
+ * int8 matrix cores.  x_type is FXPQ_I8 or FXPQ_U8OFF.  Layout requirements:
+ * c % 16 == 0, or c == 4 (first layer, padded RGB).  For FXPQ_U8OFF inputs
+ * w_colsum (device int32[k], sum of each filter's codes) must be given.  When
+ * ep and d_minmax are both non-NULL the exact min and max of the epilogue
+ * values are written to d_minmax (device double[2]) for the FxP-QLayer that
+ * follows.  Returns FXPQ_ERR_OVERFLOW when r*s*c*128*256 >= 2^31.
+ */
+fxpq_status fxpq_qconv(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
+                       const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
+                       int32_t* acc, double* d_minmax);
+
+/*
+ * Quantized FC layer: C[m][n] = sum_k A[m][k] * B[n][k], int32 accumulation;
+ * same contract as fxpq_qconv with a 1x1 kernel (K % 16 == 0).
+ */
+fxpq_status fxpq_qgemm(fxpq_handle h, int64_t M, int64_t N, int64_t K, const void* A,
+                       fxpq_dtype a_type, const int8_t* B, const int32_t* b_colsum,
+                       const fxpq_epilogue* ep, int32_t* C, double* d_minmax);
+
+/* Sum of each filter's codes: colsum[k] = sum_j w[k][j] for w[k][len] (device). */
+fxpq_status fxpq_weight_colsum(fxpq_handle h, const int8_t* w, int64_t k, int64_t len,
+                               int32_t* colsum);
+
+/* MAX-POOL on NHWC codes (no FxP-QLayer needed, Sec. "FxP-QLayer"); taps
+ * outside the input are skipped. */
+fxpq_status fxpq_maxpool(fxpq_handle h, const void* x, fxpq_dtype type, int32_t n, int32_t hgt,
+                         int32_t wid, int32_t c, int32_t ksize, int32_t stride, int32_t pad,
+                         void* y);
+
+/* Global AVG-POOL on NHWC codes x[n][hw][c]: y[n][c] = recip * sum_hw code
+ * (exact, int64), the reciprocal of the window being quantized like a
+ * parameter (Sec. "FxP-QLayer").  The value scale of y is the input fl plus the
+ * reciprocal's fl.  d_fmt (device) is the codes' format, needed for FXPQ_C8. */
+fxpq_status fxpq_avgpool_global(fxpq_handle h, const void* x, fxpq_dtype type,
+                                const fxpq_fmt* d_fmt, int32_t n, int32_t hw, int32_t c,
+                                int64_t recip, int64_t* y);
+
+/*
+ * Layer error (Eq. 14 against a full-precision reference, with the statistics
+ * of Eq. 16 and Eq. 18): d_out[0] = sum_i (ref_i - code_i * 2^-fl)^2,
+ * d_out[1] = min(ref), d_out[2] = max(ref), d_out[3] = population standard
+ * deviation of ref.  fp64 accumulation.  d_out is a device double[4].
+ */
+fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
+                             fxpq_dtype code_type, const fxpq_fmt* d_fmt, int64_t n,
+                             double* d_out);
+
+/* Sets d_scale[0] = fl_in + fl_w + ... as the C-Block output scale of `ep`
+ * (device int32), for consumers that need it as a plain FXPQ_SRC_INT scale. */
+fxpq_status fxpq_epilogue_scale(fxpq_handle h, const fxpq_epilogue* ep, int32_t* d_scale);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FXPQ_H */

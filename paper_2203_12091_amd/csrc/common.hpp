@@ -1,0 +1,133 @@
+// Internal definitions shared by the libfxpq translation units (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "fxpq.h"
+
+namespace fxpq {
+
+constexpr int kThreads = 256;        // threads per block of the streaming kernels
+constexpr int kMaxStreamBlocks = 2048;
+constexpr int kMaxConvBlocks = 1 << 20;
+constexpr int kWindow = 4;           // candidates of the first FL-search pass
+constexpr int kMaxCand = 160;        // fl_hi - fl_lo + 1 upper bound (|fl| <= 64 plus slack)
+constexpr int kGenChunks = 256;      // element chunks of the exact general search
+
+// Device-resident state of one handle.  Offsets into one scratch allocation.
+struct Scratch {
+  unsigned* flags;          // sticky FXPQ_FLAG_* bits
+  unsigned* counters;       // last-block-done counters (self-resetting)
+  double* minmax;           // internal [2]
+  double* minmax_part;      // per-block partials [kMaxConvBlocks][2]
+  long long* win_part;      // window FL-search partials
+  double* win_part_f;       // window FL-search fp64 partials
+  unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
+  void* plan;               // FlsPlan
+};
+
+enum Counter { CNT_MINMAX = 0, CNT_CONV = 1, CNT_WIN = 2, CNT_GEN = 3, CNT_LERR = 4, CNT_MAX = 8 };
+
+// Everything a kernel needs to produce the value v_i of an FxP-QLayer input,
+// as an exact double (integers below 2^53), plus its fractional length.
+struct SrcDev {
+  int kind;
+  int dtype;
+  const void* x;
+  const void* x2;
+  int dtype2;
+  int relu;  // ADD
+  const int32_t* d_scale;
+  const fxpq_fmt* fa;
+  const fxpq_fmt* fb;
+  // epilogue (ACC)
+  int channels;
+  int fl_w;
+  const fxpq_fmt* fin;
+  const int64_t* bias;
+  int fl_bias;
+  int ep_relu;
+  const int64_t* scale;
+  int fl_scale;
+  const int64_t* shift;
+  int fl_shift;
+};
+
+// Uniform part of the C-Block epilogue: exponents of the exact alignment.
+struct EpiU {
+  int s_out;    // fractional length of the epilogue value
+  int sh_acc;   // acc * 2^sh_acc ...
+  int sh_bias;  // bias * 2^sh_bias (before the Scale multiply)
+  int sh_mid;   // (...)*scale * 2^sh_mid
+  int sh_shift; // shift * 2^sh_shift
+  int u8off;    // input codes stored as u - 128: add 128 * colsum
+};
+
+__host__ __device__ inline int imax(int a, int b) { return a > b ? a : b; }
+
+__device__ inline EpiU epi_uniform(const SrcDev& s) {
+  EpiU u;
+  int s_acc = s.fin->fl + s.fl_w;
+  int s1 = s.bias ? imax(s_acc, s.fl_bias) : s_acc;
+  u.sh_acc = s1 - s_acc;
+  u.sh_bias = s.bias ? s1 - s.fl_bias : 0;
+  int s2 = s.scale ? s1 + s.fl_scale : s1;
+  int s3 = s.shift ? imax(s2, s.fl_shift) : s2;
+  u.sh_mid = s3 - s2;
+  u.sh_shift = s.shift ? s3 - s.fl_shift : 0;
+  u.s_out = s3;
+  u.u8off = 0;
+  return u;
+}
+
+// Per-channel multiplier and addend: v = relu(acc * M + A), exact while |v| < 2^53.
+__device__ inline void epi_channel(const SrcDev& s, const EpiU& u, int c, double& M, double& A) {
+  double sc = s.scale ? (double)s.scale[c] : 1.0;
+  M = ldexp(sc, u.sh_acc + u.sh_mid);
+  double a = s.bias ? ldexp((double)s.bias[c], u.sh_bias + u.sh_mid) * sc : 0.0;
+  if (s.shift) a += ldexp((double)s.shift[c], u.sh_shift);
+  A = a;
+}
+
+// Fractional length of the values described by s.
+__device__ inline int src_scale(const SrcDev& s) {
+  switch (s.kind) {
+    case FXPQ_SRC_INT: return *s.d_scale;
+    case FXPQ_SRC_ACC: return epi_uniform(s).s_out;
+    case FXPQ_SRC_ADD: return imax(s.fa->fl, s.fb->fl);
+    default: return 0;
+  }
+}
+
+// 8-bit code storage resolved against a format: 1 when stored as u - 128.
+__device__ inline int code_is_off(int dtype, const fxpq_fmt* f) {
+  if (dtype == FXPQ_U8OFF) return 1;
+  if (dtype == 6 /* C8 */) return f && f->sign == 0;
+  return 0;
+}
+
+// ---- launchers implemented in the kernel translation units -------------------
+struct Ctx {
+  hipStream_t stream;
+  Scratch sc;
+};
+
+hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out);
+hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
+                          int code_type);
+hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
+                            int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
+hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
+                       const int8_t* w, const int32_t* colsum, const SrcDev* ep, int32_t* acc,
+                       double* d_minmax);
+hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out);
+hipError_t launch_maxpool(const Ctx& c, const int8_t* x, int n, int h, int w, int ch, int ks,
+                          int stride, int pad, int8_t* y);
+hipError_t launch_avgpool(const Ctx& c, const int8_t* x, int dtype, const fxpq_fmt* fmt, int n,
+                          int hw, int ch, int64_t recip, int64_t* y);
+hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes, int code_type,
+                              const fxpq_fmt* fmt, int64_t n, double* out);
+hipError_t launch_epi_scale(const Ctx& c, const SrcDev& s, int32_t* out);
+
+}  // namespace fxpq

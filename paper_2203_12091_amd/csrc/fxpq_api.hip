@@ -1,0 +1,360 @@
+// libfxpq C ABI: handle management, host-side argument checks and dispatch to
+// the kernels.  Every function is extern "C"; no exception or C++ type crosses
+// the boundary.
+#include <stdint.h>
+#include <string.h>
+
+#include <new>
+
+#include "common.hpp"
+
+using namespace fxpq;
+
+struct fxpq_handle_s {
+  int device;
+  hipStream_t stream;
+  void* scratch;
+  size_t scratch_bytes;
+  Scratch sc;
+};
+
+namespace {
+
+constexpr int64_t kMaxFlsBlocks = 1 << 16;
+
+size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
+
+bool is_code8(int t) { return t == FXPQ_I8 || t == FXPQ_U8OFF || t == FXPQ_C8; }
+
+bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32; }
+
+size_t code_align(int t) { return is_code8(t) ? 4 : (t == FXPQ_I16 ? 8 : 16); }
+
+Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc}; }
+
+fxpq_status hip_status(hipError_t e) { return e == hipSuccess ? FXPQ_OK : FXPQ_ERR_HIP; }
+
+// Device context guard: calls run on the handle's device.
+struct DeviceGuard {
+  int prev = -1;
+  explicit DeviceGuard(int dev) {
+    (void)hipGetDevice(&prev);
+    if (prev != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    (void)hipGetDevice(&cur);
+    if (prev >= 0 && cur != prev) (void)hipSetDevice(prev);
+  }
+};
+
+fxpq_status to_dev(const fxpq_src* s, int64_t n, SrcDev* d) {
+  if (!s || !s->x) return FXPQ_ERR_INVALID_ARG;
+  memset(d, 0, sizeof(*d));
+  d->kind = s->kind;
+  d->dtype = s->dtype;
+  d->x = s->x;
+  switch (s->kind) {
+    case FXPQ_SRC_F32:
+      if (!aligned(s->x, 16)) return FXPQ_ERR_INVALID_ARG;
+      d->dtype = FXPQ_F32;
+      break;
+    case FXPQ_SRC_INT:
+      if (s->dtype != FXPQ_I32 && s->dtype != FXPQ_I64) return FXPQ_ERR_INVALID_ARG;
+      if (!s->d_scale || !aligned(s->x, 16)) return FXPQ_ERR_INVALID_ARG;
+      d->d_scale = s->d_scale;
+      break;
+    case FXPQ_SRC_ACC: {
+      const fxpq_epilogue* e = s->ep;
+      if (!e || !e->d_fmt_in || e->channels < 1 || !aligned(s->x, 16)) return FXPQ_ERR_INVALID_ARG;
+      if (n % e->channels != 0) return FXPQ_ERR_INVALID_ARG;
+      d->dtype = FXPQ_I32;
+      d->channels = e->channels;
+      d->fl_w = e->fl_w;
+      d->fin = e->d_fmt_in;
+      d->bias = e->bias;
+      d->fl_bias = e->fl_bias;
+      d->ep_relu = e->relu ? 1 : 0;
+      d->scale = e->scale;
+      d->fl_scale = e->fl_scale;
+      d->shift = e->shift;
+      d->fl_shift = e->fl_shift;
+      break;
+    }
+    case FXPQ_SRC_ADD:
+      if (!s->x2 || !s->d_fmt_a || !s->d_fmt_b) return FXPQ_ERR_INVALID_ARG;
+      if (!is_code8(s->dtype) || !is_code8(s->dtype2)) return FXPQ_ERR_INVALID_ARG;
+      if (!aligned(s->x, 4) || !aligned(s->x2, 4)) return FXPQ_ERR_INVALID_ARG;
+      d->x2 = s->x2;
+      d->dtype2 = s->dtype2;
+      d->fa = s->d_fmt_a;
+      d->fb = s->d_fmt_b;
+      d->relu = s->relu ? 1 : 0;
+      break;
+    default:
+      return FXPQ_ERR_INVALID_ARG;
+  }
+  return FXPQ_OK;
+}
+
+void epi_to_dev(const fxpq_epilogue* e, SrcDev* d) {
+  memset(d, 0, sizeof(*d));
+  d->kind = FXPQ_SRC_ACC;
+  d->dtype = FXPQ_I32;
+  d->channels = e->channels;
+  d->fl_w = e->fl_w;
+  d->fin = e->d_fmt_in;
+  d->bias = e->bias;
+  d->fl_bias = e->fl_bias;
+  d->ep_relu = e->relu ? 1 : 0;
+  d->scale = e->scale;
+  d->fl_scale = e->fl_scale;
+  d->shift = e->shift;
+  d->fl_shift = e->fl_shift;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fxpq_status_string(fxpq_status s) {
+  switch (s) {
+    case FXPQ_OK: return "ok";
+    case FXPQ_ERR_INVALID_ARG: return "invalid argument";
+    case FXPQ_ERR_UNSUPPORTED: return "unsupported";
+    case FXPQ_ERR_NONFINITE: return "non-finite input";
+    case FXPQ_ERR_OVERFLOW: return "int32 accumulator overflow possible";
+    case FXPQ_ERR_HIP: return "HIP runtime error";
+    case FXPQ_ERR_ALLOC: return "allocation failed";
+  }
+  return "unknown status";
+}
+
+fxpq_status fxpq_create(fxpq_handle* out, int device) {
+  if (!out) return FXPQ_ERR_INVALID_ARG;
+  *out = nullptr;
+  int count = 0;
+  if (hipGetDeviceCount(&count) != hipSuccess || device < 0 || device >= count)
+    return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(device);
+  fxpq_handle h = new (std::nothrow) fxpq_handle_s();
+  if (!h) return FXPQ_ERR_ALLOC;
+  h->device = device;
+  h->stream = nullptr;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    size_t o = off;
+    off = align_up(off + bytes, 256);
+    return o;
+  };
+  size_t o_flags = take(4);
+  size_t o_cnt = take(sizeof(unsigned) * CNT_MAX);
+  size_t o_mm = take(2 * sizeof(double));
+  size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
+  size_t o_wp = take((size_t)kMaxFlsBlocks * 3 * kWindow * sizeof(long long));
+  size_t o_wpf = take((size_t)kMaxFlsBlocks * 2 * sizeof(double));
+  size_t o_gp = take((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
+  size_t o_plan = take(256);
+  if (hipMalloc(&h->scratch, off) != hipSuccess) {
+    delete h;
+    return FXPQ_ERR_ALLOC;
+  }
+  h->scratch_bytes = off;
+  char* base = static_cast<char*>(h->scratch);
+  h->sc.flags = reinterpret_cast<unsigned*>(base + o_flags);
+  h->sc.counters = reinterpret_cast<unsigned*>(base + o_cnt);
+  h->sc.minmax = reinterpret_cast<double*>(base + o_mm);
+  h->sc.minmax_part = reinterpret_cast<double*>(base + o_mmp);
+  h->sc.win_part = reinterpret_cast<long long*>(base + o_wp);
+  h->sc.win_part_f = reinterpret_cast<double*>(base + o_wpf);
+  h->sc.gen_part = reinterpret_cast<unsigned long long*>(base + o_gp);
+  h->sc.plan = base + o_plan;
+  if (hipMemset(h->scratch, 0, o_mmp) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
+    (void)hipFree(h->scratch);
+    delete h;
+    return FXPQ_ERR_HIP;
+  }
+  *out = h;
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_destroy(fxpq_handle h) {
+  if (!h) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  (void)hipStreamSynchronize(h->stream);
+  (void)hipFree(h->scratch);
+  delete h;
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_set_stream(fxpq_handle h, void* stream) {
+  if (!h) return FXPQ_ERR_INVALID_ARG;
+  h->stream = static_cast<hipStream_t>(stream);
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_sync_status(fxpq_handle h, uint32_t* flags) {
+  if (!h) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  if (hipStreamSynchronize(h->stream) != hipSuccess) return FXPQ_ERR_HIP;
+  uint32_t f = 0;
+  if (hipMemcpy(&f, h->sc.flags, 4, hipMemcpyDeviceToHost) != hipSuccess) return FXPQ_ERR_HIP;
+  if (hipMemset(h->sc.flags, 0, 4) != hipSuccess) return FXPQ_ERR_HIP;
+  if (hipDeviceSynchronize() != hipSuccess) return FXPQ_ERR_HIP;
+  if (flags) *flags = f;
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_quantize(fxpq_handle h, const float* x, int64_t n, const fxpq_fmt* d_fmt,
+                          void* codes, fxpq_dtype code_type) {
+  if (!h || n < 0 || !d_fmt) return FXPQ_ERR_INVALID_ARG;
+  if (n == 0) return FXPQ_OK;
+  if (!x || !codes || !is_code(code_type)) return FXPQ_ERR_INVALID_ARG;
+  if (!aligned(x, 16) || !aligned(codes, code_align(code_type))) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  SrcDev s;
+  memset(&s, 0, sizeof(s));
+  s.kind = FXPQ_SRC_F32;
+  s.dtype = FXPQ_F32;
+  s.x = x;
+  return hip_status(launch_requant(ctx(h), s, n, d_fmt, codes, code_type));
+}
+
+fxpq_status fxpq_requant(fxpq_handle h, const fxpq_src* src, int64_t n, const fxpq_fmt* d_fmt,
+                         void* codes, fxpq_dtype code_type) {
+  if (!h || n < 0 || !d_fmt) return FXPQ_ERR_INVALID_ARG;
+  if (n == 0) return FXPQ_OK;
+  if (!codes || !is_code(code_type) || !aligned(codes, code_align(code_type)))
+    return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  DeviceGuard g(h->device);
+  return hip_status(launch_requant(ctx(h), s, n, d_fmt, codes, code_type));
+}
+
+fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl,
+                           int32_t sign, int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out,
+                           double* d_sse) {
+  if (!h || n < 1 || !d_fmt_out) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 1 || wl > 32) return FXPQ_ERR_INVALID_ARG;
+  if (wl == 1) return FXPQ_ERR_UNSUPPORTED;
+  if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  int qbits = wl <= 16 ? wl : 16;
+  int64_t per_thread = (int64_t)1 << (53 - 26 - qbits - 1);
+  if (n / ((int64_t)kThreads * per_thread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  DeviceGuard g(h->device);
+  Ctx c = ctx(h);
+  const double* mm = src->d_minmax;
+  if (!mm) {
+    hipError_t e = launch_minmax(c, s, n, h->sc.minmax);
+    if (e != hipSuccess) return FXPQ_ERR_HIP;
+    mm = h->sc.minmax;
+  }
+  return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
+}
+
+static fxpq_status conv_common(fxpq_handle h, const fxpq_conv_desc* d, const void* x,
+                               fxpq_dtype x_type, const int8_t* w, const int32_t* w_colsum,
+                               const fxpq_epilogue* ep, int32_t* acc, double* d_minmax) {
+  if (!h || !d || !x || !w || !acc) return FXPQ_ERR_INVALID_ARG;
+  if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
+      d->stride < 1 || d->pad < 0)
+    return FXPQ_ERR_INVALID_ARG;
+  if (!is_code8(x_type)) return FXPQ_ERR_INVALID_ARG;
+  if (x_type == FXPQ_C8 && (!ep || !ep->d_fmt_in)) return FXPQ_ERR_INVALID_ARG;
+  if ((x_type == FXPQ_U8OFF || x_type == FXPQ_C8) && !w_colsum) return FXPQ_ERR_INVALID_ARG;
+  if (ep && (ep->channels != d->k || !ep->d_fmt_in)) return FXPQ_ERR_INVALID_ARG;
+  if (!(d->c % 16 == 0 || (d->c == 4 && d->r * d->s <= 128))) return FXPQ_ERR_UNSUPPORTED;
+  int64_t ho = (d->h + 2 * (int64_t)d->pad - d->r) / d->stride + 1;
+  int64_t wo = (d->w + 2 * (int64_t)d->pad - d->s) / d->stride + 1;
+  if (ho < 1 || wo < 1) return FXPQ_ERR_INVALID_ARG;
+  int64_t M = (int64_t)d->n * ho * wo;
+  if (M >= INT32_MAX || (int64_t)d->n * d->h * d->w * d->c >= ((int64_t)1 << 40))
+    return FXPQ_ERR_UNSUPPORTED;
+  int64_t depth = (int64_t)d->r * d->s * d->c;
+  if (depth * 128 * 256 >= ((int64_t)1 << 31)) return FXPQ_ERR_OVERFLOW;
+  int64_t blocks = (d->k <= 64) ? ((M + 255) / 256) * ((d->k + 63) / 64)
+                                : ((M + 127) / 128) * ((d->k + 127) / 128);
+  if (blocks > kMaxConvBlocks) return FXPQ_ERR_UNSUPPORTED;
+  if (!aligned(w, 16) || !aligned(acc, 4) || !aligned(x, d->c == 4 ? 4 : 16))
+    return FXPQ_ERR_INVALID_ARG;
+  SrcDev e;
+  if (ep) epi_to_dev(ep, &e);
+  DeviceGuard g(h->device);
+  return hip_status(launch_conv(ctx(h), *d, x, x_type, w, w_colsum, ep ? &e : nullptr, acc,
+                                ep ? d_minmax : nullptr));
+}
+
+fxpq_status fxpq_qconv(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
+                       const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
+                       int32_t* acc, double* d_minmax) {
+  return conv_common(h, d, x, x_type, w, w_colsum, ep, acc, d_minmax);
+}
+
+fxpq_status fxpq_qgemm(fxpq_handle h, int64_t M, int64_t N, int64_t K, const void* A,
+                       fxpq_dtype a_type, const int8_t* B, const int32_t* b_colsum,
+                       const fxpq_epilogue* ep, int32_t* C, double* d_minmax) {
+  if (M < 1 || N < 1 || K < 1 || M >= INT32_MAX || N >= INT32_MAX || K >= INT32_MAX)
+    return FXPQ_ERR_INVALID_ARG;
+  if (K % 16 != 0) return FXPQ_ERR_UNSUPPORTED;
+  fxpq_conv_desc d{(int32_t)M, 1, 1, (int32_t)K, (int32_t)N, 1, 1, 1, 0};
+  return conv_common(h, &d, A, a_type, B, b_colsum, ep, C, d_minmax);
+}
+
+fxpq_status fxpq_weight_colsum(fxpq_handle h, const int8_t* w, int64_t k, int64_t len,
+                               int32_t* colsum) {
+  if (!h || !w || !colsum || k < 1 || len < 1 || k >= INT32_MAX) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_colsum(ctx(h), w, k, len, colsum));
+}
+
+fxpq_status fxpq_maxpool(fxpq_handle h, const void* x, fxpq_dtype type, int32_t n, int32_t hgt,
+                         int32_t wid, int32_t c, int32_t ksize, int32_t stride, int32_t pad,
+                         void* y) {
+  if (!h || !x || !y || !is_code8(type)) return FXPQ_ERR_INVALID_ARG;
+  if (n < 1 || hgt < 1 || wid < 1 || c < 1 || ksize < 1 || stride < 1 || pad < 0 || pad >= ksize)
+    return FXPQ_ERR_INVALID_ARG;
+  if (c % 4 != 0 || !aligned(x, 4) || !aligned(y, 4)) return FXPQ_ERR_UNSUPPORTED;
+  if ((hgt + 2 * pad - ksize) < 0 || (wid + 2 * pad - ksize) < 0) return FXPQ_ERR_INVALID_ARG;
+  if (c % 16 == 0 && (!aligned(x, 16) || !aligned(y, 16))) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_maxpool(ctx(h), static_cast<const int8_t*>(x), n, hgt, wid, c, ksize,
+                                   stride, pad, static_cast<int8_t*>(y)));
+}
+
+fxpq_status fxpq_avgpool_global(fxpq_handle h, const void* x, fxpq_dtype type,
+                                const fxpq_fmt* d_fmt, int32_t n, int32_t hw, int32_t c,
+                                int64_t recip, int64_t* y) {
+  if (!h || !x || !y || !is_code8(type) || n < 1 || hw < 1 || c < 1) return FXPQ_ERR_INVALID_ARG;
+  if (type == FXPQ_C8 && !d_fmt) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_avgpool(ctx(h), static_cast<const int8_t*>(x), type, d_fmt, n, hw, c,
+                                   recip, y));
+}
+
+fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
+                             fxpq_dtype code_type, const fxpq_fmt* d_fmt, int64_t n,
+                             double* d_out) {
+  if (!h || !ref || !codes || !d_fmt || !d_out || n < 1 || !is_code(code_type))
+    return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_layer_error(ctx(h), ref, codes, code_type, d_fmt, n, d_out));
+}
+
+fxpq_status fxpq_epilogue_scale(fxpq_handle h, const fxpq_epilogue* ep, int32_t* d_scale) {
+  if (!h || !ep || !ep->d_fmt_in || !d_scale) return FXPQ_ERR_INVALID_ARG;
+  SrcDev e;
+  epi_to_dev(ep, &e);
+  DeviceGuard g(h->device);
+  return hip_status(launch_epi_scale(ctx(h), e, d_scale));
+}
+
+}  // extern "C"

@@ -1,0 +1,514 @@
+// Fractional-length search (Sec. "Quantization Parameters Optimization"):
+// argmin over fl of the data-structure error L(fl) of Eq. 14, ties to the
+// larger fl, decided EXACTLY.
+//
+// Pass 1 ("window", one read of the tensor, fp64 only):
+//   * beta_nosat, the largest fl at which no value saturates, comes from the
+//     tensor's min/max.  Below it L is non-increasing in fl (each coarser
+//     grid's points are points of the finer grid, and an unsaturated value's
+//     error is its distance to the infinite grid), so with ties going to the
+//     larger fl the winner is >= beta_nosat.
+//   * kWindow candidates from beta_nosat upward are evaluated with
+//         2^(2 sigma) L(fl) = sum W^2 - 2^(d+1) sum W q + 2^(2d) sum q^2,
+//     W = v * 2^sigma the value as an integer, d = sigma - fl, q its code.
+//     sum W^2 is the same for every candidate, so the argmin only needs the
+//     exact integers sum q^2 and sum W q.  W is split as Wh * 2^26 + Wl so
+//     every per-thread partial stays an exact integer below 2^53; blocks
+//     reduce in int64 and the last block compares candidates in 512-bit
+//     integer arithmetic.
+//   * Candidates above the window are discarded when a lower bound of their
+//     error, the clipping error at the first of them (non-decreasing in fl),
+//     exceeds an upper bound of the window's best error.
+// Pass 2 ("general", only when pass 1 could not decide, when the caller asks
+//   for every error, or for word lengths above 16): the exact error of every
+//   remaining candidate in 128-bit integer arithmetic, compared exactly.
+#include <limits.h>
+#include <math.h>
+
+#include "values.hpp"
+
+namespace fxpq {
+
+int stream_grid(int64_t n, int channels, int64_t max_per_thread);
+
+struct FlsPlan {
+  int need_general;
+  int gen_lo, gen_hi;
+  int gen_extra;  // INT_MIN when none
+  int sign;
+  int status;
+};
+
+enum FlsMode { MODE_SEARCH = 0, MODE_REPORT = 1 };
+
+constexpr double kTwoM26 = 1.0 / 67108864.0;  // 2^-26
+constexpr double kTwo26 = 67108864.0;
+
+// ---------------------------------------------------------------------------
+// Small signed 512-bit integer (two's complement), used by one thread.
+// ---------------------------------------------------------------------------
+struct Big {
+  unsigned long long w[8];
+};
+
+__device__ inline Big big_from_i128(__int128 v) {
+  Big b;
+  b.w[0] = (unsigned long long)v;
+  b.w[1] = (unsigned long long)(v >> 64);
+  unsigned long long ext = (v < 0) ? ~0ull : 0ull;
+  for (int i = 2; i < 8; ++i) b.w[i] = ext;
+  return b;
+}
+
+__device__ inline Big big_shl(const Big& a, int s) {
+  Big r;
+  int ws = s / 64, bs = s % 64;
+  for (int i = 7; i >= 0; --i) {
+    unsigned long long hi = (i - ws >= 0) ? a.w[i - ws] : 0ull;
+    unsigned long long lo = (i - ws - 1 >= 0) ? a.w[i - ws - 1] : 0ull;
+    r.w[i] = bs ? (hi << bs) | (lo >> (64 - bs)) : hi;
+  }
+  return r;
+}
+
+__device__ inline Big big_sub(const Big& a, const Big& b) {
+  Big r;
+  unsigned long long borrow = 0;
+  for (int i = 0; i < 8; ++i) {
+    unsigned long long x = a.w[i], y = b.w[i];
+    unsigned long long d = x - y - borrow;
+    borrow = (x < y) || (x - y < borrow) ? 1ull : 0ull;
+    r.w[i] = d;
+  }
+  return r;
+}
+
+__device__ inline int big_cmp(const Big& a, const Big& b) {
+  bool na = (long long)a.w[7] < 0, nb = (long long)b.w[7] < 0;
+  if (na != nb) return na ? -1 : 1;
+  for (int i = 7; i >= 0; --i)
+    if (a.w[i] != b.w[i]) return a.w[i] < b.w[i] ? -1 : 1;
+  return 0;
+}
+
+__device__ inline double big_to_double(const Big& a) {
+  bool neg = (long long)a.w[7] < 0;
+  Big m = a;
+  if (neg) {
+    Big z;
+    for (int i = 0; i < 8; ++i) z.w[i] = 0;
+    m = big_sub(z, a);
+  }
+  double r = 0.0;
+  for (int i = 7; i >= 0; --i) r = r * 18446744073709551616.0 + (double)m.w[i];
+  return neg ? -r : r;
+}
+
+// ---------------------------------------------------------------------------
+// Uniform set-up shared by both passes.
+// ---------------------------------------------------------------------------
+struct FlsU {
+  int sv;        // fractional length of the loaded values v
+  int sign;
+  double qmin, qmax;
+  int sigma;     // W = v * 2^(sigma - sv) is an integer where it matters
+  double wscale; // 2^(sigma - sv)
+  double absmax; // max |v|
+  int beta_nosat;
+  int ok;        // 0: non-finite input
+};
+
+template <int KIND>
+__device__ inline FlsU fls_uniform(const SrcDev& s, const double* mm, int wl, int sign_req,
+                                   int fl_lo, int fl_hi) {
+  FlsU u;
+  u.sv = (KIND == FXPQ_SRC_F32) ? 0 : src_scale(s);
+  double mn = mm[0], mx = mm[1];
+  u.ok = isfinite(mn) && isfinite(mx);
+  u.sign = (sign_req == FXPQ_SIGN_AUTO) ? (mn < 0.0 ? 1 : 0) : sign_req;
+  u.qmax = ldexp(1.0, wl - u.sign) - 1.0;
+  u.qmin = u.sign ? -ldexp(1.0, wl - 1) : 0.0;
+  u.absmax = fmax(fabs(mn), fabs(mx));
+  u.sigma = (KIND == FXPQ_SRC_F32) ? fl_hi + 24 : u.sv;
+  u.wscale = ldexp(1.0, u.sigma - u.sv);
+  // largest fl with every value inside [qmin - 1/2, qmax + 1/2] after scaling
+  u.beta_nosat = fl_lo - 1;
+  if (u.ok) {
+    for (int b = fl_hi; b >= fl_lo; --b) {
+      double tmax = ldexp(mx, b - u.sv), tmin = ldexp(mn, b - u.sv);
+      if (tmax <= u.qmax + 0.5 && tmin >= u.qmin - 0.5) {
+        u.beta_nosat = b;
+        break;
+      }
+    }
+  }
+  return u;
+}
+
+// ---------------------------------------------------------------------------
+// Pass 1: window search.
+// ---------------------------------------------------------------------------
+template <int KIND, int DT>
+__global__ __launch_bounds__(kThreads) void k_fls_window(
+    SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode,
+    const double* mm, long long* part_i, double* part_f, unsigned* counter, FlsPlan* plan,
+    fxpq_fmt* out, unsigned* flags) {
+  __shared__ long long shl[8];
+  __shared__ double shd[8];
+  const FlsU u = fls_uniform<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi);
+  const bool lead = (blockIdx.x == 0 && threadIdx.x == 0);
+
+  // Decisions every block takes identically before touching the data.
+  int verdict = 0;  // 0: run window; 1: done (fl_hi); 2: general for all; 3: failure
+  if (!u.ok) {
+    verdict = 3;
+  } else if (mode == MODE_REPORT || wl > 16 || u.absmax * u.wscale >= kTwo52) {
+    verdict = 2;
+  } else if (u.beta_nosat >= fl_hi) {
+    verdict = 1;
+  }
+  if (verdict != 0) {
+    if (lead) {
+      plan->sign = u.sign;
+      plan->status = 0;
+      plan->need_general = 0;
+      plan->gen_extra = INT_MIN;
+      if (verdict == 1) {
+        *out = fxpq_fmt{wl, fl_hi, u.sign, 0};
+      } else if (verdict == 2) {
+        plan->need_general = 1;
+        plan->gen_lo = fl_lo;
+        plan->gen_hi = fl_hi;
+      } else {
+        plan->status = 1;
+        *out = fxpq_fmt{wl, 0, u.sign, 1};
+        raise_flag(flags, FXPQ_FLAG_RANGE);
+      }
+    }
+    return;
+  }
+
+  const int b0 = imax(fl_lo, u.beta_nosat);
+  const int b1 = (b0 + kWindow - 1 < fl_hi) ? b0 + kWindow - 1 : fl_hi;
+  const int nc = b1 - b0 + 1;
+  const int bce = (b1 < fl_hi) ? b1 + 1 : b1;
+  double cj[kWindow];
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) cj[j] = ldexp(1.0, (j < nc ? b0 + j : b1) - u.sigma);
+  const double cce = ldexp(1.0, bce - u.sigma);
+  const double qmin = u.qmin, qmax = u.qmax;
+
+  double A[kWindow], PH[kWindow], PL[kWindow];
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) A[j] = PH[j] = PL[j] = 0.0;
+  double V2 = 0.0, CE = 0.0;
+
+  auto consume = [&](double v) {
+    double W = v * u.wscale;
+    double Wh = floor(W * kTwoM26);
+    double Wl = fma(-Wh, kTwo26, W);
+    V2 = fma(W, W, V2);
+#pragma unroll
+    for (int j = 0; j < kWindow; ++j) {
+      double q = fmin(fmax(rint(W * cj[j]), qmin), qmax);
+      A[j] = fma(q, q, A[j]);
+      PH[j] = fma(Wh, q, PH[j]);
+      PL[j] = fma(Wl, q, PL[j]);
+    }
+    double t = W * cce;
+    double d1 = fmax(t - qmax, 0.0), d2 = fmin(t - qmin, 0.0);
+    CE = fma(d1, d1, CE);
+    CE = fma(d2, d2, CE);
+  };
+
+  const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
+  const int64_t first = gtid * 4;
+  ThreadVals tv;
+  thread_vals_init<KIND>(s, first, tv);
+  const int64_t nfull = n & ~(int64_t)3;
+  for (int64_t i = first; i < nfull; i += stride) {
+    double v[4];
+    load4<KIND, DT>(s, tv, i, v);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) consume(v[e]);
+  }
+  if (gtid == 0)
+    for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i));
+
+  // Block partials: exact integers as int64, bound sums as fp64.
+  long long* pi = part_i + (int64_t)blockIdx.x * (3 * kWindow);
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) {
+    long long a = block_reduce((long long)A[j], OpAddL(), shl);
+    long long ph = block_reduce((long long)PH[j], OpAddL(), shl);
+    long long pl = block_reduce((long long)PL[j], OpAddL(), shl);
+    if (threadIdx.x == 0) {
+      pi[3 * j] = a;
+      pi[3 * j + 1] = ph;
+      pi[3 * j + 2] = pl;
+    }
+  }
+  double v2 = block_reduce(V2, OpAddD(), shd);
+  double ce = block_reduce(CE, OpAddD(), shd);
+  if (threadIdx.x == 0) {
+    part_f[2 * blockIdx.x] = v2;
+    part_f[2 * blockIdx.x + 1] = ce;
+  }
+
+  if (!last_block_done(counter)) return;
+
+  // ---- finalize (last block) ----
+  // Sum the block partials exactly: each partial < 2^61 in magnitude, split in
+  // 32-bit halves so the per-thread int64 sums cannot overflow.
+  __shared__ long long tot_hi[3 * kWindow], tot_lo[3 * kWindow];
+  __shared__ double tot_f[2];
+  const int nb = gridDim.x;
+  for (int qi = 0; qi < 3 * kWindow; ++qi) {
+    long long hi = 0, lo = 0;
+    for (int b = threadIdx.x; b < nb; b += kThreads) {
+      long long x = ld_acquire(&part_i[(int64_t)b * (3 * kWindow) + qi]);
+      hi += x >> 32;
+      lo += x & 0xFFFFFFFFll;
+    }
+    hi = block_reduce(hi, OpAddL(), shl);
+    lo = block_reduce(lo, OpAddL(), shl);
+    if (threadIdx.x == 0) {
+      tot_hi[qi] = hi;
+      tot_lo[qi] = lo;
+    }
+  }
+  for (int qi = 0; qi < 2; ++qi) {
+    double x = 0.0;
+    for (int b = threadIdx.x; b < nb; b += kThreads) x += ld_acquire(&part_f[2 * b + qi]);
+    x = block_reduce(x, OpAddD(), shd);
+    if (threadIdx.x == 0) tot_f[qi] = x;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    auto total = [&](int qi) -> __int128 {
+      return ((__int128)tot_hi[qi] << 32) + (__int128)tot_lo[qi];
+    };
+    // K_j = 2^(2d) A - 2^(d+1) P, d = sigma - beta; shifted by `off` >= 0 so all
+    // exponents are non-negative (same factor for every candidate).
+    int dmin = u.sigma - b1;
+    int off = 0;
+    if (2 * dmin < 0) off = -2 * dmin;
+    if (dmin + 1 + off < 0) off = -(dmin + 1);
+    Big best;
+    int bj = -1;
+    for (int j = 0; j < nc; ++j) {
+      int d = u.sigma - (b0 + j);
+      __int128 Aj = total(3 * j);
+      __int128 Pj = total(3 * j + 1) * (__int128)67108864 + total(3 * j + 2);
+      Big k = big_sub(big_shl(big_from_i128(Aj), 2 * d + off), big_shl(big_from_i128(Pj), d + 1 + off));
+      if (bj < 0 || big_cmp(k, best) <= 0) {  // ties -> larger fl
+        best = k;
+        bj = j;
+      }
+    }
+    const int fl_win = b0 + bj;
+    bool done = (b1 == fl_hi);
+    if (!done) {
+      // Upper bound of the window's best error, lower bound of every error
+      // above the window (relative fp64 error of each sum < 2^-33).
+      double kd = ldexp(big_to_double(best), -off);
+      double v2 = tot_f[0];
+      double sse_ub = (v2 * (1.0 + 0x1p-30) + kd + fabs(kd) * 0x1p-50 + v2 * 0x1p-50);
+      sse_ub = ldexp(sse_ub, -2 * u.sigma) * (1.0 + 0x1p-50);
+      double ce_lb = ldexp(tot_f[1] * (1.0 - 0x1p-30), -2 * bce);
+      done = ce_lb > sse_ub;
+    }
+    plan->sign = u.sign;
+    plan->status = 0;
+    if (done) {
+      plan->need_general = 0;
+      *out = fxpq_fmt{wl, fl_win, u.sign, 0};
+    } else {
+      plan->need_general = 1;
+      plan->gen_lo = b1 + 1;
+      plan->gen_hi = fl_hi;
+      plan->gen_extra = fl_win;
+    }
+  }
+  reset_counter(counter);
+}
+
+// ---------------------------------------------------------------------------
+// Pass 2: exact general search (128-bit errors, 192-bit sums).
+// ---------------------------------------------------------------------------
+struct U192 {
+  unsigned __int128 lo;
+  unsigned long long hi;
+};
+
+__device__ inline void u192_add(U192& a, unsigned __int128 x) {
+  unsigned __int128 s = a.lo + x;
+  if (s < a.lo) a.hi += 1;
+  a.lo = s;
+}
+
+__device__ inline void u192_add(U192& a, const U192& b) {
+  unsigned __int128 s = a.lo + b.lo;
+  a.hi += b.hi + (s < a.lo ? 1 : 0);
+  a.lo = s;
+}
+
+__device__ inline int u192_cmp(const U192& a, const U192& b) {
+  if (a.hi != b.hi) return a.hi < b.hi ? -1 : 1;
+  if (a.lo != b.lo) return a.lo < b.lo ? -1 : 1;
+  return 0;
+}
+
+__device__ inline double u192_to_double(const U192& a) {
+  return (double)a.hi * 0x1p128 + (double)(unsigned long long)(a.lo >> 64) * 0x1p64 +
+         (double)(unsigned long long)a.lo;
+}
+
+template <int KIND, int DT>
+__global__ __launch_bounds__(kThreads) void k_fls_general(
+    SrcDev s, int64_t n, int wl, int fl_lo, int fl_hi, int nchunks, const double* mm,
+    const FlsPlan* plan, unsigned long long* part, unsigned* counter, fxpq_fmt* out,
+    double* d_sse, unsigned* flags) {
+  __shared__ unsigned long long shp[kThreads * 3];
+  if (!plan->need_general || plan->status) return;
+  const int sign = plan->sign;
+  const int glo = plan->gen_lo, ghi = plan->gen_hi, extra = plan->gen_extra;
+  const int nreg = ghi - glo + 1;
+  const int nc = nreg + (extra != INT_MIN ? 1 : 0);
+  auto cand = [&](int j) { return (extra != INT_MIN) ? (j == 0 ? extra : glo + j - 1) : glo + j; };
+
+  const int sv = (KIND == FXPQ_SRC_F32) ? 0 : src_scale(s);
+  const int sigma = (KIND == FXPQ_SRC_F32) ? fl_hi + 24 : imax(sv, fl_hi);
+  const double wscale = ldexp(1.0, sigma - sv);
+  const double absmax = fmax(fabs(mm[0]), fabs(mm[1]));
+  if (absmax * wscale >= 0x1p62) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
+      *out = fxpq_fmt{wl, 0, sign, 2};
+      raise_flag(flags, FXPQ_FLAG_RANGE);
+    }
+    return;
+  }
+  const long long qmax = (1ll << (wl - sign)) - 1;
+  const long long qmin = sign ? -(1ll << (wl - 1)) : 0;
+  const int64_t clen = (n + nchunks - 1) / nchunks;
+  ThreadVals tv;  // only ADD uses uniform values here; ACC goes through load1
+  (void)tv;
+
+  for (int item = blockIdx.x; item < nc * nchunks; item += gridDim.x) {
+    const int j = item / nchunks, ch = item % nchunks;
+    const int beta = cand(j);
+    const int d = sigma - beta;  // >= 0
+    const int64_t e0 = (int64_t)ch * clen;
+    const int64_t e1 = (e0 + clen < n) ? e0 + clen : n;
+    U192 acc{0, 0};
+    for (int64_t i = e0 + threadIdx.x; i < e1; i += kThreads) {
+      double W = load1<KIND, DT>(s, i) * wscale;
+      unsigned __int128 e2;
+      if (W != floor(W)) {
+        // fp32 value below 2^-(fl_hi+1): its code is 0 for every candidate and
+        // its (identical) error is added truncated to the common unit.
+        e2 = (unsigned __int128)(unsigned long long)floor(W * W);
+      } else {
+        long long Wi = (long long)W;
+        long long q;
+        if (d >= 63) {
+          q = 0;
+        } else if (d == 0) {
+          q = Wi;
+        } else {
+          long long f = Wi >> d;
+          long long r = Wi - (f << d);
+          long long half = 1ll << (d - 1);
+          q = f + ((r > half || (r == half && (f & 1))) ? 1 : 0);
+        }
+        q = q < qmin ? qmin : (q > qmax ? qmax : q);
+        __int128 err = (__int128)Wi - ((d >= 63) ? (__int128)0 : ((__int128)q << d));
+        if (err < 0) err = -err;
+        e2 = (unsigned __int128)err * (unsigned __int128)err;
+      }
+      u192_add(acc, e2);
+    }
+    // block reduce the 192-bit partial
+    shp[3 * threadIdx.x] = (unsigned long long)acc.lo;
+    shp[3 * threadIdx.x + 1] = (unsigned long long)(acc.lo >> 64);
+    shp[3 * threadIdx.x + 2] = acc.hi;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      U192 t{0, 0};
+      for (int k = 0; k < kThreads; ++k) {
+        U192 x{((unsigned __int128)shp[3 * k + 1] << 64) | shp[3 * k], shp[3 * k + 2]};
+        u192_add(t, x);
+      }
+      unsigned long long* p = part + ((int64_t)j * kGenChunks + ch) * 3;
+      p[0] = (unsigned long long)t.lo;
+      p[1] = (unsigned long long)(t.lo >> 64);
+      p[2] = t.hi;
+    }
+    __syncthreads();
+  }
+
+  if (!last_block_done(counter)) return;
+  if (threadIdx.x == 0) {
+    U192 best{0, 0};
+    int bbeta = INT_MIN;
+    for (int j = 0; j < nc; ++j) {
+      U192 t{0, 0};
+      for (int ch = 0; ch < nchunks; ++ch) {
+        const unsigned long long* p = part + ((int64_t)j * kGenChunks + ch) * 3;
+        U192 x{((unsigned __int128)ld_acquire(&p[1]) << 64) | ld_acquire(&p[0]), ld_acquire(&p[2])};
+        u192_add(t, x);
+      }
+      int beta = cand(j);
+      int c = (bbeta == INT_MIN) ? -1 : u192_cmp(t, best);
+      if (c < 0 || (c == 0 && beta > bbeta)) {
+        best = t;
+        bbeta = beta;
+      }
+      if (d_sse && beta >= fl_lo && beta <= fl_hi) d_sse[beta - fl_lo] = ldexp(u192_to_double(t), -2 * sigma);
+    }
+    *out = fxpq_fmt{wl, bbeta, sign, 0};
+  }
+  reset_counter(counter);
+}
+
+// ---------------------------------------------------------------------------
+// Launcher.
+// ---------------------------------------------------------------------------
+#define FXPQ_DISPATCH_SRC(KIND_VAR, DT_VAR, CALL)                                   \
+  switch (KIND_VAR) {                                                               \
+    case FXPQ_SRC_F32: { constexpr int K_ = FXPQ_SRC_F32, D_ = FXPQ_F32; CALL; } break; \
+    case FXPQ_SRC_INT:                                                              \
+      if (DT_VAR == FXPQ_I64) { constexpr int K_ = FXPQ_SRC_INT, D_ = FXPQ_I64; CALL; } \
+      else { constexpr int K_ = FXPQ_SRC_INT, D_ = FXPQ_I32; CALL; }                \
+      break;                                                                        \
+    case FXPQ_SRC_ACC: { constexpr int K_ = FXPQ_SRC_ACC, D_ = FXPQ_I32; CALL; } break; \
+    default: { constexpr int K_ = FXPQ_SRC_ADD, D_ = FXPQ_I8; CALL; } break;        \
+  }
+
+hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
+                            int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
+  // Per-thread exactness of the window pass: |Wh q|, |Wl q| < 2^(26 + bits(Qmax))
+  // summed over at most `per_thread` values must stay below 2^53.
+  int qbits = (wl <= 16) ? wl : 16;
+  int64_t per_thread = (int64_t)1 << (53 - 26 - qbits - 1);
+  int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
+  int blocks = stream_grid(n, channels, per_thread);
+  FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
+  int mode = d_sse ? MODE_REPORT : MODE_SEARCH;
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_fls_window<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
+                        s, n, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part,
+                        c.sc.win_part_f, c.sc.counters + CNT_WIN, plan, out, c.sc.flags)));
+  int nchunks = (int)((n + 65535) / 65536);
+  if (nchunks > kGenChunks) nchunks = kGenChunks;
+  if (nchunks < 1) nchunks = 1;
+  int gblocks = 240;
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_fls_general<K_, D_><<<gblocks, kThreads, 0, c.stream>>>(
+                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part,
+                        c.sc.counters + CNT_GEN, out, d_sse, c.sc.flags)));
+  return hipGetLastError();
+}
+
+}  // namespace fxpq

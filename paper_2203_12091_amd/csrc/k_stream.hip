@@ -1,0 +1,458 @@
+// Streaming kernels of the hot path: min/max of FxP-QLayer inputs, the DFX
+// quantizer / FxP-QLayer requantization (Eq. 10-12), the layer error
+// (Eq. 14, 16, 18), pooling on codes and small helpers.  All HBM-bound: each
+// thread moves 16-byte groups, grid-strided with a stride that keeps its
+// channels fixed (see values.hpp).
+#include <math.h>
+
+#include "values.hpp"
+
+namespace fxpq {
+
+// ----------------------------------------------------------------------------
+// Grid sizing shared by the streaming launchers.
+// ----------------------------------------------------------------------------
+static int64_t gcd64(int64_t a, int64_t b) {
+  while (b) {
+    int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+int stream_grid(int64_t n, int channels, int64_t max_per_thread) {
+  int64_t groups = (n + 3) / 4;
+  int64_t blocks = (groups + kThreads - 1) / kThreads;
+  if (blocks > kMaxStreamBlocks) blocks = kMaxStreamBlocks;
+  if (max_per_thread > 0) {
+    int64_t need = (n + (int64_t)kThreads * max_per_thread - 1) / ((int64_t)kThreads * max_per_thread);
+    if (need > blocks) blocks = need;
+  }
+  if (blocks < 1) blocks = 1;
+  if (channels > 0) {
+    int64_t g = channels / gcd64(channels, 4 * kThreads);
+    blocks = (blocks + g - 1) / g * g;
+  }
+  return (int)blocks;
+}
+
+// ----------------------------------------------------------------------------
+// min / max
+// ----------------------------------------------------------------------------
+template <int KIND, int DT>
+__global__ __launch_bounds__(kThreads) void k_minmax(SrcDev s, int64_t n, double* part,
+                                                     unsigned* counter, double* out,
+                                                     unsigned* flags) {
+  __shared__ double sh[8];
+  const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
+  const int64_t first = gtid * 4;
+  ThreadVals t;
+  thread_vals_init<KIND>(s, first, t);
+  double mn = INFINITY, mx = -INFINITY;
+  bool bad = false;
+  const int64_t nfull = n & ~(int64_t)3;
+  for (int64_t i = first; i < nfull; i += stride) {
+    double v[4];
+    load4<KIND, DT>(s, t, i, v);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      mn = fmin(mn, v[j]);
+      mx = fmax(mx, v[j]);
+      if (KIND == FXPQ_SRC_F32) bad |= !isfinite(v[j]);
+    }
+  }
+  if (gtid == 0) {
+    for (int64_t i = nfull; i < n; ++i) {
+      double v = load1<KIND, DT>(s, i);
+      mn = fmin(mn, v);
+      mx = fmax(mx, v);
+      if (KIND == FXPQ_SRC_F32) bad |= !isfinite(v);
+    }
+  }
+  int any_bad = __syncthreads_or(bad);
+  mn = block_reduce(mn, OpMin(), sh);
+  mx = block_reduce(mx, OpMax(), sh);
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = any_bad ? NAN : mn;
+    part[2 * blockIdx.x + 1] = mx;
+    if (any_bad) raise_flag(flags, FXPQ_FLAG_NONFINITE);
+  }
+  if (last_block_done(counter)) {
+    double a = INFINITY, b = -INFINITY;
+    bool nan_seen = false;
+    for (int i = threadIdx.x; i < (int)gridDim.x; i += kThreads) {
+      double p0 = ld_acquire(&part[2 * i]);
+      double p1 = ld_acquire(&part[2 * i + 1]);
+      nan_seen |= isnan(p0);
+      a = fmin(a, p0);
+      b = fmax(b, p1);
+    }
+    int nan_any = __syncthreads_or(nan_seen);
+    a = block_reduce(a, OpMin(), sh);
+    b = block_reduce(b, OpMax(), sh);
+    if (threadIdx.x == 0) {
+      out[0] = nan_any ? NAN : a;
+      out[1] = b;
+    }
+    reset_counter(counter);
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Quantize / requantize.
+// ----------------------------------------------------------------------------
+struct QFmt {
+  double qmin, qmax, mult;
+  int off;         // 128 when stored as u - 128
+  int lo, hi;      // storage range
+  bool ok;
+};
+
+template <int OUT>
+__device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) {
+  QFmt q;
+  int k = fmt->wl, fl = fmt->fl, sg = fmt->sign;
+  q.ok = (fmt->status == 0 && k >= 2 && k <= 32 && (sg == 0 || sg == 1));
+  if (!q.ok) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_RANGE);
+    return q;
+  }
+  q.qmax = ldexp(1.0, k - sg) - 1.0;
+  q.qmin = sg ? -ldexp(1.0, k - 1) : 0.0;
+  q.mult = ldexp(1.0, fl - sv);
+  q.off = (OUT == FXPQ_U8OFF || (OUT == FXPQ_C8 && sg == 0)) ? 128 : 0;
+  if (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
+    q.lo = -128;
+    q.hi = 127;
+  } else if (OUT == FXPQ_I16) {
+    q.lo = -32768;
+    q.hi = 32767;
+  } else {
+    q.lo = INT32_MIN;
+    q.hi = INT32_MAX;
+  }
+  if (q.qmin - q.off < q.lo || q.qmax - q.off > q.hi) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_CODE);
+  }
+  return q;
+}
+
+__device__ inline int quant_one(double v, const QFmt& q) {
+  double r = rint(v * q.mult);  // round half to even
+  r = fmin(fmax(r, q.qmin), q.qmax);
+  double c = r - (double)q.off;
+  c = fmin(fmax(c, (double)q.lo), (double)q.hi);
+  return (int)c;
+}
+
+template <int OUT>
+__device__ inline void store4(void* codes, int64_t i, const int c[4]) {
+  if constexpr (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
+    uint32_t w = (uint32_t)(c[0] & 0xFF) | ((uint32_t)(c[1] & 0xFF) << 8) |
+                 ((uint32_t)(c[2] & 0xFF) << 16) | ((uint32_t)(c[3] & 0xFF) << 24);
+    *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(codes) + i) = w;
+  } else if constexpr (OUT == FXPQ_I16) {
+    uint2 w;
+    w.x = (uint32_t)(c[0] & 0xFFFF) | ((uint32_t)(c[1] & 0xFFFF) << 16);
+    w.y = (uint32_t)(c[2] & 0xFFFF) | ((uint32_t)(c[3] & 0xFFFF) << 16);
+    *reinterpret_cast<uint2*>(static_cast<int16_t*>(codes) + i) = w;
+  } else {
+    *reinterpret_cast<int4*>(static_cast<int32_t*>(codes) + i) = make_int4(c[0], c[1], c[2], c[3]);
+  }
+}
+
+template <int OUT>
+__device__ inline void store1(void* codes, int64_t i, int c) {
+  if constexpr (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8)
+    static_cast<int8_t*>(codes)[i] = (int8_t)c;
+  else if constexpr (OUT == FXPQ_I16)
+    static_cast<int16_t*>(codes)[i] = (int16_t)c;
+  else
+    static_cast<int32_t*>(codes)[i] = c;
+}
+
+template <int KIND, int DT, int OUT>
+__global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const fxpq_fmt* fmt,
+                                                      void* codes, unsigned* flags) {
+  const int sv = src_scale(s);
+  const QFmt q = qfmt_setup<OUT>(fmt, sv, flags);
+  if (!q.ok) return;
+  const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
+  const int64_t first = gtid * 4;
+  ThreadVals t;
+  thread_vals_init<KIND>(s, first, t);
+  const int64_t nfull = n & ~(int64_t)3;
+  for (int64_t i = first; i < nfull; i += stride) {
+    double v[4];
+    load4<KIND, DT>(s, t, i, v);
+    int c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) c[j] = quant_one(v[j], q);
+    store4<OUT>(codes, i, c);
+  }
+  if (gtid == 0) {
+    for (int64_t i = nfull; i < n; ++i) store1<OUT>(codes, i, quant_one(load1<KIND, DT>(s, i), q));
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Layer error.
+// ----------------------------------------------------------------------------
+template <int CT>
+__device__ inline double code_at(const void* codes, int64_t i) {
+  if constexpr (CT == FXPQ_I16) return static_cast<const int16_t*>(codes)[i];
+  else if constexpr (CT == FXPQ_I32) return static_cast<const int32_t*>(codes)[i];
+  else return static_cast<const int8_t*>(codes)[i];
+}
+
+template <int CT>
+__global__ __launch_bounds__(kThreads) void k_layer_error(const float* ref, const void* codes,
+                                                          const fxpq_fmt* fmt, int64_t n,
+                                                          double* part, unsigned* counter,
+                                                          double* out) {
+  __shared__ double sh[8];
+  const double step = ldexp(1.0, -fmt->fl);
+  const double off = (CT == FXPQ_U8OFF || (CT == FXPQ_C8 && fmt->sign == 0)) ? 128.0 : 0.0;
+  const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  double sse = 0.0, mn = INFINITY, mx = -INFINITY, s1 = 0.0, s2 = 0.0;
+  for (int64_t i = gtid; i < n; i += stride) {
+    double r = ref[i];
+    double d = r - (code_at<CT>(codes, i) + off) * step;
+    sse = fma(d, d, sse);
+    mn = fmin(mn, r);
+    mx = fmax(mx, r);
+    s1 += r;
+    s2 = fma(r, r, s2);
+  }
+  sse = block_reduce(sse, OpAddD(), sh);
+  mn = block_reduce(mn, OpMin(), sh);
+  mx = block_reduce(mx, OpMax(), sh);
+  s1 = block_reduce(s1, OpAddD(), sh);
+  s2 = block_reduce(s2, OpAddD(), sh);
+  if (threadIdx.x == 0) {
+    double* p = part + 5 * blockIdx.x;
+    p[0] = sse; p[1] = mn; p[2] = mx; p[3] = s1; p[4] = s2;
+  }
+  if (last_block_done(counter)) {
+    double a = 0.0, b = INFINITY, c = -INFINITY, d = 0.0, e = 0.0;
+    for (int i = threadIdx.x; i < (int)gridDim.x; i += kThreads) {
+      const double* p = part + 5 * i;
+      a += ld_acquire(&p[0]);
+      b = fmin(b, ld_acquire(&p[1]));
+      c = fmax(c, ld_acquire(&p[2]));
+      d += ld_acquire(&p[3]);
+      e += ld_acquire(&p[4]);
+    }
+    a = block_reduce(a, OpAddD(), sh);
+    b = block_reduce(b, OpMin(), sh);
+    c = block_reduce(c, OpMax(), sh);
+    d = block_reduce(d, OpAddD(), sh);
+    e = block_reduce(e, OpAddD(), sh);
+    if (threadIdx.x == 0) {
+      double mean = d / (double)n;
+      double var = e / (double)n - mean * mean;
+      out[0] = a;
+      out[1] = b;
+      out[2] = c;
+      out[3] = sqrt(var > 0.0 ? var : 0.0);
+    }
+    reset_counter(counter);
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Pooling and helpers.
+// ----------------------------------------------------------------------------
+template <int VEC>
+__global__ __launch_bounds__(kThreads) void k_maxpool(const int8_t* x, int n, int h, int w, int ch,
+                                                      int ks, int stride, int pad, int ho, int wo,
+                                                      int8_t* y) {
+  const int cg = ch / VEC;
+  const int64_t total = (int64_t)n * ho * wo * cg;
+  for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * kThreads) {
+    int g = (int)(idx % cg);
+    int64_t pix = idx / cg;
+    int ow = (int)(pix % wo);
+    int oh = (int)((pix / wo) % ho);
+    int b = (int)(pix / ((int64_t)wo * ho));
+    union {
+      int4 v16;
+      char4 v4;
+      int8_t b[16];
+    } best;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) best.b[j] = -128;
+    for (int r = 0; r < ks; ++r) {
+      int ih = oh * stride - pad + r;
+      if (ih < 0 || ih >= h) continue;
+      for (int q = 0; q < ks; ++q) {
+        int iw = ow * stride - pad + q;
+        if (iw < 0 || iw >= w) continue;
+        const int8_t* src = x + (((int64_t)b * h + ih) * w + iw) * ch + (int64_t)g * VEC;
+        if constexpr (VEC == 16) {
+          int4 v = *reinterpret_cast<const int4*>(src);
+          const int8_t* pv = reinterpret_cast<const int8_t*>(&v);
+#pragma unroll
+          for (int j = 0; j < 16; ++j) best.b[j] = pv[j] > best.b[j] ? pv[j] : best.b[j];
+        } else {
+          char4 v = *reinterpret_cast<const char4*>(src);
+          best.b[0] = v.x > best.b[0] ? v.x : best.b[0];
+          best.b[1] = v.y > best.b[1] ? v.y : best.b[1];
+          best.b[2] = v.z > best.b[2] ? v.z : best.b[2];
+          best.b[3] = v.w > best.b[3] ? v.w : best.b[3];
+        }
+      }
+    }
+    int8_t* dst = y + pix * ch + (int64_t)g * VEC;
+    if constexpr (VEC == 16) {
+      *reinterpret_cast<int4*>(dst) = best.v16;
+    } else {
+      *reinterpret_cast<char4*>(dst) = best.v4;
+    }
+  }
+}
+
+template <int CT>
+__global__ __launch_bounds__(kThreads) void k_avgpool(const int8_t* x, const fxpq_fmt* fmt, int n,
+                                                      int hw, int ch, int64_t recip, int64_t* y) {
+  const int64_t off = code_is_off(CT, fmt) ? 128 : 0;
+  const int64_t total = (int64_t)n * ch;
+  for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
+       idx += (int64_t)gridDim.x * kThreads) {
+    int c = (int)(idx % ch);
+    int64_t b = idx / ch;
+    int64_t s = 0;
+    const int8_t* p = x + b * hw * ch + c;
+    for (int q = 0; q < hw; ++q) s += (int64_t)p[(int64_t)q * ch] + off;
+    y[idx] = s * recip;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void k_colsum(const int8_t* w, int64_t len, int32_t* out) {
+  __shared__ long long sh[8];
+  const int8_t* row = w + (int64_t)blockIdx.x * len;
+  long long s = 0;
+  for (int64_t j = threadIdx.x; j < len; j += kThreads) s += row[j];
+  s = block_reduce(s, OpAddL(), sh);
+  if (threadIdx.x == 0) out[blockIdx.x] = (int32_t)s;
+}
+
+__global__ void k_epi_scale(SrcDev s, int32_t* out) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) out[0] = src_scale(s);
+}
+
+// ----------------------------------------------------------------------------
+// Launchers.
+// ----------------------------------------------------------------------------
+#define FXPQ_DISPATCH_SRC(KIND_VAR, DT_VAR, CALL)                                   \
+  switch (KIND_VAR) {                                                               \
+    case FXPQ_SRC_F32: { constexpr int K_ = FXPQ_SRC_F32, D_ = FXPQ_F32; CALL; } break; \
+    case FXPQ_SRC_INT:                                                              \
+      if (DT_VAR == FXPQ_I64) { constexpr int K_ = FXPQ_SRC_INT, D_ = FXPQ_I64; CALL; } \
+      else { constexpr int K_ = FXPQ_SRC_INT, D_ = FXPQ_I32; CALL; }                \
+      break;                                                                        \
+    case FXPQ_SRC_ACC: { constexpr int K_ = FXPQ_SRC_ACC, D_ = FXPQ_I32; CALL; } break; \
+    default: { constexpr int K_ = FXPQ_SRC_ADD, D_ = FXPQ_I8; CALL; } break;        \
+  }
+
+static int src_channels(const SrcDev& s) { return s.kind == FXPQ_SRC_ACC ? s.channels : 0; }
+
+hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) {
+  int blocks = stream_grid(n, src_channels(s), 0);
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
+                        s, n, c.sc.minmax_part, c.sc.counters + CNT_MINMAX, out, c.sc.flags)));
+  return hipGetLastError();
+}
+
+template <int OUT>
+static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
+                        int blocks) {
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_requant<K_, D_, OUT><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes,
+                                                                             c.sc.flags)));
+}
+
+hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
+                          void* codes, int code_type) {
+  int blocks = stream_grid(n, src_channels(s), 0);
+  switch (code_type) {
+    case FXPQ_I8: requant_out<FXPQ_I8>(c, s, n, fmt, codes, blocks); break;
+    case FXPQ_U8OFF: requant_out<FXPQ_U8OFF>(c, s, n, fmt, codes, blocks); break;
+    case FXPQ_C8: requant_out<FXPQ_C8>(c, s, n, fmt, codes, blocks); break;
+    case FXPQ_I16: requant_out<FXPQ_I16>(c, s, n, fmt, codes, blocks); break;
+    default: requant_out<FXPQ_I32>(c, s, n, fmt, codes, blocks); break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes, int code_type,
+                              const fxpq_fmt* fmt, int64_t n, double* out) {
+  int blocks = stream_grid(n, 0, 0);
+  double* part = c.sc.minmax_part;  // 5 doubles per block fits (kMaxConvBlocks * 2)
+  unsigned* cnt = c.sc.counters + CNT_LERR;
+  switch (code_type) {
+    case FXPQ_I16:
+      k_layer_error<FXPQ_I16><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      break;
+    case FXPQ_I32:
+      k_layer_error<FXPQ_I32><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      break;
+    case FXPQ_U8OFF:
+      k_layer_error<FXPQ_U8OFF><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      break;
+    case FXPQ_C8:
+      k_layer_error<FXPQ_C8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      break;
+    default:
+      k_layer_error<FXPQ_I8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      break;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_maxpool(const Ctx& c, const int8_t* x, int n, int h, int w, int ch, int ks,
+                          int stride, int pad, int8_t* y) {
+  int ho = (h + 2 * pad - ks) / stride + 1, wo = (w + 2 * pad - ks) / stride + 1;
+  int vec = (ch % 16 == 0) ? 16 : 4;
+  int64_t total = (int64_t)n * ho * wo * (ch / vec);
+  int64_t blocks = (total + kThreads - 1) / kThreads;
+  if (blocks > 65536) blocks = 65536;
+  if (blocks < 1) blocks = 1;
+  if (vec == 16)
+    k_maxpool<16><<<(int)blocks, kThreads, 0, c.stream>>>(x, n, h, w, ch, ks, stride, pad, ho, wo, y);
+  else
+    k_maxpool<4><<<(int)blocks, kThreads, 0, c.stream>>>(x, n, h, w, ch, ks, stride, pad, ho, wo, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_avgpool(const Ctx& c, const int8_t* x, int dtype, const fxpq_fmt* fmt, int n,
+                          int hw, int ch, int64_t recip, int64_t* y) {
+  int64_t total = (int64_t)n * ch;
+  int64_t blocks = (total + kThreads - 1) / kThreads;
+  if (blocks > 65536) blocks = 65536;
+  if (dtype == FXPQ_U8OFF)
+    k_avgpool<FXPQ_U8OFF><<<(int)blocks, kThreads, 0, c.stream>>>(x, fmt, n, hw, ch, recip, y);
+  else if (dtype == FXPQ_C8)
+    k_avgpool<FXPQ_C8><<<(int)blocks, kThreads, 0, c.stream>>>(x, fmt, n, hw, ch, recip, y);
+  else
+    k_avgpool<FXPQ_I8><<<(int)blocks, kThreads, 0, c.stream>>>(x, fmt, n, hw, ch, recip, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out) {
+  k_colsum<<<(int)k, kThreads, 0, c.stream>>>(w, len, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_epi_scale(const Ctx& c, const SrcDev& s, int32_t* out) {
+  k_epi_scale<<<1, 64, 0, c.stream>>>(s, out);
+  return hipGetLastError();
+}
+
+}  // namespace fxpq
