@@ -90,20 +90,20 @@ typedef struct {
  *     v = max(v, 0)          if relu
  * Alignment is an exact left shift of the coarser operand, so v is the exact
  * value of the C-Block; only the following FxP-QLayer rounds.  bias, scale and
- * shift are per-channel integer codes (device, int64) or NULL.  `channels` is
+ * shift are per-channel integer codes (device, int32: word lengths up to 32) or NULL.  `channels` is
  * the number of output channels, the innermost dimension of the accumulators.
  */
 typedef struct {
   int32_t channels;
   int32_t fl_w;
   const fxpq_fmt* d_fmt_in;
-  const int64_t* bias;
+  const int32_t* bias;
   int32_t fl_bias;
   int32_t relu;
-  const int64_t* scale;
+  const int32_t* scale;
   int32_t fl_scale;
   int32_t pad0;
-  const int64_t* shift;
+  const int32_t* shift;
   int32_t fl_shift;
   int32_t pad1;
 } fxpq_epilogue;

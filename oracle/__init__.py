@@ -11,3 +11,4 @@ Only ``tests/``, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``paper_2203_12091_amd``.
 """
 from .core import *  # noqa: F401,F403
+from . import nets  # noqa: F401

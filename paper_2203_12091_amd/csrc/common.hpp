@@ -45,12 +45,12 @@ struct SrcDev {
   int channels;
   int fl_w;
   const fxpq_fmt* fin;
-  const int64_t* bias;
+  const int32_t* bias;
   int fl_bias;
   int ep_relu;
-  const int64_t* scale;
+  const int32_t* scale;
   int fl_scale;
-  const int64_t* shift;
+  const int32_t* shift;
   int fl_shift;
 };
 

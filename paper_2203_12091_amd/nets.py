@@ -1,0 +1,438 @@
+"""DFX calibration forwards of the five workloads through libfxpq.
+
+Each workload is a graph of C-Blocks (Sec. "FxP-QLayer": CONV/FC [+ bias]
+[+ Scale] [+ ReLU], Eltwise, AVG-POOL) with an FxP-QLayer after every C-Block
+except the last, none after MAX-POOL, and one after the network input.  Every
+FxP-QLayer searches its fractional length over the whole batch tensor
+(Eq. 14, ties to the larger fl) and requantizes (Eq. 10-12).  Parameters are
+quantized once at set-up the same way (weights at their word length, biases
+and the Scale shift at 32 bits, the Scale multiplier at 16 bits, Sec.
+"Initial Design Generation"); BN layers are turned into Scale layers first
+(Eq. 4-5).
+
+Device layouts: activations NHWC int8 codes (storage FXPQ_C8: signed codes as
+int8, unsigned ones as u - 128), conv weights KRSC int8, the RGB input padded
+to 4 channels.  A forward is a sequence of library calls on one stream with no
+host synchronization; formats stay on the device.
+
+Workloads (synthetic, seeded; tensors named as in ``synth``):
+  fc        256x512 weights ~N(0, 0.05), 32x512 ReLU(N(0,1)) activations, WL 8/6/4
+  alexnet   64x3x224x224, conv 11/5/3 (64-192-384-256-256) + FC 9216-4096-4096-1000
+  vgg16     128x3x224x224, 13 conv 3x3 + 3 FC, weight WL per layer from {4..8}
+  resnet18  256x3x224x224, BasicBlock [2,2,2,2], BN as Scale, weight WL from {4,6,8}
+  resnet50  256x3x224x224, Bottleneck [3,4,6,3] (stride on the 3x3), BN as Scale
+"""
+import numpy as np
+
+import synth
+
+from . import fxpq as fx
+
+FL_LO, FL_HI = -8, 15
+A_WL = 8
+BIAS_WL, SCALE_WL, SHIFT_WL, RECIP_WL = 32, 16, 32, 16
+BN_EPS = np.float32(1e-5)
+SEEDS = {"fc": 0, "alexnet": 1, "vgg16": 2, "resnet18": 3, "resnet50": 4}
+DEFAULT_SHAPE = {"alexnet": (64, 224), "vgg16": (128, 224), "resnet18": (256, 224),
+                 "resnet50": (256, 224)}
+
+
+# ----------------------------------------------------------------------------
+# Graph description
+# ----------------------------------------------------------------------------
+class Node:
+    def __init__(self, op, name, inp, **kw):
+        self.op, self.name, self.inp = op, name, inp
+        self.__dict__.update(kw)
+
+
+def _conv(g, name, inp, cout, k, stride, pad, relu, bias=False, bn=False, wl=8, last=False):
+    g.append(Node("conv", name, inp, cout=cout, k=k, stride=stride, pad=pad, relu=relu, bias=bias,
+                  bn=bn, wl=wl, last=last))
+    return name
+
+
+def arch_alexnet(seed):
+    g = [Node("input", "input", None)]
+    x = _conv(g, "conv1", "input", 64, 11, 4, 2, True, bias=True)
+    g.append(Node("maxpool", "pool1", x, k=3, stride=2, pad=0)); x = "pool1"
+    x = _conv(g, "conv2", x, 192, 5, 1, 2, True, bias=True)
+    g.append(Node("maxpool", "pool2", x, k=3, stride=2, pad=0)); x = "pool2"
+    x = _conv(g, "conv3", x, 384, 3, 1, 1, True, bias=True)
+    x = _conv(g, "conv4", x, 256, 3, 1, 1, True, bias=True)
+    x = _conv(g, "conv5", x, 256, 3, 1, 1, True, bias=True)
+    g.append(Node("maxpool", "pool5", x, k=3, stride=2, pad=0)); x = "pool5"
+    g.append(Node("fc", "fc6", x, cout=4096, relu=True, bias=True, wl=8, last=False))
+    g.append(Node("fc", "fc7", "fc6", cout=4096, relu=True, bias=True, wl=8, last=False))
+    g.append(Node("fc", "fc8", "fc7", cout=1000, relu=False, bias=True, wl=8, last=True))
+    return g
+
+
+def arch_vgg16(seed):
+    plan = [[64, 64], [128, 128], [256, 256, 256], [512, 512, 512], [512, 512, 512]]
+    g = [Node("input", "input", None)]
+    x = "input"
+    for gi, group in enumerate(plan, 1):
+        for li, c in enumerate(group, 1):
+            name = f"conv{gi}_{li}"
+            wl = synth.choice(seed, name + ".wl", [4, 5, 6, 7, 8], 1)[0]
+            x = _conv(g, name, x, c, 3, 1, 1, True, bias=True, wl=wl)
+        g.append(Node("maxpool", f"pool{gi}", x, k=2, stride=2, pad=0)); x = f"pool{gi}"
+    for name, cout, last in [("fc6", 4096, False), ("fc7", 4096, False), ("fc8", 1000, True)]:
+        wl = synth.choice(seed, name + ".wl", [4, 5, 6, 7, 8], 1)[0]
+        g.append(Node("fc", name, x, cout=cout, relu=not last, bias=True, wl=wl, last=last))
+        x = name
+    return g
+
+
+def arch_resnet(seed, depth):
+    bottleneck = depth == 50
+    blocks = [3, 4, 6, 3] if bottleneck else [2, 2, 2, 2]
+    wl_opts = [8] if bottleneck else [4, 6, 8]
+
+    def wl_of(name):
+        return synth.choice(seed, name + ".wl", wl_opts, 1)[0] if len(wl_opts) > 1 else wl_opts[0]
+
+    g = [Node("input", "input", None)]
+    x = _conv(g, "conv1", "input", 64, 7, 2, 3, True, bn=True, wl=wl_of("conv1"))
+    g.append(Node("maxpool", "pool1", x, k=3, stride=2, pad=1)); x = "pool1"
+    cin = 64
+    for si, (nb, width) in enumerate(zip(blocks, [64, 128, 256, 512]), 1):
+        for bi in range(nb):
+            stride = 2 if (bi == 0 and si > 1) else 1
+            p = f"layer{si}.{bi}"
+            cout = width * 4 if bottleneck else width
+            if bottleneck:
+                a = _conv(g, p + ".c1", x, width, 1, 1, 0, True, bn=True, wl=wl_of(p + ".c1"))
+                b = _conv(g, p + ".c2", a, width, 3, stride, 1, True, bn=True, wl=wl_of(p + ".c2"))
+                c = _conv(g, p + ".c3", b, cout, 1, 1, 0, False, bn=True, wl=wl_of(p + ".c3"))
+            else:
+                a = _conv(g, p + ".c1", x, width, 3, stride, 1, True, bn=True, wl=wl_of(p + ".c1"))
+                c = _conv(g, p + ".c2", a, width, 3, 1, 1, False, bn=True, wl=wl_of(p + ".c2"))
+            if stride != 1 or cin != cout:
+                sc = _conv(g, p + ".ds", x, cout, 1, stride, 0, False, bn=True, wl=wl_of(p + ".ds"))
+            else:
+                sc = x
+            g.append(Node("add", p + ".add", c, other=sc, relu=True))
+            x = p + ".add"
+            cin = cout
+    g.append(Node("avgpool", "avgpool", x))
+    g.append(Node("fc", "fc", "avgpool", cout=1000, relu=False, bias=True, wl=wl_of("fc"), last=True))
+    return g
+
+
+ARCH = {"alexnet": arch_alexnet, "vgg16": arch_vgg16,
+        "resnet18": lambda s: arch_resnet(s, 18), "resnet50": lambda s: arch_resnet(s, 50)}
+
+
+# ----------------------------------------------------------------------------
+# Runner
+# ----------------------------------------------------------------------------
+class CalibNet:
+    """One workload resident on the GPU: quantized parameters, activation
+    buffers and the input; ``forward()`` enqueues a full calibration forward."""
+
+    def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", wl_override=None,
+                 keep_acts=True):
+        import torch
+        self.torch = torch
+        self.name = name
+        self.seed = SEEDS[name] if seed is None else seed
+        b0, s0 = DEFAULT_SHAPE[name]
+        self.batch = batch or b0
+        self.image = image or s0
+        self.dev = torch.device(device)
+        self.h = fx.Handle(self.dev.index or 0)
+        fx.set_stream(self.h, torch.cuda.current_stream(self.dev))
+        self.graph = ARCH[name](self.seed)
+        if wl_override:
+            for n in self.graph:
+                if n.name in wl_override:
+                    n.wl = wl_override[n.name]
+        self.keep = []
+        self.param_fmts = {}
+        self._build()
+
+    # -- helpers --------------------------------------------------------------
+    def _t(self, a, dtype=None):
+        t = self.torch.from_numpy(np.ascontiguousarray(a)).to(self.dev)
+        self.keep.append(t)
+        return t
+
+    def _empty(self, shape, dtype):
+        t = self.torch.empty(shape, dtype=dtype, device=self.dev)
+        self.keep.append(t)
+        return t
+
+    def _fmt(self, wl=0, fl=0, sign=0):
+        return self._t(np.array([wl, fl, sign, 0], np.int32))
+
+    def _quant_param(self, key, x32, wl, code_type):
+        """FL search + quantization of one parameter tensor on the GPU."""
+        T = self.torch
+        xd = self._t(x32.astype(np.float32).ravel())
+        fmt = self._fmt()
+        fx.fl_search(self.h, fx.src_f32(xd), xd.numel(), wl, fx.SIGN_AUTO, FL_LO, FL_HI, fmt)
+        dt = {fx.I8: T.int8, fx.I32: T.int32}[code_type]
+        codes = self._empty((xd.numel(),), dt)
+        fx.quantize(self.h, xd, xd.numel(), fmt, codes, code_type)
+        self._pending[key] = fmt
+        return codes, fmt
+
+    # -- set-up ----------------------------------------------------------------
+    def _build(self):
+        T = self.torch
+        seed, B, S = self.seed, self.batch, self.image
+        self._pending = {}
+        shapes = {}  # activation name -> (H, W, C)
+        self.act_fmt = {}
+        self.act_codes = {}
+        x = synth.normal(seed, "input", (B, 3, S, S))
+        x4 = np.zeros((B, S, S, 4), np.float32)
+        x4[..., :3] = np.transpose(x, (0, 2, 3, 1))
+        self.x_dev = self._t(x4)
+        shapes["input"] = (S, S, 4)
+        self.ops = []
+        acc_max = 1
+        for n in self.graph:
+            if n.op == "input":
+                self.act_fmt["input"] = self._fmt()
+                self.act_codes["input"] = self._empty((B, S, S, 4), T.int8)
+                self.ops.append(("input", n))
+            elif n.op in ("conv", "fc"):
+                H, W, Cin = shapes[n.inp]
+                real_cin = 3 if n.inp == "input" else Cin
+                if n.op == "conv":
+                    k, st, pd = n.k, n.stride, n.pad
+                    w = synth.he_normal(seed, n.name + ".w", (n.cout, real_cin, k, k))
+                    wk = np.transpose(w, (0, 2, 3, 1))  # KRSC
+                    if n.inp == "input":
+                        wk = np.concatenate([wk, np.zeros((n.cout, k, k, 1), np.float32)], axis=3)
+                    wk = wk.reshape(n.cout, -1)
+                    if Cin == 4:
+                        kp = (wk.shape[1] + 63) // 64 * 64
+                        wk = np.concatenate([wk, np.zeros((n.cout, kp - wk.shape[1]), np.float32)], 1)
+                    Ho, Wo = (H + 2 * pd - k) // st + 1, (W + 2 * pd - k) // st + 1
+                    desc = fx.conv_desc(B, H, W, Cin, n.cout, k, k, st, pd)
+                    M = B * Ho * Wo
+                else:
+                    fan_in = H * W * Cin
+                    w = synth.he_normal(seed, n.name + ".w", (n.cout, fan_in))
+                    # canonical flatten is (c, h, w); activations here are (h, w, c)
+                    wk = w.reshape(n.cout, Cin, H, W).transpose(0, 2, 3, 1).reshape(n.cout, fan_in)
+                    Ho = Wo = 1
+                    desc = None
+                    M = B
+                wcodes, wfmt = self._quant_param(n.name + ".w", wk, n.wl, fx.I8)
+                colsum = self._empty((n.cout,), T.int32)
+                fx.weight_colsum(self.h, wcodes, n.cout, wk.shape[1], colsum)
+                p = {"w": wcodes, "colsum": colsum, "wlen": wk.shape[1], "desc": desc, "M": M,
+                     "Ho": Ho, "Wo": Wo, "Cin": Cin}
+                if n.bias:
+                    b = synth.normal(seed, n.name + ".b", (n.cout,), std=0.01)
+                    p["b"], _ = self._quant_param(n.name + ".b", b, BIAS_WL, fx.I32)
+                if getattr(n, "bn", False):
+                    gamma = synth.uniform(seed, n.name + ".bn.gamma", (n.cout,), 0.5, 1.5)
+                    beta = synth.normal(seed, n.name + ".bn.beta", (n.cout,), std=0.1)
+                    mean = np.zeros(n.cout, np.float32)
+                    var = np.ones(n.cout, np.float32)
+                    inv = np.sqrt(var + BN_EPS)
+                    a1 = (gamma / inv).astype(np.float32)           # Eq. 5
+                    a2 = (beta - gamma * mean / inv).astype(np.float32)
+                    p["a1"], _ = self._quant_param(n.name + ".a1", a1, SCALE_WL, fx.I32)
+                    p["a2"], _ = self._quant_param(n.name + ".a2", a2, SHIFT_WL, fx.I32)
+                acc_max = max(acc_max, M * n.cout)
+                p["mm"] = self._empty((2,), T.float64)
+                if not n.last:
+                    self.act_fmt[n.name] = self._fmt()
+                    self.act_codes[n.name] = self._empty((B, Ho, Wo, n.cout), T.int8)
+                    shapes[n.name] = (Ho, Wo, n.cout)
+                self.ops.append((n.op, n, p))
+            elif n.op == "maxpool":
+                H, W, C = shapes[n.inp]
+                Ho, Wo = (H + 2 * n.pad - n.k) // n.stride + 1, (W + 2 * n.pad - n.k) // n.stride + 1
+                self.act_fmt[n.name] = self.act_fmt[n.inp]
+                self.act_codes[n.name] = self._empty((B, Ho, Wo, C), T.int8)
+                shapes[n.name] = (Ho, Wo, C)
+                self.ops.append(("maxpool", n, {"H": H, "W": W, "C": C}))
+            elif n.op == "add":
+                shapes[n.name] = shapes[n.inp]
+                self.act_fmt[n.name] = self._fmt()
+                self.act_codes[n.name] = self._empty((B,) + shapes[n.inp], T.int8)
+                self.ops.append(("add", n, {}))
+            elif n.op == "avgpool":
+                H, W, C = shapes[n.inp]
+                r = np.array([np.float32(1.0) / np.float32(H * W)], np.float32)
+                rcodes, rfmt = self._quant_param("avgpool.recip", np.repeat(r, 4), RECIP_WL, fx.I32)
+                self.ops.append(("avgpool", n, {"HW": H * W, "C": C, "rcodes": rcodes,
+                                                "sum": self._empty((B, C), T.int64),
+                                                "scale": self._empty((1,), T.int32)}))
+                shapes[n.name] = (1, 1, C)
+                self.act_fmt[n.name] = self._fmt()
+                self.act_codes[n.name] = self._empty((B, 1, 1, C), T.int8)
+        self.acc = self._empty((acc_max,), T.int32)
+        self.logits = None
+        # parameter formats back to the host (once)
+        T.cuda.synchronize(self.dev)
+        for key, f in self._pending.items():
+            wl, fl, sign, st = (int(v) for v in f.cpu().numpy())
+            if st:
+                raise RuntimeError(f"parameter {key}: fractional-length search failed ({st})")
+            self.param_fmts[key] = (wl, fl, sign)
+        for op, n, *rest in self.ops:
+            if op in ("conv", "fc"):
+                p = rest[0]
+                fin = self.act_fmt[n.inp]
+                fw = self.param_fmts[n.name + ".w"][1]
+                kw = {}
+                if n.bias:
+                    kw.update(bias=p["b"], fl_bias=self.param_fmts[n.name + ".b"][1])
+                if getattr(n, "bn", False):
+                    kw.update(scale=p["a1"], fl_scale=self.param_fmts[n.name + ".a1"][1],
+                              shift=p["a2"], fl_shift=self.param_fmts[n.name + ".a2"][1])
+                p["ep"] = fx.epilogue(n.cout, fw, fin, relu=n.relu, **kw)
+                if n.last:
+                    p["logit_fmt"] = self._t(np.array([32, 0, 1, 0], np.int32))
+                    self.logits = self._empty((p["M"], n.cout), T.int32)
+            elif op == "avgpool":
+                p = rest[0]
+                p["recip"] = int(p["rcodes"].cpu().numpy()[0])
+                p["ep_scale"] = fx.epilogue(p["C"], self.param_fmts["avgpool.recip"][1],
+                                            self.act_fmt[n.inp])
+        self.n_input = self.x_dev.numel()
+        self.le_out = self._empty((4,), T.float64)
+
+    # -- forward ---------------------------------------------------------------
+    def forward(self):
+        h, B = self.h, self.batch
+        for op, n, *rest in self.ops:
+            if op == "input":
+                f, c = self.act_fmt["input"], self.act_codes["input"]
+                src = fx.src_f32(self.x_dev)
+                fx.fl_search(h, src, self.n_input, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+                fx.quantize(h, self.x_dev, self.n_input, f, c, fx.C8)
+                fx.layer_error(h, self.x_dev, c, fx.C8, f, self.n_input, self.le_out)
+            elif op in ("conv", "fc"):
+                p = rest[0]
+                xin = self.act_codes[n.inp]
+                n_out = p["M"] * n.cout
+                acc = self.acc[:n_out]
+                if op == "conv":
+                    fx.qconv(h, p["desc"], xin, fx.C8, p["w"], p["colsum"], p["ep"], acc, p["mm"])
+                else:
+                    fx.qgemm(h, p["M"], n.cout, p["wlen"], xin, fx.C8, p["w"], p["colsum"], p["ep"],
+                             acc, p["mm"])
+                src = fx.src_acc(acc, p["ep"], p["mm"])
+                if n.last:
+                    fx.epilogue_scale(h, p["ep"], p["logit_fmt"][1:])
+                    fx.requant(h, src, n_out, p["logit_fmt"], self.logits, fx.I32)
+                else:
+                    f = self.act_fmt[n.name]
+                    fx.fl_search(h, src, n_out, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+                    fx.requant(h, src, n_out, f, self.act_codes[n.name], fx.C8)
+            elif op == "maxpool":
+                p = rest[0]
+                fx.maxpool(h, self.act_codes[n.inp], fx.C8, B, p["H"], p["W"], p["C"], n.k, n.stride,
+                           n.pad, self.act_codes[n.name])
+            elif op == "add":
+                a, b = self.act_codes[n.inp], self.act_codes[n.other]
+                src = fx.src_add(a, fx.C8, self.act_fmt[n.inp], b, fx.C8, self.act_fmt[n.other], n.relu)
+                f = self.act_fmt[n.name]
+                fx.fl_search(h, src, a.numel(), A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+                fx.requant(h, src, a.numel(), f, self.act_codes[n.name], fx.C8)
+            elif op == "avgpool":
+                p = rest[0]
+                fx.avgpool_global(h, self.act_codes[n.inp], fx.C8, self.act_fmt[n.inp], B, p["HW"],
+                                  p["C"], p["recip"], p["sum"])
+                fx.epilogue_scale(h, p["ep_scale"], p["scale"])
+                src = fx.src_int(p["sum"], fx.I64, p["scale"])
+                f = self.act_fmt[n.name]
+                fx.fl_search(h, src, p["sum"].numel(), A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+                fx.requant(h, src, p["sum"].numel(), f, self.act_codes[n.name], fx.C8)
+
+    # -- results ---------------------------------------------------------------
+    def results(self, with_codes=False):
+        T = self.torch
+        T.cuda.synchronize(self.dev)
+        flags = fx.sync_status(self.h)
+        fmts = dict(self.param_fmts)
+        for name, f in self.act_fmt.items():
+            if name.startswith("pool"):
+                continue
+            wl, fl, sign, st = (int(v) for v in f.cpu().numpy())
+            fmts[name] = (wl, fl, sign)
+        last = [p for op, n, *r in self.ops if op in ("conv", "fc") and n.last for p in r][0]
+        out = {"fmts": fmts, "logits": self.logits.cpu().numpy().astype(np.int64),
+               "logit_fl": int(last["logit_fmt"].cpu().numpy()[1]), "flags": flags,
+               "input_error": self.le_out.cpu().numpy()}
+        if with_codes:
+            codes = {}
+            for name, c in self.act_codes.items():
+                if name.startswith("pool"):
+                    continue
+                sign = fmts[name][2]
+                a = c.cpu().numpy().astype(np.int64)
+                codes[name] = a + 128 if sign == 0 else a
+            out["codes"] = codes
+        return out
+
+    def close(self):
+        self.h.close()
+
+
+def run_fc(seed=0, device="cuda:0"):
+    """BASELINE config 1: one FC layer, W and A quantized at WL 8, 6 and 4, the
+    int32 product requantized to WL 8 with its own search."""
+    import torch
+    dev = torch.device(device)
+    h = fx.Handle(dev.index or 0)
+    fx.set_stream(h, torch.cuda.current_stream(dev))
+    W = synth.normal(seed, "fc.w", (256, 512), std=0.05)
+    A = synth.relu_normal(seed, "fc.a", (32, 512))
+    Wd = torch.from_numpy(W.ravel()).to(dev)
+    Ad = torch.from_numpy(A.ravel()).to(dev)
+    fmts, outs, keep = {}, {}, []
+    for wl in (8, 6, 4):
+        fw = torch.zeros(4, dtype=torch.int32, device=dev)
+        fa = torch.zeros(4, dtype=torch.int32, device=dev)
+        fy = torch.zeros(4, dtype=torch.int32, device=dev)
+        fx.fl_search(h, fx.src_f32(Wd), Wd.numel(), wl, fx.SIGN_AUTO, FL_LO, FL_HI, fw)
+        fx.fl_search(h, fx.src_f32(Ad), Ad.numel(), wl, fx.SIGN_AUTO, FL_LO, FL_HI, fa)
+        wc = torch.empty(Wd.numel(), dtype=torch.int8, device=dev)
+        ac = torch.empty(Ad.numel(), dtype=torch.int8, device=dev)
+        fx.quantize(h, Wd, Wd.numel(), fw, wc, fx.I8)
+        fx.quantize(h, Ad, Ad.numel(), fa, ac, fx.C8)
+        cs = torch.empty(256, dtype=torch.int32, device=dev)
+        fx.weight_colsum(h, wc, 256, 512, cs)
+        torch.cuda.synchronize(dev)
+        fl_w = int(fw.cpu()[1])
+        ep = fx.epilogue(256, fl_w, fa)
+        acc = torch.empty((32, 256), dtype=torch.int32, device=dev)
+        mm = torch.empty(2, dtype=torch.float64, device=dev)
+        fx.qgemm(h, 32, 256, 512, ac, fx.C8, wc, cs, ep, acc, mm)
+        src = fx.src_acc(acc, ep, mm)
+        fx.fl_search(h, src, acc.numel(), 8, fx.SIGN_AUTO, FL_LO, FL_HI, fy)
+        yc = torch.empty(acc.numel(), dtype=torch.int8, device=dev)
+        fx.requant(h, src, acc.numel(), fy, yc, fx.C8)
+        torch.cuda.synchronize(dev)
+        for key, f in (("w", fw), ("a", fa), ("y", fy)):
+            wl_, fl_, sg_, st_ = (int(v) for v in f.cpu().numpy())
+            fmts[f"wl{wl}.{key}"] = (wl_, fl_, sg_)
+        sy = fmts[f"wl{wl}.y"][2]
+        outs[wl] = {"acc": acc.cpu().numpy().astype(np.int64),
+                    "y": yc.cpu().numpy().astype(np.int64) + (128 if sy == 0 else 0)}
+        keep += [fw, fa, fy, wc, ac, cs, acc, mm, yc]
+    flags = fx.sync_status(h)
+    h.close()
+    return {"fmts": fmts, "logits": outs[8]["y"], "outs": outs, "flags": flags}
+
+
+def run_config(name, seed=None, device="cuda:0", batch=None, image=None, with_codes=False,
+               wl_override=None):
+    if name == "fc":
+        return run_fc(SEEDS["fc"] if seed is None else seed, device)
+    net = CalibNet(name, seed, batch, image, device, wl_override=wl_override)
+    net.forward()
+    res = net.results(with_codes=with_codes)
+    net.close()
+    return res

@@ -192,9 +192,9 @@ def test_fl_search_int_sources(fx, h, orc):
 # ----------------------------------------------------------------------------
 def make_epilogue_params(seed, k, with_bias, with_scale):
     g = synth.rng_for(seed, "epi")
-    bias = g.integers(-2 ** 20, 2 ** 20, k).astype(np.int64) if with_bias else None
-    a1 = g.integers(2 ** 14, 2 ** 16, k).astype(np.int64) if with_scale else None
-    a2 = g.integers(-2 ** 13, 2 ** 13, k).astype(np.int64) if with_scale else None
+    bias = g.integers(-2 ** 20, 2 ** 20, k).astype(np.int32) if with_bias else None
+    a1 = g.integers(2 ** 14, 2 ** 16, k).astype(np.int32) if with_scale else None
+    a2 = g.integers(-2 ** 13, 2 ** 13, k).astype(np.int32) if with_scale else None
     return bias, a1, a2
 
 
