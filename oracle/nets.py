@@ -30,17 +30,26 @@ SHAPE = {"alexnet": (64, 224), "vgg16": (128, 224), "resnet18": (256, 224), "res
 class Forward:
     """Runs one network exactly on the CPU and records every chosen format."""
 
-    def __init__(self, seed):
+    def __init__(self, seed, pcache=None):
         self.seed = seed
+        self.pcache = pcache  # optional: quantized parameters from an earlier run
         self.fmts = {}
         self.codes = {}
         self.act = {}  # name -> (codes NCHW int32, fl, sign)
 
     # ---- parameters ----
     def qparam(self, key, x, wl):
+        ck = (key, x.shape, wl)
+        if self.pcache is not None and ck in self.pcache:
+            q, fl, fmt = self.pcache[ck]
+            self.fmts[key] = fmt
+            return q, fl
         fl, sign, _ = orc.fl_search_f32(x.ravel(), wl, orc.SIGN_AUTO, *FL)
         self.fmts[key] = (wl, fl, sign)
-        return orc.quantize_f32(x, wl, fl, sign).astype(np.int64), fl
+        q = orc.quantize_f32(x, wl, fl, sign).astype(np.int64)
+        if self.pcache is not None:
+            self.pcache[ck] = (q, fl, self.fmts[key])
+        return q, fl
 
     def fxp_qlayer(self, name, v, s, wl=8):
         fl, sign, _ = orc.fl_search_i64(v.ravel(), s, wl, orc.SIGN_AUTO, *FL)
@@ -194,14 +203,36 @@ def run_fc(seed=0):
     return {"fmts": fmts, "logits": outs[8]["y"], "outs": outs}
 
 
-def run_config(name, seed=None, batch=None, image=None):
+BODY = {"alexnet": alexnet, "vgg16": vgg16, "resnet18": lambda q: resnet(q, False),
+        "resnet50": lambda q: resnet(q, True)}
+
+
+def run_config(name, seed=None, batch=None, image=None, pcache=None):
     seed = SEED[name] if seed is None else seed
     if name == "fc":
         return run_fc(seed)
     b0, s0 = SHAPE[name]
     batch, image = batch or b0, image or s0
-    f = Forward(seed)
+    f = Forward(seed, pcache)
     f.network_input(synth.normal(seed, "input", (batch, 3, image, image)))
-    {"alexnet": alexnet, "vgg16": vgg16, "resnet18": lambda q: resnet(q, False),
-     "resnet50": lambda q: resnet(q, True)}[name](f)
+    BODY[name](f)
     return f.result()
+
+
+class Prepared:
+    """A workload whose parameters are already quantized: run() times only the
+    calibration forward itself."""
+
+    def __init__(self, name, batch, image, seed=None):
+        self.name, self.batch, self.image = name, batch, image
+        self.seed = SEED[name] if seed is None else seed
+        self.pcache = {}
+        self.last = run_config(name, self.seed, batch, image, self.pcache)
+
+    def run(self):
+        self.last = run_config(self.name, self.seed, self.batch, self.image, self.pcache)
+        return self.last
+
+
+def prepare(name, batch, image, seed=None):
+    return Prepared(name, batch, image, seed)

@@ -18,7 +18,6 @@ constexpr int kGenChunks = 256;      // element chunks of the exact general sear
 // Device-resident state of one handle.  Offsets into one scratch allocation.
 struct Scratch {
   unsigned* flags;          // sticky FXPQ_FLAG_* bits
-  unsigned* counters;       // last-block-done counters (self-resetting)
   double* minmax;           // internal [2]
   double* minmax_part;      // per-block partials [kMaxConvBlocks][2]
   long long* win_part;      // window FL-search partials
@@ -26,8 +25,6 @@ struct Scratch {
   unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
   void* plan;               // FlsPlan
 };
-
-enum Counter { CNT_MINMAX = 0, CNT_CONV = 1, CNT_WIN = 2, CNT_GEN = 3, CNT_LERR = 4, CNT_MAX = 8 };
 
 // Everything a kernel needs to produce the value v_i of an FxP-QLayer input,
 // as an exact double (integers below 2^53), plus its fractional length.
@@ -114,6 +111,7 @@ struct Ctx {
 };
 
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out);
+hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* out);
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
                           int code_type);
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,

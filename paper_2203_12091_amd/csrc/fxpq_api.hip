@@ -150,7 +150,6 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
     return o;
   };
   size_t o_flags = take(4);
-  size_t o_cnt = take(sizeof(unsigned) * CNT_MAX);
   size_t o_mm = take(2 * sizeof(double));
   size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
   size_t o_wp = take((size_t)kMaxFlsBlocks * 3 * kWindow * sizeof(long long));
@@ -164,7 +163,6 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   h->scratch_bytes = off;
   char* base = static_cast<char*>(h->scratch);
   h->sc.flags = reinterpret_cast<unsigned*>(base + o_flags);
-  h->sc.counters = reinterpret_cast<unsigned*>(base + o_cnt);
   h->sc.minmax = reinterpret_cast<double*>(base + o_mm);
   h->sc.minmax_part = reinterpret_cast<double*>(base + o_mmp);
   h->sc.win_part = reinterpret_cast<long long*>(base + o_wp);

@@ -46,8 +46,6 @@ struct ConvArgs {
   SrcDev ep;    // kind == FXPQ_SRC_ACC when an epilogue is given
   int has_ep;
   double* mm_part;
-  unsigned* counter;
-  double* mm_out;
 };
 
 template <int BM, int BN, int LOADER>
@@ -235,21 +233,6 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
     a.mm_part[2 * bid] = mn;
     a.mm_part[2 * bid + 1] = mx;
   }
-  if (last_block_done(a.counter)) {
-    const int nb = gridDim.x * gridDim.y;
-    double p = INFINITY, q = -INFINITY;
-    for (int i = tid; i < nb; i += 256) {
-      p = fmin(p, ld_acquire(&a.mm_part[2 * i]));
-      q = fmax(q, ld_acquire(&a.mm_part[2 * i + 1]));
-    }
-    p = block_reduce(p, OpMin(), shd);
-    q = block_reduce(q, OpMax(), shd);
-    if (tid == 0) {
-      a.mm_out[0] = p;
-      a.mm_out[1] = q;
-    }
-    reset_counter(a.counter);
-  }
 }
 
 template <int BM, int BN>
@@ -284,15 +267,15 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   if (ep) a.ep = *ep;
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
-  a.counter = c.sc.counters + CNT_CONV;
-  a.mm_out = d_minmax;
+  dim3 grid;
   if (d.k <= 64) {
-    dim3 grid((a.M + 255) / 256, (d.k + 63) / 64);
+    grid = dim3((a.M + 255) / 256, (d.k + 63) / 64);
     conv_dispatch_loader<256, 64>(loader, grid, c.stream, a);
   } else {
-    dim3 grid((a.M + 127) / 128, (d.k + 127) / 128);
+    grid = dim3((a.M + 127) / 128, (d.k + 127) / 128);
     conv_dispatch_loader<128, 128>(loader, grid, c.stream, a);
   }
+  if (a.want_mm) return launch_minmax_fin(c, a.mm_part, (int)(grid.x * grid.y), d_minmax);
   return hipGetLastError();
 }
 

@@ -148,34 +148,48 @@ __device__ inline FlsU fls_uniform(const SrcDev& s, const double* mm, int wl, in
 // ---------------------------------------------------------------------------
 // Pass 1: window search.
 // ---------------------------------------------------------------------------
+struct WinSetup {
+  FlsU u;
+  int verdict;  // 0: run window; 1: done (fl_hi); 2: general for all; 3: failure
+  int b0, b1, nc, bce;
+};
+
+template <int KIND>
+__device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, int sign_req,
+                                     int fl_lo, int fl_hi, int mode) {
+  WinSetup w;
+  w.u = fls_uniform<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi);
+  w.verdict = 0;
+  if (!w.u.ok) w.verdict = 3;
+  else if (mode == MODE_REPORT || wl > 16 || w.u.absmax * w.u.wscale >= kTwo52) w.verdict = 2;
+  else if (w.u.beta_nosat >= fl_hi) w.verdict = 1;
+  w.b0 = imax(fl_lo, w.u.beta_nosat);
+  w.b1 = (w.b0 + kWindow - 1 < fl_hi) ? w.b0 + kWindow - 1 : fl_hi;
+  w.nc = w.b1 - w.b0 + 1;
+  w.bce = (w.b1 < fl_hi) ? w.b1 + 1 : w.b1;
+  return w;
+}
+
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_fls_window(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode,
-    const double* mm, long long* part_i, double* part_f, unsigned* counter, FlsPlan* plan,
-    fxpq_fmt* out, unsigned* flags) {
+    const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out,
+    unsigned* flags) {
   __shared__ long long shl[8];
   __shared__ double shd[8];
-  const FlsU u = fls_uniform<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi);
-  const bool lead = (blockIdx.x == 0 && threadIdx.x == 0);
+  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode);
+  const FlsU& u = ws.u;
 
   // Decisions every block takes identically before touching the data.
-  int verdict = 0;  // 0: run window; 1: done (fl_hi); 2: general for all; 3: failure
-  if (!u.ok) {
-    verdict = 3;
-  } else if (mode == MODE_REPORT || wl > 16 || u.absmax * u.wscale >= kTwo52) {
-    verdict = 2;
-  } else if (u.beta_nosat >= fl_hi) {
-    verdict = 1;
-  }
-  if (verdict != 0) {
-    if (lead) {
+  if (ws.verdict != 0) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) {
       plan->sign = u.sign;
       plan->status = 0;
       plan->need_general = 0;
       plan->gen_extra = INT_MIN;
-      if (verdict == 1) {
+      if (ws.verdict == 1) {
         *out = fxpq_fmt{wl, fl_hi, u.sign, 0};
-      } else if (verdict == 2) {
+      } else if (ws.verdict == 2) {
         plan->need_general = 1;
         plan->gen_lo = fl_lo;
         plan->gen_hi = fl_hi;
@@ -188,14 +202,11 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     return;
   }
 
-  const int b0 = imax(fl_lo, u.beta_nosat);
-  const int b1 = (b0 + kWindow - 1 < fl_hi) ? b0 + kWindow - 1 : fl_hi;
-  const int nc = b1 - b0 + 1;
-  const int bce = (b1 < fl_hi) ? b1 + 1 : b1;
+  const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc;
   double cj[kWindow];
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) cj[j] = ldexp(1.0, (j < nc ? b0 + j : b1) - u.sigma);
-  const double cce = ldexp(1.0, bce - u.sigma);
+  const double cce = ldexp(1.0, ws.bce - u.sigma);
   const double qmin = u.qmin, qmax = u.qmax;
 
   double A[kWindow], PH[kWindow], PL[kWindow];
@@ -255,19 +266,27 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     part_f[2 * blockIdx.x] = v2;
     part_f[2 * blockIdx.x + 1] = ce;
   }
+}
 
-  if (!last_block_done(counter)) return;
-
-  // ---- finalize (last block) ----
-  // Sum the block partials exactly: each partial < 2^61 in magnitude, split in
-  // 32-bit halves so the per-thread int64 sums cannot overflow.
+// One block: sums the window partials exactly and decides.
+template <int KIND>
+__global__ __launch_bounds__(kThreads) void k_fls_window_fin(
+    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, const double* mm,
+    const long long* part_i, const double* part_f, int nb, FlsPlan* plan, fxpq_fmt* out) {
+  __shared__ long long shl[8];
+  __shared__ double shd[8];
   __shared__ long long tot_hi[3 * kWindow], tot_lo[3 * kWindow];
   __shared__ double tot_f[2];
-  const int nb = gridDim.x;
+  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode);
+  if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
+  const FlsU& u = ws.u;
+  const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc, bce = ws.bce;
+  // Each block partial is below 2^61 in magnitude; split into 32-bit halves so
+  // the per-thread int64 sums cannot overflow.
   for (int qi = 0; qi < 3 * kWindow; ++qi) {
     long long hi = 0, lo = 0;
     for (int b = threadIdx.x; b < nb; b += kThreads) {
-      long long x = ld_acquire(&part_i[(int64_t)b * (3 * kWindow) + qi]);
+      long long x = part_i[(int64_t)b * (3 * kWindow) + qi];
       hi += x >> 32;
       lo += x & 0xFFFFFFFFll;
     }
@@ -280,58 +299,56 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
   }
   for (int qi = 0; qi < 2; ++qi) {
     double x = 0.0;
-    for (int b = threadIdx.x; b < nb; b += kThreads) x += ld_acquire(&part_f[2 * b + qi]);
+    for (int b = threadIdx.x; b < nb; b += kThreads) x += part_f[2 * b + qi];
     x = block_reduce(x, OpAddD(), shd);
     if (threadIdx.x == 0) tot_f[qi] = x;
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
-    auto total = [&](int qi) -> __int128 {
-      return ((__int128)tot_hi[qi] << 32) + (__int128)tot_lo[qi];
-    };
-    // K_j = 2^(2d) A - 2^(d+1) P, d = sigma - beta; shifted by `off` >= 0 so all
-    // exponents are non-negative (same factor for every candidate).
-    int dmin = u.sigma - b1;
-    int off = 0;
-    if (2 * dmin < 0) off = -2 * dmin;
-    if (dmin + 1 + off < 0) off = -(dmin + 1);
-    Big best;
-    int bj = -1;
-    for (int j = 0; j < nc; ++j) {
-      int d = u.sigma - (b0 + j);
-      __int128 Aj = total(3 * j);
-      __int128 Pj = total(3 * j + 1) * (__int128)67108864 + total(3 * j + 2);
-      Big k = big_sub(big_shl(big_from_i128(Aj), 2 * d + off), big_shl(big_from_i128(Pj), d + 1 + off));
-      if (bj < 0 || big_cmp(k, best) <= 0) {  // ties -> larger fl
-        best = k;
-        bj = j;
-      }
-    }
-    const int fl_win = b0 + bj;
-    bool done = (b1 == fl_hi);
-    if (!done) {
-      // Upper bound of the window's best error, lower bound of every error
-      // above the window (relative fp64 error of each sum < 2^-33).
-      double kd = ldexp(big_to_double(best), -off);
-      double v2 = tot_f[0];
-      double sse_ub = (v2 * (1.0 + 0x1p-30) + kd + fabs(kd) * 0x1p-50 + v2 * 0x1p-50);
-      sse_ub = ldexp(sse_ub, -2 * u.sigma) * (1.0 + 0x1p-50);
-      double ce_lb = ldexp(tot_f[1] * (1.0 - 0x1p-30), -2 * bce);
-      done = ce_lb > sse_ub;
-    }
-    plan->sign = u.sign;
-    plan->status = 0;
-    if (done) {
-      plan->need_general = 0;
-      *out = fxpq_fmt{wl, fl_win, u.sign, 0};
-    } else {
-      plan->need_general = 1;
-      plan->gen_lo = b1 + 1;
-      plan->gen_hi = fl_hi;
-      plan->gen_extra = fl_win;
+  if (threadIdx.x != 0) return;
+  auto total = [&](int qi) -> __int128 {
+    return ((__int128)tot_hi[qi] << 32) + (__int128)tot_lo[qi];
+  };
+  // K_j = 2^(2d) A - 2^(d+1) P, d = sigma - beta; shifted by `off` >= 0 so all
+  // exponents are non-negative (same factor for every candidate).
+  int dmin = u.sigma - b1;
+  int off = 0;
+  if (2 * dmin < 0) off = -2 * dmin;
+  if (dmin + 1 + off < 0) off = -(dmin + 1);
+  Big best;
+  int bj = -1;
+  for (int j = 0; j < nc; ++j) {
+    int d = u.sigma - (b0 + j);
+    __int128 Aj = total(3 * j);
+    __int128 Pj = total(3 * j + 1) * (__int128)67108864 + total(3 * j + 2);
+    Big k = big_sub(big_shl(big_from_i128(Aj), 2 * d + off), big_shl(big_from_i128(Pj), d + 1 + off));
+    if (bj < 0 || big_cmp(k, best) <= 0) {  // ties -> larger fl
+      best = k;
+      bj = j;
     }
   }
-  reset_counter(counter);
+  const int fl_win = b0 + bj;
+  bool done = (b1 == fl_hi);
+  if (!done) {
+    // Upper bound of the window's best error, lower bound of every error above
+    // the window (relative fp64 error of each sum < 2^-33).
+    double kd = ldexp(big_to_double(best), -off);
+    double v2 = tot_f[0];
+    double sse_ub = (v2 * (1.0 + 0x1p-30) + kd + fabs(kd) * 0x1p-50 + v2 * 0x1p-50);
+    sse_ub = ldexp(sse_ub, -2 * u.sigma) * (1.0 + 0x1p-50);
+    double ce_lb = ldexp(tot_f[1] * (1.0 - 0x1p-30), -2 * bce);
+    done = ce_lb > sse_ub;
+  }
+  plan->sign = u.sign;
+  plan->status = 0;
+  if (done) {
+    plan->need_general = 0;
+    *out = fxpq_fmt{wl, fl_win, u.sign, 0};
+  } else {
+    plan->need_general = 1;
+    plan->gen_lo = b1 + 1;
+    plan->gen_hi = fl_hi;
+    plan->gen_extra = fl_win;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -368,8 +385,7 @@ __device__ inline double u192_to_double(const U192& a) {
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_fls_general(
     SrcDev s, int64_t n, int wl, int fl_lo, int fl_hi, int nchunks, const double* mm,
-    const FlsPlan* plan, unsigned long long* part, unsigned* counter, fxpq_fmt* out,
-    double* d_sse, unsigned* flags) {
+    const FlsPlan* plan, unsigned long long* part, fxpq_fmt* out, unsigned* flags) {
   __shared__ unsigned long long shp[kThreads * 3];
   if (!plan->need_general || plan->status) return;
   const int sign = plan->sign;
@@ -448,28 +464,49 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
     __syncthreads();
   }
 
-  if (!last_block_done(counter)) return;
-  if (threadIdx.x == 0) {
-    U192 best{0, 0};
-    int bbeta = INT_MIN;
-    for (int j = 0; j < nc; ++j) {
-      U192 t{0, 0};
-      for (int ch = 0; ch < nchunks; ++ch) {
-        const unsigned long long* p = part + ((int64_t)j * kGenChunks + ch) * 3;
-        U192 x{((unsigned __int128)ld_acquire(&p[1]) << 64) | ld_acquire(&p[0]), ld_acquire(&p[2])};
-        u192_add(t, x);
-      }
-      int beta = cand(j);
-      int c = (bbeta == INT_MIN) ? -1 : u192_cmp(t, best);
-      if (c < 0 || (c == 0 && beta > bbeta)) {
-        best = t;
-        bbeta = beta;
-      }
-      if (d_sse && beta >= fl_lo && beta <= fl_hi) d_sse[beta - fl_lo] = ldexp(u192_to_double(t), -2 * sigma);
+}
+
+// One block: totals per candidate, exact comparison, ties to the larger fl.
+__global__ __launch_bounds__(kThreads) void k_fls_general_fin(int wl, int fl_lo, int fl_hi, int sigma_f32,
+                                                              int nchunks, const SrcDev s, int kind,
+                                                              const FlsPlan* plan,
+                                                              const unsigned long long* part,
+                                                              fxpq_fmt* out, double* d_sse) {
+  __shared__ unsigned long long tot[kMaxCand][3];
+  if (!plan->need_general || plan->status) return;
+  const int sign = plan->sign;
+  const int glo = plan->gen_lo, ghi = plan->gen_hi, extra = plan->gen_extra;
+  const int nc = ghi - glo + 1 + (extra != INT_MIN ? 1 : 0);
+  auto cand = [&](int j) { return (extra != INT_MIN) ? (j == 0 ? extra : glo + j - 1) : glo + j; };
+  for (int j = threadIdx.x; j < nc; j += kThreads) {
+    U192 t{0, 0};
+    for (int ch = 0; ch < nchunks; ++ch) {
+      const unsigned long long* p = part + ((int64_t)j * kGenChunks + ch) * 3;
+      U192 x{((unsigned __int128)p[1] << 64) | p[0], p[2]};
+      u192_add(t, x);
     }
-    *out = fxpq_fmt{wl, bbeta, sign, 0};
+    tot[j][0] = (unsigned long long)t.lo;
+    tot[j][1] = (unsigned long long)(t.lo >> 64);
+    tot[j][2] = t.hi;
   }
-  reset_counter(counter);
+  __syncthreads();
+  if (threadIdx.x != 0) return;
+  const int sv = (kind == FXPQ_SRC_F32) ? 0 : src_scale(s);
+  const int sigma = (kind == FXPQ_SRC_F32) ? sigma_f32 : imax(sv, fl_hi);
+  U192 best{0, 0};
+  int bbeta = INT_MIN;
+  for (int j = 0; j < nc; ++j) {
+    U192 t{((unsigned __int128)tot[j][1] << 64) | tot[j][0], tot[j][2]};
+    int beta = cand(j);
+    int c = (bbeta == INT_MIN) ? -1 : u192_cmp(t, best);
+    if (c < 0 || (c == 0 && beta > bbeta)) {
+      best = t;
+      bbeta = beta;
+    }
+    if (d_sse && beta >= fl_lo && beta <= fl_hi)
+      d_sse[beta - fl_lo] = ldexp(u192_to_double(t), -2 * sigma);
+  }
+  *out = fxpq_fmt{wl, bbeta, sign, 0};
 }
 
 // ---------------------------------------------------------------------------
@@ -499,15 +536,21 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
                         s, n, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part,
-                        c.sc.win_part_f, c.sc.counters + CNT_WIN, plan, out, c.sc.flags)));
+                        c.sc.win_part_f, plan, out, c.sc.flags)));
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_fls_window_fin<K_><<<1, kThreads, 0, c.stream>>>(
+                        s, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part, c.sc.win_part_f,
+                        blocks, plan, out)));
   int nchunks = (int)((n + 65535) / 65536);
   if (nchunks > kGenChunks) nchunks = kGenChunks;
   if (nchunks < 1) nchunks = 1;
   int gblocks = 240;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_general<K_, D_><<<gblocks, kThreads, 0, c.stream>>>(
-                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part,
-                        c.sc.counters + CNT_GEN, out, d_sse, c.sc.flags)));
+                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part, out,
+                        c.sc.flags)));
+  k_fls_general_fin<<<1, kThreads, 0, c.stream>>>(wl, fl_lo, fl_hi, fl_hi + 24, nchunks, s, s.kind,
+                                                  plan, c.sc.gen_part, out, d_sse);
   return hipGetLastError();
 }
 

@@ -42,7 +42,6 @@ int stream_grid(int64_t n, int channels, int64_t max_per_thread) {
 // ----------------------------------------------------------------------------
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_minmax(SrcDev s, int64_t n, double* part,
-                                                     unsigned* counter, double* out,
                                                      unsigned* flags) {
   __shared__ double sh[8];
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -79,25 +78,31 @@ __global__ __launch_bounds__(kThreads) void k_minmax(SrcDev s, int64_t n, double
     part[2 * blockIdx.x + 1] = mx;
     if (any_bad) raise_flag(flags, FXPQ_FLAG_NONFINITE);
   }
-  if (last_block_done(counter)) {
-    double a = INFINITY, b = -INFINITY;
-    bool nan_seen = false;
-    for (int i = threadIdx.x; i < (int)gridDim.x; i += kThreads) {
-      double p0 = ld_acquire(&part[2 * i]);
-      double p1 = ld_acquire(&part[2 * i + 1]);
-      nan_seen |= isnan(p0);
-      a = fmin(a, p0);
-      b = fmax(b, p1);
-    }
-    int nan_any = __syncthreads_or(nan_seen);
-    a = block_reduce(a, OpMin(), sh);
-    b = block_reduce(b, OpMax(), sh);
-    if (threadIdx.x == 0) {
-      out[0] = nan_any ? NAN : a;
-      out[1] = b;
-    }
-    reset_counter(counter);
+}
+
+// One block: reduces nb (min, max) partials; a NaN partial marks non-finite input.
+__global__ __launch_bounds__(kThreads) void k_minmax_fin(const double* part, int nb, double* out) {
+  __shared__ double sh[8];
+  double a = INFINITY, b = -INFINITY;
+  bool nan_seen = false;
+  for (int i = threadIdx.x; i < nb; i += kThreads) {
+    double p0 = part[2 * i], p1 = part[2 * i + 1];
+    nan_seen |= isnan(p0);
+    a = fmin(a, p0);
+    b = fmax(b, p1);
   }
+  int nan_any = __syncthreads_or(nan_seen);
+  a = block_reduce(a, OpMin(), sh);
+  b = block_reduce(b, OpMax(), sh);
+  if (threadIdx.x == 0) {
+    out[0] = nan_any ? NAN : a;
+    out[1] = b;
+  }
+}
+
+hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* out) {
+  k_minmax_fin<<<1, kThreads, 0, c.stream>>>(part, nb, out);
+  return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
@@ -211,8 +216,7 @@ __device__ inline double code_at(const void* codes, int64_t i) {
 template <int CT>
 __global__ __launch_bounds__(kThreads) void k_layer_error(const float* ref, const void* codes,
                                                           const fxpq_fmt* fmt, int64_t n,
-                                                          double* part, unsigned* counter,
-                                                          double* out) {
+                                                          double* part) {
   __shared__ double sh[8];
   const double step = ldexp(1.0, -fmt->fl);
   const double off = (CT == FXPQ_U8OFF || (CT == FXPQ_C8 && fmt->sign == 0)) ? 128.0 : 0.0;
@@ -237,30 +241,32 @@ __global__ __launch_bounds__(kThreads) void k_layer_error(const float* ref, cons
     double* p = part + 5 * blockIdx.x;
     p[0] = sse; p[1] = mn; p[2] = mx; p[3] = s1; p[4] = s2;
   }
-  if (last_block_done(counter)) {
-    double a = 0.0, b = INFINITY, c = -INFINITY, d = 0.0, e = 0.0;
-    for (int i = threadIdx.x; i < (int)gridDim.x; i += kThreads) {
-      const double* p = part + 5 * i;
-      a += ld_acquire(&p[0]);
-      b = fmin(b, ld_acquire(&p[1]));
-      c = fmax(c, ld_acquire(&p[2]));
-      d += ld_acquire(&p[3]);
-      e += ld_acquire(&p[4]);
-    }
-    a = block_reduce(a, OpAddD(), sh);
-    b = block_reduce(b, OpMin(), sh);
-    c = block_reduce(c, OpMax(), sh);
-    d = block_reduce(d, OpAddD(), sh);
-    e = block_reduce(e, OpAddD(), sh);
-    if (threadIdx.x == 0) {
-      double mean = d / (double)n;
-      double var = e / (double)n - mean * mean;
-      out[0] = a;
-      out[1] = b;
-      out[2] = c;
-      out[3] = sqrt(var > 0.0 ? var : 0.0);
-    }
-    reset_counter(counter);
+}
+
+__global__ __launch_bounds__(kThreads) void k_layer_error_fin(const double* part, int nb, int64_t n,
+                                                              double* out) {
+  __shared__ double sh[8];
+  double a = 0.0, b = INFINITY, c = -INFINITY, d = 0.0, e = 0.0;
+  for (int i = threadIdx.x; i < nb; i += kThreads) {
+    const double* p = part + 5 * i;
+    a += p[0];
+    b = fmin(b, p[1]);
+    c = fmax(c, p[2]);
+    d += p[3];
+    e += p[4];
+  }
+  a = block_reduce(a, OpAddD(), sh);
+  b = block_reduce(b, OpMin(), sh);
+  c = block_reduce(c, OpMax(), sh);
+  d = block_reduce(d, OpAddD(), sh);
+  e = block_reduce(e, OpAddD(), sh);
+  if (threadIdx.x == 0) {
+    double mean = d / (double)n;
+    double var = e / (double)n - mean * mean;
+    out[0] = a;
+    out[1] = b;
+    out[2] = c;
+    out[3] = sqrt(var > 0.0 ? var : 0.0);
   }
 }
 
@@ -365,8 +371,9 @@ static int src_channels(const SrcDev& s) { return s.kind == FXPQ_SRC_ACC ? s.cha
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) {
   int blocks = stream_grid(n, src_channels(s), 0);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
-                        s, n, c.sc.minmax_part, c.sc.counters + CNT_MINMAX, out, c.sc.flags)));
+                    (k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(s, n, c.sc.minmax_part,
+                                                                        c.sc.flags)));
+  k_minmax_fin<<<1, kThreads, 0, c.stream>>>(c.sc.minmax_part, blocks, out);
   return hipGetLastError();
 }
 
@@ -395,24 +402,24 @@ hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes,
                               const fxpq_fmt* fmt, int64_t n, double* out) {
   int blocks = stream_grid(n, 0, 0);
   double* part = c.sc.minmax_part;  // 5 doubles per block fits (kMaxConvBlocks * 2)
-  unsigned* cnt = c.sc.counters + CNT_LERR;
   switch (code_type) {
     case FXPQ_I16:
-      k_layer_error<FXPQ_I16><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      k_layer_error<FXPQ_I16><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
       break;
     case FXPQ_I32:
-      k_layer_error<FXPQ_I32><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      k_layer_error<FXPQ_I32><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
       break;
     case FXPQ_U8OFF:
-      k_layer_error<FXPQ_U8OFF><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      k_layer_error<FXPQ_U8OFF><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
       break;
     case FXPQ_C8:
-      k_layer_error<FXPQ_C8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      k_layer_error<FXPQ_C8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
       break;
     default:
-      k_layer_error<FXPQ_I8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part, cnt, out);
+      k_layer_error<FXPQ_I8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
       break;
   }
+  k_layer_error_fin<<<1, kThreads, 0, c.stream>>>(part, blocks, n, out);
   return hipGetLastError();
 }
 

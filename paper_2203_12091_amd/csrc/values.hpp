@@ -132,32 +132,9 @@ struct OpAddL {
   __device__ long long operator()(long long a, long long b) const { return a + b; }
 };
 
-// Marks this block done; returns true in exactly one block (the last one).
-__device__ inline bool last_block_done(unsigned* counter) {
-  __shared__ bool is_last;
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    unsigned prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    is_last = (prev == gridDim.x * gridDim.y * gridDim.z - 1);
-  }
-  __syncthreads();
-  if (is_last) __threadfence();
-  return is_last;
-}
-
-__device__ inline void reset_counter(unsigned* counter) {
-  if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 __device__ inline void raise_flag(unsigned* flags, unsigned f) {
   __hip_atomic_fetch_or(flags, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Loads that bypass a possibly stale cache line (partials written by other blocks).
-template <typename T>
-__device__ inline T ld_acquire(const T* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 }  // namespace fxpq

@@ -151,6 +151,8 @@ class CalibNet:
                     n.wl = wl_override[n.name]
         self.keep = []
         self.param_fmts = {}
+        self.calls = None
+        self.timers = None
         self._build()
 
     # -- helpers --------------------------------------------------------------
@@ -303,52 +305,141 @@ class CalibNet:
         self.le_out = self._empty((4,), T.float64)
 
     # -- forward ---------------------------------------------------------------
-    def forward(self):
-        h, B = self.h, self.batch
+    def _plan(self):
+        """Pre-builds every library call of one forward: (class, work, fn, args).
+        `work` is the call's algorithmic HBM bytes (streaming calls) or int8
+        operations (conv / FC), used for the roofline report."""
+        import ctypes as C
+        L = fx.lib()
+        h, B = self.h.value, self.batch
+        calls = []
+
+        def add(cls, work, fn, *args):
+            calls.append((cls, work, fn, args))
+
+        keep = self.keep
         for op, n, *rest in self.ops:
             if op == "input":
                 f, c = self.act_fmt["input"], self.act_codes["input"]
                 src = fx.src_f32(self.x_dev)
-                fx.fl_search(h, src, self.n_input, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
-                fx.quantize(h, self.x_dev, self.n_input, f, c, fx.C8)
-                fx.layer_error(h, self.x_dev, c, fx.C8, f, self.n_input, self.le_out)
+                keep.append(src)
+                add("fl_search_f32", 4 * self.n_input, L.fxpq_fl_search, h, C.byref(src),
+                    self.n_input, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), None)
+                add("quantize", 5 * self.n_input, L.fxpq_quantize, h, self.x_dev.data_ptr(),
+                    self.n_input, f.data_ptr(), c.data_ptr(), fx.C8)
+                add("layer_error", 5 * self.n_input, L.fxpq_layer_error, h, self.x_dev.data_ptr(),
+                    c.data_ptr(), fx.C8, f.data_ptr(), self.n_input, self.le_out.data_ptr())
             elif op in ("conv", "fc"):
                 p = rest[0]
                 xin = self.act_codes[n.inp]
                 n_out = p["M"] * n.cout
                 acc = self.acc[:n_out]
+                keep.append(acc)
+                ops2 = 2 * n_out * p["wlen"]
                 if op == "conv":
-                    fx.qconv(h, p["desc"], xin, fx.C8, p["w"], p["colsum"], p["ep"], acc, p["mm"])
+                    add("qconv", ops2, L.fxpq_qconv, h, C.byref(p["desc"]), xin.data_ptr(), fx.C8,
+                        p["w"].data_ptr(), p["colsum"].data_ptr(), C.byref(p["ep"]), acc.data_ptr(),
+                        p["mm"].data_ptr())
                 else:
-                    fx.qgemm(h, p["M"], n.cout, p["wlen"], xin, fx.C8, p["w"], p["colsum"], p["ep"],
-                             acc, p["mm"])
+                    add("qconv", ops2, L.fxpq_qgemm, h, p["M"], n.cout, p["wlen"], xin.data_ptr(), fx.C8,
+                        p["w"].data_ptr(), p["colsum"].data_ptr(), C.byref(p["ep"]), acc.data_ptr(),
+                        p["mm"].data_ptr())
                 src = fx.src_acc(acc, p["ep"], p["mm"])
+                keep.append(src)
                 if n.last:
-                    fx.epilogue_scale(h, p["ep"], p["logit_fmt"][1:])
-                    fx.requant(h, src, n_out, p["logit_fmt"], self.logits, fx.I32)
+                    add("other", 0, L.fxpq_epilogue_scale, h, C.byref(p["ep"]),
+                        p["logit_fmt"].data_ptr() + 4)
+                    add("requant", 8 * n_out, L.fxpq_requant, h, C.byref(src), n_out,
+                        p["logit_fmt"].data_ptr(), self.logits.data_ptr(), fx.I32)
                 else:
                     f = self.act_fmt[n.name]
-                    fx.fl_search(h, src, n_out, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
-                    fx.requant(h, src, n_out, f, self.act_codes[n.name], fx.C8)
+                    add("fl_search", 4 * n_out, L.fxpq_fl_search, h, C.byref(src), n_out, A_WL,
+                        fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), None)
+                    add("requant", 5 * n_out, L.fxpq_requant, h, C.byref(src), n_out, f.data_ptr(),
+                        self.act_codes[n.name].data_ptr(), fx.C8)
             elif op == "maxpool":
                 p = rest[0]
-                fx.maxpool(h, self.act_codes[n.inp], fx.C8, B, p["H"], p["W"], p["C"], n.k, n.stride,
-                           n.pad, self.act_codes[n.name])
+                out = self.act_codes[n.name]
+                add("other", self.act_codes[n.inp].numel() + out.numel(), L.fxpq_maxpool, h,
+                    self.act_codes[n.inp].data_ptr(), fx.C8, B, p["H"], p["W"], p["C"], n.k, n.stride,
+                    n.pad, out.data_ptr())
             elif op == "add":
                 a, b = self.act_codes[n.inp], self.act_codes[n.other]
                 src = fx.src_add(a, fx.C8, self.act_fmt[n.inp], b, fx.C8, self.act_fmt[n.other], n.relu)
+                keep.append(src)
                 f = self.act_fmt[n.name]
-                fx.fl_search(h, src, a.numel(), A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
-                fx.requant(h, src, a.numel(), f, self.act_codes[n.name], fx.C8)
+                m = a.numel()
+                add("fl_search", 2 * m, L.fxpq_fl_search, h, C.byref(src), m, A_WL, fx.SIGN_AUTO,
+                    FL_LO, FL_HI, f.data_ptr(), None)
+                add("requant", 3 * m, L.fxpq_requant, h, C.byref(src), m, f.data_ptr(),
+                    self.act_codes[n.name].data_ptr(), fx.C8)
             elif op == "avgpool":
                 p = rest[0]
-                fx.avgpool_global(h, self.act_codes[n.inp], fx.C8, self.act_fmt[n.inp], B, p["HW"],
-                                  p["C"], p["recip"], p["sum"])
-                fx.epilogue_scale(h, p["ep_scale"], p["scale"])
+                add("other", self.act_codes[n.inp].numel(), L.fxpq_avgpool_global, h,
+                    self.act_codes[n.inp].data_ptr(), fx.C8, self.act_fmt[n.inp].data_ptr(), B, p["HW"],
+                    p["C"], p["recip"], p["sum"].data_ptr())
+                add("other", 0, L.fxpq_epilogue_scale, h, C.byref(p["ep_scale"]), p["scale"].data_ptr())
                 src = fx.src_int(p["sum"], fx.I64, p["scale"])
+                keep.append(src)
                 f = self.act_fmt[n.name]
-                fx.fl_search(h, src, p["sum"].numel(), A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
-                fx.requant(h, src, p["sum"].numel(), f, self.act_codes[n.name], fx.C8)
+                m = p["sum"].numel()
+                add("fl_search", 8 * m, L.fxpq_fl_search, h, C.byref(src), m, A_WL, fx.SIGN_AUTO,
+                    FL_LO, FL_HI, f.data_ptr(), None)
+                add("requant", 9 * m, L.fxpq_requant, h, C.byref(src), m, f.data_ptr(),
+                    self.act_codes[n.name].data_ptr(), fx.C8)
+        return calls
+
+    def forward(self):
+        """Enqueues one calibration forward (no host synchronization).  When
+        ``self.timers`` is a list, every call is bracketed by HIP events on the
+        library's stream and (class, work, start, end) is appended to it."""
+        if self.calls is None:
+            self.calls = self._plan()
+        timers = self.timers
+        if timers is None:
+            for cls, work, fn, args in self.calls:
+                st = fn(*args)
+                if st:
+                    raise fx.FxpqError(fn.__name__, st)
+            return
+        T = self.torch
+        for cls, work, fn, args in self.calls:
+            e0 = T.cuda.Event(enable_timing=True)
+            e1 = T.cuda.Event(enable_timing=True)
+            e0.record()
+            st = fn(*args)
+            e1.record()
+            if st:
+                raise fx.FxpqError(fn.__name__, st)
+            timers.append((cls, work, e0, e1))
+
+    def kernel_times(self):
+        """Per call class: (calls, total ms, total work) from the recorded events."""
+        self.torch.cuda.synchronize(self.dev)
+        agg = {}
+        for cls, work, e0, e1 in self.timers or []:
+            c, t, w = agg.get(cls, (0, 0.0, 0))
+            agg[cls] = (c + 1, t + e0.elapsed_time(e1), w + work)
+        return agg
+
+    def roofline(self, peak_hbm_gbs=8000.0, peak_int8_tops=5000.0):
+        """Roofline entry for the class with the largest total time."""
+        agg = self.kernel_times()
+        if not agg:
+            return {}
+        cls = max(agg, key=lambda k: agg[k][1])
+        calls, ms, work = agg[cls]
+        if cls == "qconv":
+            ach = work / (ms * 1e-3) / 1e12
+            r = {"bound": "mfma", "achieved": round(ach, 2), "peak": peak_int8_tops, "unit": "TOP/s",
+                 "frac": round(ach / peak_int8_tops, 4)}
+        else:
+            ach = work / (ms * 1e-3) / 1e9
+            r = {"bound": "hbm", "achieved": round(ach, 1), "peak": peak_hbm_gbs, "unit": "GB/s",
+                 "frac": round(ach / peak_hbm_gbs, 4)}
+        r.update({"kernel": cls, "launches": calls, "avg_launch_ms": round(ms / calls, 4),
+                  "traffic": None, "breakdown_ms": {k: round(v[1], 3) for k, v in agg.items()}})
+        return r
 
     # -- results ---------------------------------------------------------------
     def results(self, with_codes=False):
