@@ -11,7 +11,7 @@ namespace fxpq {
 constexpr int kThreads = 256;        // threads per block of the streaming kernels
 constexpr int kMaxStreamBlocks = 2048;
 constexpr int kMaxConvBlocks = 1 << 20;
-constexpr int kWindow = 4;           // candidates of the first FL-search pass
+constexpr int kWindow = 2;           // candidates of the first FL-search pass
 constexpr int kMaxCand = 160;        // fl_hi - fl_lo + 1 upper bound (|fl| <= 64 plus slack)
 constexpr int kGenChunks = 256;      // element chunks of the exact general search
 

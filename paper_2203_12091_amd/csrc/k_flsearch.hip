@@ -170,6 +170,84 @@ __device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, 
   return w;
 }
 
+// Accumulators of one thread in the window pass.
+struct WinAcc {
+  double A[kWindow], PH[kWindow], PL[kWindow];
+  double V2, CE;
+};
+
+// Main loop, specialized on what the min/max already tell:
+//   SPLIT    W * q sums need the Wh / Wl split to stay exact per thread;
+//   NONNEG   every value is >= 0: no lower clamp, no lower clipping term;
+//   CLAMP0   the first candidate can saturate (it is not beta_nosat).
+template <int KIND, int DT, bool SPLIT, bool NONNEG, bool CLAMP0>
+__device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
+                                WinAcc& acc) {
+  const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc;
+  double cj[kWindow];
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) cj[j] = ldexp(1.0, (j < nc ? b0 + j : b1) - u.sigma);
+  const double cce = ldexp(1.0, ws.bce - u.sigma);
+  const double qmin = u.qmin, qmax = u.qmax;
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) acc.A[j] = acc.PH[j] = acc.PL[j] = 0.0;
+  acc.V2 = acc.CE = 0.0;
+
+  auto consume = [&](double W) {
+    double Wh = 0.0, Wl = W;
+    if (SPLIT) {
+      Wh = floor(W * kTwoM26);
+      Wl = fma(-Wh, kTwo26, W);
+    }
+    acc.V2 = fma(W, W, acc.V2);
+#pragma unroll
+    for (int j = 0; j < kWindow; ++j) {
+      double q = rint(W * cj[j]);
+      if (j > 0 || CLAMP0) {
+        q = fmin(q, qmax);
+        if (!NONNEG) q = fmax(q, qmin);
+      }
+      acc.A[j] = fma(q, q, acc.A[j]);
+      if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
+      acc.PL[j] = fma(Wl, q, acc.PL[j]);
+    }
+    double t = W * cce;
+    double d1 = fmax(t - qmax, 0.0);
+    acc.CE = fma(d1, d1, acc.CE);
+    if (!NONNEG) {
+      double d2 = fmin(t - qmin, 0.0);
+      acc.CE = fma(d2, d2, acc.CE);
+    }
+  };
+
+  const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
+  const int64_t first = gtid * 4;
+  ThreadVals tv;
+  thread_vals_init<KIND>(s, first, tv);
+  // Fold the integer scaling W = v * 2^(sigma - sv) into the loader constants.
+  if constexpr (KIND == FXPQ_SRC_ACC) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      tv.M[j] *= u.wscale;
+      tv.A[j] *= u.wscale;
+    }
+  } else if constexpr (KIND == FXPQ_SRC_ADD) {
+    tv.ca *= u.wscale;
+    tv.cb *= u.wscale;
+  }
+  const double post = (KIND == FXPQ_SRC_ACC || KIND == FXPQ_SRC_ADD) ? 1.0 : u.wscale;
+  const int64_t nfull = n & ~(int64_t)3;
+  for (int64_t i = first; i < nfull; i += stride) {
+    double v[4];
+    load4<KIND, DT>(s, tv, i, v);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) consume((KIND == FXPQ_SRC_ACC || KIND == FXPQ_SRC_ADD) ? v[e] : v[e] * post);
+  }
+  if (gtid == 0)
+    for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i) * u.wscale);
+}
+
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_fls_window(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode,
@@ -202,66 +280,42 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     return;
   }
 
-  const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc;
-  double cj[kWindow];
-#pragma unroll
-  for (int j = 0; j < kWindow; ++j) cj[j] = ldexp(1.0, (j < nc ? b0 + j : b1) - u.sigma);
-  const double cce = ldexp(1.0, ws.bce - u.sigma);
-  const double qmin = u.qmin, qmax = u.qmax;
-
-  double A[kWindow], PH[kWindow], PL[kWindow];
-#pragma unroll
-  for (int j = 0; j < kWindow; ++j) A[j] = PH[j] = PL[j] = 0.0;
-  double V2 = 0.0, CE = 0.0;
-
-  auto consume = [&](double v) {
-    double W = v * u.wscale;
-    double Wh = floor(W * kTwoM26);
-    double Wl = fma(-Wh, kTwo26, W);
-    V2 = fma(W, W, V2);
-#pragma unroll
-    for (int j = 0; j < kWindow; ++j) {
-      double q = fmin(fmax(rint(W * cj[j]), qmin), qmax);
-      A[j] = fma(q, q, A[j]);
-      PH[j] = fma(Wh, q, PH[j]);
-      PL[j] = fma(Wl, q, PL[j]);
-    }
-    double t = W * cce;
-    double d1 = fmax(t - qmax, 0.0), d2 = fmin(t - qmin, 0.0);
-    CE = fma(d1, d1, CE);
-    CE = fma(d2, d2, CE);
-  };
-
-  const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
-  const int64_t first = gtid * 4;
-  ThreadVals tv;
-  thread_vals_init<KIND>(s, first, tv);
-  const int64_t nfull = n & ~(int64_t)3;
-  for (int64_t i = first; i < nfull; i += stride) {
-    double v[4];
-    load4<KIND, DT>(s, tv, i, v);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) consume(v[e]);
+  // Uniform specialization.  Per-thread partial sums of W * q stay exact below
+  // 2^53 without the split when max|W| * max|q| * (values per thread) < 2^53.
+  const int64_t per_thread = ((n / 4 + (int64_t)gridDim.x * kThreads - 1) /
+                              ((int64_t)gridDim.x * kThreads)) * 4 + 4;
+  const double qabs = fmax(u.qmax, -u.qmin);
+  const bool split = u.absmax * u.wscale * qabs * (double)per_thread >= kTwo53;
+  const bool nonneg = mm[0] >= 0.0;
+  const bool clamp0 = ws.b0 != u.beta_nosat;
+  WinAcc acc;
+  const int variant = (split ? 4 : 0) | (nonneg ? 2 : 0) | (clamp0 ? 1 : 0);
+  switch (variant) {
+    case 0: win_loop<KIND, DT, false, false, false>(s, n, u, ws, acc); break;
+    case 1: win_loop<KIND, DT, false, false, true>(s, n, u, ws, acc); break;
+    case 2: win_loop<KIND, DT, false, true, false>(s, n, u, ws, acc); break;
+    case 3: win_loop<KIND, DT, false, true, true>(s, n, u, ws, acc); break;
+    case 4: win_loop<KIND, DT, true, false, false>(s, n, u, ws, acc); break;
+    case 5: win_loop<KIND, DT, true, false, true>(s, n, u, ws, acc); break;
+    case 6: win_loop<KIND, DT, true, true, false>(s, n, u, ws, acc); break;
+    default: win_loop<KIND, DT, true, true, true>(s, n, u, ws, acc); break;
   }
-  if (gtid == 0)
-    for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i));
 
   // Block partials: exact integers as int64, bound sums as fp64.
   long long* pi = part_i + (int64_t)blockIdx.x * (3 * kWindow);
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
-    long long a = block_reduce((long long)A[j], OpAddL(), shl);
-    long long ph = block_reduce((long long)PH[j], OpAddL(), shl);
-    long long pl = block_reduce((long long)PL[j], OpAddL(), shl);
+    long long a = block_reduce((long long)acc.A[j], OpAddL(), shl);
+    long long ph = block_reduce((long long)acc.PH[j], OpAddL(), shl);
+    long long pl = block_reduce((long long)acc.PL[j], OpAddL(), shl);
     if (threadIdx.x == 0) {
       pi[3 * j] = a;
       pi[3 * j + 1] = ph;
       pi[3 * j + 2] = pl;
     }
   }
-  double v2 = block_reduce(V2, OpAddD(), shd);
-  double ce = block_reduce(CE, OpAddD(), shd);
+  double v2 = block_reduce(acc.V2, OpAddD(), shd);
+  double ce = block_reduce(acc.CE, OpAddD(), shd);
   if (threadIdx.x == 0) {
     part_f[2 * blockIdx.x] = v2;
     part_f[2 * blockIdx.x + 1] = ce;
@@ -273,38 +327,62 @@ template <int KIND>
 __global__ __launch_bounds__(kThreads) void k_fls_window_fin(
     SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, const double* mm,
     const long long* part_i, const double* part_f, int nb, FlsPlan* plan, fxpq_fmt* out) {
-  __shared__ long long shl[8];
-  __shared__ double shd[8];
-  __shared__ long long tot_hi[3 * kWindow], tot_lo[3 * kWindow];
-  __shared__ double tot_f[2];
+  constexpr int NQ = 3 * kWindow;
+  __shared__ long long sh_hi[4][NQ], sh_lo[4][NQ];
+  __shared__ double sh_f[4][2];
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode);
   if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
   const FlsU& u = ws.u;
   const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc, bce = ws.bce;
-  // Each block partial is below 2^61 in magnitude; split into 32-bit halves so
-  // the per-thread int64 sums cannot overflow.
-  for (int qi = 0; qi < 3 * kWindow; ++qi) {
-    long long hi = 0, lo = 0;
-    for (int b = threadIdx.x; b < nb; b += kThreads) {
-      long long x = part_i[(int64_t)b * (3 * kWindow) + qi];
-      hi += x >> 32;
-      lo += x & 0xFFFFFFFFll;
+  // One pass over the block partials.  Each is below 2^61 in magnitude; split
+  // into 32-bit halves so the int64 sums cannot overflow.
+  long long hi[NQ], lo[NQ];
+  double f0 = 0.0, f1 = 0.0;
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) hi[qi] = lo[qi] = 0;
+  for (int b = threadIdx.x; b < nb; b += kThreads) {
+    const long long* p = part_i + (int64_t)b * NQ;
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi) {
+      long long x = p[qi];
+      hi[qi] += x >> 32;
+      lo[qi] += x & 0xFFFFFFFFll;
     }
-    hi = block_reduce(hi, OpAddL(), shl);
-    lo = block_reduce(lo, OpAddL(), shl);
-    if (threadIdx.x == 0) {
-      tot_hi[qi] = hi;
-      tot_lo[qi] = lo;
-    }
+    f0 += part_f[2 * b];
+    f1 += part_f[2 * b + 1];
   }
-  for (int qi = 0; qi < 2; ++qi) {
-    double x = 0.0;
-    for (int b = threadIdx.x; b < nb; b += kThreads) x += part_f[2 * b + qi];
-    x = block_reduce(x, OpAddD(), shd);
-    if (threadIdx.x == 0) tot_f[qi] = x;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+#pragma unroll
+  for (int qi = 0; qi < NQ; ++qi) {
+    hi[qi] = wave_reduce(hi[qi], OpAddL());
+    lo[qi] = wave_reduce(lo[qi], OpAddL());
+  }
+  f0 = wave_reduce(f0, OpAddD());
+  f1 = wave_reduce(f1, OpAddD());
+  if (lane == 0) {
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi) {
+      sh_hi[wid][qi] = hi[qi];
+      sh_lo[wid][qi] = lo[qi];
+    }
+    sh_f[wid][0] = f0;
+    sh_f[wid][1] = f1;
   }
   __syncthreads();
   if (threadIdx.x != 0) return;
+  long long tot_hi[NQ], tot_lo[NQ];
+  double tot_f[2] = {0.0, 0.0};
+  for (int qi = 0; qi < NQ; ++qi) {
+    tot_hi[qi] = tot_lo[qi] = 0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+      tot_hi[qi] += sh_hi[w][qi];
+      tot_lo[qi] += sh_lo[w][qi];
+    }
+  }
+  for (int w = 0; w < kThreads / 64; ++w) {
+    tot_f[0] += sh_f[w][0];
+    tot_f[1] += sh_f[w][1];
+  }
   auto total = [&](int qi) -> __int128 {
     return ((__int128)tot_hi[qi] << 32) + (__int128)tot_lo[qi];
   };

@@ -389,10 +389,22 @@ class CalibNet:
                     self.act_codes[n.name].data_ptr(), fx.C8)
         return calls
 
+    def prepare_timers(self, steps, classes=("fl_search",)):
+        """Pre-creates HIP events so that the next `steps` forwards bracket every
+        call of the given classes without allocating anything while timed."""
+        if self.calls is None:
+            self.calls = self._plan()
+        T = self.torch
+        per_step = sum(1 for c in self.calls if c[0] in classes)
+        self.timed_classes = set(classes)
+        self.event_pool = [(T.cuda.Event(enable_timing=True), T.cuda.Event(enable_timing=True))
+                           for _ in range(per_step * steps)]
+        self.timers = []
+
     def forward(self):
-        """Enqueues one calibration forward (no host synchronization).  When
-        ``self.timers`` is a list, every call is bracketed by HIP events on the
-        library's stream and (class, work, start, end) is appended to it."""
+        """Enqueues one calibration forward (no host synchronization).  After
+        prepare_timers(), calls of the timed classes are bracketed by HIP events
+        on the library's stream and (class, work, start, end) is recorded."""
         if self.calls is None:
             self.calls = self._plan()
         timers = self.timers
@@ -402,16 +414,19 @@ class CalibNet:
                 if st:
                     raise fx.FxpqError(fn.__name__, st)
             return
-        T = self.torch
+        timed = self.timed_classes
+        pool = self.event_pool
         for cls, work, fn, args in self.calls:
-            e0 = T.cuda.Event(enable_timing=True)
-            e1 = T.cuda.Event(enable_timing=True)
-            e0.record()
-            st = fn(*args)
-            e1.record()
+            if cls in timed:
+                e0, e1 = pool[len(timers)]
+                e0.record()
+                st = fn(*args)
+                e1.record()
+                timers.append((cls, work, e0, e1))
+            else:
+                st = fn(*args)
             if st:
                 raise fx.FxpqError(fn.__name__, st)
-            timers.append((cls, work, e0, e1))
 
     def kernel_times(self):
         """Per call class: (calls, total ms, total work) from the recorded events."""
