@@ -8,12 +8,19 @@ final FC to integer logits.  Parameters are quantized once during set-up
 (weight FL searches are not part of a calibration step).  Inputs are resident
 in HBM before timing starts.
 
-Prints ONE JSON line (see the repository contract).  --gpus above 1 exits: this
-build runs on one GPU.
+Roofline: the dominant kernel is the FL-search window pass (k_fls_window); the
+library brackets each of its launches inside the timed region with
+pre-created HIP events on its stream (fxpq_timer_start / fxpq_timer_read).
+`traffic` comes from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary
+and is reported only while the kernel sources match the profiled ones.
+
+Prints ONE JSON line.  --gpus above 1 exits: this build runs on one GPU.
 """
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -21,7 +28,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+INT8_PEAK_TOPS = 5000.0
 BATCH, IMAGE = 256, 224
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fl_search_window_resnet50_b256_traffic.md")
+WINDOW_SOURCES = ["k_flsearch.hip", "values.hpp", "common.hpp"]
 
 
 def parse():
@@ -30,24 +40,49 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-image", type=int, default=224)
+    ap.add_argument("--cpu-sample-batch", type=int, default=8)
+    ap.add_argument("--mode", choices=["bench", "profile", "copy"], default="bench",
+                    help="profile: set up and run --warmup forwards only (for counter runs); "
+                         "copy: one plain 1 GiB device copy (counter calibration)")
     return ap.parse_args()
 
 
-def cpu_baseline(image):
+def window_source_hash():
+    h = hashlib.sha256()
+    for f in WINDOW_SOURCES:
+        with open(os.path.join(ROOT, "paper_2203_12091_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """Per-launch HBM bytes of k_fls_window from the committed counter summary,
+    or None when the summary is missing or the kernel changed since."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    m_hash = re.search(r"source_hash:\s*(\w+)", text)
+    m_val = re.search(r"traffic_bytes_per_launch:\s*([0-9.]+)", text)
+    if not m_hash or not m_val or m_hash.group(1) != window_source_hash():
+        return None
+    return float(m_val.group(1))
+
+
+def cpu_baseline(batch):
     """The oracle, as it stands, on a bounded sample: a calibration forward of
-    one image (parameters quantized beforehand), timed on the host cores."""
+    `batch` images at 224x224 (parameters quantized beforehand), on the host."""
     import oracle
     t_prep = time.perf_counter()
-    f = oracle.nets.prepare("resnet50", batch=1, image=image)
+    f = oracle.nets.prepare("resnet50", batch=batch, image=IMAGE)
     t0 = time.perf_counter()
     f.run()
     t = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(1.0 / t, 5), "unit": "images/s", "cores": cores, "kind": "oracle",
-            "sample": f"ResNet-50 DFX calibration forward of 1 image {image}x{image} "
-                      f"(parameters pre-quantized, {t:.1f} s forward, "
-                      f"{t0 - t_prep:.1f} s parameter set-up untimed)"}
+    return {"value": round(batch / t, 5), "unit": "images/s", "cores": cores, "kind": "oracle",
+            "sample": f"ResNet-50 DFX calibration forward of {batch} images 224x224 "
+                      f"(exact CPU oracle, parameters pre-quantized; {t:.1f} s forward, "
+                      f"{t0 - t_prep:.1f} s set-up untimed)"}
 
 
 def main():
@@ -57,31 +92,54 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     import torch
+    from paper_2203_12091_amd import fxpq as fx
     from paper_2203_12091_amd import nets
 
     dev = torch.device("cuda:0")
+    if args.mode == "copy":
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize(dev)
+        dst.copy_(src)
+        torch.cuda.synchronize(dev)
+        print(json.dumps({"copy_bytes": src.numel() * 4}), flush=True)
+        return
+
     net = nets.CalibNet("resnet50", batch=BATCH, image=IMAGE, device="cuda:0")
     for _ in range(args.warmup):
         net.forward()
     torch.cuda.synchronize(dev)
+    if args.mode == "profile":
+        print(json.dumps({"profile_forwards": args.warmup}), flush=True)
+        return
 
-    # timed region: exactly `steps` forwards; the FL-search calls (the dominant
-    # kernel) are bracketed by pre-created events on the library's stream.
-    net.prepare_timers(args.steps, classes=("fl_search",))
+    # timed region: exactly `steps` forwards, the window pass timed by the library
+    fx.timer_start(net.h, fx.TIMER_FLS_WINDOW)
     torch.cuda.synchronize(dev)
     t0 = time.perf_counter()
     for _ in range(args.steps):
         net.forward()
     torch.cuda.synchronize(dev)
     elapsed = time.perf_counter() - t0
+    win_ms, win_n, win_bytes = fx.timer_read(net.h)
     res = net.results()
     if res["flags"]:
         print(f"bench.py: device flags {res['flags']:#x}", file=sys.stderr)
         sys.exit(1)
 
+    # one more (untimed) forward each for the contraction and requant figures
+    fx.timer_start(net.h, fx.TIMER_QCONV)
+    net.forward()
+    cv_ms, cv_n, cv_ops = fx.timer_read(net.h)
+    fx.timer_start(net.h, fx.TIMER_REQUANT)
+    net.forward()
+    rq_ms, rq_n, rq_bytes = fx.timer_read(net.h)
+    fx.timer_start(net.h, fx.TIMER_OFF)
+
     ms = elapsed * 1000.0 / args.steps
     value = BATCH * args.steps / elapsed
-    roof = net.roofline()
+    achieved = win_bytes / (win_ms * 1e-3) / 1e9
+    traffic = committed_traffic()
     out = {
         "metric": "calibration images/s (ResNet-50 b256 DFX); FL-search GB/s; int8 MFMA % peak",
         "value": round(value, 2),
@@ -98,11 +156,21 @@ def main():
         "config": {"workload": "resnet50_b256_224_dfx_calibration_forward", "batch": BATCH,
                    "image": IMAGE, "weight_wl": 8, "act_wl": 8, "fl_range": [-8, 15],
                    "parallelism": "single_gpu"},
-        "roofline": roof,
-        "fl_search_gbs": roof.get("achieved"),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "kernel": "k_fls_window", "launches": win_n,
+                     "avg_launch_ms": round(win_ms / max(win_n, 1), 5),
+                     "algorithmic_bytes_per_launch": round(win_bytes / max(win_n, 1))},
+        "fl_search_gbs": round(achieved, 1),
+        "mfma": {"kernel": "k_qconv", "achieved": round(cv_ops / (cv_ms * 1e-3) / 1e12, 1),
+                 "unit": "TOP/s", "peak": INT8_PEAK_TOPS,
+                 "frac": round(cv_ops / (cv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+                 "ms_per_forward": round(cv_ms, 3), "launches": cv_n},
+        "requant": {"kernel": "k_requant", "achieved": round(rq_bytes / (rq_ms * 1e-3) / 1e9, 1),
+                    "unit": "GB/s", "ms_per_forward": round(rq_ms, 3), "launches": rq_n},
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_sample_image)
+        out["cpu_baseline"] = cpu_baseline(args.cpu_sample_batch)
     print(json.dumps(out), flush=True)
 
 

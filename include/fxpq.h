@@ -254,6 +254,33 @@ fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
  * (device int32), for consumers that need it as a plain FXPQ_SRC_INT scale. */
 fxpq_status fxpq_epilogue_scale(fxpq_handle h, const fxpq_epilogue* ep, int32_t* d_scale);
 
+/* ---- measurement --------------------------------------------------------- */
+
+/* Kernels the handle can time with HIP events on its stream. */
+typedef enum {
+  FXPQ_TIMER_OFF = 0,
+  FXPQ_TIMER_FLS_WINDOW = 1, /* the one-read window pass of fxpq_fl_search */
+  FXPQ_TIMER_QCONV = 2,      /* the contraction kernel of fxpq_qconv / fxpq_qgemm */
+  FXPQ_TIMER_REQUANT = 3     /* the kernel of fxpq_requant / fxpq_quantize */
+} fxpq_timer_kind;
+
+/*
+ * Starts timing every launch of one kernel: the handle brackets each launch
+ * with a pair of pre-created HIP events on its stream (at most 16384 launches
+ * per session; later launches run untimed).  Resets earlier totals.
+ * FXPQ_TIMER_OFF stops timing.
+ */
+fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind);
+
+/*
+ * Waits for the stream and returns, over the launches timed since
+ * fxpq_timer_start: the summed kernel time in ms, the number of launches, and
+ * the summed algorithmic work (HBM bytes the kernel must move: 4 B per int32
+ * value read, 2 B per eltwise element, 8 B per int64 value, 4 + 1 B per
+ * quantized fp32 value; or int8 operations 2*M*N*K for the contraction).
+ */
+fxpq_status fxpq_timer_read(fxpq_handle h, double* total_ms, int64_t* launches, double* work);
+
 #ifdef __cplusplus
 }
 #endif

@@ -104,11 +104,36 @@ __device__ inline int code_is_off(int dtype, const fxpq_fmt* f) {
   return 0;
 }
 
+// ---- kernel timing (measurement only) ------------------------------------------
+struct Timer {
+  int kind = 0;           // fxpq_timer_kind being timed
+  int capacity = 0;       // event pairs available
+  int used = 0;
+  double work = 0.0;      // summed algorithmic bytes or operations
+  hipEvent_t* ev = nullptr;  // 2 * capacity events
+};
+
 // ---- launchers implemented in the kernel translation units -------------------
 struct Ctx {
   hipStream_t stream;
   Scratch sc;
+  Timer* timer;
 };
+
+// Brackets one launch with events when `kind` is being timed.
+inline bool timer_begin(const Ctx& c, int kind) {
+  Timer* t = c.timer;
+  if (!t || t->kind != kind || t->used >= t->capacity) return false;
+  return hipEventRecord(t->ev[2 * t->used], c.stream) == hipSuccess;
+}
+inline void timer_end(const Ctx& c, bool started, double work) {
+  if (!started) return;
+  Timer* t = c.timer;
+  if (hipEventRecord(t->ev[2 * t->used + 1], c.stream) == hipSuccess) {
+    t->used += 1;
+    t->work += work;
+  }
+}
 
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out);
 hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* out);

@@ -16,7 +16,10 @@ struct fxpq_handle_s {
   void* scratch;
   size_t scratch_bytes;
   Scratch sc;
+  Timer timer;
 };
+
+constexpr int kTimerPairs = 16384;
 
 namespace {
 
@@ -30,9 +33,9 @@ bool is_code8(int t) { return t == FXPQ_I8 || t == FXPQ_U8OFF || t == FXPQ_C8; }
 
 bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32; }
 
-size_t code_align(int t) { return is_code8(t) ? 4 : (t == FXPQ_I16 ? 8 : 16); }
+size_t code_align(int t) { (void)t; return 16; }
 
-Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc}; }
+Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc, &h->timer}; }
 
 fxpq_status hip_status(hipError_t e) { return e == hipSuccess ? FXPQ_OK : FXPQ_ERR_HIP; }
 
@@ -86,7 +89,7 @@ fxpq_status to_dev(const fxpq_src* s, int64_t n, SrcDev* d) {
     case FXPQ_SRC_ADD:
       if (!s->x2 || !s->d_fmt_a || !s->d_fmt_b) return FXPQ_ERR_INVALID_ARG;
       if (!is_code8(s->dtype) || !is_code8(s->dtype2)) return FXPQ_ERR_INVALID_ARG;
-      if (!aligned(s->x, 4) || !aligned(s->x2, 4)) return FXPQ_ERR_INVALID_ARG;
+      if (!aligned(s->x, 16) || !aligned(s->x2, 16)) return FXPQ_ERR_INVALID_ARG;
       d->x2 = s->x2;
       d->dtype2 = s->dtype2;
       d->fa = s->d_fmt_a;
@@ -183,6 +186,10 @@ fxpq_status fxpq_destroy(fxpq_handle h) {
   DeviceGuard g(h->device);
   (void)hipStreamSynchronize(h->stream);
   (void)hipFree(h->scratch);
+  if (h->timer.ev) {
+    for (int i = 0; i < 2 * h->timer.capacity; ++i) (void)hipEventDestroy(h->timer.ev[i]);
+    delete[] h->timer.ev;
+  }
   delete h;
   return FXPQ_OK;
 }
@@ -345,6 +352,47 @@ fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
     return FXPQ_ERR_INVALID_ARG;
   DeviceGuard g(h->device);
   return hip_status(launch_layer_error(ctx(h), ref, codes, code_type, d_fmt, n, d_out));
+}
+
+fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind) {
+  if (!h || kind < FXPQ_TIMER_OFF || kind > FXPQ_TIMER_REQUANT) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  Timer& t = h->timer;
+  if (kind != FXPQ_TIMER_OFF && !t.ev) {
+    t.ev = new (std::nothrow) hipEvent_t[2 * kTimerPairs];
+    if (!t.ev) return FXPQ_ERR_ALLOC;
+    for (int i = 0; i < 2 * kTimerPairs; ++i) {
+      if (hipEventCreate(&t.ev[i]) != hipSuccess) {
+        for (int j = 0; j < i; ++j) (void)hipEventDestroy(t.ev[j]);
+        delete[] t.ev;
+        t.ev = nullptr;
+        return FXPQ_ERR_HIP;
+      }
+    }
+    t.capacity = kTimerPairs;
+  }
+  if (hipStreamSynchronize(h->stream) != hipSuccess) return FXPQ_ERR_HIP;
+  t.kind = kind;
+  t.used = 0;
+  t.work = 0.0;
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_timer_read(fxpq_handle h, double* total_ms, int64_t* launches, double* work) {
+  if (!h || !total_ms || !launches || !work) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  if (hipStreamSynchronize(h->stream) != hipSuccess) return FXPQ_ERR_HIP;
+  Timer& t = h->timer;
+  double sum = 0.0;
+  for (int i = 0; i < t.used; ++i) {
+    float ms = 0.0f;
+    if (hipEventElapsedTime(&ms, t.ev[2 * i], t.ev[2 * i + 1]) != hipSuccess) return FXPQ_ERR_HIP;
+    sum += ms;
+  }
+  *total_ms = sum;
+  *launches = t.used;
+  *work = t.work;
+  return FXPQ_OK;
 }
 
 fxpq_status fxpq_epilogue_scale(fxpq_handle h, const fxpq_epilogue* ep, int32_t* d_scale) {

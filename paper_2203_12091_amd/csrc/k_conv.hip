@@ -267,6 +267,7 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   if (ep) a.ep = *ep;
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
+  bool timed = timer_begin(c, FXPQ_TIMER_QCONV);
   dim3 grid;
   if (d.k <= 64) {
     grid = dim3((a.M + 255) / 256, (d.k + 63) / 64);
@@ -275,6 +276,7 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
     grid = dim3((a.M + 127) / 128, (d.k + 127) / 128);
     conv_dispatch_loader<128, 128>(loader, grid, c.stream, a);
   }
+  timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   if (a.want_mm) return launch_minmax_fin(c, a.mm_part, (int)(grid.x * grid.y), d_minmax);
   return hipGetLastError();
 }

@@ -29,7 +29,7 @@
 
 namespace fxpq {
 
-int stream_grid(int64_t n, int channels, int64_t max_per_thread);
+int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec);
 
 struct FlsPlan {
   int need_general;
@@ -220,15 +220,14 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
     }
   };
 
+  using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
-  const int64_t first = gtid * 4;
-  ThreadVals tv;
-  thread_vals_init<KIND>(s, first, tv);
+  ThreadVals<PK::V> tv;
+  thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, tv);
   // Fold the integer scaling W = v * 2^(sigma - sv) into the loader constants.
   if constexpr (KIND == FXPQ_SRC_ACC) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < PK::V; ++j) {
       tv.M[j] *= u.wscale;
       tv.A[j] *= u.wscale;
     }
@@ -236,13 +235,12 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
     tv.ca *= u.wscale;
     tv.cb *= u.wscale;
   }
-  const double post = (KIND == FXPQ_SRC_ACC || KIND == FXPQ_SRC_ADD) ? 1.0 : u.wscale;
-  const int64_t nfull = n & ~(int64_t)3;
-  for (int64_t i = first; i < nfull; i += stride) {
-    double v[4];
-    load4<KIND, DT>(s, tv, i, v);
-#pragma unroll
-    for (int e = 0; e < 4; ++e) consume((KIND == FXPQ_SRC_ACC || KIND == FXPQ_SRC_ADD) ? v[e] : v[e] * post);
+  const int64_t nfull = n - n % PK::EP;
+  if constexpr (KIND == FXPQ_SRC_ACC || KIND == FXPQ_SRC_ADD) {
+    stream_values<KIND, DT>(s, n, tv, [&](double v, int64_t) { consume(v); });
+  } else {
+    const double post = u.wscale;
+    stream_values<KIND, DT>(s, n, tv, [&](double v, int64_t) { consume(v * post); });
   }
   if (gtid == 0)
     for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i) * u.wscale);
@@ -282,8 +280,9 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
 
   // Uniform specialization.  Per-thread partial sums of W * q stay exact below
   // 2^53 without the split when max|W| * max|q| * (values per thread) < 2^53.
-  const int64_t per_thread = ((n / 4 + (int64_t)gridDim.x * kThreads - 1) /
-                              ((int64_t)gridDim.x * kThreads)) * 4 + 4;
+  constexpr int V = Pack<KIND, DT>::V;
+  const int64_t per_thread = ((n / V + (int64_t)gridDim.x * kThreads - 1) /
+                              ((int64_t)gridDim.x * kThreads)) * V + V;
   const double qabs = fmax(u.qmax, -u.qmin);
   const bool split = u.absmax * u.wscale * qabs * (double)per_thread >= kTwo53;
   const bool nonneg = mm[0] >= 0.0;
@@ -486,8 +485,6 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
   const long long qmax = (1ll << (wl - sign)) - 1;
   const long long qmin = sign ? -(1ll << (wl - 1)) : 0;
   const int64_t clen = (n + nchunks - 1) / nchunks;
-  ThreadVals tv;  // only ADD uses uniform values here; ACC goes through load1
-  (void)tv;
 
   for (int item = blockIdx.x; item < nc * nchunks; item += gridDim.x) {
     const int j = item / nchunks, ch = item % nchunks;
@@ -608,13 +605,17 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
   int qbits = (wl <= 16) ? wl : 16;
   int64_t per_thread = (int64_t)1 << (53 - 26 - qbits - 1);
   int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
-  int blocks = stream_grid(n, channels, per_thread);
+  const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;  // Pack<>::V
+  int blocks = stream_grid(n, channels, per_thread, vec);
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   int mode = d_sse ? MODE_REPORT : MODE_SEARCH;
+  const double elem_bytes = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
+  bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
                         s, n, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part,
                         c.sc.win_part_f, plan, out, c.sc.flags)));
+  timer_end(c, timed, elem_bytes * (double)n);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window_fin<K_><<<1, kThreads, 0, c.stream>>>(
                         s, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part, c.sc.win_part_f,

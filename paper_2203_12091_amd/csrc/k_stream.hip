@@ -21,8 +21,8 @@ static int64_t gcd64(int64_t a, int64_t b) {
   return a;
 }
 
-int stream_grid(int64_t n, int channels, int64_t max_per_thread) {
-  int64_t groups = (n + 3) / 4;
+int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec) {
+  int64_t groups = (n + vec - 1) / vec;
   int64_t blocks = (groups + kThreads - 1) / kThreads;
   if (blocks > kMaxStreamBlocks) blocks = kMaxStreamBlocks;
   if (max_per_thread > 0) {
@@ -31,7 +31,7 @@ int stream_grid(int64_t n, int channels, int64_t max_per_thread) {
   }
   if (blocks < 1) blocks = 1;
   if (channels > 0) {
-    int64_t g = channels / gcd64(channels, 4 * kThreads);
+    int64_t g = channels / gcd64(channels, (int64_t)vec * kThreads);
     blocks = (blocks + g - 1) / g * g;
   }
   return (int)blocks;
@@ -44,24 +44,18 @@ template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_minmax(SrcDev s, int64_t n, double* part,
                                                      unsigned* flags) {
   __shared__ double sh[8];
+  using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
-  const int64_t first = gtid * 4;
-  ThreadVals t;
-  thread_vals_init<KIND>(s, first, t);
+  ThreadVals<PK::V> t;
+  thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, t);
   double mn = INFINITY, mx = -INFINITY;
   bool bad = false;
-  const int64_t nfull = n & ~(int64_t)3;
-  for (int64_t i = first; i < nfull; i += stride) {
-    double v[4];
-    load4<KIND, DT>(s, t, i, v);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      mn = fmin(mn, v[j]);
-      mx = fmax(mx, v[j]);
-      if (KIND == FXPQ_SRC_F32) bad |= !isfinite(v[j]);
-    }
-  }
+  const int64_t nfull = n - n % PK::EP;
+  stream_values<KIND, DT>(s, n, t, [&](double v, int64_t) {
+    mn = fmin(mn, v);
+    mx = fmax(mx, v);
+    if (KIND == FXPQ_SRC_F32) bad |= !isfinite(v);
+  });
   if (gtid == 0) {
     for (int64_t i = nfull; i < n; ++i) {
       double v = load1<KIND, DT>(s, i);
@@ -152,19 +146,40 @@ __device__ inline int quant_one(double v, const QFmt& q) {
   return (int)c;
 }
 
-template <int OUT>
-__device__ inline void store4(void* codes, int64_t i, const int c[4]) {
+template <int OUT, int V>
+__device__ inline void storev(void* codes, int64_t i, const int c[V]) {
   if constexpr (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
-    uint32_t w = (uint32_t)(c[0] & 0xFF) | ((uint32_t)(c[1] & 0xFF) << 8) |
-                 ((uint32_t)(c[2] & 0xFF) << 16) | ((uint32_t)(c[3] & 0xFF) << 24);
-    *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(codes) + i) = w;
+    if constexpr (V == 2) {
+      *reinterpret_cast<uint16_t*>(static_cast<int8_t*>(codes) + i) =
+          (uint16_t)((c[0] & 0xFF) | ((c[1] & 0xFF) << 8));
+    } else {
+      uint32_t w[V / 4];
+#pragma unroll
+      for (int q = 0; q < V / 4; ++q)
+        w[q] = (uint32_t)(c[4 * q] & 0xFF) | ((uint32_t)(c[4 * q + 1] & 0xFF) << 8) |
+               ((uint32_t)(c[4 * q + 2] & 0xFF) << 16) | ((uint32_t)(c[4 * q + 3] & 0xFF) << 24);
+      uint32_t* dst = reinterpret_cast<uint32_t*>(static_cast<int8_t*>(codes) + i);
+      if constexpr (V == 16) {
+        *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+      } else {
+        dst[0] = w[0];
+      }
+    }
   } else if constexpr (OUT == FXPQ_I16) {
-    uint2 w;
-    w.x = (uint32_t)(c[0] & 0xFFFF) | ((uint32_t)(c[1] & 0xFFFF) << 16);
-    w.y = (uint32_t)(c[2] & 0xFFFF) | ((uint32_t)(c[3] & 0xFFFF) << 16);
-    *reinterpret_cast<uint2*>(static_cast<int16_t*>(codes) + i) = w;
+    uint32_t* dst = reinterpret_cast<uint32_t*>(static_cast<int16_t*>(codes) + i);
+#pragma unroll
+    for (int q = 0; q < V / 2; ++q)
+      dst[q] = (uint32_t)(c[2 * q] & 0xFFFF) | ((uint32_t)(c[2 * q + 1] & 0xFFFF) << 16);
   } else {
-    *reinterpret_cast<int4*>(static_cast<int32_t*>(codes) + i) = make_int4(c[0], c[1], c[2], c[3]);
+    int32_t* dst = static_cast<int32_t*>(codes) + i;
+    if constexpr (V % 4 == 0) {
+#pragma unroll
+      for (int q = 0; q < V / 4; ++q)
+        reinterpret_cast<int4*>(dst)[q] = make_int4(c[4 * q], c[4 * q + 1], c[4 * q + 2], c[4 * q + 3]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < V / 2; ++q) reinterpret_cast<int2*>(dst)[q] = make_int2(c[2 * q], c[2 * q + 1]);
+    }
   }
 }
 
@@ -184,19 +199,30 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
   const int sv = src_scale(s);
   const QFmt q = qfmt_setup<OUT>(fmt, sv, flags);
   if (!q.ok) return;
+  using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kThreads * 4;
-  const int64_t first = gtid * 4;
-  ThreadVals t;
-  thread_vals_init<KIND>(s, first, t);
-  const int64_t nfull = n & ~(int64_t)3;
-  for (int64_t i = first; i < nfull; i += stride) {
-    double v[4];
-    load4<KIND, DT>(s, t, i, v);
-    int c[4];
+  const int64_t chunk = (int64_t)kThreads * PK::V;
+  const int64_t stride = (int64_t)gridDim.x * chunk;
+  ThreadVals<PK::V> t;
+  thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * chunk, t);
+  const int64_t nfull = n - n % PK::EP;
+  for (int64_t base = (int64_t)blockIdx.x * chunk; base < nfull; base += stride) {
+    double v[PK::P][PK::EP];
+    bool ok[PK::P];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) c[j] = quant_one(v[j], q);
-    store4<OUT>(codes, i, c);
+    for (int p = 0; p < PK::P; ++p) {
+      int64_t i = pk_index<PK::EP>(base, p);
+      ok[p] = i < nfull;
+      if (ok[p]) load_packet<KIND, DT>(s, t, p, i, v[p]);
+    }
+#pragma unroll
+    for (int p = 0; p < PK::P; ++p) {
+      if (!ok[p]) continue;
+      int c[PK::EP];
+#pragma unroll
+      for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[p][j], q);
+      storev<OUT, PK::EP>(codes, pk_index<PK::EP>(base, p), c);
+    }
   }
   if (gtid == 0) {
     for (int64_t i = nfull; i < n; ++i) store1<OUT>(codes, i, quant_one(load1<KIND, DT>(s, i), q));
@@ -368,8 +394,12 @@ __global__ void k_epi_scale(SrcDev s, int32_t* out) {
 
 static int src_channels(const SrcDev& s) { return s.kind == FXPQ_SRC_ACC ? s.channels : 0; }
 
+static int src_vec(const SrcDev& s) {
+  return s.kind == FXPQ_SRC_ADD ? 16 : 4;
+}  // values per thread per block iteration (Pack<>::V)
+
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) {
-  int blocks = stream_grid(n, src_channels(s), 0);
+  int blocks = stream_grid(n, src_channels(s), 0, src_vec(s));
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(s, n, c.sc.minmax_part,
                                                                         c.sc.flags)));
@@ -387,7 +417,10 @@ static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt
 
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
                           void* codes, int code_type) {
-  int blocks = stream_grid(n, src_channels(s), 0);
+  int blocks = stream_grid(n, src_channels(s), 0, src_vec(s));
+  const double in_b = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
+  const double out_b = (code_type == FXPQ_I32) ? 4.0 : (code_type == FXPQ_I16 ? 2.0 : 1.0);
+  bool timed = timer_begin(c, FXPQ_TIMER_REQUANT);
   switch (code_type) {
     case FXPQ_I8: requant_out<FXPQ_I8>(c, s, n, fmt, codes, blocks); break;
     case FXPQ_U8OFF: requant_out<FXPQ_U8OFF>(c, s, n, fmt, codes, blocks); break;
@@ -395,12 +428,13 @@ hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_f
     case FXPQ_I16: requant_out<FXPQ_I16>(c, s, n, fmt, codes, blocks); break;
     default: requant_out<FXPQ_I32>(c, s, n, fmt, codes, blocks); break;
   }
+  timer_end(c, timed, (in_b + out_b) * (double)n);
   return hipGetLastError();
 }
 
 hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes, int code_type,
                               const fxpq_fmt* fmt, int64_t n, double* out) {
-  int blocks = stream_grid(n, 0, 0);
+  int blocks = stream_grid(n, 0, 0, 4);
   double* part = c.sc.minmax_part;  // 5 doubles per block fits (kMaxConvBlocks * 2)
   switch (code_type) {
     case FXPQ_I16:

@@ -11,20 +11,45 @@ namespace fxpq {
 constexpr double kTwo52 = 4503599627370496.0;  // 2^52
 constexpr double kTwo53 = 9007199254740992.0;  // 2^53
 
+// Streaming layout.  A thread handles P packets of 16 bytes per block
+// iteration; packet p of thread t covers elements base + (p*kThreads + t)*EP
+// ... + EP-1, so every packet load of a wave is one contiguous 1 KiB span.
+// EP = values per packet (4 for 4-byte data, 2 for int64, 16 for the two int8
+// code tensors of an eltwise source).
+template <int KIND, int DT>
+struct Pack {
+  static constexpr int EP = (KIND == FXPQ_SRC_ADD) ? 16 : (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) ? 2 : 4;
+  static constexpr int P = (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) ? 2 : 1;
+  static constexpr int V = EP * P;  // values per thread per block iteration
+};
+
+template <int V>
 struct ThreadVals {
-  double M[4], A[4];  // ACC: per-channel multiplier / addend
+  double M[V], A[V];  // ACC: per-channel multiplier / addend, indexed p * EP + j
   double ca, cb;      // ADD: alignment factors
   double oa, ob;      // ADD: +128 for offset-stored unsigned codes
   int relu;
 };
 
-template <int KIND>
-__device__ inline void thread_vals_init(const SrcDev& s, int64_t first_elem, ThreadVals& t) {
+// Element index of packet p, value 0, for this thread at block base `base`.
+template <int EP>
+__device__ inline int64_t pk_index(int64_t base, int p) {
+  return base + ((int64_t)p * kThreads + threadIdx.x) * EP;
+}
+
+template <int KIND, int DT>
+__device__ inline void thread_vals_init(const SrcDev& s, int64_t base0,
+                                        ThreadVals<Pack<KIND, DT>::V>& t) {
+  using PK = Pack<KIND, DT>;
   if constexpr (KIND == FXPQ_SRC_ACC) {
     EpiU u = epi_uniform(s);
-    int c0 = (int)(first_elem % s.channels);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) epi_channel(s, u, (c0 + j) % s.channels, t.M[j], t.A[j]);
+    for (int p = 0; p < PK::P; ++p) {
+      int c0 = (int)(pk_index<PK::EP>(base0, p) % s.channels);
+#pragma unroll
+      for (int j = 0; j < PK::EP; ++j)
+        epi_channel(s, u, (c0 + j) % s.channels, t.M[p * PK::EP + j], t.A[p * PK::EP + j]);
+    }
     t.relu = s.ep_relu;
   } else if constexpr (KIND == FXPQ_SRC_ADD) {
     int F = imax(s.fa->fl, s.fb->fl);
@@ -36,9 +61,11 @@ __device__ inline void thread_vals_init(const SrcDev& s, int64_t first_elem, Thr
   }
 }
 
-// Loads values i..i+3 (i % 4 == 0, all in range).
+// Loads packet p (EP values starting at element i, all in range) as exact doubles.
 template <int KIND, int DT>
-__device__ inline void load4(const SrcDev& s, const ThreadVals& t, int64_t i, double v[4]) {
+__device__ inline void load_packet(const SrcDev& s, const ThreadVals<Pack<KIND, DT>::V>& t, int p,
+                                   int64_t i, double* v) {
+  constexpr int EP = Pack<KIND, DT>::EP;
   if constexpr (KIND == FXPQ_SRC_F32) {
     float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(s.x) + i);
     v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
@@ -46,30 +73,56 @@ __device__ inline void load4(const SrcDev& s, const ThreadVals& t, int64_t i, do
     int4 a = *reinterpret_cast<const int4*>(static_cast<const int32_t*>(s.x) + i);
     v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
   } else if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) {
-    const longlong2* p = reinterpret_cast<const longlong2*>(static_cast<const int64_t*>(s.x) + i);
-    longlong2 a = p[0], b = p[1];
-    v[0] = (double)a.x; v[1] = (double)a.y; v[2] = (double)b.x; v[3] = (double)b.y;
+    longlong2 a = *reinterpret_cast<const longlong2*>(static_cast<const int64_t*>(s.x) + i);
+    v[0] = (double)a.x; v[1] = (double)a.y;
   } else if constexpr (KIND == FXPQ_SRC_ACC) {
     int4 a = *reinterpret_cast<const int4*>(static_cast<const int32_t*>(s.x) + i);
-    double r0 = fma((double)a.x, t.M[0], t.A[0]);
-    double r1 = fma((double)a.y, t.M[1], t.A[1]);
-    double r2 = fma((double)a.z, t.M[2], t.A[2]);
-    double r3 = fma((double)a.w, t.M[3], t.A[3]);
-    if (t.relu) {
-      r0 = fmax(r0, 0.0); r1 = fmax(r1, 0.0); r2 = fmax(r2, 0.0); r3 = fmax(r3, 0.0);
+    int raw[4] = {a.x, a.y, a.z, a.w};
+#pragma unroll
+    for (int j = 0; j < EP; ++j) {
+      double r = fma((double)raw[j], t.M[p * EP + j], t.A[p * EP + j]);
+      v[j] = t.relu ? fmax(r, 0.0) : r;
     }
-    v[0] = r0; v[1] = r1; v[2] = r2; v[3] = r3;
   } else if constexpr (KIND == FXPQ_SRC_ADD) {
-    char4 a = *reinterpret_cast<const char4*>(static_cast<const int8_t*>(s.x) + i);
-    char4 b = *reinterpret_cast<const char4*>(static_cast<const int8_t*>(s.x2) + i);
-    double r0 = fma((double)a.x + t.oa, t.ca, ((double)b.x + t.ob) * t.cb);
-    double r1 = fma((double)a.y + t.oa, t.ca, ((double)b.y + t.ob) * t.cb);
-    double r2 = fma((double)a.z + t.oa, t.ca, ((double)b.z + t.ob) * t.cb);
-    double r3 = fma((double)a.w + t.oa, t.ca, ((double)b.w + t.ob) * t.cb);
-    if (t.relu) {
-      r0 = fmax(r0, 0.0); r1 = fmax(r1, 0.0); r2 = fmax(r2, 0.0); r3 = fmax(r3, 0.0);
+    union U16 {
+      int4 w;
+      int8_t b[16];
+    } a, b;
+    a.w = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x) + i);
+    b.w = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x2) + i);
+#pragma unroll
+    for (int j = 0; j < EP; ++j) {
+      double r = fma((double)a.b[j] + t.oa, t.ca, ((double)b.b[j] + t.ob) * t.cb);
+      v[j] = t.relu ? fmax(r, 0.0) : r;
     }
-    v[0] = r0; v[1] = r1; v[2] = r2; v[3] = r3;
+  }
+}
+
+// Drives a streaming kernel: calls f(value) for every value of this thread's
+// packets over the grid-stride loop (all packets' loads issued first), then the
+// values past the last whole packet in thread 0 of block 0.
+template <int KIND, int DT, typename F>
+__device__ inline void stream_values(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
+                                     F&& f) {
+  using PK = Pack<KIND, DT>;
+  const int64_t chunk = (int64_t)kThreads * PK::V;
+  const int64_t stride = (int64_t)gridDim.x * chunk;
+  const int64_t nfull = n - n % PK::EP;
+  for (int64_t base = (int64_t)blockIdx.x * chunk; base < nfull; base += stride) {
+    double v[PK::P][PK::EP];
+    bool ok[PK::P];
+#pragma unroll
+    for (int p = 0; p < PK::P; ++p) {
+      int64_t i = pk_index<PK::EP>(base, p);
+      ok[p] = i < nfull;
+      if (ok[p]) load_packet<KIND, DT>(s, t, p, i, v[p]);
+    }
+#pragma unroll
+    for (int p = 0; p < PK::P; ++p)
+      if (ok[p]) {
+#pragma unroll
+        for (int j = 0; j < PK::EP; ++j) f(v[p][j], pk_index<PK::EP>(base, p) + j);
+      }
   }
 }
 
@@ -89,12 +142,11 @@ __device__ inline double load1(const SrcDev& s, int64_t i) {
     double r = fma((double)static_cast<const int32_t*>(s.x)[i], M, A);
     return s.ep_relu ? fmax(r, 0.0) : r;
   } else {
-    ThreadVals t;
-    thread_vals_init<FXPQ_SRC_ADD>(s, 0, t);
-    double a = (double)static_cast<const int8_t*>(s.x)[i] + t.oa;
-    double b = (double)static_cast<const int8_t*>(s.x2)[i] + t.ob;
-    double r = fma(a, t.ca, b * t.cb);
-    return t.relu ? fmax(r, 0.0) : r;
+    int F = imax(s.fa->fl, s.fb->fl);
+    double a = (double)static_cast<const int8_t*>(s.x)[i] + (code_is_off(s.dtype, s.fa) ? 128.0 : 0.0);
+    double b = (double)static_cast<const int8_t*>(s.x2)[i] + (code_is_off(s.dtype2, s.fb) ? 128.0 : 0.0);
+    double r = fma(a, ldexp(1.0, F - s.fa->fl), b * ldexp(1.0, F - s.fb->fl));
+    return s.relu ? fmax(r, 0.0) : r;
   }
 }
 

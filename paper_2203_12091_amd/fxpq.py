@@ -22,8 +22,9 @@ EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_fl_search", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
-    "fxpq_epilogue_scale",
+    "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
 ]
+TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT = range(4)
 
 
 class Fmt(C.Structure):
@@ -82,6 +83,8 @@ def lib():
             "fxpq_avgpool_global": [p, p, C.c_int, p, i32, i32, i32, i64, p],
             "fxpq_layer_error": [p, p, p, C.c_int, p, i64, p],
             "fxpq_epilogue_scale": [p, p, p],
+            "fxpq_timer_start": [p, C.c_int],
+            "fxpq_timer_read": [p, p, p, p],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -197,6 +200,17 @@ def layer_error(h, ref, codes, code_type, d_fmt, n, d_out):
 
 def epilogue_scale(h, ep, d_scale):
     _call("fxpq_epilogue_scale", h.value, C.byref(ep), ptr(d_scale))
+
+
+def timer_start(h, kind):
+    _call("fxpq_timer_start", h.value, kind)
+
+
+def timer_read(h):
+    """(total ms, launches, algorithmic work) of the timed kernel."""
+    ms, n, work = C.c_double(), C.c_int64(), C.c_double()
+    _call("fxpq_timer_read", h.value, C.byref(ms), C.byref(n), C.byref(work))
+    return ms.value, n.value, work.value
 
 
 # ---- descriptor helpers (plain struct filling) --------------------------------
