@@ -1,0 +1,165 @@
+"""Parity at the benchmark's full size (ResNet-50, batch 256, 224x224), in the
+launch configuration bench.py times.
+
+* The first C-Block is recomputed completely by the oracle from the seeded
+  inputs: the input's FL search and all 38.5 M input codes, the 205 M conv1
+  accumulators through the BN-as-Scale epilogue, conv1's FL search over all of
+  them and all 205 M conv1 codes.
+* Deeper layers depend on every earlier tensor-wide search, so they are
+  checked through properties that hold at any size: no device flags, every
+  format valid and in range, every code inside its format's range, and two
+  forwards bit-identical.
+* Kernel-level checks at the largest layer shapes with seeded tensors: an FL
+  search and requantization over 205 M int32 accumulator-like values (exact
+  oracle over all of them) and the largest 3x3 conv at sampled outputs.
+"""
+import numpy as np
+import pytest
+
+import synth
+from gpu_util import DEV, decode8, dev, empty, fmt_host, fmt_new, host, note
+
+pytestmark = pytest.mark.gpu
+
+FL_LO, FL_HI = -8, 15
+
+
+@pytest.fixture(scope="module")
+def env():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import oracle
+    from paper_2203_12091_amd import fxpq, nets
+    oracle.lib()
+    return torch, fxpq, nets, oracle
+
+
+@pytest.fixture(scope="module")
+def full_net(env):
+    torch, fx, nets, oracle = env
+    note("fullsize resnet50 b256 forward")
+    net = nets.CalibNet("resnet50", batch=256, image=224, device=DEV)
+    net.forward()
+    return net
+
+
+def test_first_cblock_full_batch_bit_exact(env, full_net):
+    torch, fx, nets, orc = env
+    net = full_net
+    res = net.results()
+    assert res["flags"] == 0
+    x = synth.normal(4, "input", (256, 3, 224, 224))
+    note("fullsize oracle input search")
+    fl_in, s_in, _ = orc.fl_search_f32(x.ravel(), 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert res["fmts"]["input"] == (8, fl_in, s_in)
+    xq = orc.quantize_f32(x, 8, fl_in, s_in)
+    gq = net.act_codes["input"].cpu().numpy()[..., :3]
+    gq = decode8(gq, s_in == 0).transpose(0, 3, 1, 2)
+    assert np.array_equal(gq, xq)
+    del gq
+    # conv1 + BN-as-Scale + ReLU, then its FxP-QLayer, all 205 M outputs
+    w = synth.he_normal(4, "conv1.w", (64, 3, 7, 7))
+    fw = res["fmts"]["conv1.w"]
+    ofl_w, osg_w, _ = orc.fl_search_f32(w.ravel(), 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert fw == (8, ofl_w, osg_w)
+    wq = orc.quantize_f32(w, 8, ofl_w, osg_w)
+    gamma = synth.uniform(4, "conv1.bn.gamma", (64,), 0.5, 1.5)
+    beta = synth.normal(4, "conv1.bn.beta", (64,), std=0.1)
+    eps = np.float32(1e-5)
+    a1 = (gamma / np.sqrt(np.ones(64, np.float32) + eps)).astype(np.float32)
+    a2 = (beta - gamma * np.zeros(64, np.float32) / np.sqrt(np.ones(64, np.float32) + eps)).astype(np.float32)
+    f1, s1, _ = orc.fl_search_f32(a1, 16, orc.SIGN_AUTO, FL_LO, FL_HI)
+    f2, s2, _ = orc.fl_search_f32(a2, 32, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert res["fmts"]["conv1.a1"] == (16, f1, s1) and res["fmts"]["conv1.a2"] == (32, f2, s2)
+    note("fullsize oracle conv1")
+    acc = orc.conv2d(xq, wq, 2, 3)
+    v, s = orc.epilogue(acc, fl_in + ofl_w, None, 0, orc.quantize_f32(a1, 16, f1, s1), f1,
+                        orc.quantize_f32(a2, 32, f2, s2), f2, True)
+    del acc
+    note("fullsize oracle conv1 search")
+    fl_c, s_c, _ = orc.fl_search_i64(v.ravel(), s, 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert res["fmts"]["conv1"] == (8, fl_c, s_c)
+    want = orc.quantize_i64(v, s, 8, fl_c, s_c)
+    del v
+    got = decode8(net.act_codes["conv1"].cpu().numpy(), s_c == 0).transpose(0, 3, 1, 2)
+    assert np.array_equal(got, want)
+
+
+def test_full_forward_properties(env, full_net):
+    torch, fx, nets, orc = env
+    net = full_net
+    r1 = net.results()
+    assert r1["flags"] == 0
+    for name, (wl, fl, sign) in r1["fmts"].items():
+        assert 2 <= wl <= 32 and FL_LO <= fl <= FL_HI and sign in (0, 1), name
+    first = {}
+    for name, t in net.act_codes.items():
+        if name.startswith("pool"):
+            continue
+        wl, fl, sign = r1["fmts"][name]
+        lo, hi = orc.qrange(wl, sign)
+        off = 128 if sign == 0 else 0
+        assert int(t.min().item()) + off >= lo and int(t.max().item()) + off <= hi, name
+        if name.endswith(".add") or name.endswith(".c1") or name.endswith(".c2"):
+            assert sign == 0, name  # ReLU outputs are unsigned
+        first[name] = t.clone()
+    logits1 = net.logits.clone()
+    note("fullsize second forward")
+    net.forward()
+    r2 = net.results()
+    assert r2["fmts"] == r1["fmts"]
+    assert torch.equal(net.logits, logits1)
+    for name, t in first.items():
+        assert torch.equal(net.act_codes[name], t), name
+
+
+def test_largest_tensor_search_and_requant(env):
+    torch, fx, nets, orc = env
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+    n = 256 * 112 * 112 * 64  # conv1 output size of the benchmark
+    g = synth.rng_for(9, "fullsize-acc")
+    v = np.maximum(g.standard_normal(n, dtype=np.float32) * 3000.0, 0).astype(np.int32)
+    s = 14
+    sd = torch.tensor([s], dtype=torch.int32, device=DEV)
+    vd = dev(v)
+    note("fullsize int32 search")
+    out = fmt_new()
+    fx.fl_search(h, fx.src_int(vd, fx.I32, sd), n, 8, fx.SIGN_AUTO, FL_LO, FL_HI, out)
+    gwl, gfl, gsg, gst = fmt_host(out)
+    v64 = v.astype(np.int64)
+    ofl, osg, _ = orc.fl_search_i64(v64, s, 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert (gfl, gsg, gst) == (ofl, osg, 0)
+    codes = empty((n,), torch.int8)
+    fx.requant(h, fx.src_int(vd, fx.I32, sd), n, out, codes, fx.C8)
+    got = decode8(host(codes), gsg == 0)
+    assert np.array_equal(got, orc.quantize_i64(v64, s, 8, ofl, osg))
+    assert fx.sync_status(h) == 0
+    h.close()
+
+
+def test_largest_3x3_conv_sampled(env):
+    torch, fx, nets, orc = env
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+    # layer3 3x3 of ResNet-50 at batch 256: M = 50176, N = 256, K = 2304
+    N, C, H, K = 256, 256, 14, 256
+    x = synth.integers(10, "fs-x", (N, C, H, H), 0, 255)
+    w = synth.integers(10, "fs-w", (K, C, 3, 3), -128, 127)
+    xd = dev((np.transpose(x, (0, 2, 3, 1)) - 128).astype(np.int8))
+    wd = dev(np.transpose(w, (0, 2, 3, 1)).reshape(K, -1).astype(np.int8))
+    cs = empty((K,), torch.int32)
+    fx.weight_colsum(h, wd, K, 9 * C, cs)
+    acc = empty((N, H, H, K), torch.int32)
+    note("fullsize 3x3 conv")
+    fx.qconv(h, fx.conv_desc(N, H, H, C, K, 3, 3, 1, 1), xd, fx.U8OFF, wd, cs, None, acc)
+    got = host(acc)
+    x32, w32 = x.astype(np.int32), w.astype(np.int32)
+    g = synth.rng_for(11, "fs-sample")
+    for _ in range(2000):
+        n, k, oh, ow = (int(g.integers(0, N)), int(g.integers(0, K)), int(g.integers(0, H)),
+                        int(g.integers(0, H)))
+        assert got[n, oh, ow, k] == orc.conv2d_point(x32, w32, 1, 1, n, k, oh, ow)
+    assert fx.sync_status(h) == 0
+    h.close()
