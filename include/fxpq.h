@@ -222,6 +222,31 @@ fxpq_status fxpq_qgemm(fxpq_handle h, int64_t M, int64_t N, int64_t K, const voi
                        fxpq_dtype a_type, const int8_t* B, const int32_t* b_colsum,
                        const fxpq_epilogue* ep, int32_t* C, double* d_minmax);
 
+/*
+ * C-Block followed by its FxP-QLayer in one call (Sec. "Integer-Only
+ * Inference" and "FxP-QLayer"), for shallow contractions with wide outputs.
+ * Results are bit for bit those of
+ *     fxpq_qconv(h, d, x, x_type, w, w_colsum, ep, acc, d_minmax);
+ *     fxpq_fl_search(h, &src, M * d->k, wl, sign, fl_lo, fl_hi, d_fmt_out, NULL);
+ *     fxpq_requant(h, &src, M * d->k, d_fmt_out, y, y_type);
+ * with src the FXPQ_SRC_ACC source over acc with epilogue ep (M = n * Ho *
+ * Wo), but the int32 accumulators are recomputed by three passes of the
+ * contraction (min / max, window sums of the search, codes) instead of being
+ * stored and read back.  acc (device int32[M * k], caller-owned) is written
+ * only when the search needs its exact general pass; its contents are
+ * unspecified afterwards.  d_minmax (device double[2]) receives the min and max
+ * of the C-Block values.  y (device, M x k codes, NHWC) has y_type FXPQ_C8,
+ * FXPQ_I8 or FXPQ_U8OFF.  Requirements: those of fxpq_qconv, ep != NULL,
+ * c % 16 == 0, 2 <= wl <= 32, fl range as fxpq_fl_search, and at most 61440
+ * output tiles (of 128 x 128, or 256 x 64 when k <= 64); FXPQ_ERR_UNSUPPORTED
+ * otherwise.  Errors of the search are reported as by fxpq_fl_search.
+ */
+fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
+                        const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
+                        int32_t wl, int32_t sign, int32_t fl_lo, int32_t fl_hi,
+                        fxpq_fmt* d_fmt_out, void* y, fxpq_dtype y_type, int32_t* acc,
+                        double* d_minmax);
+
 /* Sum of each filter's codes: colsum[k] = sum_j w[k][j] for w[k][len] (device). */
 fxpq_status fxpq_weight_colsum(fxpq_handle h, const int8_t* w, int64_t k, int64_t len,
                                int32_t* colsum);
@@ -261,7 +286,8 @@ typedef enum {
   FXPQ_TIMER_OFF = 0,
   FXPQ_TIMER_FLS_WINDOW = 1, /* the one-read window pass of fxpq_fl_search */
   FXPQ_TIMER_QCONV = 2,      /* the contraction kernel of fxpq_qconv / fxpq_qgemm */
-  FXPQ_TIMER_REQUANT = 3     /* the kernel of fxpq_requant / fxpq_quantize */
+  FXPQ_TIMER_REQUANT = 3,    /* the kernel of fxpq_requant / fxpq_quantize */
+  FXPQ_TIMER_CBLOCK_PASS = 4 /* each contraction pass of fxpq_cblock */
 } fxpq_timer_kind;
 
 /*
@@ -277,7 +303,8 @@ fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind);
  * fxpq_timer_start: the summed kernel time in ms, the number of launches, and
  * the summed algorithmic work (HBM bytes the kernel must move: 4 B per int32
  * value read, 2 B per eltwise element, 8 B per int64 value, 4 + 1 B per
- * quantized fp32 value; or int8 operations 2*M*N*K for the contraction).
+ * quantized fp32 value; or int8 operations 2*M*N*K for the contraction, per
+ * pass for fxpq_cblock).
  */
 fxpq_status fxpq_timer_read(fxpq_handle h, double* total_ms, int64_t* launches, double* work);
 

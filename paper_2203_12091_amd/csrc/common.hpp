@@ -141,9 +141,19 @@ hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_f
                           int code_type);
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
+hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,
+                                 int fl_hi, int mode, const double* d_minmax, int nb,
+                                 fxpq_fmt* out);
+hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
+                              int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                        const int8_t* w, const int32_t* colsum, const SrcDev* ep, int32_t* acc,
                        double* d_minmax);
+int conv_fused_blocks(const fxpq_conv_desc& d);  // -1 when the fused path does not apply
+hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
+                             const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
+                             int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,
+                             double* d_minmax);
 hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out);
 hipError_t launch_maxpool(const Ctx& c, const int8_t* x, int n, int h, int w, int ch, int ks,
                           int stride, int pad, int8_t* y);

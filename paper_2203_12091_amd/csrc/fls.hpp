@@ -1,0 +1,276 @@
+// Shared pieces of the exact fractional-length search (used by the search
+// kernels and by the fused conv epilogues).
+#pragma once
+
+#include <limits.h>
+#include <math.h>
+
+#include "values.hpp"
+
+namespace fxpq {
+
+struct FlsPlan {
+  int need_general;
+  int gen_lo, gen_hi;
+  int gen_extra;  // INT_MIN when none
+  int sign;
+  int status;
+};
+
+enum FlsMode { MODE_SEARCH = 0, MODE_REPORT = 1 };
+
+constexpr double kTwoM26 = 1.0 / 67108864.0;  // 2^-26
+constexpr double kTwo26 = 67108864.0;
+
+// ---------------------------------------------------------------------------
+// Small signed 512-bit integer (two's complement), used by one thread.
+// ---------------------------------------------------------------------------
+struct Big {
+  unsigned long long w[8];
+};
+
+__device__ inline Big big_from_i128(__int128 v) {
+  Big b;
+  b.w[0] = (unsigned long long)v;
+  b.w[1] = (unsigned long long)(v >> 64);
+  unsigned long long ext = (v < 0) ? ~0ull : 0ull;
+  for (int i = 2; i < 8; ++i) b.w[i] = ext;
+  return b;
+}
+
+__device__ inline Big big_shl(const Big& a, int s) {
+  Big r;
+  int ws = s / 64, bs = s % 64;
+  for (int i = 7; i >= 0; --i) {
+    unsigned long long hi = (i - ws >= 0) ? a.w[i - ws] : 0ull;
+    unsigned long long lo = (i - ws - 1 >= 0) ? a.w[i - ws - 1] : 0ull;
+    r.w[i] = bs ? (hi << bs) | (lo >> (64 - bs)) : hi;
+  }
+  return r;
+}
+
+__device__ inline Big big_sub(const Big& a, const Big& b) {
+  Big r;
+  unsigned long long borrow = 0;
+  for (int i = 0; i < 8; ++i) {
+    unsigned long long x = a.w[i], y = b.w[i];
+    unsigned long long d = x - y - borrow;
+    borrow = (x < y) || (x - y < borrow) ? 1ull : 0ull;
+    r.w[i] = d;
+  }
+  return r;
+}
+
+__device__ inline int big_cmp(const Big& a, const Big& b) {
+  bool na = (long long)a.w[7] < 0, nb = (long long)b.w[7] < 0;
+  if (na != nb) return na ? -1 : 1;
+  for (int i = 7; i >= 0; --i)
+    if (a.w[i] != b.w[i]) return a.w[i] < b.w[i] ? -1 : 1;
+  return 0;
+}
+
+__device__ inline double big_to_double(const Big& a) {
+  bool neg = (long long)a.w[7] < 0;
+  Big m = a;
+  if (neg) {
+    Big z;
+    for (int i = 0; i < 8; ++i) z.w[i] = 0;
+    m = big_sub(z, a);
+  }
+  double r = 0.0;
+  for (int i = 7; i >= 0; --i) r = r * 18446744073709551616.0 + (double)m.w[i];
+  return neg ? -r : r;
+}
+
+// ---------------------------------------------------------------------------
+// Uniform set-up shared by both passes.
+// ---------------------------------------------------------------------------
+struct FlsU {
+  int sv;        // fractional length of the loaded values v
+  int sign;
+  double qmin, qmax;
+  int sigma;     // W = v * 2^(sigma - sv) is an integer where it matters
+  double wscale; // 2^(sigma - sv)
+  double absmax; // max |v|
+  int beta_nosat;
+  int ok;        // 0: non-finite input
+};
+
+template <int KIND>
+__device__ inline FlsU fls_uniform(const SrcDev& s, const double* mm, int wl, int sign_req,
+                                   int fl_lo, int fl_hi) {
+  FlsU u;
+  u.sv = (KIND == FXPQ_SRC_F32) ? 0 : src_scale(s);
+  double mn = mm[0], mx = mm[1];
+  u.ok = isfinite(mn) && isfinite(mx);
+  u.sign = (sign_req == FXPQ_SIGN_AUTO) ? (mn < 0.0 ? 1 : 0) : sign_req;
+  u.qmax = ldexp(1.0, wl - u.sign) - 1.0;
+  u.qmin = u.sign ? -ldexp(1.0, wl - 1) : 0.0;
+  u.absmax = fmax(fabs(mn), fabs(mx));
+  u.sigma = (KIND == FXPQ_SRC_F32) ? fl_hi + 24 : u.sv;
+  u.wscale = ldexp(1.0, u.sigma - u.sv);
+  // largest fl with every value inside [qmin - 1/2, qmax + 1/2] after scaling
+  u.beta_nosat = fl_lo - 1;
+  if (u.ok) {
+    for (int b = fl_hi; b >= fl_lo; --b) {
+      double tmax = ldexp(mx, b - u.sv), tmin = ldexp(mn, b - u.sv);
+      if (tmax <= u.qmax + 0.5 && tmin >= u.qmin - 0.5) {
+        u.beta_nosat = b;
+        break;
+      }
+    }
+  }
+  return u;
+}
+
+// ---------------------------------------------------------------------------
+// Pass 1: window search.
+// ---------------------------------------------------------------------------
+struct WinSetup {
+  FlsU u;
+  int verdict;  // 0: run window; 1: done (fl_hi); 2: general for all; 3: failure
+  int b0, b1, nc, bce;
+};
+
+template <int KIND>
+__device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, int sign_req,
+                                     int fl_lo, int fl_hi, int mode) {
+  WinSetup w;
+  w.u = fls_uniform<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi);
+  w.verdict = 0;
+  if (!w.u.ok) w.verdict = 3;
+  else if (mode == MODE_REPORT || wl > 16 || w.u.absmax * w.u.wscale >= kTwo52) w.verdict = 2;
+  else if (w.u.beta_nosat >= fl_hi) w.verdict = 1;
+  w.b0 = imax(fl_lo, w.u.beta_nosat);
+  w.b1 = (w.b0 + kWindow - 1 < fl_hi) ? w.b0 + kWindow - 1 : fl_hi;
+  w.nc = w.b1 - w.b0 + 1;
+  w.bce = (w.b1 < fl_hi) ? w.b1 + 1 : w.b1;
+  return w;
+}
+
+
+// Per-thread accumulators of the window pass.
+struct WinAcc {
+  double A[kWindow], PH[kWindow], PL[kWindow];
+  double V2, CE;
+};
+
+// Uniform constants of the window pass: candidate and clipping-bound scales.
+struct WinCtx {
+  double cj[kWindow];
+  double cce;
+  double qmin, qmax;
+};
+
+__device__ inline WinCtx win_ctx(const FlsU& u, const WinSetup& ws) {
+  WinCtx c;
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) c.cj[j] = ldexp(1.0, (j < ws.nc ? ws.b0 + j : ws.b1) - u.sigma);
+  c.cce = ldexp(1.0, ws.bce - u.sigma);
+  c.qmin = u.qmin;
+  c.qmax = u.qmax;
+  return c;
+}
+
+__device__ inline void win_acc_zero(WinAcc& acc) {
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) acc.A[j] = acc.PH[j] = acc.PL[j] = 0.0;
+  acc.V2 = acc.CE = 0.0;
+}
+
+// Adds one integer value W = v * 2^sigma.  Specialized on what the min/max
+// already tell:
+//   SPLIT    W * q sums need the Wh / Wl split to stay exact per thread;
+//   NONNEG   every value is >= 0: no lower clamp, no lower clipping term;
+//   CLAMP0   the first candidate can saturate (it is not beta_nosat).
+template <bool SPLIT, bool NONNEG, bool CLAMP0>
+__device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
+  double Wh = 0.0, Wl = W;
+  if (SPLIT) {
+    Wh = floor(W * kTwoM26);
+    Wl = fma(-Wh, kTwo26, W);
+  }
+  acc.V2 = fma(W, W, acc.V2);
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) {
+    double q = rint(W * c.cj[j]);
+    if (j > 0 || CLAMP0) {
+      q = fmin(q, c.qmax);
+      if (!NONNEG) q = fmax(q, c.qmin);
+    }
+    acc.A[j] = fma(q, q, acc.A[j]);
+    if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
+    acc.PL[j] = fma(Wl, q, acc.PL[j]);
+  }
+  double t = W * c.cce;
+  double d1 = fmax(t - c.qmax, 0.0);
+  acc.CE = fma(d1, d1, acc.CE);
+  if (!NONNEG) {
+    double d2 = fmin(t - c.qmin, 0.0);
+    acc.CE = fma(d2, d2, acc.CE);
+  }
+}
+
+// Variant index (SPLIT << 2 | NONNEG << 1 | CLAMP0) for a pass in which one
+// thread adds at most `per_thread` values.  Per-thread partial sums of W * q
+// stay exact below 2^53 without the split when
+// max|W| * max|q| * per_thread < 2^53.
+__device__ inline int win_variant(const FlsU& u, const WinSetup& ws, const double* mm,
+                                  int64_t per_thread) {
+  const double qabs = fmax(u.qmax, -u.qmin);
+  const bool split = u.absmax * u.wscale * qabs * (double)per_thread >= kTwo53;
+  const bool nonneg = mm[0] >= 0.0;
+  const bool clamp0 = ws.b0 != u.beta_nosat;
+  return (split ? 4 : 0) | (nonneg ? 2 : 0) | (clamp0 ? 1 : 0);
+}
+
+// Records a decision taken before the data is read (verdict != 0): done at
+// fl_hi, the general pass over every candidate, or a failure.
+__device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, int fl_hi,
+                                         FlsPlan* plan, fxpq_fmt* out, unsigned* flags) {
+  plan->sign = ws.u.sign;
+  plan->status = 0;
+  plan->need_general = 0;
+  plan->gen_extra = INT_MIN;
+  if (ws.verdict == 1) {
+    *out = fxpq_fmt{wl, fl_hi, ws.u.sign, 0};
+  } else if (ws.verdict == 2) {
+    plan->need_general = 1;
+    plan->gen_lo = fl_lo;
+    plan->gen_hi = fl_hi;
+  } else {
+    plan->status = 1;
+    *out = fxpq_fmt{wl, 0, ws.u.sign, 1};
+    raise_flag(flags, FXPQ_FLAG_RANGE);
+  }
+}
+
+// Block partials of the window pass: the exact integer sums as int64 (each
+// per-thread sum is an exact integer below 2^53, the block sum below 2^61),
+// the two bound sums as fp64.  Slot `bid` of part_i (3 * kWindow) / part_f (2).
+__device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long long* part_i,
+                                          double* part_f, long long* shl, double* shd) {
+  long long* pi = part_i + bid * (3 * kWindow);
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) {
+    long long a = block_reduce((long long)acc.A[j], OpAddL(), shl);
+    long long ph = block_reduce((long long)acc.PH[j], OpAddL(), shl);
+    long long pl = block_reduce((long long)acc.PL[j], OpAddL(), shl);
+    if (threadIdx.x == 0) {
+      pi[3 * j] = a;
+      pi[3 * j + 1] = ph;
+      pi[3 * j + 2] = pl;
+    }
+  }
+  double v2 = block_reduce(acc.V2, OpAddD(), shd);
+  double ce = block_reduce(acc.CE, OpAddD(), shd);
+  if (threadIdx.x == 0) {
+    part_f[2 * bid] = v2;
+    part_f[2 * bid + 1] = ce;
+  }
+}
+
+// Launch helpers shared by the streaming search and the fused C-Block.
+constexpr int kFinThreads = 1024;
+
+}  // namespace fxpq

@@ -266,10 +266,10 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
   return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
 }
 
-static fxpq_status conv_common(fxpq_handle h, const fxpq_conv_desc* d, const void* x,
-                               fxpq_dtype x_type, const int8_t* w, const int32_t* w_colsum,
-                               const fxpq_epilogue* ep, int32_t* acc, double* d_minmax) {
-  if (!h || !d || !x || !w || !acc) return FXPQ_ERR_INVALID_ARG;
+static fxpq_status conv_check(const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
+                              const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
+                              const int32_t* acc) {
+  if (!d || !x || !w || !acc) return FXPQ_ERR_INVALID_ARG;
   if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
       d->stride < 1 || d->pad < 0)
     return FXPQ_ERR_INVALID_ARG;
@@ -291,11 +291,47 @@ static fxpq_status conv_common(fxpq_handle h, const fxpq_conv_desc* d, const voi
   if (blocks > kMaxConvBlocks) return FXPQ_ERR_UNSUPPORTED;
   if (!aligned(w, 16) || !aligned(acc, 4) || !aligned(x, d->c == 4 ? 4 : 16))
     return FXPQ_ERR_INVALID_ARG;
+  return FXPQ_OK;
+}
+
+static fxpq_status conv_common(fxpq_handle h, const fxpq_conv_desc* d, const void* x,
+                               fxpq_dtype x_type, const int8_t* w, const int32_t* w_colsum,
+                               const fxpq_epilogue* ep, int32_t* acc, double* d_minmax) {
+  if (!h) return FXPQ_ERR_INVALID_ARG;
+  fxpq_status st = conv_check(d, x, x_type, w, w_colsum, ep, acc);
+  if (st) return st;
   SrcDev e;
   if (ep) epi_to_dev(ep, &e);
   DeviceGuard g(h->device);
   return hip_status(launch_conv(ctx(h), *d, x, x_type, w, w_colsum, ep ? &e : nullptr, acc,
                                 ep ? d_minmax : nullptr));
+}
+
+fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
+                        const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
+                        int32_t wl, int32_t sign, int32_t fl_lo, int32_t fl_hi,
+                        fxpq_fmt* d_fmt_out, void* y, fxpq_dtype y_type, int32_t* acc,
+                        double* d_minmax) {
+  if (!h || !ep || !d_fmt_out || !y || !d_minmax) return FXPQ_ERR_INVALID_ARG;
+  fxpq_status st = conv_check(d, x, x_type, w, w_colsum, ep, acc);
+  if (st) return st;
+  if (y_type != FXPQ_C8 && y_type != FXPQ_I8 && y_type != FXPQ_U8OFF) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 1 || wl > 32) return FXPQ_ERR_INVALID_ARG;
+  if (wl == 1) return FXPQ_ERR_UNSUPPORTED;
+  if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
+  if (d->c % 16 != 0) return FXPQ_ERR_UNSUPPORTED;
+  const int nb = conv_fused_blocks(*d);
+  if (nb < 1 || nb > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  SrcDev e;
+  epi_to_dev(ep, &e);
+  e.kind = FXPQ_SRC_ACC;
+  e.dtype = FXPQ_I32;
+  e.x = acc;
+  DeviceGuard g(h->device);
+  return hip_status(launch_conv_fused(ctx(h), *d, x, x_type, w, w_colsum, e, wl, sign, fl_lo,
+                                      fl_hi, d_fmt_out, static_cast<int8_t*>(y), y_type, d_minmax));
 }
 
 fxpq_status fxpq_qconv(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
@@ -355,7 +391,7 @@ fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
 }
 
 fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind) {
-  if (!h || kind < FXPQ_TIMER_OFF || kind > FXPQ_TIMER_REQUANT) return FXPQ_ERR_INVALID_ARG;
+  if (!h || kind < FXPQ_TIMER_OFF || kind > FXPQ_TIMER_CBLOCK_PASS) return FXPQ_ERR_INVALID_ARG;
   DeviceGuard g(h->device);
   Timer& t = h->timer;
   if (kind != FXPQ_TIMER_OFF && !t.ev) {

@@ -14,13 +14,23 @@
 // u - 128, both meaning the value 0).
 //
 // Epilogue: for inputs stored as u - 128 the exact accumulator is restored by
-// adding 128 * (sum of the filter's codes).  The int32 accumulators are
-// stored; optionally the exact min / max of the C-Block values (bias, Scale,
-// ReLU applied in fp64, exact below 2^53) are reduced for the FxP-QLayer.
+// adding 128 * (sum of the filter's codes).  Then, by mode:
+//   EPI_ACC  store the int32 accumulators; optionally reduce the exact min /
+//            max of the C-Block values (bias, Scale, ReLU applied in fp64,
+//            exact below 2^53) for the FxP-QLayer;
+//   EPI_MM   only the min / max;
+//   EPI_WIN  the window partial sums of the exact FL search over the C-Block
+//            values (the same sums the streaming window pass forms);
+//   EPI_REQ  the C-Block values requantized to the searched format (Eq. 1-2).
+// A C-Block whose contraction is shallow (R * S * C small next to the output)
+// is cheaper to recompute three times than to write, and read twice, as
+// int32: the fused launcher runs EPI_MM, EPI_WIN and EPI_REQ over the same
+// operands, and stores int32 accumulators only when the window pass cannot
+// decide and the exact general pass needs them.
 #include <limits.h>
 #include <math.h>
 
-#include "values.hpp"
+#include "fls.hpp"
 
 namespace fxpq {
 
@@ -31,6 +41,7 @@ constexpr int BK = 64;
 constexpr int LDS_STRIDE = 80;  // bytes per staged row: 64 + 16 to spread LDS banks
 
 enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2 };
+enum Epi { EPI_ACC = 0, EPI_MM = 1, EPI_WIN = 2, EPI_REQ = 3 };
 
 struct ConvArgs {
   const int8_t* x;
@@ -46,9 +57,26 @@ struct ConvArgs {
   SrcDev ep;    // kind == FXPQ_SRC_ACC when an epilogue is given
   int has_ep;
   double* mm_part;
+  // EPI_ACC: store only when the FL-search plan asks for the general pass
+  int only_if_general;
+  const FlsPlan* plan_in;
+  // EPI_WIN
+  int wl, sign_req, fl_lo, fl_hi;
+  const double* mm;      // min / max of the C-Block values
+  long long* part_i;
+  double* part_f;
+  FlsPlan* plan;
+  fxpq_fmt* fmt_win;
+  unsigned* flags;
+  // EPI_REQ
+  const fxpq_fmt* fmt_req;
+  int8_t* y;
+  int y_type;
 };
 
-template <int BM, int BN, int LOADER>
+constexpr int kConvPerThread = 64;  // accumulators per thread (BM * BN / 256)
+
+template <int BM, int BN, int LOADER, int EPI>
 __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
   constexpr int WN = BN / 64;   // waves along N
   constexpr int ACH = BM / 64;  // A chunks (16 B) per thread per slab
@@ -57,6 +85,27 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) int8_t Bs[2][BN * LDS_STRIDE];
   __shared__ int rs_tab[128];
   __shared__ double shd[8];
+  __shared__ long long shl[8];
+
+  // Decisions every block takes identically before any load.
+  WinSetup ws;
+  QFmt qf;
+  if constexpr (EPI == EPI_ACC) {
+    if (a.only_if_general && (!a.plan_in->need_general || a.plan_in->status)) return;
+  } else if constexpr (EPI == EPI_WIN) {
+    ws = win_setup<FXPQ_SRC_ACC>(a.ep, a.mm, a.wl, a.sign_req, a.fl_lo, a.fl_hi, MODE_SEARCH);
+    if (ws.verdict != 0) {
+      if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+        win_verdict_write(ws, a.wl, a.fl_lo, a.fl_hi, a.plan, a.fmt_win, a.flags);
+      return;
+    }
+  } else if constexpr (EPI == EPI_REQ) {
+    const int sv = src_scale(a.ep);
+    if (a.y_type == FXPQ_I8) qf = qfmt_setup<FXPQ_I8>(a.fmt_req, sv, a.flags);
+    else if (a.y_type == FXPQ_U8OFF) qf = qfmt_setup<FXPQ_U8OFF>(a.fmt_req, sv, a.flags);
+    else qf = qfmt_setup<FXPQ_C8>(a.fmt_req, sv, a.flags);
+    if (!qf.ok) return;
+  }
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -197,87 +246,206 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
   }
 
   // ---- epilogue ----
-  double mn = INFINITY, mx = -INFINITY;
+  // Visits this thread's in-range accumulators (restored for u - 128 inputs)
+  // with the channel's epilogue constants.
+  const bool want_vals = (EPI != EPI_ACC) || a.want_mm;
   EpiU eu;
-  if (a.want_mm) eu = epi_uniform(a.ep);
+  if (want_vals) eu = epi_uniform(a.ep);
+  auto visit = [&](auto&& f) {
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
-    const int cc = col < a.K ? col : a.K - 1;
-    const int corr = a_off ? 128 * a.colsum[cc] : 0;
-    double Mc = 1.0, Ac = 0.0;
-    if (a.want_mm) epi_channel(a.ep, eu, cc, Mc, Ac);
+    for (int ni = 0; ni < 2; ++ni) {
+      const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
+      const int cc = col < a.K ? col : a.K - 1;
+      const int corr = a_off ? 128 * a.colsum[cc] : 0;
+      double Mc = 1.0, Ac = 0.0;
+      if (want_vals) epi_channel(a.ep, eu, cc, Mc, Ac);
 #pragma unroll
-    for (int mi = 0; mi < 2; ++mi) {
+      for (int mi = 0; mi < 2; ++mi) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = m0 + wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const int v = acc[mi][ni][e] + corr;
-        if (row < a.M && col < a.K) {
-          a.acc[(int64_t)row * a.K + col] = v;
-          if (a.want_mm) {
-            double val = fma((double)v, Mc, Ac);
-            if (a.ep.ep_relu) val = fmax(val, 0.0);
-            mn = fmin(mn, val);
-            mx = fmax(mx, val);
-          }
+        for (int e = 0; e < 16; ++e) {
+          const int row = m0 + wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          if (row < a.M && col < a.K) f(acc[mi][ni][e] + corr, Mc, Ac, row, col);
         }
       }
     }
-  }
-  if (!a.want_mm) return;
-  mn = block_reduce(mn, OpMin(), shd);
-  mx = block_reduce(mx, OpMax(), shd);
+  };
+  const int relu = a.ep.ep_relu;
   const int bid = blockIdx.y * gridDim.x + blockIdx.x;
-  if (tid == 0) {
-    a.mm_part[2 * bid] = mn;
-    a.mm_part[2 * bid + 1] = mx;
+
+  if constexpr (EPI == EPI_ACC || EPI == EPI_MM) {
+    double mn = INFINITY, mx = -INFINITY;
+    visit([&](int v, double Mc, double Ac, int row, int col) {
+      if (EPI == EPI_ACC) a.acc[(int64_t)row * a.K + col] = v;
+      if (want_vals) {
+        double val = fma((double)v, Mc, Ac);
+        if (relu) val = fmax(val, 0.0);
+        mn = fmin(mn, val);
+        mx = fmax(mx, val);
+      }
+    });
+    if (!want_vals) return;
+    mn = block_reduce(mn, OpMin(), shd);
+    mx = block_reduce(mx, OpMax(), shd);
+    if (tid == 0) {
+      a.mm_part[2 * bid] = mn;
+      a.mm_part[2 * bid + 1] = mx;
+    }
+  } else if constexpr (EPI == EPI_WIN) {
+    const FlsU& u = ws.u;
+    const WinCtx wc = win_ctx(u, ws);
+    WinAcc wa;
+    win_acc_zero(wa);
+    // W = v * 2^(sigma - sv): fold the integer scaling into the constants.
+    const double wsc = u.wscale;
+#define FXPQ_WIN_VISIT(SP, NN, C0)                                          \
+  visit([&](int v, double Mc, double Ac, int, int) {                        \
+    double W = fma((double)v, Mc * wsc, Ac * wsc);                          \
+    if (relu) W = fmax(W, 0.0);                                             \
+    win_consume<SP, NN, C0>(wc, wa, W);                                     \
+  })
+    switch (win_variant(u, ws, a.mm, kConvPerThread)) {
+      case 0: FXPQ_WIN_VISIT(false, false, false); break;
+      case 1: FXPQ_WIN_VISIT(false, false, true); break;
+      case 2: FXPQ_WIN_VISIT(false, true, false); break;
+      case 3: FXPQ_WIN_VISIT(false, true, true); break;
+      case 4: FXPQ_WIN_VISIT(true, false, false); break;
+      case 5: FXPQ_WIN_VISIT(true, false, true); break;
+      case 6: FXPQ_WIN_VISIT(true, true, false); break;
+      default: FXPQ_WIN_VISIT(true, true, true); break;
+    }
+#undef FXPQ_WIN_VISIT
+    win_write_partials(wa, bid, a.part_i, a.part_f, shl, shd);
+  } else {  // EPI_REQ
+    visit([&](int v, double Mc, double Ac, int row, int col) {
+      double val = fma((double)v, Mc, Ac);
+      if (relu) val = fmax(val, 0.0);
+      a.y[(int64_t)row * a.K + col] = (int8_t)quant_one(val, qf);
+    });
   }
 }
 
-template <int BM, int BN>
+template <int BM, int BN, int EPI>
 static void conv_dispatch_loader(int loader, dim3 grid, hipStream_t st, const ConvArgs& a) {
   if (loader == LD_FAST64)
-    k_qconv<BM, BN, LD_FAST64><<<grid, 256, 0, st>>>(a);
+    k_qconv<BM, BN, LD_FAST64, EPI><<<grid, 256, 0, st>>>(a);
   else if (loader == LD_GEN16)
-    k_qconv<BM, BN, LD_GEN16><<<grid, 256, 0, st>>>(a);
-  else
-    k_qconv<BM, BN, LD_RGB4><<<grid, 256, 0, st>>>(a);
+    k_qconv<BM, BN, LD_GEN16, EPI><<<grid, 256, 0, st>>>(a);
+  else if constexpr (EPI == EPI_ACC)
+    k_qconv<BM, BN, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
 }
 
-hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
-                       const int8_t* w, const int32_t* colsum, const SrcDev* ep, int32_t* acc,
-                       double* d_minmax) {
-  ConvArgs a;
+// Tile shape and grid of a conv; loader choice and the geometry in `a`.
+static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const int8_t* w,
+                       const int32_t* colsum, const SrcDev* ep, ConvArgs& a, int& loader,
+                       bool& wide) {
   a.x = static_cast<const int8_t*>(x);
   a.w = w;
   a.colsum = colsum;
-  a.acc = acc;
   a.N = d.n; a.H = d.h; a.W = d.w; a.C = d.c; a.K = d.k; a.R = d.r; a.S = d.s;
   a.stride = d.stride; a.pad = d.pad;
   a.Ho = (d.h + 2 * d.pad - d.r) / d.stride + 1;
   a.Wo = (d.w + 2 * d.pad - d.s) / d.stride + 1;
   a.M = d.n * a.Ho * a.Wo;
   a.kdepth = d.r * d.s * d.c;
-  int loader = (d.c % 64 == 0) ? LD_FAST64 : (d.c == 4 ? LD_RGB4 : LD_GEN16);
+  loader = (d.c % 64 == 0) ? LD_FAST64 : (d.c == 4 ? LD_RGB4 : LD_GEN16);
   a.wrow = (loader == LD_RGB4) ? (a.kdepth + 63) / 64 * 64 : a.kdepth;
   if (loader == LD_RGB4) a.kdepth = a.wrow;
   a.x_type = x_type;
   a.has_ep = ep != nullptr;
   if (ep) a.ep = *ep;
+  wide = d.k <= 64;  // 256 x 64 tiles for narrow outputs, else 128 x 128
+  return wide ? dim3((a.M + 255) / 256, (d.k + 63) / 64) : dim3((a.M + 127) / 128, (d.k + 127) / 128);
+}
+
+template <int EPI>
+static void conv_run(const ConvArgs& a, int loader, bool wide, dim3 grid, hipStream_t st) {
+  if (wide)
+    conv_dispatch_loader<256, 64, EPI>(loader, grid, st, a);
+  else
+    conv_dispatch_loader<128, 128, EPI>(loader, grid, st, a);
+}
+
+hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
+                       const int8_t* w, const int32_t* colsum, const SrcDev* ep, int32_t* acc,
+                       double* d_minmax) {
+  ConvArgs a{};
+  int loader;
+  bool wide;
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, wide);
+  a.acc = acc;
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
   bool timed = timer_begin(c, FXPQ_TIMER_QCONV);
-  dim3 grid;
-  if (d.k <= 64) {
-    grid = dim3((a.M + 255) / 256, (d.k + 63) / 64);
-    conv_dispatch_loader<256, 64>(loader, grid, c.stream, a);
-  } else {
-    grid = dim3((a.M + 127) / 128, (d.k + 127) / 128);
-    conv_dispatch_loader<128, 128>(loader, grid, c.stream, a);
-  }
+  conv_run<EPI_ACC>(a, loader, wide, grid, c.stream);
   timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   if (a.want_mm) return launch_minmax_fin(c, a.mm_part, (int)(grid.x * grid.y), d_minmax);
+  return hipGetLastError();
+}
+
+int conv_fused_blocks(const fxpq_conv_desc& d) {
+  ConvArgs a{};
+  int loader;
+  bool wide;
+  const dim3 grid = conv_setup(d, nullptr, 0, nullptr, nullptr, nullptr, a, loader, wide);
+  if (loader == LD_RGB4) return -1;
+  return (int)(grid.x * grid.y);
+}
+
+// Conv + epilogue + FxP-QLayer (FL search, requantization) with the int32
+// accumulators recomputed instead of stored.  `ep` is the ACC source of the
+// C-Block values, its x pointing at the fallback int32 buffer.
+hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
+                             const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
+                             int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,
+                             double* d_minmax) {
+  ConvArgs a{};
+  int loader;
+  bool wide;
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, wide);
+  const int nb = (int)(grid.x * grid.y);
+  const double ops = 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c);
+  const int64_t n = (int64_t)a.M * d.k;
+  // 1. min / max of the C-Block values
+  a.want_mm = 1;
+  a.mm_part = c.sc.minmax_part;
+  bool timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
+  conv_run<EPI_MM>(a, loader, wide, grid, c.stream);
+  timer_end(c, timed, ops);
+  hipError_t e = launch_minmax_fin(c, a.mm_part, nb, d_minmax);
+  if (e != hipSuccess) return e;
+  // 2. window partial sums, then the exact decision
+  a.wl = wl;
+  a.sign_req = sign;
+  a.fl_lo = fl_lo;
+  a.fl_hi = fl_hi;
+  a.mm = d_minmax;
+  a.part_i = c.sc.win_part;
+  a.part_f = c.sc.win_part_f;
+  a.plan = static_cast<FlsPlan*>(c.sc.plan);
+  a.fmt_win = out;
+  a.flags = c.sc.flags;
+  timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
+  conv_run<EPI_WIN>(a, loader, wide, grid, c.stream);
+  timer_end(c, timed, ops);
+  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, fl_hi, MODE_SEARCH, d_minmax, nb, out);
+  if (e != hipSuccess) return e;
+  // 3. only when the plan asks for the general pass: int32 accumulators, then
+  //    the exact search over every remaining candidate
+  ConvArgs g = a;
+  g.acc = static_cast<int32_t*>(const_cast<void*>(ep.x));
+  g.want_mm = 0;
+  g.only_if_general = 1;
+  g.plan_in = static_cast<const FlsPlan*>(c.sc.plan);
+  conv_run<EPI_ACC>(g, loader, wide, grid, c.stream);
+  e = launch_fls_general(c, ep, n, wl, fl_lo, fl_hi, d_minmax, out, nullptr);
+  if (e != hipSuccess) return e;
+  // 4. codes in the searched format
+  a.fmt_req = out;
+  a.y = y;
+  a.y_type = y_type;
+  timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
+  conv_run<EPI_REQ>(a, loader, wide, grid, c.stream);
+  timer_end(c, timed, ops);
   return hipGetLastError();
 }
 

@@ -22,203 +22,19 @@
 // Pass 2 ("general", only when pass 1 could not decide, when the caller asks
 //   for every error, or for word lengths above 16): the exact error of every
 //   remaining candidate in 128-bit integer arithmetic, compared exactly.
-#include <limits.h>
-#include <math.h>
-
-#include "values.hpp"
+#include "fls.hpp"
 
 namespace fxpq {
 
 int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec);
 
-struct FlsPlan {
-  int need_general;
-  int gen_lo, gen_hi;
-  int gen_extra;  // INT_MIN when none
-  int sign;
-  int status;
-};
-
-enum FlsMode { MODE_SEARCH = 0, MODE_REPORT = 1 };
-
-constexpr double kTwoM26 = 1.0 / 67108864.0;  // 2^-26
-constexpr double kTwo26 = 67108864.0;
-
-// ---------------------------------------------------------------------------
-// Small signed 512-bit integer (two's complement), used by one thread.
-// ---------------------------------------------------------------------------
-struct Big {
-  unsigned long long w[8];
-};
-
-__device__ inline Big big_from_i128(__int128 v) {
-  Big b;
-  b.w[0] = (unsigned long long)v;
-  b.w[1] = (unsigned long long)(v >> 64);
-  unsigned long long ext = (v < 0) ? ~0ull : 0ull;
-  for (int i = 2; i < 8; ++i) b.w[i] = ext;
-  return b;
-}
-
-__device__ inline Big big_shl(const Big& a, int s) {
-  Big r;
-  int ws = s / 64, bs = s % 64;
-  for (int i = 7; i >= 0; --i) {
-    unsigned long long hi = (i - ws >= 0) ? a.w[i - ws] : 0ull;
-    unsigned long long lo = (i - ws - 1 >= 0) ? a.w[i - ws - 1] : 0ull;
-    r.w[i] = bs ? (hi << bs) | (lo >> (64 - bs)) : hi;
-  }
-  return r;
-}
-
-__device__ inline Big big_sub(const Big& a, const Big& b) {
-  Big r;
-  unsigned long long borrow = 0;
-  for (int i = 0; i < 8; ++i) {
-    unsigned long long x = a.w[i], y = b.w[i];
-    unsigned long long d = x - y - borrow;
-    borrow = (x < y) || (x - y < borrow) ? 1ull : 0ull;
-    r.w[i] = d;
-  }
-  return r;
-}
-
-__device__ inline int big_cmp(const Big& a, const Big& b) {
-  bool na = (long long)a.w[7] < 0, nb = (long long)b.w[7] < 0;
-  if (na != nb) return na ? -1 : 1;
-  for (int i = 7; i >= 0; --i)
-    if (a.w[i] != b.w[i]) return a.w[i] < b.w[i] ? -1 : 1;
-  return 0;
-}
-
-__device__ inline double big_to_double(const Big& a) {
-  bool neg = (long long)a.w[7] < 0;
-  Big m = a;
-  if (neg) {
-    Big z;
-    for (int i = 0; i < 8; ++i) z.w[i] = 0;
-    m = big_sub(z, a);
-  }
-  double r = 0.0;
-  for (int i = 7; i >= 0; --i) r = r * 18446744073709551616.0 + (double)m.w[i];
-  return neg ? -r : r;
-}
-
-// ---------------------------------------------------------------------------
-// Uniform set-up shared by both passes.
-// ---------------------------------------------------------------------------
-struct FlsU {
-  int sv;        // fractional length of the loaded values v
-  int sign;
-  double qmin, qmax;
-  int sigma;     // W = v * 2^(sigma - sv) is an integer where it matters
-  double wscale; // 2^(sigma - sv)
-  double absmax; // max |v|
-  int beta_nosat;
-  int ok;        // 0: non-finite input
-};
-
-template <int KIND>
-__device__ inline FlsU fls_uniform(const SrcDev& s, const double* mm, int wl, int sign_req,
-                                   int fl_lo, int fl_hi) {
-  FlsU u;
-  u.sv = (KIND == FXPQ_SRC_F32) ? 0 : src_scale(s);
-  double mn = mm[0], mx = mm[1];
-  u.ok = isfinite(mn) && isfinite(mx);
-  u.sign = (sign_req == FXPQ_SIGN_AUTO) ? (mn < 0.0 ? 1 : 0) : sign_req;
-  u.qmax = ldexp(1.0, wl - u.sign) - 1.0;
-  u.qmin = u.sign ? -ldexp(1.0, wl - 1) : 0.0;
-  u.absmax = fmax(fabs(mn), fabs(mx));
-  u.sigma = (KIND == FXPQ_SRC_F32) ? fl_hi + 24 : u.sv;
-  u.wscale = ldexp(1.0, u.sigma - u.sv);
-  // largest fl with every value inside [qmin - 1/2, qmax + 1/2] after scaling
-  u.beta_nosat = fl_lo - 1;
-  if (u.ok) {
-    for (int b = fl_hi; b >= fl_lo; --b) {
-      double tmax = ldexp(mx, b - u.sv), tmin = ldexp(mn, b - u.sv);
-      if (tmax <= u.qmax + 0.5 && tmin >= u.qmin - 0.5) {
-        u.beta_nosat = b;
-        break;
-      }
-    }
-  }
-  return u;
-}
-
-// ---------------------------------------------------------------------------
-// Pass 1: window search.
-// ---------------------------------------------------------------------------
-struct WinSetup {
-  FlsU u;
-  int verdict;  // 0: run window; 1: done (fl_hi); 2: general for all; 3: failure
-  int b0, b1, nc, bce;
-};
-
-template <int KIND>
-__device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, int sign_req,
-                                     int fl_lo, int fl_hi, int mode) {
-  WinSetup w;
-  w.u = fls_uniform<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi);
-  w.verdict = 0;
-  if (!w.u.ok) w.verdict = 3;
-  else if (mode == MODE_REPORT || wl > 16 || w.u.absmax * w.u.wscale >= kTwo52) w.verdict = 2;
-  else if (w.u.beta_nosat >= fl_hi) w.verdict = 1;
-  w.b0 = imax(fl_lo, w.u.beta_nosat);
-  w.b1 = (w.b0 + kWindow - 1 < fl_hi) ? w.b0 + kWindow - 1 : fl_hi;
-  w.nc = w.b1 - w.b0 + 1;
-  w.bce = (w.b1 < fl_hi) ? w.b1 + 1 : w.b1;
-  return w;
-}
-
-// Accumulators of one thread in the window pass.
-struct WinAcc {
-  double A[kWindow], PH[kWindow], PL[kWindow];
-  double V2, CE;
-};
-
-// Main loop, specialized on what the min/max already tell:
-//   SPLIT    W * q sums need the Wh / Wl split to stay exact per thread;
-//   NONNEG   every value is >= 0: no lower clamp, no lower clipping term;
-//   CLAMP0   the first candidate can saturate (it is not beta_nosat).
+// Main loop of the streaming window pass over this thread's values.
 template <int KIND, int DT, bool SPLIT, bool NONNEG, bool CLAMP0>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
                                 WinAcc& acc) {
-  const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc;
-  double cj[kWindow];
-#pragma unroll
-  for (int j = 0; j < kWindow; ++j) cj[j] = ldexp(1.0, (j < nc ? b0 + j : b1) - u.sigma);
-  const double cce = ldexp(1.0, ws.bce - u.sigma);
-  const double qmin = u.qmin, qmax = u.qmax;
-#pragma unroll
-  for (int j = 0; j < kWindow; ++j) acc.A[j] = acc.PH[j] = acc.PL[j] = 0.0;
-  acc.V2 = acc.CE = 0.0;
-
-  auto consume = [&](double W) {
-    double Wh = 0.0, Wl = W;
-    if (SPLIT) {
-      Wh = floor(W * kTwoM26);
-      Wl = fma(-Wh, kTwo26, W);
-    }
-    acc.V2 = fma(W, W, acc.V2);
-#pragma unroll
-    for (int j = 0; j < kWindow; ++j) {
-      double q = rint(W * cj[j]);
-      if (j > 0 || CLAMP0) {
-        q = fmin(q, qmax);
-        if (!NONNEG) q = fmax(q, qmin);
-      }
-      acc.A[j] = fma(q, q, acc.A[j]);
-      if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
-      acc.PL[j] = fma(Wl, q, acc.PL[j]);
-    }
-    double t = W * cce;
-    double d1 = fmax(t - qmax, 0.0);
-    acc.CE = fma(d1, d1, acc.CE);
-    if (!NONNEG) {
-      double d2 = fmin(t - qmin, 0.0);
-      acc.CE = fma(d2, d2, acc.CE);
-    }
-  };
+  const WinCtx wc = win_ctx(u, ws);
+  win_acc_zero(acc);
+  auto consume = [&](double W) { win_consume<SPLIT, NONNEG, CLAMP0>(wc, acc, W); };
 
   using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -258,38 +74,14 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
 
   // Decisions every block takes identically before touching the data.
   if (ws.verdict != 0) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) {
-      plan->sign = u.sign;
-      plan->status = 0;
-      plan->need_general = 0;
-      plan->gen_extra = INT_MIN;
-      if (ws.verdict == 1) {
-        *out = fxpq_fmt{wl, fl_hi, u.sign, 0};
-      } else if (ws.verdict == 2) {
-        plan->need_general = 1;
-        plan->gen_lo = fl_lo;
-        plan->gen_hi = fl_hi;
-      } else {
-        plan->status = 1;
-        *out = fxpq_fmt{wl, 0, u.sign, 1};
-        raise_flag(flags, FXPQ_FLAG_RANGE);
-      }
-    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) win_verdict_write(ws, wl, fl_lo, fl_hi, plan, out, flags);
     return;
   }
-
-  // Uniform specialization.  Per-thread partial sums of W * q stay exact below
-  // 2^53 without the split when max|W| * max|q| * (values per thread) < 2^53.
   constexpr int V = Pack<KIND, DT>::V;
   const int64_t per_thread = ((n / V + (int64_t)gridDim.x * kThreads - 1) /
                               ((int64_t)gridDim.x * kThreads)) * V + V;
-  const double qabs = fmax(u.qmax, -u.qmin);
-  const bool split = u.absmax * u.wscale * qabs * (double)per_thread >= kTwo53;
-  const bool nonneg = mm[0] >= 0.0;
-  const bool clamp0 = ws.b0 != u.beta_nosat;
   WinAcc acc;
-  const int variant = (split ? 4 : 0) | (nonneg ? 2 : 0) | (clamp0 ? 1 : 0);
-  switch (variant) {
+  switch (win_variant(u, ws, mm, per_thread)) {
     case 0: win_loop<KIND, DT, false, false, false>(s, n, u, ws, acc); break;
     case 1: win_loop<KIND, DT, false, false, true>(s, n, u, ws, acc); break;
     case 2: win_loop<KIND, DT, false, true, false>(s, n, u, ws, acc); break;
@@ -299,36 +91,20 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     case 6: win_loop<KIND, DT, true, true, false>(s, n, u, ws, acc); break;
     default: win_loop<KIND, DT, true, true, true>(s, n, u, ws, acc); break;
   }
-
-  // Block partials: exact integers as int64, bound sums as fp64.
-  long long* pi = part_i + (int64_t)blockIdx.x * (3 * kWindow);
-#pragma unroll
-  for (int j = 0; j < kWindow; ++j) {
-    long long a = block_reduce((long long)acc.A[j], OpAddL(), shl);
-    long long ph = block_reduce((long long)acc.PH[j], OpAddL(), shl);
-    long long pl = block_reduce((long long)acc.PL[j], OpAddL(), shl);
-    if (threadIdx.x == 0) {
-      pi[3 * j] = a;
-      pi[3 * j + 1] = ph;
-      pi[3 * j + 2] = pl;
-    }
-  }
-  double v2 = block_reduce(acc.V2, OpAddD(), shd);
-  double ce = block_reduce(acc.CE, OpAddD(), shd);
-  if (threadIdx.x == 0) {
-    part_f[2 * blockIdx.x] = v2;
-    part_f[2 * blockIdx.x + 1] = ce;
-  }
+  win_write_partials(acc, blockIdx.x, part_i, part_f, shl, shd);
 }
 
-// One block: sums the window partials exactly and decides.
+// One block: sums the window partials exactly and decides.  A wide block so
+// the partial loads of a pass are all in flight at once.
+
 template <int KIND>
-__global__ __launch_bounds__(kThreads) void k_fls_window_fin(
+__global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
     SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, const double* mm,
     const long long* part_i, const double* part_f, int nb, FlsPlan* plan, fxpq_fmt* out) {
   constexpr int NQ = 3 * kWindow;
-  __shared__ long long sh_hi[4][NQ], sh_lo[4][NQ];
-  __shared__ double sh_f[4][2];
+  constexpr int NW = kFinThreads / 64;
+  __shared__ long long sh_hi[NW][NQ], sh_lo[NW][NQ];
+  __shared__ double sh_f[NW][2];
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode);
   if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
   const FlsU& u = ws.u;
@@ -339,16 +115,20 @@ __global__ __launch_bounds__(kThreads) void k_fls_window_fin(
   double f0 = 0.0, f1 = 0.0;
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) hi[qi] = lo[qi] = 0;
-  for (int b = threadIdx.x; b < nb; b += kThreads) {
+#pragma unroll 2
+  for (int b = threadIdx.x; b < nb; b += kFinThreads) {
     const long long* p = part_i + (int64_t)b * NQ;
+    long long x[NQ];
+#pragma unroll
+    for (int qi = 0; qi < NQ; ++qi) x[qi] = p[qi];
+    const double g0 = part_f[2 * b], g1 = part_f[2 * b + 1];
 #pragma unroll
     for (int qi = 0; qi < NQ; ++qi) {
-      long long x = p[qi];
-      hi[qi] += x >> 32;
-      lo[qi] += x & 0xFFFFFFFFll;
+      hi[qi] += x[qi] >> 32;
+      lo[qi] += x[qi] & 0xFFFFFFFFll;
     }
-    f0 += part_f[2 * b];
-    f1 += part_f[2 * b + 1];
+    f0 += g0;
+    f1 += g1;
   }
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
 #pragma unroll
@@ -373,12 +153,12 @@ __global__ __launch_bounds__(kThreads) void k_fls_window_fin(
   double tot_f[2] = {0.0, 0.0};
   for (int qi = 0; qi < NQ; ++qi) {
     tot_hi[qi] = tot_lo[qi] = 0;
-    for (int w = 0; w < kThreads / 64; ++w) {
+    for (int w = 0; w < NW; ++w) {
       tot_hi[qi] += sh_hi[w][qi];
       tot_lo[qi] += sh_lo[w][qi];
     }
   }
-  for (int w = 0; w < kThreads / 64; ++w) {
+  for (int w = 0; w < NW; ++w) {
     tot_f[0] += sh_f[w][0];
     tot_f[1] += sh_f[w][1];
   }
@@ -598,6 +378,33 @@ __global__ __launch_bounds__(kThreads) void k_fls_general_fin(int wl, int fl_lo,
     default: { constexpr int K_ = FXPQ_SRC_ADD, D_ = FXPQ_I8; CALL; } break;        \
   }
 
+hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,
+                                 int fl_hi, int mode, const double* d_minmax, int nb,
+                                 fxpq_fmt* out) {
+  FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_fls_window_fin<K_><<<1, kFinThreads, 0, c.stream>>>(
+                        s, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part, c.sc.win_part_f,
+                        nb, plan, out)));
+  return hipGetLastError();
+}
+
+hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
+                              int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
+  FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
+  int nchunks = (int)((n + 65535) / 65536);
+  if (nchunks > kGenChunks) nchunks = kGenChunks;
+  if (nchunks < 1) nchunks = 1;
+  int gblocks = 240;
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (k_fls_general<K_, D_><<<gblocks, kThreads, 0, c.stream>>>(
+                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part, out,
+                        c.sc.flags)));
+  k_fls_general_fin<<<1, kThreads, 0, c.stream>>>(wl, fl_lo, fl_hi, fl_hi + 24, nchunks, s, s.kind,
+                                                  plan, c.sc.gen_part, out, d_sse);
+  return hipGetLastError();
+}
+
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
   // Per-thread exactness of the window pass: |Wh q|, |Wl q| < 2^(26 + bits(Qmax))
@@ -616,21 +423,9 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
                         s, n, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part,
                         c.sc.win_part_f, plan, out, c.sc.flags)));
   timer_end(c, timed, elem_bytes * (double)n);
-  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (k_fls_window_fin<K_><<<1, kThreads, 0, c.stream>>>(
-                        s, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part, c.sc.win_part_f,
-                        blocks, plan, out)));
-  int nchunks = (int)((n + 65535) / 65536);
-  if (nchunks > kGenChunks) nchunks = kGenChunks;
-  if (nchunks < 1) nchunks = 1;
-  int gblocks = 240;
-  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (k_fls_general<K_, D_><<<gblocks, kThreads, 0, c.stream>>>(
-                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part, out,
-                        c.sc.flags)));
-  k_fls_general_fin<<<1, kThreads, 0, c.stream>>>(wl, fl_lo, fl_hi, fl_hi + 24, nchunks, s, s.kind,
-                                                  plan, c.sc.gen_part, out, d_sse);
-  return hipGetLastError();
+  hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, fl_hi, mode, d_minmax, blocks, out);
+  if (e != hipSuccess) return e;
+  return launch_fls_general(c, s, n, wl, fl_lo, fl_hi, d_minmax, out, d_sse);
 }
 
 }  // namespace fxpq

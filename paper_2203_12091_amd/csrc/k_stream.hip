@@ -75,11 +75,14 @@ __global__ __launch_bounds__(kThreads) void k_minmax(SrcDev s, int64_t n, double
 }
 
 // One block: reduces nb (min, max) partials; a NaN partial marks non-finite input.
-__global__ __launch_bounds__(kThreads) void k_minmax_fin(const double* part, int nb, double* out) {
-  __shared__ double sh[8];
+constexpr int kMmFinThreads = 1024;
+
+__global__ __launch_bounds__(kMmFinThreads) void k_minmax_fin(const double* part, int nb, double* out) {
+  __shared__ double sh[kMmFinThreads / 64];
   double a = INFINITY, b = -INFINITY;
   bool nan_seen = false;
-  for (int i = threadIdx.x; i < nb; i += kThreads) {
+#pragma unroll 4
+  for (int i = threadIdx.x; i < nb; i += kMmFinThreads) {
     double p0 = part[2 * i], p1 = part[2 * i + 1];
     nan_seen |= isnan(p0);
     a = fmin(a, p0);
@@ -95,57 +98,13 @@ __global__ __launch_bounds__(kThreads) void k_minmax_fin(const double* part, int
 }
 
 hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* out) {
-  k_minmax_fin<<<1, kThreads, 0, c.stream>>>(part, nb, out);
+  k_minmax_fin<<<1, kMmFinThreads, 0, c.stream>>>(part, nb, out);
   return hipGetLastError();
 }
 
 // ----------------------------------------------------------------------------
 // Quantize / requantize.
 // ----------------------------------------------------------------------------
-struct QFmt {
-  double qmin, qmax, mult;
-  int off;         // 128 when stored as u - 128
-  int lo, hi;      // storage range
-  bool ok;
-};
-
-template <int OUT>
-__device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) {
-  QFmt q;
-  int k = fmt->wl, fl = fmt->fl, sg = fmt->sign;
-  q.ok = (fmt->status == 0 && k >= 2 && k <= 32 && (sg == 0 || sg == 1));
-  if (!q.ok) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_RANGE);
-    return q;
-  }
-  q.qmax = ldexp(1.0, k - sg) - 1.0;
-  q.qmin = sg ? -ldexp(1.0, k - 1) : 0.0;
-  q.mult = ldexp(1.0, fl - sv);
-  q.off = (OUT == FXPQ_U8OFF || (OUT == FXPQ_C8 && sg == 0)) ? 128 : 0;
-  if (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
-    q.lo = -128;
-    q.hi = 127;
-  } else if (OUT == FXPQ_I16) {
-    q.lo = -32768;
-    q.hi = 32767;
-  } else {
-    q.lo = INT32_MIN;
-    q.hi = INT32_MAX;
-  }
-  if (q.qmin - q.off < q.lo || q.qmax - q.off > q.hi) {
-    if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_CODE);
-  }
-  return q;
-}
-
-__device__ inline int quant_one(double v, const QFmt& q) {
-  double r = rint(v * q.mult);  // round half to even
-  r = fmin(fmax(r, q.qmin), q.qmax);
-  double c = r - (double)q.off;
-  c = fmin(fmax(c, (double)q.lo), (double)q.hi);
-  return (int)c;
-}
-
 template <int OUT, int V>
 __device__ inline void storev(void* codes, int64_t i, const int c[V]) {
   if constexpr (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
@@ -403,7 +362,7 @@ hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) 
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(s, n, c.sc.minmax_part,
                                                                         c.sc.flags)));
-  k_minmax_fin<<<1, kThreads, 0, c.stream>>>(c.sc.minmax_part, blocks, out);
+  k_minmax_fin<<<1, kMmFinThreads, 0, c.stream>>>(c.sc.minmax_part, blocks, out);
   return hipGetLastError();
 }
 

@@ -11,6 +11,11 @@ namespace fxpq {
 constexpr double kTwo52 = 4503599627370496.0;  // 2^52
 constexpr double kTwo53 = 9007199254740992.0;  // 2^53
 
+// Sticky device flags (vector atomic OR at device scope).
+__device__ inline void raise_flag(unsigned* flags, unsigned f) {
+  __hip_atomic_fetch_or(flags, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Streaming layout.  A thread handles P packets of 16 bytes per block
 // iteration; packet p of thread t covers elements base + (p*kThreads + t)*EP
 // ... + EP-1, so every packet load of a wave is one contiguous 1 KiB span.
@@ -150,6 +155,51 @@ __device__ inline double load1(const SrcDev& s, int64_t i) {
   }
 }
 
+// ---- quantization to a DFX format (Eq. 1 with round half to even, Eq. 2) ----
+struct QFmt {
+  double qmin, qmax, mult;
+  int off;         // 128 when stored as u - 128
+  int lo, hi;      // storage range
+  bool ok;
+};
+
+template <int OUT>
+__device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) {
+  QFmt q;
+  int k = fmt->wl, fl = fmt->fl, sg = fmt->sign;
+  q.ok = (fmt->status == 0 && k >= 2 && k <= 32 && (sg == 0 || sg == 1));
+  if (!q.ok) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_RANGE);
+    return q;
+  }
+  q.qmax = ldexp(1.0, k - sg) - 1.0;
+  q.qmin = sg ? -ldexp(1.0, k - 1) : 0.0;
+  q.mult = ldexp(1.0, fl - sv);
+  q.off = (OUT == FXPQ_U8OFF || (OUT == FXPQ_C8 && sg == 0)) ? 128 : 0;
+  if (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
+    q.lo = -128;
+    q.hi = 127;
+  } else if (OUT == FXPQ_I16) {
+    q.lo = -32768;
+    q.hi = 32767;
+  } else {
+    q.lo = INT32_MIN;
+    q.hi = INT32_MAX;
+  }
+  if (q.qmin - q.off < q.lo || q.qmax - q.off > q.hi) {
+    if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_CODE);
+  }
+  return q;
+}
+
+__device__ inline int quant_one(double v, const QFmt& q) {
+  double r = rint(v * q.mult);  // round half to even
+  r = fmin(fmax(r, q.qmin), q.qmax);
+  double c = r - (double)q.off;
+  c = fmin(fmax(c, (double)q.lo), (double)q.hi);
+  return (int)c;
+}
+
 // ---- wave / block reductions (wave64) ---------------------------------------
 template <typename T, typename Op>
 __device__ inline T wave_reduce(T v, Op op) {
@@ -184,9 +234,6 @@ struct OpAddL {
   __device__ long long operator()(long long a, long long b) const { return a + b; }
 };
 
-__device__ inline void raise_flag(unsigned* flags, unsigned f) {
-  __hip_atomic_fetch_or(flags, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 
 }  // namespace fxpq

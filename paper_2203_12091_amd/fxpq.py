@@ -21,10 +21,10 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_fl_search", "fxpq_qconv", "fxpq_qgemm",
-    "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
+    "fxpq_cblock", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
 ]
-TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT = range(4)
+TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT, TIMER_CBLOCK_PASS = range(5)
 
 
 class Fmt(C.Structure):
@@ -78,6 +78,7 @@ def lib():
             "fxpq_fl_search": [p, p, i64, i32, i32, i32, i32, p, p],
             "fxpq_qconv": [p, p, p, C.c_int, p, p, p, p, p],
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
+            "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
             "fxpq_weight_colsum": [p, p, i64, i64, p],
             "fxpq_maxpool": [p, p, C.c_int, i32, i32, i32, i32, i32, i32, i32, p],
             "fxpq_avgpool_global": [p, p, C.c_int, p, i32, i32, i32, i64, p],
@@ -180,6 +181,13 @@ def qconv(h, desc, x, x_type, w, w_colsum, ep, acc, d_minmax=None):
 def qgemm(h, M, N, K, A, a_type, B, b_colsum, ep, Cout, d_minmax=None):
     _call("fxpq_qgemm", h.value, M, N, K, ptr(A), a_type, ptr(B), ptr(b_colsum),
           C.byref(ep) if ep is not None else None, ptr(Cout), ptr(d_minmax))
+
+
+def cblock(h, desc, x, x_type, w, w_colsum, ep, wl, sign, fl_lo, fl_hi, d_fmt_out, y, y_type,
+           acc, d_minmax):
+    _call("fxpq_cblock", h.value, C.byref(desc), ptr(x), x_type, ptr(w), ptr(w_colsum),
+          C.byref(ep), wl, sign, fl_lo, fl_hi, ptr(d_fmt_out), ptr(y), y_type, ptr(acc),
+          ptr(d_minmax))
 
 
 def weight_colsum(h, w, k, length, colsum):

@@ -54,6 +54,8 @@ def test_null_handle_and_bad_args_rejected_on_host(fx):
     assert L.fxpq_fl_search(None, C.byref(src), 10, 8, -1, -8, 15, None, None) == fx.ERR_INVALID_ARG
     d = fx.ConvDesc(1, 8, 8, 64, 64, 3, 3, 1, 1)
     assert L.fxpq_qconv(None, C.byref(d), None, fx.I8, None, None, None, None, None) == fx.ERR_INVALID_ARG
+    assert L.fxpq_cblock(None, C.byref(d), None, fx.I8, None, None, None, 8, -1, -8, 15, None, None,
+                         fx.C8, None, None) == fx.ERR_INVALID_ARG
     h = C.c_void_p()
     # no GPU in this container: creating a handle must fail cleanly
     st = L.fxpq_create(C.byref(h), 0)
