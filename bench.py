@@ -134,6 +134,9 @@ def main():
     fx.timer_start(net.h, fx.TIMER_REQUANT)
     net.forward()
     rq_ms, rq_n, rq_bytes = fx.timer_read(net.h)
+    fx.timer_start(net.h, fx.TIMER_CBLOCK_PASS)
+    net.forward()
+    cb_ms, cb_n, cb_ops = fx.timer_read(net.h)
     fx.timer_start(net.h, fx.TIMER_OFF)
 
     ms = elapsed * 1000.0 / args.steps
@@ -168,6 +171,9 @@ def main():
                  "ms_per_forward": round(cv_ms, 3), "launches": cv_n},
         "requant": {"kernel": "k_requant", "achieved": round(rq_bytes / (rq_ms * 1e-3) / 1e9, 1),
                     "unit": "GB/s", "ms_per_forward": round(rq_ms, 3), "launches": rq_n},
+        "fused_cblock": {"kernel": "k_qconv (min/max, FL-window and requant epilogues)",
+                         "passes": cb_n, "ms_per_forward": round(cb_ms, 3),
+                         "executed_tops": round(cb_ops / max(cb_ms, 1e-9) * 1e-9, 1)},
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_sample_batch)

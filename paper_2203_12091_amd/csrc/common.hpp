@@ -12,6 +12,10 @@ constexpr int kThreads = 256;        // threads per block of the streaming kerne
 constexpr int kMaxStreamBlocks = 2048;
 constexpr int kMaxConvBlocks = 1 << 20;
 constexpr int kWindow = 2;           // candidates of the first FL-search pass
+constexpr int kWinPart = 6 * kWindow;  // int64 per block of window-pass partials
+// Values per thread of the streaming window pass (the grid grows beyond that):
+// sums of W * q stay exact for max|W * q| < 2^53 / 512.
+constexpr int64_t kWinMaxPerThread = 512;
 constexpr int kMaxCand = 160;        // fl_hi - fl_lo + 1 upper bound (|fl| <= 64 plus slack)
 constexpr int kGenChunks = 256;      // element chunks of the exact general search
 
@@ -23,6 +27,7 @@ struct Scratch {
   long long* win_part;      // window FL-search partials
   double* win_part_f;       // window FL-search fp64 partials
   unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
+  unsigned* gen_done;       // blocks of the general pass finished (0 between searches)
   void* plan;               // FlsPlan
 };
 
@@ -142,8 +147,8 @@ hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_f
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
 hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,
-                                 int fl_hi, int mode, const double* d_minmax, int nb,
-                                 fxpq_fmt* out);
+                                 int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
+                                 int nb, fxpq_fmt* out);
 hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
                               int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,

@@ -19,8 +19,6 @@ struct FlsPlan {
 
 enum FlsMode { MODE_SEARCH = 0, MODE_REPORT = 1 };
 
-constexpr double kTwoM26 = 1.0 / 67108864.0;  // 2^-26
-constexpr double kTwo26 = 67108864.0;
 
 // ---------------------------------------------------------------------------
 // Small signed 512-bit integer (two's complement), used by one thread.
@@ -38,13 +36,22 @@ __device__ inline Big big_from_i128(__int128 v) {
   return b;
 }
 
+// a * 2^s for 0 <= s < 512 (static indexing only: whole words first, then bits).
 __device__ inline Big big_shl(const Big& a, int s) {
-  Big r;
-  int ws = s / 64, bs = s % 64;
-  for (int i = 7; i >= 0; --i) {
-    unsigned long long hi = (i - ws >= 0) ? a.w[i - ws] : 0ull;
-    unsigned long long lo = (i - ws - 1 >= 0) ? a.w[i - ws - 1] : 0ull;
-    r.w[i] = bs ? (hi << bs) | (lo >> (64 - bs)) : hi;
+  Big r = a;
+  const int ws = s >> 6, bs = s & 63;
+#pragma unroll
+  for (int step = 0; step < 8; ++step) {
+    if (step < ws) {
+#pragma unroll
+      for (int i = 7; i > 0; --i) r.w[i] = r.w[i - 1];
+      r.w[0] = 0ull;
+    }
+  }
+  if (bs) {
+#pragma unroll
+    for (int i = 7; i > 0; --i) r.w[i] = (r.w[i] << bs) | (r.w[i - 1] >> (64 - bs));
+    r.w[0] <<= bs;
   }
   return r;
 }
@@ -132,15 +139,25 @@ struct WinSetup {
   int b0, b1, nc, bce;
 };
 
+// Decisions every block of a window pass (and its finalize) takes from the
+// min / max alone.  One thread adds at most `per_thread` values.  For integer
+// sources its sums of W * q stay exact integers below 2^53 when max|W| *
+// max|q| * per_thread < 2^53, and a tensor beyond that bound goes to the exact
+// general pass.  fp32 values (W up to 2^52) always use the split form
+// W = Wh * 2^26 + Wl, exact while 2^26 * max|q| * per_thread < 2^53, which
+// the launcher's bound on per_thread guarantees.
 template <int KIND>
 __device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, int sign_req,
-                                     int fl_lo, int fl_hi, int mode) {
+                                     int fl_lo, int fl_hi, int mode, int64_t per_thread) {
   WinSetup w;
   w.u = fls_uniform<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi);
+  const double wmax = w.u.absmax * w.u.wscale;
+  const double qabs = fmax(w.u.qmax, -w.u.qmin);
   w.verdict = 0;
   if (!w.u.ok) w.verdict = 3;
-  else if (mode == MODE_REPORT || wl > 16 || w.u.absmax * w.u.wscale >= kTwo52) w.verdict = 2;
+  else if (mode == MODE_REPORT || wl > 16 || wmax >= kTwo52) w.verdict = 2;
   else if (w.u.beta_nosat >= fl_hi) w.verdict = 1;
+  else if (KIND != FXPQ_SRC_F32 && wmax * qabs * (double)per_thread >= kTwo53) w.verdict = 2;
   w.b0 = imax(fl_lo, w.u.beta_nosat);
   w.b1 = (w.b0 + kWindow - 1 < fl_hi) ? w.b0 + kWindow - 1 : fl_hi;
   w.nc = w.b1 - w.b0 + 1;
@@ -149,11 +166,23 @@ __device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, 
 }
 
 
-// Per-thread accumulators of the window pass.
+// Per-thread accumulators of the window pass: per candidate the exact
+// integers sum q^2 and sum W q (as sum Wh q and sum Wl q in the split form;
+// all below 2^53, see win_setup), plus the two fp64 bound sums.
 struct WinAcc {
   double A[kWindow], PH[kWindow], PL[kWindow];
   double V2, CE;
 };
+
+constexpr double kTwoM26 = 1.0 / 67108864.0;  // 2^-26
+constexpr double kTwo26 = 67108864.0;
+
+// Exact int64 of an integer-valued double below 2^53 in magnitude.
+__device__ inline long long exact_i64(double x) {
+  const double hi = floor(x * 0x1p-32);
+  const double lo = fma(hi, -0x1p32, x);  // in [0, 2^32)
+  return (long long)(((unsigned long long)(unsigned)(int)hi << 32) | (unsigned)lo);
+}
 
 // Uniform constants of the window pass: candidate and clipping-bound scales.
 struct WinCtx {
@@ -178,9 +207,9 @@ __device__ inline void win_acc_zero(WinAcc& acc) {
   acc.V2 = acc.CE = 0.0;
 }
 
-// Adds one integer value W = v * 2^sigma.  Specialized on what the min/max
-// already tell:
-//   SPLIT    W * q sums need the Wh / Wl split to stay exact per thread;
+// Adds one integer value W = v * 2^sigma.  Specialized on
+//   SPLIT    W * q summed as Wh * q and Wl * q (fp32 sources);
+// and on what the min/max already tell:
 //   NONNEG   every value is >= 0: no lower clamp, no lower clipping term;
 //   CLAMP0   the first candidate can saturate (it is not beta_nosat).
 template <bool SPLIT, bool NONNEG, bool CLAMP0>
@@ -202,26 +231,20 @@ __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
     if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
     acc.PL[j] = fma(Wl, q, acc.PL[j]);
   }
-  double t = W * c.cce;
-  double d1 = fmax(t - c.qmax, 0.0);
+  const double t = W * c.cce;
+  const double d1 = fmax(t - c.qmax, 0.0);
   acc.CE = fma(d1, d1, acc.CE);
   if (!NONNEG) {
-    double d2 = fmin(t - c.qmin, 0.0);
+    const double d2 = fmin(t - c.qmin, 0.0);
     acc.CE = fma(d2, d2, acc.CE);
   }
 }
 
-// Variant index (SPLIT << 2 | NONNEG << 1 | CLAMP0) for a pass in which one
-// thread adds at most `per_thread` values.  Per-thread partial sums of W * q
-// stay exact below 2^53 without the split when
-// max|W| * max|q| * per_thread < 2^53.
-__device__ inline int win_variant(const FlsU& u, const WinSetup& ws, const double* mm,
-                                  int64_t per_thread) {
-  const double qabs = fmax(u.qmax, -u.qmin);
-  const bool split = u.absmax * u.wscale * qabs * (double)per_thread >= kTwo53;
+// Variant index (NONNEG << 1 | CLAMP0).
+__device__ inline int win_variant(const FlsU& u, const WinSetup& ws, const double* mm) {
   const bool nonneg = mm[0] >= 0.0;
   const bool clamp0 = ws.b0 != u.beta_nosat;
-  return (split ? 4 : 0) | (nonneg ? 2 : 0) | (clamp0 ? 1 : 0);
+  return (nonneg ? 2 : 0) | (clamp0 ? 1 : 0);
 }
 
 // Records a decision taken before the data is read (verdict != 0): done at
@@ -245,21 +268,24 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
   }
 }
 
-// Block partials of the window pass: the exact integer sums as int64 (each
-// per-thread sum is an exact integer below 2^53, the block sum below 2^61),
-// the two bound sums as fp64.  Slot `bid` of part_i (3 * kWindow) / part_f (2).
+// Block partials of the window pass.  Each exact per-thread sum (below 2^53)
+// is split into its high and low 32-bit halves, summed separately over the
+// block: slot `bid` of part_i holds kWinPart int64 (per candidate: A hi/lo,
+// PH hi/lo, PL hi/lo), part_f the two bound sums.
 __device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long long* part_i,
                                           double* part_f, long long* shl, double* shd) {
-  long long* pi = part_i + bid * (3 * kWindow);
+  long long* pi = part_i + bid * kWinPart;
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
-    long long a = block_reduce((long long)acc.A[j], OpAddL(), shl);
-    long long ph = block_reduce((long long)acc.PH[j], OpAddL(), shl);
-    long long pl = block_reduce((long long)acc.PL[j], OpAddL(), shl);
-    if (threadIdx.x == 0) {
-      pi[3 * j] = a;
-      pi[3 * j + 1] = ph;
-      pi[3 * j + 2] = pl;
+    const long long q3[3] = {exact_i64(acc.A[j]), exact_i64(acc.PH[j]), exact_i64(acc.PL[j])};
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+      const long long h = block_reduce(q3[k] >> 32, OpAddL(), shl);
+      const long long l = block_reduce(q3[k] & 0xFFFFFFFFll, OpAddL(), shl);
+      if (threadIdx.x == 0) {
+        pi[6 * j + 2 * k] = h;
+        pi[6 * j + 2 * k + 1] = l;
+      }
     }
   }
   double v2 = block_reduce(acc.V2, OpAddD(), shd);
@@ -271,6 +297,6 @@ __device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long l
 }
 
 // Launch helpers shared by the streaming search and the fused C-Block.
-constexpr int kFinThreads = 1024;
+constexpr int kFinThreads = 512;
 
 }  // namespace fxpq

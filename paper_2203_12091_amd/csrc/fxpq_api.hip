@@ -154,8 +154,9 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   };
   size_t o_flags = take(4);
   size_t o_mm = take(2 * sizeof(double));
+  size_t o_gd = take(4);
   size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
-  size_t o_wp = take((size_t)kMaxFlsBlocks * 3 * kWindow * sizeof(long long));
+  size_t o_wp = take((size_t)kMaxFlsBlocks * kWinPart * sizeof(long long));
   size_t o_wpf = take((size_t)kMaxFlsBlocks * 2 * sizeof(double));
   size_t o_gp = take((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
   size_t o_plan = take(256);
@@ -171,6 +172,7 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   h->sc.win_part = reinterpret_cast<long long*>(base + o_wp);
   h->sc.win_part_f = reinterpret_cast<double*>(base + o_wpf);
   h->sc.gen_part = reinterpret_cast<unsigned long long*>(base + o_gp);
+  h->sc.gen_done = reinterpret_cast<unsigned*>(base + o_gd);
   h->sc.plan = base + o_plan;
   if (hipMemset(h->scratch, 0, o_mmp) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(h->scratch);
@@ -252,9 +254,7 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
   SrcDev s;
   fxpq_status st = to_dev(src, n, &s);
   if (st) return st;
-  int qbits = wl <= 16 ? wl : 16;
-  int64_t per_thread = (int64_t)1 << (53 - 26 - qbits - 1);
-  if (n / ((int64_t)kThreads * per_thread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  if (n / ((int64_t)kThreads * kWinMaxPerThread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
   DeviceGuard g(h->device);
   Ctx c = ctx(h);
   const double* mm = src->d_minmax;

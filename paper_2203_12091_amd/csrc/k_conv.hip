@@ -93,7 +93,8 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
   if constexpr (EPI == EPI_ACC) {
     if (a.only_if_general && (!a.plan_in->need_general || a.plan_in->status)) return;
   } else if constexpr (EPI == EPI_WIN) {
-    ws = win_setup<FXPQ_SRC_ACC>(a.ep, a.mm, a.wl, a.sign_req, a.fl_lo, a.fl_hi, MODE_SEARCH);
+    ws = win_setup<FXPQ_SRC_ACC>(a.ep, a.mm, a.wl, a.sign_req, a.fl_lo, a.fl_hi, MODE_SEARCH,
+                                 kConvPerThread);
     if (ws.verdict != 0) {
       if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
         win_verdict_write(ws, a.wl, a.fl_lo, a.fl_hi, a.plan, a.fmt_win, a.flags);
@@ -269,7 +270,7 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
       }
     }
   };
-  const int relu = a.ep.ep_relu;
+  const double relo = a.ep.ep_relu ? 0.0 : -INFINITY;  // ReLU as max(v, relo)
   const int bid = blockIdx.y * gridDim.x + blockIdx.x;
 
   if constexpr (EPI == EPI_ACC || EPI == EPI_MM) {
@@ -277,8 +278,7 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
     visit([&](int v, double Mc, double Ac, int row, int col) {
       if (EPI == EPI_ACC) a.acc[(int64_t)row * a.K + col] = v;
       if (want_vals) {
-        double val = fma((double)v, Mc, Ac);
-        if (relu) val = fmax(val, 0.0);
+        const double val = fmax(fma((double)v, Mc, Ac), relo);
         mn = fmin(mn, val);
         mx = fmax(mx, val);
       }
@@ -297,28 +297,22 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
     win_acc_zero(wa);
     // W = v * 2^(sigma - sv): fold the integer scaling into the constants.
     const double wsc = u.wscale;
-#define FXPQ_WIN_VISIT(SP, NN, C0)                                          \
+#define FXPQ_WIN_VISIT(NN, C0)                                              \
   visit([&](int v, double Mc, double Ac, int, int) {                        \
-    double W = fma((double)v, Mc * wsc, Ac * wsc);                          \
-    if (relu) W = fmax(W, 0.0);                                             \
-    win_consume<SP, NN, C0>(wc, wa, W);                                     \
+    const double W = fmax(fma((double)v, Mc * wsc, Ac * wsc), relo);       \
+    win_consume<false, NN, C0>(wc, wa, W);                                  \
   })
-    switch (win_variant(u, ws, a.mm, kConvPerThread)) {
-      case 0: FXPQ_WIN_VISIT(false, false, false); break;
-      case 1: FXPQ_WIN_VISIT(false, false, true); break;
-      case 2: FXPQ_WIN_VISIT(false, true, false); break;
-      case 3: FXPQ_WIN_VISIT(false, true, true); break;
-      case 4: FXPQ_WIN_VISIT(true, false, false); break;
-      case 5: FXPQ_WIN_VISIT(true, false, true); break;
-      case 6: FXPQ_WIN_VISIT(true, true, false); break;
-      default: FXPQ_WIN_VISIT(true, true, true); break;
+    switch (win_variant(u, ws, a.mm)) {
+      case 0: FXPQ_WIN_VISIT(false, false); break;
+      case 1: FXPQ_WIN_VISIT(false, true); break;
+      case 2: FXPQ_WIN_VISIT(true, false); break;
+      default: FXPQ_WIN_VISIT(true, true); break;
     }
 #undef FXPQ_WIN_VISIT
     win_write_partials(wa, bid, a.part_i, a.part_f, shl, shd);
   } else {  // EPI_REQ
     visit([&](int v, double Mc, double Ac, int row, int col) {
-      double val = fma((double)v, Mc, Ac);
-      if (relu) val = fmax(val, 0.0);
+      const double val = fmax(fma((double)v, Mc, Ac), relo);
       a.y[(int64_t)row * a.K + col] = (int8_t)quant_one(val, qf);
     });
   }
@@ -427,7 +421,8 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
   conv_run<EPI_WIN>(a, loader, wide, grid, c.stream);
   timer_end(c, timed, ops);
-  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, fl_hi, MODE_SEARCH, d_minmax, nb, out);
+  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, fl_hi, MODE_SEARCH, kConvPerThread, d_minmax,
+                            nb, out);
   if (e != hipSuccess) return e;
   // 3. only when the plan asks for the general pass: int32 accumulators, then
   //    the exact search over every remaining candidate

@@ -29,47 +29,37 @@ namespace fxpq {
 int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec);
 
 // Main loop of the streaming window pass over this thread's values.
-template <int KIND, int DT, bool SPLIT, bool NONNEG, bool CLAMP0>
+template <int KIND, int DT, bool NONNEG, bool CLAMP0>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
                                 WinAcc& acc) {
   const WinCtx wc = win_ctx(u, ws);
   win_acc_zero(acc);
-  auto consume = [&](double W) { win_consume<SPLIT, NONNEG, CLAMP0>(wc, acc, W); };
+  auto consume = [&](double W) { win_consume<KIND == FXPQ_SRC_F32, NONNEG, CLAMP0>(wc, acc, W); };
 
   using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   ThreadVals<PK::V> tv;
   thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, tv);
-  // Fold the integer scaling W = v * 2^(sigma - sv) into the loader constants.
-  if constexpr (KIND == FXPQ_SRC_ACC) {
-#pragma unroll
-    for (int j = 0; j < PK::V; ++j) {
-      tv.M[j] *= u.wscale;
-      tv.A[j] *= u.wscale;
-    }
-  } else if constexpr (KIND == FXPQ_SRC_ADD) {
-    tv.ca *= u.wscale;
-    tv.cb *= u.wscale;
-  }
+  // Integer sources are searched at sigma = sv (W = v); fp32 values are
+  // scaled by 2^(sigma - sv) = 2^(fl_hi + 24), exactly.
+  const double post = u.wscale;
   const int64_t nfull = n - n % PK::EP;
-  if constexpr (KIND == FXPQ_SRC_ACC || KIND == FXPQ_SRC_ADD) {
-    stream_values<KIND, DT>(s, n, tv, [&](double v, int64_t) { consume(v); });
-  } else {
-    const double post = u.wscale;
-    stream_values<KIND, DT>(s, n, tv, [&](double v, int64_t) { consume(v * post); });
-  }
+  stream_packets<KIND, DT>(s, n, tv, [&](const double* v, int64_t) {
+#pragma unroll
+    for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j]);
+  });
   if (gtid == 0)
     for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i) * u.wscale);
 }
 
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_fls_window(
-    SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode,
+    SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
     const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out,
     unsigned* flags) {
   __shared__ long long shl[8];
   __shared__ double shd[8];
-  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode);
+  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
   const FlsU& u = ws.u;
 
   // Decisions every block takes identically before touching the data.
@@ -77,19 +67,12 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     if (blockIdx.x == 0 && threadIdx.x == 0) win_verdict_write(ws, wl, fl_lo, fl_hi, plan, out, flags);
     return;
   }
-  constexpr int V = Pack<KIND, DT>::V;
-  const int64_t per_thread = ((n / V + (int64_t)gridDim.x * kThreads - 1) /
-                              ((int64_t)gridDim.x * kThreads)) * V + V;
   WinAcc acc;
-  switch (win_variant(u, ws, mm, per_thread)) {
-    case 0: win_loop<KIND, DT, false, false, false>(s, n, u, ws, acc); break;
-    case 1: win_loop<KIND, DT, false, false, true>(s, n, u, ws, acc); break;
-    case 2: win_loop<KIND, DT, false, true, false>(s, n, u, ws, acc); break;
-    case 3: win_loop<KIND, DT, false, true, true>(s, n, u, ws, acc); break;
-    case 4: win_loop<KIND, DT, true, false, false>(s, n, u, ws, acc); break;
-    case 5: win_loop<KIND, DT, true, false, true>(s, n, u, ws, acc); break;
-    case 6: win_loop<KIND, DT, true, true, false>(s, n, u, ws, acc); break;
-    default: win_loop<KIND, DT, true, true, true>(s, n, u, ws, acc); break;
+  switch (win_variant(u, ws, mm)) {
+    case 0: win_loop<KIND, DT, false, false>(s, n, u, ws, acc); break;
+    case 1: win_loop<KIND, DT, false, true>(s, n, u, ws, acc); break;
+    case 2: win_loop<KIND, DT, true, false>(s, n, u, ws, acc); break;
+    default: win_loop<KIND, DT, true, true>(s, n, u, ws, acc); break;
   }
   win_write_partials(acc, blockIdx.x, part_i, part_f, shl, shd);
 }
@@ -99,33 +82,34 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
 
 template <int KIND>
 __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
-    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, const double* mm,
-    const long long* part_i, const double* part_f, int nb, FlsPlan* plan, fxpq_fmt* out) {
+    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
+    const double* mm, const long long* part_i, const double* part_f, int nb, FlsPlan* plan,
+    fxpq_fmt* out) {
   constexpr int NQ = 3 * kWindow;
   constexpr int NW = kFinThreads / 64;
   __shared__ long long sh_hi[NW][NQ], sh_lo[NW][NQ];
   __shared__ double sh_f[NW][2];
-  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode);
+  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
   if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
   const FlsU& u = ws.u;
   const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc, bce = ws.bce;
-  // One pass over the block partials.  Each is below 2^61 in magnitude; split
-  // into 32-bit halves so the int64 sums cannot overflow.
+  // One pass over the block partials: the high and low 32-bit halves of each
+  // quantity are summed separately (both sums stay far below 2^63).
   long long hi[NQ], lo[NQ];
   double f0 = 0.0, f1 = 0.0;
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) hi[qi] = lo[qi] = 0;
 #pragma unroll 2
   for (int b = threadIdx.x; b < nb; b += kFinThreads) {
-    const long long* p = part_i + (int64_t)b * NQ;
-    long long x[NQ];
+    const long long* p = part_i + (int64_t)b * kWinPart;
+    long long x[2 * NQ];
 #pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) x[qi] = p[qi];
+    for (int k = 0; k < 2 * NQ; ++k) x[k] = p[k];
     const double g0 = part_f[2 * b], g1 = part_f[2 * b + 1];
 #pragma unroll
     for (int qi = 0; qi < NQ; ++qi) {
-      hi[qi] += x[qi] >> 32;
-      lo[qi] += x[qi] & 0xFFFFFFFFll;
+      hi[qi] += x[2 * qi];
+      lo[qi] += x[2 * qi + 1];
     }
     f0 += g0;
     f1 += g1;
@@ -173,7 +157,9 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   if (dmin + 1 + off < 0) off = -(dmin + 1);
   Big best;
   int bj = -1;
-  for (int j = 0; j < nc; ++j) {
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) {
+    if (j >= nc) break;
     int d = u.sigma - (b0 + j);
     __int128 Aj = total(3 * j);
     __int128 Pj = total(3 * j + 1) * (__int128)67108864 + total(3 * j + 2);
@@ -239,11 +225,21 @@ __device__ inline double u192_to_double(const U192& a) {
          (double)(unsigned long long)a.lo;
 }
 
+__device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int sigma,
+                               const FlsPlan* plan, const unsigned long long* part, fxpq_fmt* out,
+                               double* d_sse);
+
+// Exact errors of the remaining candidates over (candidate, chunk) items; the
+// last block to finish sums the chunk partials and decides.  Nothing runs
+// unless the window pass asked for it (and only then is the device-scope
+// release / acquire paid).
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_fls_general(
     SrcDev s, int64_t n, int wl, int fl_lo, int fl_hi, int nchunks, const double* mm,
-    const FlsPlan* plan, unsigned long long* part, fxpq_fmt* out, unsigned* flags) {
+    const FlsPlan* plan, unsigned long long* part, unsigned* done, fxpq_fmt* out, double* d_sse,
+    unsigned* flags) {
   __shared__ unsigned long long shp[kThreads * 3];
+  __shared__ int last;
   if (!plan->need_general || plan->status) return;
   const int sign = plan->sign;
   const int glo = plan->gen_lo, ghi = plan->gen_hi, extra = plan->gen_extra;
@@ -318,17 +314,21 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
     }
     __syncthreads();
   }
-
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) last = atomicAdd(done, 1u) == gridDim.x - 1;
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  general_decide(wl, fl_lo, fl_hi, nchunks, sigma, plan, part, out, d_sse);
+  if (threadIdx.x == 0) *done = 0u;  // ready for the next search
 }
 
 // One block: totals per candidate, exact comparison, ties to the larger fl.
-__global__ __launch_bounds__(kThreads) void k_fls_general_fin(int wl, int fl_lo, int fl_hi, int sigma_f32,
-                                                              int nchunks, const SrcDev s, int kind,
-                                                              const FlsPlan* plan,
-                                                              const unsigned long long* part,
-                                                              fxpq_fmt* out, double* d_sse) {
+__device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int sigma,
+                               const FlsPlan* plan, const unsigned long long* part, fxpq_fmt* out,
+                               double* d_sse) {
   __shared__ unsigned long long tot[kMaxCand][3];
-  if (!plan->need_general || plan->status) return;
   const int sign = plan->sign;
   const int glo = plan->gen_lo, ghi = plan->gen_hi, extra = plan->gen_extra;
   const int nc = ghi - glo + 1 + (extra != INT_MIN ? 1 : 0);
@@ -346,8 +346,6 @@ __global__ __launch_bounds__(kThreads) void k_fls_general_fin(int wl, int fl_lo,
   }
   __syncthreads();
   if (threadIdx.x != 0) return;
-  const int sv = (kind == FXPQ_SRC_F32) ? 0 : src_scale(s);
-  const int sigma = (kind == FXPQ_SRC_F32) ? sigma_f32 : imax(sv, fl_hi);
   U192 best{0, 0};
   int bbeta = INT_MIN;
   for (int j = 0; j < nc; ++j) {
@@ -379,13 +377,13 @@ __global__ __launch_bounds__(kThreads) void k_fls_general_fin(int wl, int fl_lo,
   }
 
 hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,
-                                 int fl_hi, int mode, const double* d_minmax, int nb,
-                                 fxpq_fmt* out) {
+                                 int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
+                                 int nb, fxpq_fmt* out) {
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window_fin<K_><<<1, kFinThreads, 0, c.stream>>>(
-                        s, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part, c.sc.win_part_f,
-                        nb, plan, out)));
+                        s, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
+                        c.sc.win_part_f, nb, plan, out)));
   return hipGetLastError();
 }
 
@@ -398,32 +396,34 @@ hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
   int gblocks = 240;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_general<K_, D_><<<gblocks, kThreads, 0, c.stream>>>(
-                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part, out,
-                        c.sc.flags)));
-  k_fls_general_fin<<<1, kThreads, 0, c.stream>>>(wl, fl_lo, fl_hi, fl_hi + 24, nchunks, s, s.kind,
-                                                  plan, c.sc.gen_part, out, d_sse);
+                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part,
+                        c.sc.gen_done, out, d_sse, c.sc.flags)));
   return hipGetLastError();
+}
+
+// Values per thread of the streaming window pass for a grid of `blocks`.
+static int64_t window_per_thread(int64_t n, int blocks, int vec) {
+  const int64_t threads = (int64_t)blocks * kThreads;
+  return ((n / vec + threads - 1) / threads) * vec + vec;
 }
 
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
-  // Per-thread exactness of the window pass: |Wh q|, |Wl q| < 2^(26 + bits(Qmax))
-  // summed over at most `per_thread` values must stay below 2^53.
-  int qbits = (wl <= 16) ? wl : 16;
-  int64_t per_thread = (int64_t)1 << (53 - 26 - qbits - 1);
   int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
   const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;  // Pack<>::V
-  int blocks = stream_grid(n, channels, per_thread, vec);
+  const int blocks = stream_grid(n, channels, kWinMaxPerThread, vec);
+  const int64_t per_thread = window_per_thread(n, blocks, vec);
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   int mode = d_sse ? MODE_REPORT : MODE_SEARCH;
   const double elem_bytes = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
   bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
-                        s, n, wl, sign, fl_lo, fl_hi, mode, d_minmax, c.sc.win_part,
+                        s, n, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
                         c.sc.win_part_f, plan, out, c.sc.flags)));
   timer_end(c, timed, elem_bytes * (double)n);
-  hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, fl_hi, mode, d_minmax, blocks, out);
+  hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax,
+                                       blocks, out);
   if (e != hipSuccess) return e;
   return launch_fls_general(c, s, n, wl, fl_lo, fl_hi, d_minmax, out, d_sse);
 }

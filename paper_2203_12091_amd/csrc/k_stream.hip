@@ -160,29 +160,15 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
   if (!q.ok) return;
   using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  const int64_t chunk = (int64_t)kThreads * PK::V;
-  const int64_t stride = (int64_t)gridDim.x * chunk;
   ThreadVals<PK::V> t;
-  thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * chunk, t);
+  thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, t);
   const int64_t nfull = n - n % PK::EP;
-  for (int64_t base = (int64_t)blockIdx.x * chunk; base < nfull; base += stride) {
-    double v[PK::P][PK::EP];
-    bool ok[PK::P];
+  stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0) {
+    int c[PK::EP];
 #pragma unroll
-    for (int p = 0; p < PK::P; ++p) {
-      int64_t i = pk_index<PK::EP>(base, p);
-      ok[p] = i < nfull;
-      if (ok[p]) load_packet<KIND, DT>(s, t, p, i, v[p]);
-    }
-#pragma unroll
-    for (int p = 0; p < PK::P; ++p) {
-      if (!ok[p]) continue;
-      int c[PK::EP];
-#pragma unroll
-      for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[p][j], q);
-      storev<OUT, PK::EP>(codes, pk_index<PK::EP>(base, p), c);
-    }
-  }
+    for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[j], q);
+    storev<OUT, PK::EP>(codes, i0, c);
+  });
   if (gtid == 0) {
     for (int64_t i = nfull; i < n; ++i) store1<OUT>(codes, i, quant_one(load1<KIND, DT>(s, i), q));
   }

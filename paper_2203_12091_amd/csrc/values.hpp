@@ -31,9 +31,9 @@ struct Pack {
 template <int V>
 struct ThreadVals {
   double M[V], A[V];  // ACC: per-channel multiplier / addend, indexed p * EP + j
-  double ca, cb;      // ADD: alignment factors
-  double oa, ob;      // ADD: +128 for offset-stored unsigned codes
-  int relu;
+  int sa, sb;         // ADD: value = (a << sa) + (b << sb) + k, one shift is 0
+  double k;           // ADD: the +128 of offset-stored unsigned codes, aligned
+  double relo;        // ReLU as max(v, relo): 0, or -inf without ReLU
 };
 
 // Element index of packet p, value 0, for this thread at block base `base`.
@@ -55,80 +55,128 @@ __device__ inline void thread_vals_init(const SrcDev& s, int64_t base0,
       for (int j = 0; j < PK::EP; ++j)
         epi_channel(s, u, (c0 + j) % s.channels, t.M[p * PK::EP + j], t.A[p * PK::EP + j]);
     }
-    t.relu = s.ep_relu;
+    t.relo = s.ep_relu ? 0.0 : -INFINITY;
   } else if constexpr (KIND == FXPQ_SRC_ADD) {
     int F = imax(s.fa->fl, s.fb->fl);
-    t.ca = ldexp(1.0, F - s.fa->fl);
-    t.cb = ldexp(1.0, F - s.fb->fl);
-    t.oa = code_is_off(s.dtype, s.fa) ? 128.0 : 0.0;
-    t.ob = code_is_off(s.dtype2, s.fb) ? 128.0 : 0.0;
-    t.relu = s.relu;
+    t.sa = F - s.fa->fl;
+    t.sb = F - s.fb->fl;
+    t.k = (code_is_off(s.dtype, s.fa) ? ldexp(128.0, t.sa) : 0.0) +
+          (code_is_off(s.dtype2, s.fb) ? ldexp(128.0, t.sb) : 0.0);
+    t.relo = s.relu ? 0.0 : -INFINITY;
   }
 }
 
-// Loads packet p (EP values starting at element i, all in range) as exact doubles.
+// Exactness of the integer combination of an eltwise source: |code| <= 255,
+// so (a << sa) + (b << sb) stays inside int32 for shifts up to 22; larger
+// alignments fall back to fp64 arithmetic.
+constexpr int kAddMaxShift = 22;
+
+// Raw 16-byte packet(s) of one group of EP values, as loaded.
 template <int KIND, int DT>
-__device__ inline void load_packet(const SrcDev& s, const ThreadVals<Pack<KIND, DT>::V>& t, int p,
-                                   int64_t i, double* v) {
+struct Raw {
+  int4 a;
+  int4 b;  // second operand of an eltwise source
+};
+
+template <int KIND, int DT>
+__device__ inline Raw<KIND, DT> load_raw(const SrcDev& s, int64_t i) {
+  Raw<KIND, DT> r;
+  if constexpr (KIND == FXPQ_SRC_ADD) {
+    r.a = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x) + i);
+    r.b = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x2) + i);
+  } else if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) {
+    r.a = *reinterpret_cast<const int4*>(static_cast<const int64_t*>(s.x) + i);
+  } else {
+    r.a = *reinterpret_cast<const int4*>(static_cast<const int32_t*>(s.x) + i);
+  }
+  return r;
+}
+
+// Exact doubles of packet p from its raw bytes.
+template <int KIND, int DT>
+__device__ inline void unpack(const Raw<KIND, DT>& r, const ThreadVals<Pack<KIND, DT>::V>& t,
+                              int p, double* v) {
   constexpr int EP = Pack<KIND, DT>::EP;
   if constexpr (KIND == FXPQ_SRC_F32) {
-    float4 f = *reinterpret_cast<const float4*>(static_cast<const float*>(s.x) + i);
-    v[0] = f.x; v[1] = f.y; v[2] = f.z; v[3] = f.w;
+    v[0] = __int_as_float(r.a.x); v[1] = __int_as_float(r.a.y);
+    v[2] = __int_as_float(r.a.z); v[3] = __int_as_float(r.a.w);
   } else if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I32) {
-    int4 a = *reinterpret_cast<const int4*>(static_cast<const int32_t*>(s.x) + i);
-    v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+    v[0] = r.a.x; v[1] = r.a.y; v[2] = r.a.z; v[3] = r.a.w;
   } else if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) {
-    longlong2 a = *reinterpret_cast<const longlong2*>(static_cast<const int64_t*>(s.x) + i);
-    v[0] = (double)a.x; v[1] = (double)a.y;
+    v[0] = (double)(((long long)(unsigned)r.a.y << 32) | (unsigned)r.a.x);
+    v[1] = (double)(((long long)(unsigned)r.a.w << 32) | (unsigned)r.a.z);
   } else if constexpr (KIND == FXPQ_SRC_ACC) {
-    int4 a = *reinterpret_cast<const int4*>(static_cast<const int32_t*>(s.x) + i);
-    int raw[4] = {a.x, a.y, a.z, a.w};
+    const int raw[4] = {r.a.x, r.a.y, r.a.z, r.a.w};
 #pragma unroll
-    for (int j = 0; j < EP; ++j) {
-      double r = fma((double)raw[j], t.M[p * EP + j], t.A[p * EP + j]);
-      v[j] = t.relu ? fmax(r, 0.0) : r;
-    }
+    for (int j = 0; j < EP; ++j) v[j] = fmax(fma((double)raw[j], t.M[p * EP + j], t.A[p * EP + j]), t.relo);
   } else if constexpr (KIND == FXPQ_SRC_ADD) {
-    union U16 {
-      int4 w;
-      int8_t b[16];
-    } a, b;
-    a.w = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x) + i);
-    b.w = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x2) + i);
+    const int wa[4] = {r.a.x, r.a.y, r.a.z, r.a.w};
+    const int wb[4] = {r.b.x, r.b.y, r.b.z, r.b.w};
 #pragma unroll
     for (int j = 0; j < EP; ++j) {
-      double r = fma((double)a.b[j] + t.oa, t.ca, ((double)b.b[j] + t.ob) * t.cb);
-      v[j] = t.relu ? fmax(r, 0.0) : r;
+      const int ca = (wa[j / 4] << (24 - 8 * (j % 4))) >> 24;  // sign-extended byte
+      const int cb = (wb[j / 4] << (24 - 8 * (j % 4))) >> 24;
+      double x;
+      if (t.sa <= kAddMaxShift && t.sb <= kAddMaxShift)
+        x = (double)((ca << t.sa) + (cb << t.sb));
+      else
+        x = fma((double)ca, ldexp(1.0, t.sa), (double)cb * ldexp(1.0, t.sb));
+      v[j] = fmax(x + t.k, t.relo);
     }
   }
 }
 
-// Drives a streaming kernel: calls f(value) for every value of this thread's
-// packets over the grid-stride loop (all packets' loads issued first), then the
-// values past the last whole packet in thread 0 of block 0.
+// Drives a streaming kernel over this thread's packets of the grid-stride
+// loop: fp(values, index of the first) for every whole packet, the next
+// iteration's loads issued before this one's values are consumed.  Values
+// past the last whole packet are left to the caller.
 template <int KIND, int DT, typename F>
-__device__ inline void stream_values(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
-                                     F&& f) {
+__device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
+                                      F&& fp) {
   using PK = Pack<KIND, DT>;
   const int64_t chunk = (int64_t)kThreads * PK::V;
   const int64_t stride = (int64_t)gridDim.x * chunk;
   const int64_t nfull = n - n % PK::EP;
-  for (int64_t base = (int64_t)blockIdx.x * chunk; base < nfull; base += stride) {
-    double v[PK::P][PK::EP];
-    bool ok[PK::P];
+  int64_t base = (int64_t)blockIdx.x * chunk;
+  Raw<KIND, DT> cur[PK::P];
+  bool ok[PK::P];
+#pragma unroll
+  for (int p = 0; p < PK::P; ++p) {
+    const int64_t i = pk_index<PK::EP>(base, p);
+    ok[p] = i < nfull;
+    if (ok[p]) cur[p] = load_raw<KIND, DT>(s, i);
+  }
+  for (; base < nfull; base += stride) {
+    Raw<KIND, DT> nxt[PK::P];
+    bool okn[PK::P];
 #pragma unroll
     for (int p = 0; p < PK::P; ++p) {
-      int64_t i = pk_index<PK::EP>(base, p);
-      ok[p] = i < nfull;
-      if (ok[p]) load_packet<KIND, DT>(s, t, p, i, v[p]);
+      const int64_t i = pk_index<PK::EP>(base + stride, p);
+      okn[p] = i < nfull;
+      if (okn[p]) nxt[p] = load_raw<KIND, DT>(s, i);
     }
 #pragma unroll
-    for (int p = 0; p < PK::P; ++p)
+    for (int p = 0; p < PK::P; ++p) {
       if (ok[p]) {
-#pragma unroll
-        for (int j = 0; j < PK::EP; ++j) f(v[p][j], pk_index<PK::EP>(base, p) + j);
+        double v[PK::EP];
+        unpack<KIND, DT>(cur[p], t, p, v);
+        fp(v, pk_index<PK::EP>(base, p));
       }
+      cur[p] = nxt[p];
+      ok[p] = okn[p];
+    }
   }
+}
+
+// Per-value form of stream_packets: f(value, index).
+template <int KIND, int DT, typename F>
+__device__ inline void stream_values(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
+                                     F&& f) {
+  using PK = Pack<KIND, DT>;
+  stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0) {
+#pragma unroll
+    for (int j = 0; j < PK::EP; ++j) f(v[j], i0 + j);
+  });
 }
 
 // Loads the single value i (tail elements); computes its own channel constants.
@@ -145,7 +193,7 @@ __device__ inline double load1(const SrcDev& s, int64_t i) {
     double M, A;
     epi_channel(s, u, (int)(i % s.channels), M, A);
     double r = fma((double)static_cast<const int32_t*>(s.x)[i], M, A);
-    return s.ep_relu ? fmax(r, 0.0) : r;
+    return s.ep_relu ? fmax(r, 0.0) : r;  // tail values only
   } else {
     int F = imax(s.fa->fl, s.fb->fl);
     double a = (double)static_cast<const int8_t*>(s.x)[i] + (code_is_off(s.dtype, s.fa) ? 128.0 : 0.0);

@@ -128,13 +128,33 @@ ARCH = {"alexnet": arch_alexnet, "vgg16": arch_vgg16,
 # ----------------------------------------------------------------------------
 # Runner
 # ----------------------------------------------------------------------------
+FUSE_MAX_DEPTH = 256       # r * s * c of a contraction recomputed by fxpq_cblock
+FUSE_MAX_TILES = 61440
+
+
+def fuse_cblock(desc, Ho, Wo):
+    """Whether a conv C-Block runs as one fused fxpq_cblock call: its three
+    contraction passes must cost less than storing the int32 accumulators and
+    reading them twice, i.e. a shallow contraction (r*s*c <= 256) that reads
+    no more input bytes per pass than it has outputs (a strided 1x1 conv reads
+    only Ho*Wo of the input pixels)."""
+    depth = desc.r * desc.s * desc.c
+    M = desc.n * Ho * Wo
+    tiles = ((M + 255) // 256) * ((desc.k + 63) // 64) if desc.k <= 64 else \
+        ((M + 127) // 128) * ((desc.k + 127) // 128)
+    pixels_read = min(desc.h * desc.w, Ho * Wo * desc.r * desc.s)
+    return (desc.c % 16 == 0 and depth <= FUSE_MAX_DEPTH and pixels_read * desc.c <= desc.k * Ho * Wo
+            and tiles <= FUSE_MAX_TILES)
+
+
 class CalibNet:
     """One workload resident on the GPU: quantized parameters, activation
     buffers and the input; ``forward()`` enqueues a full calibration forward."""
 
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", wl_override=None,
-                 keep_acts=True):
+                 keep_acts=True, fused=True):
         import torch
+        self.fused = fused
         self.torch = torch
         self.name = name
         self.seed = SEEDS[name] if seed is None else seed
@@ -336,6 +356,15 @@ class CalibNet:
                 acc = self.acc[:n_out]
                 keep.append(acc)
                 ops2 = 2 * n_out * p["wlen"]
+                if op == "conv" and not n.last and self.fused and fuse_cblock(p["desc"], p["Ho"], p["Wo"]):
+                    # shallow contraction, wide output: recompute instead of an
+                    # int32 round trip (same formats and codes bit for bit)
+                    f = self.act_fmt[n.name]
+                    add("cblock", ops2, L.fxpq_cblock, h, C.byref(p["desc"]), xin.data_ptr(), fx.C8,
+                        p["w"].data_ptr(), p["colsum"].data_ptr(), C.byref(p["ep"]), A_WL,
+                        fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), self.act_codes[n.name].data_ptr(),
+                        fx.C8, acc.data_ptr(), p["mm"].data_ptr())
+                    continue
                 if op == "conv":
                     add("qconv", ops2, L.fxpq_qconv, h, C.byref(p["desc"]), xin.data_ptr(), fx.C8,
                         p["w"].data_ptr(), p["colsum"].data_ptr(), C.byref(p["ep"]), acc.data_ptr(),
@@ -487,7 +516,7 @@ class CalibNet:
 
 
 def run_fc(seed=0, device="cuda:0"):
-    """BASELINE config 1: one FC layer, W and A quantized at WL 8, 6 and 4, the
+    """The single-FC-layer workload: one FC layer, W and A quantized at WL 8, 6 and 4, the
     int32 product requantized to WL 8 with its own search."""
     import torch
     dev = torch.device(device)
@@ -534,10 +563,10 @@ def run_fc(seed=0, device="cuda:0"):
 
 
 def run_config(name, seed=None, device="cuda:0", batch=None, image=None, with_codes=False,
-               wl_override=None):
+               wl_override=None, fused=True):
     if name == "fc":
         return run_fc(SEEDS["fc"] if seed is None else seed, device)
-    net = CalibNet(name, seed, batch, image, device, wl_override=wl_override)
+    net = CalibNet(name, seed, batch, image, device, wl_override=wl_override, fused=fused)
     net.forward()
     res = net.results(with_codes=with_codes)
     net.close()

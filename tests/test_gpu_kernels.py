@@ -384,3 +384,24 @@ def test_nonfinite_input_sets_flag_and_status(fx, h):
     (gwl, gfl, gsign, gst), _ = run_fl_search(fx, h, fx.src_f32(dev(x)), x.size, 8, fx.SIGN_AUTO)
     assert gst != 0
     assert fx.sync_status(h) & fx.FLAG_NONFINITE
+
+
+def test_out_of_range_values_keep_error_status(fx, h, orc):
+    # |v * 2^max(s, fl_hi)| >= 2^62 is outside the exact range of the general
+    # pass: the format must carry a nonzero status and the range flag must be
+    # raised; a search right after it must be unaffected
+    import torch
+    v = np.array([2 ** 61, -(2 ** 60), 12345, 0, 7] * 40, np.int64)
+    sd = torch.tensor([0], dtype=torch.int32, device=DEV)
+    note("fls-int out of range")
+    (gwl, gfl, gsign, gst), _ = run_fl_search(fx, h, fx.src_int(dev(v), fx.I64, sd), v.size, 8,
+                                              fx.SIGN_AUTO)
+    assert gst != 0
+    assert fx.sync_status(h) & fx.FLAG_RANGE
+    w = synth.integers(12, "after-range", (5000,), -2 ** 40, 2 ** 40)
+    sd = torch.tensor([20], dtype=torch.int32, device=DEV)
+    (gwl, gfl, gsign, gst), _ = run_fl_search(fx, h, fx.src_int(dev(w), fx.I64, sd), w.size, 8,
+                                              fx.SIGN_AUTO)
+    ofl, osign, _ = orc.fl_search_i64(w, 20, 8, fx.SIGN_AUTO, FL_LO, FL_HI)
+    assert (gfl, gsign, gst) == (ofl, osign, 0)
+    check_flags(fx, h)

@@ -61,3 +61,23 @@ def test_network_bit_exact(mods, name, batch, image):
     ref = oracle.nets.run_config(name, batch=batch, image=image)
     compare(res, ref)
     np.testing.assert_allclose(res["input_error"][:3], ref["input_error"][:3], rtol=1e-9)
+
+
+def test_fused_cblocks_match_unfused_forward(mods):
+    # the fused C-Block calls against the qconv -> fl_search -> requant
+    # sequence over a whole ResNet-50 forward, at a size beyond the oracle's
+    nets, _ = mods
+    note("net resnet50 fused vs unfused 8x112")
+    res = {}
+    for fused in (True, False):
+        net = nets.CalibNet("resnet50", batch=8, image=112, fused=fused)
+        assert any(c[0] == "cblock" for c in net._plan()) == fused
+        net.forward()
+        res[fused] = net.results(with_codes=True)
+        net.close()
+    a, b = res[True], res[False]
+    assert a["flags"] == 0 and b["flags"] == 0
+    assert a["fmts"] == b["fmts"]
+    for name in b["codes"]:
+        assert np.array_equal(a["codes"][name], b["codes"][name]), name
+    assert np.array_equal(a["logits"], b["logits"])
