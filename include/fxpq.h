@@ -182,6 +182,24 @@ fxpq_status fxpq_requant(fxpq_handle h, const fxpq_src* src, int64_t n, const fx
                          void* codes, fxpq_dtype code_type);
 
 /*
+ * fxpq_requant of C-Block values (src of kind FXPQ_SRC_ACC, code_type
+ * FXPQ_C8, FXPQ_I8 or FXPQ_U8OFF), plus the min and max of the residual sum
+ * (Sec. "FxP-QLayer": eltwise ADD of two FxP-QLayer outputs, aligned to the
+ * finer fractional length, optionally followed by ReLU) that will consume the
+ * codes written here and the 8-bit codes b (type b_type, format d_fmt_b, n
+ * values, device):
+ *     s_i = relu?(codes_i * 2^-fl + b_i * 2^-fl_b).
+ * d_add_minmax (device double[2]) receives min and max of s_i * 2^F, F =
+ * max(fl, fl_b): the d_minmax an FXPQ_SRC_ADD source over (codes, b) takes,
+ * so that its FL search needs no min / max pass of its own.  codes and b must
+ * be 16-byte aligned.
+ */
+fxpq_status fxpq_requant_addmm(fxpq_handle h, const fxpq_src* src, int64_t n,
+                               const fxpq_fmt* d_fmt, void* codes, fxpq_dtype code_type,
+                               const void* b, fxpq_dtype b_type, const fxpq_fmt* d_fmt_b,
+                               int32_t relu, double* d_add_minmax);
+
+/*
  * Fractional-length search (Sec. "Quantization Parameters Optimization"): for
  * every fl in [fl_lo, fl_hi] the data-structure error of Eq. 14,
  *     L(fl) = sum_i (v_i - Q(v_i; wl, fl, S) * 2^-fl)^2,

@@ -123,6 +123,7 @@ struct Ctx {
   hipStream_t stream;
   Scratch sc;
   Timer* timer;
+  int cus;  // compute units of the handle's device
 };
 
 // Brackets one launch with events when `kind` is being timed.
@@ -144,6 +145,9 @@ hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out);
 hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* out);
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
                           int code_type);
+hipError_t launch_requant_addmm(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
+                                void* codes, int code_type, const int8_t* b, int b_type,
+                                const fxpq_fmt* fmt_b, int relu, double* d_add_minmax);
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
 hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,

@@ -268,16 +268,18 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
   }
 }
 
-// Block partials of the window pass.  Each exact per-thread sum (below 2^53)
+// Block partials of the window pass.  Each exact per-thread sum (below 2^62)
 // is split into its high and low 32-bit halves, summed separately over the
 // block: slot `bid` of part_i holds kWinPart int64 (per candidate: A hi/lo,
 // PH hi/lo, PL hi/lo), part_f the two bound sums.
-__device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long long* part_i,
-                                          double* part_f, long long* shl, double* shd) {
+__device__ inline void win_write_partials_i64(const long long* A, const long long* PH,
+                                              const long long* PL, double V2, double CE,
+                                              int64_t bid, long long* part_i, double* part_f,
+                                              long long* shl, double* shd) {
   long long* pi = part_i + bid * kWinPart;
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
-    const long long q3[3] = {exact_i64(acc.A[j]), exact_i64(acc.PH[j]), exact_i64(acc.PL[j])};
+    const long long q3[3] = {A[j], PH[j], PL[j]};
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
       const long long h = block_reduce(q3[k] >> 32, OpAddL(), shl);
@@ -288,12 +290,24 @@ __device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long l
       }
     }
   }
-  double v2 = block_reduce(acc.V2, OpAddD(), shd);
-  double ce = block_reduce(acc.CE, OpAddD(), shd);
+  double v2 = block_reduce(V2, OpAddD(), shd);
+  double ce = block_reduce(CE, OpAddD(), shd);
   if (threadIdx.x == 0) {
     part_f[2 * bid] = v2;
     part_f[2 * bid + 1] = ce;
   }
+}
+
+__device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long long* part_i,
+                                          double* part_f, long long* shl, double* shd) {
+  long long A[kWindow], PH[kWindow], PL[kWindow];
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) {
+    A[j] = exact_i64(acc.A[j]);
+    PH[j] = exact_i64(acc.PH[j]);
+    PL[j] = exact_i64(acc.PL[j]);
+  }
+  win_write_partials_i64(A, PH, PL, acc.V2, acc.CE, bid, part_i, part_f, shl, shd);
 }
 
 // Launch helpers shared by the streaming search and the fused C-Block.

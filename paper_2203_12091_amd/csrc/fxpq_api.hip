@@ -12,6 +12,7 @@ using namespace fxpq;
 
 struct fxpq_handle_s {
   int device;
+  int cus;  // compute units
   hipStream_t stream;
   void* scratch;
   size_t scratch_bytes;
@@ -35,7 +36,7 @@ bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32; }
 
 size_t code_align(int t) { (void)t; return 16; }
 
-Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc, &h->timer}; }
+Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc, &h->timer, h->cus}; }
 
 fxpq_status hip_status(hipError_t e) { return e == hipSuccess ? FXPQ_OK : FXPQ_ERR_HIP; }
 
@@ -146,6 +147,11 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   if (!h) return FXPQ_ERR_ALLOC;
   h->device = device;
   h->stream = nullptr;
+  if (hipDeviceGetAttribute(&h->cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+      h->cus < 1) {
+    delete h;
+    return FXPQ_ERR_HIP;
+  }
   size_t off = 0;
   auto take = [&](size_t bytes) {
     size_t o = off;
@@ -240,6 +246,24 @@ fxpq_status fxpq_requant(fxpq_handle h, const fxpq_src* src, int64_t n, const fx
   if (st) return st;
   DeviceGuard g(h->device);
   return hip_status(launch_requant(ctx(h), s, n, d_fmt, codes, code_type));
+}
+
+fxpq_status fxpq_requant_addmm(fxpq_handle h, const fxpq_src* src, int64_t n,
+                               const fxpq_fmt* d_fmt, void* codes, fxpq_dtype code_type,
+                               const void* b, fxpq_dtype b_type, const fxpq_fmt* d_fmt_b,
+                               int32_t relu, double* d_add_minmax) {
+  if (!h || !src || n < 1 || !d_fmt || !codes || !b || !d_fmt_b || !d_add_minmax)
+    return FXPQ_ERR_INVALID_ARG;
+  if (!is_code8(code_type) || !is_code8(b_type)) return FXPQ_ERR_INVALID_ARG;
+  if (src->kind != FXPQ_SRC_ACC) return FXPQ_ERR_UNSUPPORTED;
+  if (!aligned(codes, 16) || !aligned(b, 16)) return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  DeviceGuard g(h->device);
+  return hip_status(launch_requant_addmm(ctx(h), s, n, d_fmt, codes, code_type,
+                                         static_cast<const int8_t*>(b), b_type, d_fmt_b,
+                                         relu ? 1 : 0, d_add_minmax));
 }
 
 fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl,

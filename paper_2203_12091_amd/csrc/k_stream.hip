@@ -352,6 +352,67 @@ hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) 
   return hipGetLastError();
 }
 
+// Requantization of C-Block values, plus the min / max of the residual sum
+// that consumes the codes written: relu?(code * 2^(F - fl_out) + b * 2^(F -
+// fl_b)) in units of 2^-F, F = max(fl_out, fl_b), the same exact values an
+// eltwise source over (codes, b) yields.  Block partials to `part`.
+template <int OUT>
+__global__ __launch_bounds__(kThreads) void k_requant_addmm(SrcDev s, int64_t n,
+                                                            const fxpq_fmt* fmt, void* codes,
+                                                            const int8_t* b, int b_type,
+                                                            const fxpq_fmt* fmt_b, int relu,
+                                                            double* part, unsigned* flags) {
+  constexpr int KIND = FXPQ_SRC_ACC, DT = FXPQ_I32;
+  using PK = Pack<KIND, DT>;
+  __shared__ double sh[8];
+  const int sv = src_scale(s);
+  const QFmt q = qfmt_setup<OUT>(fmt, sv, flags);
+  double mn = INFINITY, mx = -INFINITY;
+  if (q.ok) {
+    const int F = imax(fmt->fl, fmt_b->fl);
+    const double ca = ldexp(1.0, F - fmt->fl), cb = ldexp(1.0, F - fmt_b->fl);
+    const double offa = (double)q.off;
+    const double offb = code_is_off(b_type, fmt_b) ? 128.0 : 0.0;
+    const double relo = relu ? 0.0 : -INFINITY;
+    auto add_value = [&](int stored_a, int stored_b) {
+      const double va = ((double)stored_a + offa) * ca;
+      return fmax(fma((double)stored_b + offb, cb, va), relo);
+    };
+    const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    ThreadVals<PK::V> t;
+    thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, t);
+    const int64_t nfull = n - n % PK::EP;
+    stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0) {
+      const int bw = *reinterpret_cast<const int*>(b + i0);
+      int c[PK::EP];
+#pragma unroll
+      for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[j], q);
+      storev<OUT, PK::EP>(codes, i0, c);
+#pragma unroll
+      for (int j = 0; j < PK::EP; ++j) {
+        const double x = add_value(c[j], (bw << (24 - 8 * j)) >> 24);
+        mn = fmin(mn, x);
+        mx = fmax(mx, x);
+      }
+    });
+    if (gtid == 0) {
+      for (int64_t i = nfull; i < n; ++i) {
+        const int ci = quant_one(load1<KIND, DT>(s, i), q);
+        store1<OUT>(codes, i, ci);
+        const double x = add_value(ci, b[i]);
+        mn = fmin(mn, x);
+        mx = fmax(mx, x);
+      }
+    }
+  }
+  mn = block_reduce(mn, OpMin(), sh);
+  mx = block_reduce(mx, OpMax(), sh);
+  if (threadIdx.x == 0) {
+    part[2 * blockIdx.x] = mn;
+    part[2 * blockIdx.x + 1] = mx;
+  }
+}
+
 template <int OUT>
 static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
                         int blocks) {
@@ -375,6 +436,30 @@ hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_f
   }
   timer_end(c, timed, (in_b + out_b) * (double)n);
   return hipGetLastError();
+}
+
+hipError_t launch_requant_addmm(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
+                                void* codes, int code_type, const int8_t* b, int b_type,
+                                const fxpq_fmt* fmt_b, int relu, double* d_add_minmax) {
+  int blocks = stream_grid(n, src_channels(s), 0, src_vec(s));
+  bool timed = timer_begin(c, FXPQ_TIMER_REQUANT);
+  double* part = c.sc.minmax_part;
+  switch (code_type) {
+    case FXPQ_I8:
+      k_requant_addmm<FXPQ_I8><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type,
+                                                                  fmt_b, relu, part, c.sc.flags);
+      break;
+    case FXPQ_U8OFF:
+      k_requant_addmm<FXPQ_U8OFF><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type,
+                                                                     fmt_b, relu, part, c.sc.flags);
+      break;
+    default:
+      k_requant_addmm<FXPQ_C8><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type,
+                                                                  fmt_b, relu, part, c.sc.flags);
+      break;
+  }
+  timer_end(c, timed, 6.0 * (double)n);
+  return launch_minmax_fin(c, part, blocks, d_add_minmax);
 }
 
 hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes, int code_type,

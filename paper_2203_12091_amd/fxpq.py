@@ -20,7 +20,7 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
-    "fxpq_quantize", "fxpq_requant", "fxpq_fl_search", "fxpq_qconv", "fxpq_qgemm",
+    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_cblock", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
 ]
@@ -75,6 +75,7 @@ def lib():
             "fxpq_sync_status": [p, p],
             "fxpq_quantize": [p, p, i64, p, p, C.c_int],
             "fxpq_requant": [p, p, i64, p, p, C.c_int],
+            "fxpq_requant_addmm": [p, p, i64, p, p, C.c_int, p, C.c_int, p, i32, p],
             "fxpq_fl_search": [p, p, i64, i32, i32, i32, i32, p, p],
             "fxpq_qconv": [p, p, p, C.c_int, p, p, p, p, p],
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
@@ -166,6 +167,11 @@ def quantize(h, x, n, d_fmt, codes, code_type):
 
 def requant(h, src, n, d_fmt, codes, code_type):
     _call("fxpq_requant", h.value, C.byref(src), n, ptr(d_fmt), ptr(codes), code_type)
+
+
+def requant_addmm(h, src, n, d_fmt, codes, code_type, b, b_type, d_fmt_b, relu, d_add_minmax):
+    _call("fxpq_requant_addmm", h.value, C.byref(src), n, ptr(d_fmt), ptr(codes), code_type, ptr(b),
+          b_type, ptr(d_fmt_b), int(relu), ptr(d_add_minmax))
 
 
 def fl_search(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, d_sse=None):

@@ -152,7 +152,7 @@ class CalibNet:
     buffers and the input; ``forward()`` enqueues a full calibration forward."""
 
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", wl_override=None,
-                 keep_acts=True, fused=True):
+                 keep_acts=True, fused=False):
         import torch
         self.fused = fused
         self.torch = torch
@@ -281,7 +281,7 @@ class CalibNet:
                 shapes[n.name] = shapes[n.inp]
                 self.act_fmt[n.name] = self._fmt()
                 self.act_codes[n.name] = self._empty((B,) + shapes[n.inp], T.int8)
-                self.ops.append(("add", n, {}))
+                self.ops.append(("add", n, {"mm": self._empty((2,), T.float64)}))
             elif n.op == "avgpool":
                 H, W, C = shapes[n.inp]
                 r = np.array([np.float32(1.0) / np.float32(H * W)], np.float32)
@@ -325,6 +325,11 @@ class CalibNet:
         self.le_out = self._empty((4,), T.float64)
 
     # -- forward ---------------------------------------------------------------
+    def _fused_conv(self, n, p):
+        """Whether conv node n runs as one fused fxpq_cblock call."""
+        return (n.op == "conv" and not n.last and self.fused
+                and fuse_cblock(p["desc"], p["Ho"], p["Wo"]))
+
     def _plan(self):
         """Pre-builds every library call of one forward: (class, work, fn, args).
         `work` is the call's algorithmic HBM bytes (streaming calls) or int8
@@ -338,6 +343,18 @@ class CalibNet:
             calls.append((cls, work, fn, args))
 
         keep = self.keep
+        # Each residual add takes its min / max from the requantization of the
+        # operand produced last, when that is an unfused conv C-Block.
+        produced_at = {n.name: i for i, (op, n, *r) in enumerate(self.ops)}
+        addmm = {}
+        for op, n, *rest in self.ops:
+            if op == "add":
+                last = max((n.inp, n.other), key=lambda nm: produced_at[nm])
+                first = n.other if last == n.inp else n.inp
+                lop, ln, *lr = self.ops[produced_at[last]]
+                if lop == "conv" and not ln.last and not self._fused_conv(ln, lr[0]):
+                    addmm[last] = (n, first, rest[0]["mm"])
+        self.addmm_adds = {v[0].name for v in addmm.values()}
         for op, n, *rest in self.ops:
             if op == "input":
                 f, c = self.act_fmt["input"], self.act_codes["input"]
@@ -356,7 +373,7 @@ class CalibNet:
                 acc = self.acc[:n_out]
                 keep.append(acc)
                 ops2 = 2 * n_out * p["wlen"]
-                if op == "conv" and not n.last and self.fused and fuse_cblock(p["desc"], p["Ho"], p["Wo"]):
+                if self._fused_conv(n, p):
                     # shallow contraction, wide output: recompute instead of an
                     # int32 round trip (same formats and codes bit for bit)
                     f = self.act_fmt[n.name]
@@ -384,8 +401,15 @@ class CalibNet:
                     f = self.act_fmt[n.name]
                     add("fl_search", 4 * n_out, L.fxpq_fl_search, h, C.byref(src), n_out, A_WL,
                         fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), None)
-                    add("requant", 5 * n_out, L.fxpq_requant, h, C.byref(src), n_out, f.data_ptr(),
-                        self.act_codes[n.name].data_ptr(), fx.C8)
+                    if n.name in addmm:
+                        an, other, mm = addmm[n.name]
+                        add("requant", 6 * n_out, L.fxpq_requant_addmm, h, C.byref(src), n_out,
+                            f.data_ptr(), self.act_codes[n.name].data_ptr(), fx.C8,
+                            self.act_codes[other].data_ptr(), fx.C8, self.act_fmt[other].data_ptr(),
+                            int(an.relu), mm.data_ptr())
+                    else:
+                        add("requant", 5 * n_out, L.fxpq_requant, h, C.byref(src), n_out, f.data_ptr(),
+                            self.act_codes[n.name].data_ptr(), fx.C8)
             elif op == "maxpool":
                 p = rest[0]
                 out = self.act_codes[n.name]
@@ -394,7 +418,9 @@ class CalibNet:
                     n.pad, out.data_ptr())
             elif op == "add":
                 a, b = self.act_codes[n.inp], self.act_codes[n.other]
-                src = fx.src_add(a, fx.C8, self.act_fmt[n.inp], b, fx.C8, self.act_fmt[n.other], n.relu)
+                mm = rest[0]["mm"] if n.name in self.addmm_adds else None
+                src = fx.src_add(a, fx.C8, self.act_fmt[n.inp], b, fx.C8, self.act_fmt[n.other], n.relu,
+                                 mm)
                 keep.append(src)
                 f = self.act_fmt[n.name]
                 m = a.numel()
@@ -563,7 +589,7 @@ def run_fc(seed=0, device="cuda:0"):
 
 
 def run_config(name, seed=None, device="cuda:0", batch=None, image=None, with_codes=False,
-               wl_override=None, fused=True):
+               wl_override=None, fused=False):
     if name == "fc":
         return run_fc(SEEDS["fc"] if seed is None else seed, device)
     net = CalibNet(name, seed, batch, image, device, wl_override=wl_override, fused=fused)

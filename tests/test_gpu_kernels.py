@@ -339,6 +339,43 @@ def test_add_source(fx, h, orc):
     check_flags(fx, h)
 
 
+def test_requant_with_residual_minmax(fx, h, orc):
+    # requantization of C-Block values that also reduces the min / max of the
+    # residual sum they feed; the ADD search then uses that min / max
+    import torch
+    for ci, case in enumerate([CONV_CASES[0], CONV_CASES[5], CONV_CASES[1]]):
+        acc, ep, mm, v, s_out, keep = gpu_conv_case(fx, h, orc, *case, seed=41 + ci)
+        n = acc.numel()  # whole rows: an ACC source covers complete channel groups
+        vn = v.transpose(0, 2, 3, 1).ravel()[:n]
+        src = fx.src_acc(acc, ep, mm)
+        out = fmt_new()
+        fx.fl_search(h, src, n, 8, fx.SIGN_AUTO, FL_LO, FL_HI, out)
+        gwl, gfl, gsign, gst = fmt_host(out)
+        ofl, osign, _ = orc.fl_search_i64(vn, s_out, 8, fx.SIGN_AUTO, FL_LO, FL_HI)
+        assert (gfl, gsign, gst) == (ofl, osign, 0)
+        b = synth.integers(51 + ci, "resid", (n,), 0, 255)
+        fb = 4 + ci
+        bd = dev((b - 128).astype(np.int8))
+        fbd = fmt_dev(8, fb, 0)
+        for relu in (True, False):
+            note("requant+addmm", case, relu)
+            codes = empty((n,), torch.int8)
+            amm = torch.full((2,), 7.0, dtype=torch.float64, device=DEV)
+            fx.requant_addmm(h, src, n, out, codes, fx.C8, bd, fx.C8, fbd, relu, amm)
+            want = orc.quantize_i64(vn, s_out, 8, ofl, osign)
+            assert np.array_equal(decode8(host(codes), gsign == 0), want)
+            va, sa = orc.eltwise_add(want, ofl, b, fb, relu)
+            gmm = host(amm)
+            assert gmm[0] == va.min() and gmm[1] == va.max()
+            # the sum's own search with that min / max
+            asrc = fx.src_add(codes, fx.C8, out, bd, fx.C8, fbd, relu, amm)
+            aout = fmt_new()
+            fx.fl_search(h, asrc, n, 8, fx.SIGN_AUTO, FL_LO, FL_HI, aout)
+            afl, asg, _ = orc.fl_search_i64(va, sa, 8, fx.SIGN_AUTO, FL_LO, FL_HI)
+            assert fmt_host(aout)[1:] == (afl, asg, 0)
+    check_flags(fx, h)
+
+
 # ----------------------------------------------------------------------------
 # pools and layer error
 # ----------------------------------------------------------------------------
