@@ -127,9 +127,13 @@ __device__ inline void unpack(const Raw<KIND, DT>& r, const ThreadVals<Pack<KIND
 }
 
 // Drives a streaming kernel over this thread's packets of the grid-stride
-// loop: fp(values, index of the first) for every whole packet, the next
-// iteration's loads issued before this one's values are consumed.  Values
-// past the last whole packet are left to the caller.
+// loop: fp(values, index of the first) for every whole packet.  Two register
+// sets alternate so that the loads of the next iteration are in flight while
+// this one's values are consumed; every load is issued unconditionally (an
+// index past the end reads the last whole packet again, which is not
+// consumed), so the number of loads in flight is fixed and the wait before
+// each use only covers the older one.  Values past the last whole packet are
+// left to the caller.
 template <int KIND, int DT, typename F>
 __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
                                       F&& fp) {
@@ -137,34 +141,35 @@ __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVa
   const int64_t chunk = (int64_t)kThreads * PK::V;
   const int64_t stride = (int64_t)gridDim.x * chunk;
   const int64_t nfull = n - n % PK::EP;
-  int64_t base = (int64_t)blockIdx.x * chunk;
-  Raw<KIND, DT> cur[PK::P];
-  bool ok[PK::P];
-#pragma unroll
-  for (int p = 0; p < PK::P; ++p) {
-    const int64_t i = pk_index<PK::EP>(base, p);
-    ok[p] = i < nfull;
-    if (ok[p]) cur[p] = load_raw<KIND, DT>(s, i);
-  }
-  for (; base < nfull; base += stride) {
-    Raw<KIND, DT> nxt[PK::P];
-    bool okn[PK::P];
+  if (nfull == 0) return;
+  const int64_t last = nfull - PK::EP;
+  auto load_set = [&](int64_t base, Raw<KIND, DT>* r) {
 #pragma unroll
     for (int p = 0; p < PK::P; ++p) {
-      const int64_t i = pk_index<PK::EP>(base + stride, p);
-      okn[p] = i < nfull;
-      if (okn[p]) nxt[p] = load_raw<KIND, DT>(s, i);
+      const int64_t i = pk_index<PK::EP>(base, p);
+      r[p] = load_raw<KIND, DT>(s, i < nfull ? i : last);
     }
+  };
+  auto use_set = [&](int64_t base, const Raw<KIND, DT>* r) {
 #pragma unroll
     for (int p = 0; p < PK::P; ++p) {
-      if (ok[p]) {
+      const int64_t i = pk_index<PK::EP>(base, p);
+      if (i < nfull) {
         double v[PK::EP];
-        unpack<KIND, DT>(cur[p], t, p, v);
-        fp(v, pk_index<PK::EP>(base, p));
+        unpack<KIND, DT>(r[p], t, p, v);
+        fp(v, i);
       }
-      cur[p] = nxt[p];
-      ok[p] = okn[p];
     }
+  };
+  int64_t base = (int64_t)blockIdx.x * chunk;
+  Raw<KIND, DT> ra[PK::P], rb[PK::P];
+  load_set(base, ra);
+  load_set(base + stride, rb);
+  for (; base < nfull; base += 2 * stride) {
+    use_set(base, ra);
+    load_set(base + 2 * stride, ra);
+    use_set(base + stride, rb);
+    load_set(base + 3 * stride, rb);
   }
 }
 
