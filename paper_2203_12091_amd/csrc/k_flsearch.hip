@@ -44,7 +44,7 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   // scaled by 2^(sigma - sv) = 2^(fl_hi + 24), exactly.
   const double post = u.wscale;
   const int64_t nfull = n - n % PK::EP;
-  stream_packets<KIND, DT>(s, n, tv, [&](const double* v, int64_t) {
+  stream_packets<KIND, DT>(s, n, tv, [&](const double* v, int64_t, int) {
 #pragma unroll
     for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j]);
   });

@@ -163,7 +163,7 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
   ThreadVals<PK::V> t;
   thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, t);
   const int64_t nfull = n - n % PK::EP;
-  stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0) {
+  stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0, int) {
     int c[PK::EP];
 #pragma unroll
     for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[j], q);
@@ -382,8 +382,7 @@ __global__ __launch_bounds__(kThreads) void k_requant_addmm(SrcDev s, int64_t n,
     ThreadVals<PK::V> t;
     thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, t);
     const int64_t nfull = n - n % PK::EP;
-    stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0) {
-      const int bw = *reinterpret_cast<const int*>(b + i0);
+    stream_packets<KIND, DT, true>(s, n, t, [&](const double* v, int64_t i0, int bw) {
       int c[PK::EP];
 #pragma unroll
       for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[j], q);
@@ -394,7 +393,7 @@ __global__ __launch_bounds__(kThreads) void k_requant_addmm(SrcDev s, int64_t n,
         mn = fmin(mn, x);
         mx = fmax(mx, x);
       }
-    });
+    }, b);
     if (gtid == 0) {
       for (int64_t i = nfull; i < n; ++i) {
         const int ci = quant_one(load1<KIND, DT>(s, i), q);

@@ -134,42 +134,48 @@ __device__ inline void unpack(const Raw<KIND, DT>& r, const ThreadVals<Pack<KIND
 // consumed), so the number of loads in flight is fixed and the wait before
 // each use only covers the older one.  Values past the last whole packet are
 // left to the caller.
-template <int KIND, int DT, typename F>
+template <int KIND, int DT, bool AUX = false, typename F>
 __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
-                                      F&& fp) {
+                                      F&& fp, const int8_t* aux = nullptr) {
+  // AUX: one byte per value of `aux`, loaded with each packet and handed to
+  // fp as the packet's EP bytes (4-value packets only).
+  static_assert(!AUX || Pack<KIND, DT>::EP == 4, "aux bytes need 4-value packets");
   using PK = Pack<KIND, DT>;
   const int64_t chunk = (int64_t)kThreads * PK::V;
   const int64_t stride = (int64_t)gridDim.x * chunk;
   const int64_t nfull = n - n % PK::EP;
   if (nfull == 0) return;
   const int64_t last = nfull - PK::EP;
-  auto load_set = [&](int64_t base, Raw<KIND, DT>* r) {
+  auto load_set = [&](int64_t base, Raw<KIND, DT>* r, int* x) {
 #pragma unroll
     for (int p = 0; p < PK::P; ++p) {
-      const int64_t i = pk_index<PK::EP>(base, p);
-      r[p] = load_raw<KIND, DT>(s, i < nfull ? i : last);
+      int64_t i = pk_index<PK::EP>(base, p);
+      i = i < nfull ? i : last;
+      r[p] = load_raw<KIND, DT>(s, i);
+      if constexpr (AUX) x[p] = *reinterpret_cast<const int*>(aux + i);
     }
   };
-  auto use_set = [&](int64_t base, const Raw<KIND, DT>* r) {
+  auto use_set = [&](int64_t base, const Raw<KIND, DT>* r, const int* x) {
 #pragma unroll
     for (int p = 0; p < PK::P; ++p) {
       const int64_t i = pk_index<PK::EP>(base, p);
       if (i < nfull) {
         double v[PK::EP];
         unpack<KIND, DT>(r[p], t, p, v);
-        fp(v, i);
+        fp(v, i, x[p]);
       }
     }
   };
   int64_t base = (int64_t)blockIdx.x * chunk;
   Raw<KIND, DT> ra[PK::P], rb[PK::P];
-  load_set(base, ra);
-  load_set(base + stride, rb);
+  int xa[PK::P] = {}, xb[PK::P] = {};
+  load_set(base, ra, xa);
+  load_set(base + stride, rb, xb);
   for (; base < nfull; base += 2 * stride) {
-    use_set(base, ra);
-    load_set(base + 2 * stride, ra);
-    use_set(base + stride, rb);
-    load_set(base + 3 * stride, rb);
+    use_set(base, ra, xa);
+    load_set(base + 2 * stride, ra, xa);
+    use_set(base + stride, rb, xb);
+    load_set(base + 3 * stride, rb, xb);
   }
 }
 
@@ -178,7 +184,7 @@ template <int KIND, int DT, typename F>
 __device__ inline void stream_values(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
                                      F&& f) {
   using PK = Pack<KIND, DT>;
-  stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0) {
+  stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0, int) {
 #pragma unroll
     for (int j = 0; j < PK::EP; ++j) f(v[j], i0 + j);
   });
