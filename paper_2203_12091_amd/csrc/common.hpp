@@ -12,7 +12,8 @@ constexpr int kThreads = 256;        // threads per block of the streaming kerne
 constexpr int kMaxStreamBlocks = 2048;
 constexpr int kMaxConvBlocks = 1 << 20;
 constexpr int kWindow = 2;           // candidates of the first FL-search pass
-constexpr int kWinPart = 6 * kWindow;  // int64 per block of window-pass partials
+constexpr int kWinPart = 6 * kWindow;  // int64 per slot of window-pass sums
+constexpr int kWinSlots = 64;          // slots the window-pass blocks add into (block % kWinSlots)
 // Values per thread of the streaming window pass (the grid grows beyond that):
 // sums of W * q stay exact for max|W * q| < 2^53 / 512.
 constexpr int64_t kWinMaxPerThread = 512;
@@ -24,8 +25,8 @@ struct Scratch {
   unsigned* flags;          // sticky FXPQ_FLAG_* bits
   double* minmax;           // internal [2]
   double* minmax_part;      // per-block partials [kMaxConvBlocks][2]
-  long long* win_part;      // window FL-search partials
-  double* win_part_f;       // window FL-search fp64 partials
+  long long* win_part;      // window FL-search integer sums [kWinSlots][kWinPart] (0 between searches)
+  double* win_part_f;       // window FL-search fp64 bound sums [kWinSlots][2] (0 between searches)
   unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
   unsigned* gen_done;       // blocks of the general pass finished (0 between searches)
   void* plan;               // FlsPlan

@@ -268,15 +268,26 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
   }
 }
 
-// Block partials of the window pass.  Each exact per-thread sum (below 2^62)
+// Block results of the window pass.  Each exact per-thread sum (below 2^62)
 // is split into its high and low 32-bit halves, summed separately over the
-// block: slot `bid` of part_i holds kWinPart int64 (per candidate: A hi/lo,
-// PH hi/lo, PL hi/lo), part_f the two bound sums.
+// block and added (int64 atomics: exact, order-free) into slot bid %
+// kWinSlots of part_i (kWinPart int64 per slot: per candidate A hi/lo, PH
+// hi/lo, PL hi/lo); the two fp64 bound sums go to part_f.  The finalize reads
+// the slots and clears them for the next search.
+__device__ inline void slot_add(long long* p, long long v) {
+  __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v,
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ inline void slot_add(double* p, double v) {
+  __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 __device__ inline void win_write_partials_i64(const long long* A, const long long* PH,
                                               const long long* PL, double V2, double CE,
                                               int64_t bid, long long* part_i, double* part_f,
                                               long long* shl, double* shd) {
-  long long* pi = part_i + bid * kWinPart;
+  const int slot = (int)(bid % kWinSlots);
+  long long* pi = part_i + slot * kWinPart;
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
     const long long q3[3] = {A[j], PH[j], PL[j]};
@@ -285,16 +296,16 @@ __device__ inline void win_write_partials_i64(const long long* A, const long lon
       const long long h = block_reduce(q3[k] >> 32, OpAddL(), shl);
       const long long l = block_reduce(q3[k] & 0xFFFFFFFFll, OpAddL(), shl);
       if (threadIdx.x == 0) {
-        pi[6 * j + 2 * k] = h;
-        pi[6 * j + 2 * k + 1] = l;
+        slot_add(pi + 6 * j + 2 * k, h);
+        slot_add(pi + 6 * j + 2 * k + 1, l);
       }
     }
   }
   double v2 = block_reduce(V2, OpAddD(), shd);
   double ce = block_reduce(CE, OpAddD(), shd);
   if (threadIdx.x == 0) {
-    part_f[2 * bid] = v2;
-    part_f[2 * bid + 1] = ce;
+    slot_add(part_f + 2 * slot, v2);
+    slot_add(part_f + 2 * slot + 1, ce);
   }
 }
 
@@ -311,6 +322,6 @@ __device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long l
 }
 
 // Launch helpers shared by the streaming search and the fused C-Block.
-constexpr int kFinThreads = 512;
+constexpr int kFinThreads = kWinSlots;  // one wave: one slot per lane
 
 }  // namespace fxpq

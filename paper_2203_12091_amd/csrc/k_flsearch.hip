@@ -77,44 +77,43 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
   win_write_partials(acc, blockIdx.x, part_i, part_f, shl, shd);
 }
 
-// One block: sums the window partials exactly and decides.  A wide block so
-// the partial loads of a pass are all in flight at once.
+// Bits of |v| (0 for v == 0).
+__device__ inline int bitlen_i128(__int128 v) {
+  unsigned __int128 m = v < 0 ? (unsigned __int128)(-v) : (unsigned __int128)v;
+  unsigned long long hi = (unsigned long long)(m >> 64), lo = (unsigned long long)m;
+  return hi ? 128 - __builtin_clzll(hi) : (lo ? 64 - __builtin_clzll(lo) : 0);
+}
 
+__device__ inline double i128_to_double(__int128 v) {
+  return (double)(long long)(v >> 64) * 0x1p64 + (double)(unsigned long long)v;
+}
+
+// One wave: lane l reads (and clears) slot l of the window sums, the wave
+// adds them exactly, lane 0 decides.
 template <int KIND>
 __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
     SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
-    const double* mm, const long long* part_i, const double* part_f, int nb, FlsPlan* plan,
-    fxpq_fmt* out) {
+    const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out) {
   constexpr int NQ = 3 * kWindow;
-  constexpr int NW = kFinThreads / 64;
-  __shared__ long long sh_hi[NW][NQ], sh_lo[NW][NQ];
-  __shared__ double sh_f[NW][2];
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
   if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
   const FlsU& u = ws.u;
   const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc, bce = ws.bce;
-  // One pass over the block partials: the high and low 32-bit halves of each
-  // quantity are summed separately (both sums stay far below 2^63).
+  const int lane = threadIdx.x;
+  // The high and low 32-bit halves of each quantity are summed separately
+  // (both sums stay far below 2^63).
+  long long* p = part_i + lane * kWinPart;
   long long hi[NQ], lo[NQ];
-  double f0 = 0.0, f1 = 0.0;
 #pragma unroll
-  for (int qi = 0; qi < NQ; ++qi) hi[qi] = lo[qi] = 0;
-#pragma unroll 2
-  for (int b = threadIdx.x; b < nb; b += kFinThreads) {
-    const long long* p = part_i + (int64_t)b * kWinPart;
-    long long x[2 * NQ];
-#pragma unroll
-    for (int k = 0; k < 2 * NQ; ++k) x[k] = p[k];
-    const double g0 = part_f[2 * b], g1 = part_f[2 * b + 1];
-#pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      hi[qi] += x[2 * qi];
-      lo[qi] += x[2 * qi + 1];
-    }
-    f0 += g0;
-    f1 += g1;
+  for (int qi = 0; qi < NQ; ++qi) {
+    hi[qi] = p[2 * qi];
+    lo[qi] = p[2 * qi + 1];
   }
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  double f0 = part_f[2 * lane], f1 = part_f[2 * lane + 1];
+#pragma unroll
+  for (int k2 = 0; k2 < kWinPart; ++k2) p[k2] = 0;
+  part_f[2 * lane] = 0.0;
+  part_f[2 * lane + 1] = 0.0;
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) {
     hi[qi] = wave_reduce(hi[qi], OpAddL());
@@ -122,59 +121,62 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   }
   f0 = wave_reduce(f0, OpAddD());
   f1 = wave_reduce(f1, OpAddD());
-  if (lane == 0) {
-#pragma unroll
-    for (int qi = 0; qi < NQ; ++qi) {
-      sh_hi[wid][qi] = hi[qi];
-      sh_lo[wid][qi] = lo[qi];
-    }
-    sh_f[wid][0] = f0;
-    sh_f[wid][1] = f1;
-  }
-  __syncthreads();
-  if (threadIdx.x != 0) return;
-  long long tot_hi[NQ], tot_lo[NQ];
-  double tot_f[2] = {0.0, 0.0};
-  for (int qi = 0; qi < NQ; ++qi) {
-    tot_hi[qi] = tot_lo[qi] = 0;
-    for (int w = 0; w < NW; ++w) {
-      tot_hi[qi] += sh_hi[w][qi];
-      tot_lo[qi] += sh_lo[w][qi];
-    }
-  }
-  for (int w = 0; w < NW; ++w) {
-    tot_f[0] += sh_f[w][0];
-    tot_f[1] += sh_f[w][1];
-  }
-  auto total = [&](int qi) -> __int128 {
-    return ((__int128)tot_hi[qi] << 32) + (__int128)tot_lo[qi];
-  };
+  if (lane != 0) return;
+  const double tot_f[2] = {f0, f1};
+  auto total = [&](int qi) -> __int128 { return ((__int128)hi[qi] << 32) + (__int128)lo[qi]; };
   // K_j = 2^(2d) A - 2^(d+1) P, d = sigma - beta; shifted by `off` >= 0 so all
   // exponents are non-negative (same factor for every candidate).
   int dmin = u.sigma - b1;
   int off = 0;
   if (2 * dmin < 0) off = -2 * dmin;
   if (dmin + 1 + off < 0) off = -(dmin + 1);
-  Big best;
-  int bj = -1;
+  // 128-bit arithmetic when both terms of every K_j stay below 2^125, else
+  // 512-bit.
+  __int128 Aj[kWindow], Pj[kWindow];
+  bool fast = true;
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
-    if (j >= nc) break;
-    int d = u.sigma - (b0 + j);
-    __int128 Aj = total(3 * j);
-    __int128 Pj = total(3 * j + 1) * (__int128)67108864 + total(3 * j + 2);
-    Big k = big_sub(big_shl(big_from_i128(Aj), 2 * d + off), big_shl(big_from_i128(Pj), d + 1 + off));
-    if (bj < 0 || big_cmp(k, best) <= 0) {  // ties -> larger fl
-      best = k;
-      bj = j;
+    Aj[j] = total(3 * j);
+    Pj[j] = total(3 * j + 1) * (__int128)67108864 + total(3 * j + 2);
+    const int d = u.sigma - (b0 + (j < nc ? j : 0));
+    fast = fast && bitlen_i128(Aj[j]) + 2 * d + off <= 125 && bitlen_i128(Pj[j]) + d + 1 + off <= 125;
+  }
+  int bj = -1;
+  double kd = 0.0;
+  if (fast) {
+    __int128 best = 0;
+#pragma unroll
+    for (int j = 0; j < kWindow; ++j) {
+      if (j >= nc) break;
+      const int d = u.sigma - (b0 + j);
+      const __int128 kj = (Aj[j] << (2 * d + off)) - (Pj[j] << (d + 1 + off));
+      if (bj < 0 || kj <= best) {  // ties -> larger fl
+        best = kj;
+        bj = j;
+      }
     }
+    kd = ldexp(i128_to_double(best), -off);
+  } else {
+    Big best;
+#pragma unroll
+    for (int j = 0; j < kWindow; ++j) {
+      if (j >= nc) break;
+      const int d = u.sigma - (b0 + j);
+      Big kj = big_sub(big_shl(big_from_i128(Aj[j]), 2 * d + off),
+                       big_shl(big_from_i128(Pj[j]), d + 1 + off));
+      if (bj < 0 || big_cmp(kj, best) <= 0) {  // ties -> larger fl
+        best = kj;
+        bj = j;
+      }
+    }
+    kd = ldexp(big_to_double(best), -off);
   }
   const int fl_win = b0 + bj;
   bool done = (b1 == fl_hi);
   if (!done) {
     // Upper bound of the window's best error, lower bound of every error above
-    // the window (relative fp64 error of each sum < 2^-33).
-    double kd = ldexp(big_to_double(best), -off);
+    // the window (relative fp64 error of each sum, in any summation order,
+    // < 2^-40).
     double v2 = tot_f[0];
     double sse_ub = (v2 * (1.0 + 0x1p-30) + kd + fabs(kd) * 0x1p-50 + v2 * 0x1p-50);
     sse_ub = ldexp(sse_ub, -2 * u.sigma) * (1.0 + 0x1p-50);
@@ -383,7 +385,7 @@ hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window_fin<K_><<<1, kFinThreads, 0, c.stream>>>(
                         s, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
-                        c.sc.win_part_f, nb, plan, out)));
+                        c.sc.win_part_f, plan, out)));
   return hipGetLastError();
 }
 
