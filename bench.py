@@ -40,7 +40,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-batch", type=int, default=8)
+    ap.add_argument("--cpu-sample-batch", type=int, default=12)
     ap.add_argument("--mode", choices=["bench", "profile", "copy"], default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
                          "copy: one plain 1 GiB device copy (counter calibration)")
