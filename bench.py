@@ -31,7 +31,7 @@ HBM_PEAK_GBS = 8000.0
 INT8_PEAK_TOPS = 5000.0
 BATCH, IMAGE = 256, 224
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fl_search_window_resnet50_b256_traffic.md")
-WINDOW_SOURCES = ["k_flsearch.hip", "values.hpp", "common.hpp"]
+WINDOW_SOURCES = ["k_flsearch.hip", "fls.hpp", "values.hpp", "common.hpp"]
 
 
 def parse():
@@ -40,6 +40,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
     ap.add_argument("--mode", choices=["bench", "profile", "copy"], default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
@@ -83,6 +85,30 @@ def cpu_baseline(batch):
             "sample": f"ResNet-50 DFX calibration forward of {batch} images 224x224 "
                       f"(exact CPU oracle, parameters pre-quantized; {t:.1f} s forward, "
                       f"{t0 - t_prep:.1f} s set-up untimed)"}
+
+
+def sweep_figures(dev):
+    """The per-layer sensitivity sweep of ResNet-50 b256 (54 layers x activation
+    WL 8..4 x weight WL 8..2 = 1890 layer evaluations), reported alongside: the
+    FP32 teacher and the weight quantization are set-up; one untimed sweep,
+    then one timed sweep between two synchronizations."""
+    import torch
+    from paper_2203_12091_amd import sweep
+    t0 = time.perf_counter()
+    sw = sweep.Sweep("resnet50", batch=BATCH, image=IMAGE, device=str(dev))
+    torch.cuda.synchronize(dev)
+    setup = time.perf_counter() - t0
+    sw.run()
+    t = sw.timed_run()
+    res = sw.results()
+    if res["flags"]:
+        print(f"bench.py: sweep device flags {res['flags']:#x}", file=sys.stderr)
+        sys.exit(1)
+    steps = len(sw.steps)
+    sw.close()
+    return {"workload": "resnet50_b256_224_sensitivity_sweep", "layer_evaluations": steps,
+            "seconds": round(t, 4), "layer_eval_images_per_s": round(BATCH * steps / t, 1),
+            "setup_seconds_untimed": round(setup, 2)}
 
 
 def main():
@@ -179,6 +205,8 @@ def main():
         out["fused_cblock"] = {"kernel": "k_qconv (min/max, FL-window and requant epilogues)",
                                "passes": cb_n, "ms_per_forward": round(cb_ms, 3),
                                "executed_tops": round(cb_ops / max(cb_ms, 1e-9) * 1e-9, 1)}
+    if not args.no_sweep:
+        out["sweep"] = sweep_figures(dev)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_sample_batch)
     print(json.dumps(out), flush=True)

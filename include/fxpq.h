@@ -297,6 +297,38 @@ fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
  * (device int32), for consumers that need it as a plain FXPQ_SRC_INT scale. */
 fxpq_status fxpq_epilogue_scale(fxpq_handle h, const fxpq_epilogue* ep, int32_t* d_scale);
 
+/* ---- FP32 teacher ---------------------------------------------------------
+ * The full-precision network whose activations are the reference of the
+ * layer error in the per-layer sensitivity sweep (Sec. "Data-Structures
+ * Sensitivity to Quantization"; the full-precision model as teacher, Sec.
+ * "Quantization Parameters Optimization").  Reference data, not the DFX hot
+ * path.  The arithmetic is fixed so that every implementation gets the same
+ * bits: a conv / FC output is the fp64 sum of the fp32 x fp32 products (exact
+ * in fp64) in the order r, s, c with padded taps skipped, rounded once to
+ * fp32; the BN-as-Scale affine is one fp32 fma; a bias one fp32 add; ReLU maps
+ * every value <= 0 to +0.  All tensors are device fp32, activations NHWC.
+ */
+
+/* y[n][oh][ow][k] from x (NHWC) and w_rsck ([r][s][c][k]). */
+fxpq_status fxpq_teacher_conv(fxpq_handle h, const fxpq_conv_desc* d, const float* x,
+                              const float* w_rsck, float* y);
+/* Per channel c = i % channels: y = relu?(fmaf(t, a1[c], a2[c])) when a1 is
+ * given, else relu?(t + bias[c]) when bias is given, else relu?(t).  In place
+ * allowed.  n % channels == 0. */
+fxpq_status fxpq_teacher_affine(fxpq_handle h, const float* t, int64_t n, int32_t channels,
+                                const float* a1, const float* a2, const float* bias,
+                                int32_t relu, float* y);
+/* y = relu?(a + b), one fp32 add (residual connection). */
+fxpq_status fxpq_teacher_add(fxpq_handle h, const float* a, const float* b, int64_t n,
+                             int32_t relu, float* y);
+/* NHWC max-pool; out-of-range taps are skipped. */
+fxpq_status fxpq_teacher_maxpool(fxpq_handle h, const float* x, int32_t n, int32_t hgt,
+                                 int32_t wid, int32_t c, int32_t ksize, int32_t stride,
+                                 int32_t pad, float* y);
+/* Global average of x[n][hw][c]: y[n][c] = (float)(fp64 sum in pixel order / hw). */
+fxpq_status fxpq_teacher_avgpool(fxpq_handle h, const float* x, int32_t n, int32_t hw, int32_t c,
+                                 float* y);
+
 /* ---- measurement --------------------------------------------------------- */
 
 /* Kernels the handle can time with HIP events on its stream. */

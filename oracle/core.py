@@ -46,6 +46,9 @@ def _declare(L):
         "orc_avgpool_global": [p, i, i, i, i64, p],
         "orc_eltwise_add": [p, i, p, i, i64, i, p, p],
         "orc_layer_error": [p, p, i64, i, i, i, p],
+        "orc_teacher_conv2d": [p, i, i, i, i, p, i, i, i, i, i, p],
+        "orc_teacher_affine": [p, i, i, i64, p, p, p, i, p],
+        "orc_teacher_avgpool": [p, i, i, i64, p],
     }
     for name, args in sigs.items():
         f = getattr(L, name)
@@ -226,4 +229,43 @@ def layer_error(ref, codes, k, fl, sign):
     out = np.empty(4, np.float64)
     _check(lib().orc_layer_error(_ptr(ref), _ptr(codes), ref.size, k, fl, sign, _ptr(out)),
            "layer_error")
+    return out
+
+
+# ---- FP32 teacher (reference activations of the sensitivity sweep) ----------
+def teacher_conv2d(x, w, stride, pad):
+    """fp32 conv, NCHW x KCRS -> NKHW: fp64 sum of the exact products in the
+    order r, s, c (padded taps skipped), rounded once to fp32."""
+    x, w = _f32(x), _f32(w)
+    N, Cc, H, W = x.shape
+    K, C2, R, S = w.shape
+    assert C2 == Cc
+    Ho, Wo = conv_out_hw(H, W, R, S, stride, pad)
+    out = np.empty((N, K, Ho, Wo), np.float32)
+    _check(lib().orc_teacher_conv2d(_ptr(x), N, Cc, H, W, _ptr(w), K, R, S, stride, pad,
+                                    _ptr(out)), "teacher_conv2d")
+    return out
+
+
+def teacher_affine(t, a1=None, a2=None, bias=None, relu=False):
+    """Per channel (axis 1): relu?(fmaf(t, a1, a2)) or relu?(t + bias)."""
+    t = _f32(t)
+    N, Cc = t.shape[0], t.shape[1]
+    hw = int(np.prod(t.shape[2:])) if t.ndim > 2 else 1
+    m1 = None if a1 is None else _f32(a1)
+    m2 = None if a2 is None else _f32(a2)
+    b = None if bias is None else _f32(bias)
+    out = np.empty_like(t)
+    _check(lib().orc_teacher_affine(_ptr(t), N, Cc, hw, _ptr(m1), _ptr(m2), _ptr(b),
+                                    int(bool(relu)), _ptr(out)), "teacher_affine")
+    return out
+
+
+def teacher_avgpool(x):
+    """NCHW -> NC: (float)(sequential fp64 sum over h, w / (h * w))."""
+    x = _f32(x)
+    N, Cc = x.shape[:2]
+    hw = int(np.prod(x.shape[2:]))
+    out = np.empty((N, Cc), np.float32)
+    _check(lib().orc_teacher_avgpool(_ptr(x), N, Cc, hw, _ptr(out)), "teacher_avgpool")
     return out

@@ -524,3 +524,62 @@ int orc_layer_error(const float* ref, const int32_t* codes, int64_t n, int k, in
   out[3] = sqrt(var / (double)n);
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------- */
+/* FP32 teacher (reference activations of the sensitivity sweep).            */
+/* ------------------------------------------------------------------------- */
+int orc_teacher_conv2d(const float* x, int N, int C, int H, int W, const float* w, int K, int R,
+                       int S, int stride, int pad, float* y) {
+  if (stride < 1 || pad < 0) return ORC_EINVAL;
+  int Ho = (H + 2 * pad - R) / stride + 1, Wo = (W + 2 * pad - S) / stride + 1;
+  if (Ho < 1 || Wo < 1) return ORC_EINVAL;
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int n = 0; n < N; ++n)
+    for (int k = 0; k < K; ++k)
+      for (int oh = 0; oh < Ho; ++oh)
+        for (int ow = 0; ow < Wo; ++ow) {
+          double acc = 0.0;
+          for (int r = 0; r < R; ++r) {
+            int ih = oh * stride - pad + r;
+            if (ih < 0 || ih >= H) continue;
+            for (int q = 0; q < S; ++q) {
+              int iw = ow * stride - pad + q;
+              if (iw < 0 || iw >= W) continue;
+              for (int c = 0; c < C; ++c) {
+                double prod = (double)x[(((int64_t)n * C + c) * H + ih) * W + iw] *
+                              (double)w[(((int64_t)k * C + c) * R + r) * S + q];
+                acc = acc + prod;
+              }
+            }
+          }
+          y[(((int64_t)n * K + k) * Ho + oh) * Wo + ow] = (float)acc;
+        }
+  return ORC_OK;
+}
+
+int orc_teacher_affine(const float* t, int N, int C, int64_t hw, const float* a1,
+                       const float* a2, const float* bias, int relu, float* y) {
+  if (N < 0 || C < 1 || hw < 0 || (a1 && !a2)) return ORC_EINVAL;
+  for (int64_t n = 0; n < N; ++n)
+    for (int c = 0; c < C; ++c)
+      for (int64_t p = 0; p < hw; ++p) {
+        int64_t i = ((int64_t)n * C + c) * hw + p;
+        float v = t[i];
+        if (a1) v = fmaf(v, a1[c], a2[c]);
+        else if (bias) v = v + bias[c];
+        if (relu) v = v > 0.0f ? v : 0.0f;
+        y[i] = v;
+      }
+  return ORC_OK;
+}
+
+int orc_teacher_avgpool(const float* x, int N, int C, int64_t hw, float* y) {
+  if (N < 0 || C < 1 || hw < 1) return ORC_EINVAL;
+  for (int64_t n = 0; n < N; ++n)
+    for (int c = 0; c < C; ++c) {
+      double acc = 0.0;
+      for (int64_t p = 0; p < hw; ++p) acc = acc + (double)x[((int64_t)n * C + c) * hw + p];
+      y[(int64_t)n * C + c] = (float)(acc / (double)hw);
+    }
+  return ORC_OK;
+}

@@ -99,6 +99,27 @@ int orc_eltwise_add(const int32_t* a, int fa, const int32_t* b, int fb, int64_t 
 int orc_layer_error(const float* ref, const int32_t* codes, int64_t n, int k, int fl, int sign,
                     double out[4]);
 
+/* ---- FP32 teacher ----------------------------------------------------------
+ * The full-precision network whose activations are the reference of the
+ * layer error in the per-layer sensitivity sweep (Sec. "Data-Structures
+ * Sensitivity to Quantization": one layer quantized, the others intact; the
+ * full-precision model as teacher, Sec. "Quantization Parameters
+ * Optimization").  Its arithmetic is fixed so that any implementation gets
+ * the same bits: a conv / FC output is the fp64 sum of the fp32 x fp32
+ * products (exact in fp64) taken in the order r, s, c with padded taps
+ * skipped, rounded once to fp32; the BN-as-Scale affine is one fp32 fma; the
+ * bias one fp32 add; ReLU maps every value <= 0 to +0. */
+
+/* NCHW x KCRS -> NKHW fp32. */
+int orc_teacher_conv2d(const float* x, int N, int C, int H, int W, const float* w, int K, int R,
+                       int S, int stride, int pad, float* y);
+/* Per channel c of NCHW t (hw pixels per channel): y = relu?(fmaf(t, a1[c], a2[c]))
+ * when a1 is given, else relu?(t + bias[c]) when bias is given, else relu?(t). */
+int orc_teacher_affine(const float* t, int N, int C, int64_t hw, const float* a1,
+                       const float* a2, const float* bias, int relu, float* y);
+/* Global average: y[n][c] = (float)(sequential fp64 sum over hw / hw). */
+int orc_teacher_avgpool(const float* x, int N, int C, int64_t hw, float* y);
+
 #ifdef __cplusplus
 }
 #endif

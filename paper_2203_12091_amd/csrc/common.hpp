@@ -172,5 +172,15 @@ hipError_t launch_avgpool(const Ctx& c, const int8_t* x, int dtype, const fxpq_f
 hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes, int code_type,
                               const fxpq_fmt* fmt, int64_t n, double* out);
 hipError_t launch_epi_scale(const Ctx& c, const SrcDev& s, int32_t* out);
+hipError_t launch_teacher_conv(const Ctx& c, const fxpq_conv_desc& d, const float* x,
+                               const float* w, float* y);
+hipError_t launch_teacher_affine(const Ctx& c, const float* t, int64_t n, int channels,
+                                 const float* a1, const float* a2, const float* bias, int relu,
+                                 float* y);
+hipError_t launch_teacher_add(const Ctx& c, const float* a, const float* b, int64_t n, int relu,
+                              float* y);
+hipError_t launch_teacher_maxpool(const Ctx& c, const float* x, int n, int h, int w, int ch,
+                                  int ks, int stride, int pad, float* y);
+hipError_t launch_teacher_avgpool(const Ctx& c, const float* x, int n, int hw, int ch, float* y);
 
 }  // namespace fxpq

@@ -414,6 +414,52 @@ fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
   return hip_status(launch_layer_error(ctx(h), ref, codes, code_type, d_fmt, n, d_out));
 }
 
+fxpq_status fxpq_teacher_conv(fxpq_handle h, const fxpq_conv_desc* d, const float* x,
+                              const float* w_rsck, float* y) {
+  if (!h || !d || !x || !w_rsck || !y) return FXPQ_ERR_INVALID_ARG;
+  if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
+      d->stride < 1 || d->pad < 0)
+    return FXPQ_ERR_INVALID_ARG;
+  if (d->h + 2 * d->pad < d->r || d->w + 2 * d->pad < d->s) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_teacher_conv(ctx(h), *d, x, w_rsck, y));
+}
+
+fxpq_status fxpq_teacher_affine(fxpq_handle h, const float* t, int64_t n, int32_t channels,
+                                const float* a1, const float* a2, const float* bias,
+                                int32_t relu, float* y) {
+  if (!h || !t || !y || n < 0 || channels < 1 || n % channels != 0 || (a1 && !a2))
+    return FXPQ_ERR_INVALID_ARG;
+  if (n == 0) return FXPQ_OK;
+  DeviceGuard g(h->device);
+  return hip_status(launch_teacher_affine(ctx(h), t, n, channels, a1, a2, bias, relu ? 1 : 0, y));
+}
+
+fxpq_status fxpq_teacher_add(fxpq_handle h, const float* a, const float* b, int64_t n,
+                             int32_t relu, float* y) {
+  if (!h || !a || !b || !y || n < 0) return FXPQ_ERR_INVALID_ARG;
+  if (n == 0) return FXPQ_OK;
+  DeviceGuard g(h->device);
+  return hip_status(launch_teacher_add(ctx(h), a, b, n, relu ? 1 : 0, y));
+}
+
+fxpq_status fxpq_teacher_maxpool(fxpq_handle h, const float* x, int32_t n, int32_t hgt,
+                                 int32_t wid, int32_t c, int32_t ksize, int32_t stride,
+                                 int32_t pad, float* y) {
+  if (!h || !x || !y || n < 1 || hgt < 1 || wid < 1 || c < 1 || ksize < 1 || stride < 1 ||
+      pad < 0 || pad >= ksize || hgt + 2 * pad < ksize || wid + 2 * pad < ksize)
+    return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_teacher_maxpool(ctx(h), x, n, hgt, wid, c, ksize, stride, pad, y));
+}
+
+fxpq_status fxpq_teacher_avgpool(fxpq_handle h, const float* x, int32_t n, int32_t hw, int32_t c,
+                                 float* y) {
+  if (!h || !x || !y || n < 1 || hw < 1 || c < 1) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_teacher_avgpool(ctx(h), x, n, hw, c, y));
+}
+
 fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind) {
   if (!h || kind < FXPQ_TIMER_OFF || kind > FXPQ_TIMER_CBLOCK_PASS) return FXPQ_ERR_INVALID_ARG;
   DeviceGuard g(h->device);

@@ -23,6 +23,8 @@ EXPORTS = [
     "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_cblock", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
+    "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
+    "fxpq_teacher_avgpool",
 ]
 TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT, TIMER_CBLOCK_PASS = range(5)
 
@@ -87,6 +89,11 @@ def lib():
             "fxpq_epilogue_scale": [p, p, p],
             "fxpq_timer_start": [p, C.c_int],
             "fxpq_timer_read": [p, p, p, p],
+            "fxpq_teacher_conv": [p, p, p, p, p],
+            "fxpq_teacher_affine": [p, p, i64, i32, p, p, p, i32, p],
+            "fxpq_teacher_add": [p, p, p, i64, i32, p],
+            "fxpq_teacher_maxpool": [p, p, i32, i32, i32, i32, i32, i32, i32, p],
+            "fxpq_teacher_avgpool": [p, p, i32, i32, i32, p],
         }
         for name, args in sig.items():
             f = getattr(L, name)
@@ -214,6 +221,27 @@ def layer_error(h, ref, codes, code_type, d_fmt, n, d_out):
 
 def epilogue_scale(h, ep, d_scale):
     _call("fxpq_epilogue_scale", h.value, C.byref(ep), ptr(d_scale))
+
+
+def teacher_conv(h, desc, x, w_rsck, y):
+    _call("fxpq_teacher_conv", h.value, C.byref(desc), ptr(x), ptr(w_rsck), ptr(y))
+
+
+def teacher_affine(h, t, n, channels, y, a1=None, a2=None, bias=None, relu=False):
+    _call("fxpq_teacher_affine", h.value, ptr(t), n, channels, ptr(a1), ptr(a2), ptr(bias),
+          int(relu), ptr(y))
+
+
+def teacher_add(h, a, b, n, relu, y):
+    _call("fxpq_teacher_add", h.value, ptr(a), ptr(b), n, int(relu), ptr(y))
+
+
+def teacher_maxpool(h, x, n, hgt, wid, c, ksize, stride, pad, y):
+    _call("fxpq_teacher_maxpool", h.value, ptr(x), n, hgt, wid, c, ksize, stride, pad, ptr(y))
+
+
+def teacher_avgpool(h, x, n, hw, c, y):
+    _call("fxpq_teacher_avgpool", h.value, ptr(x), n, hw, c, ptr(y))
 
 
 def timer_start(h, kind):
