@@ -26,8 +26,6 @@
 
 namespace fxpq {
 
-int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec);
-
 // Main loop of the streaming window pass over this thread's values.
 template <int KIND, int DT, bool NONNEG, bool CLAMP0>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
@@ -413,7 +411,10 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
   int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
   const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;  // Pack<>::V
-  const int blocks = stream_grid(n, channels, kWinMaxPerThread, vec);
+  int resident = 0;
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (resident = resident_blocks(c, (const void*)&k_fls_window<K_, D_>)));
+  const int blocks = stream_grid(n, channels, kWinMaxPerThread, vec, resident);
   const int64_t per_thread = window_per_thread(n, blocks, vec);
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   int mode = d_sse ? MODE_REPORT : MODE_SEARCH;

@@ -5,6 +5,9 @@
 // channels fixed (see values.hpp).
 #include <math.h>
 
+#include <mutex>
+#include <unordered_map>
+
 #include "values.hpp"
 
 namespace fxpq {
@@ -21,13 +24,36 @@ static int64_t gcd64(int64_t a, int64_t b) {
   return a;
 }
 
-int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec) {
+int resident_blocks(const Ctx& c, const void* kernel) {
+  static std::mutex mu;
+  static std::unordered_map<const void*, int> per_cu;
+  int b = 0;
+  {
+    std::lock_guard<std::mutex> lock(mu);
+    auto it = per_cu.find(kernel);
+    if (it != per_cu.end()) {
+      b = it->second;
+    } else {
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kernel, kThreads, 0) != hipSuccess) b = 0;
+      per_cu[kernel] = b;
+    }
+  }
+  return b > 0 ? b * c.cus : 0;
+}
+
+// One block per kThreads groups of `vec` values, capped at one full round of
+// resident blocks (the grid-stride loop covers the rest: a partial second
+// round would leave most of the chip idle at its end).  When a bound on the
+// values per thread asks for more blocks, whole rounds.  Then rounded so the
+// grid stride is a multiple of `channels`.
+int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec, int resident) {
+  const int64_t cap = resident > 0 ? resident : kMaxStreamBlocks;
   int64_t groups = (n + vec - 1) / vec;
   int64_t blocks = (groups + kThreads - 1) / kThreads;
-  if (blocks > kMaxStreamBlocks) blocks = kMaxStreamBlocks;
+  if (blocks > cap) blocks = cap;
   if (max_per_thread > 0) {
     int64_t need = (n + (int64_t)kThreads * max_per_thread - 1) / ((int64_t)kThreads * max_per_thread);
-    if (need > blocks) blocks = need;
+    if (need > blocks) blocks = (need + cap - 1) / cap * cap;
   }
   if (blocks < 1) blocks = 1;
   if (channels > 0) {
@@ -344,9 +370,11 @@ static int src_vec(const SrcDev& s) {
 }  // values per thread per block iteration (Pack<>::V)
 
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) {
-  int blocks = stream_grid(n, src_channels(s), 0, src_vec(s));
+  int blocks = 1;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(s, n, c.sc.minmax_part,
+                    (blocks = stream_grid(n, src_channels(s), 0, src_vec(s),
+                                          resident_blocks(c, (const void*)&k_minmax<K_, D_>)),
+                     k_minmax<K_, D_><<<blocks, kThreads, 0, c.stream>>>(s, n, c.sc.minmax_part,
                                                                         c.sc.flags)));
   k_minmax_fin<<<1, kMmFinThreads, 0, c.stream>>>(c.sc.minmax_part, blocks, out);
   return hipGetLastError();
@@ -413,25 +441,27 @@ __global__ __launch_bounds__(kThreads) void k_requant_addmm(SrcDev s, int64_t n,
 }
 
 template <int OUT>
-static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
-                        int blocks) {
+static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
+                        void* codes) {
+  int blocks = 1;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (k_requant<K_, D_, OUT><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes,
+                    (blocks = stream_grid(n, src_channels(s), 0, src_vec(s),
+                                          resident_blocks(c, (const void*)&k_requant<K_, D_, OUT>)),
+                     k_requant<K_, D_, OUT><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes,
                                                                              c.sc.flags)));
 }
 
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
                           void* codes, int code_type) {
-  int blocks = stream_grid(n, src_channels(s), 0, src_vec(s));
   const double in_b = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
   const double out_b = (code_type == FXPQ_I32) ? 4.0 : (code_type == FXPQ_I16 ? 2.0 : 1.0);
   bool timed = timer_begin(c, FXPQ_TIMER_REQUANT);
   switch (code_type) {
-    case FXPQ_I8: requant_out<FXPQ_I8>(c, s, n, fmt, codes, blocks); break;
-    case FXPQ_U8OFF: requant_out<FXPQ_U8OFF>(c, s, n, fmt, codes, blocks); break;
-    case FXPQ_C8: requant_out<FXPQ_C8>(c, s, n, fmt, codes, blocks); break;
-    case FXPQ_I16: requant_out<FXPQ_I16>(c, s, n, fmt, codes, blocks); break;
-    default: requant_out<FXPQ_I32>(c, s, n, fmt, codes, blocks); break;
+    case FXPQ_I8: requant_out<FXPQ_I8>(c, s, n, fmt, codes); break;
+    case FXPQ_U8OFF: requant_out<FXPQ_U8OFF>(c, s, n, fmt, codes); break;
+    case FXPQ_C8: requant_out<FXPQ_C8>(c, s, n, fmt, codes); break;
+    case FXPQ_I16: requant_out<FXPQ_I16>(c, s, n, fmt, codes); break;
+    default: requant_out<FXPQ_I32>(c, s, n, fmt, codes); break;
   }
   timer_end(c, timed, (in_b + out_b) * (double)n);
   return hipGetLastError();
@@ -440,22 +470,20 @@ hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_f
 hipError_t launch_requant_addmm(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
                                 void* codes, int code_type, const int8_t* b, int b_type,
                                 const fxpq_fmt* fmt_b, int relu, double* d_add_minmax) {
-  int blocks = stream_grid(n, src_channels(s), 0, src_vec(s));
   bool timed = timer_begin(c, FXPQ_TIMER_REQUANT);
   double* part = c.sc.minmax_part;
+  auto run = [&](auto kernel) {
+    const int blocks = stream_grid(n, src_channels(s), 0, src_vec(s),
+                                   resident_blocks(c, (const void*)kernel));
+    kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type, fmt_b, relu, part,
+                                              c.sc.flags);
+    return blocks;
+  };
+  int blocks;
   switch (code_type) {
-    case FXPQ_I8:
-      k_requant_addmm<FXPQ_I8><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type,
-                                                                  fmt_b, relu, part, c.sc.flags);
-      break;
-    case FXPQ_U8OFF:
-      k_requant_addmm<FXPQ_U8OFF><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type,
-                                                                     fmt_b, relu, part, c.sc.flags);
-      break;
-    default:
-      k_requant_addmm<FXPQ_C8><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes, b, b_type,
-                                                                  fmt_b, relu, part, c.sc.flags);
-      break;
+    case FXPQ_I8: blocks = run(&k_requant_addmm<FXPQ_I8>); break;
+    case FXPQ_U8OFF: blocks = run(&k_requant_addmm<FXPQ_U8OFF>); break;
+    default: blocks = run(&k_requant_addmm<FXPQ_C8>); break;
   }
   timer_end(c, timed, 6.0 * (double)n);
   return launch_minmax_fin(c, part, blocks, d_add_minmax);
@@ -463,24 +491,19 @@ hipError_t launch_requant_addmm(const Ctx& c, const SrcDev& s, int64_t n, const 
 
 hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes, int code_type,
                               const fxpq_fmt* fmt, int64_t n, double* out) {
-  int blocks = stream_grid(n, 0, 0, 4);
   double* part = c.sc.minmax_part;  // 5 doubles per block fits (kMaxConvBlocks * 2)
+  auto run = [&](auto kernel) {
+    const int blocks = stream_grid(n, 0, 0, 4, resident_blocks(c, (const void*)kernel));
+    kernel<<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
+    return blocks;
+  };
+  int blocks;
   switch (code_type) {
-    case FXPQ_I16:
-      k_layer_error<FXPQ_I16><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
-      break;
-    case FXPQ_I32:
-      k_layer_error<FXPQ_I32><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
-      break;
-    case FXPQ_U8OFF:
-      k_layer_error<FXPQ_U8OFF><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
-      break;
-    case FXPQ_C8:
-      k_layer_error<FXPQ_C8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
-      break;
-    default:
-      k_layer_error<FXPQ_I8><<<blocks, kThreads, 0, c.stream>>>(ref, codes, fmt, n, part);
-      break;
+    case FXPQ_I16: blocks = run(&k_layer_error<FXPQ_I16>); break;
+    case FXPQ_I32: blocks = run(&k_layer_error<FXPQ_I32>); break;
+    case FXPQ_U8OFF: blocks = run(&k_layer_error<FXPQ_U8OFF>); break;
+    case FXPQ_C8: blocks = run(&k_layer_error<FXPQ_C8>); break;
+    default: blocks = run(&k_layer_error<FXPQ_I8>); break;
   }
   k_layer_error_fin<<<1, kThreads, 0, c.stream>>>(part, blocks, n, out);
   return hipGetLastError();
