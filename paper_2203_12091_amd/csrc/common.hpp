@@ -84,13 +84,36 @@ __device__ inline EpiU epi_uniform(const SrcDev& s) {
   return u;
 }
 
+// Per-channel epilogue codes (Scale multiplier, bias, Scale addend) of channel
+// c; 1 / 0 / 0 where the epilogue has none.  The loads are unconditional
+// (absent operands read a constant) so that no wait follows them.
+struct EpiRaw {
+  int32_t sc, b, sh;
+};
+
+__device__ int32_t kEpiOne = 1;  // never written
+__device__ int32_t kEpiZero = 0;  // never written
+
+__device__ inline EpiRaw epi_channel_load(const SrcDev& s, int c) {
+  EpiRaw r;
+  r.sc = *(s.scale ? s.scale + c : &kEpiOne);
+  r.b = *(s.bias ? s.bias + c : &kEpiZero);
+  r.sh = *(s.shift ? s.shift + c : &kEpiZero);
+  return r;
+}
+
 // Per-channel multiplier and addend: v = relu(acc * M + A), exact while |v| < 2^53.
-__device__ inline void epi_channel(const SrcDev& s, const EpiU& u, int c, double& M, double& A) {
-  double sc = s.scale ? (double)s.scale[c] : 1.0;
+__device__ inline void epi_channel_raw(const SrcDev& s, const EpiU& u, const EpiRaw& r, double& M,
+                                       double& A) {
+  const double sc = (double)r.sc;
   M = ldexp(sc, u.sh_acc + u.sh_mid);
-  double a = s.bias ? ldexp((double)s.bias[c], u.sh_bias + u.sh_mid) * sc : 0.0;
-  if (s.shift) a += ldexp((double)s.shift[c], u.sh_shift);
+  double a = s.bias ? ldexp((double)r.b, u.sh_bias + u.sh_mid) * sc : 0.0;
+  if (s.shift) a += ldexp((double)r.sh, u.sh_shift);
   A = a;
+}
+
+__device__ inline void epi_channel(const SrcDev& s, const EpiU& u, int c, double& M, double& A) {
+  epi_channel_raw(s, u, epi_channel_load(s, c), M, A);
 }
 
 // Fractional length of the values described by s.

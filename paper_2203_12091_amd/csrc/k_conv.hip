@@ -77,7 +77,7 @@ struct ConvArgs {
 constexpr int kConvPerThread = 64;  // accumulators per thread (BM * BN / 256)
 
 template <int BM, int BN, int LOADER, int EPI>
-__global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
+__global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
   constexpr int WN = BN / 64;   // waves along N
   constexpr int ACH = BM / 64;  // A chunks (16 B) per thread per slab
   constexpr int BCH = BN / 64;
@@ -108,14 +108,16 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
     if (!qf.ok) return;
   }
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int wm = wave / WN, wn = wave % WN;
   const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
   const int kc = tid & 3;
 
-  int a_off = 0;
-  if (a.x_type == FXPQ_U8OFF) a_off = 1;
-  else if (a.x_type == FXPQ_C8) a_off = (a.has_ep && a.ep.fin->sign == 0) ? 1 : 0;
+  // Inputs stored as u - 128 (branch-free, so the operand loads need not wait
+  // for the format).
+  const int fin_sign = *(a.has_ep ? &a.ep.fin->sign : &kEpiOne);
+  const int a_off = (a.x_type == FXPQ_U8OFF) || (a.x_type == FXPQ_C8 && fin_sign == 0);
   const int padw = a_off ? (int)0x80808080 : 0;
   const v4i padv = {padw, padw, padw, padw};
 
@@ -158,8 +160,9 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
       for (int i = 0; i < ACH; ++i) {
         int ih = ih0[i] + r, iw = iw0[i] + s;
         bool ok = aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-        const int8_t* p = abase[i] + ((int64_t)ih * a.W + iw) * a.C + c0 + kc * 16;
-        regA[i] = ok ? *reinterpret_cast<const v4i*>(p) : padv;
+        const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 + kc * 16 : 0);
+        const v4i t = *reinterpret_cast<const v4i*>(p);
+        regA[i] = ok ? t : padv;
       }
     } else if constexpr (LOADER == LD_GEN16) {
       int k = k0 + kc * 16;
@@ -170,8 +173,9 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
       for (int i = 0; i < ACH; ++i) {
         int ih = ih0[i] + r, iw = iw0[i] + s;
         bool ok = kin && aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-        const int8_t* p = abase[i] + ((int64_t)ih * a.W + iw) * a.C + c0;
-        regA[i] = ok ? *reinterpret_cast<const v4i*>(p) : padv;
+        const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 : 0);
+        const v4i t = *reinterpret_cast<const v4i*>(p);
+        regA[i] = ok ? t : padv;
       }
     } else {  // LD_RGB4: four 4-byte pixels per 16-byte chunk
 #pragma unroll
@@ -194,11 +198,10 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
     }
 #pragma unroll
     for (int i = 0; i < BCH; ++i) {
-      int k = k0 + kc * 16;
-      if (LOADER == LD_GEN16 && k >= a.kdepth)
-        regB[i] = v4i{0, 0, 0, 0};
-      else
-        regB[i] = *reinterpret_cast<const v4i*>(bptr[i] + k);
+      const int k = k0 + kc * 16;
+      const bool kin = LOADER != LD_GEN16 || k < a.kdepth;
+      const v4i t = *reinterpret_cast<const v4i*>(bptr[i] + (kin ? k : 0));
+      regB[i] = kin ? t : v4i{0, 0, 0, 0};
     }
   };
   auto lstore = [&](int buf) {
@@ -220,6 +223,18 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
 
   const int ktiles = (a.kdepth + BK - 1) / BK;
   gload(0);
+  // Per-channel epilogue operands of this thread's two output columns, loaded
+  // before the main loop so that their latency overlaps it.
+  const bool want_vals = (EPI != EPI_ACC) || a.want_mm;
+  int csum[2];
+  EpiRaw eraw[2];
+#pragma unroll
+  for (int ni = 0; ni < 2; ++ni) {
+    const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
+    const int cc = col < a.K ? col : a.K - 1;
+    csum[ni] = *(a_off ? a.colsum + cc : &kEpiZero);
+    if (want_vals) eraw[ni] = epi_channel_load(a.ep, cc);
+  }
   lstore(0);
   __syncthreads();
   for (int kt = 0; kt < ktiles; ++kt) {
@@ -249,23 +264,22 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
   // ---- epilogue ----
   // Visits this thread's in-range accumulators (restored for u - 128 inputs)
   // with the channel's epilogue constants.
-  const bool want_vals = (EPI != EPI_ACC) || a.want_mm;
   EpiU eu;
   if (want_vals) eu = epi_uniform(a.ep);
+  const bool full = m0 + BM <= a.M && n0 + BN <= a.K;
   auto visit = [&](auto&& f) {
 #pragma unroll
     for (int ni = 0; ni < 2; ++ni) {
       const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
-      const int cc = col < a.K ? col : a.K - 1;
-      const int corr = a_off ? 128 * a.colsum[cc] : 0;
+      const int corr = 128 * csum[ni];
       double Mc = 1.0, Ac = 0.0;
-      if (want_vals) epi_channel(a.ep, eu, cc, Mc, Ac);
+      if (want_vals) epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
 #pragma unroll
       for (int mi = 0; mi < 2; ++mi) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
           const int row = m0 + wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-          if (row < a.M && col < a.K) f(acc[mi][ni][e] + corr, Mc, Ac, row, col);
+          if (full || (row < a.M && col < a.K)) f(acc[mi][ni][e] + corr, Mc, Ac, row, col);
         }
       }
     }
@@ -274,16 +288,71 @@ __global__ __launch_bounds__(256) void k_qconv(ConvArgs a) {
   const int bid = blockIdx.y * gridDim.x + blockIdx.x;
 
   if constexpr (EPI == EPI_ACC || EPI == EPI_MM) {
-    double mn = INFINITY, mx = -INFINITY;
-    visit([&](int v, double Mc, double Ac, int row, int col) {
-      if (EPI == EPI_ACC) a.acc[(int64_t)row * a.K + col] = v;
-      if (want_vals) {
-        const double val = fmax(fma((double)v, Mc, Ac), relo);
-        mn = fmin(mn, val);
-        mx = fmax(mx, val);
+    // The epilogue value is a monotonic function of the accumulator within a
+    // channel (v = relu(acc * M + A), rounding included), so the min / max of
+    // the values are those of the channel's extreme accumulators: track the
+    // integer extremes per column, evaluate the epilogue on them only.
+    int lo[2] = {INT_MAX, INT_MAX}, hi[2] = {INT_MIN, INT_MIN};
+    if (full) {
+      // Full tile: buffer stores with the row offset in a scalar register.
+      __amdgpu_buffer_rsrc_t rs;
+      int vo[2];
+      if constexpr (EPI == EPI_ACC) {
+        rs = __builtin_amdgcn_make_buffer_rsrc(a.acc + (int64_t)(m0 + wm * 64) * a.K, (short)0,
+                                               0x7fffffff, 0x00020000);
+#pragma unroll
+        for (int ni = 0; ni < 2; ++ni)
+          vo[ni] = (4 * (lane >> 5) * a.K + n0 + wn * 64 + ni * 32 + (lane & 31)) * 4;
       }
-    });
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        const int corr = 128 * csum[ni];
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int v = acc[mi][ni][e];
+            if constexpr (EPI == EPI_ACC)
+              __builtin_amdgcn_raw_buffer_store_b32(
+                  v + corr, rs, vo[ni], (mi * 32 + 8 * (e >> 2) + (e & 3)) * a.K * 4, 0);
+            lo[ni] = min(lo[ni], v);
+            hi[ni] = max(hi[ni], v);
+          }
+        }
+      }
+    } else {
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni) {
+        const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
+        const int corr = 128 * csum[ni];
+#pragma unroll
+        for (int mi = 0; mi < 2; ++mi) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int row = m0 + wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            if (row < a.M && col < a.K) {
+              const int v = acc[mi][ni][e];
+              if constexpr (EPI == EPI_ACC) a.acc[(int64_t)row * a.K + col] = v + corr;
+              lo[ni] = min(lo[ni], v);
+              hi[ni] = max(hi[ni], v);
+            }
+          }
+        }
+      }
+    }
     if (!want_vals) return;
+    double mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) {
+      if (lo[ni] > hi[ni]) continue;  // no in-range value in this column
+      double Mc, Ac;
+      epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
+      const int corr = 128 * csum[ni];
+      const double f0 = fmax(fma((double)(lo[ni] + corr), Mc, Ac), relo);
+      const double f1 = fmax(fma((double)(hi[ni] + corr), Mc, Ac), relo);
+      mn = fmin(mn, fmin(f0, f1));
+      mx = fmax(mx, fmax(f0, f1));
+    }
     mn = block_reduce(mn, OpMin(), shd);
     mx = block_reduce(mx, OpMax(), shd);
     if (tid == 0) {
