@@ -10,7 +10,9 @@ SOURCES = ["fxpq_api.hip", "k_stream.hip", "k_flsearch.hip", "k_conv.hip", "k_te
 
 
 def build(verbose: bool = False) -> str:
-    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
+    # -z defs: an undefined symbol (e.g. a kernel stub the host pass did not
+    # emit) fails the build instead of the first dlopen
+    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wl,-z,defs",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
            "-I" + os.path.join(ROOT, "include"), "-o", LIB + ".tmp"]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]

@@ -38,9 +38,43 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 64;
-constexpr int LDS_STRIDE = 80;  // bytes per staged row: 64 + 16 to spread LDS banks
 
-enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2 };
+// LDS slab layout: rows of 64 bytes (four 16-byte chunks), no padding; chunk
+// c of row r sits at chunk position c ^ f(r).  With f(r) = ((r >> 1) ^ (r >> 3))
+// & 3 the eight (or sixteen) lanes served together by a 16-byte LDS access --
+// consecutive rows of one chunk on the MFMA operand reads, or two (four) full
+// rows on the stores -- touch distinct banks.
+__device__ inline int lds_off(int row, int chunk) {
+  return row * 64 + ((chunk ^ ((row >> 1) ^ (row >> 3))) & 3) * 16;
+}
+
+// FAST64: C % 64 == 0, register-staged slabs; GEN16: C % 16 == 0; RGB4: the
+// 4-channel padded input; DMA64: C % 64 == 0, slabs loaded straight into a
+// three-stage LDS ring (global_load_lds), two slabs in flight.
+enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2, LD_DMA64 = 3 };
+
+// 16-byte padding sources of the LDS-ring loader: code 0, and code -128 for
+// inputs stored as u - 128 (both the value 0).
+__device__ int4 kPadVec[2] = {{0, 0, 0, 0},
+                              {(int)0x80808080, (int)0x80808080, (int)0x80808080, (int)0x80808080}};
+
+// s_waitcnt immediate that waits until at most n vector memory operations are
+// outstanding (gfx9 encoding: vmcnt split over bits 3:0 and 15:14; expcnt and
+// lgkmcnt left at their maxima, i.e. not waited for).
+template <int N>
+__device__ inline void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Workgroup barrier without the memory fence __syncthreads() adds: that fence
+// would wait for every outstanding LDS-ring load.  The empty asm statements
+// keep the compiler from moving memory accesses across it.
+__device__ inline void ring_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
 enum Epi { EPI_ACC = 0, EPI_MM = 1, EPI_WIN = 2, EPI_REQ = 3 };
 
 struct ConvArgs {
@@ -74,15 +108,29 @@ struct ConvArgs {
   int y_type;
 };
 
-constexpr int kConvPerThread = 64;  // accumulators per thread (BM * BN / 256)
+// Tile configurations: block BM x BN, four waves of (32 TM) x (32 TN), MINW
+// waves per SIMD requested from the register allocator.
+enum TileCfg { TC_256x64 = 0, TC_128x128 = 1, TC_256x128 = 2 };
 
-template <int BM, int BN, int LOADER, int EPI>
-__global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
-  constexpr int WN = BN / 64;   // waves along N
+// Accumulators per thread of a configuration (the per-thread bound of the
+// fused window epilogue).
+constexpr int conv_per_thread(int cfg) { return cfg == TC_256x128 ? 128 : 64; }
+
+template <int BM, int BN, int TM, int TN, int MINW, int LOADER, int EPI>
+__global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
+  constexpr int WGN = BN / (32 * TN);  // waves along N
+  static_assert((BM / (32 * TM)) * WGN == 4, "four waves per block");
+  constexpr int WROWS = 32 * TM, WCOLS = 32 * TN;
+  constexpr int PER_THREAD = TM * TN * 16;
   constexpr int ACH = BM / 64;  // A chunks (16 B) per thread per slab
   constexpr int BCH = BN / 64;
-  __shared__ __attribute__((aligned(16))) int8_t As[2][BM * LDS_STRIDE];
-  __shared__ __attribute__((aligned(16))) int8_t Bs[2][BN * LDS_STRIDE];
+  // LDS slabs: two stages for the register-staged loaders; the ring of the
+  // DMA loader is declared with it (one array per stage, so that the compiler
+  // sees which stage a read touches and does not wait for the other stages'
+  // loads in flight).
+  constexpr int NST = (LOADER == LD_DMA64) ? 1 : 2;
+  __shared__ __attribute__((aligned(16))) int8_t As[NST][BM * 64];
+  __shared__ __attribute__((aligned(16))) int8_t Bs[NST][BN * 64];
   __shared__ int rs_tab[128];
   __shared__ double shd[8];
   __shared__ long long shl[8];
@@ -94,7 +142,7 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
     if (a.only_if_general && (!a.plan_in->need_general || a.plan_in->status)) return;
   } else if constexpr (EPI == EPI_WIN) {
     ws = win_setup<FXPQ_SRC_ACC>(a.ep, a.mm, a.wl, a.sign_req, a.fl_lo, a.fl_hi, MODE_SEARCH,
-                                 kConvPerThread);
+                                 PER_THREAD);
     if (ws.verdict != 0) {
       if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
         win_verdict_write(ws, a.wl, a.fl_lo, a.fl_hi, a.plan, a.fmt_win, a.flags);
@@ -110,7 +158,7 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
-  const int wm = wave / WN, wn = wave % WN;
+  const int wm = wave / WGN, wn = wave % WGN;
   const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
   const int kc = tid & 3;
 
@@ -126,139 +174,227 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
     __syncthreads();
   }
 
-  // Rows owned by this thread for A loads.
-  const int8_t* abase[ACH];
-  int ih0[ACH], iw0[ACH];
-  bool aval[ACH];
-  const int hw_out = a.Ho * a.Wo;
+  v16i acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < ACH; ++i) {
-    int row = m0 + (tid >> 2) + 64 * i;
-    aval[i] = row < a.M;
-    int rr = aval[i] ? row : a.M - 1;
-    int n = rr / hw_out, rem = rr - n * hw_out;
-    int oh = rem / a.Wo, ow = rem - oh * a.Wo;
-    ih0[i] = oh * a.stride - a.pad;
-    iw0[i] = ow * a.stride - a.pad;
-    abase[i] = a.x + (int64_t)n * a.H * a.W * a.C;
-  }
-  const int8_t* bptr[BCH];
+  for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-  for (int i = 0; i < BCH; ++i) {
-    int col = n0 + (tid >> 2) + 64 * i;
-    int cc = col < a.K ? col : a.K - 1;
-    bptr[i] = a.w + (int64_t)cc * a.wrow;
-  }
-
-  v4i regA[ACH], regB[BCH];
-  auto gload = [&](int kt) {
-    const int k0 = kt * BK;
-    if constexpr (LOADER == LD_FAST64) {
-      int rs = k0 / a.C, c0 = k0 - rs * a.C;
-      int r = rs / a.S, s = rs - r * a.S;
-#pragma unroll
-      for (int i = 0; i < ACH; ++i) {
-        int ih = ih0[i] + r, iw = iw0[i] + s;
-        bool ok = aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-        const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 + kc * 16 : 0);
-        const v4i t = *reinterpret_cast<const v4i*>(p);
-        regA[i] = ok ? t : padv;
-      }
-    } else if constexpr (LOADER == LD_GEN16) {
-      int k = k0 + kc * 16;
-      int rs = k / a.C, c0 = k - rs * a.C;
-      int r = rs / a.S, s = rs - r * a.S;
-      bool kin = k < a.kdepth;
-#pragma unroll
-      for (int i = 0; i < ACH; ++i) {
-        int ih = ih0[i] + r, iw = iw0[i] + s;
-        bool ok = kin && aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
-        const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 : 0);
-        const v4i t = *reinterpret_cast<const v4i*>(p);
-        regA[i] = ok ? t : padv;
-      }
-    } else {  // LD_RGB4: four 4-byte pixels per 16-byte chunk
-#pragma unroll
-      for (int i = 0; i < ACH; ++i) {
-        v4i v;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          int rs = (k0 + kc * 16 + 4 * j) >> 2;
-          int t = (rs < 128) ? rs_tab[rs] : -1;
-          int word = padw;
-          if (t >= 0 && aval[i]) {
-            int ih = ih0[i] + (t >> 16), iw = iw0[i] + (t & 0xFFFF);
-            if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
-              word = *reinterpret_cast<const int*>(abase[i] + ((int64_t)ih * a.W + iw) * 4);
-          }
-          v[j] = word;
-        }
-        regA[i] = v;
-      }
-    }
-#pragma unroll
-    for (int i = 0; i < BCH; ++i) {
-      const int k = k0 + kc * 16;
-      const bool kin = LOADER != LD_GEN16 || k < a.kdepth;
-      const v4i t = *reinterpret_cast<const v4i*>(bptr[i] + (kin ? k : 0));
-      regB[i] = kin ? t : v4i{0, 0, 0, 0};
-    }
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < ACH; ++i)
-      *reinterpret_cast<v4i*>(&As[buf][((tid >> 2) + 64 * i) * LDS_STRIDE + kc * 16]) = regA[i];
-#pragma unroll
-    for (int i = 0; i < BCH; ++i)
-      *reinterpret_cast<v4i*>(&Bs[buf][((tid >> 2) + 64 * i) * LDS_STRIDE + kc * 16]) = regB[i];
-  };
-
-  v16i acc[2][2];
-#pragma unroll
-  for (int mi = 0; mi < 2; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int ni = 0; ni < TN; ++ni)
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 0;
 
-  const int ktiles = (a.kdepth + BK - 1) / BK;
-  gload(0);
-  // Per-channel epilogue operands of this thread's two output columns, loaded
-  // before the main loop so that their latency overlaps it.
-  const bool want_vals = (EPI != EPI_ACC) || a.want_mm;
-  int csum[2];
-  EpiRaw eraw[2];
-#pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
-    const int cc = col < a.K ? col : a.K - 1;
-    csum[ni] = *(a_off ? a.colsum + cc : &kEpiZero);
-    if (want_vals) eraw[ni] = epi_channel_load(a.ep, cc);
-  }
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < ktiles; ++kt) {
-    const int buf = kt & 1;
-    if (kt + 1 < ktiles) gload(kt + 1);
+  // MFMAs of one staged slab: two 32-deep steps over this wave's tile.
+  auto compute = [&](const int8_t* sa, const int8_t* sb) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      v4i af[2], bf[2];
+      v4i af[TM], bf[TN];
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int mi = 0; mi < TM; ++mi)
         af[mi] = *reinterpret_cast<const v4i*>(
-            &As[buf][(wm * 64 + mi * 32 + (lane & 31)) * LDS_STRIDE + kk * 32 + (lane >> 5) * 16]);
+            &sa[lds_off(wm * WROWS + mi * 32 + (lane & 31), kk * 2 + (lane >> 5))]);
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
+      for (int ni = 0; ni < TN; ++ni)
         bf[ni] = *reinterpret_cast<const v4i*>(
-            &Bs[buf][(wn * 64 + ni * 32 + (lane & 31)) * LDS_STRIDE + kk * 32 + (lane >> 5) * 16]);
+            &sb[lds_off(wn * WCOLS + ni * 32 + (lane & 31), kk * 2 + (lane >> 5))]);
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi)
+      for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
+        for (int ni = 0; ni < TN; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[mi], bf[ni], acc[mi][ni], 0, 0, 0);
     }
-    if (kt + 1 < ktiles) lstore(buf ^ 1);
+  };
+
+  // Per-channel epilogue operands of this thread's output columns, loaded
+  // before the main loop so that their latency overlaps it.
+  const bool want_vals = (EPI != EPI_ACC) || a.want_mm;
+  int csum[TN];
+  EpiRaw eraw[TN];
+  auto epi_loads = [&]() {
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+      const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
+      const int cc = col < a.K ? col : a.K - 1;
+      csum[ni] = *(a_off ? a.colsum + cc : &kEpiZero);
+      if (want_vals) eraw[ni] = epi_channel_load(a.ep, cc);
+    }
+  };
+  const int ktiles = (a.kdepth + BK - 1) / BK;
+  const int hw_out = a.Ho * a.Wo;
+  const int taps = a.R * a.S;
+
+  if constexpr (LOADER == LD_DMA64) {
+    // Each wave fills 1 KB pieces of a stage (16 rows of 64 bytes): piece
+    // q = 4 j + wave, lane l -> row 16 q + l / 4, physical chunk l % 4, which
+    // holds logical chunk (l % 4) ^ f(row) of the swizzled layout.  The
+    // channel chunks are walked outermost and the filter taps innermost.
+    constexpr int AJ = BM / 64, BJ = BN / 64;
+    const int8_t* asrc[AJ];
+    int aih[AJ], aiw[AJ], acoff[AJ];
+    bool aok[AJ];
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) {
+      const int row = 16 * (4 * j + wave) + (lane >> 2);
+      const int grow = m0 + row;
+      aok[j] = grow < a.M;
+      const int rr = aok[j] ? grow : a.M - 1;
+      const int n = rr / hw_out, rem = rr - n * hw_out;
+      const int oh = rem / a.Wo, ow = rem - oh * a.Wo;
+      aih[j] = oh * a.stride - a.pad;
+      aiw[j] = ow * a.stride - a.pad;
+      asrc[j] = a.x + (int64_t)n * a.H * a.W * a.C;
+      acoff[j] = (((lane & 3) ^ ((row >> 1) ^ (row >> 3))) & 3) * 16;
+    }
+    const int8_t* bsrc[BJ];
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) {
+      const int row = 16 * (4 * j + wave) + (lane >> 2);
+      const int col = n0 + row;
+      const int cc = col < a.K ? col : a.K - 1;
+      bsrc[j] = a.w + (int64_t)cc * a.wrow + (((lane & 3) ^ ((row >> 1) ^ (row >> 3))) & 3) * 16;
+    }
+    const int8_t* padp = reinterpret_cast<const int8_t*>(&kPadVec[a_off]);
+    __shared__ __attribute__((aligned(16))) int8_t A0[BM * 64], A1[BM * 64], A2[BM * 64];
+    __shared__ __attribute__((aligned(16))) int8_t B0[BN * 64], B1[BN * 64], B2[BN * 64];
+    auto issue = [&](int kt, int8_t* sa, int8_t* sb) {
+      const int cchunk = kt / taps;
+      const int rs = kt - cchunk * taps;
+      const int r = rs / a.S, sx = rs - r * a.S;
+      const int c0 = cchunk * BK;
+      const int k0 = rs * a.C + c0;
+#pragma unroll
+      for (int j = 0; j < AJ; ++j) {
+        const int ih = aih[j] + r, iw = aiw[j] + sx;
+        const bool ok = aok[j] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+        const int8_t* p = ok ? asrc[j] + ((int64_t)ih * a.W + iw) * a.C + c0 + acoff[j] : padp;
+        __builtin_amdgcn_global_load_lds(p, &sa[(4 * j + wave) * 1024], 16, 0, 0);
+      }
+#pragma unroll
+      for (int j = 0; j < BJ; ++j) {
+        const int8_t* pb = bsrc[j] + k0;  // a named pointer: hipcc's host pass drops
+                                          // the kernel stub for an inline sum here
+        __builtin_amdgcn_global_load_lds(pb, &sb[(4 * j + wave) * 1024], 16, 0, 0);
+      }
+    };
+    // One ring step: slab kt from stage (ca, cb); slab kt + 2 into the stage
+    // (ia, ib) that slab kt - 1 used.  Waiting: this wave's pieces of slab kt
+    // have landed (the next slab's may still be in flight); after the barrier
+    // every wave's have, and every wave has finished reading stage (ia, ib).
+    auto step = [&](int kt, const int8_t* ca, const int8_t* cb, int8_t* ia, int8_t* ib) {
+      if (kt + 1 < ktiles) wait_vmcnt<AJ + BJ>();
+      else wait_vmcnt<0>();
+      ring_barrier();
+      if (kt + 2 < ktiles) issue(kt + 2, ia, ib);
+      compute(ca, cb);
+    };
+    epi_loads();
+    issue(0, A0, B0);
+    if (ktiles > 1) issue(1, A1, B1);
+    for (int kt = 0; kt < ktiles; kt += 3) {
+      step(kt, A0, B0, A2, B2);
+      if (kt + 1 < ktiles) step(kt + 1, A1, B1, A0, B0);
+      if (kt + 2 < ktiles) step(kt + 2, A2, B2, A1, B1);
+    }
+  } else {
+    // Rows owned by this thread for A loads.
+    const int8_t* abase[ACH];
+    int ih0[ACH], iw0[ACH];
+    bool aval[ACH];
+#pragma unroll
+    for (int i = 0; i < ACH; ++i) {
+      int row = m0 + (tid >> 2) + 64 * i;
+      aval[i] = row < a.M;
+      int rr = aval[i] ? row : a.M - 1;
+      int n = rr / hw_out, rem = rr - n * hw_out;
+      int oh = rem / a.Wo, ow = rem - oh * a.Wo;
+      ih0[i] = oh * a.stride - a.pad;
+      iw0[i] = ow * a.stride - a.pad;
+      abase[i] = a.x + (int64_t)n * a.H * a.W * a.C;
+    }
+    const int8_t* bptr[BCH];
+#pragma unroll
+    for (int i = 0; i < BCH; ++i) {
+      int col = n0 + (tid >> 2) + 64 * i;
+      int cc = col < a.K ? col : a.K - 1;
+      bptr[i] = a.w + (int64_t)cc * a.wrow;
+    }
+    v4i regA[ACH], regB[BCH];
+    auto gload = [&](int kt) {
+      // FAST64 walks the depth channel chunk by channel chunk with the filter
+      // taps innermost, so that consecutive slabs read neighbouring pixels of
+      // the same channels (cache reuse); the integer sums do not depend on the
+      // order.
+      const int cchunk = (LOADER == LD_FAST64) ? kt / taps : 0;
+      const int rs = (LOADER == LD_FAST64) ? kt - cchunk * taps : 0;
+      const int k0 = (LOADER == LD_FAST64) ? rs * a.C + cchunk * BK : kt * BK;
+      if constexpr (LOADER == LD_FAST64) {
+        const int c0 = cchunk * BK;
+        int r = rs / a.S, s = rs - r * a.S;
+#pragma unroll
+        for (int i = 0; i < ACH; ++i) {
+          int ih = ih0[i] + r, iw = iw0[i] + s;
+          bool ok = aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+          const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 + kc * 16 : 0);
+          const v4i t = *reinterpret_cast<const v4i*>(p);
+          regA[i] = ok ? t : padv;
+        }
+      } else if constexpr (LOADER == LD_GEN16) {
+        int k = k0 + kc * 16;
+        int rs = k / a.C, c0 = k - rs * a.C;
+        int r = rs / a.S, s = rs - r * a.S;
+        bool kin = k < a.kdepth;
+#pragma unroll
+        for (int i = 0; i < ACH; ++i) {
+          int ih = ih0[i] + r, iw = iw0[i] + s;
+          bool ok = kin && aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+          const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 : 0);
+          const v4i t = *reinterpret_cast<const v4i*>(p);
+          regA[i] = ok ? t : padv;
+        }
+      } else {  // LD_RGB4: four 4-byte pixels per 16-byte chunk
+#pragma unroll
+        for (int i = 0; i < ACH; ++i) {
+          v4i v;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            int rs = (k0 + kc * 16 + 4 * j) >> 2;
+            int t = (rs < 128) ? rs_tab[rs] : -1;
+            int word = padw;
+            if (t >= 0 && aval[i]) {
+              int ih = ih0[i] + (t >> 16), iw = iw0[i] + (t & 0xFFFF);
+              if (ih >= 0 && ih < a.H && iw >= 0 && iw < a.W)
+                word = *reinterpret_cast<const int*>(abase[i] + ((int64_t)ih * a.W + iw) * 4);
+            }
+            v[j] = word;
+          }
+          regA[i] = v;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < BCH; ++i) {
+        const int k = k0 + kc * 16;
+        const bool kin = LOADER != LD_GEN16 || k < a.kdepth;
+        const v4i t = *reinterpret_cast<const v4i*>(bptr[i] + (kin ? k : 0));
+        regB[i] = kin ? t : v4i{0, 0, 0, 0};
+      }
+    };
+    auto lstore = [&](int buf) {
+#pragma unroll
+      for (int i = 0; i < ACH; ++i)
+        *reinterpret_cast<v4i*>(&As[buf][lds_off((tid >> 2) + 64 * i, kc)]) = regA[i];
+#pragma unroll
+      for (int i = 0; i < BCH; ++i)
+        *reinterpret_cast<v4i*>(&Bs[buf][lds_off((tid >> 2) + 64 * i, kc)]) = regB[i];
+    };
+    gload(0);
+    epi_loads();
+    lstore(0);
     __syncthreads();
+    for (int kt = 0; kt < ktiles; ++kt) {
+      const int buf = kt & 1;
+      if (kt + 1 < ktiles) gload(kt + 1);
+      compute(As[buf], Bs[buf]);
+      if (kt + 1 < ktiles) lstore(buf ^ 1);
+      __syncthreads();
+    }
   }
 
   // ---- epilogue ----
@@ -269,16 +405,16 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
   const bool full = m0 + BM <= a.M && n0 + BN <= a.K;
   auto visit = [&](auto&& f) {
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
+    for (int ni = 0; ni < TN; ++ni) {
+      const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
       const int corr = 128 * csum[ni];
       double Mc = 1.0, Ac = 0.0;
       if (want_vals) epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
 #pragma unroll
-      for (int mi = 0; mi < 2; ++mi) {
+      for (int mi = 0; mi < TM; ++mi) {
 #pragma unroll
         for (int e = 0; e < 16; ++e) {
-          const int row = m0 + wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+          const int row = m0 + wm * WROWS + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
           if (full || (row < a.M && col < a.K)) f(acc[mi][ni][e] + corr, Mc, Ac, row, col);
         }
       }
@@ -292,23 +428,28 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
     // channel (v = relu(acc * M + A), rounding included), so the min / max of
     // the values are those of the channel's extreme accumulators: track the
     // integer extremes per column, evaluate the epilogue on them only.
-    int lo[2] = {INT_MAX, INT_MAX}, hi[2] = {INT_MIN, INT_MIN};
+    int lo[TN], hi[TN];
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+      lo[ni] = INT_MAX;
+      hi[ni] = INT_MIN;
+    }
     if (full) {
       // Full tile: buffer stores with the row offset in a scalar register.
       __amdgpu_buffer_rsrc_t rs;
-      int vo[2];
+      int vo[TN];
       if constexpr (EPI == EPI_ACC) {
-        rs = __builtin_amdgcn_make_buffer_rsrc(a.acc + (int64_t)(m0 + wm * 64) * a.K, (short)0,
+        rs = __builtin_amdgcn_make_buffer_rsrc(a.acc + (int64_t)(m0 + wm * WROWS) * a.K, (short)0,
                                                0x7fffffff, 0x00020000);
 #pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-          vo[ni] = (4 * (lane >> 5) * a.K + n0 + wn * 64 + ni * 32 + (lane & 31)) * 4;
+        for (int ni = 0; ni < TN; ++ni)
+          vo[ni] = (4 * (lane >> 5) * a.K + n0 + wn * WCOLS + ni * 32 + (lane & 31)) * 4;
       }
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
+      for (int ni = 0; ni < TN; ++ni) {
         const int corr = 128 * csum[ni];
 #pragma unroll
-        for (int mi = 0; mi < 2; ++mi) {
+        for (int mi = 0; mi < TM; ++mi) {
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
             const int v = acc[mi][ni][e];
@@ -322,14 +463,14 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
       }
     } else {
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        const int col = n0 + wn * 64 + ni * 32 + (lane & 31);
+      for (int ni = 0; ni < TN; ++ni) {
+        const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
         const int corr = 128 * csum[ni];
 #pragma unroll
-        for (int mi = 0; mi < 2; ++mi) {
+        for (int mi = 0; mi < TM; ++mi) {
 #pragma unroll
           for (int e = 0; e < 16; ++e) {
-            const int row = m0 + wm * 64 + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            const int row = m0 + wm * WROWS + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
             if (row < a.M && col < a.K) {
               const int v = acc[mi][ni][e];
               if constexpr (EPI == EPI_ACC) a.acc[(int64_t)row * a.K + col] = v + corr;
@@ -343,7 +484,7 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
     if (!want_vals) return;
     double mn = INFINITY, mx = -INFINITY;
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
+    for (int ni = 0; ni < TN; ++ni) {
       if (lo[ni] > hi[ni]) continue;  // no in-range value in this column
       double Mc, Ac;
       epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
@@ -387,20 +528,22 @@ __global__ __launch_bounds__(256, 3) void k_qconv(ConvArgs a) {
   }
 }
 
-template <int BM, int BN, int EPI>
+template <int BM, int BN, int TM, int TN, int MINW, int EPI>
 static void conv_dispatch_loader(int loader, dim3 grid, hipStream_t st, const ConvArgs& a) {
   if (loader == LD_FAST64)
-    k_qconv<BM, BN, LD_FAST64, EPI><<<grid, 256, 0, st>>>(a);
+    k_qconv<BM, BN, TM, TN, MINW, LD_FAST64, EPI><<<grid, 256, 0, st>>>(a);
+  else if (loader == LD_DMA64)
+    k_qconv<BM, BN, TM, TN, MINW, LD_DMA64, EPI><<<grid, 256, 0, st>>>(a);
   else if (loader == LD_GEN16)
-    k_qconv<BM, BN, LD_GEN16, EPI><<<grid, 256, 0, st>>>(a);
-  else if constexpr (EPI == EPI_ACC)
-    k_qconv<BM, BN, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
+    k_qconv<BM, BN, TM, TN, MINW, LD_GEN16, EPI><<<grid, 256, 0, st>>>(a);
+  else if constexpr (EPI == EPI_ACC && BN == 64)
+    k_qconv<BM, BN, TM, TN, MINW, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
 }
 
 // Tile shape and grid of a conv; loader choice and the geometry in `a`.
 static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const int8_t* w,
                        const int32_t* colsum, const SrcDev* ep, ConvArgs& a, int& loader,
-                       bool& wide) {
+                       int& cfg) {
   a.x = static_cast<const int8_t*>(x);
   a.w = w;
   a.colsum = colsum;
@@ -416,16 +559,28 @@ static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const
   a.x_type = x_type;
   a.has_ep = ep != nullptr;
   if (ep) a.ep = *ep;
-  wide = d.k <= 64;  // 256 x 64 tiles for narrow outputs, else 128 x 128
-  return wide ? dim3((a.M + 255) / 256, (d.k + 63) / 64) : dim3((a.M + 127) / 128, (d.k + 127) / 128);
+  // 256 x 64 tiles for narrow outputs; 256 x 128 (128 x 64 per wave: fewer LDS
+  // bytes per MFMA) for deep contractions; else 128 x 128.
+  if (d.k <= 64 || loader == LD_RGB4) cfg = TC_256x64;
+  else if (loader == LD_FAST64 && a.kdepth >= 512) cfg = TC_256x128;
+  else cfg = TC_128x128;
+  // channel multiples of 64 outside the narrow tiles: slabs through the LDS ring
+  if (loader == LD_FAST64 && cfg != TC_256x64) loader = LD_DMA64;
+  switch (cfg) {
+    case TC_256x64: return dim3((a.M + 255) / 256, (d.k + 63) / 64);
+    case TC_256x128: return dim3((a.M + 255) / 256, (d.k + 127) / 128);
+    default: return dim3((a.M + 127) / 128, (d.k + 127) / 128);
+  }
 }
 
 template <int EPI>
-static void conv_run(const ConvArgs& a, int loader, bool wide, dim3 grid, hipStream_t st) {
-  if (wide)
-    conv_dispatch_loader<256, 64, EPI>(loader, grid, st, a);
+static void conv_run(const ConvArgs& a, int loader, int cfg, dim3 grid, hipStream_t st) {
+  if (cfg == TC_256x64)
+    conv_dispatch_loader<256, 64, 2, 2, 3, EPI>(loader, grid, st, a);
+  else if (cfg == TC_256x128)
+    conv_dispatch_loader<256, 128, 4, 2, 2, EPI>(loader, grid, st, a);
   else
-    conv_dispatch_loader<128, 128, EPI>(loader, grid, st, a);
+    conv_dispatch_loader<128, 128, 2, 2, 3, EPI>(loader, grid, st, a);
 }
 
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
@@ -433,13 +588,13 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
                        double* d_minmax) {
   ConvArgs a{};
   int loader;
-  bool wide;
-  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, wide);
+  int cfg;
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, cfg);
   a.acc = acc;
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
   bool timed = timer_begin(c, FXPQ_TIMER_QCONV);
-  conv_run<EPI_ACC>(a, loader, wide, grid, c.stream);
+  conv_run<EPI_ACC>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   if (a.want_mm) return launch_minmax_fin(c, a.mm_part, (int)(grid.x * grid.y), d_minmax);
   return hipGetLastError();
@@ -448,8 +603,8 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
 int conv_fused_blocks(const fxpq_conv_desc& d) {
   ConvArgs a{};
   int loader;
-  bool wide;
-  const dim3 grid = conv_setup(d, nullptr, 0, nullptr, nullptr, nullptr, a, loader, wide);
+  int cfg;
+  const dim3 grid = conv_setup(d, nullptr, 0, nullptr, nullptr, nullptr, a, loader, cfg);
   if (loader == LD_RGB4) return -1;
   return (int)(grid.x * grid.y);
 }
@@ -463,8 +618,8 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
                              double* d_minmax) {
   ConvArgs a{};
   int loader;
-  bool wide;
-  const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, wide);
+  int cfg;
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, cfg);
   const int nb = (int)(grid.x * grid.y);
   const double ops = 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c);
   const int64_t n = (int64_t)a.M * d.k;
@@ -472,7 +627,7 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   a.want_mm = 1;
   a.mm_part = c.sc.minmax_part;
   bool timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
-  conv_run<EPI_MM>(a, loader, wide, grid, c.stream);
+  conv_run<EPI_MM>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
   hipError_t e = launch_minmax_fin(c, a.mm_part, nb, d_minmax);
   if (e != hipSuccess) return e;
@@ -488,9 +643,9 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   a.fmt_win = out;
   a.flags = c.sc.flags;
   timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
-  conv_run<EPI_WIN>(a, loader, wide, grid, c.stream);
+  conv_run<EPI_WIN>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
-  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, fl_hi, MODE_SEARCH, kConvPerThread, d_minmax,
+  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, fl_hi, MODE_SEARCH, conv_per_thread(cfg), d_minmax,
                             nb, out);
   if (e != hipSuccess) return e;
   // 3. only when the plan asks for the general pass: int32 accumulators, then
@@ -500,7 +655,7 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   g.want_mm = 0;
   g.only_if_general = 1;
   g.plan_in = static_cast<const FlsPlan*>(c.sc.plan);
-  conv_run<EPI_ACC>(g, loader, wide, grid, c.stream);
+  conv_run<EPI_ACC>(g, loader, cfg, grid, c.stream);
   e = launch_fls_general(c, ep, n, wl, fl_lo, fl_hi, d_minmax, out, nullptr);
   if (e != hipSuccess) return e;
   // 4. codes in the searched format
@@ -508,7 +663,7 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   a.y = y;
   a.y_type = y_type;
   timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
-  conv_run<EPI_REQ>(a, loader, wide, grid, c.stream);
+  conv_run<EPI_REQ>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
   return hipGetLastError();
 }
