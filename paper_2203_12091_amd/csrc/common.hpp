@@ -187,7 +187,7 @@ hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                        const int8_t* w, const int32_t* colsum, const SrcDev* ep, int32_t* acc,
                        double* d_minmax);
-int conv_fused_blocks(const fxpq_conv_desc& d);  // -1 when the fused path does not apply
+int conv_fused_blocks(const fxpq_conv_desc& d, int cus);  // -1 when the fused path does not apply
 hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                              const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
                              int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,

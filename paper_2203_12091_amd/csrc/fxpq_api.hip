@@ -346,7 +346,7 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
   if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
   if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
   if (d->c % 16 != 0) return FXPQ_ERR_UNSUPPORTED;
-  const int nb = conv_fused_blocks(*d);
+  const int nb = conv_fused_blocks(*d, h->cus);
   if (nb < 1 || nb > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
   SrcDev e;
   epi_to_dev(ep, &e);

@@ -67,6 +67,17 @@ __device__ inline void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// One 16-byte global -> LDS load per lane (global_load_lds_dwordx4): lane l's
+// bytes land at lds + 16 l.  Issued as inline asm so that the compiler does
+// not add its own conservative wait for these LDS writes before later LDS
+// reads (it cannot tell the ring stages apart); the ring waits explicitly
+// (wait_vmcnt) and orders with ring_barrier().  M0 holds the wave-uniform LDS
+// address; the s_nop separates its write from the load.
+__device__ inline void dma16(const int8_t* g, int8_t* lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(l) : "memory");
+}
+
 // Workgroup barrier without the memory fence __syncthreads() adds: that fence
 // would wait for every outstanding LDS-ring load.  The empty asm statements
 // keep the compiler from moving memory accesses across it.
@@ -265,13 +276,11 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
         const int ih = aih[j] + r, iw = aiw[j] + sx;
         const bool ok = aok[j] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
         const int8_t* p = ok ? asrc[j] + ((int64_t)ih * a.W + iw) * a.C + c0 + acoff[j] : padp;
-        __builtin_amdgcn_global_load_lds(p, &sa[(4 * j + wave) * 1024], 16, 0, 0);
+        dma16(p, &sa[(4 * j + wave) * 1024]);
       }
 #pragma unroll
       for (int j = 0; j < BJ; ++j) {
-        const int8_t* pb = bsrc[j] + k0;  // a named pointer: hipcc's host pass drops
-                                          // the kernel stub for an inline sum here
-        __builtin_amdgcn_global_load_lds(pb, &sb[(4 * j + wave) * 1024], 16, 0, 0);
+        dma16(bsrc[j] + k0, &sb[(4 * j + wave) * 1024]);
       }
     };
     // One ring step: slab kt from stage (ca, cb); slab kt + 2 into the stage
@@ -543,7 +552,7 @@ static void conv_dispatch_loader(int loader, dim3 grid, hipStream_t st, const Co
 // Tile shape and grid of a conv; loader choice and the geometry in `a`.
 static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const int8_t* w,
                        const int32_t* colsum, const SrcDev* ep, ConvArgs& a, int& loader,
-                       int& cfg) {
+                       int& cfg, int cus) {
   a.x = static_cast<const int8_t*>(x);
   a.w = w;
   a.colsum = colsum;
@@ -560,9 +569,12 @@ static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const
   a.has_ep = ep != nullptr;
   if (ep) a.ep = *ep;
   // 256 x 64 tiles for narrow outputs; 256 x 128 (128 x 64 per wave: fewer LDS
-  // bytes per MFMA) for deep contractions; else 128 x 128.
+  // bytes per MFMA, two blocks per CU) for deep contractions with enough tiles
+  // to fill the chip; else 128 x 128 (three blocks per CU).
+  const int64_t tiles_256x128 = (int64_t)((a.M + 255) / 256) * ((d.k + 127) / 128);
   if (d.k <= 64 || loader == LD_RGB4) cfg = TC_256x64;
-  else if (loader == LD_FAST64 && a.kdepth >= 512) cfg = TC_256x128;
+  else if (loader == LD_FAST64 && a.kdepth >= 512 && 2 * tiles_256x128 >= 3 * (int64_t)cus)
+    cfg = TC_256x128;
   else cfg = TC_128x128;
   // channel multiples of 64 outside the narrow tiles: slabs through the LDS ring
   if (loader == LD_FAST64 && cfg != TC_256x64) loader = LD_DMA64;
@@ -589,7 +601,7 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   ConvArgs a{};
   int loader;
   int cfg;
-  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, cfg);
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, cfg, c.cus);
   a.acc = acc;
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
@@ -600,11 +612,11 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   return hipGetLastError();
 }
 
-int conv_fused_blocks(const fxpq_conv_desc& d) {
+int conv_fused_blocks(const fxpq_conv_desc& d, int cus) {
   ConvArgs a{};
   int loader;
   int cfg;
-  const dim3 grid = conv_setup(d, nullptr, 0, nullptr, nullptr, nullptr, a, loader, cfg);
+  const dim3 grid = conv_setup(d, nullptr, 0, nullptr, nullptr, nullptr, a, loader, cfg, cus);
   if (loader == LD_RGB4) return -1;
   return (int)(grid.x * grid.y);
 }
@@ -619,7 +631,7 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   ConvArgs a{};
   int loader;
   int cfg;
-  const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, cfg);
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, cfg, c.cus);
   const int nb = (int)(grid.x * grid.y);
   const double ops = 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c);
   const int64_t n = (int64_t)a.M * d.k;
