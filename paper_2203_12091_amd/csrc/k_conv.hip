@@ -40,12 +40,14 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 constexpr int BK = 64;
 
 // LDS slab layout: rows of 64 bytes (four 16-byte chunks), no padding; chunk
-// c of row r sits at chunk position c ^ f(r).  With f(r) = ((r >> 1) ^ (r >> 3))
-// & 3 the eight (or sixteen) lanes served together by a 16-byte LDS access --
-// consecutive rows of one chunk on the MFMA operand reads, or two (four) full
-// rows on the stores -- touch distinct banks.
+// c of row r sits at chunk position c ^ f(r) with f(r) = (r >> 2) & 3.  The
+// MFMA operand reads (lane l: row l % 32, one chunk) then run at the full
+// ds_read_b128 rate on gfx950 (measured: 1.5x slower with f = (r >> 1) ^
+// (r >> 3), 3x without a swizzle); the 16-byte stores of whole rows are
+// insensitive to it.
+__device__ inline int lds_swz(int row) { return (row >> 2) & 3; }
 __device__ inline int lds_off(int row, int chunk) {
-  return row * 64 + ((chunk ^ ((row >> 1) ^ (row >> 3))) & 3) * 16;
+  return row * 64 + ((chunk ^ lds_swz(row)) & 3) * 16;
 }
 
 // FAST64: C % 64 == 0, register-staged slabs; GEN16: C % 16 == 0; RGB4: the
@@ -170,7 +172,21 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
   const int wm = wave / WGN, wn = wave % WGN;
-  const int m0 = blockIdx.x * BM, n0 = blockIdx.y * BN;
+  // Tile of this block.  Blocks are dealt to the 8 XCDs round-robin by linear
+  // id; remapped so that each XCD takes a contiguous run of tiles in
+  // row-block-major order, i.e. the column tiles of one row block run on the
+  // same XCD and share its L2 copy of the input rows.
+  int tm = blockIdx.x, tn = blockIdx.y;
+  {
+    const int T = gridDim.x * gridDim.y;
+    if (T % 8 == 0) {
+      const int L = blockIdx.y * gridDim.x + blockIdx.x;
+      const int t = (L % 8) * (T / 8) + L / 8;
+      tm = t / gridDim.y;
+      tn = t - tm * gridDim.y;
+    }
+  }
+  const int m0 = tm * BM, n0 = tn * BN;
   const int kc = tid & 3;
 
   // Inputs stored as u - 128 (branch-free, so the operand loads need not wait
@@ -195,23 +211,30 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
 
   // MFMAs of one staged slab: two 32-deep steps over this wave's tile.
   auto compute = [&](const int8_t* sa, const int8_t* sb) {
+    // All fragments of the slab are read first, then the MFMAs run: the LDS
+    // latency is paid once per slab (interleaving reads and MFMAs on a few
+    // reused registers paid it before every pair of MFMAs).
+    v4i af[2][TM], bf[2][TN];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
-      v4i af[TM], bf[TN];
 #pragma unroll
       for (int mi = 0; mi < TM; ++mi)
-        af[mi] = *reinterpret_cast<const v4i*>(
+        af[kk][mi] = *reinterpret_cast<const v4i*>(
             &sa[lds_off(wm * WROWS + mi * 32 + (lane & 31), kk * 2 + (lane >> 5))]);
 #pragma unroll
       for (int ni = 0; ni < TN; ++ni)
-        bf[ni] = *reinterpret_cast<const v4i*>(
+        bf[kk][ni] = *reinterpret_cast<const v4i*>(
             &sb[lds_off(wn * WCOLS + ni * 32 + (lane & 31), kk * 2 + (lane >> 5))]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int mi = 0; mi < TM; ++mi)
 #pragma unroll
         for (int ni = 0; ni < TN; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[mi], bf[ni], acc[mi][ni], 0, 0, 0);
-    }
+          acc[mi][ni] =
+              __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][mi], bf[kk][ni], acc[mi][ni], 0, 0, 0);
   };
 
   // Per-channel epilogue operands of this thread's output columns, loaded
@@ -252,7 +275,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       aih[j] = oh * a.stride - a.pad;
       aiw[j] = ow * a.stride - a.pad;
       asrc[j] = a.x + (int64_t)n * a.H * a.W * a.C;
-      acoff[j] = (((lane & 3) ^ ((row >> 1) ^ (row >> 3))) & 3) * 16;
+      acoff[j] = (((lane & 3) ^ lds_swz(row)) & 3) * 16;
     }
     const int8_t* bsrc[BJ];
 #pragma unroll
@@ -260,7 +283,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       const int row = 16 * (4 * j + wave) + (lane >> 2);
       const int col = n0 + row;
       const int cc = col < a.K ? col : a.K - 1;
-      bsrc[j] = a.w + (int64_t)cc * a.wrow + (((lane & 3) ^ ((row >> 1) ^ (row >> 3))) & 3) * 16;
+      bsrc[j] = a.w + (int64_t)cc * a.wrow + (((lane & 3) ^ lds_swz(row)) & 3) * 16;
     }
     const int8_t* padp = reinterpret_cast<const int8_t*>(&kPadVec[a_off]);
     __shared__ __attribute__((aligned(16))) int8_t A0[BM * 64], A1[BM * 64], A2[BM * 64];
