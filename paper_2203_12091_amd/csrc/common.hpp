@@ -14,6 +14,13 @@ constexpr int kMaxConvBlocks = 1 << 20;
 constexpr int kWindow = 2;           // candidates of the first FL-search pass
 constexpr int kWinPart = 6 * kWindow;  // int64 per slot of window-pass sums
 constexpr int kWinSlots = 64;          // slots the window-pass blocks add into (block % kWinSlots)
+// Clipping-error lower bounds the window pass can take above its candidates
+// (at fl = b1 + 1, b1 + 2, ...), and fp64 sums per slot: sum W^2 and the bounds.
+constexpr int kCeBounds = 4;
+constexpr int kWinPartF = 1 + kCeBounds;
+// Word lengths up to this one take all kCeBounds bounds (their best fl lies
+// above the window more often); longer ones take one.
+constexpr int kCeMultiMaxWl = 6;
 // Values per thread of the streaming window pass (the grid grows beyond that):
 // sums of W * q stay exact for max|W * q| < 2^53 / 512.
 constexpr int64_t kWinMaxPerThread = 512;
@@ -26,7 +33,7 @@ struct Scratch {
   double* minmax;           // internal [2]
   double* minmax_part;      // per-block partials [kMaxConvBlocks][2]
   long long* win_part;      // window FL-search integer sums [kWinSlots][kWinPart] (0 between searches)
-  double* win_part_f;       // window FL-search fp64 bound sums [kWinSlots][2] (0 between searches)
+  double* win_part_f;       // window FL-search fp64 bound sums [kWinSlots][kWinPartF] (0 between searches)
   unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
   unsigned* gen_done;       // blocks of the general pass finished (0 between searches)
   void* plan;               // FlsPlan
@@ -179,7 +186,7 @@ hipError_t launch_requant_addmm(const Ctx& c, const SrcDev& s, int64_t n, const 
                                 const fxpq_fmt* fmt_b, int relu, double* d_add_minmax);
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
-hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,
+hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo, int nce,
                                  int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
                                  int nb, fxpq_fmt* out);
 hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,

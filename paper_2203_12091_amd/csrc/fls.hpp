@@ -168,10 +168,11 @@ __device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, 
 
 // Per-thread accumulators of the window pass: per candidate the exact
 // integers sum q^2 and sum W q (as sum Wh q and sum Wl q in the split form;
-// all below 2^53, see win_setup), plus the two fp64 bound sums.
+// all below 2^53, see win_setup), plus the fp64 bound sums: sum W^2 and the
+// clipping errors at fl = b1 + 1, b1 + 2, ...
 struct WinAcc {
   double A[kWindow], PH[kWindow], PL[kWindow];
-  double V2, CE;
+  double V2, CE[kCeBounds];
 };
 
 constexpr double kTwoM26 = 1.0 / 67108864.0;  // 2^-26
@@ -204,7 +205,9 @@ __device__ inline WinCtx win_ctx(const FlsU& u, const WinSetup& ws) {
 __device__ inline void win_acc_zero(WinAcc& acc) {
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) acc.A[j] = acc.PH[j] = acc.PL[j] = 0.0;
-  acc.V2 = acc.CE = 0.0;
+  acc.V2 = 0.0;
+#pragma unroll
+  for (int k = 0; k < kCeBounds; ++k) acc.CE[k] = 0.0;
 }
 
 // Adds one integer value W = v * 2^sigma.  Specialized on
@@ -212,7 +215,7 @@ __device__ inline void win_acc_zero(WinAcc& acc) {
 // and on what the min/max already tell:
 //   NONNEG   every value is >= 0: no lower clamp, no lower clipping term;
 //   CLAMP0   the first candidate can saturate (it is not beta_nosat).
-template <bool SPLIT, bool NONNEG, bool CLAMP0>
+template <bool SPLIT, bool NONNEG, bool CLAMP0, int NB = 1>
 __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
   double Wh = 0.0, Wl = W;
   if (SPLIT) {
@@ -231,12 +234,18 @@ __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
     if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
     acc.PL[j] = fma(Wl, q, acc.PL[j]);
   }
-  const double t = W * c.cce;
-  const double d1 = fmax(t - c.qmax, 0.0);
-  acc.CE = fma(d1, d1, acc.CE);
-  if (!NONNEG) {
-    const double d2 = fmin(t - c.qmin, 0.0);
-    acc.CE = fma(d2, d2, acc.CE);
+  // clipping error at the first NB fl above the window: W * 2^(fl - sigma)
+  // doubles (exactly) from one to the next
+  double t = W * c.cce;
+#pragma unroll
+  for (int k = 0; k < NB; ++k) {
+    if (k) t += t;
+    const double d1 = fmax(t - c.qmax, 0.0);
+    acc.CE[k] = fma(d1, d1, acc.CE[k]);
+    if (!NONNEG) {
+      const double d2 = fmin(t - c.qmin, 0.0);
+      acc.CE[k] = fma(d2, d2, acc.CE[k]);
+    }
   }
 }
 
@@ -272,8 +281,9 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
 // is split into its high and low 32-bit halves, summed separately over the
 // block and added (int64 atomics: exact, order-free) into slot bid %
 // kWinSlots of part_i (kWinPart int64 per slot: per candidate A hi/lo, PH
-// hi/lo, PL hi/lo); the two fp64 bound sums go to part_f.  The finalize reads
-// the slots and clears them for the next search.
+// hi/lo, PL hi/lo); the fp64 bound sums (sum W^2, then NB clipping bounds) go
+// to part_f (kWinPartF per slot).  The finalize reads the slots and clears
+// them for the next search.
 __device__ inline void slot_add(long long* p, long long v) {
   __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v,
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -283,9 +293,9 @@ __device__ inline void slot_add(double* p, double v) {
 }
 
 __device__ inline void win_write_partials_i64(const long long* A, const long long* PH,
-                                              const long long* PL, double V2, double CE,
-                                              int64_t bid, long long* part_i, double* part_f,
-                                              long long* shl, double* shd) {
+                                              const long long* PL, double V2, const double* CE,
+                                              int nb, int64_t bid, long long* part_i,
+                                              double* part_f, long long* shl, double* shd) {
   const int slot = (int)(bid % kWinSlots);
   long long* pi = part_i + slot * kWinPart;
 #pragma unroll
@@ -301,16 +311,17 @@ __device__ inline void win_write_partials_i64(const long long* A, const long lon
       }
     }
   }
-  double v2 = block_reduce(V2, OpAddD(), shd);
-  double ce = block_reduce(CE, OpAddD(), shd);
-  if (threadIdx.x == 0) {
-    slot_add(part_f + 2 * slot, v2);
-    slot_add(part_f + 2 * slot + 1, ce);
+  const double v2 = block_reduce(V2, OpAddD(), shd);
+  if (threadIdx.x == 0) slot_add(part_f + kWinPartF * slot, v2);
+  for (int k = 0; k < nb; ++k) {
+    const double ce = block_reduce(CE[k], OpAddD(), shd);
+    if (threadIdx.x == 0) slot_add(part_f + kWinPartF * slot + 1 + k, ce);
   }
 }
 
-__device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long long* part_i,
-                                          double* part_f, long long* shl, double* shd) {
+__device__ inline void win_write_partials(const WinAcc& acc, int nb, int64_t bid,
+                                          long long* part_i, double* part_f, long long* shl,
+                                          double* shd) {
   long long A[kWindow], PH[kWindow], PL[kWindow];
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
@@ -318,7 +329,7 @@ __device__ inline void win_write_partials(const WinAcc& acc, int64_t bid, long l
     PH[j] = exact_i64(acc.PH[j]);
     PL[j] = exact_i64(acc.PL[j]);
   }
-  win_write_partials_i64(A, PH, PL, acc.V2, acc.CE, bid, part_i, part_f, shl, shd);
+  win_write_partials_i64(A, PH, PL, acc.V2, acc.CE, nb, bid, part_i, part_f, shl, shd);
 }
 
 // Launch helpers shared by the streaming search and the fused C-Block.

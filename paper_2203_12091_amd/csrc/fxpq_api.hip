@@ -162,7 +162,7 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   size_t o_mm = take(2 * sizeof(double));
   size_t o_gd = take(4);
   size_t o_wp = take((size_t)kWinSlots * kWinPart * sizeof(long long));
-  size_t o_wpf = take((size_t)kWinSlots * 2 * sizeof(double));
+  size_t o_wpf = take((size_t)kWinSlots * kWinPartF * sizeof(double));
   size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
   size_t o_gp = take((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
   size_t o_plan = take(256);

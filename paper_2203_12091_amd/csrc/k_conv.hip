@@ -551,7 +551,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       default: FXPQ_WIN_VISIT(true, true); break;
     }
 #undef FXPQ_WIN_VISIT
-    win_write_partials(wa, bid, a.part_i, a.part_f, shl, shd);
+    win_write_partials(wa, 1, bid, a.part_i, a.part_f, shl, shd);
   } else {  // EPI_REQ
     visit([&](int v, double Mc, double Ac, int row, int col) {
       const double val = fmax(fma((double)v, Mc, Ac), relo);
@@ -680,7 +680,7 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
   conv_run<EPI_WIN>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
-  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, fl_hi, MODE_SEARCH, conv_per_thread(cfg), d_minmax,
+  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, 1, fl_hi, MODE_SEARCH, conv_per_thread(cfg), d_minmax,
                             nb, out);
   if (e != hipSuccess) return e;
   // 3. only when the plan asks for the general pass: int32 accumulators, then

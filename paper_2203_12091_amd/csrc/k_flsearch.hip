@@ -27,12 +27,14 @@
 namespace fxpq {
 
 // Main loop of the streaming window pass over this thread's values.
-template <int KIND, int DT, bool NONNEG, bool CLAMP0>
+template <int KIND, int DT, bool NONNEG, bool CLAMP0, int NB>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
                                 WinAcc& acc) {
   const WinCtx wc = win_ctx(u, ws);
   win_acc_zero(acc);
-  auto consume = [&](double W) { win_consume<KIND == FXPQ_SRC_F32, NONNEG, CLAMP0>(wc, acc, W); };
+  auto consume = [&](double W) {
+    win_consume<KIND == FXPQ_SRC_F32, NONNEG, CLAMP0, NB>(wc, acc, W);
+  };
 
   using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
@@ -50,7 +52,8 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
     for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i) * u.wscale);
 }
 
-template <int KIND, int DT>
+// NB clipping bounds above the window (1, or kCeBounds for short word lengths).
+template <int KIND, int DT, int NB>
 __global__ __launch_bounds__(kThreads) void k_fls_window(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
     const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out,
@@ -67,12 +70,12 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
   }
   WinAcc acc;
   switch (win_variant(u, ws, mm)) {
-    case 0: win_loop<KIND, DT, false, false>(s, n, u, ws, acc); break;
-    case 1: win_loop<KIND, DT, false, true>(s, n, u, ws, acc); break;
-    case 2: win_loop<KIND, DT, true, false>(s, n, u, ws, acc); break;
-    default: win_loop<KIND, DT, true, true>(s, n, u, ws, acc); break;
+    case 0: win_loop<KIND, DT, false, false, NB>(s, n, u, ws, acc); break;
+    case 1: win_loop<KIND, DT, false, true, NB>(s, n, u, ws, acc); break;
+    case 2: win_loop<KIND, DT, true, false, NB>(s, n, u, ws, acc); break;
+    default: win_loop<KIND, DT, true, true, NB>(s, n, u, ws, acc); break;
   }
-  win_write_partials(acc, blockIdx.x, part_i, part_f, shl, shd);
+  win_write_partials(acc, NB, blockIdx.x, part_i, part_f, shl, shd);
 }
 
 // Bits of |v| (0 for v == 0).
@@ -90,7 +93,7 @@ __device__ inline double i128_to_double(__int128 v) {
 // adds them exactly, lane 0 decides.
 template <int KIND>
 __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
-    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
+    SrcDev s, int wl, int sign_req, int fl_lo, int nce, int fl_hi, int mode, int64_t per_thread,
     const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out) {
   constexpr int NQ = 3 * kWindow;
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
@@ -107,20 +110,22 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
     hi[qi] = p[2 * qi];
     lo[qi] = p[2 * qi + 1];
   }
-  double f0 = part_f[2 * lane], f1 = part_f[2 * lane + 1];
+  double f[kWinPartF];
+#pragma unroll
+  for (int k = 0; k < kWinPartF; ++k) {
+    f[k] = part_f[kWinPartF * lane + k];
+    part_f[kWinPartF * lane + k] = 0.0;
+  }
 #pragma unroll
   for (int k2 = 0; k2 < kWinPart; ++k2) p[k2] = 0;
-  part_f[2 * lane] = 0.0;
-  part_f[2 * lane + 1] = 0.0;
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) {
     hi[qi] = wave_reduce(hi[qi], OpAddL());
     lo[qi] = wave_reduce(lo[qi], OpAddL());
   }
-  f0 = wave_reduce(f0, OpAddD());
-  f1 = wave_reduce(f1, OpAddD());
+#pragma unroll
+  for (int k = 0; k < kWinPartF; ++k) f[k] = wave_reduce(f[k], OpAddD());
   if (lane != 0) return;
-  const double tot_f[2] = {f0, f1};
   auto total = [&](int qi) -> __int128 { return ((__int128)hi[qi] << 32) + (__int128)lo[qi]; };
   // K_j = 2^(2d) A - 2^(d+1) P, d = sigma - beta; shifted by `off` >= 0 so all
   // exponents are non-negative (same factor for every candidate).
@@ -171,15 +176,23 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   }
   const int fl_win = b0 + bj;
   bool done = (b1 == fl_hi);
+  int gen_hi = fl_hi;
   if (!done) {
-    // Upper bound of the window's best error, lower bound of every error above
-    // the window (relative fp64 error of each sum, in any summation order,
-    // < 2^-40).
-    double v2 = tot_f[0];
+    // Upper bound of the window's best error; the clipping error at fl is a
+    // lower bound of the error of every candidate >= fl (it is non-decreasing
+    // in fl), so the first bound above the best error excludes the rest
+    // (relative fp64 error of each sum, in any summation order, < 2^-40).
+    double v2 = f[0];
     double sse_ub = (v2 * (1.0 + 0x1p-30) + kd + fabs(kd) * 0x1p-50 + v2 * 0x1p-50);
     sse_ub = ldexp(sse_ub, -2 * u.sigma) * (1.0 + 0x1p-50);
-    double ce_lb = ldexp(tot_f[1] * (1.0 - 0x1p-30), -2 * bce);
-    done = ce_lb > sse_ub;
+    for (int k = 0; k < nce && bce + k <= fl_hi; ++k) {
+      const double ce_lb = ldexp(f[1 + k] * (1.0 - 0x1p-30), -2 * (bce + k));
+      if (ce_lb > sse_ub) {
+        gen_hi = bce + k - 1;
+        break;
+      }
+    }
+    done = gen_hi <= b1;
   }
   plan->sign = u.sign;
   plan->status = 0;
@@ -189,7 +202,7 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   } else {
     plan->need_general = 1;
     plan->gen_lo = b1 + 1;
-    plan->gen_hi = fl_hi;
+    plan->gen_hi = gen_hi;
     plan->gen_extra = fl_win;
   }
 }
@@ -376,13 +389,13 @@ __device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int si
     default: { constexpr int K_ = FXPQ_SRC_ADD, D_ = FXPQ_I8; CALL; } break;        \
   }
 
-hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo,
+hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo, int nce,
                                  int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
                                  int nb, fxpq_fmt* out) {
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window_fin<K_><<<1, kFinThreads, 0, c.stream>>>(
-                        s, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
+                        s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
                         c.sc.win_part_f, plan, out)));
   return hipGetLastError();
 }
@@ -411,21 +424,27 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
   int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
   const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;  // Pack<>::V
-  int resident = 0;
-  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (resident = resident_blocks(c, (const void*)&k_fls_window<K_, D_>)));
-  const int blocks = stream_grid(n, channels, kWinMaxPerThread, vec, resident);
-  const int64_t per_thread = window_per_thread(n, blocks, vec);
+  const int nce = (wl <= kCeMultiMaxWl) ? kCeBounds : 1;
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   int mode = d_sse ? MODE_REPORT : MODE_SEARCH;
   const double elem_bytes = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
-  bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
-  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
-                    (k_fls_window<K_, D_><<<blocks, kThreads, 0, c.stream>>>(
-                        s, n, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
-                        c.sc.win_part_f, plan, out, c.sc.flags)));
-  timer_end(c, timed, elem_bytes * (double)n);
-  hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, fl_hi, mode, per_thread, d_minmax,
+  int64_t per_thread = 0;
+  int blocks = 0;
+  auto run = [&](auto kernel) {
+    blocks = stream_grid(n, channels, kWinMaxPerThread, vec, resident_blocks(c, (const void*)kernel));
+    per_thread = window_per_thread(n, blocks, vec);
+    bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
+    kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, mode, per_thread,
+                                              d_minmax, c.sc.win_part, c.sc.win_part_f, plan, out,
+                                              c.sc.flags);
+    timer_end(c, timed, elem_bytes * (double)n);
+  };
+  if (nce == 1) {
+    FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, 1>)));
+  } else {
+    FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, kCeBounds>)));
+  }
+  hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax,
                                        blocks, out);
   if (e != hipSuccess) return e;
   return launch_fls_general(c, s, n, wl, fl_lo, fl_hi, d_minmax, out, d_sse);

@@ -187,6 +187,54 @@ def test_fl_search_int_sources(fx, h, orc):
     check_flags(fx, h)
 
 
+def heavy_tail_case(seed, n, nout, omag):
+    """Normal bulk (std 2^10) plus nout outliers of magnitude ~2^omag: at short
+    word lengths the best fl clips the outliers and lies well above the
+    largest non-saturating fl."""
+    g = synth.rng_for(seed, "heavy")
+    v = np.rint(g.standard_normal(n) * 2 ** 10).astype(np.int64)
+    idx = g.choice(n, nout, replace=False)
+    v[idx] = (np.where(g.random(nout) < 0.5, -1, 1) * (2 ** omag) * (1 + g.random(nout))).astype(np.int64)
+    return v
+
+
+def beta_nosat(v, s, wl, sign):
+    from fractions import Fraction as F
+    qmax, qmin = 2 ** (wl - sign) - 1, (-(2 ** (wl - 1)) if sign else 0)
+    mx, mn = int(v.max()), int(v.min())
+    for b in range(FL_HI, FL_LO - 1, -1):
+        if F(mx) * F(2) ** (b - s) <= qmax + F(1, 2) and F(mn) * F(2) ** (b - s) >= qmin - F(1, 2):
+            return b
+    return FL_LO - 1
+
+
+def test_fl_search_best_fl_above_the_window(fx, h, orc):
+    # Short word lengths with outliers: the two-candidate window cannot decide
+    # and the exact pass evaluates the candidates the clipping bounds leave
+    # (1 to 5 above the window here, and the whole range above it once).
+    import torch
+    above = []
+    s = 12
+    for seed, n, nout, omag in [(11, 200_000, 3, 14), (12, 200_000, 30, 12), (13, 200_000, 300, 11),
+                                (14, 50_001, 1, 18), (16, 100_000, 10, 16)]:
+        v = heavy_tail_case(seed, n, nout, omag)
+        sd = torch.tensor([s], dtype=torch.int32, device=DEV)
+        x32 = (v.astype(np.float64) * 2.0 ** -s).astype(np.float32)  # exact
+        for wl in (3, 4, 5, 6, 8):
+            note("fls-heavy", seed, n, wl)
+            ofl, osign, _ = orc.fl_search_i64(v, s, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+            above.append(ofl - beta_nosat(v, s, wl, osign))
+            (gwl, gfl, gsign, gst), _ = run_fl_search(fx, h, fx.src_int(dev(v.astype(np.int32)), fx.I32, sd),
+                                                      n, wl, fx.SIGN_AUTO)
+            assert (gfl, gsign, gst) == (ofl, osign, 0), (seed, wl)
+            ffl, fsign, _ = orc.fl_search_f32(x32, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+            (gwl, gfl, gsign, gst), _ = run_fl_search(fx, h, fx.src_f32(dev(x32)), n, wl, fx.SIGN_AUTO)
+            assert (gfl, gsign, gst) == (ffl, fsign, 0), (seed, wl)
+    # the fixture exercises the window alone, a short exact range and a long one
+    assert min(above) <= 1 and any(2 <= a <= 5 for a in above) and max(above) >= 6, above
+    check_flags(fx, h)
+
+
 # ----------------------------------------------------------------------------
 # GEMM / conv with the C-Block epilogue
 # ----------------------------------------------------------------------------
