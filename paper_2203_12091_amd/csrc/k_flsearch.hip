@@ -26,6 +26,9 @@
 
 namespace fxpq {
 
+// Register sets of the window pass's packet pipeline.
+constexpr int kWinSets = 4;
+
 // Main loop of the streaming window pass over this thread's values.
 template <int KIND, int DT, bool NONNEG, bool CLAMP0, int NB>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
@@ -44,7 +47,7 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   // scaled by 2^(sigma - sv) = 2^(fl_hi + 24), exactly.
   const double post = u.wscale;
   const int64_t nfull = n - n % PK::EP;
-  stream_packets<KIND, DT>(s, n, tv, [&](const double* v, int64_t, int) {
+  stream_packets<KIND, DT, false, kWinSets>(s, n, tv, [&](const double* v, int64_t, int) {
 #pragma unroll
     for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j]);
   });

@@ -134,11 +134,12 @@ __device__ inline void unpack(const Raw<KIND, DT>& r, const ThreadVals<Pack<KIND
 // consumed), so the number of loads in flight is fixed and the wait before
 // each use only covers the older one.  Values past the last whole packet are
 // left to the caller.
-template <int KIND, int DT, bool AUX = false, typename F>
+template <int KIND, int DT, bool AUX = false, int NSET = 2, typename F>
 __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
                                       F&& fp, const int8_t* aux = nullptr) {
   // AUX: one byte per value of `aux`, loaded with each packet and handed to
-  // fp as the packet's EP bytes (4-value packets only).
+  // fp as the packet's EP bytes (4-value packets only).  NSET register sets
+  // rotate: NSET - 1 packets stay in flight while one is consumed.
   static_assert(!AUX || Pack<KIND, DT>::EP == 4, "aux bytes need 4-value packets");
   using PK = Pack<KIND, DT>;
   const int64_t chunk = (int64_t)kThreads * PK::V;
@@ -167,15 +168,16 @@ __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVa
     }
   };
   int64_t base = (int64_t)blockIdx.x * chunk;
-  Raw<KIND, DT> ra[PK::P], rb[PK::P];
-  int xa[PK::P] = {}, xb[PK::P] = {};
-  load_set(base, ra, xa);
-  load_set(base + stride, rb, xb);
-  for (; base < nfull; base += 2 * stride) {
-    use_set(base, ra, xa);
-    load_set(base + 2 * stride, ra, xa);
-    use_set(base + stride, rb, xb);
-    load_set(base + 3 * stride, rb, xb);
+  Raw<KIND, DT> rs[NSET][PK::P];
+  int xs[NSET][PK::P] = {};
+#pragma unroll
+  for (int k = 0; k < NSET; ++k) load_set(base + k * stride, rs[k], xs[k]);
+  for (; base < nfull; base += NSET * stride) {
+#pragma unroll
+    for (int k = 0; k < NSET; ++k) {
+      use_set(base + k * stride, rs[k], xs[k]);
+      load_set(base + (NSET + k) * stride, rs[k], xs[k]);
+    }
   }
 }
 
