@@ -43,9 +43,10 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
-    ap.add_argument("--mode", choices=["bench", "profile", "copy"], default="bench",
+    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep"], default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
-                         "copy: one plain 1 GiB device copy (counter calibration)")
+                         "copy: one plain 1 GiB device copy (counter calibration); "
+                         "sweep: the sensitivity sweep figures only")
     return ap.parse_args()
 
 
@@ -85,6 +86,39 @@ def cpu_baseline(batch):
             "sample": f"ResNet-50 DFX calibration forward of {batch} images 224x224 "
                       f"(exact CPU oracle, parameters pre-quantized; {t:.1f} s forward, "
                       f"{t0 - t_prep:.1f} s set-up untimed)"}
+
+
+def compute_bound_mfma(net, dev):
+    """int8 MFMA use over the convolutions whose arithmetic intensity (int8
+    ops per HBM byte: input codes, weights, int32 output) is above the ridge
+    point peak / HBM bandwidth (625), i.e. the ones the matrix cores bound;
+    one more untimed forward with an event pair around each conv call."""
+    import torch
+    ridge = INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    net.prepare_timers(1, classes=("qconv",))
+    net.forward()
+    torch.cuda.synchronize(dev)
+    calls = [c for c in net.calls if c[0] == "qconv"]
+    ops = ms = 0.0
+    layers = 0
+    for (cls, work, fn, args), (_, _, e0, e1) in zip(calls, net.timers):
+        if fn.__name__ != "fxpq_qconv":
+            continue
+        d = args[1]._obj
+        ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
+        wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
+        m = d.n * ho * wo
+        hbm = d.n * d.h * d.w * d.c + d.k * d.r * d.s * d.c + 4 * m * d.k
+        if work / hbm > ridge:
+            ops += work
+            ms += e0.elapsed_time(e1)
+            layers += 1
+    net.timers = None
+    if not layers:
+        return None
+    tops = ops / (ms * 1e-3) / 1e12
+    return {"layers": layers, "ridge_ops_per_byte": round(ridge, 1), "achieved": round(tops, 1),
+            "frac": round(tops / INT8_PEAK_TOPS, 4), "ms_per_forward": round(ms, 3)}
 
 
 def sweep_figures(dev):
@@ -131,6 +165,10 @@ def main():
         print(json.dumps({"copy_bytes": src.numel() * 4}), flush=True)
         return
 
+    if args.mode == "sweep":
+        print(json.dumps(sweep_figures(dev)), flush=True)
+        return
+
     net = nets.CalibNet("resnet50", batch=BATCH, image=IMAGE, device="cuda:0")
     for _ in range(args.warmup):
         net.forward()
@@ -167,6 +205,7 @@ def main():
     net.forward()
     cb_ms, cb_n, cb_ops = fx.timer_read(net.h)
     fx.timer_start(net.h, fx.TIMER_OFF)
+    cbound = compute_bound_mfma(net, dev)
 
     ms = elapsed * 1000.0 / args.steps
     value = BATCH * args.steps / elapsed
@@ -201,6 +240,8 @@ def main():
         "requant": {"kernel": "k_requant", "achieved": round(rq_bytes / (rq_ms * 1e-3) / 1e9, 1),
                     "unit": "GB/s", "ms_per_forward": round(rq_ms, 3), "launches": rq_n},
     }
+    if cbound:
+        out["mfma"]["compute_bound_layers"] = cbound
     if cb_n:
         out["fused_cblock"] = {"kernel": "k_qconv (min/max, FL-window and requant epilogues)",
                                "passes": cb_n, "ms_per_forward": round(cb_ms, 3),
