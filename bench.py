@@ -237,9 +237,10 @@ def main():
                  "unit": "TOP/s", "peak": INT8_PEAK_TOPS,
                  "frac": round(cv_ops / (cv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
                  "ms_per_forward": round(cv_ms, 3), "launches": cv_n},
-        "requant": {"kernel": "k_requant", "achieved": round(rq_bytes / (rq_ms * 1e-3) / 1e9, 1),
-                    "unit": "GB/s", "ms_per_forward": round(rq_ms, 3), "launches": rq_n},
     }
+    if rq_n:
+        out["requant"] = {"kernel": "k_requant", "achieved": round(rq_bytes / (rq_ms * 1e-3) / 1e9, 1),
+                          "unit": "GB/s", "ms_per_forward": round(rq_ms, 3), "launches": rq_n}
     if cbound:
         out["mfma"]["compute_bound_layers"] = cbound
     if cb_n:

@@ -218,6 +218,32 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
                            int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out, double* d_sse);
 
 /*
+ * FxP-QLayer in one call (Sec. "FxP-QLayer" with the search of Sec.
+ * "Quantization Parameters Optimization"): the chosen format in d_fmt_out
+ * and the codes are bit for bit those of
+ *     fxpq_fl_search(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, NULL);
+ *     fxpq_requant(h, src, n, d_fmt_out, codes, FXPQ_C8);
+ * but the search's read of the values also writes the codes of its two
+ * likeliest formats (fl = beta_nosat, the largest fl at which no value
+ * saturates, and beta_nosat + 1): one set to `codes`, the other to
+ * `codes_alt`, so the values are normally read once.  Afterwards nothing more
+ * runs when the chosen format's codes are in `codes`, a copy of n bytes when
+ * they are in `codes_alt`, and a requantization pass otherwise.  The format
+ * d_fmt_out holds on entry (e.g. this layer's format from the previous
+ * batch) picks which candidate goes to `codes`; when it is one of the two
+ * candidates (same wl and sign, status 0) the other candidate's codes are not
+ * written, and should it win, the requantization pass produces them.  Any
+ * content of d_fmt_out on entry is valid.
+ * codes_alt: device, n bytes, caller-owned scratch, contents unspecified
+ * afterwards.  Requirements: code_type FXPQ_C8, 2 <= wl <= 8, codes and
+ * codes_alt 16-byte aligned, the rest as fxpq_fl_search.  Sources with 8-byte
+ * values (FXPQ_SRC_INT over int64) run the two calls above.
+ */
+fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
+                        int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out, void* codes,
+                        fxpq_dtype code_type, void* codes_alt);
+
+/*
  * Quantized convolution (C-Block contraction, Sec. "Integer-Only Inference"):
  * acc[n][oh][ow][k] = sum_{r,s,c} x[n][oh*stride-pad+r][ow*stride-pad+s][c] * w[k][r][s][c]
  * with zero padding (value 0 in either code dtype), int32 accumulation on the

@@ -188,7 +188,17 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
 hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo, int nce,
                                  int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
-                                 int nb, fxpq_fmt* out);
+                                 int nb, fxpq_fmt* out, int codes);
+struct FlsPlan;
+// FL search + requantization to 8-bit codes (fused FxP-QLayer; C8 storage).
+hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
+                         int fl_hi, const double* d_minmax, fxpq_fmt* out, int8_t* codes,
+                         int8_t* alt);
+// Requantization to C8 codes gated by a fused search's plan: nothing when
+// `codes` already holds the chosen format's codes, a copy from `alt` when it
+// holds them, else requantization.
+hipError_t launch_requant_gated(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
+                                int8_t* codes, const FlsPlan* plan, const int8_t* alt);
 hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
                               int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,

@@ -15,6 +15,11 @@ struct FlsPlan {
   int gen_extra;  // INT_MIN when none
   int sign;
   int status;
+  // Codes written by the window pass of a fused FxP-QLayer: when spec != 0,
+  // the output codes hold the codes at fl = spec_fl[0] and the alternate
+  // buffer those at fl = spec_fl[1].
+  int spec;
+  int spec_fl[2];
 };
 
 enum FlsMode { MODE_SEARCH = 0, MODE_REPORT = 1 };
@@ -216,7 +221,7 @@ __device__ inline void win_acc_zero(WinAcc& acc) {
 //   NONNEG   every value is >= 0: no lower clamp, no lower clipping term;
 //   CLAMP0   the first candidate can saturate (it is not beta_nosat).
 template <bool SPLIT, bool NONNEG, bool CLAMP0, int NB = 1>
-__device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
+__device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W, double (&qo)[kWindow]) {
   double Wh = 0.0, Wl = W;
   if (SPLIT) {
     Wh = floor(W * kTwoM26);
@@ -233,6 +238,7 @@ __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
     acc.A[j] = fma(q, q, acc.A[j]);
     if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
     acc.PL[j] = fma(Wl, q, acc.PL[j]);
+    qo[j] = q;
   }
   // clipping error at the first NB fl above the window: W * 2^(fl - sigma)
   // doubles (exactly) from one to the next
@@ -247,6 +253,12 @@ __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
       acc.CE[k] = fma(d2, d2, acc.CE[k]);
     }
   }
+}
+
+template <bool SPLIT, bool NONNEG, bool CLAMP0, int NB = 1>
+__device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
+  double q[kWindow];
+  win_consume<SPLIT, NONNEG, CLAMP0, NB>(c, acc, W, q);
 }
 
 // Variant index (NONNEG << 1 | CLAMP0).
@@ -264,6 +276,7 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
   plan->status = 0;
   plan->need_general = 0;
   plan->gen_extra = INT_MIN;
+  plan->spec = 0;
   if (ws.verdict == 1) {
     *out = fxpq_fmt{wl, fl_hi, ws.u.sign, 0};
   } else if (ws.verdict == 2) {

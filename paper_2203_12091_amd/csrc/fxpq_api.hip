@@ -290,6 +290,39 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
   return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
 }
 
+fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
+                        int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out, void* codes,
+                        fxpq_dtype code_type, void* codes_alt) {
+  if (!h || n < 1 || !d_fmt_out || !codes || !codes_alt) return FXPQ_ERR_INVALID_ARG;
+  if (code_type != FXPQ_C8) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 1 || wl > 8) return FXPQ_ERR_INVALID_ARG;
+  if (wl == 1) return FXPQ_ERR_UNSUPPORTED;
+  if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
+  if (!aligned(codes, 16) || !aligned(codes_alt, 16)) return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  if (n / ((int64_t)kThreads * kWinMaxPerThread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  DeviceGuard g(h->device);
+  Ctx c = ctx(h);
+  const double* mm = src->d_minmax;
+  if (!mm) {
+    hipError_t e = launch_minmax(c, s, n, h->sc.minmax);
+    if (e != hipSuccess) return FXPQ_ERR_HIP;
+    mm = h->sc.minmax;
+  }
+  if (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) {
+    // 2-value packets: the search and the requantization run as two passes
+    hipError_t e = launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, nullptr);
+    if (e != hipSuccess) return hip_status(e);
+    return hip_status(launch_requant(c, s, n, d_fmt_out, codes, code_type));
+  }
+  return hip_status(launch_qlayer(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out,
+                                  static_cast<int8_t*>(codes), static_cast<int8_t*>(codes_alt)));
+}
+
 static fxpq_status conv_check(const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
                               const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
                               const int32_t* acc) {

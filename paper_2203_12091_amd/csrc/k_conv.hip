@@ -681,7 +681,7 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   conv_run<EPI_WIN>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
   e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, 1, fl_hi, MODE_SEARCH, conv_per_thread(cfg), d_minmax,
-                            nb, out);
+                            nb, out, 0);
   if (e != hipSuccess) return e;
   // 3. only when the plan asks for the general pass: int32 accumulators, then
   //    the exact search over every remaining candidate

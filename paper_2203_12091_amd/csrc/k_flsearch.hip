@@ -29,14 +29,47 @@ namespace fxpq {
 // Register sets of the window pass's packet pipeline.
 constexpr int kWinSets = 4;
 
+// 8-bit codes of the window candidates, written while the values are read
+// (fused FxP-QLayer): candidate j's codes go to y[j] (none when null), as
+// bytes q (signed formats) or q - 128 (unsigned formats; q ^ 0x80 for
+// 0 <= q <= 255).
+struct WinCodes {
+  int8_t* y[kWindow];
+  int qmax;
+  unsigned xorw;  // 0x80808080 for unsigned formats, else 0
+};
+
+// Packs EP codes (one byte each) and stores them at y + i (4-byte aligned).
+template <int EP>
+__device__ inline void store_codes(int8_t* y, int64_t i, const int* c, unsigned xorw) {
+  unsigned w[EP / 4];
+#pragma unroll
+  for (int k = 0; k < EP / 4; ++k)
+    w[k] = ((unsigned)(c[4 * k] & 0xFF) | ((unsigned)(c[4 * k + 1] & 0xFF) << 8) |
+            ((unsigned)(c[4 * k + 2] & 0xFF) << 16) | ((unsigned)c[4 * k + 3] << 24)) ^ xorw;
+  if constexpr (EP == 16)
+    *reinterpret_cast<uint4*>(y + i) = make_uint4(w[0], w[1], w[2], w[3]);
+  else
+    *reinterpret_cast<unsigned*>(y + i) = w[0];
+}
+
 // Main loop of the streaming window pass over this thread's values.
-template <int KIND, int DT, bool NONNEG, bool CLAMP0, int NB>
+template <int KIND, int DT, bool NONNEG, bool CLAMP0, int NB, bool CODES>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
-                                WinAcc& acc) {
+                                const WinCodes& wcd, WinAcc& acc) {
   const WinCtx wc = win_ctx(u, ws);
   win_acc_zero(acc);
-  auto consume = [&](double W) {
-    win_consume<KIND == FXPQ_SRC_F32, NONNEG, CLAMP0, NB>(wc, acc, W);
+  // Codes of one value: the window's codes are clamped except candidate 0
+  // when it cannot saturate (beta_nosat), where a value at qmax + 1/2 rounds
+  // to qmax + 1 (same error either way, but the code must be clamped).
+  auto consume = [&](double W, int* cq) {
+    double q[kWindow];
+    win_consume<KIND == FXPQ_SRC_F32, NONNEG, CLAMP0, NB>(wc, acc, W, q);
+    if constexpr (CODES) {
+#pragma unroll
+      for (int j = 0; j < kWindow; ++j) cq[j] = (int)q[j];
+      if (!CLAMP0) cq[0] = min(cq[0], wcd.qmax);
+    }
   };
 
   using PK = Pack<KIND, DT>;
@@ -47,20 +80,62 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   // scaled by 2^(sigma - sv) = 2^(fl_hi + 24), exactly.
   const double post = u.wscale;
   const int64_t nfull = n - n % PK::EP;
-  stream_packets<KIND, DT, false, kWinSets>(s, n, tv, [&](const double* v, int64_t, int) {
+  stream_packets<KIND, DT, false, kWinSets>(s, n, tv, [&](const double* v, int64_t i0, int) {
+    int cq[PK::EP][kWindow];
 #pragma unroll
-    for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j]);
+    for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j], cq[j]);
+    if constexpr (CODES) {
+#pragma unroll
+      for (int k = 0; k < kWindow; ++k) {
+        if (!wcd.y[k]) continue;
+        int c[PK::EP];
+#pragma unroll
+        for (int j = 0; j < PK::EP; ++j) c[j] = cq[j][k];
+        store_codes<PK::EP>(wcd.y[k], i0, c, wcd.xorw);
+      }
+    }
   });
   if (gtid == 0)
-    for (int64_t i = nfull; i < n; ++i) consume(load1<KIND, DT>(s, i) * u.wscale);
+    for (int64_t i = nfull; i < n; ++i) {
+      int cq[kWindow];
+      consume(load1<KIND, DT>(s, i) * u.wscale, cq);
+      if constexpr (CODES) {
+#pragma unroll
+        for (int k = 0; k < kWindow; ++k)
+          if (wcd.y[k]) wcd.y[k][i] = (int8_t)((cq[k] & 0xFF) ^ (wcd.xorw & 0xFF));
+      }
+    }
+}
+
+// Which window candidate's codes go to the output buffer of a fused
+// FxP-QLayer: candidate 1 when the format found by the previous search into
+// the same format (still in `out`) is that candidate's, else candidate 0.
+// When that format is one of the window's candidates (same word length and
+// sign, no error) the other candidate's codes are not written at all (a
+// requantization pass follows if it wins); otherwise they go to the
+// alternate buffer.
+struct SpecPick {
+  int pj;
+  bool both;
+};
+
+__device__ inline SpecPick spec_pick(const WinSetup& ws, int wl, const fxpq_fmt* out) {
+  const fxpq_fmt o = *out;
+  SpecPick p;
+  p.pj = (ws.nc == 2 && o.fl == ws.b0 + 1) ? 1 : 0;
+  const bool known = o.wl == wl && o.status == 0 && o.sign == ws.u.sign &&
+                     (o.fl == ws.b0 || o.fl == ws.b1);
+  p.both = !known;
+  return p;
 }
 
 // NB clipping bounds above the window (1, or kCeBounds for short word lengths).
-template <int KIND, int DT, int NB>
+// CODES: also writes both candidates' 8-bit codes (fused FxP-QLayer).
+template <int KIND, int DT, int NB, bool CODES>
 __global__ __launch_bounds__(kThreads) void k_fls_window(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
     const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out,
-    unsigned* flags) {
+    unsigned* flags, int8_t* y, int8_t* y_alt) {
   __shared__ long long shl[8];
   __shared__ double shd[8];
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
@@ -71,12 +146,21 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     if (blockIdx.x == 0 && threadIdx.x == 0) win_verdict_write(ws, wl, fl_lo, fl_hi, plan, out, flags);
     return;
   }
+  WinCodes wcd{};
+  if constexpr (CODES) {
+    const SpecPick sp = spec_pick(ws, wl, out);
+    int8_t* other = sp.both ? y_alt : nullptr;
+    wcd.y[0] = sp.pj ? other : y;
+    wcd.y[1] = sp.pj ? y : other;
+    wcd.qmax = (int)u.qmax;
+    wcd.xorw = u.sign ? 0u : 0x80808080u;
+  }
   WinAcc acc;
   switch (win_variant(u, ws, mm)) {
-    case 0: win_loop<KIND, DT, false, false, NB>(s, n, u, ws, acc); break;
-    case 1: win_loop<KIND, DT, false, true, NB>(s, n, u, ws, acc); break;
-    case 2: win_loop<KIND, DT, true, false, NB>(s, n, u, ws, acc); break;
-    default: win_loop<KIND, DT, true, true, NB>(s, n, u, ws, acc); break;
+    case 0: win_loop<KIND, DT, false, false, NB, CODES>(s, n, u, ws, wcd, acc); break;
+    case 1: win_loop<KIND, DT, false, true, NB, CODES>(s, n, u, ws, wcd, acc); break;
+    case 2: win_loop<KIND, DT, true, false, NB, CODES>(s, n, u, ws, wcd, acc); break;
+    default: win_loop<KIND, DT, true, true, NB, CODES>(s, n, u, ws, wcd, acc); break;
   }
   win_write_partials(acc, NB, blockIdx.x, part_i, part_f, shl, shd);
 }
@@ -97,7 +181,7 @@ __device__ inline double i128_to_double(__int128 v) {
 template <int KIND>
 __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
     SrcDev s, int wl, int sign_req, int fl_lo, int nce, int fl_hi, int mode, int64_t per_thread,
-    const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out) {
+    const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out, int codes) {
   constexpr int NQ = 3 * kWindow;
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
   if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
@@ -199,6 +283,14 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   }
   plan->sign = u.sign;
   plan->status = 0;
+  plan->spec = codes;
+  if (codes) {
+    // the window pass wrote candidate pj's codes to the output buffer (and
+    // the other's to the alternate buffer when both)
+    const SpecPick sp = spec_pick(ws, wl, out);
+    plan->spec_fl[0] = b0 + sp.pj;
+    plan->spec_fl[1] = sp.both ? b0 + (nc == 2 ? 1 - sp.pj : 0) : INT_MIN;
+  }
   if (done) {
     plan->need_general = 0;
     *out = fxpq_fmt{wl, fl_win, u.sign, 0};
@@ -394,12 +486,12 @@ __device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int si
 
 hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo, int nce,
                                  int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
-                                 int nb, fxpq_fmt* out) {
+                                 int nb, fxpq_fmt* out, int codes) {
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window_fin<K_><<<1, kFinThreads, 0, c.stream>>>(
                         s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
-                        c.sc.win_part_f, plan, out)));
+                        c.sc.win_part_f, plan, out, codes)));
   return hipGetLastError();
 }
 
@@ -423,14 +515,21 @@ static int64_t window_per_thread(int64_t n, int blocks, int vec) {
   return ((n / vec + threads - 1) / threads) * vec + vec;
 }
 
-hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
-                            int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
+// Window pass (+ its finalize and the general pass when needed).  With y
+// and y_alt (fused FxP-QLayer, 8-bit codes) the window pass also writes the
+// codes of its two candidates.
+static hipError_t fl_search_passes(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign,
+                                   int fl_lo, int fl_hi, const double* d_minmax, fxpq_fmt* out,
+                                   double* d_sse, int8_t* y, int8_t* y_alt) {
   int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
   const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;  // Pack<>::V
   const int nce = (wl <= kCeMultiMaxWl) ? kCeBounds : 1;
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   int mode = d_sse ? MODE_REPORT : MODE_SEARCH;
-  const double elem_bytes = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
+  const bool codes = y != nullptr;
+  // algorithmic bytes: the values read once (+ one code per value written)
+  const double elem_bytes = ((s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0) +
+                            (codes ? 1.0 : 0.0);
   int64_t per_thread = 0;
   int blocks = 0;
   auto run = [&](auto kernel) {
@@ -439,18 +538,42 @@ hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, in
     bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
     kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, mode, per_thread,
                                               d_minmax, c.sc.win_part, c.sc.win_part_f, plan, out,
-                                              c.sc.flags);
+                                              c.sc.flags, y, y_alt);
     timer_end(c, timed, elem_bytes * (double)n);
   };
-  if (nce == 1) {
-    FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, 1>)));
+  if (codes) {
+    // 4- and 16-value packets only (fp32, C-Block and eltwise sources)
+    if (nce == 1) {
+      FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, 1, Pack<K_, D_>::EP != 2>)));
+    } else {
+      FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, kCeBounds, Pack<K_, D_>::EP != 2>)));
+    }
+  } else if (nce == 1) {
+    FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, 1, false>)));
   } else {
-    FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, kCeBounds>)));
+    FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, kCeBounds, false>)));
   }
   hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax,
-                                       blocks, out);
+                                       blocks, out, codes ? 1 : 0);
   if (e != hipSuccess) return e;
   return launch_fls_general(c, s, n, wl, fl_lo, fl_hi, d_minmax, out, d_sse);
+}
+
+hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
+                            int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
+  return fl_search_passes(c, s, n, wl, sign, fl_lo, fl_hi, d_minmax, out, d_sse, nullptr, nullptr);
+}
+
+// Fused FxP-QLayer: the search writes both window candidates' codes; a gated
+// requantization then does nothing when the chosen format's codes are already
+// in `codes`, copies them from `alt` when they are there, and requantizes
+// otherwise.
+hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
+                         int fl_hi, const double* d_minmax, fxpq_fmt* out, int8_t* codes,
+                         int8_t* alt) {
+  hipError_t e = fl_search_passes(c, s, n, wl, sign, fl_lo, fl_hi, d_minmax, out, nullptr, codes, alt);
+  if (e != hipSuccess) return e;
+  return launch_requant_gated(c, s, n, out, codes, static_cast<const FlsPlan*>(c.sc.plan), alt);
 }
 
 }  // namespace fxpq

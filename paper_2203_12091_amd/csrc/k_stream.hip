@@ -8,7 +8,7 @@
 #include <mutex>
 #include <unordered_map>
 
-#include "values.hpp"
+#include "fls.hpp"
 
 namespace fxpq {
 
@@ -131,6 +131,15 @@ hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* o
 // ----------------------------------------------------------------------------
 // Quantize / requantize.
 // ----------------------------------------------------------------------------
+// dst[i] = src[i] for i < n over the grid (both 16-byte aligned).
+__device__ inline void copy_bytes(const int8_t* src, int8_t* dst, int64_t n) {
+  const int64_t n16 = n / 16;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n16; i += stride)
+    reinterpret_cast<int4*>(dst)[i] = reinterpret_cast<const int4*>(src)[i];
+  if (blockIdx.x == 0 && threadIdx.x < n % 16) dst[16 * n16 + threadIdx.x] = src[16 * n16 + threadIdx.x];
+}
+
 template <int OUT, int V>
 __device__ inline void storev(void* codes, int64_t i, const int c[V]) {
   if constexpr (OUT == FXPQ_I8 || OUT == FXPQ_U8OFF || OUT == FXPQ_C8) {
@@ -180,7 +189,17 @@ __device__ inline void store1(void* codes, int64_t i, int c) {
 
 template <int KIND, int DT, int OUT>
 __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const fxpq_fmt* fmt,
-                                                      void* codes, unsigned* flags) {
+                                                      void* codes, unsigned* flags,
+                                                      const FlsPlan* gate, const int8_t* alt) {
+  if (gate && gate->spec && fmt->status == 0) {
+    // fused FxP-QLayer: the search already wrote the codes of its window
+    const int fl = fmt->fl;
+    if (fl == gate->spec_fl[0]) return;
+    if (fl == gate->spec_fl[1]) {
+      copy_bytes(alt, static_cast<int8_t*>(codes), n);
+      return;
+    }
+  }
   const int sv = src_scale(s);
   const QFmt q = qfmt_setup<OUT>(fmt, sv, flags);
   if (!q.ok) return;
@@ -442,13 +461,19 @@ __global__ __launch_bounds__(kThreads) void k_requant_addmm(SrcDev s, int64_t n,
 
 template <int OUT>
 static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
-                        void* codes) {
+                        void* codes, const FlsPlan* gate = nullptr, const int8_t* alt = nullptr) {
   int blocks = 1;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (blocks = stream_grid(n, src_channels(s), 0, src_vec(s),
                                           resident_blocks(c, (const void*)&k_requant<K_, D_, OUT>)),
                      k_requant<K_, D_, OUT><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes,
-                                                                             c.sc.flags)));
+                                                                             c.sc.flags, gate, alt)));
+}
+
+hipError_t launch_requant_gated(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
+                                int8_t* codes, const FlsPlan* plan, const int8_t* alt) {
+  requant_out<FXPQ_C8>(c, s, n, fmt, codes, plan, alt);
+  return hipGetLastError();
 }
 
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,

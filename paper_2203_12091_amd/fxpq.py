@@ -20,7 +20,7 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
-    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qconv", "fxpq_qgemm",
+    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_cblock", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
     "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
@@ -79,6 +79,7 @@ def lib():
             "fxpq_requant": [p, p, i64, p, p, C.c_int],
             "fxpq_requant_addmm": [p, p, i64, p, p, C.c_int, p, C.c_int, p, i32, p],
             "fxpq_fl_search": [p, p, i64, i32, i32, i32, i32, p, p],
+            "fxpq_qlayer": [p, p, i64, i32, i32, i32, i32, p, p, C.c_int, p],
             "fxpq_qconv": [p, p, p, C.c_int, p, p, p, p, p],
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
             "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
@@ -184,6 +185,11 @@ def requant_addmm(h, src, n, d_fmt, codes, code_type, b, b_type, d_fmt_b, relu, 
 def fl_search(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, d_sse=None):
     _call("fxpq_fl_search", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out),
           ptr(d_sse))
+
+
+def qlayer(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, codes, code_type, codes_alt):
+    _call("fxpq_qlayer", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out), ptr(codes),
+          code_type, ptr(codes_alt))
 
 
 def qconv(h, desc, x, x_type, w, w_colsum, ep, acc, d_minmax=None):

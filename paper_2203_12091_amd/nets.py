@@ -152,9 +152,10 @@ class CalibNet:
     buffers and the input; ``forward()`` enqueues a full calibration forward."""
 
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", wl_override=None,
-                 keep_acts=True, fused=False):
+                 keep_acts=True, fused=False, qlayer=True):
         import torch
         self.fused = fused
+        self.qlayer = qlayer
         self.torch = torch
         self.name = name
         self.seed = SEEDS[name] if seed is None else seed
@@ -293,6 +294,9 @@ class CalibNet:
                 self.act_fmt[n.name] = self._fmt()
                 self.act_codes[n.name] = self._empty((B, 1, 1, C), T.int8)
         self.acc = self._empty((acc_max,), T.int32)
+        # alternate codes of the fused FxP-QLayer calls (one tensor's worth)
+        code_max = max(c.numel() for c in self.act_codes.values())
+        self.code_alt = self._empty((code_max + 16,), T.int8)
         self.logits = None
         # parameter formats back to the host (once)
         T.cuda.synchronize(self.dev)
@@ -348,7 +352,7 @@ class CalibNet:
         produced_at = {n.name: i for i, (op, n, *r) in enumerate(self.ops)}
         addmm = {}
         for op, n, *rest in self.ops:
-            if op == "add":
+            if op == "add" and not self.qlayer:
                 last = max((n.inp, n.other), key=lambda nm: produced_at[nm])
                 first = n.other if last == n.inp else n.inp
                 lop, ln, *lr = self.ops[produced_at[last]]
@@ -360,10 +364,15 @@ class CalibNet:
                 f, c = self.act_fmt["input"], self.act_codes["input"]
                 src = fx.src_f32(self.x_dev)
                 keep.append(src)
-                add("fl_search_f32", 4 * self.n_input, L.fxpq_fl_search, h, C.byref(src),
-                    self.n_input, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), None)
-                add("quantize", 5 * self.n_input, L.fxpq_quantize, h, self.x_dev.data_ptr(),
-                    self.n_input, f.data_ptr(), c.data_ptr(), fx.C8)
+                if self.qlayer:
+                    add("fl_search_f32", 5 * self.n_input, L.fxpq_qlayer, h, C.byref(src), self.n_input,
+                        A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), c.data_ptr(), fx.C8,
+                        self.code_alt.data_ptr())
+                else:
+                    add("fl_search_f32", 4 * self.n_input, L.fxpq_fl_search, h, C.byref(src),
+                        self.n_input, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f.data_ptr(), None)
+                    add("quantize", 5 * self.n_input, L.fxpq_quantize, h, self.x_dev.data_ptr(),
+                        self.n_input, f.data_ptr(), c.data_ptr(), fx.C8)
                 add("layer_error", 5 * self.n_input, L.fxpq_layer_error, h, self.x_dev.data_ptr(),
                     c.data_ptr(), fx.C8, f.data_ptr(), self.n_input, self.le_out.data_ptr())
             elif op in ("conv", "fc"):
@@ -397,6 +406,11 @@ class CalibNet:
                         p["logit_fmt"].data_ptr() + 4)
                     add("requant", 8 * n_out, L.fxpq_requant, h, C.byref(src), n_out,
                         p["logit_fmt"].data_ptr(), self.logits.data_ptr(), fx.I32)
+                elif self.qlayer:
+                    # FL search + requantization, one read of the accumulators
+                    add("fl_search", 5 * n_out, L.fxpq_qlayer, h, C.byref(src), n_out, A_WL,
+                        fx.SIGN_AUTO, FL_LO, FL_HI, self.act_fmt[n.name].data_ptr(),
+                        self.act_codes[n.name].data_ptr(), fx.C8, self.code_alt.data_ptr())
                 else:
                     f = self.act_fmt[n.name]
                     add("fl_search", 4 * n_out, L.fxpq_fl_search, h, C.byref(src), n_out, A_WL,
@@ -424,6 +438,11 @@ class CalibNet:
                 keep.append(src)
                 f = self.act_fmt[n.name]
                 m = a.numel()
+                if self.qlayer:
+                    add("fl_search", 3 * m, L.fxpq_qlayer, h, C.byref(src), m, A_WL, fx.SIGN_AUTO,
+                        FL_LO, FL_HI, f.data_ptr(), self.act_codes[n.name].data_ptr(), fx.C8,
+                        self.code_alt.data_ptr())
+                    continue
                 add("fl_search", 2 * m, L.fxpq_fl_search, h, C.byref(src), m, A_WL, fx.SIGN_AUTO,
                     FL_LO, FL_HI, f.data_ptr(), None)
                 add("requant", 3 * m, L.fxpq_requant, h, C.byref(src), m, f.data_ptr(),
@@ -589,10 +608,11 @@ def run_fc(seed=0, device="cuda:0"):
 
 
 def run_config(name, seed=None, device="cuda:0", batch=None, image=None, with_codes=False,
-               wl_override=None, fused=False):
+               wl_override=None, fused=False, qlayer=True):
     if name == "fc":
         return run_fc(SEEDS["fc"] if seed is None else seed, device)
-    net = CalibNet(name, seed, batch, image, device, wl_override=wl_override, fused=fused)
+    net = CalibNet(name, seed, batch, image, device, wl_override=wl_override, fused=fused,
+                   qlayer=qlayer)
     net.forward()
     res = net.results(with_codes=with_codes)
     net.close()

@@ -63,21 +63,27 @@ def test_network_bit_exact(mods, name, batch, image):
     np.testing.assert_allclose(res["input_error"][:3], ref["input_error"][:3], rtol=1e-9)
 
 
-def test_fused_cblocks_match_unfused_forward(mods):
-    # the fused C-Block calls against the qconv -> fl_search -> requant
-    # sequence over a whole ResNet-50 forward, at a size beyond the oracle's
+def test_fused_paths_match_two_call_forward(mods):
+    # the fused C-Block calls and the fused FxP-QLayer calls against the
+    # qconv -> fl_search -> requant sequence over whole ResNet-50 forwards, at
+    # a size beyond the oracle's; two forwards each (the second one's
+    # FxP-QLayers start from the formats the first one chose)
     nets, _ = mods
-    note("net resnet50 fused vs unfused 8x112")
     res = {}
-    for fused in (True, False):
-        net = nets.CalibNet("resnet50", batch=8, image=112, fused=fused)
-        assert any(c[0] == "cblock" for c in net._plan()) == fused
-        net.forward()
-        res[fused] = net.results(with_codes=True)
+    for fused, qlayer in ((True, True), (False, True), (False, False)):
+        note("net resnet50 8x112 fused", fused, "qlayer", qlayer)
+        net = nets.CalibNet("resnet50", batch=8, image=112, fused=fused, qlayer=qlayer)
+        plan = net._plan()
+        assert any(c[0] == "cblock" for c in plan) == fused
+        assert any(c[2].__name__ == "fxpq_qlayer" for c in plan) == qlayer
+        for _ in range(2):
+            net.forward()
+            res[(fused, qlayer, _)] = net.results(with_codes=True)
         net.close()
-    a, b = res[True], res[False]
-    assert a["flags"] == 0 and b["flags"] == 0
-    assert a["fmts"] == b["fmts"]
-    for name in b["codes"]:
-        assert np.array_equal(a["codes"][name], b["codes"][name]), name
-    assert np.array_equal(a["logits"], b["logits"])
+    b = res[(False, False, 1)]
+    for key, a in res.items():
+        assert a["flags"] == 0, key
+        assert a["fmts"] == b["fmts"], key
+        for name in b["codes"]:
+            assert np.array_equal(a["codes"][name], b["codes"][name]), (key, name)
+        assert np.array_equal(a["logits"], b["logits"]), key
