@@ -32,8 +32,9 @@ struct Scratch {
   unsigned* flags;          // sticky FXPQ_FLAG_* bits
   double* minmax;           // internal [2]
   double* minmax_part;      // per-block partials [kMaxConvBlocks][2]
-  long long* win_part;      // window FL-search integer sums [kWinSlots][kWinPart] (0 between searches)
-  double* win_part_f;       // window FL-search fp64 bound sums [kWinSlots][kWinPartF] (0 between searches)
+  long long* win_part;      // window FL-search integer sums [2][kWinSlots][kWinPart]
+  double* win_part_f;       // window FL-search fp64 bound sums [2][kWinSlots][kWinPartF]
+                            // (two sets, see fls_begin; a set is 0 when a search starts on it)
   unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
   unsigned* gen_done;       // blocks of the general pass finished (0 between searches)
   void* plan;               // FlsPlan
@@ -154,7 +155,8 @@ struct Ctx {
   hipStream_t stream;
   Scratch sc;
   Timer* timer;
-  int cus;  // compute units of the handle's device
+  int cus;                  // compute units of the handle's device
+  unsigned* search_seq;     // FL searches enqueued on the handle (host counter)
 };
 
 // Brackets one launch with events when `kind` is being timed.
@@ -186,9 +188,12 @@ hipError_t launch_requant_addmm(const Ctx& c, const SrcDev& s, int64_t n, const 
                                 const fxpq_fmt* fmt_b, int relu, double* d_add_minmax);
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
                             int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse);
-hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo, int nce,
-                                 int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
-                                 int nb, fxpq_fmt* out, int codes);
+// FL searches alternate between two sets of window slots: returns this
+// search's set (the next search's finalize clears it).
+int fls_begin(const Ctx& c);
+hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int set, int wl, int sign, int fl_lo,
+                                 int nce, int fl_hi, int mode, int64_t per_thread,
+                                 const double* d_minmax, fxpq_fmt* out);
 struct FlsPlan;
 // FL search + requantization to 8-bit codes (fused FxP-QLayer; C8 storage).
 hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,

@@ -18,6 +18,7 @@ struct fxpq_handle_s {
   size_t scratch_bytes;
   Scratch sc;
   Timer timer;
+  unsigned search_seq = 0;
 };
 
 constexpr int kTimerPairs = 16384;
@@ -36,7 +37,7 @@ bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32; }
 
 size_t code_align(int t) { (void)t; return 16; }
 
-Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc, &h->timer, h->cus}; }
+Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc, &h->timer, h->cus, &h->search_seq}; }
 
 fxpq_status hip_status(hipError_t e) { return e == hipSuccess ? FXPQ_OK : FXPQ_ERR_HIP; }
 
@@ -161,8 +162,8 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   size_t o_flags = take(4);
   size_t o_mm = take(2 * sizeof(double));
   size_t o_gd = take(4);
-  size_t o_wp = take((size_t)kWinSlots * kWinPart * sizeof(long long));
-  size_t o_wpf = take((size_t)kWinSlots * kWinPartF * sizeof(double));
+  size_t o_wp = take((size_t)2 * kWinSlots * kWinPart * sizeof(long long));
+  size_t o_wpf = take((size_t)2 * kWinSlots * kWinPartF * sizeof(double));
   size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
   size_t o_gp = take((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
   size_t o_plan = take(256);

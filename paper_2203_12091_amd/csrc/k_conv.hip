@@ -672,16 +672,17 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   a.fl_lo = fl_lo;
   a.fl_hi = fl_hi;
   a.mm = d_minmax;
-  a.part_i = c.sc.win_part;
-  a.part_f = c.sc.win_part_f;
+  const int set = fls_begin(c);
+  a.part_i = c.sc.win_part + (size_t)set * kWinSlots * kWinPart;
+  a.part_f = c.sc.win_part_f + (size_t)set * kWinSlots * kWinPartF;
   a.plan = static_cast<FlsPlan*>(c.sc.plan);
   a.fmt_win = out;
   a.flags = c.sc.flags;
   timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PASS);
   conv_run<EPI_WIN>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
-  e = launch_fls_window_fin(c, ep, wl, sign, fl_lo, 1, fl_hi, MODE_SEARCH, conv_per_thread(cfg), d_minmax,
-                            nb, out, 0);
+  e = launch_fls_window_fin(c, ep, set, wl, sign, fl_lo, 1, fl_hi, MODE_SEARCH, conv_per_thread(cfg),
+                            d_minmax, out);
   if (e != hipSuccess) return e;
   // 3. only when the plan asks for the general pass: int32 accumulators, then
   //    the exact search over every remaining candidate

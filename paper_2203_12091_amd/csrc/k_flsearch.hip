@@ -176,21 +176,24 @@ __device__ inline double i128_to_double(__int128 v) {
   return (double)(long long)(v >> 64) * 0x1p64 + (double)(unsigned long long)v;
 }
 
-// One wave: lane l reads (and clears) slot l of the window sums, the wave
-// adds them exactly, lane 0 decides.
-template <int KIND>
-__global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
-    SrcDev s, int wl, int sign_req, int fl_lo, int nce, int fl_hi, int mode, int64_t per_thread,
-    const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out, int codes) {
+// Decision of the window pass, taken by one wave from the slot sums.
+struct WinResult {
+  int done;     // the window's best candidate is the answer
+  int fl_win;   // the window's best candidate
+  int gen_hi;   // top of the candidates the exact pass still has to evaluate
+};
+
+// Lane l reads slot l of the window sums (part_i / part_f, one set), the
+// wave adds them exactly, lane 0 decides (its result only is meaningful).
+__device__ inline WinResult win_decide(const WinSetup& ws, int nce, int fl_hi,
+                                       const long long* part_i, const double* part_f) {
   constexpr int NQ = 3 * kWindow;
-  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
-  if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
   const FlsU& u = ws.u;
   const int b0 = ws.b0, b1 = ws.b1, nc = ws.nc, bce = ws.bce;
-  const int lane = threadIdx.x;
+  const int lane = threadIdx.x & 63;
   // The high and low 32-bit halves of each quantity are summed separately
   // (both sums stay far below 2^63).
-  long long* p = part_i + lane * kWinPart;
+  const long long* p = part_i + lane * kWinPart;
   long long hi[NQ], lo[NQ];
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) {
@@ -199,12 +202,7 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   }
   double f[kWinPartF];
 #pragma unroll
-  for (int k = 0; k < kWinPartF; ++k) {
-    f[k] = part_f[kWinPartF * lane + k];
-    part_f[kWinPartF * lane + k] = 0.0;
-  }
-#pragma unroll
-  for (int k2 = 0; k2 < kWinPart; ++k2) p[k2] = 0;
+  for (int k = 0; k < kWinPartF; ++k) f[k] = part_f[kWinPartF * lane + k];
 #pragma unroll
   for (int qi = 0; qi < NQ; ++qi) {
     hi[qi] = wave_reduce(hi[qi], OpAddL());
@@ -212,7 +210,8 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   }
 #pragma unroll
   for (int k = 0; k < kWinPartF; ++k) f[k] = wave_reduce(f[k], OpAddD());
-  if (lane != 0) return;
+  WinResult r{0, 0, fl_hi};
+  if (lane != 0) return r;
   auto total = [&](int qi) -> __int128 { return ((__int128)hi[qi] << 32) + (__int128)lo[qi]; };
   // K_j = 2^(2d) A - 2^(d+1) P, d = sigma - beta; shifted by `off` >= 0 so all
   // exponents are non-negative (same factor for every candidate).
@@ -261,7 +260,7 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
     }
     kd = ldexp(big_to_double(best), -off);
   }
-  const int fl_win = b0 + bj;
+  r.fl_win = b0 + bj;
   bool done = (b1 == fl_hi);
   int gen_hi = fl_hi;
   if (!done) {
@@ -281,25 +280,56 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
     }
     done = gen_hi <= b1;
   }
-  plan->sign = u.sign;
+  r.done = done;
+  r.gen_hi = gen_hi;
+  return r;
+}
+
+// Records a window decision in the plan (and the format when it is final).
+// `codes`: the window pass wrote codes (fused FxP-QLayer); `out` still holds
+// the previous format, which picked where they went.
+__device__ inline void win_record(const WinSetup& ws, const WinResult& r, int wl, int codes,
+                                  FlsPlan* plan, fxpq_fmt* out) {
+  plan->sign = ws.u.sign;
   plan->status = 0;
   plan->spec = codes;
   if (codes) {
     // the window pass wrote candidate pj's codes to the output buffer (and
     // the other's to the alternate buffer when both)
     const SpecPick sp = spec_pick(ws, wl, out);
-    plan->spec_fl[0] = b0 + sp.pj;
-    plan->spec_fl[1] = sp.both ? b0 + (nc == 2 ? 1 - sp.pj : 0) : INT_MIN;
+    plan->spec_fl[0] = ws.b0 + sp.pj;
+    plan->spec_fl[1] = sp.both ? ws.b0 + (ws.nc == 2 ? 1 - sp.pj : 0) : INT_MIN;
   }
-  if (done) {
+  if (r.done) {
     plan->need_general = 0;
-    *out = fxpq_fmt{wl, fl_win, u.sign, 0};
+    *out = fxpq_fmt{wl, r.fl_win, ws.u.sign, 0};
   } else {
     plan->need_general = 1;
-    plan->gen_lo = b1 + 1;
-    plan->gen_hi = gen_hi;
-    plan->gen_extra = fl_win;
+    plan->gen_lo = ws.b1 + 1;
+    plan->gen_hi = r.gen_hi;
+    plan->gen_extra = r.fl_win;
   }
+}
+
+// Zeroes one set of window slots (the block's threads).
+__device__ inline void win_slots_clear(long long* part_i, double* part_f) {
+  for (int k = threadIdx.x; k < kWinSlots * kWinPart; k += blockDim.x) part_i[k] = 0;
+  for (int k = threadIdx.x; k < kWinSlots * kWinPartF; k += blockDim.x) part_f[k] = 0.0;
+}
+
+// Finalize of a window pass whose decision later launches need before the
+// general pass (fused conv path): one wave decides from slot set `part_*`
+// and clears the other set `clr_*` (used by the search before).
+template <int KIND>
+__global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
+    SrcDev s, int wl, int sign_req, int fl_lo, int nce, int fl_hi, int mode, int64_t per_thread,
+    const double* mm, const long long* part_i, const double* part_f, long long* clr_i,
+    double* clr_f, FlsPlan* plan, fxpq_fmt* out) {
+  win_slots_clear(clr_i, clr_f);
+  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
+  if (ws.verdict != 0) return;  // the pass kernel already wrote the plan
+  const WinResult r = win_decide(ws, nce, fl_hi, part_i, part_f);
+  if (threadIdx.x == 0) win_record(ws, r, wl, 0, plan, out);
 }
 
 // ---------------------------------------------------------------------------
@@ -333,24 +363,64 @@ __device__ inline double u192_to_double(const U192& a) {
          (double)(unsigned long long)a.lo;
 }
 
+// What the exact pass has to do.
+struct GenPlan {
+  int need, status, sign;
+  int glo, ghi, extra;  // candidates glo..ghi, plus `extra` unless INT_MIN
+};
+
 __device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int sigma,
-                               const FlsPlan* plan, const unsigned long long* part, fxpq_fmt* out,
+                               const GenPlan& gp, const unsigned long long* part, fxpq_fmt* out,
                                double* d_sse);
+
+// The window pass's finalize, when the general kernel takes it: every block
+// decides from the slot set (pi, pf) itself (same sums, same decision), block
+// 0 records it and clears the other slot set (ci, cf).
+struct WinIn {
+  int decide;  // 0: the plan already holds the decision
+  int sign_req, nce, mode, codes;
+  int64_t per_thread;
+  const long long* pi;
+  const double* pf;
+  long long* ci;  // may be null
+  double* cf;
+};
 
 // Exact errors of the remaining candidates over (candidate, chunk) items; the
 // last block to finish sums the chunk partials and decides.  Nothing runs
-// unless the window pass asked for it (and only then is the device-scope
-// release / acquire paid).
+// unless the window pass left candidates undecided (and only then is the
+// device-scope release / acquire paid).
 template <int KIND, int DT>
 __global__ __launch_bounds__(kThreads) void k_fls_general(
-    SrcDev s, int64_t n, int wl, int fl_lo, int fl_hi, int nchunks, const double* mm,
-    const FlsPlan* plan, unsigned long long* part, unsigned* done, fxpq_fmt* out, double* d_sse,
+    SrcDev s, int64_t n, int wl, int fl_lo, int fl_hi, int nchunks, const double* mm, WinIn wi,
+    FlsPlan* plan, unsigned long long* part, unsigned* done, fxpq_fmt* out, double* d_sse,
     unsigned* flags) {
   __shared__ unsigned long long shp[kThreads * 3];
   __shared__ int last;
-  if (!plan->need_general || plan->status) return;
-  const int sign = plan->sign;
-  const int glo = plan->gen_lo, ghi = plan->gen_hi, extra = plan->gen_extra;
+  __shared__ GenPlan gp_sh;
+  if (wi.ci && blockIdx.x == 0) win_slots_clear(wi.ci, wi.cf);
+  bool from_plan = true;
+  if (wi.decide) {
+    const WinSetup ws = win_setup<KIND>(s, mm, wl, wi.sign_req, fl_lo, fl_hi, wi.mode, wi.per_thread);
+    if (ws.verdict == 0) {  // else the window pass wrote the plan
+      from_plan = false;
+      if (threadIdx.x < 64) {
+        const WinResult r = win_decide(ws, wi.nce, fl_hi, wi.pi, wi.pf);
+        if (threadIdx.x == 0) {
+          if (blockIdx.x == 0) win_record(ws, r, wl, wi.codes, plan, out);
+          gp_sh = GenPlan{r.done ? 0 : 1, 0, ws.u.sign, ws.b1 + 1, r.gen_hi, r.fl_win};
+        }
+      }
+    }
+  }
+  if (from_plan && threadIdx.x == 0)
+    gp_sh = GenPlan{plan->need_general, plan->status, plan->sign, plan->gen_lo, plan->gen_hi,
+                    plan->gen_extra};
+  __syncthreads();
+  const GenPlan gp = gp_sh;
+  if (!gp.need || gp.status) return;
+  const int sign = gp.sign;
+  const int glo = gp.glo, ghi = gp.ghi, extra = gp.extra;
   const int nreg = ghi - glo + 1;
   const int nc = nreg + (extra != INT_MIN ? 1 : 0);
   auto cand = [&](int j) { return (extra != INT_MIN) ? (j == 0 ? extra : glo + j - 1) : glo + j; };
@@ -428,17 +498,17 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
   __syncthreads();
   if (!last) return;
   __threadfence();
-  general_decide(wl, fl_lo, fl_hi, nchunks, sigma, plan, part, out, d_sse);
+  general_decide(wl, fl_lo, fl_hi, nchunks, sigma, gp, part, out, d_sse);
   if (threadIdx.x == 0) *done = 0u;  // ready for the next search
 }
 
 // One block: totals per candidate, exact comparison, ties to the larger fl.
 __device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int sigma,
-                               const FlsPlan* plan, const unsigned long long* part, fxpq_fmt* out,
+                               const GenPlan& gp, const unsigned long long* part, fxpq_fmt* out,
                                double* d_sse) {
   __shared__ unsigned long long tot[kMaxCand][3];
-  const int sign = plan->sign;
-  const int glo = plan->gen_lo, ghi = plan->gen_hi, extra = plan->gen_extra;
+  const int sign = gp.sign;
+  const int glo = gp.glo, ghi = gp.ghi, extra = gp.extra;
   const int nc = ghi - glo + 1 + (extra != INT_MIN ? 1 : 0);
   auto cand = [&](int j) { return (extra != INT_MIN) ? (j == 0 ? extra : glo + j - 1) : glo + j; };
   for (int j = threadIdx.x; j < nc; j += kThreads) {
@@ -484,19 +554,29 @@ __device__ void general_decide(int wl, int fl_lo, int fl_hi, int nchunks, int si
     default: { constexpr int K_ = FXPQ_SRC_ADD, D_ = FXPQ_I8; CALL; } break;        \
   }
 
-hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int wl, int sign, int fl_lo, int nce,
-                                 int fl_hi, int mode, int64_t per_thread, const double* d_minmax,
-                                 int nb, fxpq_fmt* out, int codes) {
+// Slot set of the current search (searches alternate between two sets: the
+// one a search adds into is cleared by the next search's finalize).
+static long long* slots_i(const Ctx& c, int set) { return c.sc.win_part + (size_t)set * kWinSlots * kWinPart; }
+static double* slots_f(const Ctx& c, int set) { return c.sc.win_part_f + (size_t)set * kWinSlots * kWinPartF; }
+
+int fls_begin(const Ctx& c) { return (int)((*c.search_seq)++ & 1u); }
+
+hipError_t launch_fls_window_fin(const Ctx& c, const SrcDev& s, int set, int wl, int sign, int fl_lo,
+                                 int nce, int fl_hi, int mode, int64_t per_thread,
+                                 const double* d_minmax, fxpq_fmt* out) {
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_window_fin<K_><<<1, kFinThreads, 0, c.stream>>>(
-                        s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax, c.sc.win_part,
-                        c.sc.win_part_f, plan, out, codes)));
+                        s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax, slots_i(c, set),
+                        slots_f(c, set), slots_i(c, 1 - set), slots_f(c, 1 - set), plan, out)));
   return hipGetLastError();
 }
 
-hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
-                              int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
+// The general pass; with `wi.decide` it first takes the window decision
+// (replacing the finalize launch).
+static hipError_t general_pass(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
+                               int fl_hi, const double* d_minmax, const WinIn& wi, fxpq_fmt* out,
+                               double* d_sse) {
   FlsPlan* plan = static_cast<FlsPlan*>(c.sc.plan);
   int nchunks = (int)((n + 65535) / 65536);
   if (nchunks > kGenChunks) nchunks = kGenChunks;
@@ -504,9 +584,15 @@ hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
   int gblocks = 240;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (k_fls_general<K_, D_><<<gblocks, kThreads, 0, c.stream>>>(
-                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, plan, c.sc.gen_part,
+                        s, n, wl, fl_lo, fl_hi, nchunks, d_minmax, wi, plan, c.sc.gen_part,
                         c.sc.gen_done, out, d_sse, c.sc.flags)));
   return hipGetLastError();
+}
+
+hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, int fl_lo,
+                              int fl_hi, const double* d_minmax, fxpq_fmt* out, double* d_sse) {
+  WinIn wi{};
+  return general_pass(c, s, n, wl, fl_lo, fl_hi, d_minmax, wi, out, d_sse);
 }
 
 // Values per thread of the streaming window pass for a grid of `blocks`.
@@ -532,12 +618,13 @@ static hipError_t fl_search_passes(const Ctx& c, const SrcDev& s, int64_t n, int
                             (codes ? 1.0 : 0.0);
   int64_t per_thread = 0;
   int blocks = 0;
+  const int set = fls_begin(c);
   auto run = [&](auto kernel) {
     blocks = stream_grid(n, channels, kWinMaxPerThread, vec, resident_blocks(c, (const void*)kernel));
     per_thread = window_per_thread(n, blocks, vec);
     bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
     kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, mode, per_thread,
-                                              d_minmax, c.sc.win_part, c.sc.win_part_f, plan, out,
+                                              d_minmax, slots_i(c, set), slots_f(c, set), plan, out,
                                               c.sc.flags, y, y_alt);
     timer_end(c, timed, elem_bytes * (double)n);
   };
@@ -553,10 +640,11 @@ static hipError_t fl_search_passes(const Ctx& c, const SrcDev& s, int64_t n, int
   } else {
     FXPQ_DISPATCH_SRC(s.kind, s.dtype, (run(&k_fls_window<K_, D_, kCeBounds, false>)));
   }
-  hipError_t e = launch_fls_window_fin(c, s, wl, sign, fl_lo, nce, fl_hi, mode, per_thread, d_minmax,
-                                       blocks, out, codes ? 1 : 0);
+  hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_fls_general(c, s, n, wl, fl_lo, fl_hi, d_minmax, out, d_sse);
+  WinIn wi{1, sign, nce, mode, codes ? 1 : 0, per_thread, slots_i(c, set), slots_f(c, set),
+           slots_i(c, 1 - set), slots_f(c, 1 - set)};
+  return general_pass(c, s, n, wl, fl_lo, fl_hi, d_minmax, wi, out, d_sse);
 }
 
 hipError_t launch_fl_search(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign, int fl_lo,
