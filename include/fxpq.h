@@ -291,6 +291,17 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
                         fxpq_fmt* d_fmt_out, void* y, fxpq_dtype y_type, int32_t* acc,
                         double* d_minmax);
 
+/*
+ * Tile family of fxpq_qconv (results are the same integers either way):
+ * FXPQ_TILING_AUTO (default) and FXPQ_TILING_GEMM use implicit-GEMM tiles;
+ * FXPQ_TILING_HALO uses halo tiles where the shape allows them (3x3 filters,
+ * stride 1 or 2, c % 64 == 0, k % 256 == 0, r*s*c >= 1024, an input patch of
+ * at most 512 pixels per tile): whole output-image rows per tile, the input
+ * patch loaded into LDS once per channel chunk for all nine taps.
+ */
+typedef enum { FXPQ_TILING_AUTO = 0, FXPQ_TILING_GEMM = 1, FXPQ_TILING_HALO = 2 } fxpq_conv_tiling;
+fxpq_status fxpq_set_conv_tiling(fxpq_handle h, int32_t mode);
+
 /* Sum of each filter's codes: colsum[k] = sum_j w[k][j] for w[k][len] (device). */
 fxpq_status fxpq_weight_colsum(fxpq_handle h, const int8_t* w, int64_t k, int64_t len,
                                int32_t* colsum);

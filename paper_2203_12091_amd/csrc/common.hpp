@@ -38,6 +38,7 @@ struct Scratch {
   unsigned long long* gen_part;  // general search partials [kMaxCand][kGenChunks][3]
   unsigned* gen_done;       // blocks of the general pass finished (0 between searches)
   void* plan;               // FlsPlan
+  int32_t* sink;            // target of discarded stores [64]
 };
 
 // Everything a kernel needs to produce the value v_i of an FxP-QLayer input,
@@ -157,6 +158,7 @@ struct Ctx {
   Timer* timer;
   int cus;                  // compute units of the handle's device
   unsigned* search_seq;     // FL searches enqueued on the handle (host counter)
+  int conv_tiling;          // fxpq_conv_tiling
 };
 
 // Brackets one launch with events when `kind` is being timed.

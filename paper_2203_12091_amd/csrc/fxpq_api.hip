@@ -19,6 +19,7 @@ struct fxpq_handle_s {
   Scratch sc;
   Timer timer;
   unsigned search_seq = 0;
+  int conv_tiling = FXPQ_TILING_AUTO;
 };
 
 constexpr int kTimerPairs = 16384;
@@ -37,7 +38,9 @@ bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32; }
 
 size_t code_align(int t) { (void)t; return 16; }
 
-Ctx ctx(fxpq_handle h) { return Ctx{h->stream, h->sc, &h->timer, h->cus, &h->search_seq}; }
+Ctx ctx(fxpq_handle h) {
+  return Ctx{h->stream, h->sc, &h->timer, h->cus, &h->search_seq, h->conv_tiling};
+}
 
 fxpq_status hip_status(hipError_t e) { return e == hipSuccess ? FXPQ_OK : FXPQ_ERR_HIP; }
 
@@ -167,6 +170,7 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
   size_t o_gp = take((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
   size_t o_plan = take(256);
+  size_t o_sink = take(64 * sizeof(int32_t));
   if (hipMalloc(&h->scratch, off) != hipSuccess) {
     delete h;
     return FXPQ_ERR_ALLOC;
@@ -181,6 +185,7 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   h->sc.gen_part = reinterpret_cast<unsigned long long*>(base + o_gp);
   h->sc.gen_done = reinterpret_cast<unsigned*>(base + o_gd);
   h->sc.plan = base + o_plan;
+  h->sc.sink = reinterpret_cast<int32_t*>(base + o_sink);
   if (hipMemset(h->scratch, 0, o_mmp) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(h->scratch);
     delete h;
@@ -289,6 +294,12 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
     mm = h->sc.minmax;
   }
   return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
+}
+
+fxpq_status fxpq_set_conv_tiling(fxpq_handle h, int32_t mode) {
+  if (!h || mode < FXPQ_TILING_AUTO || mode > FXPQ_TILING_HALO) return FXPQ_ERR_INVALID_ARG;
+  h->conv_tiling = mode;
+  return FXPQ_OK;
 }
 
 fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,

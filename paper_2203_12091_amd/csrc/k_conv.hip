@@ -52,8 +52,16 @@ __device__ inline int lds_off(int row, int chunk) {
 
 // FAST64: C % 64 == 0, register-staged slabs; GEN16: C % 16 == 0; RGB4: the
 // 4-channel padded input; DMA64: C % 64 == 0, slabs loaded straight into a
-// three-stage LDS ring (global_load_lds), two slabs in flight.
-enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2, LD_DMA64 = 3 };
+// three-stage LDS ring (global_load_lds), two slabs in flight.  HALO4 /
+// HALO8: C % 64 == 0, tiles of whole output-image rows whose input patch
+// (up to 256 / 512 pixels per channel chunk) is loaded into LDS once and read
+// by every filter tap, weights through the DMA ring.
+enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2, LD_DMA64 = 3, LD_HALO4 = 4, LD_HALO8 = 5 };
+
+constexpr bool is_halo(int loader) { return loader == LD_HALO4 || loader == LD_HALO8; }
+
+// Weight stages of the halo tiles' LDS ring (HD - 1 slabs in flight).
+constexpr int kHaloStages = 3;
 
 // 16-byte padding sources of the LDS-ring loader: code 0, and code -128 for
 // inputs stored as u - 128 (both the value 0).
@@ -119,11 +127,16 @@ struct ConvArgs {
   const fxpq_fmt* fmt_req;
   int8_t* y;
   int y_type;
+  // halo tiles: hG images of hTH output rows each (hG > 1 only with hTH ==
+  // Ho), hTPI tiles per image (hG == 1), input patch hPH x hPW per image;
+  // stores of rows that do not exist go to `sink` (32 int32)
+  int hG, hTH, hTPI, hPH, hPW;
+  int32_t* sink;
 };
 
 // Tile configurations: block BM x BN, four waves of (32 TM) x (32 TN), MINW
 // waves per SIMD requested from the register allocator.
-enum TileCfg { TC_256x64 = 0, TC_128x128 = 1, TC_256x128 = 2 };
+enum TileCfg { TC_256x64 = 0, TC_128x128 = 1, TC_256x128 = 2, TC_H224x256 = 3, TC_H128x256 = 4 };
 
 // Accumulators per thread of a configuration (the per-thread bound of the
 // fused window epilogue).
@@ -186,8 +199,23 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       tn = t - tm * gridDim.y;
     }
   }
-  const int m0 = tm * BM, n0 = tn * BN;
+  int m0 = tm * BM;
+  const int n0 = tn * BN;
   const int kc = tid & 3;
+  // Halo tiles: output rows oh0 .. oh0 + hTH - 1 (all columns) of images
+  // img0 .. img0 + hG - 1; vrows of the BM rows exist.
+  int img0 = 0, oh0 = 0, vrows = BM;
+  if constexpr (is_halo(LOADER)) {
+    if (a.hG > 1) {
+      img0 = tm * a.hG;
+      vrows = min(a.hG, a.N - img0) * a.Ho * a.Wo;
+    } else {
+      img0 = tm / a.hTPI;
+      oh0 = (tm - img0 * a.hTPI) * a.hTH;
+      vrows = min(a.hTH, a.Ho - oh0) * a.Wo;
+    }
+    m0 = (img0 * a.Ho + oh0) * a.Wo;
+  }
 
   // Inputs stored as u - 128 (branch-free, so the operand loads need not wait
   // for the format).
@@ -324,6 +352,125 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       step(kt, A0, B0, A2, B2);
       if (kt + 1 < ktiles) step(kt + 1, A1, B1, A0, B0);
       if (kt + 2 < ktiles) step(kt + 2, A2, B2, A1, B1);
+    }
+  } else if constexpr (is_halo(LOADER)) {
+    // Patch row R (pixel of the padded input patch) of a chunk sits at LDS row
+    // R of a patch buffer; the DMA pieces of 16 rows are dealt to the waves as
+    // in LD_DMA64.  Filter tap (r, s) of output row p reads patch row
+    // pbase(p) + r * hPW + s.  Weights: one 64-byte slab per (chunk, tap).
+    static_assert(WGN == 4, "halo tiles split the block's columns over the four waves");
+    constexpr int AJ = (LOADER == LD_HALO8) ? 8 : 4, BJ = BN / 64;
+    constexpr int NPR = 64 * AJ;  // patch rows per buffer
+    constexpr int HD = kHaloStages;
+    __shared__ __attribute__((aligned(16))) int8_t P0[NPR * 64], P1[NPR * 64];
+    __shared__ __attribute__((aligned(16))) int8_t Bst[HD][BN * 64];
+    const int ppx = a.hPH * a.hPW;
+    const int npx = a.hG * ppx;
+    const int8_t* psrc[AJ];
+    bool pok[AJ];
+#pragma unroll
+    for (int j = 0; j < AJ; ++j) {
+      const int R = 16 * (4 * j + wave) + (lane >> 2);
+      const int g = R / ppx, rem = R - g * ppx;
+      const int py = rem / a.hPW, px = rem - py * a.hPW;
+      const int ih = oh0 * a.stride - a.pad + py, iw = px - a.pad, img = img0 + g;
+      pok[j] = R < npx && img < a.N && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
+      const int lch = ((lane & 3) ^ lds_swz(R)) & 3;
+      psrc[j] = a.x + (pok[j] ? (((int64_t)img * a.H + ih) * a.W + iw) * a.C + lch * 16 : 0);
+    }
+    const int8_t* bsrc[BJ];
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) {
+      const int row = 16 * (4 * j + wave) + (lane >> 2);
+      const int col = n0 + row;
+      const int cc = col < a.K ? col : a.K - 1;
+      bsrc[j] = a.w + (int64_t)cc * a.wrow + (((lane & 3) ^ lds_swz(row)) & 3) * 16;
+    }
+    // patch row of tap (0, 0) for each of this lane's output rows
+    int pbase[TM];
+    const int rows_img = a.hTH * a.Wo;
+#pragma unroll
+    for (int mi = 0; mi < TM; ++mi) {
+      const int p = mi * 32 + (lane & 31);
+      const int g = p / rows_img, q = p - g * rows_img;
+      const int ohl = q / a.Wo, ow = q - ohl * a.Wo;
+      pbase[mi] = (p < vrows) ? g * ppx + ohl * a.stride * a.hPW + ow * a.stride : 0;
+    }
+    const int8_t* padp = reinterpret_cast<const int8_t*>(&kPadVec[a_off]);
+    auto issue = [&](int kt, int8_t* sb) {
+      const int cchunk = kt / taps;
+      const int rs = kt - cchunk * taps;
+      const int c0 = cchunk * BK;
+      if (rs == 0) {
+        int8_t* pb = (cchunk & 1) ? P1 : P0;
+#pragma unroll
+        for (int j = 0; j < AJ; ++j) dma16(pok[j] ? psrc[j] + c0 : padp, &pb[(4 * j + wave) * 1024]);
+      }
+      const int k0 = rs * a.C + c0;
+#pragma unroll
+      for (int j = 0; j < BJ; ++j) dma16(bsrc[j] + k0, &sb[(4 * j + wave) * 1024]);
+    };
+    auto compute_tap = [&](int kt, const int8_t* sb) {
+      const int cchunk = kt / taps;
+      const int rs = kt - cchunk * taps;
+      const int r = rs / a.S, sx = rs - r * a.S;
+      const int toff = r * a.hPW + sx;
+      const int8_t* pb = (cchunk & 1) ? P1 : P0;
+      v4i af[2][TM], bf[2][TN];
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi)
+          af[kk][mi] = *reinterpret_cast<const v4i*>(&pb[lds_off(pbase[mi] + toff, kk * 2 + (lane >> 5))]);
+#pragma unroll
+        for (int ni = 0; ni < TN; ++ni)
+          bf[kk][ni] = *reinterpret_cast<const v4i*>(
+              &sb[lds_off(wn * WCOLS + ni * 32 + (lane & 31), kk * 2 + (lane >> 5))]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < TN; ++ni)
+            acc[mi][ni] =
+                __builtin_amdgcn_mfma_i32_32x32x32_i8(af[kk][mi], bf[kk][ni], acc[mi][ni], 0, 0, 0);
+    };
+    // Ring of HD weight stages: slab kt + HD - 1 is issued at step kt into
+    // the stage slab kt - 1 used.  Waiting at step kt: slab kt's loads have
+    // landed while the (up to HD - 2) later slabs' may be in flight; at most
+    // one of those carries a chunk's patch (a chunk has taps >= HD - 1 slabs).
+    auto wait_slab = [&](int kt) {
+      const int later = min(HD - 2, ktiles - 1 - kt);
+      bool patch = false;
+      for (int j = 1; j <= later; ++j) patch = patch || (kt + j) % taps == 0;
+      switch (later * 2 + (patch ? 1 : 0)) {
+        case 0: wait_vmcnt<0>(); break;
+        case 2: wait_vmcnt<BJ>(); break;
+        case 3: wait_vmcnt<BJ + AJ>(); break;
+        case 4: wait_vmcnt<2 * BJ>(); break;
+        case 5: wait_vmcnt<2 * BJ + AJ>(); break;
+        case 6: wait_vmcnt<3 * BJ>(); break;
+        default: wait_vmcnt<3 * BJ + AJ>(); break;
+      }
+    };
+    static_assert(HD >= 3 && HD <= 5, "ring depth");
+    epi_loads();
+#pragma unroll
+    for (int j = 0; j < HD - 1; ++j)
+      if (j < ktiles) issue(j, Bst[j]);
+    for (int kt0 = 0; kt0 < ktiles; kt0 += HD) {
+#pragma unroll
+      for (int j = 0; j < HD; ++j) {
+        const int kt = kt0 + j;
+        if (kt < ktiles) {
+          wait_slab(kt);
+          ring_barrier();
+          if (kt + HD - 1 < ktiles) issue(kt + HD - 1, Bst[(j + HD - 1) % HD]);
+          compute_tap(kt, Bst[j]);
+        }
+      }
     }
   } else {
     // Rows owned by this thread for A loads.
@@ -466,7 +613,30 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       lo[ni] = INT_MAX;
       hi[ni] = INT_MIN;
     }
-    if (full) {
+    if constexpr (is_halo(LOADER)) {
+      // Rows past vrows do not exist (padding of the last MFMA row tile, or a
+      // partial tile): their stores go to a scratch sink, their values are not
+      // counted (branch-free selects).
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) {
+        const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
+        const int corr = 128 * csum[ni];
+        int32_t* dst = a.acc + (int64_t)m0 * a.K + col;
+        int32_t* sink = a.sink + (lane & 31);
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int lr = mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+            const bool ok = lr < vrows;
+            const int v = acc[mi][ni][e];
+            if constexpr (EPI == EPI_ACC) *(ok ? dst + (int64_t)lr * a.K : sink) = v + corr;
+            lo[ni] = min(lo[ni], ok ? v : INT_MAX);
+            hi[ni] = max(hi[ni], ok ? v : INT_MIN);
+          }
+        }
+      }
+    } else if (full) {
       // Full tile: buffer stores with the row offset in a scalar register.
       __amdgpu_buffer_rsrc_t rs;
       int vo[TN];
@@ -568,14 +738,24 @@ static void conv_dispatch_loader(int loader, dim3 grid, hipStream_t st, const Co
     k_qconv<BM, BN, TM, TN, MINW, LD_DMA64, EPI><<<grid, 256, 0, st>>>(a);
   else if (loader == LD_GEN16)
     k_qconv<BM, BN, TM, TN, MINW, LD_GEN16, EPI><<<grid, 256, 0, st>>>(a);
+  else if (loader == LD_HALO4 || loader == LD_HALO8)
+    return;  // halo tiles have their own configurations
   else if constexpr (EPI == EPI_ACC && BN == 64)
     k_qconv<BM, BN, TM, TN, MINW, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
+}
+
+// Convolutions the halo tiles take: 3x3 filters (stride 1 or 2), 64-channel
+// multiples in, 256-channel multiples out, contraction deep enough to be
+// bound by the matrix cores.
+static bool ep_halo_ok(const fxpq_conv_desc& d) {
+  return d.r == 3 && d.s == 3 && (d.stride == 1 || d.stride == 2) && d.pad <= 2 && d.c % 64 == 0 &&
+         d.k % 256 == 0 && d.r * d.s * d.c >= 1024;
 }
 
 // Tile shape and grid of a conv; loader choice and the geometry in `a`.
 static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const int8_t* w,
                        const int32_t* colsum, const SrcDev* ep, ConvArgs& a, int& loader,
-                       int& cfg, int cus) {
+                       int& cfg, int cus, int halo = FXPQ_TILING_GEMM) {
   a.x = static_cast<const int8_t*>(x);
   a.w = w;
   a.colsum = colsum;
@@ -601,6 +781,42 @@ static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const
   else cfg = TC_128x128;
   // channel multiples of 64 outside the narrow tiles: slabs through the LDS ring
   if (loader == LD_FAST64 && cfg != TC_256x64) loader = LD_DMA64;
+  // 3x3 filters over small images with 256-channel multiples, on request:
+  // halo tiles of whole output rows (224 rows in 7 MFMA row tiles, else 128
+  // in 4) when the patch fits 512 LDS rows and, first choice, the tiles fill
+  // the chip.  (Measured slower than the implicit-GEMM tiles on ResNet-50's
+  // 14x14 and 7x7 layers: one block per CU cannot hide the LDS and barrier
+  // latency of each slab.)
+  if (halo == FXPQ_TILING_HALO && loader == LD_DMA64 && ep_halo_ok(d)) {
+    for (int opt = 0; opt < 2; ++opt) {
+      const int bm = opt == 0 ? 224 : 128;
+      const int howo = a.Ho * a.Wo;
+      int G, TH;
+      if (howo <= bm) {
+        G = bm / howo;
+        TH = a.Ho;
+      } else {
+        G = 1;
+        TH = bm / a.Wo;
+        if (TH < 1) continue;
+      }
+      const int PH = (TH - 1) * d.stride + d.r, PW = (a.Wo - 1) * d.stride + d.s;
+      const int npx = G * PH * PW;
+      if (npx > 512) continue;
+      const int tpi = (a.Ho + TH - 1) / TH;
+      const int64_t tm = (G > 1) ? (d.n + G - 1) / G : (int64_t)d.n * tpi;
+      const int64_t tiles = tm * (d.k / 256);
+      if (opt == 0 && tiles < cus) continue;
+      a.hG = G;
+      a.hTH = TH;
+      a.hTPI = tpi;
+      a.hPH = PH;
+      a.hPW = PW;
+      loader = npx <= 256 ? LD_HALO4 : LD_HALO8;
+      cfg = opt == 0 ? TC_H224x256 : TC_H128x256;
+      return dim3((unsigned)tm, d.k / 256);
+    }
+  }
   switch (cfg) {
     case TC_256x64: return dim3((a.M + 255) / 256, (d.k + 63) / 64);
     case TC_256x128: return dim3((a.M + 255) / 256, (d.k + 127) / 128);
@@ -610,6 +826,18 @@ static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const
 
 template <int EPI>
 static void conv_run(const ConvArgs& a, int loader, int cfg, dim3 grid, hipStream_t st) {
+  if constexpr (EPI == EPI_ACC) {
+    if (cfg == TC_H224x256) {
+      if (loader == LD_HALO4) k_qconv<224, 256, 7, 2, 1, LD_HALO4, EPI><<<grid, 256, 0, st>>>(a);
+      else k_qconv<224, 256, 7, 2, 1, LD_HALO8, EPI><<<grid, 256, 0, st>>>(a);
+      return;
+    }
+    if (cfg == TC_H128x256) {
+      if (loader == LD_HALO4) k_qconv<128, 256, 4, 2, 1, LD_HALO4, EPI><<<grid, 256, 0, st>>>(a);
+      else k_qconv<128, 256, 4, 2, 1, LD_HALO8, EPI><<<grid, 256, 0, st>>>(a);
+      return;
+    }
+  }
   if (cfg == TC_256x64)
     conv_dispatch_loader<256, 64, 2, 2, 3, EPI>(loader, grid, st, a);
   else if (cfg == TC_256x128)
@@ -624,8 +852,9 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   ConvArgs a{};
   int loader;
   int cfg;
-  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, cfg, c.cus);
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, ep, a, loader, cfg, c.cus, c.conv_tiling);
   a.acc = acc;
+  a.sink = c.sc.sink;
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
   bool timed = timer_begin(c, FXPQ_TIMER_QCONV);

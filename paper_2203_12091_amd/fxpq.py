@@ -21,12 +21,13 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_qconv", "fxpq_qgemm",
-    "fxpq_cblock", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
+    "fxpq_cblock", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
     "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
     "fxpq_teacher_avgpool",
 ]
 TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT, TIMER_CBLOCK_PASS = range(5)
+TILING_AUTO, TILING_GEMM, TILING_HALO = range(3)
 
 
 class Fmt(C.Structure):
@@ -84,6 +85,7 @@ def lib():
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
             "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
             "fxpq_weight_colsum": [p, p, i64, i64, p],
+            "fxpq_set_conv_tiling": [p, i32],
             "fxpq_maxpool": [p, p, C.c_int, i32, i32, i32, i32, i32, i32, i32, p],
             "fxpq_avgpool_global": [p, p, C.c_int, p, i32, i32, i32, i64, p],
             "fxpq_layer_error": [p, p, p, C.c_int, p, i64, p],
@@ -185,6 +187,10 @@ def requant_addmm(h, src, n, d_fmt, codes, code_type, b, b_type, d_fmt_b, relu, 
 def fl_search(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, d_sse=None):
     _call("fxpq_fl_search", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out),
           ptr(d_sse))
+
+
+def set_conv_tiling(h, mode):
+    _call("fxpq_set_conv_tiling", h.value, mode)
 
 
 def qlayer(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, codes, code_type, codes_alt):

@@ -161,5 +161,11 @@ def test_largest_3x3_conv_sampled(env):
         n, k, oh, ow = (int(g.integers(0, N)), int(g.integers(0, K)), int(g.integers(0, H)),
                         int(g.integers(0, H)))
         assert got[n, oh, ow, k] == orc.conv2d_point(x32, w32, 1, 1, n, k, oh, ow)
+    # the halo tiles give the same integers over the whole tensor
+    note("fullsize 3x3 conv, halo tiles")
+    fx.set_conv_tiling(h, fx.TILING_HALO)
+    acc2 = empty((N, H, H, K), torch.int32)
+    fx.qconv(h, fx.conv_desc(N, H, H, C, K, 3, 3, 1, 1), xd, fx.U8OFF, wd, cs, None, acc2)
+    assert torch.equal(acc, acc2)
     assert fx.sync_status(h) == 0
     h.close()

@@ -313,6 +313,32 @@ def test_qconv_accumulators_and_epilogue_minmax(fx, h, orc, case):
     check_flags(fx, h)
 
 
+# 3x3 shapes the halo tiles take (c % 64 == 0, k % 256 == 0, r*s*c >= 1024):
+# whole images per tile (one, two or four), output rows split over several
+# tiles with a partial last one, stride 2, odd sizes, partial last image group
+HALO_CASES = [
+    (3, 128, 14, 14, 256, 3, 1, 1, False, True, False, True),
+    (5, 128, 7, 7, 512, 3, 1, 1, True, False, True, False),
+    (3, 128, 14, 14, 256, 3, 2, 1, False, True, True, True),
+    (2, 192, 9, 11, 256, 3, 1, 1, False, False, False, True),
+    (1, 128, 28, 28, 256, 3, 1, 1, True, True, True, False),
+    (2, 128, 30, 17, 256, 3, 2, 1, False, True, False, True),  # patch too big: implicit GEMM
+]
+
+
+@pytest.mark.parametrize("case", HALO_CASES, ids=[str(i) for i in range(len(HALO_CASES))])
+def test_qconv_halo_and_gemm_tiles(fx, h, orc, case):
+    # the same accumulators and min / max from both tile families
+    try:
+        for mode in (fx.TILING_HALO, fx.TILING_GEMM):
+            fx.set_conv_tiling(h, mode)
+            note("tiling", mode)
+            gpu_conv_case(fx, h, orc, *case, seed=17)
+    finally:
+        fx.set_conv_tiling(h, fx.TILING_AUTO)
+    check_flags(fx, h)
+
+
 def test_c8_input_storage_follows_format(fx, h, orc):
     gpu_conv_case(fx, h, orc, 2, 64, 8, 8, 64, 3, 1, 1, False, True, False, True, seed=12,
                   x_type=fx.C8)
