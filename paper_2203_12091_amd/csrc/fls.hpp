@@ -290,13 +290,12 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
   }
 }
 
-// Block results of the window pass.  Each exact per-thread sum (below 2^62)
-// is split into its high and low 32-bit halves, summed separately over the
-// block and added (int64 atomics: exact, order-free) into slot bid %
-// kWinSlots of part_i (kWinPart int64 per slot: per candidate A hi/lo, PH
-// hi/lo, PL hi/lo); the fp64 bound sums (sum W^2, then NB clipping bounds) go
-// to part_f (kWinPartF per slot).  The finalize reads the slots and clears
-// them for the next search.
+// LDS table of the block reduction (one row per wave of a 256-thread block).
+struct WinShared {
+  long long i[4][kWinPart];
+  double f[4][kWinPartF];
+};
+
 __device__ inline void slot_add(long long* p, long long v) {
   __hip_atomic_fetch_add(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v,
                          __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -305,36 +304,57 @@ __device__ inline void slot_add(double* p, double v) {
   __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Block results of the window pass (256 threads).  Each exact per-thread sum
+// (below 2^62) is split into its high and low 32-bit halves, summed
+// separately over the block and added (int64 atomics: exact, order-free) into
+// slot bid % kWinSlots of part_i (kWinPart int64 per slot: per candidate A
+// hi/lo, PH hi/lo, PL hi/lo); the fp64 bound sums (sum W^2, then nb clipping
+// bounds) go to part_f (kWinPartF per slot).  The search's decision reads the
+// slots; the next search's decision clears them.
 __device__ inline void win_write_partials_i64(const long long* A, const long long* PH,
                                               const long long* PL, double V2, const double* CE,
                                               int nb, int64_t bid, long long* part_i,
-                                              double* part_f, long long* shl, double* shd) {
-  const int slot = (int)(bid % kWinSlots);
-  long long* pi = part_i + slot * kWinPart;
+                                              double* part_f, WinShared& sh) {
+  // Each wave reduces every quantity; lane 0 of wave w writes row w of the
+  // table; after one barrier thread t adds the four rows of quantity t and
+  // adds the result into the slot.
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  long long q[kWinPart];
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
     const long long q3[3] = {A[j], PH[j], PL[j]};
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
-      const long long h = block_reduce(q3[k] >> 32, OpAddL(), shl);
-      const long long l = block_reduce(q3[k] & 0xFFFFFFFFll, OpAddL(), shl);
-      if (threadIdx.x == 0) {
-        slot_add(pi + 6 * j + 2 * k, h);
-        slot_add(pi + 6 * j + 2 * k + 1, l);
-      }
+      q[6 * j + 2 * k] = q3[k] >> 32;
+      q[6 * j + 2 * k + 1] = q3[k] & 0xFFFFFFFFll;
     }
   }
-  const double v2 = block_reduce(V2, OpAddD(), shd);
-  if (threadIdx.x == 0) slot_add(part_f + kWinPartF * slot, v2);
-  for (int k = 0; k < nb; ++k) {
-    const double ce = block_reduce(CE[k], OpAddD(), shd);
-    if (threadIdx.x == 0) slot_add(part_f + kWinPartF * slot + 1 + k, ce);
+  double f[kWinPartF];
+  f[0] = V2;
+#pragma unroll
+  for (int k = 0; k < kCeBounds; ++k) f[1 + k] = (k < nb) ? CE[k] : 0.0;
+#pragma unroll
+  for (int i = 0; i < kWinPart; ++i) q[i] = wave_reduce(q[i], OpAddL());
+#pragma unroll
+  for (int i = 0; i < kWinPartF; ++i) f[i] = wave_reduce(f[i], OpAddD());
+  if (lane == 0) {
+#pragma unroll
+    for (int i = 0; i < kWinPart; ++i) sh.i[w][i] = q[i];
+#pragma unroll
+    for (int i = 0; i < kWinPartF; ++i) sh.f[w][i] = f[i];
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  const int slot = (int)(bid % kWinSlots);
+  if (t < kWinPart) {
+    slot_add(part_i + slot * kWinPart + t, sh.i[0][t] + sh.i[1][t] + sh.i[2][t] + sh.i[3][t]);
+  } else if (t < kWinPart + 1 + nb) {
+    const int i = t - kWinPart;
+    slot_add(part_f + kWinPartF * slot + i, ((sh.f[0][i] + sh.f[1][i]) + sh.f[2][i]) + sh.f[3][i]);
   }
 }
-
 __device__ inline void win_write_partials(const WinAcc& acc, int nb, int64_t bid,
-                                          long long* part_i, double* part_f, long long* shl,
-                                          double* shd) {
+                                          long long* part_i, double* part_f, WinShared& sh) {
   long long A[kWindow], PH[kWindow], PL[kWindow];
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
@@ -342,7 +362,7 @@ __device__ inline void win_write_partials(const WinAcc& acc, int nb, int64_t bid
     PH[j] = exact_i64(acc.PH[j]);
     PL[j] = exact_i64(acc.PL[j]);
   }
-  win_write_partials_i64(A, PH, PL, acc.V2, acc.CE, nb, bid, part_i, part_f, shl, shd);
+  win_write_partials_i64(A, PH, PL, acc.V2, acc.CE, nb, bid, part_i, part_f, sh);
 }
 
 // Launch helpers shared by the streaming search and the fused C-Block.

@@ -159,7 +159,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
   __shared__ __attribute__((aligned(16))) int8_t Bs[NST][BN * 64];
   __shared__ int rs_tab[128];
   __shared__ double shd[8];
-  __shared__ long long shl[8];
+  __shared__ WinShared wsh;
 
   // Decisions every block takes identically before any load.
   WinSetup ws;
@@ -721,7 +721,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       default: FXPQ_WIN_VISIT(true, true); break;
     }
 #undef FXPQ_WIN_VISIT
-    win_write_partials(wa, 1, bid, a.part_i, a.part_f, shl, shd);
+    win_write_partials(wa, 1, bid, a.part_i, a.part_f, wsh);
   } else {  // EPI_REQ
     visit([&](int v, double Mc, double Ac, int row, int col) {
       const double val = fmax(fma((double)v, Mc, Ac), relo);

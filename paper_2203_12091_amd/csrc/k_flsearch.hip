@@ -136,8 +136,7 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int mode, int64_t per_thread,
     const double* mm, long long* part_i, double* part_f, FlsPlan* plan, fxpq_fmt* out,
     unsigned* flags, int8_t* y, int8_t* y_alt) {
-  __shared__ long long shl[8];
-  __shared__ double shd[8];
+  __shared__ WinShared wsh;
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, mode, per_thread);
   const FlsU& u = ws.u;
 
@@ -162,7 +161,7 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     case 2: win_loop<KIND, DT, true, false, NB, CODES>(s, n, u, ws, wcd, acc); break;
     default: win_loop<KIND, DT, true, true, NB, CODES>(s, n, u, ws, wcd, acc); break;
   }
-  win_write_partials(acc, NB, blockIdx.x, part_i, part_f, shl, shd);
+  win_write_partials(acc, NB, blockIdx.x, part_i, part_f, wsh);
 }
 
 // Bits of |v| (0 for v == 0).
