@@ -244,6 +244,27 @@ fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t w
                         fxpq_dtype code_type, void* codes_alt);
 
 /*
+ * Preprocessor initial format (Sec. "Initial Design Generation", Eq. 6-9):
+ *   S = 1 when the smallest value is negative (Eq. 6);
+ *   psi = X_max / (2^k - 1) for S = 0, and for S = 1
+ *   psi = min(X_min / -2^(k-1), X_max / (2^(k-1) - 1)) (Eq. 7 as printed,
+ *   FXPQ_PSI_PRINTED) or the max of the two (FXPQ_PSI_MAX);
+ *   fl = floor, nearest or ceil of -log2(psi) (Eq. 8-9) for the conservative,
+ *   neutral or aggressive strategy, clamped to [fl_lo, fl_hi].
+ * The integer length is wl - fl.  Decided exactly from the exact min / max of
+ * the values described by src (src->d_minmax when given, else a min / max
+ * pass).  Readings: all-zero data takes fl_hi; signed data without a positive
+ * value takes the negative side alone.  d_fmt_out (device) receives
+ * {wl, fl, S, 0}; non-finite data gives status 1 and FXPQ_FLAG_RANGE.
+ * Requirements: 2 <= wl <= 32, -64 <= fl_lo <= fl_hi <= 64, n >= 1.
+ */
+typedef enum { FXPQ_ROUND_CONSERVATIVE = 0, FXPQ_ROUND_NEUTRAL = 1, FXPQ_ROUND_AGGRESSIVE = 2 } fxpq_round_strategy;
+typedef enum { FXPQ_PSI_PRINTED = 0, FXPQ_PSI_MAX = 1 } fxpq_psi_rule;
+fxpq_status fxpq_preprocess(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl,
+                            int32_t strategy, int32_t psi_rule, int32_t fl_lo, int32_t fl_hi,
+                            fxpq_fmt* d_fmt_out);
+
+/*
  * Quantized convolution (C-Block contraction, Sec. "Integer-Only Inference"):
  * acc[n][oh][ow][k] = sum_{r,s,c} x[n][oh*stride-pad+r][ow*stride-pad+s][c] * w[k][r][s][c]
  * with zero padding (value 0 in either code dtype), int32 accumulation on the

@@ -216,6 +216,8 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
                              const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
                              int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,
                              double* d_minmax);
+hipError_t launch_preprocess(const Ctx& c, const SrcDev& s, const double* d_minmax, int wl,
+                             int strategy, int rule, int fl_lo, int fl_hi, fxpq_fmt* out);
 hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out);
 hipError_t launch_maxpool(const Ctx& c, const int8_t* x, int n, int h, int w, int ch, int ks,
                           int stride, int pad, int8_t* y);

@@ -296,6 +296,28 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
   return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
 }
 
+fxpq_status fxpq_preprocess(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl,
+                            int32_t strategy, int32_t psi_rule, int32_t fl_lo, int32_t fl_hi,
+                            fxpq_fmt* d_fmt_out) {
+  if (!h || n < 1 || !d_fmt_out) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 2 || wl > 32) return wl == 1 ? FXPQ_ERR_UNSUPPORTED : FXPQ_ERR_INVALID_ARG;
+  if (strategy < FXPQ_ROUND_CONSERVATIVE || strategy > FXPQ_ROUND_AGGRESSIVE) return FXPQ_ERR_INVALID_ARG;
+  if (psi_rule != FXPQ_PSI_PRINTED && psi_rule != FXPQ_PSI_MAX) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  DeviceGuard g(h->device);
+  Ctx c = ctx(h);
+  const double* mm = src->d_minmax;
+  if (!mm) {
+    hipError_t e = launch_minmax(c, s, n, h->sc.minmax);
+    if (e != hipSuccess) return FXPQ_ERR_HIP;
+    mm = h->sc.minmax;
+  }
+  return hip_status(launch_preprocess(c, s, mm, wl, strategy, psi_rule, fl_lo, fl_hi, d_fmt_out));
+}
+
 fxpq_status fxpq_set_conv_tiling(fxpq_handle h, int32_t mode) {
   if (!h || mode < FXPQ_TILING_AUTO || mode > FXPQ_TILING_HALO) return FXPQ_ERR_INVALID_ARG;
   h->conv_tiling = mode;

@@ -574,3 +574,108 @@ hipError_t launch_epi_scale(const Ctx& c, const SrcDev& s, int32_t* out) {
 }
 
 }  // namespace fxpq
+
+namespace fxpq {
+
+// ----------------------------------------------------------------------------
+// Preprocessor initial format (Sec. "Initial Design Generation", Eq. 6-9).
+// With psi = r / D for an extreme r of the data (exact double, r > 0) and an
+// integer D, beta_hat = -log2(psi):
+//   floor(beta_hat) = largest b with r 2^b <= D,
+//   ceil(beta_hat)  = smallest b with r 2^b >= D,
+//   nearest         = largest b with (r 2^b)^2 <= 2 D^2 (beta_hat is never a
+//                     half-integer: psi is rational).
+// Every comparison is exact: r 2^b is exact in fp64, and the squared one falls
+// back to 128-bit integers when fp64 cannot tell.
+// ----------------------------------------------------------------------------
+__device__ inline bool sq_le_2d2(double y, double d) {
+  const double l = y * y, r = 2.0 * d * d;
+  if (l < r * (1.0 - 0x1p-48)) return true;
+  if (l > r * (1.0 + 0x1p-48)) return false;
+  // near the boundary: y = M 2^E (M < 2^53), both sides below 2^110
+  int e;
+  const double m = frexp(y, &e);  // y = m 2^e, 0.5 <= m < 1
+  const unsigned long long M = (unsigned long long)ldexp(m, 53);
+  const int E = e - 53;
+  const unsigned __int128 L0 = (unsigned __int128)M * M;
+  const unsigned long long D = (unsigned long long)d;
+  const unsigned __int128 R0 = (unsigned __int128)(2ull * D) * D;
+  if (E >= 0) return (L0 << (2 * E)) <= R0;
+  return L0 <= (R0 << (-2 * E));
+}
+
+// Ratio side: value magnitude r (in real units, exact) over the integer D.
+struct PsiSide {
+  double r, d;
+  bool ok;
+};
+
+__device__ inline bool side_le(const PsiSide& p, int b, bool squared) {
+  const double y = ldexp(p.r, b);
+  return squared ? sq_le_2d2(y, p.d) : y <= p.d;
+}
+__device__ inline bool side_ge(const PsiSide& p, int b) { return ldexp(p.r, b) >= p.d; }
+
+__global__ void k_preprocess(SrcDev s, const double* mm, int wl, int strategy, int rule, int fl_lo,
+                             int fl_hi, fxpq_fmt* out, unsigned* flags) {
+  if (blockIdx.x != 0 || threadIdx.x != 0) return;
+  const int sv = src_scale(s);
+  const double mn = ldexp(mm[0], -sv), mx = ldexp(mm[1], -sv);  // real units, exact
+  if (!isfinite(mn) || !isfinite(mx)) {
+    *out = fxpq_fmt{wl, 0, 0, 1};
+    raise_flag(flags, FXPQ_FLAG_RANGE);
+    return;
+  }
+  const int sign = mn < 0.0 ? 1 : 0;
+  PsiSide a{0.0, 1.0, false}, c{0.0, 1.0, false};  // psi = min / max of a and c
+  if (sign == 0) {
+    a = PsiSide{mx, ldexp(1.0, wl) - 1.0, mx > 0.0};
+  } else {
+    a = PsiSide{-mn, ldexp(1.0, wl - 1), true};
+    c = PsiSide{mx, ldexp(1.0, wl - 1) - 1.0, mx > 0.0};
+  }
+  int fl = fl_hi;
+  if (a.ok) {
+    const bool use_min = (rule == FXPQ_PSI_PRINTED);
+    // psi 2^b <= bound: min rule -> either side, max rule -> both (sides
+    // that are not ok are left out)
+    auto le = [&](int b, bool sq) {
+      const bool x = side_le(a, b, sq);
+      if (!c.ok) return x;
+      const bool y = side_le(c, b, sq);
+      return use_min ? (x || y) : (x && y);
+    };
+    auto ge = [&](int b) {
+      const bool x = side_ge(a, b);
+      if (!c.ok) return x;
+      const bool y = side_ge(c, b);
+      return use_min ? (x && y) : (x || y);
+    };
+    if (strategy == FXPQ_ROUND_AGGRESSIVE) {
+      fl = fl_hi;
+      for (int b = fl_lo; b <= fl_hi; ++b)
+        if (ge(b)) {
+          fl = b;
+          break;
+        }
+    } else {
+      const bool sq = (strategy == FXPQ_ROUND_NEUTRAL);
+      fl = fl_lo;
+      for (int b = fl_hi; b >= fl_lo; --b)
+        if (le(b, sq)) {
+          fl = b;
+          break;
+        }
+    }
+  }
+  *out = fxpq_fmt{wl, fl, sign, 0};
+}
+
+hipError_t launch_preprocess(const Ctx& c, const SrcDev& s, const double* d_minmax, int wl,
+                             int strategy, int rule, int fl_lo, int fl_hi, fxpq_fmt* out) {
+  k_preprocess<<<1, 64, 0, c.stream>>>(s, d_minmax, wl, strategy, rule, fl_lo, fl_hi, out,
+                                       c.sc.flags);
+  return hipGetLastError();
+}
+
+}  // namespace fxpq

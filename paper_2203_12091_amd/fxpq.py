@@ -20,7 +20,7 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
-    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_qconv", "fxpq_qgemm",
+    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_cblock", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
     "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
@@ -28,6 +28,8 @@ EXPORTS = [
 ]
 TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT, TIMER_CBLOCK_PASS = range(5)
 TILING_AUTO, TILING_GEMM, TILING_HALO = range(3)
+ROUND_CONSERVATIVE, ROUND_NEUTRAL, ROUND_AGGRESSIVE = range(3)
+PSI_PRINTED, PSI_MAX = range(2)
 
 
 class Fmt(C.Structure):
@@ -81,6 +83,7 @@ def lib():
             "fxpq_requant_addmm": [p, p, i64, p, p, C.c_int, p, C.c_int, p, i32, p],
             "fxpq_fl_search": [p, p, i64, i32, i32, i32, i32, p, p],
             "fxpq_qlayer": [p, p, i64, i32, i32, i32, i32, p, p, C.c_int, p],
+            "fxpq_preprocess": [p, p, i64, i32, i32, i32, i32, i32, p],
             "fxpq_qconv": [p, p, p, C.c_int, p, p, p, p, p],
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
             "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
@@ -187,6 +190,11 @@ def requant_addmm(h, src, n, d_fmt, codes, code_type, b, b_type, d_fmt_b, relu, 
 def fl_search(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, d_sse=None):
     _call("fxpq_fl_search", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out),
           ptr(d_sse))
+
+
+def preprocess(h, src, n, wl, strategy, psi_rule, fl_lo, fl_hi, d_fmt_out):
+    _call("fxpq_preprocess", h.value, C.byref(src), n, wl, strategy, psi_rule, fl_lo, fl_hi,
+          ptr(d_fmt_out))
 
 
 def set_conv_tiling(h, mode):
