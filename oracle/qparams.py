@@ -1,0 +1,299 @@
+"""Oracle of the forward optimizer with Algorithm 1 (QParamsOpt) -- TEST
+INFRASTRUCTURE ONLY.
+
+Sec. "Quantization Parameters Optimization", Algorithm 1, Eq. 15-21, written
+from the text in NCHW with the oracle's own operations: for every data
+structure in order (the input image; then per conv / FC layer its weights,
+bias and output activations), starting from the preprocessor's initial
+format (Eq. 6-9, conservative rounding), step the fractional length away in
+each direction (alpha + beta fixed), evaluating each candidate by running the
+calibration batch with earlier layers quantized at their chosen formats, the
+current layer at the candidate and later layers in FP32 (the order-fixed
+teacher), and keep the smallest cost
+
+    F = sum_{i >= l} sum_j pi_i^j L(X_i^j) / R_i^j + UnClass + MisPred;
+
+a direction continues K steps past its last improvement.
+
+The same readings as the GPU driver: activations are layer outputs, the
+input image is the first data structure; L is the parameter quantization
+error for the current layer (zero for FP32 layers) and the distance from the
+teacher's activation for activations; pi = sigma * size normalized over a
+layer's data structures (sigma over the whole tensor); R = max - min of the
+FP32 data structure; eltwise / avg-pool FxP-QLayers keep their Eq. 14
+searches, Scale parameters their searched formats.  ResNets only (their FC
+follows a global pooling, so the FP32 FC sums in the same order on both
+sides).
+
+parity unpinned: no printed example exists for the search; it is pinned
+through its parts (tests/test_oracle_preprocess.py, tests/test_oracle_pins.py,
+tests/test_oracle_teacher.py) and by a brute-force check of the search rule
+(tests/test_oracle_qparams.py).
+"""
+import math
+
+import numpy as np
+
+import synth
+
+from . import core as orc
+from . import preprocess as pre
+from .nets import FL, SEED, resnet
+from .sweep import Teacher
+
+
+class Graph(Teacher):
+    """The FP32 teacher, also recording every node in order."""
+
+    def __init__(self, seed):
+        super().__init__(seed)
+        self.nodes = []
+
+    def network_input(self, x):
+        super().network_input(x)
+        self.x = x
+        self.nodes.append(("input", "input", {}))
+
+    def cblock(self, name, src, cout, k, stride, pad, wl, relu, bias, bn, fc=False, last=False):
+        super().cblock(name, src, cout, k, stride, pad, wl, relu, bias, bn, fc, last)
+        spec = self.layers[-1][2]
+        spec.update(wl=wl, cout=cout, src=src)
+        self.nodes.append(("conv", name, spec))
+
+    def maxpool(self, name, src, k, stride, pad):
+        super().maxpool(name, src, k, stride, pad)
+        self.nodes.append(("maxpool", name, {"src": src, "k": k, "stride": stride, "pad": pad}))
+
+    def add(self, name, a, b):
+        super().add(name, a, b)
+        self.nodes.append(("add", name, {"a": a, "b": b}))
+
+    def avgpool(self, name, src):
+        super().avgpool(name, src)
+        self.nodes.append(("avgpool", name, {"src": src}))
+
+
+def _stats(x):
+    x = np.asarray(x, np.float64).ravel()
+    return float(x.std()), x.size, float(x.max() - x.min())
+
+
+def _sse(ref, y):
+    d = np.asarray(ref, np.float64).ravel() - np.asarray(y, np.float64).ravel()
+    return math.fsum(d * d)
+
+
+def _ties(scores):
+    s = np.asarray(scores).reshape(scores.shape[0], -1)
+    c = (s == s.max(axis=1, keepdims=True)).sum(axis=1)
+    return int((c > 1).sum()), int((c - 1).sum())
+
+
+class ForwardOptimizer:
+    def __init__(self, name="resnet18", seed=None, batch=2, image=32, K=1,
+                 strategy=pre.CONSERVATIVE):
+        self.seed = SEED[name] if seed is None else seed
+        g = Graph(self.seed)
+        g.network_input(synth.normal(self.seed, "input", (batch, 3, image, image)))
+        resnet(g, name == "resnet50")
+        self.g, self.K, self.B = g, K, batch
+        self.spec = {nm: sp for op, nm, sp in g.nodes if op == "conv"}
+        self.order = [("input", "a")]
+        for op, nm, sp in g.nodes:
+            if op == "conv":
+                self.order.append((nm, "w"))
+                if "b" in sp:
+                    self.order.append((nm, "b"))
+                if not sp["last"]:
+                    self.order.append((nm, "a"))
+        self.qp, self.stat = {}, {}
+        last = [nm for nm, sp in self.spec.items() if sp["last"]][0]
+        for ln, d in self.order + [(last, "a")]:
+            x, wl = self._tensor(ln, d)
+            xmin, xmax = pre.exact_extremes_f32(x)
+            fl, sign = pre.init_fl(xmin, xmax, wl, strategy, pre.PSI_PRINTED, *FL)
+            self.qp[(ln, d)] = [wl, fl, sign]
+            self.stat[(ln, d)] = _stats(x)
+        self.pi = {}
+        for ln in ["input"] + list(self.spec):
+            ds = [d for d in ("a", "w", "b") if (ln, d) in self.stat]
+            tot = sum(self.stat[(ln, d)][0] * self.stat[(ln, d)][1] for d in ds)
+            for d in ds:
+                self.pi[(ln, d)] = self.stat[(ln, d)][0] * self.stat[(ln, d)][1] / tot if tot > 0 else 0.0
+        # Scale parameters: searched formats, fixed
+        self.scale = {}
+        for ln, sp in self.spec.items():
+            if "a1" in sp:
+                f1, s1, _ = orc.fl_search_f32(sp["a1"], 16, orc.SIGN_AUTO, *FL)
+                f2, s2, _ = orc.fl_search_f32(sp["a2"], 32, orc.SIGN_AUTO, *FL)
+                self.scale[ln] = (orc.quantize_f32(sp["a1"], 16, f1, s1).astype(np.int64), f1,
+                                  orc.quantize_f32(sp["a2"], 32, f2, s2).astype(np.int64), f2)
+        self.q = {}  # finalized nodes: (codes, fl, sign) NCHW
+        self.trace = []
+        self.last = last
+
+    def _tensor(self, ln, d):
+        if ln == "input":
+            return self.g.x, 8
+        sp = self.spec[ln]
+        if d == "w":
+            return sp["w"], sp["wl"]
+        if d == "b":
+            return sp["b"], 32
+        return self.g.act[ln], 8
+
+    # ---- one quantized layer ----
+    def _quant_layer(self, ln):
+        """(codes, fl, sign, errors {key: sse}) of layer ln at the current formats."""
+        if ln == "input":
+            wl, fl, sign = self.qp[("input", "a")]
+            q = orc.quantize_f32(self.g.x, wl, fl, sign)
+            return q, fl, sign, {("input", "a"): orc.layer_error(self.g.x.ravel(), q.ravel(), wl, fl, sign)[0]}
+        sp = self.spec[ln]
+        errs = {}
+        x, fl_x, _ = self.q[sp["src"]]
+        ww, flw, sw = self.qp[(ln, "w")]
+        wq = orc.quantize_f32(sp["w"], ww, flw, sw).astype(np.int64)
+        errs[(ln, "w")] = orc.layer_error(sp["w"].ravel(), wq.ravel(), ww, flw, sw)[0]
+        b = a1 = a2 = None
+        fl_b = fl_a1 = fl_a2 = 0
+        if "b" in sp:
+            bw, fl_b, sb = self.qp[(ln, "b")]
+            b = orc.quantize_f32(sp["b"], bw, fl_b, sb).astype(np.int64)
+            errs[(ln, "b")] = orc.layer_error(sp["b"].ravel(), b.ravel(), bw, fl_b, sb)[0]
+        if ln in self.scale:
+            a1, fl_a1, a2, fl_a2 = self.scale[ln]
+        if sp["fc"]:
+            acc = orc.gemm(x.reshape(x.shape[0], -1), wq)
+        else:
+            acc = orc.conv2d(x, wq, sp["stride"], sp["pad"])
+        v, s = orc.epilogue(acc, fl_x + flw, b, fl_b, a1, fl_a1, a2, fl_a2, sp["relu"])
+        ref = self.g.act[ln]
+        if sp["last"]:
+            q = orc.quantize_i64(v, s, 32, s, 1)
+            errs[(ln, "a")] = orc.layer_error(ref.ravel(), q.ravel(), 32, s, 1)[0]
+            return q, s, 1, errs
+        wl, fl, sign = self.qp[(ln, "a")]
+        q = orc.quantize_i64(v, s, wl, fl, sign)
+        errs[(ln, "a")] = orc.layer_error(ref.ravel(), q.ravel(), wl, fl, sign)[0]
+        return q, fl, sign, errs
+
+    def _fp32(self, codes, fl):
+        return (np.asarray(codes, np.float64) * 2.0 ** -fl).astype(np.float32)
+
+    def evaluate(self, ln):
+        q, fl, sign, errs = self._quant_layer(ln)
+        fp = {ln: self._fp32(q, fl)}
+        after = False if ln != "input" else True
+        logits = q if (ln != "input" and self.spec[ln]["last"]) else None
+        for op, nm, sp in self.g.nodes:
+            if nm == ln:
+                after = True
+                continue
+            if not after or op == "input":
+                continue
+            get = lambda k: fp[k] if k in fp else self._fp32(self.q[k][0], self.q[k][1])
+            if op == "conv":
+                x = get(sp["src"])
+                if sp["fc"]:
+                    xin = x.reshape(x.shape[0], -1)
+                    y = orc.teacher_conv2d(xin.reshape(xin.shape[0], -1, 1, 1),
+                                           sp["w"].reshape(sp["cout"], -1, 1, 1), 1, 0)
+                else:
+                    y = orc.teacher_conv2d(x, sp["w"], sp["stride"], sp["pad"])
+                if "b" in sp:
+                    y = orc.teacher_affine(y, bias=sp["b"], relu=sp["relu"])
+                elif "a1" in sp:
+                    y = orc.teacher_affine(y, sp["a1"], sp["a2"], relu=sp["relu"])
+                else:
+                    y = orc.teacher_affine(y, relu=sp["relu"])
+                errs[(nm, "a")] = _sse(self.g.act[nm], y)
+            elif op == "maxpool":
+                x = get(sp["src"])
+                N, C, H, W = x.shape
+                k, st, pd = sp["k"], sp["stride"], sp["pad"]
+                Ho, Wo = (H + 2 * pd - k) // st + 1, (W + 2 * pd - k) // st + 1
+                xp = np.full((N, C, H + 2 * pd, W + 2 * pd), -np.inf, np.float32)
+                xp[:, :, pd:pd + H, pd:pd + W] = x
+                y = np.full((N, C, Ho, Wo), -np.inf, np.float32)
+                for r in range(k):
+                    for s in range(k):
+                        y = np.maximum(y, xp[:, :, r:r + st * Ho:st, s:s + st * Wo:st])
+            elif op == "add":
+                v = get(sp["a"]) + get(sp["b"])
+                y = np.where(v > 0, v, np.float32(0)).astype(np.float32)
+            else:
+                y = orc.teacher_avgpool(get(sp["src"]))
+                y = y.reshape(y.shape[0], y.shape[1], 1, 1)
+            fp[nm] = y
+        scores = logits if logits is not None else fp[self.last]
+        un, extra = _ties(np.asarray(scores).reshape(self.B, -1))
+        E = sum(self.pi[k] * e / self.stat[k][2] for k, e in errs.items()
+                if k in self.pi and self.stat[k][2] > 0)
+        C = int(np.asarray(scores).reshape(self.B, -1).shape[1])
+        return E + un / self.B + extra / (self.B * C)
+
+    def qparams_opt(self, ln, d):
+        key = (ln, d)
+        fl0 = self.qp[key][1]
+        best = self.evaluate(ln)
+        fl_best = fl0
+        self.trace.append((ln, d, fl0, best))
+        for i in (-1, +1):
+            k, j = 1, 0
+            while k <= self.K + j:
+                fl = fl0 + i * k
+                if fl < FL[0] or fl > FL[1]:
+                    break
+                self.qp[key][1] = fl
+                cost = self.evaluate(ln)
+                self.trace.append((ln, d, fl, cost))
+                if cost < best:
+                    best, fl_best, j = cost, fl, j + 1
+                k += 1
+        self.qp[key][1] = fl_best
+        return fl_best
+
+    def finalize(self, ln):
+        q, fl, sign, _ = self._quant_layer(ln)
+        self.q[ln] = (q, fl, sign)
+        after = ln == "input"
+        for op, nm, sp in self.g.nodes:
+            if nm == ln:
+                after = True
+                continue
+            if not after or op == "input":
+                continue
+            if op == "conv":
+                break
+            if op == "maxpool":
+                x, f, s = self.q[sp["src"]]
+                self.q[nm] = (orc.maxpool(x, sp["k"], sp["stride"], sp["pad"]), f, s)
+            elif op == "add":
+                xa, fa, _ = self.q[sp["a"]]
+                xb, fb, _ = self.q[sp["b"]]
+                v, s = orc.eltwise_add(xa, fa, xb, fb, relu=True)
+                f, sg, _ = orc.fl_search_i64(v.ravel(), s, 8, orc.SIGN_AUTO, *FL)
+                self.q[nm] = (orc.quantize_i64(v, s, 8, f, sg), f, sg)
+            else:
+                x, f, _ = self.q[sp["src"]]
+                hw = x.shape[2] * x.shape[3]
+                r = np.repeat(np.array([np.float32(1.0) / np.float32(hw)], np.float32), 4)
+                fr, sr, _ = orc.fl_search_f32(r, 16, orc.SIGN_AUTO, *FL)
+                rq = orc.quantize_f32(r, 16, fr, sr)
+                y = orc.avgpool_global(x, int(rq[0])).reshape(x.shape[0], x.shape[1], 1, 1)
+                fo, so, _ = orc.fl_search_i64(y.ravel(), f + fr, 8, orc.SIGN_AUTO, *FL)
+                self.q[nm] = (orc.quantize_i64(y, f + fr, 8, fo, so), fo, so)
+
+    def run(self):
+        layers = []
+        for ln, d in self.order:
+            if ln not in layers:
+                layers.append(ln)
+        keys = set(self.order)
+        for ln in layers:
+            for d in ("w", "b", "a"):
+                if (ln, d) in keys:
+                    self.qparams_opt(ln, d)
+            self.finalize(ln)
+        return {k: tuple(self.qp[k]) for k in self.order}
