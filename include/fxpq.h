@@ -346,10 +346,31 @@ fxpq_status fxpq_avgpool_global(fxpq_handle h, const void* x, fxpq_dtype type,
  * of Eq. 16 and Eq. 18): d_out[0] = sum_i (ref_i - code_i * 2^-fl)^2,
  * d_out[1] = min(ref), d_out[2] = max(ref), d_out[3] = population standard
  * deviation of ref.  fp64 accumulation.  d_out is a device double[4].
+ * code_type FXPQ_F32 compares two fp32 tensors (codes holds fp32 values,
+ * d_fmt unused and may be NULL).
  */
 fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
                              fxpq_dtype code_type, const fxpq_fmt* d_fmt, int64_t n,
                              double* d_out);
+
+/*
+ * Dequantization (Eq. 1): out[i] = code_i * 2^-fl (codes stored as u - 128
+ * restored), exact in fp32 for codes below 2^24 in magnitude.  code_type any
+ * code dtype; d_fmt (device) the codes' format; out device float[n].
+ */
+fxpq_status fxpq_dequantize(fxpq_handle h, const void* codes, fxpq_dtype code_type,
+                            const fxpq_fmt* d_fmt, int64_t n, float* out);
+
+/*
+ * Prediction ties of a classifier (Sec. "Quantization Parameters
+ * Optimization", Eq. 19-20): for each of `rows` rows of `cols` scores
+ * (FXPQ_F32 or FXPQ_I32, row-major, device), c = the number of classes
+ * sharing the highest score (exact comparison).  d_out (device int64[2]):
+ * d_out[0] = rows with c > 1 (UnClass = d_out[0] / rows), d_out[1] = sum of
+ * c - 1 (MisPred = d_out[1] / (rows * cols)).
+ */
+fxpq_status fxpq_prediction_ties(fxpq_handle h, const void* scores, fxpq_dtype dtype, int32_t rows,
+                                 int32_t cols, int64_t* d_out);
 
 /* Sets d_scale[0] = fl_in + fl_w + ... as the C-Block output scale of `ep`
  * (device int32), for consumers that need it as a plain FXPQ_SRC_INT scale. */

@@ -216,6 +216,10 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
                              const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
                              int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,
                              double* d_minmax);
+hipError_t launch_dequant(const Ctx& c, const void* codes, int code_type, const fxpq_fmt* fmt,
+                          int64_t n, float* out);
+hipError_t launch_logit_ties(const Ctx& c, const void* scores, int dtype, int rows, int cols,
+                             long long* out);
 hipError_t launch_preprocess(const Ctx& c, const SrcDev& s, const double* d_minmax, int wl,
                              int strategy, int rule, int fl_lo, int fl_hi, fxpq_fmt* out);
 hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out);

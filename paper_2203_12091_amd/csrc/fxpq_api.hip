@@ -475,10 +475,27 @@ fxpq_status fxpq_avgpool_global(fxpq_handle h, const void* x, fxpq_dtype type,
 fxpq_status fxpq_layer_error(fxpq_handle h, const float* ref, const void* codes,
                              fxpq_dtype code_type, const fxpq_fmt* d_fmt, int64_t n,
                              double* d_out) {
-  if (!h || !ref || !codes || !d_fmt || !d_out || n < 1 || !is_code(code_type))
-    return FXPQ_ERR_INVALID_ARG;
+  if (!h || !ref || !codes || !d_out || n < 1) return FXPQ_ERR_INVALID_ARG;
+  if (code_type != FXPQ_F32 && (!is_code(code_type) || !d_fmt)) return FXPQ_ERR_INVALID_ARG;
   DeviceGuard g(h->device);
   return hip_status(launch_layer_error(ctx(h), ref, codes, code_type, d_fmt, n, d_out));
+}
+
+fxpq_status fxpq_dequantize(fxpq_handle h, const void* codes, fxpq_dtype code_type,
+                            const fxpq_fmt* d_fmt, int64_t n, float* out) {
+  if (!h || !codes || !d_fmt || !out || n < 0 || !is_code(code_type)) return FXPQ_ERR_INVALID_ARG;
+  if (n == 0) return FXPQ_OK;
+  DeviceGuard g(h->device);
+  return hip_status(launch_dequant(ctx(h), codes, code_type, d_fmt, n, out));
+}
+
+fxpq_status fxpq_prediction_ties(fxpq_handle h, const void* scores, fxpq_dtype dtype, int32_t rows,
+                                 int32_t cols, int64_t* d_out) {
+  if (!h || !scores || !d_out || rows < 1 || cols < 1) return FXPQ_ERR_INVALID_ARG;
+  if (dtype != FXPQ_F32 && dtype != FXPQ_I32) return FXPQ_ERR_INVALID_ARG;
+  DeviceGuard g(h->device);
+  return hip_status(launch_logit_ties(ctx(h), scores, dtype, rows, cols,
+                                      reinterpret_cast<long long*>(d_out)));
 }
 
 fxpq_status fxpq_teacher_conv(fxpq_handle h, const fxpq_conv_desc* d, const float* x,

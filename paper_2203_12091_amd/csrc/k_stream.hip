@@ -226,6 +226,7 @@ template <int CT>
 __device__ inline double code_at(const void* codes, int64_t i) {
   if constexpr (CT == FXPQ_I16) return static_cast<const int16_t*>(codes)[i];
   else if constexpr (CT == FXPQ_I32) return static_cast<const int32_t*>(codes)[i];
+  else if constexpr (CT == FXPQ_F32) return static_cast<const float*>(codes)[i];
   else return static_cast<const int8_t*>(codes)[i];
 }
 
@@ -234,7 +235,8 @@ __global__ __launch_bounds__(kThreads) void k_layer_error(const float* ref, cons
                                                           const fxpq_fmt* fmt, int64_t n,
                                                           double* part) {
   __shared__ double sh[8];
-  const double step = ldexp(1.0, -fmt->fl);
+  // fp32 values (CT == FXPQ_F32) are compared as they are
+  const double step = (CT == FXPQ_F32) ? 1.0 : ldexp(1.0, -fmt->fl);
   const double off = (CT == FXPQ_U8OFF || (CT == FXPQ_C8 && fmt->sign == 0)) ? 128.0 : 0.0;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
@@ -528,9 +530,92 @@ hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes,
     case FXPQ_I32: blocks = run(&k_layer_error<FXPQ_I32>); break;
     case FXPQ_U8OFF: blocks = run(&k_layer_error<FXPQ_U8OFF>); break;
     case FXPQ_C8: blocks = run(&k_layer_error<FXPQ_C8>); break;
+    case FXPQ_F32: blocks = run(&k_layer_error<FXPQ_F32>); break;
     default: blocks = run(&k_layer_error<FXPQ_I8>); break;
   }
   k_layer_error_fin<<<1, kThreads, 0, c.stream>>>(part, blocks, n, out);
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// Dequantization (Eq. 1): out[i] = code_i * 2^-fl (+128 for codes stored as
+// u - 128), exact in fp32 for codes below 2^24 in magnitude.
+// ----------------------------------------------------------------------------
+template <int CT>
+__global__ __launch_bounds__(kThreads) void k_dequant(const void* codes, const fxpq_fmt* fmt,
+                                                      int64_t n, float* out) {
+  const double step = ldexp(1.0, -fmt->fl);
+  const double off = (CT == FXPQ_U8OFF || (CT == FXPQ_C8 && fmt->sign == 0)) ? 128.0 : 0.0;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads)
+    out[i] = (float)((code_at<CT>(codes, i) + off) * step);
+}
+
+hipError_t launch_dequant(const Ctx& c, const void* codes, int code_type, const fxpq_fmt* fmt,
+                          int64_t n, float* out) {
+  auto run = [&](auto kernel) {
+    const int blocks = stream_grid(n, 0, 0, 1, resident_blocks(c, (const void*)kernel));
+    kernel<<<blocks, kThreads, 0, c.stream>>>(codes, fmt, n, out);
+  };
+  switch (code_type) {
+    case FXPQ_I16: run(&k_dequant<FXPQ_I16>); break;
+    case FXPQ_I32: run(&k_dequant<FXPQ_I32>); break;
+    case FXPQ_U8OFF: run(&k_dequant<FXPQ_U8OFF>); break;
+    case FXPQ_C8: run(&k_dequant<FXPQ_C8>); break;
+    default: run(&k_dequant<FXPQ_I8>); break;
+  }
+  return hipGetLastError();
+}
+
+// ----------------------------------------------------------------------------
+// Prediction ties of a classifier (Eq. 19-20): per row of `rows` x `cols`
+// scores, the number c of classes sharing the highest score (exact
+// comparison); out[0] = number of rows with c > 1, out[1] = sum of (c - 1).
+// One block; a wave per row.
+// ----------------------------------------------------------------------------
+template <typename T>
+__global__ __launch_bounds__(kThreads) void k_logit_ties(const T* s, int rows, int cols,
+                                                         long long* out) {
+  __shared__ long long sh[2][kThreads / 64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  long long un = 0, extra = 0;
+  for (int r = w; r < rows; r += kThreads / 64) {
+    const T* row = s + (int64_t)r * cols;
+    T mx = row[lane < cols ? lane : 0];
+    for (int j = lane; j < cols; j += 64) mx = row[j] > mx ? row[j] : mx;
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      const T o = __shfl_xor(mx, off, 64);
+      mx = o > mx ? o : mx;
+    }
+    int cnt = 0;
+    for (int j = lane; j < cols; j += 64) cnt += (row[j] == mx) ? 1 : 0;
+    cnt = wave_reduce(cnt, [](int a, int b) { return a + b; });
+    un += (cnt > 1) ? 1 : 0;
+    extra += cnt - 1;
+  }
+  if (lane == 0) {
+    sh[0][w] = un;
+    sh[1][w] = extra;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    long long a = 0, b = 0;
+    for (int i = 0; i < kThreads / 64; ++i) {
+      a += sh[0][i];
+      b += sh[1][i];
+    }
+    out[0] = a;
+    out[1] = b;
+  }
+}
+
+hipError_t launch_logit_ties(const Ctx& c, const void* scores, int dtype, int rows, int cols,
+                             long long* out) {
+  if (dtype == FXPQ_F32)
+    k_logit_ties<float><<<1, kThreads, 0, c.stream>>>(static_cast<const float*>(scores), rows, cols, out);
+  else
+    k_logit_ties<int32_t><<<1, kThreads, 0, c.stream>>>(static_cast<const int32_t*>(scores), rows, cols, out);
   return hipGetLastError();
 }
 

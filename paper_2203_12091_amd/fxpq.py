@@ -22,7 +22,8 @@ EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_cblock", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
-    "fxpq_epilogue_scale", "fxpq_timer_start", "fxpq_timer_read",
+    "fxpq_epilogue_scale", "fxpq_dequantize", "fxpq_prediction_ties", "fxpq_timer_start",
+    "fxpq_timer_read",
     "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
     "fxpq_teacher_avgpool",
 ]
@@ -93,6 +94,8 @@ def lib():
             "fxpq_avgpool_global": [p, p, C.c_int, p, i32, i32, i32, i64, p],
             "fxpq_layer_error": [p, p, p, C.c_int, p, i64, p],
             "fxpq_epilogue_scale": [p, p, p],
+            "fxpq_dequantize": [p, p, C.c_int, p, i64, p],
+            "fxpq_prediction_ties": [p, p, C.c_int, i32, i32, p],
             "fxpq_timer_start": [p, C.c_int],
             "fxpq_timer_read": [p, p, p, p],
             "fxpq_teacher_conv": [p, p, p, p, p],
@@ -237,6 +240,14 @@ def avgpool_global(h, x, dtype, d_fmt, n, hw, c, recip, y):
 
 def layer_error(h, ref, codes, code_type, d_fmt, n, d_out):
     _call("fxpq_layer_error", h.value, ptr(ref), ptr(codes), code_type, ptr(d_fmt), n, ptr(d_out))
+
+
+def dequantize(h, codes, code_type, d_fmt, n, out):
+    _call("fxpq_dequantize", h.value, ptr(codes), code_type, ptr(d_fmt), n, ptr(out))
+
+
+def prediction_ties(h, scores, dtype, rows, cols, d_out):
+    _call("fxpq_prediction_ties", h.value, ptr(scores), dtype, rows, cols, ptr(d_out))
 
 
 def epilogue_scale(h, ep, d_scale):

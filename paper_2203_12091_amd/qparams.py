@@ -1,0 +1,364 @@
+"""Forward optimizer with Algorithm 1 (QParamsOpt) over libfxpq.
+
+Sec. "Quantization Parameters Optimization" and Algorithm 1: the fractional
+length of each data structure (weights, then bias, then output activations of
+each conv / FC layer, layer by layer from the input) is moved from the
+preprocessor's initial value (Eq. 6-9) in both directions, one step at a
+time, keeping the word length (alpha + beta = k), and the one with the
+smallest cost
+
+    F(d, l) = E(d, l) + UnClass + MisPred                         (Eq. 21)
+
+is kept; a direction is searched K steps past the last improvement.  Every
+candidate runs the network on the calibration batch with layers before l
+quantized at their chosen formats, layer l quantized at the candidate, and
+the layers after l in FP32 (the order-fixed teacher kernels), then
+
+    E(d, l) = sum_{i >= l} sum_j pi_i^j L(X_i^j) / R_i^j          (Eq. 17)
+
+with pi from Eq. 15-16 (dispersion x size, normalized per layer), R the
+range of the FP32 data structure (Eq. 18), and L the squared error (Eq. 14):
+for parameters their quantization error at the current format (zero for the
+FP32 layers after l), for activations the distance of the network's
+activation from the FP32 teacher's (post-training self-distillation), and
+UnClass / MisPred from ties of the final scores (Eq. 19-20).
+
+Readings: activations are the layers' outputs (the input image is the first
+data structure, optimized before layer 1); eltwise and avg-pool FxP-QLayers
+keep their Eq. 14 searches; BN-as-Scale parameters keep their word lengths
+and searched formats; sigma of an activation is taken over the whole batch
+tensor; accuracy has no labels here, so the report is the agreement of the
+quantized network's top-1 with the FP32 teacher's.
+
+Every tensor operation is a libfxpq call; the host only sequences the
+candidates and adds up the per-tensor error sums the library returns.
+"""
+import numpy as np
+
+from . import fxpq as fx
+from .nets import A_WL, BIAS_WL, FL_HI, FL_LO, RECIP_WL
+from .sweep import Sweep
+
+
+class ForwardOptimizer:
+    def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", K=1,
+                 strategy=fx.ROUND_CONSERVATIVE, psi_rule=fx.PSI_PRINTED):
+        self.sw = Sweep(name, seed, batch, image, device, wwls=(), awls=())
+        self.T, self.h, self.B, self.K = self.sw.T, self.sw.h, self.sw.batch, K
+        T = self.T
+        self.nodes = list(self.sw.graph)
+        self.L = {L["node"].name: L for L in self.sw.layers}
+        self.act = self.sw.act  # FP32 teacher activations, NHWC
+        self.keep = []
+        self.bufs = {}
+        self.held = {}  # per layer: the ctypes structures its last calls used
+        self.evals = 0
+        # data structures in optimization order: the input, then per layer
+        # weights, bias, output activations (none for the last layer)
+        self.order = [("input", "a")]
+        for n in self.nodes:
+            if n.op in ("conv", "fc"):
+                self.order.append((n.name, "w"))
+                if n.bias:
+                    self.order.append((n.name, "b"))
+                if not n.last:
+                    self.order.append((n.name, "a"))
+        # per-tensor statistics and initial formats
+        self.fmt = {}   # (layer, d) -> device int32[4] {wl, fl, sign, 0}
+        self.qp = {}    # (layer, d) -> [wl, fl, sign] on the host
+        self.stat = {}  # (layer, d) -> (sigma, size, range)
+        out4 = self._empty((4,), T.float64)
+        for (ln, d) in self.order + [(n.name, "a") for n in self.nodes if getattr(n, "last", False)]:
+            ref, wl = self._tensor(ln, d)
+            real = self._real(ln, d)  # without the layout's zero padding
+            fmt = self._fmt()
+            fx.preprocess(self.h, fx.src_f32(real), real.numel(), wl, strategy, psi_rule, FL_LO, FL_HI, fmt)
+            fx.layer_error(self.h, real, real, fx.F32, None, real.numel(), out4)
+            f, e = fmt.cpu().numpy(), out4.cpu().numpy()
+            self.fmt[(ln, d)], self.qp[(ln, d)] = fmt, [int(f[0]), int(f[1]), int(f[2])]
+            self.stat[(ln, d)] = (float(e[3]), real.numel(), float(e[2] - e[1]))
+        self.pi = {}
+        for n in [None] + self.nodes:
+            ln = "input" if n is None else n.name
+            if n is not None and n.op not in ("conv", "fc"):
+                continue
+            ds = [d for d in ("a", "w", "b") if (ln, d) in self.stat]
+            tot = sum(self.stat[(ln, d)][0] * self.stat[(ln, d)][1] for d in ds)
+            for d in ds:
+                self.pi[(ln, d)] = self.stat[(ln, d)][0] * self.stat[(ln, d)][1] / tot if tot > 0 else 0.0
+        # quantized prefix: codes and formats of finalized nodes
+        self.qcodes, self.qfmt, self.deq = {}, {}, {}
+        self.pos = {n.name: i for i, n in enumerate(self.nodes)}
+        self.logit_fmt = self._t(np.array([32, 0, 1, 0], np.int32))
+        self.ties = self._empty((2,), T.int64)
+        self.trace = []
+
+    # -- helpers ----------------------------------------------------------------
+    def _t(self, a):
+        t = self.T.from_numpy(np.ascontiguousarray(a)).to(self.sw.dev)
+        self.keep.append(t)
+        return t
+
+    def _empty(self, shape, dtype):
+        t = self.T.empty(shape, dtype=dtype, device=self.sw.dev)
+        self.keep.append(t)
+        return t
+
+    def _fmt(self):
+        return self._t(np.zeros(4, np.int32))
+
+    def _buf(self, key, shape, dtype):
+        """A device buffer reused by every evaluation (allocated once per key)."""
+        b = self.bufs.get(key)
+        if b is None or tuple(b.shape) != tuple(shape) or b.dtype != dtype:
+            b = self.T.empty(shape, dtype=dtype, device=self.sw.dev)
+            self.bufs[key] = b
+        return b
+
+    def _tensor(self, ln, d):
+        """FP32 data structure (device) and its word length."""
+        if ln == "input":
+            return self.act["input"], A_WL
+        L = self.L[ln]
+        if d == "w":
+            return L["w_krsc"], L["node"].wl
+        if d == "b":
+            return L["b_f32"], BIAS_WL
+        return L["y_ref"], A_WL
+
+    def _real(self, ln, d):
+        """The data structure as the model defines it (the input's three
+        channels, the weights without the padded channel / row): its
+        statistics and initial format do not see the layout's zeros."""
+        if ln == "input":
+            x = self.act["input"]
+            return x[..., :3].contiguous()
+        if d == "w":
+            w = self.L[ln]["w_host"]
+            return self._t(np.asarray(w, np.float32).ravel())
+        return self._tensor(ln, d)[0]
+
+    def _set(self, key, fl):
+        self.qp[key][1] = fl
+        wl, _, sign = self.qp[key]
+        self.fmt[key].copy_(self.T.tensor([wl, fl, sign, 0], dtype=self.T.int32))
+
+    # -- one quantized layer at the current formats ---------------------------------
+    def _quant_layer(self, ln, errs):
+        """Runs layer ln on the quantized prefix at the current formats: its
+        output codes (or integer logits), with the parameter and output error
+        sums appended to errs as (key, device double[4])."""
+        T, h, B = self.T, self.h, self.B
+        if ln == "input":
+            x = self.act["input"]
+            codes = self._buf(("input", "codes"), x.shape, T.int8)
+            fx.quantize(h, x, x.numel(), self.fmt[("input", "a")], codes, fx.C8)
+            e = self._buf(("input", "a", "err"), (4,), T.float64)
+            fx.layer_error(h, x, codes, fx.C8, self.fmt[("input", "a")], x.numel(), e)
+            errs.append((("input", "a"), e))
+            return codes, self.fmt[("input", "a")], fx.C8
+        L = self.L[ln]
+        n = L["node"]
+        wcodes = self._buf((ln, "wcodes"), (L["w_krsc"].numel(),), T.int8)
+        fx.quantize(h, L["w_krsc"], L["w_krsc"].numel(), self.fmt[(ln, "w")], wcodes, fx.I8)
+        cs = self._buf((ln, "colsum"), (n.cout,), T.int32)
+        fx.weight_colsum(h, wcodes, n.cout, L["wlen"], cs)
+        e = self._buf((ln, "w", "err"), (4,), T.float64)
+        fx.layer_error(h, L["w_krsc"], wcodes, fx.I8, self.fmt[(ln, "w")], wcodes.numel(), e)
+        errs.append(((ln, "w"), e))
+        kw = {}
+        if n.bias:
+            bcodes = self._buf((ln, "bcodes"), (n.cout,), T.int32)
+            fx.quantize(h, L["b_f32"], n.cout, self.fmt[(ln, "b")], bcodes, fx.I32)
+            e = self._buf((ln, "b", "err"), (4,), T.float64)
+            fx.layer_error(h, L["b_f32"], bcodes, fx.I32, self.fmt[(ln, "b")], n.cout, e)
+            errs.append(((ln, "b"), e))
+            kw.update(bias=bcodes, fl_bias=self.qp[(ln, "b")][1])
+        if "a1" in L:
+            kw.update(scale=L["a1"], fl_scale=L["fl"][("a1", None)][1], shift=L["a2"],
+                      fl_shift=L["fl"][("a2", None)][1])
+        xin = self.qcodes[n.inp]
+        ep = fx.epilogue(n.cout, self.qp[(ln, "w")][1], self.qfmt[n.inp], relu=n.relu, **kw)
+        acc = self._buf(("acc",), (L["M"], n.cout), T.int32)
+        mm = self._buf((ln, "mm"), (2,), T.float64)
+        if L["fc"]:
+            fx.qgemm(h, L["M"], n.cout, L["wlen"], xin, fx.C8, wcodes, cs, ep, acc, mm)
+        else:
+            fx.qconv(h, L["desc"], xin, fx.C8, wcodes, cs, ep, acc, mm)
+        src = fx.src_acc(acc, ep, mm)
+        self.held[ln] = (ep, src)
+        y_ref = L["y_ref"]
+        e = self._buf((ln, "a", "err"), (4,), T.float64)
+        if n.last:
+            fx.epilogue_scale(h, ep, self.logit_fmt[1:2])
+            logits = self._buf((ln, "logits"), (L["M"], n.cout), T.int32)
+            fx.requant(h, src, acc.numel(), self.logit_fmt, logits, fx.I32)
+            fx.layer_error(h, y_ref, logits, fx.I32, self.logit_fmt, logits.numel(), e)
+            errs.append(((ln, "a"), e))
+            return logits, self.logit_fmt, fx.I32
+        codes = self._buf((ln, "codes"), (L["M"], n.cout), T.int8)
+        fx.requant(h, src, acc.numel(), self.fmt[(ln, "a")], codes, fx.C8)
+        fx.layer_error(h, y_ref, codes, fx.C8, self.fmt[(ln, "a")], codes.numel(), e)
+        errs.append(((ln, "a"), e))
+        return codes, self.fmt[(ln, "a")], fx.C8
+
+    def _quant_node(self, n):
+        """Quantized max-pool / eltwise / avg-pool node on finalized inputs (the
+        eltwise and avg-pool FxP-QLayers search their own formats)."""
+        T, h, B = self.T, self.h, self.B
+        H, W, C = self.act[n.inp].shape[1:]
+        if n.op == "maxpool":
+            Ho, Wo = self.act[n.name].shape[1:3]
+            y = self._empty((B, Ho, Wo, C), T.int8)
+            fx.maxpool(h, self.qcodes[n.inp], fx.C8, B, H, W, C, n.k, n.stride, n.pad, y)
+            return y, self.qfmt[n.inp]
+        f = self._fmt()
+        if n.op == "add":
+            src = fx.src_add(self.qcodes[n.inp], fx.C8, self.qfmt[n.inp], self.qcodes[n.other], fx.C8,
+                             self.qfmt[n.other], n.relu)
+            m = self.qcodes[n.inp].numel()
+        else:  # global avg-pool with the quantized reciprocal (same as the runner)
+            r = np.repeat(np.array([np.float32(1.0) / np.float32(H * W)], np.float32), 4)
+            rd, rf = self._t(r), self._fmt()
+            fx.fl_search(h, fx.src_f32(rd), 4, RECIP_WL, fx.SIGN_AUTO, FL_LO, FL_HI, rf)
+            rc = self._empty((4,), T.int32)
+            fx.quantize(h, rd, 4, rf, rc, fx.I32)
+            s = self._empty((B, C), T.int64)
+            fx.avgpool_global(h, self.qcodes[n.inp], fx.C8, self.qfmt[n.inp], B, H * W, C,
+                              int(rc.cpu().numpy()[0]), s)
+            ep = fx.epilogue(C, int(rf.cpu().numpy()[1]), self.qfmt[n.inp])
+            sc = self._empty((1,), T.int32)
+            fx.epilogue_scale(h, ep, sc)
+            src = fx.src_int(s, fx.I64, sc)
+            self.keep += [ep]
+            m = s.numel()
+        self.keep.append(src)
+        fx.fl_search(h, src, m, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+        y = self._empty(self.act[n.name].shape, T.int8)
+        fx.requant(h, src, m, f, y, fx.C8)
+        return y, f
+
+    def _dequant(self, name):
+        if name not in self.deq:
+            c = self.qcodes[name]
+            y = self._empty(c.shape, self.T.float32)
+            fx.dequantize(self.h, c, fx.C8, self.qfmt[name], c.numel(), y)
+            self.deq[name] = y
+        return self.deq[name]
+
+    # -- cost of the current formats for layer ln --------------------------------
+    def evaluate(self, ln):
+        T, h, B = self.T, self.h, self.B
+        self.evals += 1
+        errs = []
+        codes, cfmt, ctype = self._quant_layer(ln, errs)
+        if ctype == fx.C8:
+            y = self._buf((ln, "deq-cur"), codes.shape, T.float32)
+            fx.dequantize(h, codes, fx.C8, cfmt, codes.numel(), y)
+        fp = {ln: y if ctype == fx.C8 else None}
+        start = 0 if ln == "input" else self.pos[ln] + 1
+        logits32 = codes if ctype == fx.I32 else None
+        for n in self.nodes[start:]:
+            if n.op == "input":
+                continue
+            get = lambda nm: fp[nm] if nm in fp else self._dequant(nm)
+            ref = self.act[n.name]
+            y = self._buf((n.name, "fp32"), ref.shape, T.float32)
+            if n.op in ("conv", "fc"):
+                L = self.L[n.name]
+                fx.teacher_conv(h, L["tdesc"], get(n.inp), L["w_rsck"], y)
+                aff = {}
+                if n.bias:
+                    aff["bias"] = L["b_f32"]
+                if "a1_f32" in L:
+                    aff = {"a1": L["a1_f32"], "a2": L["a2_f32"]}
+                fx.teacher_affine(h, y, y.numel(), n.cout, y, relu=n.relu, **aff)
+                e = self._buf((n.name, "a", "err"), (4,), T.float64)
+                fx.layer_error(h, ref, y, fx.F32, None, y.numel(), e)
+                errs.append(((n.name, "a"), e))
+            elif n.op == "maxpool":
+                H, W, C = self.act[n.inp].shape[1:]
+                fx.teacher_maxpool(h, get(n.inp), B, H, W, C, n.k, n.stride, n.pad, y)
+            elif n.op == "add":
+                fx.teacher_add(h, get(n.inp), get(n.other), y.numel(), n.relu, y)
+            elif n.op == "avgpool":
+                H, W, C = self.act[n.inp].shape[1:]
+                fx.teacher_avgpool(h, get(n.inp), B, H * W, C, y)
+            fp[n.name] = y
+        last = [n for n in self.nodes if getattr(n, "last", False)][0]
+        if logits32 is not None:
+            fx.prediction_ties(h, logits32, fx.I32, B, last.cout, self.ties)
+        else:
+            fx.prediction_ties(h, fp[last.name], fx.F32, B, last.cout, self.ties)
+        T.cuda.synchronize(self.sw.dev)
+        E = 0.0
+        for key, e in errs:
+            if key in self.pi and self.stat[key][2] > 0:
+                E += self.pi[key] * float(e[0].item()) / self.stat[key][2]
+        t = self.ties.cpu().numpy()
+        unclass = float(t[0]) / B
+        mispred = float(t[1]) / (B * last.cout)
+        return E + unclass + mispred, (E, unclass, mispred)
+
+    # -- Algorithm 1 ------------------------------------------------------------------
+    def qparams_opt(self, ln, d):
+        key = (ln, d)
+        fl0 = self.qp[key][1]
+        best, parts = self.evaluate(ln)
+        fl_best = fl0
+        self.trace.append((ln, d, fl0, best))
+        for i in (-1, +1):
+            k, j = 1, 0
+            while k <= self.K + j:
+                fl = fl0 + i * k
+                if fl < FL_LO or fl > FL_HI:
+                    break
+                self._set(key, fl)
+                cost, _ = self.evaluate(ln)
+                self.trace.append((ln, d, fl, cost))
+                if cost < best:
+                    best, fl_best, j = cost, fl, j + 1
+                k += 1
+        self._set(key, fl_best)
+        return fl_best, best
+
+    def finalize(self, ln):
+        """Quantizes layer ln at its chosen formats into the prefix, then the
+        max-pool / eltwise / avg-pool nodes that follow it."""
+        errs = []
+        codes, cfmt, ctype = self._quant_layer(ln, errs)
+        self.qcodes[ln], self.qfmt[ln] = codes, cfmt
+        start = 0 if ln == "input" else self.pos[ln] + 1
+        for n in self.nodes[start:]:
+            if n.op in ("input",):
+                continue
+            if n.op in ("conv", "fc"):
+                break
+            self.qcodes[n.name], self.qfmt[n.name] = self._quant_node(n)
+
+    def run(self):
+        """The forward optimizer: every data structure in order; returns the
+        chosen formats."""
+        layers = []
+        for ln, d in self.order:
+            if ln not in layers:
+                layers.append(ln)
+        for ln in layers:
+            for d in ("w", "b", "a"):
+                if (ln, d) in self.qp and (ln, d) in dict.fromkeys(self.order):
+                    self.qparams_opt(ln, d)
+            self.finalize(ln)
+        return {k: tuple(v) for k, v in self.qp.items() if k in dict.fromkeys(self.order)}
+
+    def top1_agreement(self):
+        """Share of samples whose quantized top-1 (unique maximum) is the
+        teacher's top-1."""
+        last = [n for n in self.nodes if getattr(n, "last", False)][0]
+        q = self.qcodes[last.name].cpu().numpy().reshape(self.B, -1)
+        t = self.act[last.name].cpu().numpy().reshape(self.B, -1)
+        qa = q.argmax(1)
+        unique = (q == q.max(1, keepdims=True)).sum(1) == 1
+        return float(np.mean(unique & (qa == t.argmax(1))))
+
+    def close(self):
+        self.sw.close()

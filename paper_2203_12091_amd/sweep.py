@@ -113,7 +113,9 @@ class Sweep:
                 # teacher: conv, then BN-as-Scale or bias, then ReLU
                 y = self._empty((B, Ho, Wo, n.cout), T.float32)
                 tdesc = desc if n.op == "conv" else fx.conv_desc(B, 1, 1, H * W * Cin, n.cout, 1, 1, 1, 0)
-                fx.teacher_conv(self.h, tdesc, act[n.inp], self._t(w_rsck.astype(np.float32)), y)
+                L["w_rsck"] = self._t(w_rsck.astype(np.float32))
+                L["w_krsc"], L["w_host"], L["tdesc"] = wkd, w, tdesc
+                fx.teacher_conv(self.h, tdesc, act[n.inp], L["w_rsck"], y)
                 aff = {}
                 if n.bias:
                     b = synth.normal(seed, n.name + ".b", (n.cout,), std=0.01)
