@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
-    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep"], default="bench",
+    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams"], default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
                          "copy: one plain 1 GiB device copy (counter calibration); "
                          "sweep: the sensitivity sweep figures only")
@@ -86,6 +86,51 @@ def cpu_baseline(batch):
             "sample": f"ResNet-50 DFX calibration forward of {batch} images 224x224 "
                       f"(exact CPU oracle, parameters pre-quantized; {t:.1f} s forward, "
                       f"{t0 - t_prep:.1f} s set-up untimed)"}
+
+
+def qparams_figures(dev, batch=32, image=224):
+    """The forward optimizer (Algorithm 1, K = 1, conservative preprocessor
+    formats) over ResNet-18 on a calibration batch, timed from the teacher
+    onwards; the oracle's optimizer on a bounded sample beside it; and the
+    preprocessor's initial-format call over the network input."""
+    import torch
+    from paper_2203_12091_amd import fxpq as fx
+    from paper_2203_12091_amd import qparams
+    t0 = time.perf_counter()
+    fo = qparams.ForwardOptimizer("resnet18", batch=batch, image=image, device=str(dev))
+    torch.cuda.synchronize(dev)
+    t1 = time.perf_counter()
+    fo.run()
+    torch.cuda.synchronize(dev)
+    t2 = time.perf_counter()
+    out = {"metric": "forward optimizer (Algorithm 1) seconds, ResNet-18", "batch": batch,
+           "image": image, "K": fo.K, "data_structures": len(fo.order), "evaluations": fo.evals,
+           "setup_s": round(t1 - t0, 3), "optimize_s": round(t2 - t1, 3),
+           "evaluations_per_s": round(fo.evals / (t2 - t1), 2),
+           "top1_agreement_with_fp32": round(fo.top1_agreement(), 4)}
+    # the preprocessor over the network input (min / max pass + exact decision)
+    x = fo.act["input"]
+    fmt = torch.zeros(4, dtype=torch.int32, device=dev)
+    src = fx.src_f32(x)
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fx.preprocess(fo.h, src, x.numel(), 8, fx.ROUND_CONSERVATIVE, fx.PSI_PRINTED, -8, 15, fmt)
+    e1.record()
+    torch.cuda.synchronize(dev)
+    ms = e0.elapsed_time(e1) / reps
+    out["preprocess"] = {"tensor": f"input {tuple(x.shape)} fp32", "ms": round(ms, 4),
+                         "gbs": round(4 * x.numel() / (ms * 1e-3) / 1e9, 1)}
+    fo.close()
+    import oracle.qparams as oq
+    t0 = time.perf_counter()
+    ref = oq.ForwardOptimizer("resnet18", batch=1, image=16)
+    ref.run()
+    t = time.perf_counter() - t0
+    out["cpu_baseline"] = {"seconds": round(t, 2), "evaluations": len(ref.trace), "kind": "oracle",
+                           "sample": "ResNet-18, 1 image 16x16, K = 1 (exact CPU oracle)"}
+    return out
 
 
 def compute_bound_mfma(net, dev):
@@ -167,6 +212,9 @@ def main():
 
     if args.mode == "sweep":
         print(json.dumps(sweep_figures(dev)), flush=True)
+        return
+    if args.mode == "qparams":
+        print(json.dumps(qparams_figures(dev)), flush=True)
         return
 
     net = nets.CalibNet("resnet50", batch=BATCH, image=IMAGE, device="cuda:0")
