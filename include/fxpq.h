@@ -167,7 +167,10 @@ fxpq_status fxpq_sync_status(fxpq_handle h, uint32_t* flags);
  * format read from d_fmt (device).  rne rounds half to even.  code_type is
  * FXPQ_I8, FXPQ_U8OFF (unsigned 8-bit formats only), FXPQ_I16 or FXPQ_I32 and
  * must hold the format's code range.  n >= 0; n == 0 launches nothing.
- * Word lengths 2..32 (the 1-bit binary rule of Eq. 13 returns UNSUPPORTED).
+ * Word lengths 1..32.  A signed 1-bit format follows Eq. 13 (code -1 for
+ * x < 0, code 0 otherwise, decoded as +1) and is stored decoded: -1 or +1,
+ * so that a C-Block consumes it as it is; the same holds for every call that
+ * writes codes.
  */
 fxpq_status fxpq_quantize(fxpq_handle h, const float* x, int64_t n, const fxpq_fmt* d_fmt,
                           void* codes, fxpq_dtype code_type);
@@ -208,11 +211,13 @@ fxpq_status fxpq_requant_addmm(fxpq_handle h, const fxpq_src* src, int64_t n,
  * format {wl, fl, sign, 0} is written to d_fmt_out (device).  When d_sse is not
  * NULL it receives fl_hi - fl_lo + 1 errors (device doubles; fp64 sums whose
  * relative error is far below 1e-9); otherwise candidates that provably cannot
- * win are skipped.  Requirements: 2 <= wl <= 32, -64 <= fl_lo <= fl_hi <= 64,
+ * win are skipped.  Requirements: 1 <= wl <= 32, -64 <= fl_lo <= fl_hi <= 64,
  * n >= 1.  Exact range: |v| * 2^(fl_hi+24) < 2^52 for fp32 values and
  * |v * 2^s| < 2^52 for integer values when wl <= 16; |v * 2^max(s, fl_hi)| <
  * 2^62 when wl > 16.  Outside it FXPQ_FLAG_RANGE is raised and d_fmt_out gets a
- * nonzero status.
+ * nonzero status.  Word length 1 with a signed format evaluates every
+ * candidate with the Eq. 13 values (+-2^-fl) exactly; fp32 values below
+ * 2^-(fl_hi+24) in magnitude enter its errors truncated to that unit.
  */
 fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
                            int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out, double* d_sse);
@@ -235,7 +240,7 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
  * written, and should it win, the requantization pass produces them.  Any
  * content of d_fmt_out on entry is valid.
  * codes_alt: device, n bytes, caller-owned scratch, contents unspecified
- * afterwards.  Requirements: code_type FXPQ_C8, 2 <= wl <= 8, codes and
+ * afterwards.  Requirements: code_type FXPQ_C8, 1 <= wl <= 8, codes and
  * codes_alt 16-byte aligned, the rest as fxpq_fl_search.  Sources with 8-byte
  * values (FXPQ_SRC_INT over int64) run the two calls above.
  */
@@ -256,7 +261,8 @@ fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t w
  * pass).  Readings: all-zero data takes fl_hi; signed data without a positive
  * value takes the negative side alone.  d_fmt_out (device) receives
  * {wl, fl, S, 0}; non-finite data gives status 1 and FXPQ_FLAG_RANGE.
- * Requirements: 2 <= wl <= 32, -64 <= fl_lo <= fl_hi <= 64, n >= 1.
+ * Requirements: 2 <= wl <= 32 (Eq. 7 has no scale for 1 bit), -64 <= fl_lo <=
+ * fl_hi <= 64, n >= 1.
  */
 typedef enum { FXPQ_ROUND_CONSERVATIVE = 0, FXPQ_ROUND_NEUTRAL = 1, FXPQ_ROUND_AGGRESSIVE = 2 } fxpq_round_strategy;
 typedef enum { FXPQ_PSI_PRINTED = 0, FXPQ_PSI_MAX = 1 } fxpq_psi_rule;

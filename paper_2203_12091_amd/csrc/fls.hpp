@@ -160,7 +160,7 @@ __device__ inline WinSetup win_setup(const SrcDev& s, const double* mm, int wl, 
   const double qabs = fmax(w.u.qmax, -w.u.qmin);
   w.verdict = 0;
   if (!w.u.ok) w.verdict = 3;
-  else if (mode == MODE_REPORT || wl > 16 || wmax >= kTwo52) w.verdict = 2;
+  else if (mode == MODE_REPORT || wl > 16 || wl == 1 || wmax >= kTwo52) w.verdict = 2;
   else if (w.u.beta_nosat >= fl_hi) w.verdict = 1;
   else if (KIND != FXPQ_SRC_F32 && wmax * qabs * (double)per_thread >= kTwo53) w.verdict = 2;
   w.b0 = imax(fl_lo, w.u.beta_nosat);

@@ -277,7 +277,6 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
                            double* d_sse) {
   if (!h || n < 1 || !d_fmt_out) return FXPQ_ERR_INVALID_ARG;
   if (wl < 1 || wl > 32) return FXPQ_ERR_INVALID_ARG;
-  if (wl == 1) return FXPQ_ERR_UNSUPPORTED;
   if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
   if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
   if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
@@ -330,7 +329,6 @@ fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t w
   if (!h || n < 1 || !d_fmt_out || !codes || !codes_alt) return FXPQ_ERR_INVALID_ARG;
   if (code_type != FXPQ_C8) return FXPQ_ERR_INVALID_ARG;
   if (wl < 1 || wl > 8) return FXPQ_ERR_INVALID_ARG;
-  if (wl == 1) return FXPQ_ERR_UNSUPPORTED;
   if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
   if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
   if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;

@@ -428,7 +428,9 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
   const int sigma = (KIND == FXPQ_SRC_F32) ? fl_hi + 24 : imax(sv, fl_hi);
   const double wscale = ldexp(1.0, sigma - sv);
   const double absmax = fmax(fabs(mm[0]), fabs(mm[1]));
-  if (absmax * wscale >= 0x1p62) {
+  // signed 1 bit (Eq. 13): the decoded value is sign(x) * 2^-beta, 2^d units
+  const bool binary = (wl == 1 && sign == 1);
+  if (absmax * wscale >= 0x1p62 || (binary && sigma - fl_lo > 62)) {
     if (blockIdx.x == 0 && threadIdx.x == 0) {
       *out = fxpq_fmt{wl, 0, sign, 2};
       raise_flag(flags, FXPQ_FLAG_RANGE);
@@ -449,7 +451,21 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
     for (int64_t i = e0 + threadIdx.x; i < e1; i += kThreads) {
       double W = load1<KIND, DT>(s, i) * wscale;
       unsigned __int128 e2;
-      if (W != floor(W)) {
+      if (binary) {
+        // |x - sign(x) 2^-beta| = | |x| - 2^-beta |; an fp32 value below
+        // 2^-(fl_hi+24) has a fractional |W|: (2^d - |W|)^2 is then summed
+        // truncated to the unit (error below 2 units per such value)
+        const double aw = fabs(W);
+        if (aw != floor(aw)) {
+          const unsigned __int128 u = (unsigned __int128)1 << d;
+          e2 = u * u - (unsigned __int128)(unsigned long long)floor(ldexp(aw, d + 1)) +
+               (unsigned __int128)(unsigned long long)floor(aw * aw);
+        } else {
+          __int128 err = (__int128)(long long)aw - ((__int128)1 << d);
+          if (err < 0) err = -err;
+          e2 = (unsigned __int128)err * (unsigned __int128)err;
+        }
+      } else if (W != floor(W)) {
         // fp32 value below 2^-(fl_hi+1): its code is 0 for every candidate and
         // its (identical) error is added truncated to the common unit.
         e2 = (unsigned __int128)(unsigned long long)floor(W * W);

@@ -221,6 +221,7 @@ struct QFmt {
   double qmin, qmax, mult;
   int off;         // 128 when stored as u - 128
   int lo, hi;      // storage range
+  bool binary;     // signed 1-bit format (Eq. 13): stored decoded, -1 or +1
   bool ok;
 };
 
@@ -228,7 +229,8 @@ template <int OUT>
 __device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) {
   QFmt q;
   int k = fmt->wl, fl = fmt->fl, sg = fmt->sign;
-  q.ok = (fmt->status == 0 && k >= 2 && k <= 32 && (sg == 0 || sg == 1));
+  q.ok = (fmt->status == 0 && k >= 1 && k <= 32 && (sg == 0 || sg == 1));
+  q.binary = (k == 1 && sg == 1);
   if (!q.ok) {
     if (blockIdx.x == 0 && threadIdx.x == 0) raise_flag(flags, FXPQ_FLAG_RANGE);
     return q;
@@ -254,6 +256,9 @@ __device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) 
 }
 
 __device__ inline int quant_one(double v, const QFmt& q) {
+  // Eq. 13: negative values take code -1, the rest code 0, which decodes to
+  // +1; the decoded value is what is stored, so a C-Block uses it as it is
+  if (q.binary) return v < 0.0 ? -1 : 1;
   double r = rint(v * q.mult);  // round half to even
   r = fmin(fmax(r, q.qmin), q.qmax);
   double c = r - (double)q.off;

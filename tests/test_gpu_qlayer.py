@@ -198,6 +198,6 @@ def test_qlayer_host_checks(fx, h):
     assert L.fxpq_qlayer(*args(8, fx.C8, codes.data_ptr(), None)) == fx.ERR_INVALID_ARG
     assert L.fxpq_qlayer(*args(8, fx.I8, codes.data_ptr(), codes.data_ptr())) == fx.ERR_INVALID_ARG
     assert L.fxpq_qlayer(*args(9, fx.C8, codes.data_ptr(), codes.data_ptr())) == fx.ERR_INVALID_ARG
-    assert L.fxpq_qlayer(*args(1, fx.C8, codes.data_ptr(), codes.data_ptr())) == fx.ERR_UNSUPPORTED
+    assert L.fxpq_qlayer(*args(0, fx.C8, codes.data_ptr(), codes.data_ptr())) == fx.ERR_INVALID_ARG
     assert L.fxpq_qlayer(*args(8, fx.C8, codes.data_ptr() + 1, codes.data_ptr())) == fx.ERR_INVALID_ARG
     check_flags(fx, h)
