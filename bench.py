@@ -43,7 +43,8 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
-    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams"], default="bench",
+    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams", "reduction"],
+                    default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
                          "copy: one plain 1 GiB device copy (counter calibration); "
                          "sweep: the sensitivity sweep figures only")
@@ -133,6 +134,51 @@ def qparams_figures(dev, batch=32, image=224):
     return out
 
 
+def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=8):
+    """Bit-precision level reduction (Algorithm 2) over ResNet-18 on a
+    calibration batch: the forward optimizer's 8-bit design first (untimed
+    set-up), then Algorithm 2 capped at max_changes applied reductions,
+    timed; the memory model before and after; the oracle's reduction on a
+    bounded sample beside it."""
+    import torch
+    from paper_2203_12091_amd import qparams, reduction
+    fo = qparams.ForwardOptimizer("resnet18", batch=batch, image=image, device=str(dev), w_wl=8)
+    fo.run()
+    torch.cuda.synchronize(dev)
+    before = reduction.memory_model(fo)
+    acc0 = fo.top1_agreement()
+    r = reduction.QReduction(fo, thld, max_changes=max_changes)
+    e0 = fo.evals
+    t0 = time.perf_counter()
+    r.run()
+    torch.cuda.synchronize(dev)
+    t = time.perf_counter() - t0
+    after = reduction.memory_model(fo)
+    ev = fo.evals - e0
+    out = {"metric": "bit-precision reduction (Algorithm 2) seconds, ResNet-18", "batch": batch,
+           "image": image, "threshold": thld, "max_changes": max_changes,
+           "changes": [f"{ln}.{d}: -{th} -> {wl} bits" for ln, d, th, wl, _, _ in r.changes],
+           "trials": len(r.trials), "evaluations": ev, "seconds": round(t, 3),
+           "evaluations_per_s": round(ev / t, 2), "top1_agreement_before": round(acc0, 4),
+           "top1_agreement_after": round(r.accuracy(), 4),
+           "memory_mb_before": {k: round(v, 4) for k, v in before.items()},
+           "memory_mb_after": {k: round(v, 4) for k, v in after.items()}}
+    fo.close()
+    import oracle.qparams as oq
+    import oracle.reduction as orr
+    ref = oq.ForwardOptimizer("resnet18", batch=1, image=16, w_wl=8)
+    ref.run()
+    rr = orr.QReduction(ref, thld, max_changes=2)
+    n0 = len(ref.trace)
+    t0 = time.perf_counter()
+    rr.run()
+    t = time.perf_counter() - t0
+    out["cpu_baseline"] = {"seconds": round(t, 2), "evaluations": len(ref.trace) - n0,
+                           "changes": len(rr.changes), "kind": "oracle",
+                           "sample": "ResNet-18, 1 image 16x16, 2 changes (exact CPU oracle)"}
+    return out
+
+
 def compute_bound_mfma(net, dev):
     """int8 MFMA use over the convolutions whose arithmetic intensity (int8
     ops per HBM byte: input codes, weights, int32 output) is above the ridge
@@ -215,6 +261,9 @@ def main():
         return
     if args.mode == "qparams":
         print(json.dumps(qparams_figures(dev)), flush=True)
+        return
+    if args.mode == "reduction":
+        print(json.dumps(reduction_figures(dev)), flush=True)
         return
 
     net = nets.CalibNet("resnet50", batch=BATCH, image=IMAGE, device="cuda:0")

@@ -83,6 +83,14 @@ def _sse(ref, y):
     return math.fsum(d * d)
 
 
+def _dec(q, wl, sign):
+    """Eq. 13: the 1-bit signed code 0 stands for +1 (the values the
+    arithmetic uses); other formats use their codes as they are."""
+    if wl == 1 and sign == 1:
+        return np.where(np.asarray(q) == 0, 1, -1).astype(np.int64)
+    return q
+
+
 def _ties(scores):
     s = np.asarray(scores).reshape(scores.shape[0], -1)
     c = (s == s.max(axis=1, keepdims=True)).sum(axis=1)
@@ -91,12 +99,12 @@ def _ties(scores):
 
 class ForwardOptimizer:
     def __init__(self, name="resnet18", seed=None, batch=2, image=32, K=1,
-                 strategy=pre.CONSERVATIVE):
+                 strategy=pre.CONSERVATIVE, w_wl=None):
         self.seed = SEED[name] if seed is None else seed
         g = Graph(self.seed)
         g.network_input(synth.normal(self.seed, "input", (batch, 3, image, image)))
         resnet(g, name == "resnet50")
-        self.g, self.K, self.B = g, K, batch
+        self.g, self.K, self.B, self.w_wl = g, K, batch, w_wl
         self.spec = {nm: sp for op, nm, sp in g.nodes if op == "conv"}
         self.order = [("input", "a")]
         for op, nm, sp in g.nodes:
@@ -129,6 +137,7 @@ class ForwardOptimizer:
                 self.scale[ln] = (orc.quantize_f32(sp["a1"], 16, f1, s1).astype(np.int64), f1,
                                   orc.quantize_f32(sp["a2"], 32, f2, s2).astype(np.int64), f2)
         self.q = {}  # finalized nodes: (codes, fl, sign) NCHW
+        self._pcache = {}
         self.trace = []
         self.last = last
 
@@ -137,30 +146,48 @@ class ForwardOptimizer:
             return self.g.x, 8
         sp = self.spec[ln]
         if d == "w":
-            return sp["w"], sp["wl"]
+            return sp["w"], self.w_wl or sp["wl"]
         if d == "b":
             return sp["b"], 32
         return self.g.act[ln], 8
 
     # ---- one quantized layer ----
-    def _quant_layer(self, ln):
-        """(codes, fl, sign, errors {key: sse}) of layer ln at the current formats."""
+    def _param(self, ln, d):
+        """Codes (Eq. 12-13) and squared error of parameter d of layer ln at
+        its current format (kept per format: parameters do not change)."""
+        wl, fl, sign = self.qp[(ln, d)]
+        hit = self._pcache.get((ln, d))
+        if hit is not None and hit[0] == (wl, fl, sign):
+            return hit[1], hit[2]
+        x = self.spec[ln][d]
+        c = orc.quantize_f32(x, wl, fl, sign).astype(np.int64)
+        e = orc.layer_error(x.ravel(), c.ravel(), wl, fl, sign)[0]
+        self._pcache[(ln, d)] = ((wl, fl, sign), c, e)
+        return c, e
+
+    def _quant_layer(self, ln, q=None):
+        """(codes, fl, sign, errors {key: sse}) of layer ln at the current
+        formats, its input taken from q (default: the finalized prefix).  The
+        codes returned are the values the next layer multiplies (Eq. 13
+        decoded); the errors use the codes as Eq. 12-13 define them."""
+        q = self.q if q is None else q
         if ln == "input":
             wl, fl, sign = self.qp[("input", "a")]
-            q = orc.quantize_f32(self.g.x, wl, fl, sign)
-            return q, fl, sign, {("input", "a"): orc.layer_error(self.g.x.ravel(), q.ravel(), wl, fl, sign)[0]}
+            c = orc.quantize_f32(self.g.x, wl, fl, sign)
+            return (_dec(c, wl, sign), fl, sign,
+                    {("input", "a"): orc.layer_error(self.g.x.ravel(), c.ravel(), wl, fl, sign)[0]})
         sp = self.spec[ln]
         errs = {}
-        x, fl_x, _ = self.q[sp["src"]]
+        x, fl_x, _ = q[sp["src"]]
         ww, flw, sw = self.qp[(ln, "w")]
-        wq = orc.quantize_f32(sp["w"], ww, flw, sw).astype(np.int64)
-        errs[(ln, "w")] = orc.layer_error(sp["w"].ravel(), wq.ravel(), ww, flw, sw)[0]
+        wc, errs[(ln, "w")] = self._param(ln, "w")
+        wq = _dec(wc, ww, sw)
         b = a1 = a2 = None
         fl_b = fl_a1 = fl_a2 = 0
         if "b" in sp:
             bw, fl_b, sb = self.qp[(ln, "b")]
-            b = orc.quantize_f32(sp["b"], bw, fl_b, sb).astype(np.int64)
-            errs[(ln, "b")] = orc.layer_error(sp["b"].ravel(), b.ravel(), bw, fl_b, sb)[0]
+            bc, errs[(ln, "b")] = self._param(ln, "b")
+            b = _dec(bc, bw, sb)
         if ln in self.scale:
             a1, fl_a1, a2, fl_a2 = self.scale[ln]
         if sp["fc"]:
@@ -174,9 +201,9 @@ class ForwardOptimizer:
             errs[(ln, "a")] = orc.layer_error(ref.ravel(), q.ravel(), 32, s, 1)[0]
             return q, s, 1, errs
         wl, fl, sign = self.qp[(ln, "a")]
-        q = orc.quantize_i64(v, s, wl, fl, sign)
-        errs[(ln, "a")] = orc.layer_error(ref.ravel(), q.ravel(), wl, fl, sign)[0]
-        return q, fl, sign, errs
+        c = orc.quantize_i64(v, s, wl, fl, sign)
+        errs[(ln, "a")] = orc.layer_error(ref.ravel(), c.ravel(), wl, fl, sign)[0]
+        return _dec(c, wl, sign), fl, sign, errs
 
     def _fp32(self, codes, fl):
         return (np.asarray(codes, np.float64) * 2.0 ** -fl).astype(np.float32)
@@ -233,10 +260,20 @@ class ForwardOptimizer:
         C = int(np.asarray(scores).reshape(self.B, -1).shape[1])
         return E + un / self.B + extra / (self.B * C)
 
-    def qparams_opt(self, ln, d):
+    def qparams_opt(self, ln, d, quantized=False):
+        """Algorithm 1 for data structure (ln, d) from its current format;
+        with quantized=True every candidate runs the whole quantized network
+        (evaluate_quant) and self.acc_best receives the top-1 agreement of the
+        chosen candidate."""
         key = (ln, d)
         fl0 = self.qp[key][1]
-        best = self.evaluate(ln)
+
+        def ev():
+            if quantized:
+                return self.evaluate_quant(ln)
+            return self.evaluate(ln), None
+
+        best, acc = ev()
         fl_best = fl0
         self.trace.append((ln, d, fl0, best))
         for i in (-1, +1):
@@ -246,44 +283,87 @@ class ForwardOptimizer:
                 if fl < FL[0] or fl > FL[1]:
                     break
                 self.qp[key][1] = fl
-                cost = self.evaluate(ln)
+                cost, a = ev()
                 self.trace.append((ln, d, fl, cost))
                 if cost < best:
-                    best, fl_best, j = cost, fl, j + 1
+                    best, fl_best, acc, j = cost, fl, a, j + 1
                 k += 1
         self.qp[key][1] = fl_best
+        self.acc_best = acc
         return fl_best
+
+    def _after(self, ln):
+        """The nodes after ln in network order (all nodes for the input)."""
+        names = [nm for _, nm, _ in self.g.nodes]
+        i = 0 if ln == "input" else names.index(ln)
+        return [nd for nd in self.g.nodes[i + 1:] if nd[0] != "input"]
+
+    def _node_q(self, op, sp, q):
+        """A quantized max-pool / eltwise / avg-pool node on the codes in q
+        (the eltwise and avg-pool FxP-QLayers search their formats, Eq. 14)."""
+        if op == "maxpool":
+            x, f, s = q[sp["src"]]
+            return orc.maxpool(x, sp["k"], sp["stride"], sp["pad"]), f, s
+        if op == "add":
+            xa, fa, _ = q[sp["a"]]
+            xb, fb, _ = q[sp["b"]]
+            v, s = orc.eltwise_add(xa, fa, xb, fb, relu=True)
+            f, sg, _ = orc.fl_search_i64(v.ravel(), s, 8, orc.SIGN_AUTO, *FL)
+            return orc.quantize_i64(v, s, 8, f, sg), f, sg
+        x, f, _ = q[sp["src"]]
+        hw = x.shape[2] * x.shape[3]
+        r = np.repeat(np.array([np.float32(1.0) / np.float32(hw)], np.float32), 4)
+        fr, sr, _ = orc.fl_search_f32(r, 16, orc.SIGN_AUTO, *FL)
+        rq = orc.quantize_f32(r, 16, fr, sr)
+        y = orc.avgpool_global(x, int(rq[0])).reshape(x.shape[0], x.shape[1], 1, 1)
+        fo, so, _ = orc.fl_search_i64(y.ravel(), f + fr, 8, orc.SIGN_AUTO, *FL)
+        return orc.quantize_i64(y, f + fr, 8, fo, so), fo, so
 
     def finalize(self, ln):
         q, fl, sign, _ = self._quant_layer(ln)
         self.q[ln] = (q, fl, sign)
-        after = ln == "input"
-        for op, nm, sp in self.g.nodes:
-            if nm == ln:
-                after = True
-                continue
-            if not after or op == "input":
-                continue
+        for op, nm, sp in self._after(ln):
             if op == "conv":
                 break
-            if op == "maxpool":
-                x, f, s = self.q[sp["src"]]
-                self.q[nm] = (orc.maxpool(x, sp["k"], sp["stride"], sp["pad"]), f, s)
-            elif op == "add":
-                xa, fa, _ = self.q[sp["a"]]
-                xb, fb, _ = self.q[sp["b"]]
-                v, s = orc.eltwise_add(xa, fa, xb, fb, relu=True)
-                f, sg, _ = orc.fl_search_i64(v.ravel(), s, 8, orc.SIGN_AUTO, *FL)
-                self.q[nm] = (orc.quantize_i64(v, s, 8, f, sg), f, sg)
+            self.q[nm] = self._node_q(op, sp, self.q)
+
+    def refinalize(self, ln):
+        """Re-quantizes the finalized network from layer ln on (after a
+        format of ln changed)."""
+        self.finalize(ln)
+        for op, nm, _ in self._after(ln):
+            if op == "conv":
+                self.finalize(nm)
+
+    def top1(self, logits):
+        """Share of samples whose scores have a unique maximum at the
+        teacher's top-1 class."""
+        s = np.asarray(logits).reshape(self.B, -1)
+        t = np.asarray(self.g.act[self.last]).reshape(self.B, -1).argmax(axis=1)
+        unique = (s == s.max(axis=1, keepdims=True)).sum(axis=1) == 1
+        return float(np.mean(unique & (s.argmax(axis=1) == t)))
+
+    def evaluate_quant(self, ln):
+        """Cost F of the current formats with the whole network quantized:
+        the finalized prefix, layer ln at its current formats and every later
+        layer quantized at its formats (the errors of all data structures
+        from ln on, parameters included); also the top-1 agreement."""
+        cur = dict(self.q)
+        c, fl, sign, errs = self._quant_layer(ln, cur)
+        cur[ln] = (c, fl, sign)
+        for op, nm, sp in self._after(ln):
+            if op == "conv":
+                c, f, s, e = self._quant_layer(nm, cur)
+                errs.update(e)
+                cur[nm] = (c, f, s)
             else:
-                x, f, _ = self.q[sp["src"]]
-                hw = x.shape[2] * x.shape[3]
-                r = np.repeat(np.array([np.float32(1.0) / np.float32(hw)], np.float32), 4)
-                fr, sr, _ = orc.fl_search_f32(r, 16, orc.SIGN_AUTO, *FL)
-                rq = orc.quantize_f32(r, 16, fr, sr)
-                y = orc.avgpool_global(x, int(rq[0])).reshape(x.shape[0], x.shape[1], 1, 1)
-                fo, so, _ = orc.fl_search_i64(y.ravel(), f + fr, 8, orc.SIGN_AUTO, *FL)
-                self.q[nm] = (orc.quantize_i64(y, f + fr, 8, fo, so), fo, so)
+                cur[nm] = self._node_q(op, sp, cur)
+        scores = np.asarray(cur[self.last][0]).reshape(self.B, -1)
+        un, extra = _ties(scores)
+        E = sum(self.pi[k] * e / self.stat[k][2] for k, e in errs.items()
+                if k in self.pi and self.stat[k][2] > 0)
+        cost = E + un / self.B + extra / (self.B * scores.shape[1])
+        return cost, self.top1(scores)
 
     def run(self):
         layers = []

@@ -42,9 +42,10 @@ from .sweep import Sweep
 
 class ForwardOptimizer:
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", K=1,
-                 strategy=fx.ROUND_CONSERVATIVE, psi_rule=fx.PSI_PRINTED):
+                 strategy=fx.ROUND_CONSERVATIVE, psi_rule=fx.PSI_PRINTED, w_wl=None):
         self.sw = Sweep(name, seed, batch, image, device, wwls=(), awls=())
         self.T, self.h, self.B, self.K = self.sw.T, self.sw.h, self.sw.batch, K
+        self.w_wl = w_wl  # one word length for every layer's weights (else the network's)
         T = self.T
         self.nodes = list(self.sw.graph)
         self.L = {L["node"].name: L for L in self.sw.layers}
@@ -92,6 +93,8 @@ class ForwardOptimizer:
         self.logit_fmt = self._t(np.array([32, 0, 1, 0], np.int32))
         self.ties = self._empty((2,), T.int64)
         self.trace = []
+        self.pfmt = {}  # (layer, d) -> the format its parameter codes hold
+        self.acc_best = None
 
     # -- helpers ----------------------------------------------------------------
     def _t(self, a):
@@ -121,7 +124,7 @@ class ForwardOptimizer:
             return self.act["input"], A_WL
         L = self.L[ln]
         if d == "w":
-            return L["w_krsc"], L["node"].wl
+            return L["w_krsc"], self.w_wl or L["node"].wl
         if d == "b":
             return L["b_f32"], BIAS_WL
         return L["y_ref"], A_WL
@@ -138,17 +141,37 @@ class ForwardOptimizer:
             return self._t(np.asarray(w, np.float32).ravel())
         return self._tensor(ln, d)[0]
 
-    def _set(self, key, fl):
+    def _set(self, key, fl, wl=None):
+        if wl is not None:
+            self.qp[key][0] = wl
         self.qp[key][1] = fl
         wl, _, sign = self.qp[key]
         self.fmt[key].copy_(self.T.tensor([wl, fl, sign, 0], dtype=self.T.int32))
 
     # -- one quantized layer at the current formats ---------------------------------
-    def _quant_layer(self, ln, errs):
-        """Runs layer ln on the quantized prefix at the current formats: its
-        output codes (or integer logits), with the parameter and output error
-        sums appended to errs as (key, device double[4])."""
+    def _param(self, ln, d, codes, ctype, errs):
+        """Quantizes parameter d of layer ln into codes at its current format
+        (skipped while the format is the one its codes hold) and appends its
+        error sums to errs."""
+        L, key = self.L[ln], (ln, d)
+        e = self._buf((ln, d, "err"), (4,), self.T.float64)
+        fq = tuple(self.qp[key])
+        if self.pfmt.get(key) != fq:
+            x = L["w_krsc"] if d == "w" else L["b_f32"]
+            fx.quantize(self.h, x, x.numel(), self.fmt[key], codes, ctype)
+            if d == "w":
+                fx.weight_colsum(self.h, codes, L["node"].cout, L["wlen"], self._buf((ln, "colsum"), (L["node"].cout,), self.T.int32))
+            fx.layer_error(self.h, x, codes, ctype, self.fmt[key], x.numel(), e)
+            self.pfmt[key] = fq
+        errs.append((key, e))
+
+    def _quant_layer(self, ln, errs, src=None):
+        """Runs layer ln at the current formats on its quantized input (from
+        src = (codes, formats) by node name, default the finalized prefix):
+        its output codes (or integer logits), with the parameter and output
+        error sums appended to errs as (key, device double[4])."""
         T, h, B = self.T, self.h, self.B
+        qcodes, qfmt = src if src is not None else (self.qcodes, self.qfmt)
         if ln == "input":
             x = self.act["input"]
             codes = self._buf(("input", "codes"), x.shape, T.int8)
@@ -160,25 +183,18 @@ class ForwardOptimizer:
         L = self.L[ln]
         n = L["node"]
         wcodes = self._buf((ln, "wcodes"), (L["w_krsc"].numel(),), T.int8)
-        fx.quantize(h, L["w_krsc"], L["w_krsc"].numel(), self.fmt[(ln, "w")], wcodes, fx.I8)
+        self._param(ln, "w", wcodes, fx.I8, errs)
         cs = self._buf((ln, "colsum"), (n.cout,), T.int32)
-        fx.weight_colsum(h, wcodes, n.cout, L["wlen"], cs)
-        e = self._buf((ln, "w", "err"), (4,), T.float64)
-        fx.layer_error(h, L["w_krsc"], wcodes, fx.I8, self.fmt[(ln, "w")], wcodes.numel(), e)
-        errs.append(((ln, "w"), e))
         kw = {}
         if n.bias:
             bcodes = self._buf((ln, "bcodes"), (n.cout,), T.int32)
-            fx.quantize(h, L["b_f32"], n.cout, self.fmt[(ln, "b")], bcodes, fx.I32)
-            e = self._buf((ln, "b", "err"), (4,), T.float64)
-            fx.layer_error(h, L["b_f32"], bcodes, fx.I32, self.fmt[(ln, "b")], n.cout, e)
-            errs.append(((ln, "b"), e))
+            self._param(ln, "b", bcodes, fx.I32, errs)
             kw.update(bias=bcodes, fl_bias=self.qp[(ln, "b")][1])
         if "a1" in L:
             kw.update(scale=L["a1"], fl_scale=L["fl"][("a1", None)][1], shift=L["a2"],
                       fl_shift=L["fl"][("a2", None)][1])
-        xin = self.qcodes[n.inp]
-        ep = fx.epilogue(n.cout, self.qp[(ln, "w")][1], self.qfmt[n.inp], relu=n.relu, **kw)
+        xin = qcodes[n.inp]
+        ep = fx.epilogue(n.cout, self.qp[(ln, "w")][1], qfmt[n.inp], relu=n.relu, **kw)
         acc = self._buf(("acc",), (L["M"], n.cout), T.int32)
         mm = self._buf((ln, "mm"), (2,), T.float64)
         if L["fc"]:
@@ -202,40 +218,48 @@ class ForwardOptimizer:
         errs.append(((ln, "a"), e))
         return codes, self.fmt[(ln, "a")], fx.C8
 
-    def _quant_node(self, n):
-        """Quantized max-pool / eltwise / avg-pool node on finalized inputs (the
-        eltwise and avg-pool FxP-QLayers search their own formats)."""
-        T, h, B = self.T, self.h, self.B
-        H, W, C = self.act[n.inp].shape[1:]
-        if n.op == "maxpool":
-            Ho, Wo = self.act[n.name].shape[1:3]
-            y = self._empty((B, Ho, Wo, C), T.int8)
-            fx.maxpool(h, self.qcodes[n.inp], fx.C8, B, H, W, C, n.k, n.stride, n.pad, y)
-            return y, self.qfmt[n.inp]
-        f = self._fmt()
-        if n.op == "add":
-            src = fx.src_add(self.qcodes[n.inp], fx.C8, self.qfmt[n.inp], self.qcodes[n.other], fx.C8,
-                             self.qfmt[n.other], n.relu)
-            m = self.qcodes[n.inp].numel()
-        else:  # global avg-pool with the quantized reciprocal (same as the runner)
-            r = np.repeat(np.array([np.float32(1.0) / np.float32(H * W)], np.float32), 4)
+    def _recip(self, n, HW):
+        """The avg-pool's reciprocal 1 / HW at its searched 16-bit format
+        (code, fractional length), once per node."""
+        key = (n.name, "recip")
+        if key not in self.held:
+            r = np.repeat(np.array([np.float32(1.0) / np.float32(HW)], np.float32), 4)
             rd, rf = self._t(r), self._fmt()
-            fx.fl_search(h, fx.src_f32(rd), 4, RECIP_WL, fx.SIGN_AUTO, FL_LO, FL_HI, rf)
-            rc = self._empty((4,), T.int32)
-            fx.quantize(h, rd, 4, rf, rc, fx.I32)
-            s = self._empty((B, C), T.int64)
-            fx.avgpool_global(h, self.qcodes[n.inp], fx.C8, self.qfmt[n.inp], B, H * W, C,
-                              int(rc.cpu().numpy()[0]), s)
-            ep = fx.epilogue(C, int(rf.cpu().numpy()[1]), self.qfmt[n.inp])
-            sc = self._empty((1,), T.int32)
+            fx.fl_search(self.h, fx.src_f32(rd), 4, RECIP_WL, fx.SIGN_AUTO, FL_LO, FL_HI, rf)
+            rc = self._empty((4,), self.T.int32)
+            fx.quantize(self.h, rd, 4, rf, rc, fx.I32)
+            self.held[key] = (int(rc.cpu().numpy()[0]), int(rf.cpu().numpy()[1]))
+        return self.held[key]
+
+    def _quant_node(self, n, src=None):
+        """Quantized max-pool / eltwise / avg-pool node on quantized inputs
+        (src as in _quant_layer; the eltwise and avg-pool FxP-QLayers search
+        their own formats).  Writes per-node buffers reused by every call."""
+        T, h, B = self.T, self.h, self.B
+        qcodes, qfmt = src if src is not None else (self.qcodes, self.qfmt)
+        H, W, C = self.act[n.inp].shape[1:]
+        y = self._buf((n.name, "codes"), tuple(self.act[n.name].shape), T.int8)
+        if n.op == "maxpool":
+            fx.maxpool(h, qcodes[n.inp], fx.C8, B, H, W, C, n.k, n.stride, n.pad, y)
+            return y, qfmt[n.inp]
+        f = self._buf((n.name, "fmt"), (4,), T.int32)
+        if n.op == "add":
+            s = fx.src_add(qcodes[n.inp], fx.C8, qfmt[n.inp], qcodes[n.other], fx.C8,
+                           qfmt[n.other], n.relu)
+            m = qcodes[n.inp].numel()
+            self.held[(n.name, "src")] = s
+        else:  # global avg-pool with the quantized reciprocal (same as the runner)
+            rc, rfl = self._recip(n, H * W)
+            acc = self._buf((n.name, "sum"), (B, C), T.int64)
+            fx.avgpool_global(h, qcodes[n.inp], fx.C8, qfmt[n.inp], B, H * W, C, rc, acc)
+            ep = fx.epilogue(C, rfl, qfmt[n.inp])
+            sc = self._buf((n.name, "scale"), (1,), T.int32)
             fx.epilogue_scale(h, ep, sc)
-            src = fx.src_int(s, fx.I64, sc)
-            self.keep += [ep]
-            m = s.numel()
-        self.keep.append(src)
-        fx.fl_search(h, src, m, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
-        y = self._empty(self.act[n.name].shape, T.int8)
-        fx.requant(h, src, m, f, y, fx.C8)
+            s = fx.src_int(acc, fx.I64, sc)
+            self.held[(n.name, "src")] = (ep, s)
+            m = acc.numel()
+        fx.fl_search(h, s, m, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+        fx.requant(h, s, m, f, y, fx.C8)
         return y, f
 
     def _dequant(self, name):
@@ -301,10 +325,20 @@ class ForwardOptimizer:
         return E + unclass + mispred, (E, unclass, mispred)
 
     # -- Algorithm 1 ------------------------------------------------------------------
-    def qparams_opt(self, ln, d):
+    def qparams_opt(self, ln, d, quantized=False):
+        """Algorithm 1 for data structure (ln, d) from its current format;
+        with quantized=True every candidate runs the whole quantized network
+        (evaluate_quant) and acc_best receives the chosen candidate's top-1
+        agreement."""
         key = (ln, d)
         fl0 = self.qp[key][1]
-        best, parts = self.evaluate(ln)
+
+        def ev():
+            if quantized:
+                return self.evaluate_quant(ln)
+            return self.evaluate(ln)[0], None
+
+        best, acc = ev()
         fl_best = fl0
         self.trace.append((ln, d, fl0, best))
         for i in (-1, +1):
@@ -314,27 +348,79 @@ class ForwardOptimizer:
                 if fl < FL_LO or fl > FL_HI:
                     break
                 self._set(key, fl)
-                cost, _ = self.evaluate(ln)
+                cost, a = ev()
                 self.trace.append((ln, d, fl, cost))
                 if cost < best:
-                    best, fl_best, j = cost, fl, j + 1
+                    best, fl_best, acc, j = cost, fl, a, j + 1
                 k += 1
         self._set(key, fl_best)
+        self.acc_best = acc
         return fl_best, best
+
+    def _after(self, ln):
+        start = 0 if ln == "input" else self.pos[ln] + 1
+        return [n for n in self.nodes[start:] if n.op != "input"]
 
     def finalize(self, ln):
         """Quantizes layer ln at its chosen formats into the prefix, then the
-        max-pool / eltwise / avg-pool nodes that follow it."""
+        max-pool / eltwise / avg-pool nodes that follow it (copies: the
+        evaluation buffers are reused)."""
         errs = []
         codes, cfmt, ctype = self._quant_layer(ln, errs)
-        self.qcodes[ln], self.qfmt[ln] = codes, cfmt
-        start = 0 if ln == "input" else self.pos[ln] + 1
-        for n in self.nodes[start:]:
-            if n.op in ("input",):
-                continue
+        self.qcodes[ln], self.qfmt[ln] = codes.clone(), cfmt
+        self.deq.pop(ln, None)
+        for n in self._after(ln):
             if n.op in ("conv", "fc"):
                 break
-            self.qcodes[n.name], self.qfmt[n.name] = self._quant_node(n)
+            y, f = self._quant_node(n)
+            self.qcodes[n.name], self.qfmt[n.name] = y.clone(), f.clone()
+            self.deq.pop(n.name, None)
+
+    def refinalize(self, ln):
+        """Re-quantizes the finalized network from layer ln on (after a format
+        of ln changed)."""
+        self.finalize(ln)
+        for n in self._after(ln):
+            if n.op in ("conv", "fc"):
+                self.finalize(n.name)
+
+    def _top1(self, logits):
+        """Share of samples whose integer scores have a unique maximum at the
+        teacher's top-1 class."""
+        last = [n for n in self.nodes if getattr(n, "last", False)][0]
+        q = logits.cpu().numpy().reshape(self.B, -1)
+        t = self.act[last.name].cpu().numpy().reshape(self.B, -1)
+        unique = (q == q.max(1, keepdims=True)).sum(1) == 1
+        return float(np.mean(unique & (q.argmax(1) == t.argmax(1))))
+
+    def evaluate_quant(self, ln):
+        """Cost F of the current formats with the whole network quantized:
+        the finalized prefix, layer ln at its current formats and every later
+        layer at its formats (the error sums of every data structure from ln
+        on, parameters included), and the top-1 agreement."""
+        T, h, B = self.T, self.h, self.B
+        self.evals += 1
+        errs = []
+        cc, cf = dict(self.qcodes), dict(self.qfmt)
+        codes, cfmt, ctype = self._quant_layer(ln, errs, (cc, cf))
+        cc[ln], cf[ln] = codes, cfmt
+        for n in self._after(ln):
+            if n.op in ("conv", "fc"):
+                codes, cfmt, ctype = self._quant_layer(n.name, errs, (cc, cf))
+            else:
+                codes, cfmt = self._quant_node(n, (cc, cf))
+            cc[n.name], cf[n.name] = codes, cfmt
+        last = [n for n in self.nodes if getattr(n, "last", False)][0]
+        logits = cc[last.name]
+        fx.prediction_ties(h, logits, fx.I32, B, last.cout, self.ties)
+        T.cuda.synchronize(self.sw.dev)
+        E = 0.0
+        for key, e in errs:
+            if key in self.pi and self.stat[key][2] > 0:
+                E += self.pi[key] * float(e[0].item()) / self.stat[key][2]
+        t = self.ties.cpu().numpy()
+        cost = E + float(t[0]) / B + float(t[1]) / (B * last.cout)
+        return cost, self._top1(logits)
 
     def run(self):
         """The forward optimizer: every data structure in order; returns the
@@ -354,11 +440,7 @@ class ForwardOptimizer:
         """Share of samples whose quantized top-1 (unique maximum) is the
         teacher's top-1."""
         last = [n for n in self.nodes if getattr(n, "last", False)][0]
-        q = self.qcodes[last.name].cpu().numpy().reshape(self.B, -1)
-        t = self.act[last.name].cpu().numpy().reshape(self.B, -1)
-        qa = q.argmax(1)
-        unique = (q == q.max(1, keepdims=True)).sum(1) == 1
-        return float(np.mean(unique & (qa == t.argmax(1))))
+        return self._top1(self.qcodes[last.name])
 
     def close(self):
         self.sw.close()
