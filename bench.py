@@ -134,12 +134,12 @@ def qparams_figures(dev, batch=32, image=224):
     return out
 
 
-def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=8):
+def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     """Bit-precision level reduction (Algorithm 2) over ResNet-18 on a
     calibration batch: the forward optimizer's 8-bit design first (untimed
-    set-up), then Algorithm 2 capped at max_changes applied reductions,
-    timed; the memory model before and after; the oracle's reduction on a
-    bounded sample beside it."""
+    set-up), then Algorithm 2 to convergence (or max_changes applied
+    reductions), timed; the memory model before and after; the oracle's
+    reduction on a bounded sample beside it."""
     import torch
     from paper_2203_12091_amd import qparams, reduction
     fo = qparams.ForwardOptimizer("resnet18", batch=batch, image=image, device=str(dev), w_wl=8)
@@ -157,7 +157,8 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=8):
     ev = fo.evals - e0
     out = {"metric": "bit-precision reduction (Algorithm 2) seconds, ResNet-18", "batch": batch,
            "image": image, "threshold": thld, "max_changes": max_changes,
-           "changes": [f"{ln}.{d}: -{th} -> {wl} bits" for ln, d, th, wl, _, _ in r.changes],
+           "changes": len(r.changes),
+           "word_lengths": {f"{ln}.{d}": v[0] for (ln, d), v in r.formats().items()},
            "trials": len(r.trials), "evaluations": ev, "seconds": round(t, 3),
            "evaluations_per_s": round(ev / t, 2), "top1_agreement_before": round(acc0, 4),
            "top1_agreement_after": round(r.accuracy(), 4),
