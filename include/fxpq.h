@@ -319,6 +319,41 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
                         double* d_minmax);
 
 /*
+ * C-Block contraction over codes of up to 32 bits (Sec. "Integer-Only
+ * Inference"; the first and last layers start at 32-bit activations and
+ * weights, Sec. "Initial Design Generation"), followed by its epilogue:
+ *     v[m][k] = epilogue(sum_{r,s,c} x[..][c] * w[k][r][s][c])     (exact)
+ * with the shapes, zero padding and layout of fxpq_qconv (NHWC input, KRSC
+ * weights; c % 16 == 0, or c == 4 with each weight row padded with zeros to
+ * a multiple of 64; an FC layer is the 1x1 convolution of a 1x1 image).
+ * x (device int32[n*h*w*c]) holds codes of the format (wl_x, sign_x),
+ * w (device int32[k * row]) codes of (wl_w, sign_w); a signed 1-bit format
+ * holds its decoded codes (-1 / +1).  ep (required) is the epilogue, with
+ * ep->d_fmt_in the input's format on the device (its fl sets the scale).
+ * The result v (device int64[M * k], M = n * Ho * Wo, channels innermost) is
+ * the exact C-Block value times 2^s, s written to d_scale (device int32):
+ * FXPQ_SRC_INT with dtype FXPQ_I64 and this d_scale describes the values
+ * for fxpq_fl_search / fxpq_requant / fxpq_qlayer.
+ * Computed on the int8 matrix cores: x splits into ceil(wl_x / 8) base-256
+ * planes (unsigned low bytes, the top byte signed for signed formats), w into
+ * balanced base-256 digits in [-128, 127] (up to 5 for 32-bit weights), one
+ * int8 contraction per plane pair, and an exact 128-bit combination.
+ * workspace (device, 256-byte aligned, caller-owned) must hold at least the
+ * bytes fxpq_qconv_wide_workspace reports for the same arguments; its
+ * contents are unspecified afterwards.  Codes outside their format's range
+ * raise FXPQ_FLAG_CODE; values of magnitude 2^62 or more raise
+ * FXPQ_FLAG_RANGE and are written as 0.  Requirements: 1 <= wl <= 32 for
+ * signed formats, <= 31 for unsigned ones (int32 storage), and every plane
+ * contraction within the limits of fxpq_qconv (else its error).
+ */
+fxpq_status fxpq_qconv_wide_workspace(const fxpq_conv_desc* d, int32_t wl_x, int32_t sign_x,
+                                      int32_t wl_w, int32_t sign_w, int64_t* bytes);
+fxpq_status fxpq_qconv_wide(fxpq_handle h, const fxpq_conv_desc* d, const int32_t* x,
+                            int32_t wl_x, int32_t sign_x, const int32_t* w, int32_t wl_w,
+                            int32_t sign_w, const fxpq_epilogue* ep, int64_t* v,
+                            int32_t* d_scale, void* workspace, int64_t workspace_bytes);
+
+/*
  * Tile family of fxpq_qconv (results are the same integers either way):
  * FXPQ_TILING_AUTO (default) and FXPQ_TILING_GEMM use implicit-GEMM tiles;
  * FXPQ_TILING_HALO uses halo tiles where the shape allows them (3x3 filters,

@@ -6,7 +6,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfxpq.so")
-SOURCES = ["fxpq_api.hip", "k_stream.hip", "k_flsearch.hip", "k_conv.hip", "k_teacher.hip"]
+SOURCES = ["fxpq_api.hip", "k_stream.hip", "k_flsearch.hip", "k_conv.hip", "k_teacher.hip",
+           "k_wide.hip"]
 
 
 def build(verbose: bool = False) -> str:

@@ -223,6 +223,14 @@ hipError_t launch_logit_ties(const Ctx& c, const void* scores, int dtype, int ro
 hipError_t launch_preprocess(const Ctx& c, const SrcDev& s, const double* d_minmax, int wl,
                              int strategy, int rule, int fl_lo, int fl_hi, fxpq_fmt* out);
 hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out);
+// Wide C-Blocks (k_wide.hip): digit planes of int32 codes, and the exact
+// combination of the plane contractions with the epilogue.
+hipError_t launch_wide_split_x(const Ctx& c, const int32_t* x, int64_t n, int np, int sign,
+                               int64_t plane_stride, int8_t* planes);
+hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np,
+                               int64_t plane_stride, int8_t* planes);
+hipError_t launch_wide_combine(const Ctx& c, const int32_t* acc, int64_t mk, int np_x, int np_w,
+                               const SrcDev& ep, int64_t* v, int32_t* d_scale);
 hipError_t launch_maxpool(const Ctx& c, const int8_t* x, int n, int h, int w, int ch, int ks,
                           int stride, int pad, int8_t* y);
 hipError_t launch_avgpool(const Ctx& c, const int8_t* x, int dtype, const fxpq_fmt* fmt, int n,

@@ -429,6 +429,110 @@ fxpq_status fxpq_qconv(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fx
   return conv_common(h, d, x, x_type, w, w_colsum, ep, acc, d_minmax);
 }
 
+}  // extern "C"
+
+namespace {
+
+// Plane counts and workspace layout of a wide C-Block.
+struct WideLayout {
+  int np_x = 0, np_w = 0;
+  int64_t n_in = 0, wrow = 0, M = 0, mk = 0;
+  int64_t xs = 0, ws = 0;                  // bytes per input / weight plane (256-aligned)
+  int64_t off_w = 0, off_cs = 0, off_acc = 0, total = 0;
+};
+
+int64_t align256(int64_t b) { return (b + 255) / 256 * 256; }
+
+// Balanced base-256 digits needed for the code range of (wl, sign).
+int wide_weight_planes(int wl, int sign) {
+  const int64_t qmin = sign ? -((int64_t)1 << (wl - 1)) : 0;
+  const int64_t qmax = sign ? ((int64_t)1 << (wl - 1)) - 1 : ((int64_t)1 << wl) - 1;
+  for (int n = 1; n <= 5; ++n) {
+    const int64_t m = (((int64_t)1 << (8 * n)) - 1) / 255;  // 1 + 256 + ... + 256^(n-1)
+    if (qmin >= -128 * m && qmax <= 127 * m) return n;
+  }
+  return 5;
+}
+
+bool wide_layout(const fxpq_conv_desc* d, int wl_x, int sign_x, int wl_w, int sign_w,
+                 WideLayout* L) {
+  if (!d || wl_x < 1 || wl_x > 32 || wl_w < 1 || wl_w > 32) return false;
+  if ((sign_x != 0 && sign_x != 1) || (sign_w != 0 && sign_w != 1)) return false;
+  if ((!sign_x && wl_x > 31) || (!sign_w && wl_w > 31)) return false;  // int32 storage
+  if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
+      d->stride < 1 || d->pad < 0)
+    return false;
+  const int64_t ho = (d->h + 2 * (int64_t)d->pad - d->r) / d->stride + 1;
+  const int64_t wo = (d->w + 2 * (int64_t)d->pad - d->s) / d->stride + 1;
+  if (ho < 1 || wo < 1) return false;
+  L->np_x = (wl_x + 7) / 8;
+  L->np_w = wide_weight_planes(wl_w, sign_w);
+  L->n_in = (int64_t)d->n * d->h * d->w * d->c;
+  const int64_t depth = (int64_t)d->r * d->s * d->c;
+  L->wrow = d->c == 4 ? (depth + 63) / 64 * 64 : depth;
+  L->M = (int64_t)d->n * ho * wo;
+  L->mk = L->M * d->k;
+  L->xs = align256(L->n_in);
+  L->ws = align256((int64_t)d->k * L->wrow);
+  L->off_w = L->np_x * L->xs;
+  L->off_cs = L->off_w + L->np_w * L->ws;
+  L->off_acc = L->off_cs + align256((int64_t)L->np_w * d->k * 4);
+  L->total = L->off_acc + (int64_t)L->np_x * L->np_w * L->mk * 4;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+fxpq_status fxpq_qconv_wide_workspace(const fxpq_conv_desc* d, int32_t wl_x, int32_t sign_x,
+                                      int32_t wl_w, int32_t sign_w, int64_t* bytes) {
+  WideLayout L;
+  if (!bytes || !wide_layout(d, wl_x, sign_x, wl_w, sign_w, &L)) return FXPQ_ERR_INVALID_ARG;
+  *bytes = L.total;
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_qconv_wide(fxpq_handle h, const fxpq_conv_desc* d, const int32_t* x,
+                            int32_t wl_x, int32_t sign_x, const int32_t* w, int32_t wl_w,
+                            int32_t sign_w, const fxpq_epilogue* ep, int64_t* v,
+                            int32_t* d_scale, void* workspace, int64_t workspace_bytes) {
+  WideLayout L;
+  if (!h || !x || !w || !ep || !v || !d_scale || !workspace) return FXPQ_ERR_INVALID_ARG;
+  if (!wide_layout(d, wl_x, sign_x, wl_w, sign_w, &L)) return FXPQ_ERR_INVALID_ARG;
+  if (workspace_bytes < L.total || !aligned(workspace, 256) || !aligned(x, 4) ||
+      !aligned(w, 4) || !aligned(v, 8) || !aligned(d_scale, 4))
+    return FXPQ_ERR_INVALID_ARG;
+  if (ep->channels != d->k || !ep->d_fmt_in) return FXPQ_ERR_INVALID_ARG;
+  char* ws = static_cast<char*>(workspace);
+  int8_t* px = reinterpret_cast<int8_t*>(ws);
+  int8_t* pw = reinterpret_cast<int8_t*>(ws + L.off_w);
+  int32_t* cs = reinterpret_cast<int32_t*>(ws + L.off_cs);
+  int32_t* acc = reinterpret_cast<int32_t*>(ws + L.off_acc);
+  // every plane contraction must be one fxpq_qconv accepts
+  for (int p = 0; p < L.np_x; ++p) {
+    const fxpq_dtype t = (p < L.np_x - 1 || !sign_x) ? FXPQ_U8OFF : FXPQ_I8;
+    fxpq_status st = conv_check(d, px + p * L.xs, t, pw, cs, nullptr, acc);
+    if (st) return st;
+  }
+  SrcDev e;
+  epi_to_dev(ep, &e);
+  DeviceGuard g(h->device);
+  const Ctx c = ctx(h);
+  hipError_t err = launch_wide_split_x(c, x, L.n_in, L.np_x, sign_x, L.xs, px);
+  if (err == hipSuccess) err = launch_wide_split_w(c, w, (int64_t)d->k * L.wrow, L.np_w, L.ws, pw);
+  for (int q = 0; q < L.np_w && err == hipSuccess; ++q)
+    err = launch_colsum(c, pw + q * L.ws, d->k, L.wrow, cs + (int64_t)q * d->k);
+  for (int p = 0; p < L.np_x && err == hipSuccess; ++p) {
+    const int t = (p < L.np_x - 1 || !sign_x) ? FXPQ_U8OFF : FXPQ_I8;
+    for (int q = 0; q < L.np_w && err == hipSuccess; ++q)
+      err = launch_conv(c, *d, px + p * L.xs, t, pw + q * L.ws, cs + (int64_t)q * d->k, nullptr,
+                        acc + (int64_t)(p * L.np_w + q) * L.mk, nullptr);
+  }
+  if (err == hipSuccess) err = launch_wide_combine(c, acc, L.mk, L.np_x, L.np_w, e, v, d_scale);
+  return hip_status(err);
+}
+
 fxpq_status fxpq_qgemm(fxpq_handle h, int64_t M, int64_t N, int64_t K, const void* A,
                        fxpq_dtype a_type, const int8_t* B, const int32_t* b_colsum,
                        const fxpq_epilogue* ep, int32_t* C, double* d_minmax) {

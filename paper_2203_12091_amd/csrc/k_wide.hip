@@ -1,0 +1,142 @@
+// C-Blocks over codes wider than 8 bits (Sec. "Integer-Only Inference": the
+// first and last layers start at 32-bit activations and weights, Sec.
+// "Initial Design Generation"), on the int8 matrix cores.
+//
+// A code of up to 32 bits is written in base 256.  Input codes x split into
+// np_x byte planes: planes below the top hold the unsigned bytes (stored as
+// byte - 128, the U8OFF storage the int8 contraction already corrects with the
+// weight column sums), the top plane holds the rest (signed storage for
+// signed formats).  Weight codes split into balanced digits in [-128, 127]
+// (int8 as they are).  Then
+//     sum_k x_k w_k = sum_{p,q} 256^(p+q) sum_k xp_k wq_k,
+// each inner sum an ordinary int8 contraction with exact int32 accumulation;
+// the combine kernel adds them with exact shifts in 128-bit integers and
+// applies the C-Block epilogue in integers, writing int64 values at the
+// epilogue's scale (an FXPQ_SRC_INT source for the FxP-QLayer that follows).
+#include "common.hpp"
+
+namespace fxpq {
+
+namespace {
+
+__device__ inline void flag(unsigned* flags, unsigned bit) { atomicOr(flags, bit); }
+
+__global__ __launch_bounds__(kThreads) void k_split_x(const int32_t* __restrict__ x, int64_t n,
+                                                      int np, int sign, int64_t ps,
+                                                      int8_t* __restrict__ planes,
+                                                      unsigned* flags) {
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads) {
+    const int32_t v = x[i];
+    for (int p = 0; p < np - 1; ++p) planes[p * ps + i] = (int8_t)(((v >> (8 * p)) & 255) - 128);
+    const int32_t top = v >> (8 * (np - 1));
+    if (sign) {
+      bad |= top < -128 || top > 127;
+      planes[(np - 1) * ps + i] = (int8_t)top;
+    } else {
+      bad |= v < 0 || top > 255;
+      planes[(np - 1) * ps + i] = (int8_t)(top - 128);
+    }
+  }
+  if (bad) flag(flags, FXPQ_FLAG_CODE);
+}
+
+__global__ __launch_bounds__(kThreads) void k_split_w(const int32_t* __restrict__ w, int64_t n,
+                                                      int np, int64_t ps,
+                                                      int8_t* __restrict__ planes,
+                                                      unsigned* flags) {
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads) {
+    int64_t r = w[i];
+    for (int p = 0; p < np; ++p) {
+      const int d = (int)((r + 128) & 255) - 128;
+      planes[p * ps + i] = (int8_t)d;
+      r = (r - d) >> 8;
+    }
+    bad |= r != 0;
+  }
+  if (bad) flag(flags, FXPQ_FLAG_CODE);
+}
+
+// Bits of |v| (0 for v == 0).
+__device__ inline int bits128(__int128 v) {
+  unsigned __int128 m = v < 0 ? (unsigned __int128)(-v) : (unsigned __int128)v;
+  unsigned long long hi = (unsigned long long)(m >> 64), lo = (unsigned long long)m;
+  return hi ? 128 - __builtin_clzll(hi) : (lo ? 64 - __builtin_clzll(lo) : 0);
+}
+
+// v * 2^sh, with `bad` set where the result would not stay below 2^120.
+__device__ inline __int128 shl_checked(__int128 v, int sh, bool& bad) {
+  if (v == 0) return 0;
+  if (sh > 119 || bits128(v) + sh > 120) {
+    bad = true;
+    return 0;
+  }
+  return v * ((__int128)1 << sh);
+}
+
+__global__ __launch_bounds__(kThreads) void k_wide_combine(const int32_t* __restrict__ acc,
+                                                           int64_t mk, int np_x, int np_w,
+                                                           SrcDev ep, int64_t* __restrict__ v,
+                                                           int32_t* d_scale, unsigned* flags) {
+  const EpiU u = epi_uniform(ep);
+  if (blockIdx.x == 0 && threadIdx.x == 0) *d_scale = u.s_out;
+  const int K = ep.channels;
+  bool bad = false;
+  for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < mk;
+       i += (int64_t)gridDim.x * kThreads) {
+    __int128 a = 0;
+    for (int p = 0; p < np_x; ++p)
+      for (int q = 0; q < np_w; ++q)
+        a += (__int128)acc[(int64_t)(p * np_w + q) * mk + i] * ((__int128)1 << (8 * (p + q)));
+    const EpiRaw r = epi_channel_load(ep, (int)(i % K));
+    bool b = false;
+    __int128 t = shl_checked(a, u.sh_acc, b);
+    if (ep.bias) t += shl_checked((__int128)r.b, u.sh_bias, b);
+    if (ep.scale) {
+      if (bits128(t) > 90) b = true;
+      else t *= (__int128)r.sc;
+    }
+    t = shl_checked(t, u.sh_mid, b);
+    if (ep.shift) t += shl_checked((__int128)r.sh, u.sh_shift, b);
+    if (ep.ep_relu && t < 0) t = 0;
+    if (b || bits128(t) > 62) {
+      bad = true;
+      t = 0;
+    }
+    v[i] = (int64_t)t;
+  }
+  if (bad) flag(flags, FXPQ_FLAG_RANGE);
+}
+
+int stream_blocks(int64_t n) {
+  int64_t b = (n + kThreads - 1) / kThreads;
+  return (int)(b < 4096 ? (b < 1 ? 1 : b) : 4096);
+}
+
+}  // namespace
+
+hipError_t launch_wide_split_x(const Ctx& c, const int32_t* x, int64_t n, int np, int sign,
+                               int64_t plane_stride, int8_t* planes) {
+  k_split_x<<<stream_blocks(n), kThreads, 0, c.stream>>>(x, n, np, sign, plane_stride, planes,
+                                                         c.sc.flags);
+  return hipGetLastError();
+}
+
+hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np,
+                               int64_t plane_stride, int8_t* planes) {
+  k_split_w<<<stream_blocks(n), kThreads, 0, c.stream>>>(w, n, np, plane_stride, planes,
+                                                         c.sc.flags);
+  return hipGetLastError();
+}
+
+hipError_t launch_wide_combine(const Ctx& c, const int32_t* acc, int64_t mk, int np_x, int np_w,
+                               const SrcDev& ep, int64_t* v, int32_t* d_scale) {
+  k_wide_combine<<<stream_blocks(mk), kThreads, 0, c.stream>>>(acc, mk, np_x, np_w, ep, v,
+                                                               d_scale, c.sc.flags);
+  return hipGetLastError();
+}
+
+}  // namespace fxpq

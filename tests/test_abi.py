@@ -69,3 +69,32 @@ def test_missing_library_fails_loudly(fx, monkeypatch, tmp_path):
     monkeypatch.setattr(fx, "_lib", None)
     with pytest.raises(FileNotFoundError):
         fx.lib()
+
+
+def test_wide_workspace_layout_on_host(fx):
+    """Plane counts and workspace bytes of fxpq_qconv_wide (host arithmetic):
+    ceil(wl / 8) input planes; balanced base-256 digits for the weights'
+    code range (16-bit signed needs 3: 32767 > 127 * 257); 256-byte aligned
+    regions for the input planes, weight planes, column sums and one int32
+    accumulator tensor per plane pair."""
+    d = fx.ConvDesc(2, 8, 8, 16, 32, 3, 3, 1, 1)
+
+    def want(px, pw):
+        a = lambda b: (b + 255) // 256 * 256
+        n_in, wrow, mk = 2 * 8 * 8 * 16, 9 * 16, 2 * 8 * 8 * 32
+        return px * a(n_in) + pw * a(32 * wrow) + a(pw * 32 * 4) + px * pw * mk * 4
+
+    for (wx, sx, ww, sw), (px, pw) in [((16, 1, 16, 1), (2, 3)), ((16, 1, 15, 1), (2, 2)),
+                                       ((8, 1, 8, 1), (1, 1)), ((8, 0, 8, 0), (1, 2)),
+                                       ((32, 1, 32, 1), (4, 5)), ((31, 0, 24, 1), (4, 4)),
+                                       ((1, 1, 1, 1), (1, 1)), ((9, 1, 17, 1), (2, 3))]:
+        assert fx.qconv_wide_workspace(d, wx, sx, ww, sw) == want(px, pw), (wx, sx, ww, sw)
+    # the padded RGB layout rounds each weight row up to 64 bytes
+    d4 = fx.ConvDesc(1, 10, 10, 4, 64, 7, 7, 2, 3)
+    ho = (10 + 6 - 7) // 2 + 1
+    a = lambda b: (b + 255) // 256 * 256
+    assert fx.qconv_wide_workspace(d4, 16, 1, 8, 1) == (
+        2 * a(400) + a(64 * 256) + a(64 * 4) + 2 * ho * ho * 64 * 4)
+    for bad in [(32, 0, 8, 1), (8, 1, 32, 0), (0, 1, 8, 1), (8, 2, 8, 1), (33, 1, 8, 1)]:
+        with pytest.raises(fx.FxpqError):
+            fx.qconv_wide_workspace(d, *bad)
