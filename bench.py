@@ -43,7 +43,8 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
-    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams", "reduction"],
+    ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams", "reduction",
+                                       "wide"],
                     default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
                          "copy: one plain 1 GiB device copy (counter calibration); "
@@ -147,6 +148,7 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     torch.cuda.synchronize(dev)
     before = reduction.memory_model(fo)
     acc0 = fo.top1_agreement()
+    ovf0 = fo.mac_overflow(16)
     r = reduction.QReduction(fo, thld, max_changes=max_changes)
     e0 = fo.evals
     t0 = time.perf_counter()
@@ -154,6 +156,7 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     torch.cuda.synchronize(dev)
     t = time.perf_counter() - t0
     after = reduction.memory_model(fo)
+    ovf1 = fo.mac_overflow(16)
     ev = fo.evals - e0
     out = {"metric": "bit-precision reduction (Algorithm 2) seconds, ResNet-18", "batch": batch,
            "image": image, "threshold": thld, "max_changes": max_changes,
@@ -163,7 +166,9 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
            "evaluations_per_s": round(ev / t, 2), "top1_agreement_before": round(acc0, 4),
            "top1_agreement_after": round(r.accuracy(), 4),
            "memory_mb_before": {k: round(v, 4) for k, v in before.items()},
-           "memory_mb_after": {k: round(v, 4) for k, v in after.items()}}
+           "memory_mb_after": {k: round(v, 4) for k, v in after.items()},
+           "mac16_overflow_before": [sum(c for c, _ in ovf0.values()), sum(m for _, m in ovf0.values())],
+           "mac16_overflow_after": [sum(c for c, _ in ovf1.values()), sum(m for _, m in ovf1.values())]}
     fo.close()
     import oracle.qparams as oq
     import oracle.reduction as orr
@@ -177,6 +182,72 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     out["cpu_baseline"] = {"seconds": round(t, 2), "evaluations": len(ref.trace) - n0,
                            "changes": len(rr.changes), "kind": "oracle",
                            "sample": "ResNet-18, 1 image 16x16, 2 changes (exact CPU oracle)"}
+    return out
+
+
+def wide_figures(dev, batch=256):
+    """Wide C-Blocks (fxpq_qconv_wide) at the shapes of ResNet-50's first and
+    last layers with 16-bit activations and weights: the first conv (7x7/2
+    over 224x224 RGB, Scale + ReLU epilogue) and the FC (2048 -> 1000, bias),
+    each timed over 5 calls after one untimed call; int8 operations of the
+    plane contractions and the combine's algorithmic bytes (4 B per plane-pair
+    accumulator read, 8 B per value written)."""
+    import torch
+    from paper_2203_12091_amd import fxpq as fx
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+    gen = torch.Generator(device=dev).manual_seed(11)
+
+    def codes(shape, wl):
+        return torch.randint(-(1 << (wl - 1)), 1 << (wl - 1), shape, generator=gen, device=dev,
+                             dtype=torch.int32)
+
+    out = {}
+    shapes = {"resnet50_conv1_b256": (fx.conv_desc(batch, 224, 224, 4, 64, 7, 7, 2, 3), True),
+              "resnet50_fc_b256": (fx.conv_desc(batch, 1, 1, 2048, 1000, 1, 1, 1, 0), False)}
+    for name, (d, first) in shapes.items():
+        depth = d.r * d.s * d.c
+        wrow = (depth + 63) // 64 * 64 if d.c == 4 else depth
+        x = codes((d.n, d.h, d.w, d.c), 16)
+        if d.c == 4:
+            x[..., 3] = 0
+        w = codes((d.k, wrow), 16)
+        if d.c == 4:
+            w.view(d.k, -1)[:, depth:] = 0
+        fin = torch.tensor([16, 12, 1, 0], dtype=torch.int32, device=dev)
+        if first:
+            a1 = codes((d.k,), 16)
+            a2 = codes((d.k,), 32)
+            ep = fx.epilogue(d.k, 14, fin, relu=True, scale=a1, fl_scale=14, shift=a2, fl_shift=20)
+        else:
+            b = codes((d.k,), 32)
+            ep = fx.epilogue(d.k, 14, fin, bias=b, fl_bias=20)
+        nb = fx.qconv_wide_workspace(d, 16, 1, 16, 1)
+        ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+        Ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
+        Wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
+        mk = d.n * Ho * Wo * d.k
+        v = torch.empty(mk, dtype=torch.int64, device=dev)
+        sc = torch.empty(1, dtype=torch.int32, device=dev)
+        call = lambda: fx.qconv_wide(h, d, x, 16, 1, w, 16, 1, ep, v, sc, ws, nb)
+        call()
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        reps = 5
+        e0.record()
+        for _ in range(reps):
+            call()
+        e1.record()
+        torch.cuda.synchronize(dev)
+        ms = e0.elapsed_time(e1) / reps
+        pairs = 2 * 3  # 16-bit inputs: 2 byte planes; 16-bit signed weights: 3 balanced digits
+        ops = pairs * 2.0 * (mk // d.k) * d.k * (wrow if d.c == 4 else depth)
+        out[name] = {"ms": round(ms, 4), "plane_pairs": pairs, "workspace_mb": round(nb / 2 ** 20, 1),
+                     "int8_tops_per_call": round(ops / (ms * 1e-3) / 1e12, 1),
+                     "outputs": mk, "combine_bytes": (4 * pairs + 8) * mk}
+        assert fx.sync_status(h) == 0
+        del ws
+    h.close()
     return out
 
 
@@ -265,6 +336,9 @@ def main():
         return
     if args.mode == "reduction":
         print(json.dumps(reduction_figures(dev)), flush=True)
+        return
+    if args.mode == "wide":
+        print(json.dumps(wide_figures(dev)), flush=True)
         return
 
     net = nets.CalibNet("resnet50", batch=BATCH, image=IMAGE, device="cuda:0")

@@ -354,6 +354,18 @@ fxpq_status fxpq_qconv_wide(fxpq_handle h, const fxpq_conv_desc* d, const int32_
                             int32_t* d_scale, void* workspace, int64_t workspace_bytes);
 
 /*
+ * Accumulator overflow accounting (Sec. "Integer-Only Inference": the MAC
+ * results of the layers between the first and the last are kept in 16 bits).
+ * Adds to *d_count (device int64, caller-initialized) the number of int32
+ * accumulators acc[0..n) (device) outside the two's-complement range of
+ * `bits` bits, [-2^(bits-1), 2^(bits-1) - 1]: the outputs a MAC of that
+ * width cannot hold (with wrap-around arithmetic, partial sums may leave the
+ * range harmlessly as long as the result is inside).  2 <= bits <= 32.
+ */
+fxpq_status fxpq_acc_overflow(fxpq_handle h, const int32_t* acc, int64_t n, int32_t bits,
+                              int64_t* d_count);
+
+/*
  * Tile family of fxpq_qconv (results are the same integers either way):
  * FXPQ_TILING_AUTO (default) and FXPQ_TILING_GEMM use implicit-GEMM tiles;
  * FXPQ_TILING_HALO uses halo tiles where the shape allows them (3x3 filters,

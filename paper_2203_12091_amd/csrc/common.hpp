@@ -231,6 +231,8 @@ hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np
                                int64_t plane_stride, int8_t* planes);
 hipError_t launch_wide_combine(const Ctx& c, const int32_t* acc, int64_t mk, int np_x, int np_w,
                                const SrcDev& ep, int64_t* v, int32_t* d_scale);
+hipError_t launch_acc_overflow(const Ctx& c, const int32_t* acc, int64_t n, int bits,
+                               int64_t* count);
 hipError_t launch_maxpool(const Ctx& c, const int8_t* x, int n, int h, int w, int ch, int ks,
                           int stride, int pad, int8_t* y);
 hipError_t launch_avgpool(const Ctx& c, const int8_t* x, int dtype, const fxpq_fmt* fmt, int n,

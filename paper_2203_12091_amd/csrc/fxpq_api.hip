@@ -533,6 +533,15 @@ fxpq_status fxpq_qconv_wide(fxpq_handle h, const fxpq_conv_desc* d, const int32_
   return hip_status(err);
 }
 
+fxpq_status fxpq_acc_overflow(fxpq_handle h, const int32_t* acc, int64_t n, int32_t bits,
+                              int64_t* d_count) {
+  if (!h || !acc || !d_count || n < 0 || bits < 2 || bits > 32) return FXPQ_ERR_INVALID_ARG;
+  if (!aligned(acc, 4) || !aligned(d_count, 8)) return FXPQ_ERR_INVALID_ARG;
+  if (n == 0) return FXPQ_OK;
+  DeviceGuard g(h->device);
+  return hip_status(launch_acc_overflow(ctx(h), acc, n, bits, d_count));
+}
+
 fxpq_status fxpq_qgemm(fxpq_handle h, int64_t M, int64_t N, int64_t K, const void* A,
                        fxpq_dtype a_type, const int8_t* B, const int32_t* b_colsum,
                        const fxpq_epilogue* ep, int32_t* C, double* d_minmax) {

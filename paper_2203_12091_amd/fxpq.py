@@ -21,7 +21,7 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
-    "fxpq_qconv_wide_workspace", "fxpq_qconv_wide",
+    "fxpq_qconv_wide_workspace", "fxpq_qconv_wide", "fxpq_acc_overflow",
     "fxpq_cblock", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_dequantize", "fxpq_prediction_ties", "fxpq_timer_start",
     "fxpq_timer_read",
@@ -90,6 +90,7 @@ def lib():
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
             "fxpq_qconv_wide_workspace": [p, i32, i32, i32, i32, p],
             "fxpq_qconv_wide": [p, p, p, i32, i32, p, i32, i32, p, p, p, p, i64],
+            "fxpq_acc_overflow": [p, p, i64, i32, p],
             "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
             "fxpq_weight_colsum": [p, p, i64, i64, p],
             "fxpq_set_conv_tiling": [p, i32],
@@ -226,6 +227,10 @@ def qconv_wide_workspace(desc, wl_x, sign_x, wl_w, sign_w):
 def qconv_wide(h, desc, x, wl_x, sign_x, w, wl_w, sign_w, ep, v, d_scale, workspace, ws_bytes):
     _call("fxpq_qconv_wide", h.value, C.byref(desc), ptr(x), wl_x, sign_x, ptr(w), wl_w, sign_w,
           C.byref(ep), ptr(v), ptr(d_scale), ptr(workspace), ws_bytes)
+
+
+def acc_overflow(h, acc, n, bits, d_count):
+    _call("fxpq_acc_overflow", h.value, ptr(acc), n, bits, ptr(d_count))
 
 
 def qgemm(h, M, N, K, A, a_type, B, b_colsum, ep, Cout, d_minmax=None):

@@ -436,6 +436,23 @@ class ForwardOptimizer:
             self.finalize(ln)
         return {k: tuple(v) for k, v in self.qp.items() if k in dict.fromkeys(self.order)}
 
+    def mac_overflow(self, bits=16):
+        """Per conv / FC layer between the first and the last: (accumulators
+        outside `bits`-bit two's complement, accumulators) of the finalized
+        network (Sec. "Integer-Only Inference" keeps those MAC results in 16
+        bits)."""
+        convs = [n for n in self.nodes if n.op in ("conv", "fc")]
+        cnt = self._buf(("ovf",), (1,), self.T.int64)
+        out = {}
+        for n in convs[1:-1]:
+            self._quant_layer(n.name, [])
+            acc = self.bufs[("acc",)]
+            m = self.L[n.name]["M"] * n.cout
+            cnt.zero_()
+            fx.acc_overflow(self.h, acc, m, bits, cnt)
+            out[n.name] = (int(cnt.item()), m)
+        return out
+
     def top1_agreement(self):
         """Share of samples whose quantized top-1 (unique maximum) is the
         teacher's top-1."""

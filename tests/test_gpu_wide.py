@@ -152,3 +152,41 @@ def test_wide_cblock_out_of_range_raises_flag(fx, h):
     assert fx.sync_status(h) & fx.FLAG_RANGE
     assert np.all(host(v) == 0)
     assert fx.sync_status(h) == 0
+    # 16-bit codes (sums combined in int64): the bias alignment shifts the
+    # accumulators past 2^62
+    x16 = np.full((N, 1, 1, C), 2 ** 15 - 1, np.int32)
+    w16 = np.full((K, C), 2 ** 15 - 1, np.int32)
+    b = dev(np.ones(K, np.int32))
+    ep = fx.epilogue(K, 0, fmt_dev(16, 0, 1), bias=b, fl_bias=40)
+    nb = fx.qconv_wide_workspace(desc, 16, 1, 16, 1)
+    ws = empty((nb,), torch.uint8)
+    note("qconv_wide range flag int64")
+    fx.qconv_wide(h, desc, dev(x16), 16, 1, dev(w16), 16, 1, ep, v, sc, ws, nb)
+    assert fx.sync_status(h) & fx.FLAG_RANGE
+    assert np.all(host(v) == 0)
+    assert fx.sync_status(h) == 0
+
+
+def test_accumulator_overflow_count(fx, h):
+    """Counts of accumulators outside the two's-complement range of 2..32
+    bits, with the boundary values planted, against the plain count."""
+    import torch
+    g = synth.rng_for(72, "ovf")
+    a = (g.standard_normal(100_003) * 2 ** 15).astype(np.int64)
+    a[:8] = [2 ** 15 - 1, 2 ** 15, -2 ** 15, -2 ** 15 - 1, 2 ** 31 - 1, -2 ** 31, 0, -1]
+    a = np.clip(a, -2 ** 31, 2 ** 31 - 1).astype(np.int32)
+    ad = dev(a)
+    for bits in (2, 8, 15, 16, 17, 31, 32):
+        note("acc_overflow", bits)
+        cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+        fx.acc_overflow(h, ad, a.size, bits, cnt)
+        lo, hi = -(1 << (bits - 1)), (1 << (bits - 1)) - 1
+        want = int(np.sum((a.astype(np.int64) < lo) | (a.astype(np.int64) > hi)))
+        assert int(host(cnt)[0]) == want, bits
+    # counts add up across calls
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    fx.acc_overflow(h, ad, a.size, 16, cnt)
+    fx.acc_overflow(h, ad, a.size, 16, cnt)
+    want16 = int(np.sum((a.astype(np.int64) < -2 ** 15) | (a.astype(np.int64) > 2 ** 15 - 1)))
+    assert int(host(cnt)[0]) == 2 * want16
+    assert fx.sync_status(h) == 0
