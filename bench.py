@@ -137,39 +137,46 @@ def qparams_figures(dev, batch=32, image=224):
 
 def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     """Bit-precision level reduction (Algorithm 2) over ResNet-18 on a
-    calibration batch: the forward optimizer's 8-bit design first (untimed
-    set-up), then Algorithm 2 to convergence (or max_changes applied
-    reductions), timed; the memory model before and after; the oracle's
-    reduction on a bounded sample beside it."""
+    calibration batch, from two initial designs: 8-bit everywhere (biases 32)
+    and the paper's wide first / last layers (16-bit input, first and last
+    weights and last-layer input, over wide C-Blocks).  Each: the forward
+    optimizer first (untimed set-up), then Algorithm 2 to convergence (or
+    max_changes applied reductions), timed; the memory model and the 16-bit
+    MAC accounting before and after; the oracle's reduction on a bounded
+    sample beside it."""
     import torch
     from paper_2203_12091_amd import qparams, reduction
-    fo = qparams.ForwardOptimizer("resnet18", batch=batch, image=image, device=str(dev), w_wl=8)
-    fo.run()
-    torch.cuda.synchronize(dev)
-    before = reduction.memory_model(fo)
-    acc0 = fo.top1_agreement()
-    ovf0 = fo.mac_overflow(16)
-    r = reduction.QReduction(fo, thld, max_changes=max_changes)
-    e0 = fo.evals
-    t0 = time.perf_counter()
-    r.run()
-    torch.cuda.synchronize(dev)
-    t = time.perf_counter() - t0
-    after = reduction.memory_model(fo)
-    ovf1 = fo.mac_overflow(16)
-    ev = fo.evals - e0
     out = {"metric": "bit-precision reduction (Algorithm 2) seconds, ResNet-18", "batch": batch,
-           "image": image, "threshold": thld, "max_changes": max_changes,
-           "changes": len(r.changes),
-           "word_lengths": {f"{ln}.{d}": v[0] for (ln, d), v in r.formats().items()},
-           "trials": len(r.trials), "evaluations": ev, "seconds": round(t, 3),
-           "evaluations_per_s": round(ev / t, 2), "top1_agreement_before": round(acc0, 4),
-           "top1_agreement_after": round(r.accuracy(), 4),
-           "memory_mb_before": {k: round(v, 4) for k, v in before.items()},
-           "memory_mb_after": {k: round(v, 4) for k, v in after.items()},
-           "mac16_overflow_before": [sum(c for c, _ in ovf0.values()), sum(m for _, m in ovf0.values())],
-           "mac16_overflow_after": [sum(c for c, _ in ovf1.values()), sum(m for _, m in ovf1.values())]}
-    fo.close()
+           "image": image, "threshold": thld, "max_changes": max_changes}
+    for design, flw in (("design_8bit", None), ("design_wide16", 16)):
+        fo = qparams.ForwardOptimizer("resnet18", batch=batch, image=image, device=str(dev), w_wl=8,
+                                      first_last_wl=flw)
+        fo.run()
+        torch.cuda.synchronize(dev)
+        before = reduction.memory_model(fo)
+        acc0 = fo.top1_agreement()
+        ovf0 = fo.mac_overflow(16)
+        r = reduction.QReduction(fo, thld, max_changes=max_changes)
+        e0 = fo.evals
+        t0 = time.perf_counter()
+        r.run()
+        torch.cuda.synchronize(dev)
+        t = time.perf_counter() - t0
+        after = reduction.memory_model(fo)
+        ovf1 = fo.mac_overflow(16)
+        ev = fo.evals - e0
+        out[design] = {
+            "changes": len(r.changes),
+            "word_lengths": {f"{ln}.{d}": v[0] for (ln, d), v in r.formats().items()},
+            "trials": len(r.trials), "evaluations": ev, "seconds": round(t, 3),
+            "evaluations_per_s": round(ev / t, 2), "top1_agreement_before": round(acc0, 4),
+            "top1_agreement_after": round(r.accuracy(), 4),
+            "memory_mb_before": {k: round(v, 4) for k, v in before.items()},
+            "memory_mb_after": {k: round(v, 4) for k, v in after.items()},
+            "mac16_overflow_before": [sum(c for c, _ in ovf0.values()), sum(m for _, m in ovf0.values())],
+            "mac16_overflow_after": [sum(c for c, _ in ovf1.values()), sum(m for _, m in ovf1.values())]}
+        fo.close()
+        del fo, r
     import oracle.qparams as oq
     import oracle.reduction as orr
     ref = oq.ForwardOptimizer("resnet18", batch=1, image=16, w_wl=8)

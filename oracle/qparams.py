@@ -99,12 +99,17 @@ def _ties(scores):
 
 class ForwardOptimizer:
     def __init__(self, name="resnet18", seed=None, batch=2, image=32, K=1,
-                 strategy=pre.CONSERVATIVE, w_wl=None):
+                 strategy=pre.CONSERVATIVE, w_wl=None, first_last_wl=None):
         self.seed = SEED[name] if seed is None else seed
         g = Graph(self.seed)
         g.network_input(synth.normal(self.seed, "input", (batch, 3, image, image)))
         resnet(g, name == "resnet50")
         self.g, self.K, self.B, self.w_wl = g, K, batch, w_wl
+        # the network input, the first and last layers' weights and the last
+        # layer's input (avg-pool FxP-QLayer) at this word length when given
+        self.fl_wl = first_last_wl
+        convs = [nm for op, nm, _ in g.nodes if op == "conv"]
+        self.edge = (convs[0], convs[-1])
         self.spec = {nm: sp for op, nm, sp in g.nodes if op == "conv"}
         self.order = [("input", "a")]
         for op, nm, sp in g.nodes:
@@ -143,9 +148,11 @@ class ForwardOptimizer:
 
     def _tensor(self, ln, d):
         if ln == "input":
-            return self.g.x, 8
+            return self.g.x, self.fl_wl or 8
         sp = self.spec[ln]
         if d == "w":
+            if self.fl_wl is not None and ln in self.edge:
+                return sp["w"], self.fl_wl
             return sp["w"], self.w_wl or sp["wl"]
         if d == "b":
             return sp["b"], 32
@@ -316,8 +323,9 @@ class ForwardOptimizer:
         fr, sr, _ = orc.fl_search_f32(r, 16, orc.SIGN_AUTO, *FL)
         rq = orc.quantize_f32(r, 16, fr, sr)
         y = orc.avgpool_global(x, int(rq[0])).reshape(x.shape[0], x.shape[1], 1, 1)
-        fo, so, _ = orc.fl_search_i64(y.ravel(), f + fr, 8, orc.SIGN_AUTO, *FL)
-        return orc.quantize_i64(y, f + fr, 8, fo, so), fo, so
+        wl = self.fl_wl or 8  # the last layer's input
+        fo, so, _ = orc.fl_search_i64(y.ravel(), f + fr, wl, orc.SIGN_AUTO, *FL)
+        return orc.quantize_i64(y, f + fr, wl, fo, so), fo, so
 
     def finalize(self, ln):
         q, fl, sign, _ = self._quant_layer(ln)

@@ -242,7 +242,7 @@ def memory_model(fo, formats=None):
             k[nm] = 8
         else:
             ins = [sp["src"]]
-            k[nm] = 8
+            k[nm] = fo.fl_wl or 8
         layers.append((nm, ins))
     k32 = {key: 32 for key in k}
     rw_fp, rw_q = rw_required(layers, nu, k32), rw_required(layers, nu, k)

@@ -42,10 +42,15 @@ from .sweep import Sweep
 
 class ForwardOptimizer:
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", K=1,
-                 strategy=fx.ROUND_CONSERVATIVE, psi_rule=fx.PSI_PRINTED, w_wl=None):
+                 strategy=fx.ROUND_CONSERVATIVE, psi_rule=fx.PSI_PRINTED, w_wl=None,
+                 first_last_wl=None):
         self.sw = Sweep(name, seed, batch, image, device, wwls=(), awls=())
         self.T, self.h, self.B, self.K = self.sw.T, self.sw.h, self.sw.batch, K
         self.w_wl = w_wl  # one word length for every layer's weights (else the network's)
+        # word length of the network input, the first and last layers' weights
+        # and the last layer's input (the avg-pool FxP-QLayer); wide C-Blocks
+        # above 8 bits
+        self.fl_wl = first_last_wl
         T = self.T
         self.nodes = list(self.sw.graph)
         self.L = {L["node"].name: L for L in self.sw.layers}
@@ -118,12 +123,24 @@ class ForwardOptimizer:
             self.bufs[key] = b
         return b
 
+    def _edge(self, ln):
+        convs = [n.name for n in self.nodes if n.op in ("conv", "fc")]
+        return self.fl_wl is not None and ln in (convs[0], convs[-1])
+
+    def _first_wide(self):
+        """The first layer's C-Block runs on int32 codes (input or weights
+        wider than 8 bits); the input is stored as int32 codes then."""
+        first = [n.name for n in self.nodes if n.op in ("conv", "fc")][0]
+        return self.qp[("input", "a")][0] > 8 or self.qp[(first, "w")][0] > 8
+
     def _tensor(self, ln, d):
         """FP32 data structure (device) and its word length."""
         if ln == "input":
-            return self.act["input"], A_WL
+            return self.act["input"], self.fl_wl or A_WL
         L = self.L[ln]
         if d == "w":
+            if self._edge(ln):
+                return L["w_krsc"], self.fl_wl
             return L["w_krsc"], self.w_wl or L["node"].wl
         if d == "b":
             return L["b_f32"], BIAS_WL
@@ -156,13 +173,13 @@ class ForwardOptimizer:
         L, key = self.L[ln], (ln, d)
         e = self._buf((ln, d, "err"), (4,), self.T.float64)
         fq = tuple(self.qp[key])
-        if self.pfmt.get(key) != fq:
+        if self.pfmt.get((key, ctype)) != fq:
             x = L["w_krsc"] if d == "w" else L["b_f32"]
             fx.quantize(self.h, x, x.numel(), self.fmt[key], codes, ctype)
-            if d == "w":
+            if d == "w" and ctype == fx.I8:
                 fx.weight_colsum(self.h, codes, L["node"].cout, L["wlen"], self._buf((ln, "colsum"), (L["node"].cout,), self.T.int32))
             fx.layer_error(self.h, x, codes, ctype, self.fmt[key], x.numel(), e)
-            self.pfmt[key] = fq
+            self.pfmt[(key, ctype)] = fq
         errs.append((key, e))
 
     def _quant_layer(self, ln, errs, src=None):
@@ -174,16 +191,21 @@ class ForwardOptimizer:
         qcodes, qfmt = src if src is not None else (self.qcodes, self.qfmt)
         if ln == "input":
             x = self.act["input"]
-            codes = self._buf(("input", "codes"), x.shape, T.int8)
-            fx.quantize(h, x, x.numel(), self.fmt[("input", "a")], codes, fx.C8)
+            wide = self._first_wide()
+            ct = fx.I32 if wide else fx.C8
+            codes = self._buf(("input", "codes", ct), x.shape, T.int32 if wide else T.int8)
+            fx.quantize(h, x, x.numel(), self.fmt[("input", "a")], codes, ct)
             e = self._buf(("input", "a", "err"), (4,), T.float64)
-            fx.layer_error(h, x, codes, fx.C8, self.fmt[("input", "a")], x.numel(), e)
+            fx.layer_error(h, x, codes, ct, self.fmt[("input", "a")], x.numel(), e)
             errs.append((("input", "a"), e))
-            return codes, self.fmt[("input", "a")], fx.C8
+            return codes, self.fmt[("input", "a")], ct
         L = self.L[ln]
         n = L["node"]
-        wcodes = self._buf((ln, "wcodes"), (L["w_krsc"].numel(),), T.int8)
-        self._param(ln, "w", wcodes, fx.I8, errs)
+        wide = qcodes[n.inp].dtype == T.int32
+        assert wide or self.qp[(ln, "w")][0] <= 8, ln
+        wct = fx.I32 if wide else fx.I8
+        wcodes = self._buf((ln, "wcodes", wct), (L["w_krsc"].numel(),), T.int32 if wide else T.int8)
+        self._param(ln, "w", wcodes, wct, errs)
         cs = self._buf((ln, "colsum"), (n.cout,), T.int32)
         kw = {}
         if n.bias:
@@ -195,13 +217,26 @@ class ForwardOptimizer:
                       fl_shift=L["fl"][("a2", None)][1])
         xin = qcodes[n.inp]
         ep = fx.epilogue(n.cout, self.qp[(ln, "w")][1], qfmt[n.inp], relu=n.relu, **kw)
-        acc = self._buf(("acc",), (L["M"], n.cout), T.int32)
-        mm = self._buf((ln, "mm"), (2,), T.float64)
-        if L["fc"]:
-            fx.qgemm(h, L["M"], n.cout, L["wlen"], xin, fx.C8, wcodes, cs, ep, acc, mm)
+        if wide:
+            # codes wider than 8 bits: the int8 plane contractions of fxpq_qconv_wide
+            xf = qfmt[n.inp].cpu().numpy()
+            wl_w, _, sw = self.qp[(ln, "w")]
+            d = L["desc"]
+            nb = fx.qconv_wide_workspace(d, int(xf[0]), int(xf[2]), wl_w, sw)
+            ws = self._buf((ln, "wide-ws"), (nb,), T.uint8)
+            v = self._buf((ln, "wide-v"), (L["M"] * n.cout,), T.int64)
+            sc = self._buf((ln, "wide-s"), (1,), T.int32)
+            fx.qconv_wide(h, d, xin, int(xf[0]), int(xf[2]), wcodes, wl_w, sw, ep, v, sc, ws, nb)
+            src = fx.src_int(v, fx.I64, sc)
+            acc = v
         else:
-            fx.qconv(h, L["desc"], xin, fx.C8, wcodes, cs, ep, acc, mm)
-        src = fx.src_acc(acc, ep, mm)
+            acc = self._buf(("acc",), (L["M"], n.cout), T.int32)
+            mm = self._buf((ln, "mm"), (2,), T.float64)
+            if L["fc"]:
+                fx.qgemm(h, L["M"], n.cout, L["wlen"], xin, fx.C8, wcodes, cs, ep, acc, mm)
+            else:
+                fx.qconv(h, L["desc"], xin, fx.C8, wcodes, cs, ep, acc, mm)
+            src = fx.src_acc(acc, ep, mm)
         self.held[ln] = (ep, src)
         y_ref = L["y_ref"]
         e = self._buf((ln, "a", "err"), (4,), T.float64)
@@ -258,6 +293,11 @@ class ForwardOptimizer:
             s = fx.src_int(acc, fx.I64, sc)
             self.held[(n.name, "src")] = (ep, s)
             m = acc.numel()
+            if self.fl_wl is not None:  # the last layer's input, int32 codes
+                y32 = self._buf((n.name, "codes32"), tuple(self.act[n.name].shape), T.int32)
+                fx.fl_search(h, s, m, self.fl_wl, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+                fx.requant(h, s, m, f, y32, fx.I32)
+                return y32, f
         fx.fl_search(h, s, m, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
         fx.requant(h, s, m, f, y, fx.C8)
         return y, f
@@ -266,7 +306,8 @@ class ForwardOptimizer:
         if name not in self.deq:
             c = self.qcodes[name]
             y = self._empty(c.shape, self.T.float32)
-            fx.dequantize(self.h, c, fx.C8, self.qfmt[name], c.numel(), y)
+            ct = fx.I32 if c.dtype == self.T.int32 else fx.C8
+            fx.dequantize(self.h, c, ct, self.qfmt[name], c.numel(), y)
             self.deq[name] = y
         return self.deq[name]
 
@@ -276,12 +317,14 @@ class ForwardOptimizer:
         self.evals += 1
         errs = []
         codes, cfmt, ctype = self._quant_layer(ln, errs)
-        if ctype == fx.C8:
+        is_last = ln != "input" and self.L[ln]["node"].last
+        y = None
+        if not is_last:
             y = self._buf((ln, "deq-cur"), codes.shape, T.float32)
-            fx.dequantize(h, codes, fx.C8, cfmt, codes.numel(), y)
-        fp = {ln: y if ctype == fx.C8 else None}
+            fx.dequantize(h, codes, ctype, cfmt, codes.numel(), y)
+        fp = {ln: y}
         start = 0 if ln == "input" else self.pos[ln] + 1
-        logits32 = codes if ctype == fx.I32 else None
+        logits32 = codes if is_last else None
         for n in self.nodes[start:]:
             if n.op == "input":
                 continue

@@ -199,6 +199,8 @@ def memory_model(fo):
                     params.append((n.name, d))
         elif n.op == "maxpool":
             bits[n.name] = bits[n.inp]
+        elif n.op == "avgpool" and fo.fl_wl is not None:
+            bits[n.name] = fo.fl_wl  # the last layer's input
         else:
             bits[n.name] = 8
         steps.append((n.name, ins))

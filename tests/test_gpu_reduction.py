@@ -66,3 +66,40 @@ def test_reduction_matches_oracle(fx):
     same_trace(fo.trace[n1:], ref.trace[n1:])
     assert fx.sync_status(fo.h) == 0
     fo.close()
+
+
+def test_wide_first_last_layers_match_oracle(fx):
+    """The paper's initial design with wide first / last layers (here 16-bit
+    input, first and last weights and last-layer input; wide C-Blocks on the
+    GPU): the forward optimizer, two changes of Algorithm 2, then the binary
+    searches of the 16-bit input and FC weights from their 16 bits."""
+    from oracle import qparams as OQ
+    from oracle import reduction as OR
+    from paper_2203_12091_amd import qparams as GQ
+    from paper_2203_12091_amd import reduction as GR
+    note("wide first/last oracle resnet18 2x16")
+    ref = OQ.ForwardOptimizer("resnet18", batch=2, image=16, w_wl=8, first_last_wl=16)
+    want = ref.run()
+    note("wide first/last gpu resnet18 2x16")
+    fo = GQ.ForwardOptimizer("resnet18", batch=2, image=16, device=DEV, w_wl=8, first_last_wl=16)
+    got = fo.run()
+    assert got == {k: tuple(v) for k, v in want.items()}
+    assert got[("input", "a")][0] == 16 and got[("fc", "w")][0] == 16
+    same_trace(fo.trace, ref.trace)
+    assert fo.top1_agreement() == ref.top1(ref.q[ref.last][0])
+    rr, rg = OR.QReduction(ref, 0.5, max_changes=2), GR.QReduction(fo, 0.5, max_changes=2)
+    n0 = len(ref.trace)
+    note("wide first/last reduction")
+    assert rg.run() == rr.run()
+    assert rg.trials == rr.trials and rg.changes == rr.changes
+    for key in (("input", "a"), ("fc", "w")):
+        t0 = len(rr.trials)
+        note("wide first/last reduce", key)
+        cr = [c for c in rr.clusters[1] if key in c][0]
+        cg = [c for c in rg.clusters[1] if key in c][0]
+        assert rg.reduce(cg, 0.5, 1) == rr.reduce(cr, 0.5, 1)
+        assert rg.trials[t0:] == rr.trials[t0:] and len(rr.trials) - t0 >= 3
+    same_trace(fo.trace[n0:], ref.trace[n0:])
+    assert GR.memory_model(fo) == OR.memory_model(ref)
+    assert fx.sync_status(fo.h) == 0
+    fo.close()
