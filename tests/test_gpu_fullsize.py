@@ -169,3 +169,51 @@ def test_largest_3x3_conv_sampled(env):
     assert torch.equal(acc, acc2)
     assert fx.sync_status(h) == 0
     h.close()
+
+
+def test_wide_first_layer_full_batch_sampled(env):
+    """The wide C-Block in bench.py's --mode wide configuration: ResNet-50's
+    first conv over 256 x 224 x 224 padded RGB with 16-bit input codes and
+    16-bit weights (Scale + ReLU epilogue), exact int64 values checked
+    against the oracle's integer convolution and epilogue at 256 sampled
+    output pixels (all 64 channels each), plus the scale and the flags."""
+    torch, fx, nets, orc = env
+    N, H, C, K, R = 256, 224, 3, 64, 7
+    g = synth.rng_for(81, "wide-full")
+    xc = g.integers(-2 ** 15, 2 ** 15, (N, C, H, H), dtype=np.int32)
+    wc = g.integers(-2 ** 15, 2 ** 15, (K, C, R, R), dtype=np.int32)
+    a1 = g.integers(-2 ** 15, 2 ** 15, K).astype(np.int32)
+    a2 = g.integers(-2 ** 31, 2 ** 31 - 1, K).astype(np.int32)
+    x4 = np.zeros((N, H, H, 4), np.int32)
+    x4[..., :3] = xc.transpose(0, 2, 3, 1)
+    depth = R * R * 4
+    w4 = np.zeros((K, R, R, 4), np.int32)
+    w4[..., :3] = wc.transpose(0, 2, 3, 1)
+    wrow = np.zeros((K, (depth + 63) // 64 * 64), np.int32)
+    wrow[:, :depth] = w4.reshape(K, -1)
+    fin = torch.tensor([16, 12, 1, 0], dtype=torch.int32, device=DEV)
+    a1d, a2d = dev(a1), dev(a2)
+    ep = fx.epilogue(K, 14, fin, relu=True, scale=a1d, fl_scale=14, shift=a2d, fl_shift=20)
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+    d = fx.conv_desc(N, H, H, 4, K, R, R, 2, 3)
+    nb = fx.qconv_wide_workspace(d, 16, 1, 16, 1)
+    ws = empty((nb,), torch.uint8)
+    Ho = (H + 6 - R) // 2 + 1
+    v = empty((N * Ho * Ho * K,), torch.int64)
+    sc = empty((1,), torch.int32)
+    note("fullsize wide conv1 16x16")
+    fx.qconv_wide(h, d, dev(x4), 16, 1, dev(wrow), 16, 1, ep, v, sc, ws, nb)
+    assert fx.sync_status(h) == 0
+    del ws
+    got = host(v).reshape(N, Ho, Ho, K)
+    pix = [(int(n), int(p), int(q)) for n, p, q in
+           zip(g.integers(0, N, 256), g.integers(0, Ho, 256), g.integers(0, Ho, 256))]
+    pix += [(0, 0, 0), (N - 1, Ho - 1, Ho - 1), (7, 0, Ho - 1)]
+    acc = np.array([[orc.conv2d_point(xc, wc, 2, 3, n, k, p, q) for k in range(K)] for n, p, q in pix],
+                   np.int64)
+    want, s_out = orc.epilogue(acc, 12 + 14, None, 0, a1.astype(np.int64), 14, a2.astype(np.int64), 20,
+                               True)
+    assert int(host(sc)[0]) == s_out
+    assert np.array_equal(np.array([got[n, p, q] for n, p, q in pix]), want)
+    h.close()
