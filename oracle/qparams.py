@@ -25,9 +25,10 @@ searches, Scale parameters their searched formats.  ResNets only (their FC
 follows a global pooling, so the FP32 FC sums in the same order on both
 sides).
 
-parity unpinned: no printed example exists for the search; it is pinned
-through its parts (tests/test_oracle_preprocess.py, tests/test_oracle_pins.py,
-tests/test_oracle_teacher.py) and by a brute-force check of the search rule
+parity unpinned for the network cost F as composed (no printed example
+exists); its parts are pinned (tests/test_oracle_preprocess.py,
+tests/test_oracle_pins.py, tests/test_oracle_teacher.py), and the search rule
+on hand-worked cost curves and against brute force
 (tests/test_oracle_qparams.py).
 """
 import math

@@ -40,8 +40,10 @@ Readings (the GPU driver takes the same):
     channels), the model's counts for parameters; the sums in phi run over
     the data structures of that type taking part (G1 / G2 members).
 
-parity unpinned: there is no printed run; the rules are pinned on stub
-accuracy curves worked by hand and the composed run by invariants
+parity unpinned for the composed run over a network (the paper prints
+none); the Reduce / select / traversal rules are pinned on stub accuracy
+functions worked by hand, the memory model on the paper's CONV-1 saving and
+ResNet-18's parameter count, the composed run by invariants
 (tests/test_oracle_reduction.py).
 """
 import math
