@@ -136,20 +136,24 @@ def qparams_figures(dev, batch=32, image=224):
 
 
 def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
-    """Bit-precision level reduction (Algorithm 2) over ResNet-18 on a
-    calibration batch, from two initial designs: 8-bit everywhere (biases 32)
-    and the paper's wide first / last layers (16-bit input, first and last
-    weights and last-layer input, over wide C-Blocks).  Each: the forward
+    """Bit-precision level reduction (Algorithm 2) on a calibration batch:
+    ResNet-18 from two initial designs, 8-bit everywhere (biases 32) and the
+    paper's wide first / last layers (16-bit input, first and last weights
+    and last-layer input, over wide C-Blocks), and AlexNet and VGG-16 from
+    the 8-bit design.  Each: the forward
     optimizer first (untimed set-up), then Algorithm 2 to convergence (or
     max_changes applied reductions), timed; the memory model and the 16-bit
     MAC accounting before and after; the oracle's reduction on a bounded
     sample beside it."""
     import torch
     from paper_2203_12091_amd import qparams, reduction
-    out = {"metric": "bit-precision reduction (Algorithm 2) seconds, ResNet-18", "batch": batch,
+    out = {"metric": "bit-precision reduction (Algorithm 2) seconds", "batch": batch,
            "image": image, "threshold": thld, "max_changes": max_changes}
-    for design, flw in (("design_8bit", None), ("design_wide16", 16)):
-        fo = qparams.ForwardOptimizer("resnet18", batch=batch, image=image, device=str(dev), w_wl=8,
+    runs = (("resnet18", "design_8bit", None), ("resnet18", "design_wide16", 16),
+            ("alexnet", "design_8bit", None), ("vgg16", "design_8bit", None))
+    for net, design, flw in runs:
+        design = f"{net}_{design}"
+        fo = qparams.ForwardOptimizer(net, batch=batch, image=image, device=str(dev), w_wl=8,
                                       first_last_wl=flw)
         fo.run()
         torch.cuda.synchronize(dev)

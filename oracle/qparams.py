@@ -21,9 +21,10 @@ error for the current layer (zero for FP32 layers) and the distance from the
 teacher's activation for activations; pi = sigma * size normalized over a
 layer's data structures (sigma over the whole tensor); R = max - min of the
 FP32 data structure; eltwise / avg-pool FxP-QLayers keep their Eq. 14
-searches, Scale parameters their searched formats.  ResNets only (their FC
-follows a global pooling, so the FP32 FC sums in the same order on both
-sides).
+searches, Scale parameters their searched formats.  Any of the workloads'
+networks; the FP32 FC sums the flattened input channel-major, the GPU's
+order whenever the FC input is 1x1 spatially (the ResNets, and AlexNet /
+VGG-16 on the small images of the parity tests).
 
 parity unpinned for the network cost F as composed (no printed example
 exists); its parts are pinned (tests/test_oracle_preprocess.py,
@@ -39,7 +40,10 @@ import synth
 
 from . import core as orc
 from . import preprocess as pre
-from .nets import FL, SEED, resnet
+from .nets import FL, SEED, alexnet, resnet, vgg16
+
+BUILD = {"alexnet": alexnet, "vgg16": vgg16, "resnet18": lambda g: resnet(g, False),
+         "resnet50": lambda g: resnet(g, True)}
 from .sweep import Teacher
 
 
@@ -104,7 +108,7 @@ class ForwardOptimizer:
         self.seed = SEED[name] if seed is None else seed
         g = Graph(self.seed)
         g.network_input(synth.normal(self.seed, "input", (batch, 3, image, image)))
-        resnet(g, name == "resnet50")
+        BUILD[name](g)
         self.g, self.K, self.B, self.w_wl = g, K, batch, w_wl
         # the network input, the first and last layers' weights and the last
         # layer's input (avg-pool FxP-QLayer) at this word length when given

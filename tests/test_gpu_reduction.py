@@ -103,3 +103,30 @@ def test_wide_first_last_layers_match_oracle(fx):
     assert GR.memory_model(fo) == OR.memory_model(ref)
     assert fx.sync_status(fo.h) == 0
     fo.close()
+
+
+@pytest.mark.parametrize("name,image", [("alexnet", 63), ("vgg16", 32)])
+def test_alexnet_vgg_match_oracle(fx, name, image):
+    """The paper's other two networks (2 images, small enough that the FC
+    input is 1x1): the forward optimizer's candidates and formats, one
+    change of Algorithm 2 and the memory model, identical to the oracle."""
+    from oracle import qparams as OQ
+    from oracle import reduction as OR
+    from paper_2203_12091_amd import qparams as GQ
+    from paper_2203_12091_amd import reduction as GR
+    note("optimizer oracle", name, image)
+    ref = OQ.ForwardOptimizer(name, batch=2, image=image, w_wl=8)
+    want = ref.run()
+    note("optimizer gpu", name, image)
+    fo = GQ.ForwardOptimizer(name, batch=2, image=image, device=DEV, w_wl=8)
+    got = fo.run()
+    assert got == {k: tuple(v) for k, v in want.items()}
+    same_trace(fo.trace, ref.trace)
+    assert fo.top1_agreement() == ref.top1(ref.q[ref.last][0])
+    rr, rg = OR.QReduction(ref, 0.5, max_changes=1), GR.QReduction(fo, 0.5, max_changes=1)
+    note("reduction", name)
+    assert rg.run() == rr.run()
+    assert rg.trials == rr.trials and rg.changes == rr.changes and len(rr.changes) == 1
+    assert GR.memory_model(fo) == OR.memory_model(ref)
+    assert fx.sync_status(fo.h) == 0
+    fo.close()
