@@ -80,7 +80,9 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   // scaled by 2^(sigma - sv) = 2^(fl_hi + 24), exactly.
   const double post = u.wscale;
   const int64_t nfull = n - n % PK::EP;
-  stream_packets<KIND, DT, false, kWinSets>(s, n, tv, [&](const double* v, int64_t i0, int) {
+  // backwards: the pass starts with the lines the previous kernel (the
+  // conv, or the eltwise min / max pass, which reads forwards) touched last
+  stream_packets<KIND, DT, false, kWinSets, true>(s, n, tv, [&](const double* v, int64_t i0, int) {
     int cq[PK::EP][kWindow];
 #pragma unroll
     for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j], cq[j]);

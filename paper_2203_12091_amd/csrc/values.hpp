@@ -134,7 +134,11 @@ __device__ inline void unpack(const Raw<KIND, DT>& r, const ThreadVals<Pack<KIND
 // consumed), so the number of loads in flight is fixed and the wait before
 // each use only covers the older one.  Values past the last whole packet are
 // left to the caller.
-template <int KIND, int DT, bool AUX = false, int NSET = 2, typename F>
+// REV: the thread visits its packets from the last to the first (the same
+// packets and channels), so that a pass right after the kernel that wrote the
+// tensor starts with its most recently written lines, still in the
+// memory-side cache.
+template <int KIND, int DT, bool AUX = false, int NSET = 2, bool REV = false, typename F>
 __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
                                       F&& fp, const int8_t* aux = nullptr) {
   // AUX: one byte per value of `aux`, loaded with each packet and handed to
@@ -170,6 +174,23 @@ __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVa
   int64_t base = (int64_t)blockIdx.x * chunk;
   Raw<KIND, DT> rs[NSET][PK::P];
   int xs[NSET][PK::P] = {};
+  if constexpr (REV) {
+    // packets j = 0 .. J-1 at base + j * stride, visited from J-1 down; a
+    // load for j < 0 reads packet 0 again and is not consumed
+    if (base >= nfull) return;
+    const int64_t top = (nfull - 1 - base) / stride;
+    auto at = [&](int64_t j) { return base + (j < 0 ? 0 : j) * stride; };
+#pragma unroll
+    for (int k = 0; k < NSET; ++k) load_set(at(top - k), rs[k], xs[k]);
+    for (int64_t j = top; j >= 0; j -= NSET) {
+#pragma unroll
+      for (int k = 0; k < NSET; ++k) {
+        if (j - k >= 0) use_set(at(j - k), rs[k], xs[k]);
+        load_set(at(j - NSET - k), rs[k], xs[k]);
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int k = 0; k < NSET; ++k) load_set(base + k * stride, rs[k], xs[k]);
   for (; base < nfull; base += NSET * stride) {
