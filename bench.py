@@ -44,7 +44,7 @@ def parse():
                     help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
     ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams", "reduction",
-                                       "wide"],
+                                       "wide", "steps"],
                     default="bench",
                     help="profile: set up and run --warmup forwards only (for counter runs); "
                          "copy: one plain 1 GiB device copy (counter calibration); "
@@ -262,6 +262,63 @@ def wide_figures(dev, batch=256):
     return out
 
 
+def steps_figures(dev):
+    """Each hot-path call alone at ResNet-50 b256's largest tensors, inputs
+    resident in HBM: quantize of the padded network input (256x224x224x4
+    fp32), and over conv1-shaped int32 accumulators (256x112x112x64, Scale +
+    ReLU epilogue) the FL search (min / max pass included), the
+    requantization, the fused FxP-QLayer and the layer error against an fp32
+    reference.  Algorithmic bytes: 4 B per fp32 or int32 value read, 1 B per
+    code written (the search writes none); 5 timed calls after one untimed."""
+    import torch
+    from paper_2203_12091_amd import fxpq as fx
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+    gen = torch.Generator(device=dev).manual_seed(12)
+    x = torch.randn((256, 224, 224, 4), generator=gen, device=dev)
+    acc = torch.randint(-2 ** 20, 2 ** 20, (256 * 112 * 112, 64), generator=gen, device=dev,
+                        dtype=torch.int32)
+    ref = torch.randn(acc.shape, generator=gen, device=dev)
+    a1 = torch.randint(2 ** 14, 2 ** 15, (64,), generator=gen, device=dev, dtype=torch.int32)
+    a2 = torch.randint(-2 ** 20, 2 ** 20, (64,), generator=gen, device=dev, dtype=torch.int32)
+    fin = torch.tensor([8, 5, 1, 0], dtype=torch.int32, device=dev)
+    ep = fx.epilogue(64, 9, fin, relu=True, scale=a1, fl_scale=15, shift=a2, fl_shift=20)
+    fmt_x = torch.tensor([8, 5, 1, 0], dtype=torch.int32, device=dev)
+    fmt_a = torch.zeros(4, dtype=torch.int32, device=dev)
+    fmt_q = torch.zeros(4, dtype=torch.int32, device=dev)
+    cx = torch.empty(x.numel(), dtype=torch.int8, device=dev)
+    ca = torch.empty(acc.numel(), dtype=torch.int8, device=dev)
+    alt = torch.empty(acc.numel(), dtype=torch.int8, device=dev)
+    err = torch.empty(4, dtype=torch.float64, device=dev)
+    n_x, n_a = x.numel(), acc.numel()
+    src = fx.src_acc(acc, ep)
+    calls = {
+        "a1_quantize_fp32": (lambda: fx.quantize(h, x, n_x, fmt_x, cx, fx.C8), 5 * n_x),
+        "a2_fl_search_acc": (lambda: fx.fl_search(h, src, n_a, 8, fx.SIGN_AUTO, -8, 15, fmt_a), 4 * n_a),
+        "a4_requant_acc": (lambda: fx.requant(h, src, n_a, fmt_a, ca, fx.C8), 5 * n_a),
+        "a2a4_qlayer_acc": (lambda: fx.qlayer(h, src, n_a, 8, fx.SIGN_AUTO, -8, 15, fmt_q, ca, fx.C8, alt),
+                            5 * n_a),
+        "a5_layer_error": (lambda: fx.layer_error(h, ref, ca, fx.C8, fmt_a, n_a, err), 5 * n_a),
+    }
+    out = {"tensors": {"input": list(x.shape), "acc": [256, 112, 112, 64]}}
+    for name, (call, nbytes) in calls.items():
+        call()
+        torch.cuda.synchronize(dev)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(5):
+            call()
+        e1.record()
+        torch.cuda.synchronize(dev)
+        ms = e0.elapsed_time(e1) / 5
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        out[name] = {"ms": round(ms, 4), "algorithmic_bytes": nbytes, "gbs": round(gbs, 1),
+                     "frac_of_hbm_peak": round(gbs / HBM_PEAK_GBS, 4)}
+    assert fx.sync_status(h) == 0
+    h.close()
+    return out
+
+
 def compute_bound_mfma(net, dev):
     """int8 MFMA use over the convolutions whose arithmetic intensity (int8
     ops per HBM byte: input codes, weights, int32 output) is above the ridge
@@ -350,6 +407,9 @@ def main():
         return
     if args.mode == "wide":
         print(json.dumps(wide_figures(dev)), flush=True)
+        return
+    if args.mode == "steps":
+        print(json.dumps(steps_figures(dev)), flush=True)
         return
 
     net = nets.CalibNet("resnet50", batch=BATCH, image=IMAGE, device="cuda:0")
