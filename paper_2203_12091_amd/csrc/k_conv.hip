@@ -38,6 +38,9 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 64;
+// Cache policy of the int32 accumulator stores: non-temporal (the tensor is
+// read once, by the FL search that follows, not by this kernel).
+constexpr int kAccPolicy = 2;
 
 // LDS slab layout: rows of 64 bytes (four 16-byte chunks), no padding; chunk
 // c of row r sits at chunk position c ^ f(r) with f(r) = (r >> 2) & 3.  The
@@ -630,7 +633,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
             const int lr = mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
             const bool ok = lr < vrows;
             const int v = acc[mi][ni][e];
-            if constexpr (EPI == EPI_ACC) *(ok ? dst + (int64_t)lr * a.K : sink) = v + corr;
+            if constexpr (EPI == EPI_ACC)
+              __builtin_nontemporal_store(v + corr, ok ? dst + (int64_t)lr * a.K : sink);
             lo[ni] = min(lo[ni], ok ? v : INT_MAX);
             hi[ni] = max(hi[ni], ok ? v : INT_MIN);
           }
@@ -657,7 +661,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
             const int v = acc[mi][ni][e];
             if constexpr (EPI == EPI_ACC)
               __builtin_amdgcn_raw_buffer_store_b32(
-                  v + corr, rs, vo[ni], (mi * 32 + 8 * (e >> 2) + (e & 3)) * a.K * 4, 0);
+                  v + corr, rs, vo[ni], (mi * 32 + 8 * (e >> 2) + (e & 3)) * a.K * 4, kAccPolicy);
             lo[ni] = min(lo[ni], v);
             hi[ni] = max(hi[ni], v);
           }
@@ -675,7 +679,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
             const int row = m0 + wm * WROWS + mi * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
             if (row < a.M && col < a.K) {
               const int v = acc[mi][ni][e];
-              if constexpr (EPI == EPI_ACC) a.acc[(int64_t)row * a.K + col] = v + corr;
+              if constexpr (EPI == EPI_ACC)
+                __builtin_nontemporal_store(v + corr, a.acc + (int64_t)row * a.K + col);
               lo[ni] = min(lo[ni], v);
               hi[ni] = max(hi[ni], v);
             }
