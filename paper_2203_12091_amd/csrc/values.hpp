@@ -86,6 +86,12 @@ __device__ inline Raw<KIND, DT> load_raw(const SrcDev& s, int64_t i) {
     r.b = *reinterpret_cast<const int4*>(static_cast<const int8_t*>(s.x2) + i);
   } else if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) {
     r.a = *reinterpret_cast<const int4*>(static_cast<const int64_t*>(s.x) + i);
+  } else if constexpr (KIND == FXPQ_SRC_ACC) {
+    // conv accumulators are read once (by the FL search): non-temporal
+    typedef int v4 __attribute__((ext_vector_type(4)));
+    const v4 t = __builtin_nontemporal_load(
+        reinterpret_cast<const v4*>(static_cast<const int32_t*>(s.x) + i));
+    r.a = make_int4(t.x, t.y, t.z, t.w);
   } else {
     r.a = *reinterpret_cast<const int4*>(static_cast<const int32_t*>(s.x) + i);
   }
