@@ -77,11 +77,39 @@ __global__ __launch_bounds__(kThreads) void k_minmax(SrcDev s, int64_t n, double
   double mn = INFINITY, mx = -INFINITY;
   bool bad = false;
   const int64_t nfull = n - n % PK::EP;
-  stream_values<KIND, DT>(s, n, t, [&](double v, int64_t) {
-    mn = fmin(mn, v);
-    mx = fmax(mx, v);
-    if (KIND == FXPQ_SRC_F32) bad |= !isfinite(v);
-  });
+  bool done = false;
+  if constexpr (KIND == FXPQ_SRC_ADD) {
+    if (t.sa <= kAddMaxShift && t.sb <= kAddMaxShift) {
+      // eltwise sums in integers: value = relu(x + k) is non-decreasing in
+      // x = (a << sa) + (b << sb) (|x| < 2^30), so the extremes of the values
+      // are those of x, finished once
+      int lo = INT_MAX, hi = INT_MIN;
+      stream_packets<KIND, DT, false, 2, false, true>(
+          s, n, t, [&](const Raw<KIND, DT>& r, int64_t, int) {
+            const int wa[4] = {r.a.x, r.a.y, r.a.z, r.a.w};
+            const int wb[4] = {r.b.x, r.b.y, r.b.z, r.b.w};
+#pragma unroll
+            for (int j = 0; j < PK::EP; ++j) {
+              const int ca = (wa[j / 4] << (24 - 8 * (j % 4))) >> 24;
+              const int cb = (wb[j / 4] << (24 - 8 * (j % 4))) >> 24;
+              const int x = (ca << t.sa) + (cb << t.sb);
+              lo = min(lo, x);
+              hi = max(hi, x);
+            }
+          });
+      if (lo <= hi) {
+        mn = fmax((double)lo + t.k, t.relo);
+        mx = fmax((double)hi + t.k, t.relo);
+      }
+      done = true;
+    }
+  }
+  if (!done)
+    stream_values<KIND, DT>(s, n, t, [&](double v, int64_t) {
+      mn = fmin(mn, v);
+      mx = fmax(mx, v);
+      if (KIND == FXPQ_SRC_F32) bad |= !isfinite(v);
+    });
   if (gtid == 0) {
     for (int64_t i = nfull; i < n; ++i) {
       double v = load1<KIND, DT>(s, i);

@@ -144,7 +144,10 @@ __device__ inline void unpack(const Raw<KIND, DT>& r, const ThreadVals<Pack<KIND
 // packets and channels), so that a pass right after the kernel that wrote the
 // tensor starts with its most recently written lines, still in the
 // memory-side cache.
-template <int KIND, int DT, bool AUX = false, int NSET = 2, bool REV = false, typename F>
+// RAWCB: fp receives the packet's raw bytes (Raw<KIND, DT>) instead of its
+// values.
+template <int KIND, int DT, bool AUX = false, int NSET = 2, bool REV = false, bool RAWCB = false,
+          typename F>
 __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVals<Pack<KIND, DT>::V>& t,
                                       F&& fp, const int8_t* aux = nullptr) {
   // AUX: one byte per value of `aux`, loaded with each packet and handed to
@@ -171,9 +174,13 @@ __device__ inline void stream_packets(const SrcDev& s, int64_t n, const ThreadVa
     for (int p = 0; p < PK::P; ++p) {
       const int64_t i = pk_index<PK::EP>(base, p);
       if (i < nfull) {
-        double v[PK::EP];
-        unpack<KIND, DT>(r[p], t, p, v);
-        fp(v, i, x[p]);
+        if constexpr (RAWCB) {
+          fp(r[p], i, x[p]);
+        } else {
+          double v[PK::EP];
+          unpack<KIND, DT>(r[p], t, p, v);
+          fp(v, i, x[p]);
+        }
       }
     }
   };
