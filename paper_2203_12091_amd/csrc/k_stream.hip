@@ -489,13 +489,19 @@ __global__ __launch_bounds__(kThreads) void k_requant_addmm(SrcDev s, int64_t n,
   }
 }
 
+// The gated launch after a fused FxP-QLayer usually finds its codes written
+// and does nothing: a grid of at most kGatedBlocks keeps that launch short
+// (a real requantization then loops more per thread).
+constexpr int kGatedBlocks = 256;
+
 template <int OUT>
 static void requant_out(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
                         void* codes, const FlsPlan* gate = nullptr, const int8_t* alt = nullptr) {
   int blocks = 1;
+  const int cap = gate ? kGatedBlocks : 0;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,
                     (blocks = stream_grid(n, src_channels(s), 0, src_vec(s),
-                                          resident_blocks(c, (const void*)&k_requant<K_, D_, OUT>)),
+                                          cap ? cap : resident_blocks(c, (const void*)&k_requant<K_, D_, OUT>)),
                      k_requant<K_, D_, OUT><<<blocks, kThreads, 0, c.stream>>>(s, n, fmt, codes,
                                                                              c.sc.flags, gate, alt)));
 }
