@@ -16,21 +16,27 @@ teacher), and keep the smallest cost
 a direction continues K steps past its last improvement.
 
 The same readings as the GPU driver: activations are layer outputs, the
-input image is the first data structure; L is the parameter quantization
-error for the current layer (zero for FP32 layers) and the distance from the
-teacher's activation for activations; pi = sigma * size normalized over a
-layer's data structures (sigma over the whole tensor); R = max - min of the
-FP32 data structure; eltwise / avg-pool FxP-QLayers keep their Eq. 14
-searches, Scale parameters their searched formats.  Any of the workloads'
-networks; the FP32 FC sums the flattened input channel-major, the GPU's
-order whenever the FC input is 1x1 spatially (the ResNets, and AlexNet /
-VGG-16 on the small images of the parity tests).
+input image is the first data structure; a C-Block's data structures are
+its output activations, its conv / FC weights and bias, and its Scale
+parameters aleph_1 / aleph_2 (Eq. 4-5), optimized in the order w, b,
+aleph_1, aleph_2, a; L is the parameter quantization error for the current
+layer (zero for FP32 layers) and the distance from the teacher's activation
+for activations; pi = sigma * nu normalized over a layer's data structures
+(Eq. 15), where for activations sigma is the population standard deviation
+of each calibration sample averaged over the samples and nu is the size of
+one sample, and for parameters both are taken over the tensor (Eq. 16); R =
+max - min of the FP32 data structure over the whole batch (Eq. 18);
+eltwise / avg-pool FxP-QLayers keep their Eq. 14 searches.  Any of the
+workloads' networks; the FP32 FC sums the flattened input channel-major, the
+GPU's order whenever the FC input is 1x1 spatially (the ResNets, and AlexNet
+/ VGG-16 on the small images of the parity tests).
 
-parity unpinned for the network cost F as composed (no printed example
-exists); its parts are pinned (tests/test_oracle_preprocess.py,
-tests/test_oracle_pins.py, tests/test_oracle_teacher.py), and the search rule
-on hand-worked cost curves and against brute force
-(tests/test_oracle_qparams.py).
+The statistics, pi and E (Eq. 15-17) are pinned on a hand-worked two-sample
+layer (tests/golden/importance_pi.txt); the search rule on hand-worked cost
+curves and against brute force (tests/test_oracle_qparams.py).  parity
+unpinned for the network cost F as composed over a network (no printed
+example exists): its parts are pinned (tests/test_oracle_preprocess.py,
+tests/test_oracle_pins.py, tests/test_oracle_teacher.py and the above).
 """
 import math
 
@@ -45,6 +51,12 @@ from .nets import FL, SEED, alexnet, resnet, vgg16
 BUILD = {"alexnet": alexnet, "vgg16": vgg16, "resnet18": lambda g: resnet(g, False),
          "resnet50": lambda g: resnet(g, True)}
 from .sweep import Teacher
+
+# The Scale parameters of a C-Block (Eq. 4-5) as data structures: s1 is the
+# multiplier aleph_1 (16 bits, the C-Block's 16-bit multiplier), s2 the
+# offset aleph_2 (32 bits); both learnable parameters outside G1 (Eq. 22).
+PARAM = {"s1": "a1", "s2": "a2"}
+SCALE_WL = {"s1": 16, "s2": 32}
 
 
 class Graph(Teacher):
@@ -78,9 +90,35 @@ class Graph(Teacher):
         self.nodes.append(("avgpool", name, {"src": src}))
 
 
-def _stats(x):
-    x = np.asarray(x, np.float64).ravel()
-    return float(x.std()), x.size, float(x.max() - x.min())
+def _stats(x, per_sample=False):
+    """(sigma, nu, R) of one data structure.  Eq. 16: sigma is the population
+    standard deviation about the arithmetic mean and nu the size; for
+    activations (per_sample, x holding the calibration samples along its
+    first axis) sigma is taken per sample and averaged over the samples,
+    and nu is the size of one sample (Eq. 15-16 and the text after them).
+    Eq. 18: R = largest minus smallest FP32 value of the whole data
+    structure."""
+    x = np.asarray(x, np.float64)
+    flat = x.ravel()
+    rng = float(flat.max() - flat.min())
+    if per_sample:
+        per = x.reshape(x.shape[0], -1)
+        sig = [float(np.sqrt(np.mean((r - r.mean()) ** 2))) for r in per]
+        return float(np.mean(sig)), per.shape[1], rng
+    return float(np.sqrt(np.mean((flat - flat.mean()) ** 2))), flat.size, rng
+
+
+def importance(stats):
+    """Eq. 15: pi of each data structure of one layer, sigma * nu normalized
+    so that the layer's values sum to one.  stats: {key: (sigma, nu, R)}."""
+    tot = sum(sg * nu for sg, nu, _ in stats.values())
+    return {k: (sg * nu / tot if tot > 0 else 0.0) for k, (sg, nu, _) in stats.items()}
+
+
+def distillation_error(pi, stat, errs):
+    """Eq. 17: sum of pi * L / R over the data structures with an error
+    (errs: {key: L}); a data structure with R = 0 (constant) adds nothing."""
+    return sum(pi[k] * e / stat[k][2] for k, e in errs.items() if k in pi and stat[k][2] > 0)
 
 
 def _sse(ref, y):
@@ -116,12 +154,17 @@ class ForwardOptimizer:
         convs = [nm for op, nm, _ in g.nodes if op == "conv"]
         self.edge = (convs[0], convs[-1])
         self.spec = {nm: sp for op, nm, sp in g.nodes if op == "conv"}
+        # per C-Block: weights, bias, Scale multiplier (s1 = aleph_1) and
+        # offset (s2 = aleph_2), in the order the C-Block applies them, then
+        # the output activations (none for the last layer)
         self.order = [("input", "a")]
         for op, nm, sp in g.nodes:
             if op == "conv":
                 self.order.append((nm, "w"))
                 if "b" in sp:
                     self.order.append((nm, "b"))
+                if "a1" in sp:
+                    self.order += [(nm, "s1"), (nm, "s2")]
                 if not sp["last"]:
                     self.order.append((nm, "a"))
         self.qp, self.stat = {}, {}
@@ -131,21 +174,11 @@ class ForwardOptimizer:
             xmin, xmax = pre.exact_extremes_f32(x)
             fl, sign = pre.init_fl(xmin, xmax, wl, strategy, pre.PSI_PRINTED, *FL)
             self.qp[(ln, d)] = [wl, fl, sign]
-            self.stat[(ln, d)] = _stats(x)
+            self.stat[(ln, d)] = _stats(x, per_sample=(d == "a"))
+        # Eq. 15, normalized over each layer's data structures
         self.pi = {}
         for ln in ["input"] + list(self.spec):
-            ds = [d for d in ("a", "w", "b") if (ln, d) in self.stat]
-            tot = sum(self.stat[(ln, d)][0] * self.stat[(ln, d)][1] for d in ds)
-            for d in ds:
-                self.pi[(ln, d)] = self.stat[(ln, d)][0] * self.stat[(ln, d)][1] / tot if tot > 0 else 0.0
-        # Scale parameters: searched formats, fixed
-        self.scale = {}
-        for ln, sp in self.spec.items():
-            if "a1" in sp:
-                f1, s1, _ = orc.fl_search_f32(sp["a1"], 16, orc.SIGN_AUTO, *FL)
-                f2, s2, _ = orc.fl_search_f32(sp["a2"], 32, orc.SIGN_AUTO, *FL)
-                self.scale[ln] = (orc.quantize_f32(sp["a1"], 16, f1, s1).astype(np.int64), f1,
-                                  orc.quantize_f32(sp["a2"], 32, f2, s2).astype(np.int64), f2)
+            self.pi.update(importance({k: v for k, v in self.stat.items() if k[0] == ln}))
         self.q = {}  # finalized nodes: (codes, fl, sign) NCHW
         self._pcache = {}
         self.trace = []
@@ -161,6 +194,8 @@ class ForwardOptimizer:
             return sp["w"], self.w_wl or sp["wl"]
         if d == "b":
             return sp["b"], 32
+        if d in PARAM:
+            return sp[PARAM[d]], SCALE_WL[d]
         return self.g.act[ln], 8
 
     # ---- one quantized layer ----
@@ -171,7 +206,7 @@ class ForwardOptimizer:
         hit = self._pcache.get((ln, d))
         if hit is not None and hit[0] == (wl, fl, sign):
             return hit[1], hit[2]
-        x = self.spec[ln][d]
+        x = self.spec[ln][PARAM.get(d, d)]
         c = orc.quantize_f32(x, wl, fl, sign).astype(np.int64)
         e = orc.layer_error(x.ravel(), c.ravel(), wl, fl, sign)[0]
         self._pcache[(ln, d)] = ((wl, fl, sign), c, e)
@@ -200,8 +235,12 @@ class ForwardOptimizer:
             bw, fl_b, sb = self.qp[(ln, "b")]
             bc, errs[(ln, "b")] = self._param(ln, "b")
             b = _dec(bc, bw, sb)
-        if ln in self.scale:
-            a1, fl_a1, a2, fl_a2 = self.scale[ln]
+        if "a1" in sp:
+            w1, fl_a1, g1 = self.qp[(ln, "s1")]
+            c1, errs[(ln, "s1")] = self._param(ln, "s1")
+            w2, fl_a2, g2 = self.qp[(ln, "s2")]
+            c2, errs[(ln, "s2")] = self._param(ln, "s2")
+            a1, a2 = _dec(c1, w1, g1), _dec(c2, w2, g2)
         if sp["fc"]:
             acc = orc.gemm(x.reshape(x.shape[0], -1), wq)
         else:
@@ -267,8 +306,7 @@ class ForwardOptimizer:
             fp[nm] = y
         scores = logits if logits is not None else fp[self.last]
         un, extra = _ties(np.asarray(scores).reshape(self.B, -1))
-        E = sum(self.pi[k] * e / self.stat[k][2] for k, e in errs.items()
-                if k in self.pi and self.stat[k][2] > 0)
+        E = distillation_error(self.pi, self.stat, errs)
         C = int(np.asarray(scores).reshape(self.B, -1).shape[1])
         return E + un / self.B + extra / (self.B * C)
 
@@ -373,8 +411,7 @@ class ForwardOptimizer:
                 cur[nm] = self._node_q(op, sp, cur)
         scores = np.asarray(cur[self.last][0]).reshape(self.B, -1)
         un, extra = _ties(scores)
-        E = sum(self.pi[k] * e / self.stat[k][2] for k, e in errs.items()
-                if k in self.pi and self.stat[k][2] > 0)
+        E = distillation_error(self.pi, self.stat, errs)
         cost = E + un / self.B + extra / (self.B * scores.shape[1])
         return cost, self.top1(scores)
 
@@ -385,7 +422,7 @@ class ForwardOptimizer:
                 layers.append(ln)
         keys = set(self.order)
         for ln in layers:
-            for d in ("w", "b", "a"):
+            for d in ("w", "b", "s1", "s2", "a"):
                 if (ln, d) in keys:
                     self.qparams_opt(ln, d)
             self.finalize(ln)

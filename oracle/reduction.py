@@ -3,8 +3,8 @@ and of the memory model (Eq. 26-30) -- TEST INFRASTRUCTURE ONLY.
 
 Sec. "Bit-Precision Level Reduction": the data structures of a quantized
 network are clustered (Eq. 22: G1 = activations and conv / FC weights, G2 =
-the other learnable parameters; Eq. 23: within each, one sub-cluster per
-distinct size, larger sizes first).  The traversal visits G1's sub-clusters
+the other learnable parameters, i.e. biases and Scale parameters; Eq. 23:
+within each, one sub-cluster per distinct size, larger sizes first).  The traversal visits G1's sub-clusters
 in order; in a sub-cluster, every data structure competes (Reduce): it tries
 word length k - theta with its fractional length lowered by theta (the
 integer length stays), re-optimizes the fractional length with Algorithm 1
@@ -14,15 +14,16 @@ candidates).  A trial is valid when the accuracy drop is at most
 phi * threshold, phi = lambda + (1 - lambda) * theta * size / (sum of the
 sizes of that type), lambda = 0 on the first visit of G1 and 1 afterwards
 (Eq. 24); G2 gets threshold 0.  The best valid candidate (largest theta,
-then smallest drop, then deepest layer, then w / a / b) is applied and the
+then smallest drop, then deepest layer, then type) is applied and the
 sub-cluster is visited again; a data structure that reaches 1 bit leaves its
 sub-cluster.  The traversal alternates between G1 and G2 until an episode
 changes nothing.
 
 Readings (the GPU driver takes the same):
   * the network is the forward optimizer's result (Algorithm 1 on every data
-    structure) from 8-bit weights and activations and 32-bit biases; Scale
-    parameters keep their formats (not in G2);
+    structure) from 8-bit weights and activations, 32-bit biases and the
+    Scale parameters at 16 (multiplier aleph_1) and 32 (offset aleph_2)
+    bits; the Scale parameters are G2 members like the biases (Eq. 22);
   * accuracy without labels is the top-1 agreement with the FP32 teacher on
     the calibration batch, so the FP32 accuracy is 1;
   * a trial's Algorithm 1 runs the whole network quantized (the prefix at
@@ -38,7 +39,9 @@ Readings (the GPU driver takes the same):
     has no zero;
   * sizes are per image for activations (C x H x W, the input's three
     channels), the model's counts for parameters; the sums in phi run over
-    the data structures of that type taking part (G1 / G2 members).
+    the data structures of that type taking part (G1 / G2 members), the
+    Scale multipliers and offsets each forming a type of their own;
+  * select()'s last tie rule orders w / a / b / aleph_1 / aleph_2.
 
 parity unpinned for the composed run over a network (the paper prints
 none); the Reduce / select / traversal rules are pinned on stub accuracy
@@ -49,8 +52,20 @@ ResNet-18's parameter count, the composed run by invariants
 import math
 
 from .nets import FL
+from .qparams import PARAM
 
-TYPE_ORDER = {"w": 0, "a": 1, "b": 2}
+# tie order of select(): conv / FC weights, activations, bias, then the Scale
+# multiplier and offset
+TYPE_ORDER = {"w": 0, "a": 1, "b": 2, "s1": 3, "s2": 4}
+
+
+def level1(order):
+    """Eq. 22: (G1, G2) of the data structures in network order: G1 holds
+    every activation and the conv / FC weights, G2 every other learnable
+    parameter (biases, Scale multipliers and offsets)."""
+    G1 = [k for k in order if k[1] in ("a", "w")]
+    G2 = [k for k in order if k[1] not in ("a", "w")]
+    return G1, G2
 
 
 def level2(G, nu):
@@ -76,12 +91,11 @@ class QReduction:
             elif d == "a":
                 self.nu[(ln, d)] = int(g.act[ln][0].size)
             else:
-                self.nu[(ln, d)] = int(fo.spec[ln][d].size)
+                self.nu[(ln, d)] = int(fo.spec[ln][PARAM.get(d, d)].size)
         first = [nm for op, nm, _ in g.nodes if op == "conv"][0]
         self.floor = {("input", "a"): 2, (first, "w"): 2}
-        G1 = [k for k in fo.order if k[1] in ("a", "w")]
-        G2 = [k for k in fo.order if k[1] == "b"]
-        self.nu_sum = {d: sum(v for k, v in self.nu.items() if k[1] == d) for d in ("a", "w", "b")}
+        G1, G2 = level1(fo.order)
+        self.nu_sum = {d: sum(v for k, v in self.nu.items() if k[1] == d) for d in TYPE_ORDER}
         self.clusters = {1: level2(G1, self.nu), 2: level2(G2, self.nu)}
         self.acc_fp32 = 1.0
         self.trials = []   # (ln, d, theta, fl_start, fl_chosen, acc, valid)
@@ -215,7 +229,7 @@ def memory_model(fo, formats=None):
     given formats, and the compression rates of Eq. 29-30.  Activations of
     the output layer stay at 32 bits; max-pool outputs keep their input's
     word length; eltwise / avg-pool outputs have their 8-bit FxP-QLayers;
-    Scale parameters count at 16 (multiplier) and 32 (offset) bits."""
+    Scale parameters count at their formats' word lengths."""
     qp = fo.qp if formats is None else formats
     g = fo.g
     nu, k, layers = {}, {}, []
@@ -233,8 +247,8 @@ def memory_model(fo, formats=None):
                     nu[(nm, d)], k[(nm, d)] = int(sp[d].size), qp[(nm, d)][0]
                     params.append((nm, d))
             if "a1" in sp:
-                for d, wl in (("a1", 16), ("a2", 32)):
-                    nu[(nm, d)], k[(nm, d)] = int(sp[d].size), wl
+                for d in ("s1", "s2"):
+                    nu[(nm, d)], k[(nm, d)] = int(sp[PARAM[d]].size), qp[(nm, d)][0]
                     params.append((nm, d))
         elif op == "maxpool":
             ins = [sp["src"]]

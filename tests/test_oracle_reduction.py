@@ -35,9 +35,8 @@ class Stub(R.QReduction):
         for u, _, _ in members:
             self.layer_id.setdefault(u[0], len(self.layer_id))
         self.floor = floor or {}
-        G1 = [u for u, _, _ in members if u[1] in ("a", "w")]
-        G2 = [u for u, _, _ in members if u[1] == "b"]
-        self.nu_sum = {d: sum(v for k, v in self.nu.items() if k[1] == d) for d in ("a", "w", "b")}
+        G1, G2 = R.level1([u for u, _, _ in members])
+        self.nu_sum = {d: sum(v for k, v in self.nu.items() if k[1] == d) for d in R.TYPE_ORDER}
         self.clusters = {1: R.level2(G1, self.nu), 2: R.level2(G2, self.nu)}
         self.acc_fp32 = 1.0
         self.trials, self.changes, self.calls = [], [], []
@@ -52,6 +51,16 @@ class Stub(R.QReduction):
 
 
 A, B, C = ("l2", "w"), ("l1", "a"), ("l3", "b")
+
+
+def test_level1_clusters():
+    """Eq. 22 worked by hand: activations and conv / FC weights in G1; the
+    bias and both Scale parameters (multiplier, offset) in G2."""
+    order = [("input", "a"), ("c1", "w"), ("c1", "s1"), ("c1", "s2"), ("c1", "a"),
+             ("fc", "w"), ("fc", "b")]
+    G1, G2 = R.level1(order)
+    assert G1 == [("input", "a"), ("c1", "w"), ("c1", "a"), ("fc", "w")]
+    assert G2 == [("c1", "s1"), ("c1", "s2"), ("fc", "b")]
 
 
 def test_level2_clusters():
@@ -201,3 +210,21 @@ def test_composed_run_invariants(tiny):
     seen = [c for (l2, d2, f2, c) in fo.trace if (l2, d2, f2) == (ln, d, fl)]
     assert cost in seen and acc == 1.0 - drop
     assert tuple(fo.qp[(ln, d)][:2]) == (wl, fl)
+
+
+def test_scale_parameters_reduced_in_g2(tiny):
+    """A G2 visit reduces Scale parameters (Eq. 22): with G1 left out, the
+    first change comes from G2's largest sub-cluster (the FC bias, 1000
+    values, then the 512-channel Scale parameters), at zero accuracy drop."""
+    import copy
+    fo = copy.deepcopy(tiny)
+    r = R.QReduction(fo, 0.5, max_changes=3)
+    scale = [u for u in fo.order if u[1] in ("s1", "s2")]
+    assert scale and all(any(u in c for c in r.clusters[2]) for u in scale)
+    assert not any(u in c for c in r.clusters[1] for u in scale)
+    r.clusters[1] = []
+    r.run()
+    assert r.changes and all(d in ("b", "s1", "s2") and drop <= 0 for _, d, _, _, _, drop in r.changes)
+    assert any(d in ("s1", "s2") for _, d, _, _, _, _ in r.changes)
+    for ln, d, theta, wl, fl, drop in r.changes:
+        assert tuple(fo.qp[(ln, d)][:2]) == (wl, fl)
