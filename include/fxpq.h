@@ -170,7 +170,8 @@ fxpq_status fxpq_sync_status(fxpq_handle h, uint32_t* flags);
  * Word lengths 1..32.  A signed 1-bit format follows Eq. 13 (code -1 for
  * x < 0, code 0 otherwise, decoded as +1) and is stored decoded: -1 or +1,
  * so that a C-Block consumes it as it is; the same holds for every call that
- * writes codes.
+ * writes codes.  A NaN or Inf in x has no code: it raises the sticky
+ * FXPQ_FLAG_NONFINITE (read by fxpq_sync_status) and its code is unspecified.
  */
 fxpq_status fxpq_quantize(fxpq_handle h, const float* x, int64_t n, const fxpq_fmt* d_fmt,
                           void* codes, fxpq_dtype code_type);

@@ -236,14 +236,27 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
   ThreadVals<PK::V> t;
   thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, t);
   const int64_t nfull = n - n % PK::EP;
+  // fp32 sources (quantize, Eq. 10): NaN / Inf has no code; it raises the
+  // sticky non-finite flag (its code is unspecified)
+  bool bad = false;
   stream_packets<KIND, DT>(s, n, t, [&](const double* v, int64_t i0, int) {
     int c[PK::EP];
 #pragma unroll
-    for (int j = 0; j < PK::EP; ++j) c[j] = quant_one(v[j], q);
+    for (int j = 0; j < PK::EP; ++j) {
+      if constexpr (KIND == FXPQ_SRC_F32) bad |= !isfinite(v[j]);
+      c[j] = quant_one(v[j], q);
+    }
     storev<OUT, PK::EP>(codes, i0, c);
   });
   if (gtid == 0) {
-    for (int64_t i = nfull; i < n; ++i) store1<OUT>(codes, i, quant_one(load1<KIND, DT>(s, i), q));
+    for (int64_t i = nfull; i < n; ++i) {
+      const double v = load1<KIND, DT>(s, i);
+      if constexpr (KIND == FXPQ_SRC_F32) bad |= !isfinite(v);
+      store1<OUT>(codes, i, quant_one(v, q));
+    }
+  }
+  if constexpr (KIND == FXPQ_SRC_F32) {
+    if (bad) raise_flag(flags, FXPQ_FLAG_NONFINITE);
   }
 }
 

@@ -24,11 +24,16 @@ activation from the FP32 teacher's (post-training self-distillation), and
 UnClass / MisPred from ties of the final scores (Eq. 19-20).
 
 Readings: activations are the layers' outputs (the input image is the first
-data structure, optimized before layer 1); eltwise and avg-pool FxP-QLayers
-keep their Eq. 14 searches; BN-as-Scale parameters keep their word lengths
-and searched formats; sigma of an activation is taken over the whole batch
-tensor; accuracy has no labels here, so the report is the agreement of the
-quantized network's top-1 with the FP32 teacher's.
+data structure, optimized before layer 1); a C-Block's data structures are
+its output activations, its conv / FC weights and bias, and its Scale
+parameters aleph_1 (multiplier, 16 bits) and aleph_2 (offset, 32 bits) of
+Eq. 4-5, optimized in the order w, b, aleph_1, aleph_2, a; pi is normalized
+over a layer's data structures; for activations sigma is the population
+standard deviation of each calibration sample, averaged over the samples,
+and the size nu is that of one sample (parameters: over the tensor);
+eltwise and avg-pool FxP-QLayers keep their Eq. 14 searches; accuracy has no
+labels here, so the report is the agreement of the quantized network's
+top-1 with the FP32 teacher's.
 
 Every tensor operation is a libfxpq call; the host only sequences the
 candidates and adds up the per-tensor error sums the library returns.
@@ -37,7 +42,11 @@ import numpy as np
 
 from . import fxpq as fx
 from .nets import A_WL, BIAS_WL, FL_HI, FL_LO, RECIP_WL
-from .sweep import Sweep
+from .sweep import SCALE_WL, SHIFT_WL, Sweep
+
+# Scale parameters of a C-Block as data structures (Eq. 4-5): s1 = aleph_1,
+# s2 = aleph_2 (FP32 tensor key of the layer, initial word length)
+SCALE = {"s1": ("a1_f32", SCALE_WL), "s2": ("a2_f32", SHIFT_WL)}
 
 
 class ForwardOptimizer:
@@ -60,13 +69,16 @@ class ForwardOptimizer:
         self.held = {}  # per layer: the ctypes structures its last calls used
         self.evals = 0
         # data structures in optimization order: the input, then per layer
-        # weights, bias, output activations (none for the last layer)
+        # weights, bias, Scale multiplier and offset, output activations
+        # (none for the last layer)
         self.order = [("input", "a")]
         for n in self.nodes:
             if n.op in ("conv", "fc"):
                 self.order.append((n.name, "w"))
                 if n.bias:
                     self.order.append((n.name, "b"))
+                if "a1_f32" in self.L[n.name]:
+                    self.order += [(n.name, "s1"), (n.name, "s2")]
                 if not n.last:
                     self.order.append((n.name, "a"))
         # per-tensor statistics and initial formats
@@ -82,16 +94,24 @@ class ForwardOptimizer:
             fx.layer_error(self.h, real, real, fx.F32, None, real.numel(), out4)
             f, e = fmt.cpu().numpy(), out4.cpu().numpy()
             self.fmt[(ln, d)], self.qp[(ln, d)] = fmt, [int(f[0]), int(f[1]), int(f[2])]
-            self.stat[(ln, d)] = (float(e[3]), real.numel(), float(e[2] - e[1]))
+            sigma, nu = float(e[3]), real.numel()
+            if d == "a":
+                # Eq. 16 for activations: sigma per calibration sample,
+                # averaged; nu = the size of one sample
+                per = real.reshape(self.B, -1)
+                sig = []
+                for i in range(self.B):
+                    fx.layer_error(self.h, per[i], per[i], fx.F32, None, per.shape[1], out4)
+                    sig.append(float(out4[3].item()))
+                sigma, nu = float(np.mean(sig)), per.shape[1]
+            self.stat[(ln, d)] = (sigma, nu, float(e[2] - e[1]))
+        # Eq. 15, normalized over each layer's data structures
         self.pi = {}
-        for n in [None] + self.nodes:
-            ln = "input" if n is None else n.name
-            if n is not None and n.op not in ("conv", "fc"):
-                continue
-            ds = [d for d in ("a", "w", "b") if (ln, d) in self.stat]
-            tot = sum(self.stat[(ln, d)][0] * self.stat[(ln, d)][1] for d in ds)
-            for d in ds:
-                self.pi[(ln, d)] = self.stat[(ln, d)][0] * self.stat[(ln, d)][1] / tot if tot > 0 else 0.0
+        for ln in {k[0] for k in self.stat}:
+            ks = [k for k in self.stat if k[0] == ln]
+            tot = sum(self.stat[k][0] * self.stat[k][1] for k in ks)
+            for k in ks:
+                self.pi[k] = self.stat[k][0] * self.stat[k][1] / tot if tot > 0 else 0.0
         # quantized prefix: codes and formats of finalized nodes
         self.qcodes, self.qfmt, self.deq = {}, {}, {}
         self.pos = {n.name: i for i, n in enumerate(self.nodes)}
@@ -144,6 +164,8 @@ class ForwardOptimizer:
             return L["w_krsc"], self.w_wl or L["node"].wl
         if d == "b":
             return L["b_f32"], BIAS_WL
+        if d in SCALE:
+            return L[SCALE[d][0]], SCALE[d][1]
         return L["y_ref"], A_WL
 
     def _real(self, ln, d):
@@ -174,7 +196,7 @@ class ForwardOptimizer:
         e = self._buf((ln, d, "err"), (4,), self.T.float64)
         fq = tuple(self.qp[key])
         if self.pfmt.get((key, ctype)) != fq:
-            x = L["w_krsc"] if d == "w" else L["b_f32"]
+            x = L["w_krsc"] if d == "w" else L[SCALE[d][0]] if d in SCALE else L["b_f32"]
             fx.quantize(self.h, x, x.numel(), self.fmt[key], codes, ctype)
             if d == "w" and ctype == fx.I8:
                 fx.weight_colsum(self.h, codes, L["node"].cout, L["wlen"], self._buf((ln, "colsum"), (L["node"].cout,), self.T.int32))
@@ -212,9 +234,13 @@ class ForwardOptimizer:
             bcodes = self._buf((ln, "bcodes"), (n.cout,), T.int32)
             self._param(ln, "b", bcodes, fx.I32, errs)
             kw.update(bias=bcodes, fl_bias=self.qp[(ln, "b")][1])
-        if "a1" in L:
-            kw.update(scale=L["a1"], fl_scale=L["fl"][("a1", None)][1], shift=L["a2"],
-                      fl_shift=L["fl"][("a2", None)][1])
+        if "a1_f32" in L:
+            c1 = self._buf((ln, "s1codes"), (n.cout,), T.int32)
+            c2 = self._buf((ln, "s2codes"), (n.cout,), T.int32)
+            self._param(ln, "s1", c1, fx.I32, errs)
+            self._param(ln, "s2", c2, fx.I32, errs)
+            kw.update(scale=c1, fl_scale=self.qp[(ln, "s1")][1], shift=c2,
+                      fl_shift=self.qp[(ln, "s2")][1])
         xin = qcodes[n.inp]
         ep = fx.epilogue(n.cout, self.qp[(ln, "w")][1], qfmt[n.inp], relu=n.relu, **kw)
         if wide:
@@ -473,7 +499,7 @@ class ForwardOptimizer:
             if ln not in layers:
                 layers.append(ln)
         for ln in layers:
-            for d in ("w", "b", "a"):
+            for d in ("w", "b", "s1", "s2", "a"):
                 if (ln, d) in self.qp and (ln, d) in dict.fromkeys(self.order):
                     self.qparams_opt(ln, d)
             self.finalize(ln)

@@ -3,8 +3,9 @@ model (Eq. 26-30) over the GPU forward optimizer.
 
 Sec. "Bit-Precision Level Reduction": the data structures of the quantized
 network are clustered (Eq. 22: G1 holds the activations and the conv / FC
-weights, G2 the other learnable parameters; Eq. 23: one sub-cluster per
-distinct size, larger first).  Sub-clusters are visited in order; inside one,
+weights, G2 the other learnable parameters, i.e. biases and the Scale
+multipliers and offsets; Eq. 23: one sub-cluster per distinct size, larger
+first).  Sub-clusters are visited in order; inside one,
 every member tries a lower word length k - theta (fractional length lowered
 by theta, integer length kept), re-optimized by Algorithm 1 with the whole
 network quantized, and is scored by its accuracy drop.  theta is 1 for
@@ -14,18 +15,20 @@ at most phi * threshold with phi = lambda + (1 - lambda) * theta * size /
 (sum of the sizes of its type) (Eq. 24; lambda = 0 only on the first visit
 of G1, and G2 gets threshold 0).  Of the valid trials the one with the
 largest theta, then the smallest drop, then the deepest layer, then type
-w / a / b is applied; the sub-cluster is visited again until nothing
-changes, and the traversal alternates between G1 and G2 until an episode
+(w / a / b / aleph_1 / aleph_2) is applied; the sub-cluster is visited again
+until nothing changes, and the traversal alternates between G1 and G2 until an episode
 changes nothing.
 
 Readings: the network is the forward optimizer's result from 8-bit weights
-and activations and 32-bit biases, Scale parameters keep their formats;
-accuracy is the top-1 agreement with the FP32 teacher on the calibration
+and activations, 32-bit biases and the Scale parameters at 16 (aleph_1) and
+32 (aleph_2) bits; accuracy is the top-1 agreement with the FP32 teacher on the calibration
 batch (no labels), so the FP32 accuracy is 1; a trial whose lowered
 fractional length falls below the format range is not valid; hill climbing
 tries theta = 2 only where k - 2 is allowed; the input and the first layer's
 weights stop at 2 bits (the RGB input is padded to four channels with zeros,
-which a 1-bit code cannot hold); sizes are per image for activations.
+which a 1-bit code cannot hold); sizes are per image for activations; the
+sums in phi run over the data structures of the same type, the Scale
+multipliers and offsets each forming a type of their own.
 
 Every evaluation is a sequence of libfxpq calls; the host only keeps the
 clusters, compares accuracies and ranks the candidates.
@@ -34,7 +37,14 @@ import math
 
 from .nets import FL_LO
 
-TYPE_ORDER = {"w": 0, "a": 1, "b": 2}
+TYPE_ORDER = {"w": 0, "a": 1, "b": 2, "s1": 3, "s2": 4}
+
+
+def level1(order):
+    """Eq. 22: (G1, G2) in network order; G1 = activations and conv / FC
+    weights, G2 = every other learnable parameter."""
+    return ([u for u in order if u[1] in ("a", "w")],
+            [u for u in order if u[1] not in ("a", "w")])
 
 
 def sub_clusters(G, nu):
@@ -65,9 +75,8 @@ class QReduction:
             else:
                 self.nu[(ln, d)] = fo.L[ln]["node"].cout
         self.floor = {("input", "a"): 2, (convs[0].name, "w"): 2}
-        G1 = [u for u in fo.order if u[1] in ("a", "w")]
-        G2 = [u for u in fo.order if u[1] == "b"]
-        self.type_size = {t: sum(v for u, v in self.nu.items() if u[1] == t) for t in "awb"}
+        G1, G2 = level1(fo.order)
+        self.type_size = {t: sum(v for u, v in self.nu.items() if u[1] == t) for t in TYPE_ORDER}
         self.clusters = {1: sub_clusters(G1, self.nu), 2: sub_clusters(G2, self.nu)}
         self.acc_fp32 = 1.0
         self.trials = []   # (layer, d, theta, fl start, fl chosen, accuracy, valid)
@@ -176,7 +185,7 @@ def memory_model(fo):
     and at the current formats of fo, and the compression rates (Eq. 29-30).
     Output-layer activations stay at 32 bits, max-pool outputs keep their
     input's word length, eltwise / avg-pool outputs are 8-bit FxP-QLayers,
-    Scale parameters count at 16 (multiplier) and 32 (offset) bits."""
+    Scale parameters count at their formats' word lengths."""
     size, bits, steps, params = {}, {}, [], []
     _, H, W, _ = fo.act["input"].shape
     size["input"], bits["input"] = 3 * H * W, fo.qp[("input", "a")][0]
@@ -194,8 +203,8 @@ def memory_model(fo):
                 size[(n.name, "b")], bits[(n.name, "b")] = n.cout, fo.qp[(n.name, "b")][0]
                 params.append((n.name, "b"))
             if "a1_f32" in L:
-                for d, b in (("a1", 16), ("a2", 32)):
-                    size[(n.name, d)], bits[(n.name, d)] = n.cout, b
+                for d in ("s1", "s2"):
+                    size[(n.name, d)], bits[(n.name, d)] = n.cout, fo.qp[(n.name, d)][0]
                     params.append((n.name, d))
         elif n.op == "maxpool":
             bits[n.name] = bits[n.inp]

@@ -87,6 +87,30 @@ def test_quantize_codes_bit_exact(fx, h, orc, n):
     check_flags(fx, h)
 
 
+def test_quantize_non_finite_raises_flag(fx, h, orc):
+    """NaN / Inf in an fp32 input has no code (the oracle rejects it): the
+    sticky non-finite flag is raised, the finite values' codes stay exact,
+    and the flag is cleared by the read (the next clean call has none)."""
+    import torch
+    n = 100_003
+    x = adversarial_f32(11, n)
+    bad = {7: np.nan, 4096: np.inf, n - 1: -np.inf}
+    for i, v in bad.items():
+        x[i] = v
+    ok = np.ones(n, bool)
+    ok[list(bad)] = False
+    for (k, fl, sign, ct, dt) in [(8, 4, 1, fx.I8, torch.int8), (16, 10, 1, fx.I16, torch.int16)]:
+        note("quantize non-finite", k, fl, sign, ct)
+        codes = empty((n,), dt)
+        fx.quantize(h, dev(x), n, fmt_dev(k, fl, sign), codes, ct)
+        assert fx.sync_status(h) & fx.FLAG_NONFINITE
+        got = host(codes).astype(np.int64)[ok]
+        assert np.array_equal(got, orc.quantize_f32(x[ok], k, fl, sign))
+    clean = empty((n,), torch.int8)
+    fx.quantize(h, dev(np.where(ok, x, 0).astype(np.float32)), n, fmt_dev(8, 4, 1), clean, fx.I8)
+    check_flags(fx, h)
+
+
 def test_requant_int_sources_bit_exact(fx, h, orc):
     import torch
     g = synth.rng_for(7, "req")

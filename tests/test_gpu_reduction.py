@@ -6,7 +6,8 @@ Bit-exact: every trial (data structure, theta, fractional lengths, accuracy,
 validity), every applied change, every candidate of Algorithm 1 inside the
 trials, and the memory model; costs agree to a relative 1e-9 (fp64 sums in
 different orders).  The run is capped at three changes, then the FC bias
-(G2, 32 bits) runs one Reduce with its binary search at threshold 0."""
+(G2, 32 bits) and two Scale parameters of the 512-channel layers (G2, 16 and
+32 bits) run Reduce with its binary search at threshold 0."""
 import pytest
 
 from gpu_util import DEV, note
@@ -64,6 +65,15 @@ def test_reduction_matches_oracle(fx):
     assert sg == sr
     assert rg.trials[t1:] == rr.trials[t1:] and len(rr.trials) - t1 >= 4
     same_trace(fo.trace[n1:], ref.trace[n1:])
+    # G2 holds the Scale parameters too (Eq. 22): the first two members of
+    # the 512-channel sub-cluster (aleph_1 from 16 bits, aleph_2 from 32)
+    sub_r, sub_g = rr.clusters[2][1][:2], rg.clusters[2][1][:2]
+    assert sub_r == sub_g and [d for _, d in sub_r] == ["s1", "s2"]
+    n2, t2 = len(ref.trace), len(rr.trials)
+    note("reduction g2 scale reduce")
+    assert rg.reduce(sub_g, 0.0, 1) == rr.reduce(sub_r, 0.0, 1)
+    assert rg.trials[t2:] == rr.trials[t2:] and len(rr.trials) - t2 >= 6
+    same_trace(fo.trace[n2:], ref.trace[n2:])
     assert fx.sync_status(fo.h) == 0
     fo.close()
 
