@@ -224,6 +224,30 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
                            int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out, double* d_sse);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the search
+ * of fxpq_fl_search without a handle, with the same arguments, requirements
+ * and results (d_fmt_out, and d_sse when not NULL).  It runs on hip_stream
+ * (NULL: the default stream) of the calling thread's current device and
+ * allocates nothing: its scratch is a fixed array of
+ * FXPQ_STATIC_SCRATCH_BYTES in the library's device memory, one copy per
+ * device (devices 0..63), held until the process ends.  The first call on a
+ * device looks up that copy's address (hipGetSymbolAddress).  Every call
+ * clears the parts of the array a search needs at zero with a small kernel
+ * (no memset); calls that overlap on one device race on the array and must
+ * be serialized (e.g. one stream).  There are no sticky flags to read:
+ * non-finite or out-of-range data give d_fmt_out a nonzero status.  Returns
+ * FXPQ_ERR_UNSUPPORTED when the tensor needs more min / max partials than the
+ * array holds (n * sizeof(value) beyond what 16384 blocks stream; never for
+ * resident-capped grids on one MI355X), or more than 2^16 - 4096 window
+ * blocks (the limit of fxpq_fl_search).
+ */
+#define FXPQ_STATIC_SCRATCH_BYTES 1269760
+fxpq_status fxpq_fl_search_static(const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
+                                  int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out,
+                                  double* d_sse, void* hip_stream);
+
+/*
  * FxP-QLayer in one call (Sec. "FxP-QLayer" with the search of Sec.
  * "Quantization Parameters Optimization"): the chosen format in d_fmt_out
  * and the codes are bit for bit those of

@@ -182,6 +182,7 @@ int resident_blocks(const Ctx& c, const void* kernel);
 // Grid of a streaming launch over n values, `vec` per thread per iteration.
 int stream_grid(int64_t n, int channels, int64_t max_per_thread, int vec, int resident);
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out);
+int minmax_blocks(const Ctx& c, const SrcDev& s, int64_t n);
 hipError_t launch_minmax_fin(const Ctx& c, const double* part, int nb, double* out);
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt, void* codes,
                           int code_type);

@@ -4,6 +4,7 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <mutex>
 #include <new>
 
 #include "common.hpp"
@@ -124,6 +125,46 @@ void epi_to_dev(const fxpq_epilogue* e, SrcDev* d) {
 }
 
 }  // namespace
+
+// ---------------------------------------------------------------------------
+// FL search that allocates nothing: its scratch is a fixed array in the
+// library's device memory (one copy per device, held until the process
+// ends), addressed through hipGetSymbolAddress.
+// ---------------------------------------------------------------------------
+namespace {
+
+constexpr size_t a256(size_t v) { return (v + 255) / 256 * 256; }
+constexpr int kStaticMmBlocks = 16384;  // min / max partials the array holds
+constexpr int kStaticDevices = 64;
+// Layout (bytes).  [0, kSoClearEnd) is cleared by every call: the sticky
+// flags, the general pass's block counter and both window slot sets.
+constexpr size_t kSoFlags = 0;
+constexpr size_t kSoMinmax = 256;
+constexpr size_t kSoGenDone = 512;
+constexpr size_t kSoWin = 768;
+constexpr size_t kSoWinF = kSoWin + a256((size_t)2 * kWinSlots * kWinPart * sizeof(long long));
+constexpr size_t kSoClearEnd = kSoWinF + a256((size_t)2 * kWinSlots * kWinPartF * sizeof(double));
+constexpr size_t kSoMmPart = kSoClearEnd;
+constexpr size_t kSoGen = kSoMmPart + a256((size_t)kStaticMmBlocks * 2 * sizeof(double));
+constexpr size_t kSoPlan = kSoGen + a256((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
+constexpr size_t kStaticBytes = kSoPlan + 256;
+static_assert(kStaticBytes == FXPQ_STATIC_SCRATCH_BYTES, "static scratch size in fxpq.h");
+static_assert(kSoClearEnd % sizeof(unsigned) == 0, "cleared in 32-bit words");
+
+struct StaticDev {
+  void* ptr = nullptr;  // device address of `scratch` on this device
+  int cus = 0;
+};
+std::mutex g_static_mu;
+StaticDev g_static[kStaticDevices];
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kStaticBytes];
+
+__global__ __launch_bounds__(256) void k_static_clear(unsigned* p, int words) {
+  for (int i = threadIdx.x; i < words; i += 256) p[i] = 0u;
+}
 
 extern "C" {
 
@@ -291,6 +332,66 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
     hipError_t e = launch_minmax(c, s, n, h->sc.minmax);
     if (e != hipSuccess) return FXPQ_ERR_HIP;
     mm = h->sc.minmax;
+  }
+  return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
+}
+
+fxpq_status fxpq_fl_search_static(const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
+                                  int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out,
+                                  double* d_sse, void* hip_stream) {
+  if (n < 1 || !d_fmt_out) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 1 || wl > 32) return FXPQ_ERR_INVALID_ARG;
+  if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  if (n / ((int64_t)kThreads * kWinMaxPerThread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return FXPQ_ERR_HIP;
+  if (dev >= kStaticDevices) return FXPQ_ERR_UNSUPPORTED;
+  StaticDev sd;
+  {
+    // set-up once per device, with that device current: the array's device
+    // address (the host-side name `scratch` is not one) and its CU count
+    std::lock_guard<std::mutex> lock(g_static_mu);
+    if (!g_static[dev].ptr) {
+      void* ptr = nullptr;
+      int cus = 0;
+      if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return FXPQ_ERR_HIP;
+      if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+          cus < 1)
+        return FXPQ_ERR_HIP;
+      g_static[dev].cus = cus;
+      g_static[dev].ptr = ptr;
+    }
+    sd = g_static[dev];
+  }
+  char* base = static_cast<char*>(sd.ptr);
+  Scratch sc{};
+  sc.flags = reinterpret_cast<unsigned*>(base + kSoFlags);
+  sc.minmax = reinterpret_cast<double*>(base + kSoMinmax);
+  sc.gen_done = reinterpret_cast<unsigned*>(base + kSoGenDone);
+  sc.win_part = reinterpret_cast<long long*>(base + kSoWin);
+  sc.win_part_f = reinterpret_cast<double*>(base + kSoWinF);
+  sc.minmax_part = reinterpret_cast<double*>(base + kSoMmPart);
+  sc.gen_part = reinterpret_cast<unsigned long long*>(base + kSoGen);
+  sc.plan = base + kSoPlan;
+  sc.sink = nullptr;  // not used by the search
+  unsigned seq = 0;   // both slot sets are cleared below: any set will do
+  Ctx c{static_cast<hipStream_t>(hip_stream), sc, nullptr, sd.cus, &seq, FXPQ_TILING_AUTO};
+  if (!src->d_minmax && minmax_blocks(c, s, n) > kStaticMmBlocks) return FXPQ_ERR_UNSUPPORTED;
+  // the array keeps the previous call's contents: zero what a search
+  // expects at zero (a fill kernel, not a memset, so the call can be captured)
+  k_static_clear<<<1, 256, 0, c.stream>>>(reinterpret_cast<unsigned*>(base),
+                                          (int)(kSoClearEnd / sizeof(unsigned)));
+  if (hipGetLastError() != hipSuccess) return FXPQ_ERR_HIP;
+  const double* mm = src->d_minmax;
+  if (!mm) {
+    hipError_t e = launch_minmax(c, s, n, sc.minmax);
+    if (e != hipSuccess) return FXPQ_ERR_HIP;
+    mm = sc.minmax;
   }
   return hip_status(launch_fl_search(c, s, n, wl, sign, fl_lo, fl_hi, mm, d_fmt_out, d_sse));
 }

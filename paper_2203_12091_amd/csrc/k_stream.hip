@@ -431,6 +431,15 @@ static int src_vec(const SrcDev& s) {
   return s.kind == FXPQ_SRC_ADD ? 16 : 4;
 }  // values per thread per block iteration (Pack<>::V)
 
+// Blocks (one min / max partial each) of launch_minmax's first kernel.
+int minmax_blocks(const Ctx& c, const SrcDev& s, int64_t n) {
+  int blocks = 1;
+  FXPQ_DISPATCH_SRC(s.kind, s.dtype,
+                    (blocks = stream_grid(n, src_channels(s), 0, src_vec(s),
+                                          resident_blocks(c, (const void*)&k_minmax<K_, D_>))));
+  return blocks;
+}
+
 hipError_t launch_minmax(const Ctx& c, const SrcDev& s, int64_t n, double* out) {
   int blocks = 1;
   FXPQ_DISPATCH_SRC(s.kind, s.dtype,

@@ -20,7 +20,7 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
-    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
+    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_fl_search_static", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_qconv_wide_workspace", "fxpq_qconv_wide", "fxpq_acc_overflow",
     "fxpq_cblock", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_dequantize", "fxpq_prediction_ties", "fxpq_timer_start",
@@ -84,6 +84,7 @@ def lib():
             "fxpq_requant": [p, p, i64, p, p, C.c_int],
             "fxpq_requant_addmm": [p, p, i64, p, p, C.c_int, p, C.c_int, p, i32, p],
             "fxpq_fl_search": [p, p, i64, i32, i32, i32, i32, p, p],
+            "fxpq_fl_search_static": [p, i64, i32, i32, i32, i32, p, p, p],
             "fxpq_qlayer": [p, p, i64, i32, i32, i32, i32, p, p, C.c_int, p],
             "fxpq_preprocess": [p, p, i64, i32, i32, i32, i32, i32, p],
             "fxpq_qconv": [p, p, p, C.c_int, p, p, p, p, p],
@@ -197,6 +198,14 @@ def requant_addmm(h, src, n, d_fmt, codes, code_type, b, b_type, d_fmt_b, relu, 
 def fl_search(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, d_sse=None):
     _call("fxpq_fl_search", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out),
           ptr(d_sse))
+
+
+def fl_search_static(src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, d_sse=None, stream=None):
+    """fxpq_fl_search_static: no handle, no allocation; stream is a raw HIP
+    stream (int), a torch stream, or None for the default stream."""
+    st = getattr(stream, "cuda_stream", stream)
+    _call("fxpq_fl_search_static", C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out),
+          ptr(d_sse), st)
 
 
 def preprocess(h, src, n, wl, strategy, psi_rule, fl_lo, fl_hi, d_fmt_out):

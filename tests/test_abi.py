@@ -52,6 +52,14 @@ def test_null_handle_and_bad_args_rejected_on_host(fx):
     assert L.fxpq_quantize(None, None, 10, None, None, fx.I8) == fx.ERR_INVALID_ARG
     src = fx.Src(kind=fx.SRC_F32, dtype=fx.F32, x=None)
     assert L.fxpq_fl_search(None, C.byref(src), 10, 8, -1, -8, 15, None, None) == fx.ERR_INVALID_ARG
+    # the no-allocation search: the same host checks, before any device call
+    fmt = C.c_void_p(16)  # never dereferenced: every call below is rejected first
+    assert L.fxpq_fl_search_static(C.byref(src), 10, 8, -1, -8, 15, None, None, None) == fx.ERR_INVALID_ARG
+    assert L.fxpq_fl_search_static(C.byref(src), 0, 8, -1, -8, 15, fmt, None, None) == fx.ERR_INVALID_ARG
+    assert L.fxpq_fl_search_static(C.byref(src), 10, 33, -1, -8, 15, fmt, None, None) == fx.ERR_INVALID_ARG
+    assert L.fxpq_fl_search_static(C.byref(src), 10, 8, 2, -8, 15, fmt, None, None) == fx.ERR_INVALID_ARG
+    assert L.fxpq_fl_search_static(C.byref(src), 10, 8, -1, 15, -8, fmt, None, None) == fx.ERR_INVALID_ARG
+    assert L.fxpq_fl_search_static(None, 10, 8, -1, -8, 15, fmt, None, None) == fx.ERR_INVALID_ARG
     d = fx.ConvDesc(1, 8, 8, 64, 64, 3, 3, 1, 1)
     assert L.fxpq_qconv(None, C.byref(d), None, fx.I8, None, None, None, None, None) == fx.ERR_INVALID_ARG
     assert L.fxpq_cblock(None, C.byref(d), None, fx.I8, None, None, None, 8, -1, -8, 15, None, None,
