@@ -11,7 +11,11 @@ launch configuration bench.py times.
   forwards bit-identical.
 * Kernel-level checks at the largest layer shapes with seeded tensors: an FL
   search and requantization over 205 M int32 accumulator-like values (exact
-  oracle over all of them) and the largest 3x3 conv at sampled outputs.
+  oracle over all of them) and the largest 3x3 conv at sampled outputs
+  (every layer class of the network at full size, exactly:
+  tests/test_gpu_fullsize_layers.py).
+* The paper's other networks at their full sizes (AlexNet b64, VGG-16 b128,
+  ResNet-18 b256, 224x224): the same first-C-Block recompute and properties.
 """
 import numpy as np
 import pytest
@@ -217,3 +221,85 @@ def test_wide_first_layer_full_batch_sampled(env):
     assert int(host(sc)[0]) == s_out
     assert np.array_equal(np.array([got[n, p, q] for n, p, q in pix]), want)
     h.close()
+
+
+@pytest.mark.parametrize("name,batch", [("alexnet", 64), ("vgg16", 128), ("resnet18", 256)])
+def test_other_networks_full_size(env, name, batch):
+    """AlexNet b64, VGG-16 b128 and ResNet-18 b256 at 224x224 in the
+    forward's launch configuration: the input's FL search and every input
+    code, the first C-Block's weights (and bias or Scale), all its outputs
+    through the epilogue, its FL search and every code recomputed by the
+    oracle; then every format valid, every code in range, and a second
+    forward bit-identical."""
+    torch, fx, nets, orc = env
+    note("fullsize forward", name, batch)
+    net = nets.CalibNet(name, batch=batch, image=224, device=DEV)
+    net.forward()
+    res = net.results()
+    assert res["flags"] == 0
+    seed = nets.SEEDS[name]
+    x = synth.normal(seed, "input", (batch, 3, 224, 224))
+    note("fullsize oracle input search", name)
+    fl_in, s_in, _ = orc.fl_search_f32(x.ravel(), 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert res["fmts"]["input"] == (8, fl_in, s_in)
+    xq = orc.quantize_f32(x, 8, fl_in, s_in)
+    del x
+    gq = decode8(net.act_codes["input"].cpu().numpy()[..., :3], s_in == 0).transpose(0, 3, 1, 2)
+    assert np.array_equal(gq, xq)
+    del gq
+    n = [n for n in net.graph if n.op == "conv"][0]
+    K, k = n.cout, n.k
+    w = synth.he_normal(seed, n.name + ".w", (K, 3, k, k))
+    fl_w, sg_w, _ = orc.fl_search_f32(w.ravel(), n.wl, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert res["fmts"][n.name + ".w"] == (n.wl, fl_w, sg_w)
+    wq = orc.quantize_f32(w, n.wl, fl_w, sg_w)
+    kw = {}
+    if n.bias:
+        b = synth.normal(seed, n.name + ".b", (K,), std=0.01)
+        fb, sb, _ = orc.fl_search_f32(b, 32, orc.SIGN_AUTO, FL_LO, FL_HI)
+        assert res["fmts"][n.name + ".b"] == (32, fb, sb)
+        kw.update(bias=orc.quantize_f32(b, 32, fb, sb), fl_b=fb)
+    if n.bn:
+        gamma = synth.uniform(seed, n.name + ".bn.gamma", (K,), 0.5, 1.5)
+        beta = synth.normal(seed, n.name + ".bn.beta", (K,), std=0.1)
+        inv = np.sqrt(np.ones(K, np.float32) + np.float32(1e-5))
+        a1 = (gamma / inv).astype(np.float32)
+        a2 = (beta - gamma * np.zeros(K, np.float32) / inv).astype(np.float32)
+        f1, s1, _ = orc.fl_search_f32(a1, 16, orc.SIGN_AUTO, FL_LO, FL_HI)
+        f2, s2, _ = orc.fl_search_f32(a2, 32, orc.SIGN_AUTO, FL_LO, FL_HI)
+        assert res["fmts"][n.name + ".a1"] == (16, f1, s1) and res["fmts"][n.name + ".a2"] == (32, f2, s2)
+        kw.update(a1=orc.quantize_f32(a1, 16, f1, s1), fl_a1=f1, a2=orc.quantize_f32(a2, 32, f2, s2),
+                  fl_a2=f2)
+    note("fullsize oracle first conv", name, n.name)
+    acc = orc.conv2d(xq, wq, n.stride, n.pad)
+    del xq
+    v, s = orc.epilogue(acc, fl_in + fl_w, relu=n.relu, **kw)
+    del acc
+    note("fullsize oracle first search", name, v.size)
+    fl_c, s_c, _ = orc.fl_search_i64(v.ravel(), s, 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert res["fmts"][n.name] == (8, fl_c, s_c)
+    want = orc.quantize_i64(v, s, 8, fl_c, s_c)
+    del v
+    got = decode8(net.act_codes[n.name].cpu().numpy(), s_c == 0).transpose(0, 3, 1, 2)
+    assert np.array_equal(got, want)
+    del got, want
+    # every layer: valid formats, codes in range; a second forward identical
+    for nm, (wl, fl, sign) in res["fmts"].items():
+        assert 2 <= wl <= 32 and FL_LO <= fl <= FL_HI and sign in (0, 1), nm
+    first = {}
+    for nm, t in net.act_codes.items():
+        if nm.startswith("pool"):
+            continue
+        wl, fl, sign = res["fmts"][nm]
+        lo, hi = orc.qrange(wl, sign)
+        off = 128 if sign == 0 else 0
+        assert int(t.min().item()) + off >= lo and int(t.max().item()) + off <= hi, nm
+        first[nm] = t.clone()
+    logits = net.logits.clone()
+    note("fullsize second forward", name)
+    net.forward()
+    assert net.results()["fmts"] == res["fmts"]
+    assert torch.equal(net.logits, logits)
+    for nm, t in first.items():
+        assert torch.equal(net.act_codes[nm], t), nm
+    net.close()
