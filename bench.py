@@ -43,6 +43,8 @@ def parse():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the per-layer sensitivity sweep reported alongside")
     ap.add_argument("--cpu-sample-batch", type=int, default=12)
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the other workloads' figures (FC layer, AlexNet, VGG-16, ResNet-18)")
     ap.add_argument("--mode", choices=["bench", "profile", "copy", "sweep", "qparams", "reduction",
                                        "wide", "steps"],
                     default="bench",
@@ -74,20 +76,102 @@ def committed_traffic():
     return float(m_val.group(1))
 
 
+def host_info():
+    """The GPU machine's host as the oracle sees it: CPU model, logical CPUs, the
+    threads the oracle's OpenMP regions use, compiler and flags."""
+    import subprocess
+    from oracle import build as ob
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    try:
+        cc = subprocess.run(["gcc", "--version"], capture_output=True, text=True).stdout.splitlines()[0]
+    except (OSError, IndexError):
+        cc = None
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(),
+            "threads": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)),
+            "compiler": cc, "flags": " ".join(ob.CFLAGS)}
+
+
 def cpu_baseline(batch):
     """The oracle, as it stands, on a bounded sample: a calibration forward of
-    `batch` images at 224x224 (parameters quantized beforehand), on the host."""
+    `batch` images at 224x224 (parameters quantized beforehand), on the host;
+    plus the single-core rates of its streaming steps."""
     import oracle
     t_prep = time.perf_counter()
     f = oracle.nets.prepare("resnet50", batch=batch, image=IMAGE)
     t0 = time.perf_counter()
     f.run()
     t = time.perf_counter() - t0
-    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
-    return {"value": round(batch / t, 5), "unit": "images/s", "cores": cores, "kind": "oracle",
-            "sample": f"ResNet-50 DFX calibration forward of {batch} images 224x224 "
-                      f"(exact CPU oracle, parameters pre-quantized; {t:.1f} s forward, "
-                      f"{t0 - t_prep:.1f} s set-up untimed)"}
+    info = host_info()
+    out = {"value": round(batch / t, 5), "unit": "images/s", "cores": info["threads"],
+           "kind": "oracle",
+           "sample": f"ResNet-50 DFX calibration forward of {batch} images 224x224 "
+                     f"(exact CPU oracle, parameters pre-quantized; {t:.1f} s forward, "
+                     f"{t0 - t_prep:.1f} s set-up untimed)"}
+    out.update({k: v for k, v in info.items() if k != "threads"})
+    out["single_core"] = cpu_single_core()
+    return out
+
+
+def cpu_single_core():
+    """GB/s of the oracle's quantize, FL search, requantization and layer
+    error on one core (its OpenMP regions limited to one thread): fp32 /
+    int32 values in, codes out, the algorithmic bytes of the GPU steps."""
+    import ctypes
+    import numpy as np
+    import oracle
+    import synth
+    gomp = ctypes.CDLL("libgomp.so.1")
+    gomp.omp_get_max_threads.restype = ctypes.c_int
+    prev = gomp.omp_get_max_threads()
+    n = 1 << 22
+    x = synth.normal(1, "cpu-x", (n,))
+    v = synth.integers(1, "cpu-v", (n,), -2 ** 20, 2 ** 20).astype(np.int64)
+    out = {"values": n}
+    gomp.omp_set_num_threads(1)
+    try:
+        steps = {
+            "quantize": (lambda: oracle.quantize_f32(x, 8, 5, 1), 5),
+            "fl_search": (lambda: oracle.fl_search_f32(x, 8, oracle.SIGN_AUTO, -8, 15), 4),
+            "requant": (lambda: oracle.quantize_i64(v, 14, 8, -3, 1), 5),
+        }
+        codes = oracle.quantize_f32(x, 8, 5, 1)
+        steps["layer_error"] = (lambda: oracle.layer_error(x, codes, 8, 5, 1), 5)
+        for name, (fn, bpv) in steps.items():
+            t0 = time.perf_counter()
+            fn()
+            t = time.perf_counter() - t0
+            out[name + "_gbs"] = round(bpv * n / t / 1e9, 4)
+    finally:
+        gomp.omp_set_num_threads(prev)
+    return out
+
+
+def cpu_configs():
+    """The oracle's forwards of the other workloads on bounded samples (all
+    host threads): the FC layer at its full size, AlexNet / VGG-16 /
+    ResNet-18 on a few images at 224x224 (parameters quantized beforehand)."""
+    import oracle
+    out = {}
+    t0 = time.perf_counter()
+    oracle.nets.run_fc(0)
+    out["fc"] = {"us_per_call": round((time.perf_counter() - t0) * 1e6, 1),
+                 "sample": "the whole FC workload (WL 8, 6 and 4), exact CPU oracle"}
+    for name, b in (("alexnet", 4), ("vgg16", 1), ("resnet18", 4)):
+        f = oracle.nets.prepare(name, batch=b, image=IMAGE)
+        t0 = time.perf_counter()
+        f.run()
+        t = time.perf_counter() - t0
+        out[name] = {"images_per_s": round(b / t, 4),
+                     "sample": f"{b} image(s) 224x224, exact CPU oracle, {t:.1f} s"}
+    return out
 
 
 def qparams_figures(dev, batch=32, image=224):
@@ -319,37 +403,163 @@ def steps_figures(dev):
     return out
 
 
-def compute_bound_mfma(net, dev):
-    """int8 MFMA use over the convolutions whose arithmetic intensity (int8
-    ops per HBM byte: input codes, weights, int32 output) is above the ridge
-    point peak / HBM bandwidth (625), i.e. the ones the matrix cores bound;
-    one more untimed forward with an event pair around each conv call."""
+def conv_rooflines(net, dev):
+    """Per conv / FC call of one more (untimed) forward, an event pair around
+    each: its int8 TOP/s against its own roofline min(peak, AI x HBM peak),
+    AI = int8 ops per HBM byte of input codes, weights and int32 output; and
+    the aggregate over the convolutions above the ridge point (peak / HBM
+    bandwidth = 625 ops/B), the ones the matrix cores bound."""
     import torch
     ridge = INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
     net.prepare_timers(1, classes=("qconv",))
     net.forward()
     torch.cuda.synchronize(dev)
     calls = [c for c in net.calls if c[0] == "qconv"]
+    names = [n.name for op, n, *r in net.ops if op in ("conv", "fc")]
     ops = ms = 0.0
     layers = 0
-    for (cls, work, fn, args), (_, _, e0, e1) in zip(calls, net.timers):
-        if fn.__name__ != "fxpq_qconv":
-            continue
-        d = args[1]._obj
-        ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
-        wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
-        m = d.n * ho * wo
-        hbm = d.n * d.h * d.w * d.c + d.k * d.r * d.s * d.c + 4 * m * d.k
-        if work / hbm > ridge:
+    per = []
+    for name, (cls, work, fn, args), (_, _, e0, e1) in zip(names, calls, net.timers):
+        t = e0.elapsed_time(e1)
+        if fn.__name__ == "fxpq_qconv":
+            d = args[1]._obj
+            ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
+            wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
+            m, n_, k = d.n * ho * wo, d.k, d.r * d.s * d.c
+            hbm = d.n * d.h * d.w * d.c + n_ * k + 4 * m * n_
+        else:  # fxpq_qgemm: M, N, K
+            m, n_, k = args[1], args[2], args[3]
+            hbm = m * k + n_ * k + 4 * m * n_
+        ai = work / hbm
+        roof = min(INT8_PEAK_TOPS, ai * HBM_PEAK_GBS / 1000.0)
+        tops = work / (t * 1e-3) / 1e12
+        per.append({"layer": name, "M": m, "N": n_, "K": k, "ms": round(t, 4),
+                    "tops": round(tops, 1), "ai": round(ai, 1), "roofline_tops": round(roof, 1),
+                    "frac_of_roofline": round(tops / roof, 3)})
+        if ai > ridge:
             ops += work
-            ms += e0.elapsed_time(e1)
+            ms += t
             layers += 1
     net.timers = None
-    if not layers:
-        return None
-    tops = ops / (ms * 1e-3) / 1e12
-    return {"layers": layers, "ridge_ops_per_byte": round(ridge, 1), "achieved": round(tops, 1),
-            "frac": round(tops / INT8_PEAK_TOPS, 4), "ms_per_forward": round(ms, 3)}
+    agg = None
+    if layers:
+        tops = ops / (ms * 1e-3) / 1e12
+        agg = {"layers": layers, "ridge_ops_per_byte": round(ridge, 1), "achieved": round(tops, 1),
+               "frac": round(tops / INT8_PEAK_TOPS, 4), "ms_per_forward": round(ms, 3)}
+    roof_ms = sum(p["ms"] * p["frac_of_roofline"] for p in per)
+    tot_ms = sum(p["ms"] for p in per)
+    return agg, per, {"ms_at_own_roofline": round(roof_ms, 3), "ms": round(tot_ms, 3),
+                      "frac": round(roof_ms / tot_ms, 4) if tot_ms else None}
+
+
+def cold_forward_ms(net, dev, reps=3):
+    """A forward right after every activation format changed (the formats
+    reset to zero): each fused FxP-QLayer then writes both window candidates'
+    codes and its gated requantization copies or recomputes them, as in an
+    Algorithm 1 / 2 trial; the average over reps such forwards."""
+    import torch
+    tot = 0.0
+    for _ in range(reps):
+        for f in net.act_fmt.values():
+            f.zero_()
+        torch.cuda.synchronize(dev)
+        t0 = time.perf_counter()
+        net.forward()
+        torch.cuda.synchronize(dev)
+        tot += time.perf_counter() - t0
+    return round(tot * 1000.0 / reps, 3)
+
+
+def network_figures(dev, name, steps=5):
+    """Another workload at its stated size (AlexNet b64, VGG-16 b128,
+    ResNet-18 b256, 224x224): one untimed forward, `steps` timed forwards,
+    then one forward each with the window pass and the contraction timed by
+    the library's events, the compute-bound convolutions, and a cold
+    forward."""
+    import torch
+    from paper_2203_12091_amd import fxpq as fx
+    from paper_2203_12091_amd import nets
+    net = nets.CalibNet(name, device=str(dev))
+    b = net.batch
+    net.forward()
+    torch.cuda.synchronize(dev)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        net.forward()
+    torch.cuda.synchronize(dev)
+    el = time.perf_counter() - t0
+    fx.timer_start(net.h, fx.TIMER_FLS_WINDOW)
+    net.forward()
+    win_ms, win_n, win_bytes = fx.timer_read(net.h)
+    fx.timer_start(net.h, fx.TIMER_QCONV)
+    net.forward()
+    cv_ms, cv_n, cv_ops = fx.timer_read(net.h)
+    fx.timer_start(net.h, fx.TIMER_OFF)
+    agg, _, own = conv_rooflines(net, dev)
+    if net.results()["flags"]:
+        print(f"bench.py: {name}: device flags", file=sys.stderr)
+        sys.exit(1)
+    gbs = win_bytes / (win_ms * 1e-3) / 1e9
+    out = {"workload": f"{name}_b{b}_{net.image}_dfx_calibration_forward", "batch": b,
+           "images_per_s": round(b * steps / el, 1), "ms_per_forward": round(el * 1000 / steps, 3),
+           "ms_per_forward_cold": cold_forward_ms(net, dev),
+           "fl_search_gbs": round(gbs, 1), "fl_search_frac": round(gbs / HBM_PEAK_GBS, 4),
+           "mfma_tops": round(cv_ops / (cv_ms * 1e-3) / 1e12, 1),
+           "mfma_frac": round(cv_ops / (cv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
+           "conv_frac_of_own_roofline": own["frac"], "compute_bound_layers": agg}
+    net.close()
+    return out
+
+
+def fc_figures(dev, reps=200):
+    """The single-FC-layer workload at WL 8 as one device pipeline: FL
+    search + quantize of W (256x512) and A (32x512), the int8 GEMM with
+    int32 accumulation, the fused FxP-QLayer of the 32x256 product (FL search
+    + requantization to WL 8); microseconds per pipeline over `reps` calls
+    after one untimed one (latency-bound: no roofline fraction)."""
+    import torch
+    import synth
+    from paper_2203_12091_amd import fxpq as fx
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+    W = torch.from_numpy(synth.normal(0, "fc.w", (256, 512), std=0.05).ravel()).to(dev)
+    A = torch.from_numpy(synth.relu_normal(0, "fc.a", (32, 512)).ravel()).to(dev)
+    fw, fa, fy = (torch.zeros(4, dtype=torch.int32, device=dev) for _ in range(3))
+    wc = torch.empty(W.numel(), dtype=torch.int8, device=dev)
+    ac = torch.empty(A.numel(), dtype=torch.int8, device=dev)
+    cs = torch.empty(256, dtype=torch.int32, device=dev)
+    acc = torch.empty((32, 256), dtype=torch.int32, device=dev)
+    mm = torch.empty(2, dtype=torch.float64, device=dev)
+    yc = torch.empty(acc.numel(), dtype=torch.int8, device=dev)
+    alt = torch.empty(acc.numel() + 16, dtype=torch.int8, device=dev)
+    sw, sa = fx.src_f32(W), fx.src_f32(A)
+    fx.fl_search(h, sw, W.numel(), 8, fx.SIGN_AUTO, -8, 15, fw)
+    torch.cuda.synchronize(dev)
+    ep = fx.epilogue(256, int(fw.cpu()[1]), fa)
+    sy = fx.src_acc(acc, ep, mm)
+
+    def pipeline():
+        fx.fl_search(h, sw, W.numel(), 8, fx.SIGN_AUTO, -8, 15, fw)
+        fx.fl_search(h, sa, A.numel(), 8, fx.SIGN_AUTO, -8, 15, fa)
+        fx.quantize(h, W, W.numel(), fw, wc, fx.I8)
+        fx.quantize(h, A, A.numel(), fa, ac, fx.C8)
+        fx.weight_colsum(h, wc, 256, 512, cs)
+        fx.qgemm(h, 32, 256, 512, ac, fx.C8, wc, cs, ep, acc, mm)
+        fx.qlayer(h, sy, acc.numel(), 8, fx.SIGN_AUTO, -8, 15, fy, yc, fx.C8, alt)
+
+    pipeline()
+    torch.cuda.synchronize(dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        pipeline()
+    e1.record()
+    torch.cuda.synchronize(dev)
+    us = e0.elapsed_time(e1) * 1000.0 / reps
+    assert fx.sync_status(h) == 0
+    h.close()
+    return {"workload": "fc_256x512_b32_wl8", "us_per_call": round(us, 2),
+            "calls": "fl_search W, fl_search A, quantize W, quantize A, colsum, qgemm, qlayer"}
 
 
 def sweep_figures(dev):
@@ -448,7 +658,9 @@ def main():
     net.forward()
     cb_ms, cb_n, cb_ops = fx.timer_read(net.h)
     fx.timer_start(net.h, fx.TIMER_OFF)
-    cbound = compute_bound_mfma(net, dev)
+    cbound, per_layer, own = conv_rooflines(net, dev)
+    cold_ms = cold_forward_ms(net, dev)
+    net.forward()  # back to the steady state (formats of the batch known)
 
     ms = elapsed * 1000.0 / args.steps
     value = BATCH * args.steps / elapsed
@@ -462,6 +674,7 @@ def main():
         "steps": args.steps,
         "warmup": args.warmup,
         "ms_per_step": round(ms, 3),
+        "ms_per_step_cold": cold_ms,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -486,14 +699,24 @@ def main():
                           "unit": "GB/s", "ms_per_forward": round(rq_ms, 3), "launches": rq_n}
     if cbound:
         out["mfma"]["compute_bound_layers"] = cbound
+    out["mfma"]["own_roofline"] = own
+    out["mfma"]["per_layer"] = per_layer
     if cb_n:
         out["fused_cblock"] = {"kernel": "k_qconv (min/max, FL-window and requant epilogues)",
                                "passes": cb_n, "ms_per_forward": round(cb_ms, 3),
                                "executed_tops": round(cb_ops / max(cb_ms, 1e-9) * 1e-9, 1)}
     if not args.no_sweep:
         out["sweep"] = sweep_figures(dev)
+    net.close()
+    del net
+    if not args.no_configs:
+        out["configs"] = {"fc": fc_figures(dev)}
+        for name in ("alexnet", "vgg16", "resnet18"):
+            out["configs"][name] = network_figures(dev, name)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_sample_batch)
+        if not args.no_configs:
+            out["cpu_baseline"]["configs"] = cpu_configs()
     print(json.dumps(out), flush=True)
 
 

@@ -7,9 +7,12 @@ SRC = os.path.join(HERE, "fxpq_oracle.c")
 LIB = os.path.join(HERE, "liboracle.so")
 
 
+CFLAGS = ["-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+          "-fno-fast-math", "-ffp-contract=off"]
+
+
 def build(verbose: bool = False) -> str:
-    cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
-           "-fno-fast-math", "-ffp-contract=off", "-o", LIB + ".tmp", SRC, "-lm"]
+    cmd = ["gcc"] + CFLAGS + ["-o", LIB + ".tmp", SRC, "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)
