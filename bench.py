@@ -404,36 +404,42 @@ def steps_figures(dev):
 
 
 def conv_rooflines(net, dev):
-    """Per conv / FC call of one more (untimed) forward, an event pair around
-    each: its int8 TOP/s against its own roofline min(peak, AI x HBM peak),
-    AI = int8 ops per HBM byte of input codes, weights and int32 output; and
-    the aggregate over the convolutions above the ridge point (peak / HBM
-    bandwidth = 625 ops/B), the ones the matrix cores bound."""
+    """Per conv / FC call of one more (untimed, warm) forward, an event pair
+    around each: its int8 TOP/s against its own roofline min(peak, AI x HBM
+    peak), AI = int8 ops per HBM byte the call must move: input codes and
+    weights, plus the int32 accumulators (fxpq_qconv) or the 8-bit codes
+    (fxpq_cblock_predicted, which keeps the accumulators on chip); and the
+    aggregate over the calls above the ridge point (peak / HBM bandwidth =
+    625 ops/B), the ones the matrix cores bound."""
     import torch
     ridge = INT8_PEAK_TOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
-    net.prepare_timers(1, classes=("qconv",))
+    classes = ("qconv", "cblock_pred")
+    net.prepare_timers(1, classes=classes)
+    m0 = net.misses
     net.forward()
     torch.cuda.synchronize(dev)
-    calls = [c for c in net.calls if c[0] == "qconv"]
+    run = net.pcalls if net.predict else net.calls
+    calls = [c for c in run if c[0] in classes]
+    assert net.misses == m0 and len(calls) == len(net.timers), "a warm forward missed"
     names = [n.name for op, n, *r in net.ops if op in ("conv", "fc")]
     ops = ms = 0.0
     layers = 0
     per = []
     for name, (cls, work, fn, args), (_, _, e0, e1) in zip(names, calls, net.timers):
         t = e0.elapsed_time(e1)
-        if fn.__name__ == "fxpq_qconv":
+        if fn.__name__ == "fxpq_qgemm":  # M, N, K
+            m, n_, k, cin_bytes = args[1], args[2], args[3], args[1] * args[3]
+        else:
             d = args[1]._obj
             ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
             wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
-            m, n_, k = d.n * ho * wo, d.k, d.r * d.s * d.c
-            hbm = d.n * d.h * d.w * d.c + n_ * k + 4 * m * n_
-        else:  # fxpq_qgemm: M, N, K
-            m, n_, k = args[1], args[2], args[3]
-            hbm = m * k + n_ * k + 4 * m * n_
+            m, n_, k, cin_bytes = d.n * ho * wo, d.k, d.r * d.s * d.c, d.n * d.h * d.w * d.c
+        out_bytes = (1 if cls == "cblock_pred" else 4) * m * n_
+        hbm = cin_bytes + n_ * k + out_bytes
         ai = work / hbm
         roof = min(INT8_PEAK_TOPS, ai * HBM_PEAK_GBS / 1000.0)
         tops = work / (t * 1e-3) / 1e12
-        per.append({"layer": name, "M": m, "N": n_, "K": k, "ms": round(t, 4),
+        per.append({"layer": name, "call": cls, "M": m, "N": n_, "K": k, "ms": round(t, 4),
                     "tops": round(tops, 1), "ai": round(ai, 1), "roofline_tops": round(roof, 1),
                     "frac_of_roofline": round(tops / roof, 3)})
         if ai > ridge:
@@ -450,6 +456,21 @@ def conv_rooflines(net, dev):
     tot_ms = sum(p["ms"] for p in per)
     return agg, per, {"ms_at_own_roofline": round(roof_ms, 3), "ms": round(tot_ms, 3),
                       "frac": round(roof_ms / tot_ms, 4) if tot_ms else None}
+
+
+def contraction_times(net):
+    """(ms, launches, int8 ops) of every contraction of one forward: the
+    fxpq_qconv / fxpq_qgemm kernels and the predicted C-Blocks' (one more
+    untimed forward each)."""
+    from paper_2203_12091_amd import fxpq as fx
+    tot = [0.0, 0, 0.0]
+    for kind in (fx.TIMER_QCONV, fx.TIMER_CBLOCK_PRED):
+        fx.timer_start(net.h, kind)
+        net.forward()
+        for i, v in enumerate(fx.timer_read(net.h)):
+            tot[i] += v
+    fx.timer_start(net.h, fx.TIMER_OFF)
+    return tuple(tot)
 
 
 def cold_forward_ms(net, dev, reps=3):
@@ -491,10 +512,7 @@ def network_figures(dev, name, steps=5):
     fx.timer_start(net.h, fx.TIMER_FLS_WINDOW)
     net.forward()
     win_ms, win_n, win_bytes = fx.timer_read(net.h)
-    fx.timer_start(net.h, fx.TIMER_QCONV)
-    net.forward()
-    cv_ms, cv_n, cv_ops = fx.timer_read(net.h)
-    fx.timer_start(net.h, fx.TIMER_OFF)
+    cv_ms, cv_n, cv_ops = contraction_times(net)
     agg, _, own = conv_rooflines(net, dev)
     if net.results()["flags"]:
         print(f"bench.py: {name}: device flags", file=sys.stderr)
@@ -634,6 +652,7 @@ def main():
     # launches of the last one with events (one forward's worth of event
     # records instead of all of them)
     torch.cuda.synchronize(dev)
+    m0 = net.misses
     t0 = time.perf_counter()
     for i in range(args.steps):
         if i == args.steps - 1:
@@ -641,16 +660,15 @@ def main():
         net.forward()
     torch.cuda.synchronize(dev)
     elapsed = time.perf_counter() - t0
+    timed_misses = net.misses - m0
     win_ms, win_n, win_bytes = fx.timer_read(net.h)
     res = net.results()
     if res["flags"]:
         print(f"bench.py: device flags {res['flags']:#x}", file=sys.stderr)
         sys.exit(1)
 
-    # one more (untimed) forward each for the contraction and requant figures
-    fx.timer_start(net.h, fx.TIMER_QCONV)
-    net.forward()
-    cv_ms, cv_n, cv_ops = fx.timer_read(net.h)
+    # more (untimed) forwards for the contraction and requant figures
+    cv_ms, cv_n, cv_ops = contraction_times(net)
     fx.timer_start(net.h, fx.TIMER_REQUANT)
     net.forward()
     rq_ms, rq_n, rq_bytes = fx.timer_read(net.h)
@@ -682,7 +700,9 @@ def main():
         "data": "synthetic",
         "config": {"workload": "resnet50_b256_224_dfx_calibration_forward", "batch": BATCH,
                    "image": IMAGE, "weight_wl": 8, "act_wl": 8, "fl_range": [-8, 15],
-                   "parallelism": "single_gpu"},
+                   "parallelism": "single_gpu", "predicted_cblocks": sum(
+                       1 for c in (net.pcalls if net.predict else []) if c[0] == "cblock_pred"),
+                   "timed_forwards_rerun": timed_misses},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "kernel": "k_fls_window", "launches": win_n,

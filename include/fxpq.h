@@ -344,6 +344,36 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
                         double* d_minmax);
 
 /*
+ * Predicted C-Block (Sec. "FxP-QLayer"; Eq. 10-14): the C-Block of
+ * fxpq_cblock and its FxP-QLayer in ONE contraction, without int32
+ * accumulators, for a layer evaluated again on data like its previous call's
+ * (the calibration loop re-runs the network on the same batch).  The
+ * epilogue evaluates the FL search's window (the two candidates from
+ * beta_nosat up, Eq. 14 sums and the clipping bound) for the min / max held
+ * in d_minmax on entry, i.e. the previous call's C-Block values, and writes
+ * the 8-bit codes of the window candidate that the format held in d_fmt_out
+ * on entry picks (the previous call's choice: the second candidate when its
+ * fl is that one, else the first).  A one-block decision then reduces this
+ * call's exact min / max and checks the prediction: when those give the same
+ * window (same beta_nosat, sign and variant) and the window decides, exactly,
+ * on the candidate whose codes were written, d_fmt_out and y hold what
+ * fxpq_qconv + fxpq_qlayer would write (bit for bit) and *d_miss is left
+ * unchanged; otherwise *d_miss is set to 1 and d_fmt_out / y are unspecified:
+ * the caller runs the layer again with fxpq_qconv + fxpq_qlayer (and every
+ * layer fed by it).  In both cases d_minmax ends with this call's min / max,
+ * the next call's prediction; NaN in d_minmax predicts nothing (a miss).
+ * d_minmax: device double[2], caller-owned, in units of 2^-s of the C-Block
+ * value (as fxpq_qconv writes it); d_miss: device uint32, caller-owned.
+ * Requirements: as fxpq_cblock (C % 16 == 0; the padded RGB layout is not
+ * supported), K % 4 == 0, 2 <= wl <= 8, y_type FXPQ_C8, y 16-byte aligned.
+ */
+fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const void* x,
+                                  fxpq_dtype x_type, const int8_t* w, const int32_t* w_colsum,
+                                  const fxpq_epilogue* ep, int32_t wl, int32_t sign, int32_t fl_lo,
+                                  int32_t fl_hi, fxpq_fmt* d_fmt_out, void* y, fxpq_dtype y_type,
+                                  double* d_minmax, uint32_t* d_miss);
+
+/*
  * C-Block contraction over codes of up to 32 bits (Sec. "Integer-Only
  * Inference"; the first and last layers start at 32-bit activations and
  * weights, Sec. "Initial Design Generation"), followed by its epilogue:
@@ -494,7 +524,8 @@ typedef enum {
   FXPQ_TIMER_FLS_WINDOW = 1, /* the one-read window pass of fxpq_fl_search */
   FXPQ_TIMER_QCONV = 2,      /* the contraction kernel of fxpq_qconv / fxpq_qgemm */
   FXPQ_TIMER_REQUANT = 3,    /* the kernel of fxpq_requant / fxpq_quantize */
-  FXPQ_TIMER_CBLOCK_PASS = 4 /* each contraction pass of fxpq_cblock */
+  FXPQ_TIMER_CBLOCK_PASS = 4, /* each contraction pass of fxpq_cblock */
+  FXPQ_TIMER_CBLOCK_PRED = 5  /* the contraction of fxpq_cblock_predicted */
 } fxpq_timer_kind;
 
 /*
@@ -511,7 +542,7 @@ fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind);
  * the summed algorithmic work (HBM bytes the kernel must move: 4 B per int32
  * value read, 2 B per eltwise element, 8 B per int64 value, 4 + 1 B per
  * quantized fp32 value; or int8 operations 2*M*N*K for the contraction, per
- * pass for fxpq_cblock).
+ * pass for fxpq_cblock, per call for fxpq_cblock_predicted).
  */
 fxpq_status fxpq_timer_read(fxpq_handle h, double* total_ms, int64_t* launches, double* work);
 

@@ -232,8 +232,8 @@ __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W, doubl
   for (int j = 0; j < kWindow; ++j) {
     double q = rint(W * c.cj[j]);
     if (j > 0 || CLAMP0) {
-      q = fmin(q, c.qmax);
-      if (!NONNEG) q = fmax(q, c.qmin);
+      q = min64(q, c.qmax);
+      if (!NONNEG) q = max64(q, c.qmin);
     }
     acc.A[j] = fma(q, q, acc.A[j]);
     if (SPLIT) acc.PH[j] = fma(Wh, q, acc.PH[j]);
@@ -246,10 +246,10 @@ __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W, doubl
 #pragma unroll
   for (int k = 0; k < NB; ++k) {
     if (k) t += t;
-    const double d1 = fmax(t - c.qmax, 0.0);
+    const double d1 = max64z(t - c.qmax);
     acc.CE[k] = fma(d1, d1, acc.CE[k]);
     if (!NONNEG) {
-      const double d2 = fmin(t - c.qmin, 0.0);
+      const double d2 = min64z(t - c.qmin);
       acc.CE[k] = fma(d2, d2, acc.CE[k]);
     }
   }
@@ -259,6 +259,13 @@ template <bool SPLIT, bool NONNEG, bool CLAMP0, int NB = 1>
 __device__ inline void win_consume(const WinCtx& c, WinAcc& acc, double W) {
   double q[kWindow];
   win_consume<SPLIT, NONNEG, CLAMP0, NB>(c, acc, W, q);
+}
+
+// Window candidate whose codes a predicted FxP-QLayer writes: the second
+// when the format the previous call chose (still in the output format) is
+// its fractional length, else the first.
+__device__ inline int pred_pick(const WinSetup& ws, const fxpq_fmt& prev) {
+  return (ws.nc == 2 && prev.fl == ws.b0 + 1) ? 1 : 0;
 }
 
 // Variant index (NONNEG << 1 | CLAMP0).

@@ -456,10 +456,11 @@ fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t w
                                   static_cast<int8_t*>(codes), static_cast<int8_t*>(codes_alt)));
 }
 
+// acc_used: the call writes int32 accumulators to acc (else acc is ignored).
 static fxpq_status conv_check(const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
                               const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,
-                              const int32_t* acc) {
-  if (!d || !x || !w || !acc) return FXPQ_ERR_INVALID_ARG;
+                              const int32_t* acc, bool acc_used = true) {
+  if (!d || !x || !w || (acc_used && !acc)) return FXPQ_ERR_INVALID_ARG;
   if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
       d->stride < 1 || d->pad < 0)
     return FXPQ_ERR_INVALID_ARG;
@@ -479,7 +480,7 @@ static fxpq_status conv_check(const fxpq_conv_desc* d, const void* x, fxpq_dtype
   int64_t blocks = (d->k <= 64) ? ((M + 255) / 256) * ((d->k + 63) / 64)
                                 : ((M + 127) / 128) * ((d->k + 127) / 128);
   if (blocks > kMaxConvBlocks) return FXPQ_ERR_UNSUPPORTED;
-  if (!aligned(w, 16) || !aligned(acc, 4) || !aligned(x, d->c == 4 ? 4 : 16))
+  if (!aligned(w, 16) || (acc_used && !aligned(acc, 4)) || !aligned(x, d->c == 4 ? 4 : 16))
     return FXPQ_ERR_INVALID_ARG;
   return FXPQ_OK;
 }
@@ -522,6 +523,31 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
   DeviceGuard g(h->device);
   return hip_status(launch_conv_fused(ctx(h), *d, x, x_type, w, w_colsum, e, wl, sign, fl_lo,
                                       fl_hi, d_fmt_out, static_cast<int8_t*>(y), y_type, d_minmax));
+}
+
+fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const void* x,
+                                  fxpq_dtype x_type, const int8_t* w, const int32_t* w_colsum,
+                                  const fxpq_epilogue* ep, int32_t wl, int32_t sign, int32_t fl_lo,
+                                  int32_t fl_hi, fxpq_fmt* d_fmt_out, void* y, fxpq_dtype y_type,
+                                  double* d_minmax, uint32_t* d_miss) {
+  if (!h || !ep || !d_fmt_out || !y || !d_minmax || !d_miss) return FXPQ_ERR_INVALID_ARG;
+  fxpq_status st = conv_check(d, x, x_type, w, w_colsum, ep, nullptr, false);
+  if (st) return st;
+  if (y_type != FXPQ_C8 || !aligned(y, 16)) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 2 || wl > 8) return wl == 1 ? FXPQ_ERR_UNSUPPORTED : FXPQ_ERR_INVALID_ARG;
+  if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  if (d->c % 16 != 0 || d->k % 4 != 0) return FXPQ_ERR_UNSUPPORTED;
+  const int nb = conv_fused_blocks(*d, h->cus);
+  if (nb < 1 || nb > kMaxConvBlocks) return FXPQ_ERR_UNSUPPORTED;
+  SrcDev e;
+  epi_to_dev(ep, &e);
+  e.kind = FXPQ_SRC_ACC;
+  e.dtype = FXPQ_I32;
+  e.x = nullptr;
+  DeviceGuard g(h->device);
+  return hip_status(launch_conv_pred(ctx(h), *d, x, x_type, w, w_colsum, e, wl, sign, fl_lo, fl_hi,
+                                     d_fmt_out, static_cast<int8_t*>(y), d_minmax, d_miss));
 }
 
 fxpq_status fxpq_qconv(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
@@ -757,7 +783,7 @@ fxpq_status fxpq_teacher_avgpool(fxpq_handle h, const float* x, int32_t n, int32
 }
 
 fxpq_status fxpq_timer_start(fxpq_handle h, fxpq_timer_kind kind) {
-  if (!h || kind < FXPQ_TIMER_OFF || kind > FXPQ_TIMER_CBLOCK_PASS) return FXPQ_ERR_INVALID_ARG;
+  if (!h || kind < FXPQ_TIMER_OFF || kind > FXPQ_TIMER_CBLOCK_PRED) return FXPQ_ERR_INVALID_ARG;
   DeviceGuard g(h->device);
   Timer& t = h->timer;
   if (kind != FXPQ_TIMER_OFF && !t.ev) {

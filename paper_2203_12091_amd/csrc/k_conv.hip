@@ -21,7 +21,11 @@
 //   EPI_MM   only the min / max;
 //   EPI_WIN  the window partial sums of the exact FL search over the C-Block
 //            values (the same sums the streaming window pass forms);
-//   EPI_REQ  the C-Block values requantized to the searched format (Eq. 1-2).
+//   EPI_REQ  the C-Block values requantized to the searched format (Eq. 1-2);
+//   EPI_PRED the predicted FxP-QLayer in one pass: the window partial sums at
+//            the window the previous call's min / max give, the codes of the
+//            candidate the previous call chose, and this call's min / max (no
+//            int32 accumulators); a one-block decision checks the prediction.
 // A C-Block whose contraction is shallow (R * S * C small next to the output)
 // is cheaper to recompute three times than to write, and read twice, as
 // int32: the fused launcher runs EPI_MM, EPI_WIN and EPI_REQ over the same
@@ -29,6 +33,8 @@
 // decide and the exact general pass needs them.
 #include <limits.h>
 #include <math.h>
+
+#include <type_traits>
 
 #include "fls.hpp"
 
@@ -99,7 +105,7 @@ __device__ inline void ring_barrier() {
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
-enum Epi { EPI_ACC = 0, EPI_MM = 1, EPI_WIN = 2, EPI_REQ = 3 };
+enum Epi { EPI_ACC = 0, EPI_MM = 1, EPI_WIN = 2, EPI_REQ = 3, EPI_PRED = 4 };
 
 struct ConvArgs {
   const int8_t* x;
@@ -177,6 +183,11 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
         win_verdict_write(ws, a.wl, a.fl_lo, a.fl_hi, a.plan, a.fmt_win, a.flags);
       return;
     }
+  } else if constexpr (EPI == EPI_PRED) {
+    // the window of the predicted min / max (verdict != 0: none to evaluate,
+    // the decision counts the call a miss; the min / max still go out)
+    ws = win_setup<FXPQ_SRC_ACC>(a.ep, a.mm, a.wl, a.sign_req, a.fl_lo, a.fl_hi, MODE_SEARCH,
+                                 PER_THREAD);
   } else if constexpr (EPI == EPI_REQ) {
     const int sv = src_scale(a.ep);
     if (a.y_type == FXPQ_I8) qf = qfmt_setup<FXPQ_I8>(a.fmt_req, sv, a.flags);
@@ -727,6 +738,124 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     }
 #undef FXPQ_WIN_VISIT
     win_write_partials(wa, 1, bid, a.part_i, a.part_f, wsh);
+  } else if constexpr (EPI == EPI_PRED) {
+    // Every value: W = the C-Block value (exact; at the source's own scale,
+    // so W is also what the min / max report), its min / max, and when the
+    // predicted window exists its window sums and the code of candidate pj
+    // (the previous call's choice) as a byte (q - 128 when unsigned).  The
+    // codes leave as dwords: a lane holds one column at 4 consecutive rows
+    // (e = 4g .. 4g + 3), and a 4 x 4 byte transpose inside each lane quad
+    // (two DPP exchanges) gives lane 4k + j row j at 4 consecutive columns.
+    const FlsU& u = ws.u;
+    const bool win = ws.verdict == 0;
+    const int pj = pred_pick(ws, *a.fmt_win);
+    const int qmax = (int)u.qmax;
+    const unsigned xorw = u.sign ? 0u : 0x80808080u;
+    WinCtx wc;
+    if (win) wc = win_ctx(u, ws);
+    WinAcc wa;
+    win_acc_zero(wa);
+    const int qj = lane & 3;
+    const unsigned m1 = (qj & 1) ? 0xFFFFFFFFu : 0u, m2 = (qj & 2) ? 0xFFFFFFFFu : 0u;
+    // min / max from the integer extremes of each column (the epilogue is
+    // monotonic in the accumulator within a channel), as EPI_ACC does
+    int lo[TN], hi[TN];
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+      lo[ni] = INT_MAX;
+      hi[ni] = INT_MIN;
+    }
+    // Every value is checked against the tile's extent even in full tiles:
+    // as straight-line code over 64 values the unchecked form runs out of
+    // registers, and the checks keep the live ranges short.
+    auto tile = [&](auto nn, auto c0, auto wn_, auto pj_) {
+      constexpr bool NN = decltype(nn)::value, C0 = decltype(c0)::value;
+      constexpr bool WIN = decltype(wn_)::value;
+      constexpr int PJ = decltype(pj_)::value ? 1 : 0;
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni) {
+        const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
+        const int corr = 128 * csum[ni];
+        double Mc, Ac;
+        epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
+        const int scol = n0 + wn * WCOLS + ni * 32 + ((lane & 31) & ~3);
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi) {
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const int rbase = m0 + wm * WROWS + mi * 32 + 8 * g + 4 * (lane >> 5);
+            unsigned w4 = 0;
+#pragma unroll
+            for (int jj = 0; jj < 4; ++jj) {
+              const int v = acc[mi][ni][4 * g + jj] + corr;
+              const bool ok = full || (rbase + jj < a.M && col < a.K);
+              lo[ni] = min(lo[ni], ok ? v : INT_MAX);
+              hi[ni] = max(hi[ni], ok ? v : INT_MIN);
+              if constexpr (WIN) {
+                int c = 0;
+                if (ok) {
+                  const double W = max64s(fma((double)v, Mc, Ac), relo);
+                  double q[kWindow];
+                  win_consume<false, NN, C0>(wc, wa, W, q);
+                  c = (int)q[PJ];
+                  if (PJ == 0 && !C0) c = min(c, qmax);
+                }
+                w4 |= (unsigned)(c & 0xFF) << (8 * jj);
+              }
+            }
+            if constexpr (WIN) {
+              // lane j of the quad holds rows 0..3 of column j: transpose
+              // (branch-free: every lane computes both forms and keeps one)
+              const unsigned x1 = (unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0xB1, 0xF, 0xF, false);
+              const unsigned o1 = ((x1 & 0xFF00FF00u) >> 8) | (w4 & 0xFF00FF00u);
+              const unsigned e1 = (w4 & 0x00FF00FFu) | ((x1 & 0x00FF00FFu) << 8);
+              w4 = e1 ^ ((o1 ^ e1) & m1);
+              const unsigned x2 = (unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0x4E, 0xF, 0xF, false);
+              const unsigned o2 = ((x2 & 0xFFFF0000u) >> 16) | (w4 & 0xFFFF0000u);
+              const unsigned e2 = (w4 & 0x0000FFFFu) | ((x2 & 0x0000FFFFu) << 16);
+              w4 = e2 ^ ((o2 ^ e2) & m2);
+              const int srow = rbase + qj;
+              if (srow < a.M && scol < a.K)
+                *reinterpret_cast<unsigned*>(a.y + (int64_t)srow * a.K + scol) = w4 ^ xorw;
+
+            }
+          }
+        }
+      }
+    };
+    using F = std::false_type;
+    using T = std::true_type;
+    if (!win) {
+      tile(F(), F(), F(), F());
+    } else {
+      const int var = win_variant(u, ws, a.mm);
+#define FXPQ_PRED_TILE(NN, C0) (pj ? tile(NN(), C0(), T(), T()) : tile(NN(), C0(), T(), F()))
+      switch (var) {
+        case 0: FXPQ_PRED_TILE(F, F); break;
+        case 1: FXPQ_PRED_TILE(F, T); break;
+        case 2: FXPQ_PRED_TILE(T, F); break;
+        default: FXPQ_PRED_TILE(T, T); break;
+      }
+#undef FXPQ_PRED_TILE
+      win_write_partials(wa, 1, bid, a.part_i, a.part_f, wsh);
+    }
+    double mn = INFINITY, mx = -INFINITY;
+#pragma unroll
+    for (int ni = 0; ni < TN; ++ni) {
+      if (lo[ni] > hi[ni]) continue;  // no in-range value in this column
+      double Mc, Ac;
+      epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
+      const double f0 = fmax(fma((double)lo[ni], Mc, Ac), relo);
+      const double f1 = fmax(fma((double)hi[ni], Mc, Ac), relo);
+      mn = fmin(mn, fmin(f0, f1));
+      mx = fmax(mx, fmax(f0, f1));
+    }
+    mn = block_reduce(mn, OpMin(), shd);
+    mx = block_reduce(mx, OpMax(), shd);
+    if (tid == 0) {
+      a.mm_part[2 * bid] = mn;
+      a.mm_part[2 * bid + 1] = mx;
+    }
   } else {  // EPI_REQ
     visit([&](int v, double Mc, double Ac, int row, int col) {
       const double val = fmax(fma((double)v, Mc, Ac), relo);
@@ -760,7 +889,7 @@ static bool ep_halo_ok(const fxpq_conv_desc& d) {
 // Tile shape and grid of a conv; loader choice and the geometry in `a`.
 static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const int8_t* w,
                        const int32_t* colsum, const SrcDev* ep, ConvArgs& a, int& loader,
-                       int& cfg, int cus, int halo = FXPQ_TILING_GEMM) {
+                       int& cfg, int cus, int halo = FXPQ_TILING_GEMM, bool wide_ok = true) {
   a.x = static_cast<const int8_t*>(x);
   a.w = w;
   a.colsum = colsum;
@@ -781,7 +910,7 @@ static dim3 conv_setup(const fxpq_conv_desc& d, const void* x, int x_type, const
   // to fill the chip; else 128 x 128 (three blocks per CU).
   const int64_t tiles_256x128 = (int64_t)((a.M + 255) / 256) * ((d.k + 127) / 128);
   if (d.k <= 64 || loader == LD_RGB4) cfg = TC_256x64;
-  else if (loader == LD_FAST64 && a.kdepth >= 512 && 2 * tiles_256x128 >= 3 * (int64_t)cus)
+  else if (wide_ok && loader == LD_FAST64 && a.kdepth >= 512 && 2 * tiles_256x128 >= 3 * (int64_t)cus)
     cfg = TC_256x128;
   else cfg = TC_128x128;
   // channel multiples of 64 outside the narrow tiles: slabs through the LDS ring
@@ -843,12 +972,13 @@ static void conv_run(const ConvArgs& a, int loader, int cfg, dim3 grid, hipStrea
       return;
     }
   }
+  constexpr int W3 = 3;
   if (cfg == TC_256x64)
-    conv_dispatch_loader<256, 64, 2, 2, 3, EPI>(loader, grid, st, a);
-  else if (cfg == TC_256x128)
-    conv_dispatch_loader<256, 128, 4, 2, 2, EPI>(loader, grid, st, a);
-  else
-    conv_dispatch_loader<128, 128, 2, 2, 3, EPI>(loader, grid, st, a);
+    conv_dispatch_loader<256, 64, 2, 2, W3, EPI>(loader, grid, st, a);
+  else if (cfg == TC_256x128) {
+    if constexpr (EPI != EPI_PRED) conv_dispatch_loader<256, 128, 4, 2, 2, EPI>(loader, grid, st, a);
+  } else
+    conv_dispatch_loader<128, 128, 2, 2, W3, EPI>(loader, grid, st, a);
 }
 
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
@@ -936,6 +1066,45 @@ hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* 
   conv_run<EPI_REQ>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, ops);
   return hipGetLastError();
+}
+
+// Predicted C-Block (conv + epilogue + FxP-QLayer in one contraction): the
+// epilogue evaluates the window of the min / max in d_minmax (the previous
+// call's) and writes the codes of the candidate the format in `out` picks;
+// the decision checks the prediction and sets *miss when it fails.
+hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
+                            const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
+                            int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y,
+                            double* d_minmax, unsigned* miss) {
+  ConvArgs a{};
+  int loader;
+  int cfg;
+  // no 256 x 128 tiles: their 128 accumulators per thread and the window
+  // state of this epilogue do not fit the registers of two blocks per CU
+  const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, cfg, c.cus,
+                               FXPQ_TILING_GEMM, false);
+  const int nb = (int)(grid.x * grid.y);
+  a.want_mm = 1;
+  a.mm_part = c.sc.minmax_part;
+  a.wl = wl;
+  a.sign_req = sign;
+  a.fl_lo = fl_lo;
+  a.fl_hi = fl_hi;
+  a.mm = d_minmax;
+  const int set = fls_begin(c);
+  a.part_i = c.sc.win_part + (size_t)set * kWinSlots * kWinPart;
+  a.part_f = c.sc.win_part_f + (size_t)set * kWinSlots * kWinPartF;
+  a.fmt_win = out;
+  a.y = y;
+  a.y_type = FXPQ_C8;
+  a.flags = c.sc.flags;
+  bool timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PRED);
+  conv_run<EPI_PRED>(a, loader, cfg, grid, c.stream);
+  timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_pred_fin(c, ep, set, wl, sign, fl_lo, fl_hi, conv_per_thread(cfg), nb, d_minmax,
+                         out, miss);
 }
 
 }  // namespace fxpq

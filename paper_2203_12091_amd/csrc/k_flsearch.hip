@@ -333,6 +333,61 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   if (threadIdx.x == 0) win_record(ws, r, wl, 0, plan, out);
 }
 
+// Decision of a predicted C-Block (one block of 1024 threads, after the
+// contraction): reduces the contraction's min / max partials to this call's
+// exact min / max, and checks that the window its epilogue evaluated (from
+// the predicted min / max held in mm) is this call's window: same verdict 0,
+// candidates, clipping bound, sign and variant.  Then one wave decides from
+// the window sums; the format is recorded when the decision is final and is
+// the candidate whose codes the epilogue wrote, else *miss is set.  mm ends
+// with this call's min / max; the other slot set is cleared for the next
+// search.
+constexpr int kPredFinThreads = 1024;
+
+__global__ __launch_bounds__(kPredFinThreads) void k_cblock_pred_fin(
+    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int64_t per_thread, const double* part_mm,
+    int nb, double* mm, const long long* part_i, const double* part_f, long long* clr_i,
+    double* clr_f, fxpq_fmt* out, unsigned* miss) {
+  __shared__ double sh[kPredFinThreads / 64];
+  __shared__ double act_sh[2];
+  const double pred[2] = {mm[0], mm[1]};
+  double mn = INFINITY, mx = -INFINITY;
+  for (int i = threadIdx.x; i < nb; i += blockDim.x) {
+    mn = fmin(mn, part_mm[2 * i]);
+    mx = fmax(mx, part_mm[2 * i + 1]);
+  }
+  mn = block_reduce(mn, OpMin(), sh);
+  mx = block_reduce(mx, OpMax(), sh);
+  win_slots_clear(clr_i, clr_f);
+  if (threadIdx.x == 0) {
+    act_sh[0] = mn;
+    act_sh[1] = mx;
+  }
+  __syncthreads();
+  if (threadIdx.x >= 64) return;
+  const double act[2] = {act_sh[0], act_sh[1]};
+  const WinSetup wp = win_setup<FXPQ_SRC_ACC>(s, pred, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
+  const WinSetup wa = win_setup<FXPQ_SRC_ACC>(s, act, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
+  const bool same = wp.verdict == 0 && wa.verdict == 0 && wp.b0 == wa.b0 && wp.b1 == wa.b1 &&
+                    wp.nc == wa.nc && wp.bce == wa.bce && wp.u.sign == wa.u.sign &&
+                    win_variant(wp.u, wp, pred) == win_variant(wa.u, wa, act);
+  bool hit = false;
+  int fl = 0;
+  if (same) {  // uniform over the wave
+    const WinResult r = win_decide(wa, 1, fl_hi, part_i, part_f);
+    if (threadIdx.x == 0) {
+      fl = r.fl_win;
+      hit = r.done && r.fl_win == wa.b0 + pred_pick(wp, *out);
+    }
+  }
+  if (threadIdx.x == 0) {
+    if (hit) *out = fxpq_fmt{wl, fl, wa.u.sign, 0};
+    else *miss = 1u;
+    mm[0] = act[0];
+    mm[1] = act[1];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Pass 2: exact general search (128-bit errors, 192-bit sums).
 // ---------------------------------------------------------------------------
@@ -679,6 +734,16 @@ hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int s
   hipError_t e = fl_search_passes(c, s, n, wl, sign, fl_lo, fl_hi, d_minmax, out, nullptr, codes, alt);
   if (e != hipSuccess) return e;
   return launch_requant_gated(c, s, n, out, codes, static_cast<const FlsPlan*>(c.sc.plan), alt);
+}
+
+hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int sign, int fl_lo,
+                           int fl_hi, int64_t per_thread, int nb, double* d_minmax, fxpq_fmt* out,
+                           unsigned* miss) {
+  k_cblock_pred_fin<<<1, kPredFinThreads, 0, c.stream>>>(ep, wl, sign, fl_lo, fl_hi, per_thread,
+                                             c.sc.minmax_part, nb, d_minmax, slots_i(c, set),
+                                             slots_f(c, set), slots_i(c, 1 - set),
+                                             slots_f(c, 1 - set), out, miss);
+  return hipGetLastError();
 }
 
 }  // namespace fxpq

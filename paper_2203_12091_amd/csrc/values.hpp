@@ -11,6 +11,41 @@ namespace fxpq {
 constexpr double kTwo52 = 4503599627370496.0;  // 2^52
 constexpr double kTwo53 = 9007199254740992.0;  // 2^53
 
+// fp64 max / min of values that are never NaN (exact integers and their
+// scaled codes), as single v_max_f64 / v_min_f64: written as the instruction
+// itself so that the compiler adds no NaN-quieting of the operands (which
+// IEEE-mode maxnum semantics would make it add before every use).  Same
+// results as fmax / fmin on non-NaN operands (+0 above -0).
+__device__ inline double max64(double a, double b) {
+  double r;
+  asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ inline double min64(double a, double b) {
+  double r;
+  asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// max(a, b) for a wave-uniform b held in scalar registers.
+__device__ inline double max64s(double a, double b) {
+  double r;
+  asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "s"(b));
+  return r;
+}
+
+// max(a, 0) and min(a, 0) with the zero as an inline constant.
+__device__ inline double max64z(double a) {
+  double r;
+  asm("v_max_f64 %0, %1, 0" : "=v"(r) : "v"(a));
+  return r;
+}
+__device__ inline double min64z(double a) {
+  double r;
+  asm("v_min_f64 %0, %1, 0" : "=v"(r) : "v"(a));
+  return r;
+}
+
 // Sticky device flags (vector atomic OR at device scope).
 __device__ inline void raise_flag(unsigned* flags, unsigned f) {
   __hip_atomic_fetch_or(flags, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

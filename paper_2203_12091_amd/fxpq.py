@@ -22,13 +22,13 @@ EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_fl_search_static", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_qconv_wide_workspace", "fxpq_qconv_wide", "fxpq_acc_overflow",
-    "fxpq_cblock", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
+    "fxpq_cblock", "fxpq_cblock_predicted", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_dequantize", "fxpq_prediction_ties", "fxpq_timer_start",
     "fxpq_timer_read",
     "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
     "fxpq_teacher_avgpool",
 ]
-TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT, TIMER_CBLOCK_PASS = range(5)
+TIMER_OFF, TIMER_FLS_WINDOW, TIMER_QCONV, TIMER_REQUANT, TIMER_CBLOCK_PASS, TIMER_CBLOCK_PRED = range(6)
 TILING_AUTO, TILING_GEMM, TILING_HALO = range(3)
 ROUND_CONSERVATIVE, ROUND_NEUTRAL, ROUND_AGGRESSIVE = range(3)
 PSI_PRINTED, PSI_MAX = range(2)
@@ -93,6 +93,8 @@ def lib():
             "fxpq_qconv_wide": [p, p, p, i32, i32, p, i32, i32, p, p, p, p, i64],
             "fxpq_acc_overflow": [p, p, i64, i32, p],
             "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
+            "fxpq_cblock_predicted": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int,
+                                      p, p],
             "fxpq_weight_colsum": [p, p, i64, i64, p],
             "fxpq_set_conv_tiling": [p, i32],
             "fxpq_maxpool": [p, p, C.c_int, i32, i32, i32, i32, i32, i32, i32, p],
@@ -220,6 +222,13 @@ def set_conv_tiling(h, mode):
 def qlayer(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, codes, code_type, codes_alt):
     _call("fxpq_qlayer", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi, ptr(d_fmt_out), ptr(codes),
           code_type, ptr(codes_alt))
+
+
+def cblock_predicted(h, desc, x, x_type, w, w_colsum, ep, wl, sign, fl_lo, fl_hi, d_fmt_out, y,
+                     y_type, d_minmax, d_miss):
+    _call("fxpq_cblock_predicted", h.value, C.byref(desc), ptr(x), x_type, ptr(w), ptr(w_colsum),
+          C.byref(ep), wl, sign, fl_lo, fl_hi, ptr(d_fmt_out), ptr(y), y_type, ptr(d_minmax),
+          ptr(d_miss))
 
 
 def qconv(h, desc, x, x_type, w, w_colsum, ep, acc, d_minmax=None):

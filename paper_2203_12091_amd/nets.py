@@ -152,10 +152,14 @@ class CalibNet:
     buffers and the input; ``forward()`` enqueues a full calibration forward."""
 
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", wl_override=None,
-                 keep_acts=True, fused=False, qlayer=True):
+                 keep_acts=True, fused=False, qlayer=True, predict=True):
         import torch
         self.fused = fused
         self.qlayer = qlayer
+        # predicted C-Blocks (fxpq_cblock_predicted) with a rerun of the
+        # standard calls from the first miss
+        self.predict = predict and qlayer and not fused
+        self.misses = 0
         self.torch = torch
         self.name = name
         self.seed = SEEDS[name] if seed is None else seed
@@ -265,7 +269,9 @@ class CalibNet:
                     p["a1"], _ = self._quant_param(n.name + ".a1", a1, SCALE_WL, fx.I32)
                     p["a2"], _ = self._quant_param(n.name + ".a2", a2, SHIFT_WL, fx.I32)
                 acc_max = max(acc_max, M * n.cout)
+                # min / max of the C-Block values; NaN: no prediction yet
                 p["mm"] = self._empty((2,), T.float64)
+                p["mm"].fill_(float("nan"))
                 if not n.last:
                     self.act_fmt[n.name] = self._fmt()
                     self.act_codes[n.name] = self._empty((B, Ho, Wo, n.cout), T.int8)
@@ -327,6 +333,8 @@ class CalibNet:
                                             self.act_fmt[n.inp])
         self.n_input = self.x_dev.numel()
         self.le_out = self._empty((4,), T.float64)
+        self.miss = self._empty((len(self.ops),), T.int32)
+        self.miss.zero_()
 
     # -- forward ---------------------------------------------------------------
     def _fused_conv(self, n, p):
@@ -359,7 +367,9 @@ class CalibNet:
                 if lop == "conv" and not ln.last and not self._fused_conv(ln, lr[0]):
                     addmm[last] = (n, first, rest[0]["mm"])
         self.addmm_adds = {v[0].name for v in addmm.values()}
+        self.starts = []
         for op, n, *rest in self.ops:
+            self.starts.append(len(calls))
             if op == "input":
                 f, c = self.act_fmt["input"], self.act_codes["input"]
                 src = fx.src_f32(self.x_dev)
@@ -461,7 +471,41 @@ class CalibNet:
                     FL_LO, FL_HI, f.data_ptr(), None)
                 add("requant", 9 * m, L.fxpq_requant, h, C.byref(src), m, f.data_ptr(),
                     self.act_codes[n.name].data_ptr(), fx.C8)
+        self.starts.append(len(calls))
+        if self.predict:
+            self.pcalls = self._plan_predicted(calls)
         return calls
+
+    def _predictable(self, op, n, p):
+        """A C-Block followed by its FxP-QLayer whose contraction the
+        predicted C-Block takes (channels a multiple of 16)."""
+        if op not in ("conv", "fc") or n.last:
+            return False
+        cin = p["Cin"] if op == "conv" else p["wlen"]
+        return cin % 16 == 0
+
+    def _plan_predicted(self, calls):
+        """The forward with every predictable C-Block as one
+        fxpq_cblock_predicted call (its miss flag: element i of self.miss for
+        op i); the other ops' calls as in the standard plan."""
+        import ctypes as C
+        L = fx.lib()
+        h = self.h.value
+        out = []
+        for i, (op, n, *rest) in enumerate(self.ops):
+            if not rest or not self._predictable(op, n, rest[0]):
+                out += calls[self.starts[i]:self.starts[i + 1]]
+                continue
+            p = rest[0]
+            desc = p["desc"] if op == "conv" else fx.conv_desc(p["M"], 1, 1, p["wlen"], n.cout, 1, 1, 1, 0)
+            self.keep.append(desc)
+            n_out = p["M"] * n.cout
+            out.append(("cblock_pred", 2 * n_out * p["wlen"], L.fxpq_cblock_predicted,
+                        (h, C.byref(desc), self.act_codes[n.inp].data_ptr(), fx.C8, p["w"].data_ptr(),
+                         p["colsum"].data_ptr(), C.byref(p["ep"]), A_WL, fx.SIGN_AUTO, FL_LO, FL_HI,
+                         self.act_fmt[n.name].data_ptr(), self.act_codes[n.name].data_ptr(), fx.C8,
+                         p["mm"].data_ptr(), self.miss.data_ptr() + 4 * i)))
+        return out
 
     def prepare_timers(self, steps, classes=("fl_search",)):
         """Pre-creates HIP events so that the next `steps` forwards bracket every
@@ -469,28 +513,48 @@ class CalibNet:
         if self.calls is None:
             self.calls = self._plan()
         T = self.torch
+        # a predicted forward may also rerun standard calls
         per_step = sum(1 for c in self.calls if c[0] in classes)
+        if self.predict:
+            per_step += sum(1 for c in self.pcalls if c[0] in classes)
         self.timed_classes = set(classes)
         self.event_pool = [(T.cuda.Event(enable_timing=True), T.cuda.Event(enable_timing=True))
                            for _ in range(per_step * steps)]
         self.timers = []
 
     def forward(self):
-        """Enqueues one calibration forward (no host synchronization).  After
-        prepare_timers(), calls of the timed classes are bracketed by HIP events
-        on the library's stream and (class, work, start, end) is recorded."""
+        """Enqueues one calibration forward.  Standard plan: no host
+        synchronization.  With predicted C-Blocks: the predicted plan, one
+        host synchronization to read the miss flags, and when a prediction
+        failed the standard calls again from the first op that missed (every
+        later op depended on it), so the results are always those of the
+        standard plan.  After prepare_timers(), calls of the timed classes are
+        bracketed by HIP events on the library's stream and (class, work,
+        start, end) is recorded."""
         if self.calls is None:
             self.calls = self._plan()
+        if not self.predict:
+            self._run(self.calls)
+            return
+        self._run(self.pcalls)
+        miss = self.miss.cpu().numpy()
+        if miss.any():
+            first = int(np.flatnonzero(miss)[0])
+            self.miss.zero_()
+            self.misses += 1
+            self._run(self.calls[self.starts[first]:])
+
+    def _run(self, calls):
         timers = self.timers
         if timers is None:
-            for cls, work, fn, args in self.calls:
+            for cls, work, fn, args in calls:
                 st = fn(*args)
                 if st:
                     raise fx.FxpqError(fn.__name__, st)
             return
         timed = self.timed_classes
         pool = self.event_pool
-        for cls, work, fn, args in self.calls:
+        for cls, work, fn, args in calls:
             if cls in timed:
                 e0, e1 = pool[len(timers)]
                 e0.record()

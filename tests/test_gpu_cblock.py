@@ -127,6 +127,14 @@ class Case:
                   FL_LO, FL_HI, out, y, fx.C8, acc, mm)
         return fmt_host(out), host(y), host(mm)
 
+    def predicted(self, fx, h, wl, mm, out, miss):
+        """fxpq_cblock_predicted with the prediction in mm and out (device)."""
+        import torch
+        y = torch.full((self.n,), 99, dtype=torch.int8, device=DEV)
+        fx.cblock_predicted(h, self.desc, self.xd, self.x_type, self.wd, self.colsum, self.ep, wl,
+                            fx.SIGN_AUTO, FL_LO, FL_HI, out, y, fx.C8, mm, miss)
+        return y
+
     def unfused(self, fx, h, wl, sign=None):
         import torch
         sign = fx.SIGN_AUTO if sign is None else sign
@@ -242,3 +250,50 @@ def test_cblock_rejects_unsupported(fx, h):
     with pytest.raises(fx.FxpqError):
         fx.cblock(h, rgb, c.xd, c.x_type, c.wd, c.colsum, c.ep, 8, fx.SIGN_AUTO, FL_LO, FL_HI,
                   out, y, fx.C8, acc, mm)
+
+
+@pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
+def test_cblock_predicted(fx, h, orc, case):
+    """The predicted C-Block: with no prediction (NaN min / max) a miss that
+    still leaves the exact min / max; with the previous call's min / max and
+    format (here: the oracle's) a hit whose format and codes equal the
+    oracle's, or a miss when the window cannot decide alone; with the other
+    window candidate's format, or a min / max from other data, a miss."""
+    import torch
+    c = Case(*case, seed=51 + CASES.index(case)).upload(fx, h)
+    v, s = c.oracle_values(orc)
+    hits = 0
+    for wl in (8, 6, 4):
+        note("cblock predicted", case, wl)
+        ofl, osg, _ = orc.fl_search_i64(v, s, wl, orc.SIGN_AUTO, FL_LO, FL_HI)
+        b0 = max(FL_LO, beta_nosat(v, s, wl, osg))
+        mm = torch.full((2,), float("nan"), dtype=torch.float64, device=DEV)
+        miss = torch.zeros(1, dtype=torch.int32, device=DEV)
+        c.predicted(fx, h, wl, mm, fmt_dev(wl, ofl, osg), miss)
+        assert int(host(miss)[0]) == 1
+        assert tuple(host(mm)) == (float(v.min()), float(v.max()))
+        # the steady state: the previous call's min / max and format
+        out = fmt_dev(wl, ofl, osg)
+        miss.zero_()
+        y = c.predicted(fx, h, wl, mm, out, miss)
+        if int(host(miss)[0]) == 0:
+            hits += 1
+            assert ofl in (b0, b0 + 1)
+            assert fmt_host(out) == (wl, ofl, osg, 0)
+            assert np.array_equal(decode8(host(y), osg == 0), orc.quantize_i64(v, s, wl, ofl, osg))
+        assert tuple(host(mm)) == (float(v.min()), float(v.max()))
+        if ofl in (b0, b0 + 1) and b0 + 1 <= FL_HI:
+            # the other window candidate's codes written: never a hit
+            other = b0 + 1 if ofl == b0 else b0
+            miss.zero_()
+            c.predicted(fx, h, wl, mm, fmt_dev(wl, other, osg), miss)
+            assert int(host(miss)[0]) == 1
+            assert tuple(host(mm)) == (float(v.min()), float(v.max()))
+        # a min / max four times larger: another window, a miss
+        miss.zero_()
+        mm4 = torch.tensor([4.0 * v.min(), 4.0 * v.max()], dtype=torch.float64, device=DEV)
+        c.predicted(fx, h, wl, mm4, fmt_dev(wl, ofl, osg), miss)
+        if max(FL_LO, beta_nosat(4 * v, s, wl, osg)) != b0:
+            assert int(host(miss)[0]) == 1
+    assert hits >= 1, "no case decided by the window alone"
+    assert fx.sync_status(h) == 0

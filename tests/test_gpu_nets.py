@@ -70,20 +70,59 @@ def test_fused_paths_match_two_call_forward(mods):
     # FxP-QLayers start from the formats the first one chose)
     nets, _ = mods
     res = {}
-    for fused, qlayer in ((True, True), (False, True), (False, False)):
-        note("net resnet50 8x112 fused", fused, "qlayer", qlayer)
-        net = nets.CalibNet("resnet50", batch=8, image=112, fused=fused, qlayer=qlayer)
+    for fused, qlayer, predict in ((True, True, False), (False, True, False), (False, False, False),
+                                   (False, True, True)):
+        note("net resnet50 8x112 fused", fused, "qlayer", qlayer, "predict", predict)
+        net = nets.CalibNet("resnet50", batch=8, image=112, fused=fused, qlayer=qlayer,
+                            predict=predict)
         plan = net._plan()
         assert any(c[0] == "cblock" for c in plan) == fused
         assert any(c[2].__name__ == "fxpq_qlayer" for c in plan) == qlayer
+        assert net.predict == predict
         for _ in range(2):
             net.forward()
-            res[(fused, qlayer, _)] = net.results(with_codes=True)
+            res[(fused, qlayer, predict, _)] = net.results(with_codes=True)
+        if predict:
+            assert net.misses == 1  # the first forward only
         net.close()
-    b = res[(False, False, 1)]
+    b = res[(False, False, False, 1)]
     for key, a in res.items():
         assert a["flags"] == 0, key
         assert a["fmts"] == b["fmts"], key
         for name in b["codes"]:
             assert np.array_equal(a["codes"][name], b["codes"][name]), (key, name)
         assert np.array_equal(a["logits"], b["logits"]), key
+
+
+@pytest.mark.parametrize("name,batch,image", [
+    ("resnet50", 2, 64), ("resnet18", 2, 75), ("alexnet", 2, 67), ("vgg16", 2, 64)])
+def test_predicted_forward_bit_exact(mods, name, batch, image):
+    """Predicted C-Blocks (fxpq_cblock_predicted): the first forward has no
+    prediction (every predicted C-Block misses and the standard calls run
+    again from the first), the second is predicted from the first; both
+    bit-identical to the oracle.  Then another batch (the images scaled by
+    1.5, predictions from the first batch) against the standard calls on that
+    batch."""
+    nets, oracle = mods
+    net = nets.CalibNet(name, batch=batch, image=image)
+    net._plan()
+    assert net.predict and any(c[0] == "cblock_pred" for c in net.pcalls)
+    ref = oracle.nets.run_config(name, batch=batch, image=image)
+    for k in range(2):
+        note("net predicted", name, batch, image, "forward", k)
+        net.forward()
+        compare(net.results(with_codes=True), ref)
+    assert net.misses >= 1
+    std = nets.CalibNet(name, batch=batch, image=image, predict=False)
+    for t in (net, std):
+        t.x_dev.mul_(1.5)
+    note("net predicted", name, "other batch")
+    net.forward()
+    std.forward()
+    a, b = net.results(with_codes=True), std.results(with_codes=True)
+    assert a["flags"] == 0 and a["fmts"] == b["fmts"]
+    for nm in b["codes"]:
+        assert np.array_equal(a["codes"][nm], b["codes"][nm]), nm
+    assert np.array_equal(a["logits"], b["logits"])
+    net.close()
+    std.close()
