@@ -274,6 +274,28 @@ fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t w
                         fxpq_dtype code_type, void* codes_alt);
 
 /*
+ * Predicted FxP-QLayer (Sec. "FxP-QLayer"; Eq. 10-14) for a layer evaluated
+ * again on data like its previous call's: ONE read of the values evaluates
+ * the FL search's window for the min / max held in d_minmax on entry (the
+ * previous call's values), writes the codes of the window candidate that the
+ * format in d_fmt_out on entry picks (as fxpq_cblock_predicted), and reduces
+ * this call's min / max (no separate min / max pass, no alternate buffer).
+ * A one-block decision then checks the prediction: when this call's min /
+ * max give the same window and the window decides, exactly, on the written
+ * candidate, d_fmt_out and codes hold what fxpq_qlayer writes (bit for bit);
+ * otherwise *d_miss is set to 1 or 2 (as fxpq_cblock_predicted) and both
+ * are unspecified (the caller runs fxpq_qlayer, and every layer fed by it,
+ * again).  d_minmax always ends with
+ * this call's min / max (NaN in it predicts nothing).  src->d_minmax is not
+ * used.  Sources: fp32, int32 values, C-Block values (FXPQ_SRC_ACC) and
+ * eltwise sums; 2 <= wl <= 8; code_type FXPQ_C8; codes 16-byte aligned.
+ */
+fxpq_status fxpq_qlayer_predicted(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl,
+                                  int32_t sign, int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out,
+                                  void* codes, fxpq_dtype code_type, double* d_minmax,
+                                  uint32_t* d_miss);
+
+/*
  * Preprocessor initial format (Sec. "Initial Design Generation", Eq. 6-9):
  *   S = 1 when the smallest value is negative (Eq. 6);
  *   psi = X_max / (2^k - 1) for S = 0, and for S = 1
@@ -358,9 +380,10 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
  * window (same beta_nosat, sign and variant) and the window decides, exactly,
  * on the candidate whose codes were written, d_fmt_out and y hold what
  * fxpq_qconv + fxpq_qlayer would write (bit for bit) and *d_miss is left
- * unchanged; otherwise *d_miss is set to 1 and d_fmt_out / y are unspecified:
- * the caller runs the layer again with fxpq_qconv + fxpq_qlayer (and every
- * layer fed by it).  In both cases d_minmax ends with this call's min / max,
+ * unchanged; otherwise *d_miss is set to 1 (2 when the prediction was right
+ * but the window alone cannot decide, so that the same data miss again) and
+ * d_fmt_out / y are unspecified: the caller runs the layer again with
+ * fxpq_qconv + fxpq_qlayer (and every layer fed by it).  In both cases d_minmax ends with this call's min / max,
  * the next call's prediction; NaN in d_minmax predicts nothing (a miss).
  * d_minmax: device double[2], caller-owned, in units of 2^-s of the C-Block
  * value (as fxpq_qconv writes it); d_miss: device uint32, caller-owned.

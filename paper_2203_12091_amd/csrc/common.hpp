@@ -220,6 +220,9 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
 hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int sign, int fl_lo,
                            int fl_hi, int64_t per_thread, int nb, double* d_minmax, fxpq_fmt* out,
                            unsigned* miss);
+hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign,
+                              int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, double* d_minmax,
+                              unsigned* miss);
 hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                              const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
                              int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,

@@ -372,6 +372,53 @@ __device__ inline void win_write_partials(const WinAcc& acc, int nb, int64_t bid
   win_write_partials_i64(A, PH, PL, acc.V2, acc.CE, nb, bid, part_i, part_f, sh);
 }
 
+// Block results of a window pass over integer values (no W split: PH is
+// zero).  Fewer reductions than win_write_partials: sum q^2 per candidate is
+// reduced in fp64, where it is exact (below 2^53 for word lengths up to 16
+// and at most 2^17 values per block); sum W q as the 32-bit halves of its
+// exact per-thread int64; the bound sums in fp64.  Same slot contents.
+__device__ inline void win_write_partials_int(const WinAcc& acc, int nb, int64_t bid,
+                                              long long* part_i, double* part_f, WinShared& sh) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  double a[kWindow];
+  long long ph[kWindow], pl[kWindow];
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) {
+    a[j] = wave_reduce(acc.A[j], OpAddD());
+    const long long p = exact_i64(acc.PL[j]);
+    ph[j] = wave_reduce(p >> 32, OpAddL());
+    pl[j] = wave_reduce(p & 0xFFFFFFFFll, OpAddL());
+  }
+  double f[kWinPartF];
+  f[0] = wave_reduce(acc.V2, OpAddD());
+#pragma unroll
+  for (int k = 0; k < kCeBounds; ++k) f[1 + k] = (k < nb) ? wave_reduce(acc.CE[k], OpAddD()) : 0.0;
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < kWindow; ++j) {
+      const long long aj = exact_i64(a[j]);
+      sh.i[w][6 * j + 0] = aj >> 32;
+      sh.i[w][6 * j + 1] = aj & 0xFFFFFFFFll;
+      sh.i[w][6 * j + 2] = 0;  // W q summed unsplit: the high part is zero
+      sh.i[w][6 * j + 3] = 0;
+      sh.i[w][6 * j + 4] = ph[j];
+      sh.i[w][6 * j + 5] = pl[j];
+    }
+#pragma unroll
+    for (int i = 0; i < kWinPartF; ++i) sh.f[w][i] = f[i];
+  }
+  __syncthreads();
+  const int t = threadIdx.x;
+  const int slot = (int)(bid % kWinSlots);
+  if (t < kWinPart) {
+    if ((t % 6) != 2 && (t % 6) != 3)
+      slot_add(part_i + slot * kWinPart + t, sh.i[0][t] + sh.i[1][t] + sh.i[2][t] + sh.i[3][t]);
+  } else if (t < kWinPart + 1 + nb) {
+    const int i = t - kWinPart;
+    slot_add(part_f + kWinPartF * slot + i, ((sh.f[0][i] + sh.f[1][i]) + sh.f[2][i]) + sh.f[3][i]);
+  }
+}
+
 // Launch helpers shared by the streaming search and the fused C-Block.
 constexpr int kFinThreads = kWinSlots;  // one wave: one slot per lane
 

@@ -456,6 +456,26 @@ fxpq_status fxpq_qlayer(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t w
                                   static_cast<int8_t*>(codes), static_cast<int8_t*>(codes_alt)));
 }
 
+fxpq_status fxpq_qlayer_predicted(fxpq_handle h, const fxpq_src* src, int64_t n, int32_t wl,
+                                  int32_t sign, int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out,
+                                  void* codes, fxpq_dtype code_type, double* d_minmax,
+                                  uint32_t* d_miss) {
+  if (!h || n < 1 || !d_fmt_out || !codes || !d_minmax || !d_miss) return FXPQ_ERR_INVALID_ARG;
+  if (code_type != FXPQ_C8 || !aligned(codes, 16)) return FXPQ_ERR_INVALID_ARG;
+  if (wl < 2 || wl > 8) return wl == 1 ? FXPQ_ERR_UNSUPPORTED : FXPQ_ERR_INVALID_ARG;
+  if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
+  if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
+  if (fl_hi - fl_lo + 1 > kMaxCand - 1) return FXPQ_ERR_INVALID_ARG;
+  SrcDev s;
+  fxpq_status st = to_dev(src, n, &s);
+  if (st) return st;
+  if (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) return FXPQ_ERR_UNSUPPORTED;
+  if (n / ((int64_t)kThreads * kWinMaxPerThread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  DeviceGuard g(h->device);
+  return hip_status(launch_qlayer_pred(ctx(h), s, n, wl, sign, fl_lo, fl_hi, d_fmt_out,
+                                       static_cast<int8_t*>(codes), d_minmax, d_miss));
+}
+
 // acc_used: the call writes int32 accumulators to acc (else acc is ignored).
 static fxpq_status conv_check(const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,
                               const int8_t* w, const int32_t* w_colsum, const fxpq_epilogue* ep,

@@ -737,7 +737,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       default: FXPQ_WIN_VISIT(true, true); break;
     }
 #undef FXPQ_WIN_VISIT
-    win_write_partials(wa, 1, bid, a.part_i, a.part_f, wsh);
+    win_write_partials_int(wa, 1, bid, a.part_i, a.part_f, wsh);
   } else if constexpr (EPI == EPI_PRED) {
     // Every value: W = the C-Block value (exact; at the source's own scale,
     // so W is also what the min / max report), its min / max, and when the
@@ -837,7 +837,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
         default: FXPQ_PRED_TILE(T, T); break;
       }
 #undef FXPQ_PRED_TILE
-      win_write_partials(wa, 1, bid, a.part_i, a.part_f, wsh);
+      win_write_partials_int(wa, 1, bid, a.part_i, a.part_f, wsh);
     }
     double mn = INFINITY, mx = -INFINITY;
 #pragma unroll

@@ -54,11 +54,14 @@ __device__ inline void store_codes(int8_t* y, int64_t i, const int* c, unsigned 
 }
 
 // Main loop of the streaming window pass over this thread's values.
-template <int KIND, int DT, bool NONNEG, bool CLAMP0, int NB, bool CODES>
+// MM: also the min / max of the values (predicted FxP-QLayer) into mn / mx.
+template <int KIND, int DT, bool NONNEG, bool CLAMP0, int NB, bool CODES, bool MM = false>
 __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const WinSetup& ws,
-                                const WinCodes& wcd, WinAcc& acc) {
+                                const WinCodes& wcd, WinAcc& acc, double* mn = nullptr,
+                                double* mx = nullptr) {
   const WinCtx wc = win_ctx(u, ws);
   win_acc_zero(acc);
+  double lo = INFINITY, hi = -INFINITY;
   // Codes of one value: the window's codes are clamped except candidate 0
   // when it cannot saturate (beta_nosat), where a value at qmax + 1/2 rounds
   // to qmax + 1 (same error either way, but the code must be clamped).
@@ -85,7 +88,13 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   stream_packets<KIND, DT, false, kWinSets, true>(s, n, tv, [&](const double* v, int64_t i0, int) {
     int cq[PK::EP][kWindow];
 #pragma unroll
-    for (int j = 0; j < PK::EP; ++j) consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j], cq[j]);
+    for (int j = 0; j < PK::EP; ++j) {
+      if constexpr (MM) {
+        lo = min64(lo, v[j]);
+        hi = max64(hi, v[j]);
+      }
+      consume(KIND == FXPQ_SRC_F32 ? v[j] * post : v[j], cq[j]);
+    }
     if constexpr (CODES) {
 #pragma unroll
       for (int k = 0; k < kWindow; ++k) {
@@ -100,13 +109,22 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   if (gtid == 0)
     for (int64_t i = nfull; i < n; ++i) {
       int cq[kWindow];
-      consume(load1<KIND, DT>(s, i) * u.wscale, cq);
+      const double vi = load1<KIND, DT>(s, i);
+      if constexpr (MM) {
+        lo = min64(lo, vi);
+        hi = max64(hi, vi);
+      }
+      consume(vi * u.wscale, cq);
       if constexpr (CODES) {
 #pragma unroll
         for (int k = 0; k < kWindow; ++k)
           if (wcd.y[k]) wcd.y[k][i] = (int8_t)((cq[k] & 0xFF) ^ (wcd.xorw & 0xFF));
       }
     }
+  if constexpr (MM) {
+    *mn = lo;
+    *mx = hi;
+  }
 }
 
 // Which window candidate's codes go to the output buffer of a fused
@@ -163,7 +181,64 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     case 2: win_loop<KIND, DT, true, false, NB, CODES>(s, n, u, ws, wcd, acc); break;
     default: win_loop<KIND, DT, true, true, NB, CODES>(s, n, u, ws, wcd, acc); break;
   }
-  win_write_partials(acc, NB, blockIdx.x, part_i, part_f, wsh);
+  if constexpr (KIND == FXPQ_SRC_F32) win_write_partials(acc, NB, blockIdx.x, part_i, part_f, wsh);
+  else win_write_partials_int(acc, NB, blockIdx.x, part_i, part_f, wsh);
+}
+
+// Predicted FxP-QLayer over a streaming source: the window of the min / max
+// held in mm (the previous call's values), the codes of the candidate the
+// format in `out` picks (the previous call's choice) into y, and this call's
+// min / max as block partials; the decision (k_pred_fin) checks the
+// prediction.  verdict != 0: no window, the min / max only (a miss).
+template <int KIND, int DT, int NB>
+__global__ __launch_bounds__(kThreads) void k_qlayer_pred(
+    SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int64_t per_thread,
+    const double* mm, long long* part_i, double* part_f, double* mm_part, const fxpq_fmt* out,
+    int8_t* y) {
+  __shared__ WinShared wsh;
+  __shared__ double shd[kThreads / 64];
+  const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
+  const FlsU& u = ws.u;
+  double mn = INFINITY, mx = -INFINITY;
+  if (ws.verdict == 0) {
+    WinCodes wcd{};
+    const int pj = pred_pick(ws, *out);
+    wcd.y[pj] = y;
+    wcd.qmax = (int)u.qmax;
+    wcd.xorw = u.sign ? 0u : 0x80808080u;
+    WinAcc acc;
+    switch (win_variant(u, ws, mm)) {
+      case 0: win_loop<KIND, DT, false, false, NB, true, true>(s, n, u, ws, wcd, acc, &mn, &mx); break;
+      case 1: win_loop<KIND, DT, false, true, NB, true, true>(s, n, u, ws, wcd, acc, &mn, &mx); break;
+      case 2: win_loop<KIND, DT, true, false, NB, true, true>(s, n, u, ws, wcd, acc, &mn, &mx); break;
+      default: win_loop<KIND, DT, true, true, NB, true, true>(s, n, u, ws, wcd, acc, &mn, &mx); break;
+    }
+    if constexpr (KIND == FXPQ_SRC_F32) win_write_partials(acc, NB, blockIdx.x, part_i, part_f, wsh);
+    else win_write_partials_int(acc, NB, blockIdx.x, part_i, part_f, wsh);
+  } else {
+    using PK = Pack<KIND, DT>;
+    ThreadVals<PK::V> tv;
+    thread_vals_init<KIND, DT>(s, (int64_t)blockIdx.x * kThreads * PK::V, tv);
+    stream_packets<KIND, DT>(s, n, tv, [&](const double* v, int64_t, int) {
+#pragma unroll
+      for (int j = 0; j < PK::EP; ++j) {
+        mn = min64(mn, v[j]);
+        mx = max64(mx, v[j]);
+      }
+    });
+    if ((int64_t)blockIdx.x * kThreads + threadIdx.x == 0)
+      for (int64_t i = n - n % PK::EP; i < n; ++i) {
+        const double vi = load1<KIND, DT>(s, i);
+        mn = min64(mn, vi);
+        mx = max64(mx, vi);
+      }
+  }
+  mn = block_reduce(mn, OpMin(), shd);
+  mx = block_reduce(mx, OpMax(), shd);
+  if (threadIdx.x == 0) {
+    mm_part[2 * blockIdx.x] = mn;
+    mm_part[2 * blockIdx.x + 1] = mx;
+  }
 }
 
 // Bits of |v| (0 for v == 0).
@@ -333,8 +408,8 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   if (threadIdx.x == 0) win_record(ws, r, wl, 0, plan, out);
 }
 
-// Decision of a predicted C-Block (one block of 1024 threads, after the
-// contraction): reduces the contraction's min / max partials to this call's
+// Decision of a predicted C-Block or FxP-QLayer (one block of 1024 threads,
+// after the pass): reduces the pass's min / max partials to this call's
 // exact min / max, and checks that the window its epilogue evaluated (from
 // the predicted min / max held in mm) is this call's window: same verdict 0,
 // candidates, clipping bound, sign and variant.  Then one wave decides from
@@ -344,8 +419,9 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
 // search.
 constexpr int kPredFinThreads = 1024;
 
-__global__ __launch_bounds__(kPredFinThreads) void k_cblock_pred_fin(
-    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int64_t per_thread, const double* part_mm,
+template <int KIND>
+__global__ __launch_bounds__(kPredFinThreads) void k_pred_fin(
+    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int nce, int64_t per_thread, const double* part_mm,
     int nb, double* mm, const long long* part_i, const double* part_f, long long* clr_i,
     double* clr_f, fxpq_fmt* out, unsigned* miss) {
   __shared__ double sh[kPredFinThreads / 64];
@@ -366,23 +442,27 @@ __global__ __launch_bounds__(kPredFinThreads) void k_cblock_pred_fin(
   __syncthreads();
   if (threadIdx.x >= 64) return;
   const double act[2] = {act_sh[0], act_sh[1]};
-  const WinSetup wp = win_setup<FXPQ_SRC_ACC>(s, pred, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
-  const WinSetup wa = win_setup<FXPQ_SRC_ACC>(s, act, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
+  const WinSetup wp = win_setup<KIND>(s, pred, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
+  const WinSetup wa = win_setup<KIND>(s, act, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const bool same = wp.verdict == 0 && wa.verdict == 0 && wp.b0 == wa.b0 && wp.b1 == wa.b1 &&
                     wp.nc == wa.nc && wp.bce == wa.bce && wp.u.sign == wa.u.sign &&
                     win_variant(wp.u, wp, pred) == win_variant(wa.u, wa, act);
-  bool hit = false;
+  bool hit = false, undecided = false;
   int fl = 0;
   if (same) {  // uniform over the wave
-    const WinResult r = win_decide(wa, 1, fl_hi, part_i, part_f);
+    const WinResult r = win_decide(wa, nce, fl_hi, part_i, part_f);
     if (threadIdx.x == 0) {
       fl = r.fl_win;
       hit = r.done && r.fl_win == wa.b0 + pred_pick(wp, *out);
+      undecided = !r.done;
     }
   }
   if (threadIdx.x == 0) {
+    // miss 1: the prediction was wrong; 2: right, but the window alone
+    // cannot decide (the exact search needs more candidates), so the next
+    // call on the same data misses again
     if (hit) *out = fxpq_fmt{wl, fl, wa.u.sign, 0};
-    else *miss = 1u;
+    else *miss = undecided ? 2u : 1u;
     mm[0] = act[0];
     mm[1] = act[1];
   }
@@ -739,10 +819,47 @@ hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int s
 hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int sign, int fl_lo,
                            int fl_hi, int64_t per_thread, int nb, double* d_minmax, fxpq_fmt* out,
                            unsigned* miss) {
-  k_cblock_pred_fin<<<1, kPredFinThreads, 0, c.stream>>>(ep, wl, sign, fl_lo, fl_hi, per_thread,
-                                             c.sc.minmax_part, nb, d_minmax, slots_i(c, set),
+  const int nce = 1;  // the conv epilogue evaluates one clipping bound
+  k_pred_fin<FXPQ_SRC_ACC><<<1, kPredFinThreads, 0, c.stream>>>(
+      ep, wl, sign, fl_lo, fl_hi, nce, per_thread, c.sc.minmax_part, nb, d_minmax, slots_i(c, set),
+      slots_f(c, set), slots_i(c, 1 - set), slots_f(c, 1 - set), out, miss);
+  return hipGetLastError();
+}
+
+// Predicted FxP-QLayer over a streaming source (fp32, int32 C-Block values,
+// eltwise sums): one pass writing the predicted candidate's codes and the
+// min / max, then the decision.
+hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign,
+                              int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, double* d_minmax,
+                              unsigned* miss) {
+  const int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
+  const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;
+  const int nce = (wl <= kCeMultiMaxWl) ? kCeBounds : 1;
+  const int set = fls_begin(c);
+  int blocks = 0;
+  int64_t per_thread = 0;
+  auto run = [&](auto kernel, auto fin) {
+    blocks = stream_grid(n, channels, kWinMaxPerThread, vec, resident_blocks(c, (const void*)kernel));
+    per_thread = window_per_thread(n, blocks, vec);
+    bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
+    kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, per_thread, d_minmax,
+                                              slots_i(c, set), slots_f(c, set), c.sc.minmax_part,
+                                              out, y);
+    const double elem = (s.kind == FXPQ_SRC_ADD) ? 2.0 : 4.0;
+    timer_end(c, timed, (elem + 1.0) * (double)n);
+    fin<<<1, kPredFinThreads, 0, c.stream>>>(s, wl, sign, fl_lo, fl_hi, nce, per_thread,
+                                             c.sc.minmax_part, blocks, d_minmax, slots_i(c, set),
                                              slots_f(c, set), slots_i(c, 1 - set),
                                              slots_f(c, 1 - set), out, miss);
+  };
+#define FXPQ_QPRED(K, D)                                                            \
+  (nce == 1 ? run(&k_qlayer_pred<K, D, 1>, &k_pred_fin<K>)                         \
+            : run(&k_qlayer_pred<K, D, kCeBounds>, &k_pred_fin<K>))
+  if (s.kind == FXPQ_SRC_F32) FXPQ_QPRED(FXPQ_SRC_F32, FXPQ_F32);
+  else if (s.kind == FXPQ_SRC_ADD) FXPQ_QPRED(FXPQ_SRC_ADD, FXPQ_I8);
+  else if (s.kind == FXPQ_SRC_ACC) FXPQ_QPRED(FXPQ_SRC_ACC, FXPQ_I32);
+  else FXPQ_QPRED(FXPQ_SRC_INT, FXPQ_I32);
+#undef FXPQ_QPRED
   return hipGetLastError();
 }
 

@@ -20,7 +20,7 @@ FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4
 
 EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
-    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_fl_search_static", "fxpq_qlayer", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
+    "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_fl_search_static", "fxpq_qlayer", "fxpq_qlayer_predicted", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_qconv_wide_workspace", "fxpq_qconv_wide", "fxpq_acc_overflow",
     "fxpq_cblock", "fxpq_cblock_predicted", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_dequantize", "fxpq_prediction_ties", "fxpq_timer_start",
@@ -86,6 +86,7 @@ def lib():
             "fxpq_fl_search": [p, p, i64, i32, i32, i32, i32, p, p],
             "fxpq_fl_search_static": [p, i64, i32, i32, i32, i32, p, p, p],
             "fxpq_qlayer": [p, p, i64, i32, i32, i32, i32, p, p, C.c_int, p],
+            "fxpq_qlayer_predicted": [p, p, i64, i32, i32, i32, i32, p, p, C.c_int, p, p],
             "fxpq_preprocess": [p, p, i64, i32, i32, i32, i32, i32, p],
             "fxpq_qconv": [p, p, p, C.c_int, p, p, p, p, p],
             "fxpq_qgemm": [p, i64, i64, i64, p, C.c_int, p, p, p, p, p],
@@ -229,6 +230,12 @@ def cblock_predicted(h, desc, x, x_type, w, w_colsum, ep, wl, sign, fl_lo, fl_hi
     _call("fxpq_cblock_predicted", h.value, C.byref(desc), ptr(x), x_type, ptr(w), ptr(w_colsum),
           C.byref(ep), wl, sign, fl_lo, fl_hi, ptr(d_fmt_out), ptr(y), y_type, ptr(d_minmax),
           ptr(d_miss))
+
+
+def qlayer_predicted(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, codes, code_type, d_minmax,
+                     d_miss):
+    _call("fxpq_qlayer_predicted", h.value, C.byref(src), n, wl, sign, fl_lo, fl_hi,
+          ptr(d_fmt_out), ptr(codes), code_type, ptr(d_minmax), ptr(d_miss))
 
 
 def qconv(h, desc, x, x_type, w, w_colsum, ep, acc, d_minmax=None):

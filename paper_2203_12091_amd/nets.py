@@ -160,6 +160,7 @@ class CalibNet:
         # standard calls from the first miss
         self.predict = predict and qlayer and not fused
         self.misses = 0
+        self.no_predict = set()  # ops whose window cannot decide alone
         self.torch = torch
         self.name = name
         self.seed = SEEDS[name] if seed is None else seed
@@ -288,7 +289,9 @@ class CalibNet:
                 shapes[n.name] = shapes[n.inp]
                 self.act_fmt[n.name] = self._fmt()
                 self.act_codes[n.name] = self._empty((B,) + shapes[n.inp], T.int8)
-                self.ops.append(("add", n, {"mm": self._empty((2,), T.float64)}))
+                mm = self._empty((2,), T.float64)
+                mm.fill_(float("nan"))  # no prediction yet
+                self.ops.append(("add", n, {"mm": mm}))
             elif n.op == "avgpool":
                 H, W, C = shapes[n.inp]
                 r = np.array([np.float32(1.0) / np.float32(H * W)], np.float32)
@@ -335,6 +338,8 @@ class CalibNet:
         self.le_out = self._empty((4,), T.float64)
         self.miss = self._empty((len(self.ops),), T.int32)
         self.miss.zero_()
+        self.input_mm = self._empty((2,), T.float64)
+        self.input_mm.fill_(float("nan"))
 
     # -- forward ---------------------------------------------------------------
     def _fused_conv(self, n, p):
@@ -493,6 +498,28 @@ class CalibNet:
         h = self.h.value
         out = []
         for i, (op, n, *rest) in enumerate(self.ops):
+            miss = self.miss.data_ptr() + 4 * i
+            if i in self.no_predict:
+                out += calls[self.starts[i]:self.starts[i + 1]]
+                continue
+            if op == "input" or (op == "add" and n.name not in self.addmm_adds):
+                # the FxP-QLayer of the network input / of an eltwise sum:
+                # predicted from its previous min / max and format
+                std = calls[self.starts[i]:self.starts[i + 1]]
+                if op == "input":
+                    src, m, mm = fx.src_f32(self.x_dev), self.n_input, self.input_mm
+                else:
+                    a, b = self.act_codes[n.inp], self.act_codes[n.other]
+                    src = fx.src_add(a, fx.C8, self.act_fmt[n.inp], b, fx.C8, self.act_fmt[n.other],
+                                     n.relu)
+                    m, mm = a.numel(), rest[0]["mm"]
+                self.keep.append(src)
+                out.append(("fl_search", std[0][1], L.fxpq_qlayer_predicted,
+                            (h, C.byref(src), m, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI,
+                             self.act_fmt[n.name].data_ptr(), self.act_codes[n.name].data_ptr(),
+                             fx.C8, mm.data_ptr(), miss)))
+                out += std[1:]  # the input's layer error
+                continue
             if not rest or not self._predictable(op, n, rest[0]):
                 out += calls[self.starts[i]:self.starts[i + 1]]
                 continue
@@ -504,7 +531,7 @@ class CalibNet:
                         (h, C.byref(desc), self.act_codes[n.inp].data_ptr(), fx.C8, p["w"].data_ptr(),
                          p["colsum"].data_ptr(), C.byref(p["ep"]), A_WL, fx.SIGN_AUTO, FL_LO, FL_HI,
                          self.act_fmt[n.name].data_ptr(), self.act_codes[n.name].data_ptr(), fx.C8,
-                         p["mm"].data_ptr(), self.miss.data_ptr() + 4 * i)))
+                         p["mm"].data_ptr(), miss)))
         return out
 
     def prepare_timers(self, steps, classes=("fl_search",)):
@@ -522,18 +549,20 @@ class CalibNet:
                            for _ in range(per_step * steps)]
         self.timers = []
 
-    def forward(self):
+    def forward(self, predict=None):
         """Enqueues one calibration forward.  Standard plan: no host
         synchronization.  With predicted C-Blocks: the predicted plan, one
         host synchronization to read the miss flags, and when a prediction
         failed the standard calls again from the first op that missed (every
         later op depended on it), so the results are always those of the
-        standard plan.  After prepare_timers(), calls of the timed classes are
+        standard plan.  predict=False runs the standard plan on a predicting
+        net (a caller that changed formats or data knows the predictions will
+        fail).  After prepare_timers(), calls of the timed classes are
         bracketed by HIP events on the library's stream and (class, work,
         start, end) is recorded."""
         if self.calls is None:
             self.calls = self._plan()
-        if not self.predict:
+        if not self.predict or predict is False:
             self._run(self.calls)
             return
         self._run(self.pcalls)
@@ -543,6 +572,11 @@ class CalibNet:
             self.miss.zero_()
             self.misses += 1
             self._run(self.calls[self.starts[first]:])
+            if miss[first] == 2:
+                # predicted right but undecidable by the window: this op runs
+                # the standard calls from now on
+                self.no_predict.add(first)
+                self.pcalls = self._plan_predicted(self.calls)
 
     def _run(self, calls):
         timers = self.timers

@@ -83,7 +83,13 @@ def test_fused_paths_match_two_call_forward(mods):
             net.forward()
             res[(fused, qlayer, predict, _)] = net.results(with_codes=True)
         if predict:
-            assert net.misses == 1  # the first forward only
+            # the first forward has no predictions; a layer whose window
+            # cannot decide alone misses once more, then runs unpredicted
+            assert net.misses <= 2
+            m = net.misses
+            net.forward()
+            assert net.misses == m
+            res[(fused, qlayer, predict, 2)] = net.results(with_codes=True)
         net.close()
     b = res[(False, False, False, 1)]
     for key, a in res.items():

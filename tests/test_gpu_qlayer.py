@@ -201,3 +201,79 @@ def test_qlayer_host_checks(fx, h):
     assert L.fxpq_qlayer(*args(0, fx.C8, codes.data_ptr(), codes.data_ptr())) == fx.ERR_INVALID_ARG
     assert L.fxpq_qlayer(*args(8, fx.C8, codes.data_ptr() + 1, codes.data_ptr())) == fx.ERR_INVALID_ARG
     check_flags(fx, h)
+
+
+def run_predicted(fx, h, src, n, wl, mm_exact, want_fmt, want_codes, bnosat, tag):
+    """fxpq_qlayer_predicted: no prediction (NaN) -> a miss leaving the exact
+    min / max; the previous call's min / max and format -> a hit equal to the
+    oracle (or a miss when the window alone cannot decide); the other window
+    candidate's format -> a miss.  Nothing is written past n."""
+    import torch
+    b0 = max(FL_LO, bnosat)
+    osign = want_fmt[2]
+    mm = torch.full((2,), float("nan"), dtype=torch.float64, device=DEV)
+    miss = torch.zeros(1, dtype=torch.int32, device=DEV)
+    codes = torch.full((n + 16,), 0x55, dtype=torch.int8, device=DEV)
+    note("qlayer predicted", tag, n, wl, "no prediction")
+    fx.qlayer_predicted(h, src, n, wl, fx.SIGN_AUTO, FL_LO, FL_HI, fmt_dev(*want_fmt[:3]), codes,
+                        fx.C8, mm, miss)
+    assert int(host(miss)[0]) == 1 and tuple(host(mm)) == mm_exact, tag
+    out = fmt_dev(*want_fmt[:3])
+    miss.zero_()
+    note("qlayer predicted", tag, n, wl, "steady state")
+    fx.qlayer_predicted(h, src, n, wl, fx.SIGN_AUTO, FL_LO, FL_HI, out, codes, fx.C8, mm, miss)
+    hit = int(host(miss)[0]) == 0
+    got = host(codes)
+    assert np.all(got[n:] == 0x55), "wrote past n"
+    if hit:
+        assert want_fmt[1] in (b0, b0 + 1), tag
+        assert fmt_host(out) == want_fmt, tag
+        assert np.array_equal(decode8(got[:n], osign == 0), want_codes), tag
+    assert tuple(host(mm)) == mm_exact, tag
+    if want_fmt[1] in (b0, b0 + 1) and b0 + 1 <= FL_HI:
+        other = b0 + 1 if want_fmt[1] == b0 else b0
+        miss.zero_()
+        fx.qlayer_predicted(h, src, n, wl, fx.SIGN_AUTO, FL_LO, FL_HI, fmt_dev(wl, other, osign),
+                            codes, fx.C8, mm, miss)
+        assert int(host(miss)[0]) == 1, tag
+    return hit
+
+
+def test_qlayer_predicted(fx, h, orc):
+    """The predicted FxP-QLayer over fp32, eltwise-sum and C-Block sources
+    against the oracle."""
+    from test_gpu_kernels import CONV_CASES, gpu_conv_case
+    hits = 0
+    for name, x in [("normal", synth.normal(91, "qp", (100_003,), std=1.0)),
+                    ("relu", np.maximum(synth.normal(92, "qpr", (4099,), std=2.0), 0))]:
+        x = np.asarray(x, np.float32)
+        for wl in (8, 5):
+            ofl, osign, _ = orc.fl_search_f32(x, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+            bn = beta_nosat([F(float(v)) for v in (x.min(), x.max())], wl, osign)
+            hits += run_predicted(fx, h, fx.src_f32(dev(x)), x.size, wl,
+                                  (float(x.min()), float(x.max())), (wl, ofl, osign, 0),
+                                  orc.quantize_f32(x, wl, ofl, osign), bn, f"f32-{name}")
+    n = 100_003
+    a = synth.integers(93, "a", (n,), -128, 127)
+    b = synth.integers(93, "b", (n,), 0, 255)
+    ad, bd = dev(a.astype(np.int8)), dev((b - 128).astype(np.int8))
+    for relu in (True, False):
+        for m in (n, 16 * 1000 + 7):
+            src = fx.src_add(ad, fx.C8, fmt_dev(8, 3, 1), bd, fx.C8, fmt_dev(8, 6, 0), relu)
+            v, s = orc.eltwise_add(a[:m], 3, b[:m], 6, relu)
+            for wl in (8, 5):
+                ofl, osign, _ = orc.fl_search_i64(v, s, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+                bn = beta_nosat([fr(v.min(), s), fr(v.max(), s)], wl, osign)
+                hits += run_predicted(fx, h, src, m, wl, (float(v.min()), float(v.max())),
+                                      (wl, ofl, osign, 0), orc.quantize_i64(v, s, wl, ofl, osign), bn,
+                                      f"add-relu{int(relu)}-{m}")
+    acc, ep, mm, v, s_out, keep = gpu_conv_case(fx, h, orc, *CONV_CASES[0], seed=94)
+    vn = v.transpose(0, 2, 3, 1).ravel()[:acc.numel()]
+    for wl in (8, 6):
+        ofl, osign, _ = orc.fl_search_i64(vn, s_out, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+        bn = beta_nosat([fr(vn.min(), s_out), fr(vn.max(), s_out)], wl, osign)
+        hits += run_predicted(fx, h, fx.src_acc(acc, ep), acc.numel(), wl,
+                              (float(vn.min()), float(vn.max())), (wl, ofl, osign, 0),
+                              orc.quantize_i64(vn, s_out, wl, ofl, osign), bn, "acc")
+    assert hits >= 8, hits
+    check_flags(fx, h)
