@@ -6,13 +6,20 @@ epilogue, FL search over the whole output tensor, requantization), max-pool,
 residual adds (FL search + requant), global avg-pool (+ FxP-QLayer) and the
 final FC to integer logits.  Parameters are quantized once during set-up
 (weight FL searches are not part of a calibration step).  Inputs are resident
-in HBM before timing starts.
+in HBM before timing starts.  The runner predicts each C-Block's and each
+eltwise FxP-QLayer's window from the previous forward on the same batch and
+reruns the standard calls from the first failed prediction, so every
+forward's results are the standard calls' bits; the timed forwards are the
+repeated (warm) ones, and the line also reports cold forwards.
 
-Roofline: the FL-search window pass (k_fls_window); the library brackets each
-of its launches in the last forward of the timed region with pre-created HIP
-events on its stream (fxpq_timer_start / fxpq_timer_read).
-`traffic` comes from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE summary
-and is reported only while the kernel sources match the profiled ones.
+Roofline: the predicted C-Block, the kernel that takes most of the forward:
+conv + epilogue + the FL-search window + codes in one contraction, bound by
+its fp64 / int32 vector arithmetic (PRED_OPS_PER_VALUE lane-ops per output
+value against 256 CUs x 64 lanes x 2.4 GHz), timed by the library's events
+(fxpq_timer_start / fxpq_timer_read).  `traffic` comes from the committed
+rocprofv3 FETCH_SIZE / WRITE_SIZE summary and is reported only while the
+kernel sources match the profiled ones.  The contraction alone, the window
+passes and per-layer rooflines are reported beside it.
 
 Prints ONE JSON line.  --gpus above 1 exits: this build runs on one GPU.
 """
@@ -29,9 +36,16 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 INT8_PEAK_TOPS = 5000.0
+# fp64 / int32 vector ALU: 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz lane-ops/s
+ALU_PEAK_TOPS = 256 * 64 * 2.4e9 / 1e12
+# lane-ops per output value the predicted C-Block's epilogue must execute:
+# value (colsum restore, convert, Scale / bias fma, ReLU) 4; per window
+# candidate (scale, round, clamp, sum q^2, sum W q) 2 x 5; clipping bound 3;
+# sum W^2 1; min / max 2; code (convert, pack) 2
+PRED_OPS_PER_VALUE = 22
 BATCH, IMAGE = 256, 224
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "fl_search_window_resnet50_b256_traffic.md")
-WINDOW_SOURCES = ["k_flsearch.hip", "fls.hpp", "values.hpp", "common.hpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cblock_predicted_resnet50_b256_traffic.md")
+WINDOW_SOURCES = ["k_conv.hip", "fls.hpp", "values.hpp", "common.hpp"]
 
 
 def parse():
@@ -55,6 +69,7 @@ def parse():
 
 
 def window_source_hash():
+    """Hash of the sources of the kernel the committed traffic summary covers."""
     h = hashlib.sha256()
     for f in WINDOW_SOURCES:
         with open(os.path.join(ROOT, "paper_2203_12091_amd", "csrc", f), "rb") as fh:
@@ -63,8 +78,8 @@ def window_source_hash():
 
 
 def committed_traffic():
-    """Per-launch HBM bytes of k_fls_window from the committed counter summary,
-    or None when the summary is missing or the kernel changed since."""
+    """Per-launch HBM bytes of the predicted C-Block from the committed counter
+    summary, or None when the summary is missing or the kernel changed since."""
     try:
         text = open(TRAFFIC_FILE).read()
     except OSError:
@@ -403,7 +418,7 @@ def steps_figures(dev):
     return out
 
 
-def conv_rooflines(net, dev):
+def conv_rooflines(net, dev, predict=False):
     """Per conv / FC call of one more (untimed, warm) forward, an event pair
     around each: its int8 TOP/s against its own roofline min(peak, AI x HBM
     peak), AI = int8 ops per HBM byte the call must move: input codes and
@@ -416,9 +431,9 @@ def conv_rooflines(net, dev):
     classes = ("qconv", "cblock_pred")
     net.prepare_timers(1, classes=classes)
     m0 = net.misses
-    net.forward()
+    net.forward(predict=predict)
     torch.cuda.synchronize(dev)
-    run = net.pcalls if net.predict else net.calls
+    run = net.pcalls if (net.predict and predict) else net.calls
     calls = [c for c in run if c[0] in classes]
     assert net.misses == m0 and len(calls) == len(net.timers), "a warm forward missed"
     names = [n.name for op, n, *r in net.ops if op in ("conv", "fc")]
@@ -439,9 +454,13 @@ def conv_rooflines(net, dev):
         ai = work / hbm
         roof = min(INT8_PEAK_TOPS, ai * HBM_PEAK_GBS / 1000.0)
         tops = work / (t * 1e-3) / 1e12
-        per.append({"layer": name, "call": cls, "M": m, "N": n_, "K": k, "ms": round(t, 4),
-                    "tops": round(tops, 1), "ai": round(ai, 1), "roofline_tops": round(roof, 1),
-                    "frac_of_roofline": round(tops / roof, 3)})
+        e = {"layer": name, "call": cls, "M": m, "N": n_, "K": k, "ms": round(t, 4),
+             "tops": round(tops, 1), "ai": round(ai, 1), "roofline_tops": round(roof, 1),
+             "frac_of_roofline": round(tops / roof, 3)}
+        if cls == "cblock_pred":
+            alu = PRED_OPS_PER_VALUE * m * n_ / (t * 1e-3) / 1e12
+            e.update(alu_tops=round(alu, 2), alu_frac=round(alu / ALU_PEAK_TOPS, 3))
+        per.append(e)
         if ai > ridge:
             ops += work
             ms += t
@@ -459,18 +478,37 @@ def conv_rooflines(net, dev):
 
 
 def contraction_times(net):
-    """(ms, launches, int8 ops) of every contraction of one forward: the
-    fxpq_qconv / fxpq_qgemm kernels and the predicted C-Blocks' (one more
-    untimed forward each)."""
+    """(ms, launches, int8 ops) of the contraction alone: every conv / FC of
+    one more (untimed) forward with the standard calls (fxpq_qconv /
+    fxpq_qgemm, int32 accumulators)."""
     from paper_2203_12091_amd import fxpq as fx
-    tot = [0.0, 0, 0.0]
-    for kind in (fx.TIMER_QCONV, fx.TIMER_CBLOCK_PRED):
-        fx.timer_start(net.h, kind)
-        net.forward()
-        for i, v in enumerate(fx.timer_read(net.h)):
-            tot[i] += v
+    fx.timer_start(net.h, fx.TIMER_QCONV)
+    net.forward(predict=False)
+    out = fx.timer_read(net.h)
     fx.timer_start(net.h, fx.TIMER_OFF)
-    return tuple(tot)
+    return out
+
+
+def predicted_times(net):
+    """(ms, launches, int8 ops, output values) of the predicted C-Blocks of
+    one more (untimed, warm) forward."""
+    from paper_2203_12091_amd import fxpq as fx
+    if not net.predict:
+        return 0.0, 0, 0.0, 0
+    vals = 0
+    for cls, work, fn, args in net.pcalls:
+        if cls == "cblock_pred":
+            d = args[1]._obj
+            ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
+            wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
+            vals += d.n * ho * wo * d.k
+    fx.timer_start(net.h, fx.TIMER_CBLOCK_PRED)
+    m0 = net.misses
+    net.forward()
+    ms, n, ops = fx.timer_read(net.h)
+    fx.timer_start(net.h, fx.TIMER_OFF)
+    assert net.misses == m0, "a warm forward missed"
+    return ms, n, ops, vals
 
 
 def cold_forward_ms(net, dev, reps=3):
@@ -676,16 +714,18 @@ def main():
         print(f"bench.py: device flags {res['flags']:#x}", file=sys.stderr)
         sys.exit(1)
 
-    # more (untimed) forwards for the contraction and requant figures
+    # more (untimed) forwards: the predicted C-Blocks (the dominant kernel),
+    # the contraction alone and the requantization (standard calls), the
+    # per-layer rooflines of both, cold forwards
+    pr_ms, pr_n, pr_ops, pr_vals = predicted_times(net)
     cv_ms, cv_n, cv_ops = contraction_times(net)
     fx.timer_start(net.h, fx.TIMER_REQUANT)
-    net.forward()
+    net.forward(predict=False)
     rq_ms, rq_n, rq_bytes = fx.timer_read(net.h)
-    fx.timer_start(net.h, fx.TIMER_CBLOCK_PASS)
-    net.forward()
-    cb_ms, cb_n, cb_ops = fx.timer_read(net.h)
     fx.timer_start(net.h, fx.TIMER_OFF)
-    cbound, per_layer, own = conv_rooflines(net, dev)
+    net.forward()
+    cbound, per_layer, own = conv_rooflines(net, dev, predict=False)
+    _, per_pred, _ = conv_rooflines(net, dev, predict=True) if net.predict else (None, [], None)
     cold_ms, miss_ms = cold_forward_ms(net, dev)
     net.forward()  # back to the steady state (formats of the batch known)
 
@@ -693,6 +733,7 @@ def main():
     value = BATCH * args.steps / elapsed
     achieved = win_bytes / (win_ms * 1e-3) / 1e9
     traffic = committed_traffic()
+    pr_alu = PRED_OPS_PER_VALUE * pr_vals / (pr_ms * 1e-3) / 1e12 if pr_ms else 0.0
     out = {
         "metric": "calibration images/s (ResNet-50 b256 DFX); FL-search GB/s; int8 MFMA % peak",
         "value": round(value, 2),
@@ -713,12 +754,19 @@ def main():
                    "parallelism": "single_gpu", "predicted_cblocks": sum(
                        1 for c in (net.pcalls if net.predict else []) if c[0] == "cblock_pred"),
                    "timed_forwards_rerun": timed_misses},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
-                     "traffic": traffic, "kernel": "k_fls_window", "launches": win_n,
-                     "avg_launch_ms": round(win_ms / max(win_n, 1), 5),
-                     "algorithmic_bytes_per_launch": round(win_bytes / max(win_n, 1))},
+        "roofline": {"bound": "alu", "achieved": round(pr_alu, 2), "peak": round(ALU_PEAK_TOPS, 2),
+                     "unit": "TOP/s", "frac": round(pr_alu / ALU_PEAK_TOPS, 4), "traffic": traffic,
+                     "kernel": "k_qconv predicted C-Block (conv + epilogue + FL-search window + codes)",
+                     "launches": pr_n, "avg_launch_ms": round(pr_ms / max(pr_n, 1), 5),
+                     "algorithmic_ops_per_launch": round(PRED_OPS_PER_VALUE * pr_vals / max(pr_n, 1)),
+                     "ops_per_output_value": PRED_OPS_PER_VALUE, "ms_per_forward": round(pr_ms, 3),
+                     "int8_tops": round(pr_ops / (pr_ms * 1e-3) / 1e12, 1) if pr_ms else None},
         "fl_search_gbs": round(achieved, 1),
+        "fl_search": {"kernel": "predicted / standard FL-search window passes over the network input "
+                                "and the eltwise sums", "achieved": round(achieved, 1), "unit": "GB/s",
+                      "frac": round(achieved / HBM_PEAK_GBS, 4), "launches": win_n,
+                      "ms_per_forward": round(win_ms, 3),
+                      "algorithmic_bytes_per_launch": round(win_bytes / max(win_n, 1))},
         "mfma": {"kernel": "k_qconv", "achieved": round(cv_ops / (cv_ms * 1e-3) / 1e12, 1),
                  "unit": "TOP/s", "peak": INT8_PEAK_TOPS,
                  "frac": round(cv_ops / (cv_ms * 1e-3) / 1e12 / INT8_PEAK_TOPS, 4),
@@ -731,10 +779,7 @@ def main():
         out["mfma"]["compute_bound_layers"] = cbound
     out["mfma"]["own_roofline"] = own
     out["mfma"]["per_layer"] = per_layer
-    if cb_n:
-        out["fused_cblock"] = {"kernel": "k_qconv (min/max, FL-window and requant epilogues)",
-                               "passes": cb_n, "ms_per_forward": round(cb_ms, 3),
-                               "executed_tops": round(cb_ops / max(cb_ms, 1e-9) * 1e-9, 1)}
+    out["predicted_cblock"] = {"per_layer": per_pred}
     if not args.no_sweep:
         out["sweep"] = sweep_figures(dev)
     net.close()
