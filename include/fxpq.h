@@ -242,7 +242,7 @@ fxpq_status fxpq_fl_search(fxpq_handle h, const fxpq_src* src, int64_t n, int32_
  * resident-capped grids on one MI355X), or more than 2^16 - 4096 window
  * blocks (the limit of fxpq_fl_search).
  */
-#define FXPQ_STATIC_SCRATCH_BYTES 1269760
+#define FXPQ_STATIC_SCRATCH_BYTES 1271808
 fxpq_status fxpq_fl_search_static(const fxpq_src* src, int64_t n, int32_t wl, int32_t sign,
                                   int32_t fl_lo, int32_t fl_hi, fxpq_fmt* d_fmt_out,
                                   double* d_sse, void* hip_stream);

@@ -12,7 +12,9 @@ constexpr int kThreads = 256;        // threads per block of the streaming kerne
 constexpr int kMaxStreamBlocks = 2048;
 constexpr int kMaxConvBlocks = 1 << 20;
 constexpr int kWindow = 2;           // candidates of the first FL-search pass
-constexpr int kWinPart = 6 * kWindow;  // int64 per slot of window-pass sums
+constexpr int kWinSums = 6 * kWindow;  // int64 window-pass sums per slot
+// int64 per slot: the sums, then the min / max keys of a predicted call
+constexpr int kWinPart = kWinSums + 2;
 constexpr int kWinSlots = 64;          // slots the window-pass blocks add into (block % kWinSlots)
 // Clipping-error lower bounds the window pass can take above its candidates
 // (at fl = b1 + 1, b1 + 2, ...), and fp64 sums per slot: sum W^2 and the bounds.
@@ -218,7 +220,7 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
                             int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y,
                             double* d_minmax, unsigned* miss);
 hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int sign, int fl_lo,
-                           int fl_hi, int64_t per_thread, int nb, double* d_minmax, fxpq_fmt* out,
+                           int fl_hi, int64_t per_thread, double* d_minmax, fxpq_fmt* out,
                            unsigned* miss);
 hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign,
                               int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, double* d_minmax,

@@ -299,7 +299,7 @@ __device__ inline void win_verdict_write(const WinSetup& ws, int wl, int fl_lo, 
 
 // LDS table of the block reduction (one row per wave of a 256-thread block).
 struct WinShared {
-  long long i[4][kWinPart];
+  long long i[4][kWinSums];
   double f[4][kWinPartF];
 };
 
@@ -311,11 +311,42 @@ __device__ inline void slot_add(double* p, double v) {
   __hip_atomic_fetch_add(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Min / max of a predicted call, combined across blocks without a finish
+// pass: each fp64 value maps to an unsigned key that orders like the value
+// (mm_key), and the slot keeps the 64-bit atomic maximum of the key of the
+// max (at kWinSums + 1) and of the complemented key of the min (at
+// kWinSums).  Every key of a non-NaN value is above 0, so a cleared slot
+// means "no value".
+__device__ inline unsigned long long mm_key(double v) {
+  const long long b = __double_as_longlong(v);
+  return (unsigned long long)(b >= 0 ? b : b ^ 0x7FFFFFFFFFFFFFFFll) ^ 0x8000000000000000ull;
+}
+__device__ inline double mm_unkey(unsigned long long k) {
+  const long long b = (long long)(k ^ 0x8000000000000000ull);
+  return __longlong_as_double(b >= 0 ? b : b ^ 0x7FFFFFFFFFFFFFFFll);
+}
+__device__ inline void slot_max(long long* p, unsigned long long v) {
+  __hip_atomic_fetch_max(reinterpret_cast<unsigned long long*>(p), v, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+}
+// Every lane of the wave passes its min / max (mn > mx: none); lane 0 adds
+// the wave's into slot bid % kWinSlots.
+__device__ inline void mm_slot_add(double mn, double mx, int64_t bid, long long* part_i) {
+  mn = wave_reduce(mn, OpMin());
+  mx = wave_reduce(mx, OpMax());
+  if ((threadIdx.x & 63) == 0 && mn <= mx) {
+    long long* p = part_i + (int)(bid % kWinSlots) * kWinPart + kWinSums;
+    slot_max(p, ~mm_key(mn));
+    slot_max(p + 1, mm_key(mx));
+  }
+}
+
 // Block results of the window pass (256 threads).  Each exact per-thread sum
 // (below 2^62) is split into its high and low 32-bit halves, summed
 // separately over the block and added (int64 atomics: exact, order-free) into
 // slot bid % kWinSlots of part_i (kWinPart int64 per slot: per candidate A
-// hi/lo, PH hi/lo, PL hi/lo); the fp64 bound sums (sum W^2, then nb clipping
+// hi/lo, PH hi/lo, PL hi/lo, then two min / max keys, see mm_slot_add); the
+// fp64 bound sums (sum W^2, then nb clipping
 // bounds) go to part_f (kWinPartF per slot).  The search's decision reads the
 // slots; the next search's decision clears them.
 __device__ inline void win_write_partials_i64(const long long* A, const long long* PH,
@@ -326,7 +357,7 @@ __device__ inline void win_write_partials_i64(const long long* A, const long lon
   // table; after one barrier thread t adds the four rows of quantity t and
   // adds the result into the slot.
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  long long q[kWinPart];
+  long long q[kWinSums];
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
     const long long q3[3] = {A[j], PH[j], PL[j]};
@@ -341,22 +372,22 @@ __device__ inline void win_write_partials_i64(const long long* A, const long lon
 #pragma unroll
   for (int k = 0; k < kCeBounds; ++k) f[1 + k] = (k < nb) ? CE[k] : 0.0;
 #pragma unroll
-  for (int i = 0; i < kWinPart; ++i) q[i] = wave_reduce(q[i], OpAddL());
+  for (int i = 0; i < kWinSums; ++i) q[i] = wave_reduce(q[i], OpAddL());
 #pragma unroll
   for (int i = 0; i < kWinPartF; ++i) f[i] = wave_reduce(f[i], OpAddD());
   if (lane == 0) {
 #pragma unroll
-    for (int i = 0; i < kWinPart; ++i) sh.i[w][i] = q[i];
+    for (int i = 0; i < kWinSums; ++i) sh.i[w][i] = q[i];
 #pragma unroll
     for (int i = 0; i < kWinPartF; ++i) sh.f[w][i] = f[i];
   }
   __syncthreads();
   const int t = threadIdx.x;
   const int slot = (int)(bid % kWinSlots);
-  if (t < kWinPart) {
+  if (t < kWinSums) {
     slot_add(part_i + slot * kWinPart + t, sh.i[0][t] + sh.i[1][t] + sh.i[2][t] + sh.i[3][t]);
-  } else if (t < kWinPart + 1 + nb) {
-    const int i = t - kWinPart;
+  } else if (t < kWinSums + 1 + nb) {
+    const int i = t - kWinSums;
     slot_add(part_f + kWinPartF * slot + i, ((sh.f[0][i] + sh.f[1][i]) + sh.f[2][i]) + sh.f[3][i]);
   }
 }
@@ -375,19 +406,20 @@ __device__ inline void win_write_partials(const WinAcc& acc, int nb, int64_t bid
 // Block results of a window pass over integer values (no W split: PH is
 // zero).  Fewer reductions than win_write_partials: sum q^2 per candidate is
 // reduced in fp64, where it is exact (below 2^53 for word lengths up to 16
-// and at most 2^17 values per block); sum W q as the 32-bit halves of its
-// exact per-thread int64; the bound sums in fp64.  Same slot contents.
-__device__ inline void win_write_partials_int(const WinAcc& acc, int nb, int64_t bid,
-                                              long long* part_i, double* part_f, WinShared& sh) {
+// and at most 2^17 values per block); sum W q as the 32-bit halves of the
+// thread's exact int64 sum wq (below 2^62); the bound sums in fp64.  Same
+// slot contents.
+__device__ inline void win_write_partials_wq(const WinAcc& acc, const long long* wq, int nb,
+                                             int64_t bid, long long* part_i, double* part_f,
+                                             WinShared& sh) {
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   double a[kWindow];
   long long ph[kWindow], pl[kWindow];
 #pragma unroll
   for (int j = 0; j < kWindow; ++j) {
     a[j] = wave_reduce(acc.A[j], OpAddD());
-    const long long p = exact_i64(acc.PL[j]);
-    ph[j] = wave_reduce(p >> 32, OpAddL());
-    pl[j] = wave_reduce(p & 0xFFFFFFFFll, OpAddL());
+    ph[j] = wave_reduce(wq[j] >> 32, OpAddL());
+    pl[j] = wave_reduce(wq[j] & 0xFFFFFFFFll, OpAddL());
   }
   double f[kWinPartF];
   f[0] = wave_reduce(acc.V2, OpAddD());
@@ -410,13 +442,22 @@ __device__ inline void win_write_partials_int(const WinAcc& acc, int nb, int64_t
   __syncthreads();
   const int t = threadIdx.x;
   const int slot = (int)(bid % kWinSlots);
-  if (t < kWinPart) {
+  if (t < kWinSums) {
     if ((t % 6) != 2 && (t % 6) != 3)
       slot_add(part_i + slot * kWinPart + t, sh.i[0][t] + sh.i[1][t] + sh.i[2][t] + sh.i[3][t]);
-  } else if (t < kWinPart + 1 + nb) {
-    const int i = t - kWinPart;
+  } else if (t < kWinSums + 1 + nb) {
+    const int i = t - kWinSums;
     slot_add(part_f + kWinPartF * slot + i, ((sh.f[0][i] + sh.f[1][i]) + sh.f[2][i]) + sh.f[3][i]);
   }
+}
+
+// The same with the sums of W * q still in fp64 (exact below 2^53).
+__device__ inline void win_write_partials_int(const WinAcc& acc, int nb, int64_t bid,
+                                              long long* part_i, double* part_f, WinShared& sh) {
+  long long wq[kWindow];
+#pragma unroll
+  for (int j = 0; j < kWindow; ++j) wq[j] = exact_i64(acc.PL[j]);
+  win_write_partials_wq(acc, wq, nb, bid, part_i, part_f, sh);
 }
 
 // Launch helpers shared by the streaming search and the fused C-Block.

@@ -850,12 +850,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       mn = fmin(mn, fmin(f0, f1));
       mx = fmax(mx, fmax(f0, f1));
     }
-    mn = block_reduce(mn, OpMin(), shd);
-    mx = block_reduce(mx, OpMax(), shd);
-    if (tid == 0) {
-      a.mm_part[2 * bid] = mn;
-      a.mm_part[2 * bid + 1] = mx;
-    }
+    // into the slots, beside the window sums (no per-block partials to finish)
+    mm_slot_add(mn, mx, bid, a.part_i);
   } else {  // EPI_REQ
     visit([&](int v, double Mc, double Ac, int row, int col) {
       const double val = fmax(fma((double)v, Mc, Ac), relo);
@@ -1083,9 +1079,7 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
   // state of this epilogue do not fit the registers of two blocks per CU
   const dim3 grid = conv_setup(d, x, x_type, w, colsum, &ep, a, loader, cfg, c.cus,
                                FXPQ_TILING_GEMM, false);
-  const int nb = (int)(grid.x * grid.y);
   a.want_mm = 1;
-  a.mm_part = c.sc.minmax_part;
   a.wl = wl;
   a.sign_req = sign;
   a.fl_lo = fl_lo;
@@ -1103,8 +1097,8 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
   timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  return launch_pred_fin(c, ep, set, wl, sign, fl_lo, fl_hi, conv_per_thread(cfg), nb, d_minmax,
-                         out, miss);
+  return launch_pred_fin(c, ep, set, wl, sign, fl_lo, fl_hi, conv_per_thread(cfg), d_minmax, out,
+                         miss);
 }
 
 }  // namespace fxpq

@@ -193,10 +193,8 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
 template <int KIND, int DT, int NB>
 __global__ __launch_bounds__(kThreads) void k_qlayer_pred(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int64_t per_thread,
-    const double* mm, long long* part_i, double* part_f, double* mm_part, const fxpq_fmt* out,
-    int8_t* y) {
+    const double* mm, long long* part_i, double* part_f, const fxpq_fmt* out, int8_t* y) {
   __shared__ WinShared wsh;
-  __shared__ double shd[kThreads / 64];
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const FlsU& u = ws.u;
   double mn = INFINITY, mx = -INFINITY;
@@ -233,12 +231,7 @@ __global__ __launch_bounds__(kThreads) void k_qlayer_pred(
         mx = max64(mx, vi);
       }
   }
-  mn = block_reduce(mn, OpMin(), shd);
-  mx = block_reduce(mx, OpMax(), shd);
-  if (threadIdx.x == 0) {
-    mm_part[2 * blockIdx.x] = mn;
-    mm_part[2 * blockIdx.x + 1] = mx;
-  }
+  mm_slot_add(mn, mx, blockIdx.x, part_i);
 }
 
 // Bits of |v| (0 for v == 0).
@@ -408,40 +401,25 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
   if (threadIdx.x == 0) win_record(ws, r, wl, 0, plan, out);
 }
 
-// Decision of a predicted C-Block or FxP-QLayer (one block of 1024 threads,
-// after the pass): reduces the pass's min / max partials to this call's
-// exact min / max, and checks that the window its epilogue evaluated (from
-// the predicted min / max held in mm) is this call's window: same verdict 0,
-// candidates, clipping bound, sign and variant.  Then one wave decides from
-// the window sums; the format is recorded when the decision is final and is
-// the candidate whose codes the epilogue wrote, else *miss is set.  mm ends
-// with this call's min / max; the other slot set is cleared for the next
-// search.
-constexpr int kPredFinThreads = 1024;
-
+// Decision of a predicted C-Block or FxP-QLayer (one wave, after the pass):
+// combines the min / max keys of the slots into this call's exact min / max
+// and checks that the window the pass evaluated (from the predicted min / max
+// held in mm) is this call's window: same verdict 0, candidates, clipping
+// bound, sign and variant.  Then the wave decides from the window sums; the
+// format is recorded when the decision is final and is the candidate whose
+// codes the pass wrote, else *miss is set.  mm ends with this call's
+// min / max; the other slot set is cleared for the next search.
 template <int KIND>
-__global__ __launch_bounds__(kPredFinThreads) void k_pred_fin(
-    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int nce, int64_t per_thread, const double* part_mm,
-    int nb, double* mm, const long long* part_i, const double* part_f, long long* clr_i,
-    double* clr_f, fxpq_fmt* out, unsigned* miss) {
-  __shared__ double sh[kPredFinThreads / 64];
-  __shared__ double act_sh[2];
+__global__ __launch_bounds__(kFinThreads) void k_pred_fin(
+    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int nce, int64_t per_thread, double* mm,
+    const long long* part_i, const double* part_f, long long* clr_i, double* clr_f, fxpq_fmt* out,
+    unsigned* miss) {
   const double pred[2] = {mm[0], mm[1]};
-  double mn = INFINITY, mx = -INFINITY;
-  for (int i = threadIdx.x; i < nb; i += blockDim.x) {
-    mn = fmin(mn, part_mm[2 * i]);
-    mx = fmax(mx, part_mm[2 * i + 1]);
-  }
-  mn = block_reduce(mn, OpMin(), sh);
-  mx = block_reduce(mx, OpMax(), sh);
+  const long long* p = part_i + (threadIdx.x & 63) * kWinPart + kWinSums;
+  const unsigned long long kmn = wave_reduce((unsigned long long)p[0], OpMaxU());
+  const unsigned long long kmx = wave_reduce((unsigned long long)p[1], OpMaxU());
+  const double act[2] = {kmn ? mm_unkey(~kmn) : INFINITY, kmx ? mm_unkey(kmx) : -INFINITY};
   win_slots_clear(clr_i, clr_f);
-  if (threadIdx.x == 0) {
-    act_sh[0] = mn;
-    act_sh[1] = mx;
-  }
-  __syncthreads();
-  if (threadIdx.x >= 64) return;
-  const double act[2] = {act_sh[0], act_sh[1]};
   const WinSetup wp = win_setup<KIND>(s, pred, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const WinSetup wa = win_setup<KIND>(s, act, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const bool same = wp.verdict == 0 && wa.verdict == 0 && wp.b0 == wa.b0 && wp.b1 == wa.b1 &&
@@ -817,12 +795,12 @@ hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int s
 }
 
 hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int sign, int fl_lo,
-                           int fl_hi, int64_t per_thread, int nb, double* d_minmax, fxpq_fmt* out,
+                           int fl_hi, int64_t per_thread, double* d_minmax, fxpq_fmt* out,
                            unsigned* miss) {
   const int nce = 1;  // the conv epilogue evaluates one clipping bound
-  k_pred_fin<FXPQ_SRC_ACC><<<1, kPredFinThreads, 0, c.stream>>>(
-      ep, wl, sign, fl_lo, fl_hi, nce, per_thread, c.sc.minmax_part, nb, d_minmax, slots_i(c, set),
-      slots_f(c, set), slots_i(c, 1 - set), slots_f(c, 1 - set), out, miss);
+  k_pred_fin<FXPQ_SRC_ACC><<<1, kFinThreads, 0, c.stream>>>(
+      ep, wl, sign, fl_lo, fl_hi, nce, per_thread, d_minmax, slots_i(c, set), slots_f(c, set),
+      slots_i(c, 1 - set), slots_f(c, 1 - set), out, miss);
   return hipGetLastError();
 }
 
@@ -843,14 +821,12 @@ hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
     per_thread = window_per_thread(n, blocks, vec);
     bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
     kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, per_thread, d_minmax,
-                                              slots_i(c, set), slots_f(c, set), c.sc.minmax_part,
-                                              out, y);
+                                              slots_i(c, set), slots_f(c, set), out, y);
     const double elem = (s.kind == FXPQ_SRC_ADD) ? 2.0 : 4.0;
     timer_end(c, timed, (elem + 1.0) * (double)n);
-    fin<<<1, kPredFinThreads, 0, c.stream>>>(s, wl, sign, fl_lo, fl_hi, nce, per_thread,
-                                             c.sc.minmax_part, blocks, d_minmax, slots_i(c, set),
-                                             slots_f(c, set), slots_i(c, 1 - set),
-                                             slots_f(c, 1 - set), out, miss);
+    fin<<<1, kFinThreads, 0, c.stream>>>(s, wl, sign, fl_lo, fl_hi, nce, per_thread, d_minmax,
+                                         slots_i(c, set), slots_f(c, set), slots_i(c, 1 - set),
+                                         slots_f(c, 1 - set), out, miss);
   };
 #define FXPQ_QPRED(K, D)                                                            \
   (nce == 1 ? run(&k_qlayer_pred<K, D, 1>, &k_pred_fin<K>)                         \

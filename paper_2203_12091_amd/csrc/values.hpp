@@ -368,6 +368,11 @@ struct OpAddD {
 struct OpAddL {
   __device__ long long operator()(long long a, long long b) const { return a + b; }
 };
+struct OpMaxU {
+  __device__ unsigned long long operator()(unsigned long long a, unsigned long long b) const {
+    return a > b ? a : b;
+  }
+};
 
 
 
