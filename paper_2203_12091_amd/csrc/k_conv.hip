@@ -293,6 +293,19 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       if (want_vals) eraw[ni] = epi_channel_load(a.ep, cc);
     }
   };
+  // EPI_PRED: the accumulators start at the restoring term 128 * (sum of
+  // the filter's codes) of inputs stored as u - 128 (zero otherwise), so the
+  // matrix cores return the restored accumulator (exact in int32 like it)
+  auto acc_start = [&]() {
+    if constexpr (EPI == EPI_PRED) {
+#pragma unroll
+      for (int ni = 0; ni < TN; ++ni)
+#pragma unroll
+        for (int mi = 0; mi < TM; ++mi)
+#pragma unroll
+          for (int e = 0; e < 16; ++e) acc[mi][ni][e] = 128 * csum[ni];
+    }
+  };
   const int ktiles = (a.kdepth + BK - 1) / BK;
   const int hw_out = a.Ho * a.Wo;
   const int taps = a.R * a.S;
@@ -362,6 +375,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     epi_loads();
     issue(0, A0, B0);
     if (ktiles > 1) issue(1, A1, B1);
+    acc_start();
     for (int kt = 0; kt < ktiles; kt += 3) {
       step(kt, A0, B0, A2, B2);
       if (kt + 1 < ktiles) step(kt + 1, A1, B1, A0, B0);
@@ -580,6 +594,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     gload(0);
     epi_loads();
     lstore(0);
+    acc_start();
     __syncthreads();
     for (int kt = 0; kt < ktiles; ++kt) {
       const int buf = kt & 1;
@@ -746,6 +761,9 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     // codes leave as dwords: a lane holds one column at 4 consecutive rows
     // (e = 4g .. 4g + 3), and a 4 x 4 byte transpose inside each lane quad
     // (two DPP exchanges) gives lane 4k + j row j at 4 consecutive columns.
+    // Full tiles run straight-line code without checks; partial tiles check
+    // every value (as straight-line selects their 64 compare masks would not
+    // fit the registers).
     const FlsU& u = ws.u;
     const bool win = ws.verdict == 0;
     const int pj = pred_pick(ws, *a.fmt_win);
@@ -765,17 +783,13 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       lo[ni] = INT_MAX;
       hi[ni] = INT_MIN;
     }
-    // Every value is checked against the tile's extent even in full tiles:
-    // as straight-line code over 64 values the unchecked form runs out of
-    // registers, and the checks keep the live ranges short.
-    auto tile = [&](auto nn, auto c0, auto wn_, auto pj_) {
+    auto tile = [&](auto nn, auto c0, auto wn_, auto pj_, auto full_) {
       constexpr bool NN = decltype(nn)::value, C0 = decltype(c0)::value;
-      constexpr bool WIN = decltype(wn_)::value;
+      constexpr bool WIN = decltype(wn_)::value, FULL = decltype(full_)::value;
       constexpr int PJ = decltype(pj_)::value ? 1 : 0;
 #pragma unroll
       for (int ni = 0; ni < TN; ++ni) {
         const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
-        const int corr = 128 * csum[ni];
         double Mc, Ac;
         epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
         const int scol = n0 + wn * WCOLS + ni * 32 + ((lane & 31) & ~3);
@@ -784,26 +798,29 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
 #pragma unroll
           for (int g = 0; g < 4; ++g) {
             const int rbase = m0 + wm * WROWS + mi * 32 + 8 * g + 4 * (lane >> 5);
-            unsigned w4 = 0;
+            int c[4];
 #pragma unroll
             for (int jj = 0; jj < 4; ++jj) {
-              const int v = acc[mi][ni][4 * g + jj] + corr;
-              const bool ok = full || (rbase + jj < a.M && col < a.K);
+              const int v = acc[mi][ni][4 * g + jj];
+              const bool ok = FULL || (rbase + jj < a.M && col < a.K);
               lo[ni] = min(lo[ni], ok ? v : INT_MAX);
               hi[ni] = max(hi[ni], ok ? v : INT_MIN);
+              c[jj] = 0;
               if constexpr (WIN) {
-                int c = 0;
                 if (ok) {
                   const double W = max64s(fma((double)v, Mc, Ac), relo);
                   double q[kWindow];
                   win_consume<false, NN, C0>(wc, wa, W, q);
-                  c = (int)q[PJ];
-                  if (PJ == 0 && !C0) c = min(c, qmax);
+                  c[jj] = (int)q[PJ];
+                  if (PJ == 0 && !C0) c[jj] = min(c[jj], qmax);
                 }
-                w4 |= (unsigned)(c & 0xFF) << (8 * jj);
               }
             }
             if constexpr (WIN) {
+              // the four codes' low bytes into one dword (row jj in byte jj)
+              const unsigned p01 = __builtin_amdgcn_perm((unsigned)c[1], (unsigned)c[0], 0x0C0C0400u);
+              const unsigned p23 = __builtin_amdgcn_perm((unsigned)c[3], (unsigned)c[2], 0x0C0C0400u);
+              unsigned w4 = __builtin_amdgcn_perm(p23, p01, 0x05040100u);
               // lane j of the quad holds rows 0..3 of column j: transpose
               // (branch-free: every lane computes both forms and keeps one)
               const unsigned x1 = (unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0xB1, 0xF, 0xF, false);
@@ -815,9 +832,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
               const unsigned e2 = (w4 & 0x0000FFFFu) | ((x2 & 0x0000FFFFu) << 16);
               w4 = e2 ^ ((o2 ^ e2) & m2);
               const int srow = rbase + qj;
-              if (srow < a.M && scol < a.K)
+              if (FULL || (srow < a.M && scol < a.K))
                 *reinterpret_cast<unsigned*>(a.y + (int64_t)srow * a.K + scol) = w4 ^ xorw;
-
             }
           }
         }
@@ -826,10 +842,13 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     using F = std::false_type;
     using T = std::true_type;
     if (!win) {
-      tile(F(), F(), F(), F());
+      if (full) tile(F(), F(), F(), F(), T());
+      else tile(F(), F(), F(), F(), F());
     } else {
       const int var = win_variant(u, ws, a.mm);
-#define FXPQ_PRED_TILE(NN, C0) (pj ? tile(NN(), C0(), T(), T()) : tile(NN(), C0(), T(), F()))
+#define FXPQ_PRED_TILE(NN, C0)                                                                  \
+  (full ? (pj ? tile(NN(), C0(), T(), T(), T()) : tile(NN(), C0(), T(), F(), T()))              \
+        : (pj ? tile(NN(), C0(), T(), T(), F()) : tile(NN(), C0(), T(), F(), F())))
       switch (var) {
         case 0: FXPQ_PRED_TILE(F, F); break;
         case 1: FXPQ_PRED_TILE(F, T); break;
