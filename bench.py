@@ -237,7 +237,7 @@ def qparams_figures(dev, batch=32, image=224):
 def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     """Bit-precision level reduction (Algorithm 2) on a calibration batch:
     ResNet-18 from two initial designs, 8-bit everywhere (biases 32) and the
-    paper's wide first / last layers (16-bit input, first and last weights
+    paper's wide first / last layers (32-bit input, first and last weights
     and last-layer input, over wide C-Blocks), and AlexNet and VGG-16 from
     the 8-bit design.  Each: the forward
     optimizer first (untimed set-up), then Algorithm 2 to convergence (or
@@ -248,7 +248,7 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
     from paper_2203_12091_amd import qparams, reduction
     out = {"metric": "bit-precision reduction (Algorithm 2) seconds", "batch": batch,
            "image": image, "threshold": thld, "max_changes": max_changes}
-    runs = (("resnet18", "design_8bit", None), ("resnet18", "design_wide16", 16),
+    runs = (("resnet18", "design_8bit", None), ("resnet18", "design_wide32", 32),
             ("alexnet", "design_8bit", None), ("vgg16", "design_8bit", None))
     for net, design, flw in runs:
         design = f"{net}_{design}"

@@ -55,8 +55,10 @@ typedef enum {
   FXPQ_I32 = 3,
   FXPQ_I64 = 4,
   FXPQ_F32 = 5,
-  FXPQ_C8 = 6     /* 8-bit code whose storage follows the device format: I8 when
+  FXPQ_C8 = 6,    /* 8-bit code whose storage follows the device format: I8 when
                      the format is signed, U8OFF when it is unsigned */
+  FXPQ_U32 = 7    /* unsigned codes of up to 32 bits stored as uint32 (the only
+                     storage an unsigned 32-bit format's codes fit) */
 } fxpq_dtype;
 
 #define FXPQ_SIGN_AUTO (-1) /* Eq. 6: signed iff the smallest value is negative */
@@ -165,8 +167,9 @@ fxpq_status fxpq_sync_status(fxpq_handle h, uint32_t* flags);
 /*
  * Quantize (Eq. 10-12): codes[i] = clip(rne(x[i] * 2^fl), Qmin, Qmax) with the
  * format read from d_fmt (device).  rne rounds half to even.  code_type is
- * FXPQ_I8, FXPQ_U8OFF (unsigned 8-bit formats only), FXPQ_I16 or FXPQ_I32 and
- * must hold the format's code range.  n >= 0; n == 0 launches nothing.
+ * FXPQ_I8, FXPQ_U8OFF (unsigned 8-bit formats only), FXPQ_I16, FXPQ_I32 or
+ * FXPQ_U32 (unsigned formats only) and must hold the format's code range (a
+ * range it cannot hold raises FXPQ_FLAG_CODE and the codes saturate to it).  n >= 0; n == 0 launches nothing.
  * Word lengths 1..32.  A signed 1-bit format follows Eq. 13 (code -1 for
  * x < 0, code 0 otherwise, decoded as +1) and is stored decoded: -1 or +1,
  * so that a C-Block consumes it as it is; the same holds for every call that
@@ -405,8 +408,9 @@ fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const 
  * weights; c % 16 == 0, or c == 4 with each weight row padded with zeros to
  * a multiple of 64; an FC layer is the 1x1 convolution of a 1x1 image).
  * x (device int32[n*h*w*c]) holds codes of the format (wl_x, sign_x),
- * w (device int32[k * row]) codes of (wl_w, sign_w); a signed 1-bit format
- * holds its decoded codes (-1 / +1).  ep (required) is the epilogue, with
+ * w (device int32[k * row]) codes of (wl_w, sign_w): int32 codes for signed
+ * formats, uint32 codes (FXPQ_U32 storage) for unsigned ones; a signed 1-bit
+ * format holds its decoded codes (-1 / +1).  ep (required) is the epilogue, with
  * ep->d_fmt_in the input's format on the device (its fl sets the scale).
  * The result v (device int64[M * k], M = n * Ho * Wo, channels innermost) is
  * the exact C-Block value times 2^s, s written to d_scale (device int32):
@@ -420,9 +424,8 @@ fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const 
  * bytes fxpq_qconv_wide_workspace reports for the same arguments; its
  * contents are unspecified afterwards.  Codes outside their format's range
  * raise FXPQ_FLAG_CODE; values of magnitude 2^62 or more raise
- * FXPQ_FLAG_RANGE and are written as 0.  Requirements: 1 <= wl <= 32 for
- * signed formats, <= 31 for unsigned ones (int32 storage), and every plane
- * contraction within the limits of fxpq_qconv (else its error).
+ * FXPQ_FLAG_RANGE and are written as 0.  Requirements: 1 <= wl <= 32, and
+ * every plane contraction within the limits of fxpq_qconv (else its error).
  */
 fxpq_status fxpq_qconv_wide_workspace(const fxpq_conv_desc* d, int32_t wl_x, int32_t sign_x,
                                       int32_t wl_w, int32_t sign_w, int64_t* bytes);

@@ -40,7 +40,7 @@ def _declare(L):
         "orc_fl_search_i64": [p, i64, i, i, i, i, i, p, p, p],
         "orc_gemm": [p, p, i64, i64, i64, p],
         "orc_conv2d": [p, i, i, i, i, p, i, i, i, i, i, p],
-        "orc_conv2d_point": [p, i, i, i, i, p, i, i, i, i, i, i, i, i, i],
+        "orc_conv2d_point": [p, i, i, i, i, p, i, i, i, i, i, i, i, i, i, p],
         "orc_epilogue": [p, i, i, i64, i, p, i, p, i, p, i, i, p, p],
         "orc_maxpool": [p, i, i, i, i, i, i, i, p],
         "orc_avgpool_global": [p, i, i, i, i64, p],
@@ -53,7 +53,7 @@ def _declare(L):
     for name, args in sigs.items():
         f = getattr(L, name)
         f.argtypes = args
-        f.restype = C.c_int64 if name == "orc_conv2d_point" else C.c_int
+        f.restype = C.c_int
 
 
 def _ptr(a):
@@ -143,8 +143,9 @@ def fl_search_i64(v, s, k, sign=SIGN_AUTO, fl_lo=-8, fl_hi=15):
 
 
 def gemm(A, B):
-    """C[m][n] = sum_k A[m][k] * B[n][k] in int64."""
-    A, B = _i32(A), _i32(B)
+    """C[m][n] = sum_k A[m][k] * B[n][k], exact (codes of up to 32 bits, signed
+    or unsigned); int64 result."""
+    A, B = _i64(A), _i64(B)
     M, K = A.shape
     N = B.shape[0]
     assert B.shape[1] == K
@@ -158,8 +159,8 @@ def conv_out_hw(H, W, R, S, stride, pad):
 
 
 def conv2d(x, w, stride, pad):
-    """Direct convolution, NCHW x KCRS -> NKHW int64."""
-    x, w = _i32(x), _i32(w)
+    """Direct convolution, NCHW x KCRS -> NKHW int64 (codes as gemm)."""
+    x, w = _i64(x), _i64(w)
     N, Cc, H, W = x.shape
     K, C2, R, S = w.shape
     assert C2 == Cc
@@ -171,11 +172,13 @@ def conv2d(x, w, stride, pad):
 
 
 def conv2d_point(x, w, stride, pad, n, k, oh, ow):
-    x, w = _i32(x), _i32(w)
+    x, w = _i64(x), _i64(w)
     N, Cc, H, W = x.shape
     K, _, R, S = w.shape
-    return int(lib().orc_conv2d_point(_ptr(x), N, Cc, H, W, _ptr(w), K, R, S, stride, pad,
-                                      n, k, oh, ow))
+    y = C.c_int64()
+    _check(lib().orc_conv2d_point(_ptr(x), N, Cc, H, W, _ptr(w), K, R, S, stride, pad,
+                                  n, k, oh, ow, C.byref(y)), "conv2d_point")
+    return y.value
 
 
 def epilogue(acc, s_acc, bias=None, fl_b=0, a1=None, fl_a1=0, a2=None, fl_a2=0, relu=False):

@@ -338,23 +338,34 @@ int orc_fl_search_i64(const int64_t* v, int64_t n, int s, int k, int sign, int f
 /* ------------------------------------------------------------------------- */
 /* Integer contraction and convolution.                                       */
 /* ------------------------------------------------------------------------- */
-int orc_gemm(const int32_t* A, const int32_t* B, int64_t M, int64_t N, int64_t K, int64_t* C) {
-  if (M < 0 || N < 0 || K < 0) return ORC_EINVAL;
-#pragma omp parallel for schedule(static)
-  for (int64_t m = 0; m < M; ++m)
-    for (int64_t n = 0; n < N; ++n) {
-      int64_t s = 0;
-      for (int64_t k = 0; k < K; ++k) s += (int64_t)A[m * K + k] * (int64_t)B[n * K + k];
-      C[m * N + n] = s;
-    }
+/* The sum s as int64, or ORC_ERANGE. */
+static int fit_i64(i128 s, int64_t* out) {
+  if (s > (i128)INT64_MAX || s < (i128)INT64_MIN) return ORC_ERANGE;
+  *out = (int64_t)s;
   return ORC_OK;
 }
 
-int64_t orc_conv2d_point(const int32_t* x, int N, int C, int H, int W, const int32_t* w, int K,
-                         int R, int S, int stride, int pad, int n, int k, int oh, int ow) {
+int orc_gemm(const int64_t* A, const int64_t* B, int64_t M, int64_t N, int64_t K, int64_t* C) {
+  if (M < 0 || N < 0 || K < 0) return ORC_EINVAL;
+  int status = ORC_OK;
+#pragma omp parallel for schedule(static)
+  for (int64_t m = 0; m < M; ++m)
+    for (int64_t n = 0; n < N; ++n) {
+      i128 s = 0;
+      for (int64_t k = 0; k < K; ++k) s += (i128)A[m * K + k] * (i128)B[n * K + k];
+      if (fit_i64(s, &C[m * N + n])) {
+#pragma omp atomic write
+        status = ORC_ERANGE;
+      }
+    }
+  return status;
+}
+
+int orc_conv2d_point(const int64_t* x, int N, int C, int H, int W, const int64_t* w, int K,
+                     int R, int S, int stride, int pad, int n, int k, int oh, int ow, int64_t* y) {
   (void)N;
   (void)K;
-  int64_t s = 0;
+  i128 s = 0;
   for (int c = 0; c < C; ++c)
     for (int r = 0; r < R; ++r) {
       int ih = oh * stride - pad + r;
@@ -362,26 +373,30 @@ int64_t orc_conv2d_point(const int32_t* x, int N, int C, int H, int W, const int
       for (int q = 0; q < S; ++q) {
         int iw = ow * stride - pad + q;
         if (iw < 0 || iw >= W) continue;
-        s += (int64_t)x[(((int64_t)n * C + c) * H + ih) * W + iw] *
-             (int64_t)w[(((int64_t)k * C + c) * R + r) * S + q];
+        s += (i128)x[(((int64_t)n * C + c) * H + ih) * W + iw] *
+             (i128)w[(((int64_t)k * C + c) * R + r) * S + q];
       }
     }
-  return s;
+  return fit_i64(s, y);
 }
 
-int orc_conv2d(const int32_t* x, int N, int C, int H, int W, const int32_t* w, int K, int R,
+int orc_conv2d(const int64_t* x, int N, int C, int H, int W, const int64_t* w, int K, int R,
                int S, int stride, int pad, int64_t* y) {
   if (stride < 1 || pad < 0) return ORC_EINVAL;
   int Ho = (H + 2 * pad - R) / stride + 1, Wo = (W + 2 * pad - S) / stride + 1;
   if (Ho < 1 || Wo < 1) return ORC_EINVAL;
+  int status = ORC_OK;
 #pragma omp parallel for collapse(2) schedule(static)
   for (int n = 0; n < N; ++n)
     for (int k = 0; k < K; ++k)
       for (int oh = 0; oh < Ho; ++oh)
         for (int ow = 0; ow < Wo; ++ow)
-          y[(((int64_t)n * K + k) * Ho + oh) * Wo + ow] =
-              orc_conv2d_point(x, N, C, H, W, w, K, R, S, stride, pad, n, k, oh, ow);
-  return ORC_OK;
+          if (orc_conv2d_point(x, N, C, H, W, w, K, R, S, stride, pad, n, k, oh, ow,
+                               &y[(((int64_t)n * K + k) * Ho + oh) * Wo + ow])) {
+#pragma omp atomic write
+            status = ORC_ERANGE;
+          }
+  return status;
 }
 
 /* ------------------------------------------------------------------------- */

@@ -62,15 +62,19 @@ int orc_fl_search_f32(const float* x, int64_t n, int k, int sign, int fl_lo, int
 int orc_fl_search_i64(const int64_t* v, int64_t n, int s, int k, int sign, int fl_lo, int fl_hi,
                       int* fl_best, int* sign_used, double* sse);
 
-/* Integer contraction: C[m][n] = sum_k A[m][k] * B[n][k] (codes as plain integers). */
-int orc_gemm(const int32_t* A, const int32_t* B, int64_t M, int64_t N, int64_t K, int64_t* C);
+/* Integer contraction: C[m][n] = sum_k A[m][k] * B[n][k] (codes as plain
+ * integers, any format up to 32 bits: Eq. 12 puts signed codes in
+ * [-2^31, 2^31 - 1] and unsigned ones in [0, 2^32 - 1]).  Summed exactly in
+ * 128 bits; a result outside int64 is ORC_ERANGE. */
+int orc_gemm(const int64_t* A, const int64_t* B, int64_t M, int64_t N, int64_t K, int64_t* C);
 
-/* Direct convolution, NCHW input, KCRS weights, zero padding (code 0 = value 0). */
-int orc_conv2d(const int32_t* x, int N, int C, int H, int W, const int32_t* w, int K, int R,
+/* Direct convolution, NCHW input, KCRS weights, zero padding (code 0 = value 0);
+ * codes and range as orc_gemm. */
+int orc_conv2d(const int64_t* x, int N, int C, int H, int W, const int64_t* w, int K, int R,
                int S, int stride, int pad, int64_t* y);
-/* One output y[n][k][oh][ow] of the same convolution. */
-int64_t orc_conv2d_point(const int32_t* x, int N, int C, int H, int W, const int32_t* w, int K,
-                         int R, int S, int stride, int pad, int n, int k, int oh, int ow);
+/* One output y[n][k][oh][ow] of the same convolution into *y. */
+int orc_conv2d_point(const int64_t* x, int N, int C, int H, int W, const int64_t* w, int K,
+                     int R, int S, int stride, int pad, int n, int k, int oh, int ow, int64_t* y);
 
 /*
  * C-Block epilogue on the accumulators acc (NCHW, `channels` channels, `hw`

@@ -1,26 +1,45 @@
-"""Builds libfxpq.so (gfx950) in-tree with hipcc."""
+"""Builds libfxpq.so (gfx950) in-tree with hipcc: one object per source,
+compiled in parallel, then linked."""
 import os
 import subprocess
+from concurrent.futures import ThreadPoolExecutor
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libfxpq.so")
+OBJ = os.path.join(HERE, "_build")
 SOURCES = ["fxpq_api.hip", "k_stream.hip", "k_flsearch.hip", "k_conv.hip", "k_teacher.hip",
            "k_wide.hip"]
+FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
+         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         "-I" + os.path.join(ROOT, "include")]
+
+
+def _compile(src, verbose):
+    obj = os.path.join(OBJ, os.path.splitext(src)[0] + ".o")
+    cmd = ["hipcc"] + FLAGS + ["-c", "-o", obj + ".tmp", os.path.join(CSRC, src)]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    r = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed on {src}:\n{r.stderr}")
+    os.replace(obj + ".tmp", obj)
+    return obj
 
 
 def build(verbose: bool = False) -> str:
+    os.makedirs(OBJ, exist_ok=True)
+    jobs = min(len(SOURCES), max(1, min(16, os.cpu_count() or 1)))
+    with ThreadPoolExecutor(jobs) as pool:
+        objs = list(pool.map(lambda s: _compile(s, verbose), SOURCES))
     # -z defs: an undefined symbol (e.g. a kernel stub the host pass did not
     # emit) fails the build instead of the first dlopen
-    cmd = ["hipcc", "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared", "-Wl,-z,defs",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-           "-I" + os.path.join(ROOT, "include"), "-o", LIB + ".tmp"]
-    cmd += [os.path.join(CSRC, s) for s in SOURCES]
+    cmd = ["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-Wl,-z,defs", "-o", LIB + ".tmp"]
+    cmd += objs
     if verbose:
         print(" ".join(cmd), flush=True)
-    subprocess.run(cmd, check=True, stdout=subprocess.DEVNULL if not verbose else None,
-                   stderr=subprocess.PIPE if not verbose else None)
+    subprocess.run(cmd, check=True)
     os.replace(LIB + ".tmp", LIB)
     return LIB
 

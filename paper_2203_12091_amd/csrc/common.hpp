@@ -240,7 +240,7 @@ hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, 
 // combination of the plane contractions with the epilogue.
 hipError_t launch_wide_split_x(const Ctx& c, const int32_t* x, int64_t n, int np, int sign,
                                int64_t plane_stride, int8_t* planes);
-hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np,
+hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np, int sign,
                                int64_t plane_stride, int8_t* planes);
 hipError_t launch_wide_combine(const Ctx& c, const int32_t* acc, int64_t mk, int np_x, int np_w,
                                const SrcDev& ep, int64_t* v, int32_t* d_scale);

@@ -35,7 +35,7 @@ bool aligned(const void* p, size_t a) { return ((uintptr_t)p % a) == 0; }
 
 bool is_code8(int t) { return t == FXPQ_I8 || t == FXPQ_U8OFF || t == FXPQ_C8; }
 
-bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32; }
+bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32 || t == FXPQ_U32; }
 
 size_t code_align(int t) { (void)t; return 16; }
 
@@ -605,7 +605,6 @@ bool wide_layout(const fxpq_conv_desc* d, int wl_x, int sign_x, int wl_w, int si
                  WideLayout* L) {
   if (!d || wl_x < 1 || wl_x > 32 || wl_w < 1 || wl_w > 32) return false;
   if ((sign_x != 0 && sign_x != 1) || (sign_w != 0 && sign_w != 1)) return false;
-  if ((!sign_x && wl_x > 31) || (!sign_w && wl_w > 31)) return false;  // int32 storage
   if (d->n < 1 || d->h < 1 || d->w < 1 || d->c < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
       d->stride < 1 || d->pad < 0)
     return false;
@@ -667,7 +666,8 @@ fxpq_status fxpq_qconv_wide(fxpq_handle h, const fxpq_conv_desc* d, const int32_
   DeviceGuard g(h->device);
   const Ctx c = ctx(h);
   hipError_t err = launch_wide_split_x(c, x, L.n_in, L.np_x, sign_x, L.xs, px);
-  if (err == hipSuccess) err = launch_wide_split_w(c, w, (int64_t)d->k * L.wrow, L.np_w, L.ws, pw);
+  if (err == hipSuccess)
+    err = launch_wide_split_w(c, w, (int64_t)d->k * L.wrow, L.np_w, sign_w, L.ws, pw);
   for (int q = 0; q < L.np_w && err == hipSuccess; ++q)
     err = launch_colsum(c, pw + q * L.ws, d->k, L.wrow, cs + (int64_t)q * d->k);
   for (int p = 0; p < L.np_x && err == hipSuccess; ++p) {

@@ -555,6 +555,10 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
   const long long qmax = (1ll << (wl - sign)) - 1;
   const long long qmin = sign ? -(1ll << (wl - 1)) : 0;
   const int64_t clen = (n + nchunks - 1) / nchunks;
+  // int64 values are scaled in integers (fp64 holds them exactly only below
+  // 2^53); |v| 2^(sigma - sv) < 2^62 after the check above (a shift of 62 or
+  // more leaves only zeros)
+  const long long wmul = (sigma - sv < 62) ? (1ll << (sigma - sv)) : 0ll;
 
   for (int item = blockIdx.x; item < nc * nchunks; item += gridDim.x) {
     const int j = item / nchunks, ch = item % nchunks;
@@ -564,28 +568,36 @@ __global__ __launch_bounds__(kThreads) void k_fls_general(
     const int64_t e1 = (e0 + clen < n) ? e0 + clen : n;
     U192 acc{0, 0};
     for (int64_t i = e0 + threadIdx.x; i < e1; i += kThreads) {
-      double W = load1<KIND, DT>(s, i) * wscale;
+      double W = 0.0;
+      long long Wi = 0;
+      bool frac = false;  // W not an integer (fp32 values only)
+      if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) {
+        Wi = static_cast<const int64_t*>(s.x)[i] * wmul;
+      } else {
+        W = load1<KIND, DT>(s, i) * wscale;
+        frac = W != floor(W);
+        if (!frac) Wi = (long long)W;
+      }
       unsigned __int128 e2;
       if (binary) {
         // |x - sign(x) 2^-beta| = | |x| - 2^-beta |; an fp32 value below
         // 2^-(fl_hi+24) has a fractional |W|: (2^d - |W|)^2 is then summed
         // truncated to the unit (error below 2 units per such value)
-        const double aw = fabs(W);
-        if (aw != floor(aw)) {
+        if (frac) {
+          const double aw = fabs(W);
           const unsigned __int128 u = (unsigned __int128)1 << d;
           e2 = u * u - (unsigned __int128)(unsigned long long)floor(ldexp(aw, d + 1)) +
                (unsigned __int128)(unsigned long long)floor(aw * aw);
         } else {
-          __int128 err = (__int128)(long long)aw - ((__int128)1 << d);
+          __int128 err = (__int128)(Wi < 0 ? -Wi : Wi) - ((__int128)1 << d);
           if (err < 0) err = -err;
           e2 = (unsigned __int128)err * (unsigned __int128)err;
         }
-      } else if (W != floor(W)) {
+      } else if (frac) {
         // fp32 value below 2^-(fl_hi+1): its code is 0 for every candidate and
         // its (identical) error is added truncated to the common unit.
         e2 = (unsigned __int128)(unsigned long long)floor(W * W);
       } else {
-        long long Wi = (long long)W;
         long long q;
         if (d >= 63) {
           q = 0;

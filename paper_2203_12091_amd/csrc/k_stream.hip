@@ -231,6 +231,15 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
   const int sv = src_scale(s);
   const QFmt q = qfmt_setup<OUT>(fmt, sv, flags);
   if (!q.ok) return;
+  if constexpr (KIND == FXPQ_SRC_INT && DT == FXPQ_I64) {
+    // int64 values (wide C-Blocks, pooled sums): the exact integer quantizer
+    const int sh = fmt->fl - sv;
+    const int64_t* x = static_cast<const int64_t*>(s.x);
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kThreads)
+      store1<OUT>(codes, i, quant_one_i64(x[i], sh, q));
+    return;
+  }
   using PK = Pack<KIND, DT>;
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   ThreadVals<PK::V> t;
@@ -244,7 +253,7 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
 #pragma unroll
     for (int j = 0; j < PK::EP; ++j) {
       if constexpr (KIND == FXPQ_SRC_F32) bad |= !isfinite(v[j]);
-      c[j] = quant_one(v[j], q);
+      c[j] = quant_one<OUT>(v[j], q);
     }
     storev<OUT, PK::EP>(codes, i0, c);
   });
@@ -252,7 +261,7 @@ __global__ __launch_bounds__(kThreads) void k_requant(SrcDev s, int64_t n, const
     for (int64_t i = nfull; i < n; ++i) {
       const double v = load1<KIND, DT>(s, i);
       if constexpr (KIND == FXPQ_SRC_F32) bad |= !isfinite(v);
-      store1<OUT>(codes, i, quant_one(v, q));
+      store1<OUT>(codes, i, quant_one<OUT>(v, q));
     }
   }
   if constexpr (KIND == FXPQ_SRC_F32) {
@@ -267,6 +276,7 @@ template <int CT>
 __device__ inline double code_at(const void* codes, int64_t i) {
   if constexpr (CT == FXPQ_I16) return static_cast<const int16_t*>(codes)[i];
   else if constexpr (CT == FXPQ_I32) return static_cast<const int32_t*>(codes)[i];
+  else if constexpr (CT == FXPQ_U32) return static_cast<const uint32_t*>(codes)[i];
   else if constexpr (CT == FXPQ_F32) return static_cast<const float*>(codes)[i];
   else return static_cast<const int8_t*>(codes)[i];
 }
@@ -537,13 +547,14 @@ hipError_t launch_requant_gated(const Ctx& c, const SrcDev& s, int64_t n, const 
 hipError_t launch_requant(const Ctx& c, const SrcDev& s, int64_t n, const fxpq_fmt* fmt,
                           void* codes, int code_type) {
   const double in_b = (s.kind == FXPQ_SRC_ADD) ? 2.0 : (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) ? 8.0 : 4.0;
-  const double out_b = (code_type == FXPQ_I32) ? 4.0 : (code_type == FXPQ_I16 ? 2.0 : 1.0);
+  const double out_b = (code_type == FXPQ_I32 || code_type == FXPQ_U32) ? 4.0 : (code_type == FXPQ_I16 ? 2.0 : 1.0);
   bool timed = timer_begin(c, FXPQ_TIMER_REQUANT);
   switch (code_type) {
     case FXPQ_I8: requant_out<FXPQ_I8>(c, s, n, fmt, codes); break;
     case FXPQ_U8OFF: requant_out<FXPQ_U8OFF>(c, s, n, fmt, codes); break;
     case FXPQ_C8: requant_out<FXPQ_C8>(c, s, n, fmt, codes); break;
     case FXPQ_I16: requant_out<FXPQ_I16>(c, s, n, fmt, codes); break;
+    case FXPQ_U32: requant_out<FXPQ_U32>(c, s, n, fmt, codes); break;
     default: requant_out<FXPQ_I32>(c, s, n, fmt, codes); break;
   }
   timer_end(c, timed, (in_b + out_b) * (double)n);
@@ -584,6 +595,7 @@ hipError_t launch_layer_error(const Ctx& c, const float* ref, const void* codes,
   switch (code_type) {
     case FXPQ_I16: blocks = run(&k_layer_error<FXPQ_I16>); break;
     case FXPQ_I32: blocks = run(&k_layer_error<FXPQ_I32>); break;
+    case FXPQ_U32: blocks = run(&k_layer_error<FXPQ_U32>); break;
     case FXPQ_U8OFF: blocks = run(&k_layer_error<FXPQ_U8OFF>); break;
     case FXPQ_C8: blocks = run(&k_layer_error<FXPQ_C8>); break;
     case FXPQ_F32: blocks = run(&k_layer_error<FXPQ_F32>); break;
@@ -616,6 +628,7 @@ hipError_t launch_dequant(const Ctx& c, const void* codes, int code_type, const 
   switch (code_type) {
     case FXPQ_I16: run(&k_dequant<FXPQ_I16>); break;
     case FXPQ_I32: run(&k_dequant<FXPQ_I32>); break;
+    case FXPQ_U32: run(&k_dequant<FXPQ_U32>); break;
     case FXPQ_U8OFF: run(&k_dequant<FXPQ_U8OFF>); break;
     case FXPQ_C8: run(&k_dequant<FXPQ_C8>); break;
     default: run(&k_dequant<FXPQ_I8>); break;

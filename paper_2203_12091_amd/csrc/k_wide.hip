@@ -30,26 +30,29 @@ __global__ __launch_bounds__(kThreads) void k_split_x(const int32_t* __restrict_
        i += (int64_t)gridDim.x * kThreads) {
     const int32_t v = x[i];
     for (int p = 0; p < np - 1; ++p) planes[p * ps + i] = (int8_t)(((v >> (8 * p)) & 255) - 128);
-    const int32_t top = v >> (8 * (np - 1));
     if (sign) {
+      const int32_t top = v >> (8 * (np - 1));
       bad |= top < -128 || top > 127;
       planes[(np - 1) * ps + i] = (int8_t)top;
     } else {
-      bad |= v < 0 || top > 255;
-      planes[(np - 1) * ps + i] = (int8_t)(top - 128);
+      // unsigned codes are read as uint32 (the storage of 32-bit ones)
+      const uint32_t top = (uint32_t)v >> (8 * (np - 1));
+      bad |= top > 255;
+      planes[(np - 1) * ps + i] = (int8_t)((int)top - 128);
     }
   }
   if (bad) flag(flags, FXPQ_FLAG_CODE);
 }
 
 __global__ __launch_bounds__(kThreads) void k_split_w(const int32_t* __restrict__ w, int64_t n,
-                                                      int np, int64_t ps,
+                                                      int np, int sign, int64_t ps,
                                                       int8_t* __restrict__ planes,
                                                       unsigned* flags) {
   bool bad = false;
   for (int64_t i = blockIdx.x * (int64_t)kThreads + threadIdx.x; i < n;
        i += (int64_t)gridDim.x * kThreads) {
-    int64_t r = w[i];
+    // unsigned codes are read as uint32 (the storage of 32-bit ones)
+    int64_t r = sign ? (int64_t)w[i] : (int64_t)(uint32_t)w[i];
     for (int p = 0; p < np; ++p) {
       const int d = (int)((r + 128) & 255) - 128;
       planes[p * ps + i] = (int8_t)d;
@@ -198,9 +201,9 @@ hipError_t launch_wide_split_x(const Ctx& c, const int32_t* x, int64_t n, int np
   return hipGetLastError();
 }
 
-hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np,
+hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np, int sign,
                                int64_t plane_stride, int8_t* planes) {
-  k_split_w<<<stream_blocks(n), kThreads, 0, c.stream>>>(w, n, np, plane_stride, planes,
+  k_split_w<<<stream_blocks(n), kThreads, 0, c.stream>>>(w, n, np, sign, plane_stride, planes,
                                                          c.sc.flags);
   return hipGetLastError();
 }

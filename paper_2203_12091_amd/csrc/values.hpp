@@ -289,7 +289,7 @@ __device__ inline double load1(const SrcDev& s, int64_t i) {
 struct QFmt {
   double qmin, qmax, mult;
   int off;         // 128 when stored as u - 128
-  int lo, hi;      // storage range
+  double lo, hi;   // storage range
   bool binary;     // signed 1-bit format (Eq. 13): stored decoded, -1 or +1
   bool ok;
 };
@@ -314,6 +314,9 @@ __device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) 
   } else if (OUT == FXPQ_I16) {
     q.lo = -32768;
     q.hi = 32767;
+  } else if (OUT == FXPQ_U32) {
+    q.lo = 0;
+    q.hi = 4294967295.0;
   } else {
     q.lo = INT32_MIN;
     q.hi = INT32_MAX;
@@ -324,6 +327,38 @@ __device__ inline QFmt qfmt_setup(const fxpq_fmt* fmt, int sv, unsigned* flags) 
   return q;
 }
 
+// Exact Eq. 10-13 for an int64 value v at fractional length sv, sh = fl - sv:
+// the code of v * 2^sh in integer arithmetic (fp64 holds int64 values exactly
+// only below 2^53).  Products beyond the code range saturate (|qmin|, qmax <
+// 2^33); right shifts round half to even.
+__device__ inline int quant_one_i64(long long v, int sh, const QFmt& q) {
+  if (q.binary) return v < 0 ? -1 : 1;
+  const long long qmin = (long long)q.qmin, qmax = (long long)q.qmax;
+  long long r;
+  if (sh >= 0) {
+    const unsigned long long m = v < 0 ? 0ull - (unsigned long long)v : (unsigned long long)v;
+    if (v == 0) r = 0;
+    else if (sh >= 33 || (m >> (33 - sh)) != 0ull) r = v < 0 ? qmin : qmax;
+    else r = v * (1ll << sh);
+  } else {
+    const int d = -sh;
+    if (d >= 64) {
+      r = 0;  // |v| < 2^63 <= 2^(d - 1): below one half
+    } else {
+      const __int128 f = (__int128)v >> d;
+      const __int128 rem = (__int128)v - f * ((__int128)1 << d);
+      const __int128 half = (__int128)1 << (d - 1);
+      r = (long long)(f + ((rem > half || (rem == half && (f & 1) != 0)) ? 1 : 0));
+    }
+  }
+  r = r < qmin ? qmin : (r > qmax ? qmax : r);
+  long long c = r - q.off;
+  const long long lo = (long long)q.lo, hi = (long long)q.hi;
+  c = c < lo ? lo : (c > hi ? hi : c);
+  return (int)(unsigned)c;  // the storage's 32 bits (uint32 codes keep their bits)
+}
+
+template <int OUT = FXPQ_I32>
 __device__ inline int quant_one(double v, const QFmt& q) {
   // Eq. 13: negative values take code -1, the rest code 0, which decodes to
   // +1; the decoded value is what is stored, so a C-Block uses it as it is
@@ -331,8 +366,9 @@ __device__ inline int quant_one(double v, const QFmt& q) {
   double r = rint(v * q.mult);  // round half to even
   r = fmin(fmax(r, q.qmin), q.qmax);
   double c = r - (double)q.off;
-  c = fmin(fmax(c, (double)q.lo), (double)q.hi);
-  return (int)c;
+  c = fmin(fmax(c, q.lo), q.hi);
+  if constexpr (OUT == FXPQ_U32) return (int)(unsigned)c;  // uint32 storage bits
+  else return (int)c;
 }
 
 // ---- wave / block reductions (wave64) ---------------------------------------

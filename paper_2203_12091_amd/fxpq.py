@@ -13,7 +13,7 @@ LIB_PATH = os.path.join(HERE, "libfxpq.so")
 
 # enums (keep in sync with include/fxpq.h)
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_NONFINITE, ERR_OVERFLOW, ERR_HIP, ERR_ALLOC = range(7)
-I8, U8OFF, I16, I32, I64, F32, C8 = range(7)
+I8, U8OFF, I16, I32, I64, F32, C8, U32 = range(8)
 SRC_F32, SRC_INT, SRC_ACC, SRC_ADD = range(4)
 SIGN_AUTO = -1
 FLAG_NONFINITE, FLAG_RANGE, FLAG_CODE = 0x1, 0x2, 0x4

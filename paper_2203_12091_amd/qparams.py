@@ -147,6 +147,11 @@ class ForwardOptimizer:
         convs = [n.name for n in self.nodes if n.op in ("conv", "fc")]
         return self.fl_wl is not None and ln in (convs[0], convs[-1])
 
+    def _ct32(self, key):
+        """Storage of data structure key's codes wider than 8 bits: int32 for
+        a signed format, uint32 for an unsigned one."""
+        return fx.I32 if self.qp[key][2] else fx.U32
+
     def _first_wide(self):
         """The first layer's C-Block runs on int32 codes (input or weights
         wider than 8 bits); the input is stored as int32 codes then."""
@@ -214,7 +219,7 @@ class ForwardOptimizer:
         if ln == "input":
             x = self.act["input"]
             wide = self._first_wide()
-            ct = fx.I32 if wide else fx.C8
+            ct = self._ct32(("input", "a")) if wide else fx.C8
             codes = self._buf(("input", "codes", ct), x.shape, T.int32 if wide else T.int8)
             fx.quantize(h, x, x.numel(), self.fmt[("input", "a")], codes, ct)
             e = self._buf(("input", "a", "err"), (4,), T.float64)
@@ -225,7 +230,7 @@ class ForwardOptimizer:
         n = L["node"]
         wide = qcodes[n.inp].dtype == T.int32
         assert wide or self.qp[(ln, "w")][0] <= 8, ln
-        wct = fx.I32 if wide else fx.I8
+        wct = self._ct32((ln, "w")) if wide else fx.I8
         wcodes = self._buf((ln, "wcodes", wct), (L["w_krsc"].numel(),), T.int32 if wide else T.int8)
         self._param(ln, "w", wcodes, wct, errs)
         cs = self._buf((ln, "colsum"), (n.cout,), T.int32)
@@ -319,10 +324,12 @@ class ForwardOptimizer:
             s = fx.src_int(acc, fx.I64, sc)
             self.held[(n.name, "src")] = (ep, s)
             m = acc.numel()
-            if self.fl_wl is not None:  # the last layer's input, int32 codes
+            if self.fl_wl is not None:  # the last layer's input, 32-bit storage
                 y32 = self._buf((n.name, "codes32"), tuple(self.act[n.name].shape), T.int32)
                 fx.fl_search(h, s, m, self.fl_wl, fx.SIGN_AUTO, FL_LO, FL_HI, f)
-                fx.requant(h, s, m, f, y32, fx.I32)
+                # unsigned codes as uint32 (an unsigned 32-bit format's storage)
+                ct = fx.U32 if int(f[2].item()) == 0 else fx.I32
+                fx.requant(h, s, m, f, y32, ct)
                 return y32, f
         fx.fl_search(h, s, m, A_WL, fx.SIGN_AUTO, FL_LO, FL_HI, f)
         fx.requant(h, s, m, f, y, fx.C8)
@@ -332,7 +339,10 @@ class ForwardOptimizer:
         if name not in self.deq:
             c = self.qcodes[name]
             y = self._empty(c.shape, self.T.float32)
-            ct = fx.I32 if c.dtype == self.T.int32 else fx.C8
+            if c.dtype == self.T.int32:  # uint32 storage for unsigned formats
+                ct = fx.U32 if int(self.qfmt[name][2].item()) == 0 else fx.I32
+            else:
+                ct = fx.C8
             fx.dequantize(self.h, c, ct, self.qfmt[name], c.numel(), y)
             self.deq[name] = y
         return self.deq[name]

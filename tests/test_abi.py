@@ -95,7 +95,8 @@ def test_wide_workspace_layout_on_host(fx):
     for (wx, sx, ww, sw), (px, pw) in [((16, 1, 16, 1), (2, 3)), ((16, 1, 15, 1), (2, 2)),
                                        ((8, 1, 8, 1), (1, 1)), ((8, 0, 8, 0), (1, 2)),
                                        ((32, 1, 32, 1), (4, 5)), ((31, 0, 24, 1), (4, 4)),
-                                       ((1, 1, 1, 1), (1, 1)), ((9, 1, 17, 1), (2, 3))]:
+                                       ((1, 1, 1, 1), (1, 1)), ((9, 1, 17, 1), (2, 3)),
+                                       ((32, 0, 8, 1), (4, 1)), ((8, 1, 32, 0), (1, 5))]:
         assert fx.qconv_wide_workspace(d, wx, sx, ww, sw) == want(px, pw), (wx, sx, ww, sw)
     # the padded RGB layout rounds each weight row up to 64 bytes
     d4 = fx.ConvDesc(1, 10, 10, 4, 64, 7, 7, 2, 3)
@@ -103,6 +104,6 @@ def test_wide_workspace_layout_on_host(fx):
     a = lambda b: (b + 255) // 256 * 256
     assert fx.qconv_wide_workspace(d4, 16, 1, 8, 1) == (
         2 * a(400) + a(64 * 256) + a(64 * 4) + 2 * ho * ho * 64 * 4)
-    for bad in [(32, 0, 8, 1), (8, 1, 32, 0), (0, 1, 8, 1), (8, 2, 8, 1), (33, 1, 8, 1)]:
+    for bad in [(0, 1, 8, 1), (8, 2, 8, 1), (33, 1, 8, 1), (8, 1, 33, 0), (32, -1, 8, 1)]:
         with pytest.raises(fx.FxpqError):
             fx.qconv_wide_workspace(d, *bad)

@@ -159,12 +159,12 @@ def test_largest_3x3_conv_sampled(env):
     note("fullsize 3x3 conv")
     fx.qconv(h, fx.conv_desc(N, H, H, C, K, 3, 3, 1, 1), xd, fx.U8OFF, wd, cs, None, acc)
     got = host(acc)
-    x32, w32 = x.astype(np.int32), w.astype(np.int32)
+    x64, w64 = np.ascontiguousarray(x, np.int64), np.ascontiguousarray(w, np.int64)
     g = synth.rng_for(11, "fs-sample")
     for _ in range(2000):
         n, k, oh, ow = (int(g.integers(0, N)), int(g.integers(0, K)), int(g.integers(0, H)),
                         int(g.integers(0, H)))
-        assert got[n, oh, ow, k] == orc.conv2d_point(x32, w32, 1, 1, n, k, oh, ow)
+        assert got[n, oh, ow, k] == orc.conv2d_point(x64, w64, 1, 1, n, k, oh, ow)
     # the halo tiles give the same integers over the whole tensor
     note("fullsize 3x3 conv, halo tiles")
     fx.set_conv_tiling(h, fx.TILING_HALO)
@@ -214,12 +214,99 @@ def test_wide_first_layer_full_batch_sampled(env):
     pix = [(int(n), int(p), int(q)) for n, p, q in
            zip(g.integers(0, N, 256), g.integers(0, Ho, 256), g.integers(0, Ho, 256))]
     pix += [(0, 0, 0), (N - 1, Ho - 1, Ho - 1), (7, 0, Ho - 1)]
-    acc = np.array([[orc.conv2d_point(xc, wc, 2, 3, n, k, p, q) for k in range(K)] for n, p, q in pix],
-                   np.int64)
+    xc64, wc64 = np.ascontiguousarray(xc, np.int64), np.ascontiguousarray(wc, np.int64)
+    acc = np.array([[orc.conv2d_point(xc64, wc64, 2, 3, n, k, p, q) for k in range(K)]
+                    for n, p, q in pix], np.int64)
     want, s_out = orc.epilogue(acc, 12 + 14, None, 0, a1.astype(np.int64), 14, a2.astype(np.int64), 20,
                                True)
     assert int(host(sc)[0]) == s_out
     assert np.array_equal(np.array([got[n, p, q] for n, p, q in pix]), want)
+    h.close()
+
+
+def test_wide_first_layer_32bit_full_batch(env):
+    """The paper's initial design for the first layer (Sec. "Initial Design
+    Generation"): ResNet-50's first C-Block at batch 256 with the network
+    input and the weights at 32 bits, on fxpq_qconv_wide.  The 32-bit input
+    format and all 38.5 M input codes, the weight, Scale multiplier (16-bit)
+    and offset (32-bit) formats and codes are checked against the oracle; the
+    exact int64 C-Block values at 256 sampled output pixels (all 64 channels
+    each); then the FxP-QLayer at WL 8 over all 205 M values: the FL search
+    and every code, exactly.  (With fractional lengths capped at 15 the
+    32-bit codes of these data stay near 2^17 and the values near 2^48.)"""
+    torch, fx, nets, orc = env
+    N, H, C, K, R = 256, 224, 3, 64, 7
+    h = fx.Handle(0)
+    fx.set_stream(h, torch.cuda.current_stream())
+
+    def param(x, wl):
+        xd = dev(np.ascontiguousarray(x, np.float32).ravel())
+        f = fmt_new()
+        fx.fl_search(h, fx.src_f32(xd), xd.numel(), wl, fx.SIGN_AUTO, FL_LO, FL_HI, f)
+        codes = empty((xd.numel(),), torch.int32)
+        fx.quantize(h, xd, xd.numel(), f, codes, fx.I32)
+        gwl, gfl, gsg, gst = fmt_host(f)
+        ofl, osg, _ = orc.fl_search_f32(np.ravel(x), wl, orc.SIGN_AUTO, FL_LO, FL_HI)
+        assert (gwl, gfl, gsg, gst) == (wl, ofl, osg, 0)
+        want = orc.quantize_f32(np.ravel(x), wl, ofl, osg)
+        assert np.array_equal(host(codes).astype(np.int64), want)
+        return f, ofl, want.reshape(np.shape(x))
+
+    note("fullsize wide conv1 32x32: parameters")
+    x = synth.normal(9, "wide32.input", (N, C, H, H))
+    w = synth.normal(9, "wide32.w", (K, C, R, R), std=float(np.sqrt(2.0 / (C * R * R))))
+    gamma = synth.uniform(9, "wide32.gamma", (K,), 0.5, 1.5)
+    beta = synth.normal(9, "wide32.beta", (K,), std=0.1)
+    a1 = (gamma / np.sqrt(np.float32(1.0) + np.float32(1e-5))).astype(np.float32)
+    fin, fl_x, xc = param(x, 32)
+    _, fl_w, wc = param(w, 32)
+    _, fl_a1, c1 = param(a1, 16)
+    _, fl_a2, c2 = param(beta, 32)
+    del x
+    x4 = np.zeros((N, H, H, 4), np.int32)
+    x4[..., :3] = xc.transpose(0, 2, 3, 1)
+    depth = R * R * 4
+    w4 = np.zeros((K, R, R, 4), np.int32)
+    w4[..., :3] = wc.transpose(0, 2, 3, 1)
+    wrow = np.zeros((K, (depth + 63) // 64 * 64), np.int32)
+    wrow[:, :depth] = w4.reshape(K, -1)
+    ep = fx.epilogue(K, fl_w, fin, relu=True, scale=dev(c1.astype(np.int32)), fl_scale=fl_a1,
+                     shift=dev(c2.astype(np.int32)), fl_shift=fl_a2)
+    d = fx.conv_desc(N, H, H, 4, K, R, R, 2, 3)
+    nb = fx.qconv_wide_workspace(d, 32, 1, 32, 1)
+    ws = empty((nb,), torch.uint8)
+    Ho = (H + 6 - R) // 2 + 1
+    n = N * Ho * Ho * K
+    v = empty((n,), torch.int64)
+    sc = empty((1,), torch.int32)
+    note("fullsize wide conv1 32x32: contraction")
+    fx.qconv_wide(h, d, dev(x4), 32, 1, dev(wrow), 32, 1, ep, v, sc, ws, nb)
+    assert fx.sync_status(h) == 0
+    del ws, x4
+    got = host(v)
+    g = synth.rng_for(82, "wide32-pix")
+    pix = [(int(a), int(b), int(c)) for a, b, c in
+           zip(g.integers(0, N, 256), g.integers(0, Ho, 256), g.integers(0, Ho, 256))]
+    pix += [(0, 0, 0), (N - 1, Ho - 1, Ho - 1), (7, 0, Ho - 1)]
+    g4 = got.reshape(N, Ho, Ho, K)
+    xc64, wc64 = np.ascontiguousarray(xc, np.int64), np.ascontiguousarray(wc, np.int64)
+    acc = np.array([[orc.conv2d_point(xc64, wc64, 2, 3, a, k, b, c) for k in range(K)]
+                    for a, b, c in pix], np.int64)
+    want, s_out = orc.epilogue(acc, fl_x + fl_w, None, 0, c1.astype(np.int64), fl_a1,
+                               c2.astype(np.int64), fl_a2, True)
+    assert int(host(sc)[0]) == s_out
+    assert np.array_equal(np.array([g4[a, b, c] for a, b, c in pix]), want)
+    note("fullsize wide conv1 32x32: FxP-QLayer over all values")
+    out = fmt_new()
+    src = fx.src_int(v, fx.I64, sc)
+    fx.fl_search(h, src, n, 8, fx.SIGN_AUTO, FL_LO, FL_HI, out)
+    codes = empty((n,), torch.int8)
+    fx.requant(h, src, n, out, codes, fx.C8)
+    gwl, gfl, gsg, gst = fmt_host(out)
+    ofl, osg, _ = orc.fl_search_i64(got, s_out, 8, orc.SIGN_AUTO, FL_LO, FL_HI)
+    assert (gwl, gfl, gsg, gst) == (8, ofl, osg, 0)
+    assert np.array_equal(decode8(host(codes), osg == 0), orc.quantize_i64(got, s_out, 8, ofl, osg))
+    assert fx.sync_status(h) == 0
     h.close()
 
 

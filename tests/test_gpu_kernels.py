@@ -135,6 +135,42 @@ def test_requant_int_sources_bit_exact(fx, h, orc):
     check_flags(fx, h, allowed=fx.FLAG_CODE)
 
 
+def test_int64_values_beyond_fp64_exact(fx, h, orc):
+    """int64 values of magnitude 2^53 .. 2^62 (what wide C-Blocks produce; fp64
+    holds them exactly only below 2^53): the FL search (its exact general
+    pass) and the requantization match the oracle bit for bit, with exact
+    rounding ties planted at every shift the formats use."""
+    import torch
+    g = synth.rng_for(53, "big-int64")
+    n = 50_001
+    v = (g.standard_normal(n) * 2.0 ** 58).astype(np.int64)
+    v[::7] = g.integers(-2 ** 61, 2 ** 61, v[::7].size, dtype=np.int64)
+    for s, k, fl in [(55, 8, 3), (50, 16, 6), (58, 32, 15), (40, 8, -8)]:
+        d = s - fl
+        # (2j + 1) * 2^(d - 1): exactly half way between two codes
+        j = g.integers(-100, 100, 64, dtype=np.int64)
+        v[1000:1064] = (2 * j + 1) << (d - 1)
+        vd = dev(v)
+        sd = torch.tensor([s], dtype=torch.int32, device=DEV)
+        note("int64 beyond fp64", s, k, fl)
+        for sign in ((1,) if k == 32 else (0, 1)):  # no code type holds unsigned 32-bit codes
+            f = fmt_dev(k, fl, sign)
+            # the code type holds the format's range (unsigned 16-bit: int32)
+            ct = fx.I32 if k - sign >= 16 else (fx.I16 if k > 8 else fx.C8)
+            codes = empty((n,), {fx.I32: torch.int32, fx.I16: torch.int16, fx.C8: torch.int8}[ct])
+            fx.requant(h, fx.src_int(vd, fx.I64, sd), n, f, codes, ct)
+            got = host(codes).astype(np.int64)
+            if ct == fx.C8 and sign == 0:
+                got += 128
+            assert np.array_equal(got, orc.quantize_i64(v, s, k, fl, sign)), (s, k, fl, sign)
+        for wl in (8, 16, 32):
+            (gwl, gfl, gsign, gst), _ = run_fl_search(fx, h, fx.src_int(vd, fx.I64, sd), n, wl,
+                                                      fx.SIGN_AUTO)
+            ofl, osign, _ = orc.fl_search_i64(v, s, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+            assert (gfl, gsign, gst) == (ofl, osign, 0), (s, wl)
+    check_flags(fx, h)
+
+
 # ----------------------------------------------------------------------------
 # FL search
 # ----------------------------------------------------------------------------

@@ -78,23 +78,25 @@ def test_reduction_matches_oracle(fx):
     fo.close()
 
 
-def test_wide_first_last_layers_match_oracle(fx):
-    """The paper's initial design with wide first / last layers (here 16-bit
-    input, first and last weights and last-layer input; wide C-Blocks on the
-    GPU): the forward optimizer, two changes of Algorithm 2, then the binary
-    searches of the 16-bit input and FC weights from their 16 bits."""
+@pytest.mark.parametrize("flw", [32, 16])
+def test_wide_first_last_layers_match_oracle(fx, flw):
+    """The paper's initial design with wide first / last layers (the input,
+    the first and last weights and the last layer's input at 32 bits, as the
+    paper starts them, and at 16; wide C-Blocks on the GPU): the forward
+    optimizer, two changes of Algorithm 2, then the binary searches of the
+    wide input and FC weights from their initial word length."""
     from oracle import qparams as OQ
     from oracle import reduction as OR
     from paper_2203_12091_amd import qparams as GQ
     from paper_2203_12091_amd import reduction as GR
-    note("wide first/last oracle resnet18 2x16")
-    ref = OQ.ForwardOptimizer("resnet18", batch=2, image=16, w_wl=8, first_last_wl=16)
+    note("wide first/last oracle resnet18 2x16", flw)
+    ref = OQ.ForwardOptimizer("resnet18", batch=2, image=16, w_wl=8, first_last_wl=flw)
     want = ref.run()
-    note("wide first/last gpu resnet18 2x16")
-    fo = GQ.ForwardOptimizer("resnet18", batch=2, image=16, device=DEV, w_wl=8, first_last_wl=16)
+    note("wide first/last gpu resnet18 2x16", flw)
+    fo = GQ.ForwardOptimizer("resnet18", batch=2, image=16, device=DEV, w_wl=8, first_last_wl=flw)
     got = fo.run()
     assert got == {k: tuple(v) for k, v in want.items()}
-    assert got[("input", "a")][0] == 16 and got[("fc", "w")][0] == 16
+    assert got[("input", "a")][0] == flw and got[("fc", "w")][0] == flw
     same_trace(fo.trace, ref.trace)
     assert fo.top1_agreement() == ref.top1(ref.q[ref.last][0])
     rr, rg = OR.QReduction(ref, 0.5, max_changes=2), GR.QReduction(fo, 0.5, max_changes=2)

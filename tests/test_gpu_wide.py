@@ -67,6 +67,9 @@ CASES = [
     (2, 16, 8, 8, 32, 3, 1, 1, (16, 1), (1, 1), True, False, True),
     (1, 32, 5, 5, 48, 3, 1, 1, (24, 1), (24, 1), False, True, False),
     (1, 16, 6, 6, 16, 3, 1, 1, (31, 0), (15, 0), False, False, False),
+    # unsigned 32-bit codes (uint32 storage): input, then weights
+    (1, 16, 6, 6, 16, 3, 1, 1, (32, 0), (16, 1), True, False, False),
+    (2, 16, 5, 5, 8, 1, 1, 0, (8, 1), (32, 0), False, True, False),
 ]
 
 
