@@ -400,6 +400,27 @@ fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const 
                                   double* d_minmax, uint32_t* d_miss);
 
 /*
+ * Deferred decisions of the predicted calls (fxpq_cblock_predicted,
+ * fxpq_qlayer_predicted; the same decisions of Eq. 14's FL search, taken
+ * later).  With on = 1 a predicted call launches only its pass: the pass
+ * records what its decision needs (in the handle) and its window sums go to
+ * the call's own slot set; fxpq_predicted_decide then decides every call
+ * recorded since the last decide in ONE launch, in call order.  Because the
+ * calls after a predicted call already consumed its codes with the format
+ * held in d_fmt_out on entry (the prediction), a deferred decision is a hit
+ * only when the searched format is that one (and the window conditions of
+ * fxpq_cblock_predicted hold); otherwise *d_miss is set as there and the
+ * caller reruns with the standard calls from the first call that missed.
+ * d_minmax gets each call's min / max at the decision.  Up to 256 calls may
+ * be pending (more: FXPQ_ERR_UNSUPPORTED from the predicted call).  The
+ * mode can change only with no decision pending (else FXPQ_ERR_INVALID_ARG).
+ * fxpq_predicted_decide with none pending does nothing.  The caller must
+ * keep every buffer a pending call names alive until its decision ran.
+ */
+fxpq_status fxpq_predicted_defer(fxpq_handle h, int32_t on);
+fxpq_status fxpq_predicted_decide(fxpq_handle h);
+
+/*
  * C-Block contraction over codes of up to 32 bits (Sec. "Integer-Only
  * Inference"; the first and last layers start at 32-bit activations and
  * weights, Sec. "Initial Design Generation"), followed by its epilogue:

@@ -41,7 +41,16 @@ struct Scratch {
   unsigned* gen_done;       // blocks of the general pass finished (0 between searches)
   void* plan;               // FlsPlan
   int32_t* sink;            // target of discarded stores [64]
+  // deferred decisions of predicted calls: one record and one slot set per
+  // call since the last fxpq_predicted_decide (slot sets zero between uses)
+  struct PredJob* pred_jobs;     // [kMaxPredJobs]
+  long long* pred_slots_i;       // [kMaxPredJobs][kWinSlots][kWinPart]
+  double* pred_slots_f;          // [kMaxPredJobs][kWinSlots][kWinPartF]
 };
+
+// Pending decisions of predicted calls in deferred mode (at most this many
+// between two fxpq_predicted_decide calls).
+constexpr int kMaxPredJobs = 256;
 
 // Everything a kernel needs to produce the value v_i of an FxP-QLayer input,
 // as an exact double (integers below 2^53), plus its fractional length.
@@ -69,6 +78,19 @@ struct SrcDev {
 };
 
 // Uniform part of the C-Block epilogue: exponents of the exact alignment.
+// What the decision of a predicted call needs, written by block 0 of the
+// call's own kernel in deferred mode and read by the batched decision.
+struct PredJob {
+  SrcDev s;
+  int wl, sign, fl_lo, fl_hi, nce;
+  int64_t per_thread;
+  double* mm;          // predicted min / max in, this call's out
+  fxpq_fmt* out;       // the format the codes were written with (prediction)
+  unsigned* miss;
+  long long* pi;       // the call's slot set
+  double* pf;
+};
+
 struct EpiU {
   int s_out;    // fractional length of the epilogue value
   int sh_acc;   // acc * 2^sh_acc ...
@@ -161,6 +183,7 @@ struct Ctx {
   int cus;                  // compute units of the handle's device
   unsigned* search_seq;     // FL searches enqueued on the handle (host counter)
   int conv_tiling;          // fxpq_conv_tiling
+  int* pred_jobs_n;         // deferred mode: pending predicted calls (host counter), else null
 };
 
 // Brackets one launch with events when `kind` is being timed.
@@ -225,6 +248,8 @@ hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int 
 hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, int sign,
                               int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, double* d_minmax,
                               unsigned* miss);
+// One launch deciding the n pending predicted calls recorded in jobs.
+hipError_t launch_pred_decide(const Ctx& c, const PredJob* jobs, int n);
 hipError_t launch_conv_fused(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                              const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
                              int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y, int y_type,

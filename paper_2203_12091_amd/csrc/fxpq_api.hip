@@ -21,6 +21,8 @@ struct fxpq_handle_s {
   Timer timer;
   unsigned search_seq = 0;
   int conv_tiling = FXPQ_TILING_AUTO;
+  int pred_defer = 0;  // predicted calls defer their decisions
+  int pred_n = 0;      // pending deferred decisions
 };
 
 constexpr int kTimerPairs = 16384;
@@ -40,7 +42,8 @@ bool is_code(int t) { return is_code8(t) || t == FXPQ_I16 || t == FXPQ_I32 || t 
 size_t code_align(int t) { (void)t; return 16; }
 
 Ctx ctx(fxpq_handle h) {
-  return Ctx{h->stream, h->sc, &h->timer, h->cus, &h->search_seq, h->conv_tiling};
+  return Ctx{h->stream, h->sc, &h->timer, h->cus, &h->search_seq, h->conv_tiling,
+             h->pred_defer ? &h->pred_n : nullptr};
 }
 
 fxpq_status hip_status(hipError_t e) { return e == hipSuccess ? FXPQ_OK : FXPQ_ERR_HIP; }
@@ -208,10 +211,13 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   size_t o_gd = take(4);
   size_t o_wp = take((size_t)2 * kWinSlots * kWinPart * sizeof(long long));
   size_t o_wpf = take((size_t)2 * kWinSlots * kWinPartF * sizeof(double));
+  size_t o_psi = take((size_t)kMaxPredJobs * kWinSlots * kWinPart * sizeof(long long));
+  size_t o_psf = take((size_t)kMaxPredJobs * kWinSlots * kWinPartF * sizeof(double));
   size_t o_mmp = take((size_t)kMaxConvBlocks * 2 * sizeof(double));
   size_t o_gp = take((size_t)(kMaxCand + 1) * kGenChunks * 3 * sizeof(unsigned long long));
   size_t o_plan = take(256);
   size_t o_sink = take(64 * sizeof(int32_t));
+  size_t o_jobs = take((size_t)kMaxPredJobs * sizeof(PredJob));
   if (hipMalloc(&h->scratch, off) != hipSuccess) {
     delete h;
     return FXPQ_ERR_ALLOC;
@@ -227,6 +233,9 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   h->sc.gen_done = reinterpret_cast<unsigned*>(base + o_gd);
   h->sc.plan = base + o_plan;
   h->sc.sink = reinterpret_cast<int32_t*>(base + o_sink);
+  h->sc.pred_jobs = reinterpret_cast<PredJob*>(base + o_jobs);
+  h->sc.pred_slots_i = reinterpret_cast<long long*>(base + o_psi);
+  h->sc.pred_slots_f = reinterpret_cast<double*>(base + o_psf);
   if (hipMemset(h->scratch, 0, o_mmp) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(h->scratch);
     delete h;
@@ -471,6 +480,7 @@ fxpq_status fxpq_qlayer_predicted(fxpq_handle h, const fxpq_src* src, int64_t n,
   if (st) return st;
   if (s.kind == FXPQ_SRC_INT && s.dtype == FXPQ_I64) return FXPQ_ERR_UNSUPPORTED;
   if (n / ((int64_t)kThreads * kWinMaxPerThread) + 1 > kMaxFlsBlocks - 4096) return FXPQ_ERR_UNSUPPORTED;
+  if (h->pred_defer && h->pred_n >= kMaxPredJobs) return FXPQ_ERR_UNSUPPORTED;
   DeviceGuard g(h->device);
   return hip_status(launch_qlayer_pred(ctx(h), s, n, wl, sign, fl_lo, fl_hi, d_fmt_out,
                                        static_cast<int8_t*>(codes), d_minmax, d_miss));
@@ -560,6 +570,7 @@ fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const 
   if (d->c % 16 != 0 || d->k % 4 != 0) return FXPQ_ERR_UNSUPPORTED;
   const int nb = conv_fused_blocks(*d, h->cus);
   if (nb < 1 || nb > kMaxConvBlocks) return FXPQ_ERR_UNSUPPORTED;
+  if (h->pred_defer && h->pred_n >= kMaxPredJobs) return FXPQ_ERR_UNSUPPORTED;
   SrcDev e;
   epi_to_dev(ep, &e);
   e.kind = FXPQ_SRC_ACC;
@@ -568,6 +579,22 @@ fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const 
   DeviceGuard g(h->device);
   return hip_status(launch_conv_pred(ctx(h), *d, x, x_type, w, w_colsum, e, wl, sign, fl_lo, fl_hi,
                                      d_fmt_out, static_cast<int8_t*>(y), d_minmax, d_miss));
+}
+
+fxpq_status fxpq_predicted_defer(fxpq_handle h, int32_t on) {
+  if (!h || (on != 0 && on != 1)) return FXPQ_ERR_INVALID_ARG;
+  if (h->pred_n != 0) return FXPQ_ERR_INVALID_ARG;  // decisions pending: decide first
+  h->pred_defer = on;
+  return FXPQ_OK;
+}
+
+fxpq_status fxpq_predicted_decide(fxpq_handle h) {
+  if (!h) return FXPQ_ERR_INVALID_ARG;
+  const int n = h->pred_n;
+  if (n == 0) return FXPQ_OK;
+  h->pred_n = 0;
+  DeviceGuard g(h->device);
+  return hip_status(launch_pred_decide(ctx(h), h->sc.pred_jobs, n));
 }
 
 fxpq_status fxpq_qconv(fxpq_handle h, const fxpq_conv_desc* d, const void* x, fxpq_dtype x_type,

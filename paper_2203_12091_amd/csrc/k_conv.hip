@@ -136,6 +136,10 @@ struct ConvArgs {
   const fxpq_fmt* fmt_req;
   int8_t* y;
   int y_type;
+  // EPI_PRED in deferred mode: block (0, 0) records the decision's inputs
+  PredJob* job;
+  unsigned* job_miss;
+  int64_t job_per_thread;
   // halo tiles: hG images of hTH output rows each (hG > 1 only with hTH ==
   // Ho), hTPI tiles per image (hG == 1), input patch hPH x hPW per image;
   // stores of rows that do not exist go to `sink` (32 int32)
@@ -188,6 +192,9 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     // the decision counts the call a miss; the min / max still go out)
     ws = win_setup<FXPQ_SRC_ACC>(a.ep, a.mm, a.wl, a.sign_req, a.fl_lo, a.fl_hi, MODE_SEARCH,
                                  PER_THREAD);
+    if (a.job && blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x == 0)
+      *a.job = PredJob{a.ep, a.wl, a.sign_req, a.fl_lo, a.fl_hi, 1, a.job_per_thread,
+                       const_cast<double*>(a.mm), a.fmt_win, a.job_miss, a.part_i, a.part_f};
   } else if constexpr (EPI == EPI_REQ) {
     const int sv = src_scale(a.ep);
     if (a.y_type == FXPQ_I8) qf = qfmt_setup<FXPQ_I8>(a.fmt_req, sv, a.flags);
@@ -1104,9 +1111,19 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
   a.fl_lo = fl_lo;
   a.fl_hi = fl_hi;
   a.mm = d_minmax;
-  const int set = fls_begin(c);
-  a.part_i = c.sc.win_part + (size_t)set * kWinSlots * kWinPart;
-  a.part_f = c.sc.win_part_f + (size_t)set * kWinSlots * kWinPartF;
+  // deferred mode: the call's own slot set and record, no decision launch
+  const int job = c.pred_jobs_n ? (*c.pred_jobs_n)++ : -1;
+  const int set = job < 0 ? fls_begin(c) : 0;
+  if (job < 0) {
+    a.part_i = c.sc.win_part + (size_t)set * kWinSlots * kWinPart;
+    a.part_f = c.sc.win_part_f + (size_t)set * kWinSlots * kWinPartF;
+  } else {
+    a.part_i = c.sc.pred_slots_i + (size_t)job * kWinSlots * kWinPart;
+    a.part_f = c.sc.pred_slots_f + (size_t)job * kWinSlots * kWinPartF;
+    a.job = c.sc.pred_jobs + job;
+    a.job_miss = miss;
+    a.job_per_thread = conv_per_thread(cfg);
+  }
   a.fmt_win = out;
   a.y = y;
   a.y_type = FXPQ_C8;
@@ -1115,7 +1132,7 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
   conv_run<EPI_PRED>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || job >= 0) return e;
   return launch_pred_fin(c, ep, set, wl, sign, fl_lo, fl_hi, conv_per_thread(cfg), d_minmax, out,
                          miss);
 }

@@ -193,8 +193,11 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
 template <int KIND, int DT, int NB>
 __global__ __launch_bounds__(kThreads) void k_qlayer_pred(
     SrcDev s, int64_t n, int wl, int sign_req, int fl_lo, int fl_hi, int64_t per_thread,
-    const double* mm, long long* part_i, double* part_f, const fxpq_fmt* out, int8_t* y) {
+    double* mm, long long* part_i, double* part_f, fxpq_fmt* out, int8_t* y, PredJob* job,
+    unsigned* miss) {
   __shared__ WinShared wsh;
+  if (job && blockIdx.x == 0 && threadIdx.x == 0)
+    *job = PredJob{s, wl, sign_req, fl_lo, fl_hi, NB, per_thread, mm, out, miss, part_i, part_f};
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const FlsU& u = ws.u;
   double mn = INFINITY, mx = -INFINITY;
@@ -409,29 +412,34 @@ __global__ __launch_bounds__(kFinThreads) void k_fls_window_fin(
 // format is recorded when the decision is final and is the candidate whose
 // codes the pass wrote, else *miss is set.  mm ends with this call's
 // min / max; the other slot set is cleared for the next search.
+// The decision itself, by one wave.  deferred: the calls that consumed this
+// call's codes have already run with the format held in *out (the
+// prediction), so a hit also needs the decision to be that format; the
+// slots are the call's own set, cleared afterwards for its next use.
 template <int KIND>
-__global__ __launch_bounds__(kFinThreads) void k_pred_fin(
-    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int nce, int64_t per_thread, double* mm,
-    const long long* part_i, const double* part_f, long long* clr_i, double* clr_f, fxpq_fmt* out,
-    unsigned* miss) {
+__device__ inline void pred_decision(const SrcDev& s, int wl, int sign_req, int fl_lo, int fl_hi,
+                                     int nce, int64_t per_thread, double* mm,
+                                     const long long* part_i, const double* part_f, fxpq_fmt* out,
+                                     unsigned* miss, bool deferred) {
   const double pred[2] = {mm[0], mm[1]};
   const long long* p = part_i + (threadIdx.x & 63) * kWinPart + kWinSums;
   const unsigned long long kmn = wave_reduce((unsigned long long)p[0], OpMaxU());
   const unsigned long long kmx = wave_reduce((unsigned long long)p[1], OpMaxU());
   const double act[2] = {kmn ? mm_unkey(~kmn) : INFINITY, kmx ? mm_unkey(kmx) : -INFINITY};
-  win_slots_clear(clr_i, clr_f);
   const WinSetup wp = win_setup<KIND>(s, pred, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const WinSetup wa = win_setup<KIND>(s, act, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const bool same = wp.verdict == 0 && wa.verdict == 0 && wp.b0 == wa.b0 && wp.b1 == wa.b1 &&
                     wp.nc == wa.nc && wp.bce == wa.bce && wp.u.sign == wa.u.sign &&
                     win_variant(wp.u, wp, pred) == win_variant(wa.u, wa, act);
+  const fxpq_fmt used = *out;
   bool hit = false, undecided = false;
   int fl = 0;
   if (same) {  // uniform over the wave
     const WinResult r = win_decide(wa, nce, fl_hi, part_i, part_f);
     if (threadIdx.x == 0) {
       fl = r.fl_win;
-      hit = r.done && r.fl_win == wa.b0 + pred_pick(wp, *out);
+      hit = r.done && r.fl_win == wa.b0 + pred_pick(wp, used);
+      if (deferred) hit = hit && used.fl == fl && used.sign == wa.u.sign && used.status == 0;
       undecided = !r.done;
     }
   }
@@ -444,6 +452,50 @@ __global__ __launch_bounds__(kFinThreads) void k_pred_fin(
     mm[0] = act[0];
     mm[1] = act[1];
   }
+}
+
+// Decision of a predicted C-Block or FxP-QLayer (one wave, after the pass):
+// combines the min / max keys of the slots into this call's exact min / max
+// and checks that the window the pass evaluated (from the predicted min / max
+// held in mm) is this call's window: same verdict 0, candidates, clipping
+// bound, sign and variant.  Then the wave decides from the window sums; the
+// format is recorded when the decision is final and is the candidate whose
+// codes the pass wrote, else *miss is set.  mm ends with this call's
+// min / max; the other slot set is cleared for the next search.
+template <int KIND>
+__global__ __launch_bounds__(kFinThreads) void k_pred_fin(
+    SrcDev s, int wl, int sign_req, int fl_lo, int fl_hi, int nce, int64_t per_thread, double* mm,
+    const long long* part_i, const double* part_f, long long* clr_i, double* clr_f, fxpq_fmt* out,
+    unsigned* miss) {
+  win_slots_clear(clr_i, clr_f);
+  pred_decision<KIND>(s, wl, sign_req, fl_lo, fl_hi, nce, per_thread, mm, part_i, part_f, out,
+                      miss, false);
+}
+
+// Deferred decisions: block b decides pending call b (recorded by the call's
+// own kernel), then clears that call's slot set.
+__global__ __launch_bounds__(kFinThreads) void k_pred_decide(const PredJob* jobs) {
+  const PredJob& j = jobs[blockIdx.x];
+  switch (j.s.kind) {
+    case FXPQ_SRC_ACC:
+      pred_decision<FXPQ_SRC_ACC>(j.s, j.wl, j.sign, j.fl_lo, j.fl_hi, j.nce, j.per_thread, j.mm,
+                                  j.pi, j.pf, j.out, j.miss, true);
+      break;
+    case FXPQ_SRC_ADD:
+      pred_decision<FXPQ_SRC_ADD>(j.s, j.wl, j.sign, j.fl_lo, j.fl_hi, j.nce, j.per_thread, j.mm,
+                                  j.pi, j.pf, j.out, j.miss, true);
+      break;
+    case FXPQ_SRC_F32:
+      pred_decision<FXPQ_SRC_F32>(j.s, j.wl, j.sign, j.fl_lo, j.fl_hi, j.nce, j.per_thread, j.mm,
+                                  j.pi, j.pf, j.out, j.miss, true);
+      break;
+    default:
+      pred_decision<FXPQ_SRC_INT>(j.s, j.wl, j.sign, j.fl_lo, j.fl_hi, j.nce, j.per_thread, j.mm,
+                                  j.pi, j.pf, j.out, j.miss, true);
+      break;
+  }
+  __syncthreads();
+  win_slots_clear(j.pi, j.pf);
 }
 
 // ---------------------------------------------------------------------------
@@ -806,6 +858,11 @@ hipError_t launch_qlayer(const Ctx& c, const SrcDev& s, int64_t n, int wl, int s
   return launch_requant_gated(c, s, n, out, codes, static_cast<const FlsPlan*>(c.sc.plan), alt);
 }
 
+hipError_t launch_pred_decide(const Ctx& c, const PredJob* jobs, int n) {
+  if (n > 0) k_pred_decide<<<n, kFinThreads, 0, c.stream>>>(jobs);
+  return hipGetLastError();
+}
+
 hipError_t launch_pred_fin(const Ctx& c, const SrcDev& ep, int set, int wl, int sign, int fl_lo,
                            int fl_hi, int64_t per_thread, double* d_minmax, fxpq_fmt* out,
                            unsigned* miss) {
@@ -825,7 +882,12 @@ hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
   const int channels = (s.kind == FXPQ_SRC_ACC) ? s.channels : 0;
   const int vec = (s.kind == FXPQ_SRC_ADD) ? 16 : 4;
   const int nce = (wl <= kCeMultiMaxWl) ? kCeBounds : 1;
-  const int set = fls_begin(c);
+  // deferred mode: the call's own slot set and record, no decision launch
+  const int job = c.pred_jobs_n ? (*c.pred_jobs_n)++ : -1;
+  const int set = job < 0 ? fls_begin(c) : 0;
+  long long* pi = job < 0 ? slots_i(c, set) : c.sc.pred_slots_i + (size_t)job * kWinSlots * kWinPart;
+  double* pf = job < 0 ? slots_f(c, set) : c.sc.pred_slots_f + (size_t)job * kWinSlots * kWinPartF;
+  PredJob* rec = job < 0 ? nullptr : c.sc.pred_jobs + job;
   int blocks = 0;
   int64_t per_thread = 0;
   auto run = [&](auto kernel, auto fin) {
@@ -833,12 +895,13 @@ hipError_t launch_qlayer_pred(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
     per_thread = window_per_thread(n, blocks, vec);
     bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
     kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, per_thread, d_minmax,
-                                              slots_i(c, set), slots_f(c, set), out, y);
+                                              pi, pf, out, y, rec, miss);
     const double elem = (s.kind == FXPQ_SRC_ADD) ? 2.0 : 4.0;
     timer_end(c, timed, (elem + 1.0) * (double)n);
-    fin<<<1, kFinThreads, 0, c.stream>>>(s, wl, sign, fl_lo, fl_hi, nce, per_thread, d_minmax,
-                                         slots_i(c, set), slots_f(c, set), slots_i(c, 1 - set),
-                                         slots_f(c, 1 - set), out, miss);
+    if (job < 0)
+      fin<<<1, kFinThreads, 0, c.stream>>>(s, wl, sign, fl_lo, fl_hi, nce, per_thread, d_minmax,
+                                           pi, pf, slots_i(c, 1 - set), slots_f(c, 1 - set), out,
+                                           miss);
   };
 #define FXPQ_QPRED(K, D)                                                            \
   (nce == 1 ? run(&k_qlayer_pred<K, D, 1>, &k_pred_fin<K>)                         \

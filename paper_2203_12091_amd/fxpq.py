@@ -22,7 +22,8 @@ EXPORTS = [
     "fxpq_create", "fxpq_destroy", "fxpq_set_stream", "fxpq_status_string", "fxpq_sync_status",
     "fxpq_quantize", "fxpq_requant", "fxpq_requant_addmm", "fxpq_fl_search", "fxpq_fl_search_static", "fxpq_qlayer", "fxpq_qlayer_predicted", "fxpq_preprocess", "fxpq_qconv", "fxpq_qgemm",
     "fxpq_qconv_wide_workspace", "fxpq_qconv_wide", "fxpq_acc_overflow",
-    "fxpq_cblock", "fxpq_cblock_predicted", "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
+    "fxpq_cblock", "fxpq_cblock_predicted", "fxpq_predicted_defer", "fxpq_predicted_decide",
+    "fxpq_set_conv_tiling", "fxpq_weight_colsum", "fxpq_maxpool", "fxpq_avgpool_global", "fxpq_layer_error",
     "fxpq_epilogue_scale", "fxpq_dequantize", "fxpq_prediction_ties", "fxpq_timer_start",
     "fxpq_timer_read",
     "fxpq_teacher_conv", "fxpq_teacher_affine", "fxpq_teacher_add", "fxpq_teacher_maxpool",
@@ -96,6 +97,8 @@ def lib():
             "fxpq_cblock": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int, p, p],
             "fxpq_cblock_predicted": [p, p, p, C.c_int, p, p, p, i32, i32, i32, i32, p, p, C.c_int,
                                       p, p],
+            "fxpq_predicted_defer": [p, i32],
+            "fxpq_predicted_decide": [p],
             "fxpq_weight_colsum": [p, p, i64, i64, p],
             "fxpq_set_conv_tiling": [p, i32],
             "fxpq_maxpool": [p, p, C.c_int, i32, i32, i32, i32, i32, i32, i32, p],
@@ -218,6 +221,14 @@ def preprocess(h, src, n, wl, strategy, psi_rule, fl_lo, fl_hi, d_fmt_out):
 
 def set_conv_tiling(h, mode):
     _call("fxpq_set_conv_tiling", h.value, mode)
+
+
+def predicted_defer(h, on):
+    _call("fxpq_predicted_defer", h.value, int(bool(on)))
+
+
+def predicted_decide(h):
+    _call("fxpq_predicted_decide", h.value)
 
 
 def qlayer(h, src, n, wl, sign, fl_lo, fl_hi, d_fmt_out, codes, code_type, codes_alt):

@@ -152,13 +152,15 @@ class CalibNet:
     buffers and the input; ``forward()`` enqueues a full calibration forward."""
 
     def __init__(self, name, seed=None, batch=None, image=None, device="cuda:0", wl_override=None,
-                 keep_acts=True, fused=False, qlayer=True, predict=True):
+                 keep_acts=True, fused=False, qlayer=True, predict=True, defer=True):
         import torch
         self.fused = fused
         self.qlayer = qlayer
         # predicted C-Blocks (fxpq_cblock_predicted) with a rerun of the
-        # standard calls from the first miss
+        # standard calls from the first miss; defer: their decisions all in
+        # one launch at the end of the forward (fxpq_predicted_decide)
         self.predict = predict and qlayer and not fused
+        self.defer = defer and self.predict
         self.misses = 0
         self.no_predict = set()  # ops whose window cannot decide alone
         self.torch = torch
@@ -170,6 +172,8 @@ class CalibNet:
         self.dev = torch.device(device)
         self.h = fx.Handle(self.dev.index or 0)
         fx.set_stream(self.h, torch.cuda.current_stream(self.dev))
+        if self.defer:
+            fx.predicted_defer(self.h, 1)
         self.graph = ARCH[name](self.seed)
         if wl_override:
             for n in self.graph:
@@ -555,7 +559,8 @@ class CalibNet:
         host synchronization to read the miss flags, and when a prediction
         failed the standard calls again from the first op that missed (every
         later op depended on it), so the results are always those of the
-        standard plan.  predict=False runs the standard plan on a predicting
+        standard plan.  With defer, the predicted calls' decisions run as one
+        launch after the last of them.  predict=False runs the standard plan on a predicting
         net (a caller that changed formats or data knows the predictions will
         fail).  After prepare_timers(), calls of the timed classes are
         bracketed by HIP events on the library's stream and (class, work,
@@ -566,6 +571,8 @@ class CalibNet:
             self._run(self.calls)
             return
         self._run(self.pcalls)
+        if self.defer:
+            fx.predicted_decide(self.h)
         miss = self.miss.cpu().numpy()
         if miss.any():
             first = int(np.flatnonzero(miss)[0])

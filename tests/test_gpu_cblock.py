@@ -253,6 +253,56 @@ def test_cblock_rejects_unsupported(fx, h):
 
 
 @pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
+def test_cblock_predicted_deferred(fx, h, orc, case):
+    """Deferred decisions (fxpq_predicted_defer / fxpq_predicted_decide):
+    several predicted calls, then one decision launch.  No prediction: a
+    miss; the oracle's format and min / max: a hit with the oracle's codes
+    (or a miss when the window cannot decide); the other window candidate's
+    format, or a format outside the window (which the standard decision
+    would have replaced, but the calls after it already used): a miss.
+    Every call's min / max ends exact."""
+    import torch
+    c = Case(*case, seed=71 + CASES.index(case)).upload(fx, h)
+    v, s = c.oracle_values(orc)
+    exact = (float(v.min()), float(v.max()))
+    fx.predicted_defer(h, 1)
+    try:
+        for wl in (8, 5):
+            note("cblock predicted deferred", case, wl)
+            ofl, osg, _ = orc.fl_search_i64(v, s, wl, orc.SIGN_AUTO, FL_LO, FL_HI)
+            b0 = max(FL_LO, beta_nosat(v, s, wl, osg))
+            calls = [("none", float("nan"), float("nan"), ofl), ("steady", *exact, ofl)]
+            if ofl in (b0, b0 + 1) and b0 + 1 <= FL_HI:
+                calls.append(("other", *exact, b0 + 1 if ofl == b0 else b0))
+            if ofl == b0 and b0 - 1 >= FL_LO:
+                calls.append(("outside", *exact, b0 - 1))
+            pend = []
+            for kind, lo, hi, fl in calls:
+                mm = torch.tensor([lo, hi], dtype=torch.float64, device=DEV)
+                miss = torch.zeros(1, dtype=torch.int32, device=DEV)
+                out = fmt_dev(wl, fl, osg)
+                pend.append((kind, fl, mm, miss, out, c.predicted(fx, h, wl, mm, out, miss)))
+            fx.predicted_decide(h)
+            steady = int(host(pend[1][3])[0])  # 2: the window alone cannot decide
+            assert steady in (0, 2), steady
+            for kind, fl, mm, miss, out, y in pend:
+                m = int(host(miss)[0])
+                assert tuple(host(mm)) == exact, kind
+                if kind == "steady":
+                    if m == 0:
+                        assert fmt_host(out) == (wl, ofl, osg, 0)
+                        assert np.array_equal(decode8(host(y), osg == 0),
+                                              orc.quantize_i64(v, s, wl, ofl, osg))
+                else:
+                    want = 1 if kind == "none" or steady == 0 else 2
+                    assert m == want, (kind, m)
+                    assert fmt_host(out) == (wl, fl, osg, 0), kind  # left as the calls used it
+    finally:
+        fx.predicted_defer(h, 0)
+    assert fx.sync_status(h) == 0
+
+
+@pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
 def test_cblock_predicted(fx, h, orc, case):
     """The predicted C-Block: with no prediction (NaN min / max) a miss that
     still leaves the exact min / max; with the previous call's min / max and

@@ -70,18 +70,19 @@ def test_fused_paths_match_two_call_forward(mods):
     # FxP-QLayers start from the formats the first one chose)
     nets, _ = mods
     res = {}
-    for fused, qlayer, predict in ((True, True, False), (False, True, False), (False, False, False),
-                                   (False, True, True)):
-        note("net resnet50 8x112 fused", fused, "qlayer", qlayer, "predict", predict)
+    for fused, qlayer, predict, defer in ((True, True, False, True), (False, True, False, True),
+                                          (False, False, False, True), (False, True, True, True),
+                                          (False, True, True, False)):
+        note("net resnet50 8x112 fused", fused, "qlayer", qlayer, "predict", predict, "defer", defer)
         net = nets.CalibNet("resnet50", batch=8, image=112, fused=fused, qlayer=qlayer,
-                            predict=predict)
+                            predict=predict, defer=defer)
         plan = net._plan()
         assert any(c[0] == "cblock" for c in plan) == fused
         assert any(c[2].__name__ == "fxpq_qlayer" for c in plan) == qlayer
         assert net.predict == predict
         for _ in range(2):
             net.forward()
-            res[(fused, qlayer, predict, _)] = net.results(with_codes=True)
+            res[(fused, qlayer, predict, defer, _)] = net.results(with_codes=True)
         if predict:
             # the first forward has no predictions; a layer whose window
             # cannot decide alone misses once more, then runs unpredicted
@@ -89,9 +90,9 @@ def test_fused_paths_match_two_call_forward(mods):
             m = net.misses
             net.forward()
             assert net.misses == m
-            res[(fused, qlayer, predict, 2)] = net.results(with_codes=True)
+            res[(fused, qlayer, predict, defer, 2)] = net.results(with_codes=True)
         net.close()
-    b = res[(False, False, False, 1)]
+    b = res[(False, False, False, True, 1)]
     for key, a in res.items():
         assert a["flags"] == 0, key
         assert a["fmts"] == b["fmts"], key
