@@ -297,11 +297,12 @@ def reduction_figures(dev, batch=32, image=224, thld=0.5, max_changes=None):
 
 def wide_figures(dev, batch=256):
     """Wide C-Blocks (fxpq_qconv_wide) at the shapes of ResNet-50's first and
-    last layers with 16-bit activations and weights: the first conv (7x7/2
-    over 224x224 RGB, Scale + ReLU epilogue) and the FC (2048 -> 1000, bias),
-    each timed over 5 calls after one untimed call; int8 operations of the
-    plane contractions and the combine's algorithmic bytes (4 B per plane-pair
-    accumulator read, 8 B per value written)."""
+    last layers, with 32-bit activations and weights (the paper's initial
+    design) and with 16-bit ones: the first conv (7x7/2 over 224x224 RGB,
+    Scale + ReLU epilogue) and the FC (2048 -> 1000, bias), each timed over 5
+    calls after one untimed call.  One contraction walks the plane pairs
+    (int8 operations: pairs x 2 M N depth) and writes the int64 values (8 B
+    each); the codes are random over the whole 32- / 16-bit range."""
     import torch
     from paper_2203_12091_amd import fxpq as fx
     h = fx.Handle(0)
@@ -310,53 +311,63 @@ def wide_figures(dev, batch=256):
 
     def codes(shape, wl):
         return torch.randint(-(1 << (wl - 1)), 1 << (wl - 1), shape, generator=gen, device=dev,
-                             dtype=torch.int32)
+                             dtype=torch.int64).to(torch.int32)
+
+    def planes(wl_x, wl_w):
+        px = (wl_x + 7) // 8
+        pw = next(n for n in range(1, 6) if (2 ** (wl_w - 1) - 1) <= 127 * ((256 ** n - 1) // 255))
+        return px * pw
 
     out = {}
     shapes = {"resnet50_conv1_b256": (fx.conv_desc(batch, 224, 224, 4, 64, 7, 7, 2, 3), True),
               "resnet50_fc_b256": (fx.conv_desc(batch, 1, 1, 2048, 1000, 1, 1, 1, 0), False)}
-    for name, (d, first) in shapes.items():
-        depth = d.r * d.s * d.c
-        wrow = (depth + 63) // 64 * 64 if d.c == 4 else depth
-        x = codes((d.n, d.h, d.w, d.c), 16)
-        if d.c == 4:
-            x[..., 3] = 0
-        w = codes((d.k, wrow), 16)
-        if d.c == 4:
-            w.view(d.k, -1)[:, depth:] = 0
-        fin = torch.tensor([16, 12, 1, 0], dtype=torch.int32, device=dev)
-        if first:
-            a1 = codes((d.k,), 16)
-            a2 = codes((d.k,), 32)
-            ep = fx.epilogue(d.k, 14, fin, relu=True, scale=a1, fl_scale=14, shift=a2, fl_shift=20)
-        else:
-            b = codes((d.k,), 32)
-            ep = fx.epilogue(d.k, 14, fin, bias=b, fl_bias=20)
-        nb = fx.qconv_wide_workspace(d, 16, 1, 16, 1)
-        ws = torch.empty(nb, dtype=torch.uint8, device=dev)
-        Ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
-        Wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
-        mk = d.n * Ho * Wo * d.k
-        v = torch.empty(mk, dtype=torch.int64, device=dev)
-        sc = torch.empty(1, dtype=torch.int32, device=dev)
-        call = lambda: fx.qconv_wide(h, d, x, 16, 1, w, 16, 1, ep, v, sc, ws, nb)
-        call()
-        torch.cuda.synchronize(dev)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        reps = 5
-        e0.record()
-        for _ in range(reps):
+    for bits in (32, 16):
+        for name, (d, first) in shapes.items():
+            depth = d.r * d.s * d.c
+            wrow = (depth + 63) // 64 * 64 if d.c == 4 else depth
+            x = codes((d.n, d.h, d.w, d.c), bits)
+            if d.c == 4:
+                x[..., 3] = 0
+            w = codes((d.k, wrow), bits)
+            if d.c == 4:
+                w.view(d.k, -1)[:, depth:] = 0
+            # fractional lengths small enough that full-range codes stay exact
+            fin = torch.tensor([bits, 2, 1, 0], dtype=torch.int32, device=dev)
+            if first:
+                a1 = codes((d.k,), 16)
+                a2 = codes((d.k,), 32)
+                ep = fx.epilogue(d.k, 2, fin, relu=True, scale=a1, fl_scale=1, shift=a2,
+                                 fl_shift=5)
+            else:
+                b = codes((d.k,), 32)
+                ep = fx.epilogue(d.k, 2, fin, bias=b, fl_bias=4)
+            nb = fx.qconv_wide_workspace(d, bits, 1, bits, 1)
+            ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+            Ho = (d.h + 2 * d.pad - d.r) // d.stride + 1
+            Wo = (d.w + 2 * d.pad - d.s) // d.stride + 1
+            mk = d.n * Ho * Wo * d.k
+            v = torch.empty(mk, dtype=torch.int64, device=dev)
+            sc = torch.empty(1, dtype=torch.int32, device=dev)
+            call = lambda: fx.qconv_wide(h, d, x, bits, 1, w, bits, 1, ep, v, sc, ws, nb)
             call()
-        e1.record()
-        torch.cuda.synchronize(dev)
-        ms = e0.elapsed_time(e1) / reps
-        pairs = 2 * 3  # 16-bit inputs: 2 byte planes; 16-bit signed weights: 3 balanced digits
-        ops = pairs * 2.0 * (mk // d.k) * d.k * (wrow if d.c == 4 else depth)
-        out[name] = {"ms": round(ms, 4), "plane_pairs": pairs, "workspace_mb": round(nb / 2 ** 20, 1),
-                     "int8_tops_per_call": round(ops / (ms * 1e-3) / 1e12, 1),
-                     "outputs": mk, "combine_bytes": (4 * pairs + 8) * mk}
-        assert fx.sync_status(h) == 0
-        del ws
+            torch.cuda.synchronize(dev)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            reps = 5
+            e0.record()
+            for _ in range(reps):
+                call()
+            e1.record()
+            torch.cuda.synchronize(dev)
+            ms = e0.elapsed_time(e1) / reps
+            pairs = planes(bits, bits)
+            ops = pairs * 2.0 * (mk // d.k) * d.k * wrow
+            out[f"{name}_{bits}x{bits}"] = {
+                "ms": round(ms, 4), "plane_pairs": pairs, "workspace_mb": round(nb / 2 ** 20, 1),
+                "int8_tops_per_call": round(ops / (ms * 1e-3) / 1e12, 1), "outputs": mk,
+                "value_bytes": 8 * mk}
+            flags = fx.sync_status(h)
+            assert flags & ~fx.FLAG_RANGE == 0, flags
+            del ws
     h.close()
     return out
 

@@ -439,8 +439,13 @@ fxpq_status fxpq_predicted_decide(fxpq_handle h);
  * for fxpq_fl_search / fxpq_requant / fxpq_qlayer.
  * Computed on the int8 matrix cores: x splits into ceil(wl_x / 8) base-256
  * planes (unsigned low bytes, the top byte signed for signed formats), w into
- * balanced base-256 digits in [-128, 127] (up to 5 for 32-bit weights), one
- * int8 contraction per plane pair, and an exact 128-bit combination.
+ * balanced base-256 digits in [-128, 127] (up to 5 for 32-bit weights); one
+ * contraction walks the plane pairs by shift 256^(p+q), sums each shift's
+ * pairs in int32 and folds them exactly into a 128-bit (or, when provably
+ * enough, 64-bit) accumulator per value, then applies the epilogue.  When
+ * min(planes of x, digits of w) * (r * s * c rounded up to 64) reaches 2^17
+ * the int32 group sums could overflow: one int8 contraction per plane pair
+ * into an int32 tensor and an exact combination pass instead.
  * workspace (device, 256-byte aligned, caller-owned) must hold at least the
  * bytes fxpq_qconv_wide_workspace reports for the same arguments; its
  * contents are unspecified afterwards.  Codes outside their format's range

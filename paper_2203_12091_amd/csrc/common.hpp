@@ -263,6 +263,21 @@ hipError_t launch_preprocess(const Ctx& c, const SrcDev& s, const double* d_minm
 hipError_t launch_colsum(const Ctx& c, const int8_t* w, int64_t k, int64_t len, int32_t* out);
 // Wide C-Blocks (k_wide.hip): digit planes of int32 codes, and the exact
 // combination of the plane contractions with the epilogue.
+// One fused wide C-Block contraction (see k_wide_fused).
+struct WideFusedArgs {
+  const int8_t* px;   // np_x input byte planes (NHWC), plane stride xs
+  int64_t xs;
+  const int8_t* pw;   // np_w weight digit planes [K][wrow], plane stride ws
+  int64_t ws;
+  const int32_t* cs;  // column sums of the weight planes [np_w][K]
+  int np_x, np_w, sign_x;
+  int N, H, W, C, K, R, S, stride, pad, Ho, Wo, M, kdepth, wrow;
+  SrcDev ep;
+  int64_t* v;
+  int32_t* d_scale;
+  unsigned* flags;
+};
+hipError_t launch_wide_fused(const Ctx& c, const WideFusedArgs& a, bool wide);
 hipError_t launch_wide_split_x(const Ctx& c, const int32_t* x, int64_t n, int np, int sign,
                                int64_t plane_stride, int8_t* planes);
 hipError_t launch_wide_split_w(const Ctx& c, const int32_t* w, int64_t n, int np, int sign,

@@ -610,6 +610,7 @@ namespace {
 // Plane counts and workspace layout of a wide C-Block.
 struct WideLayout {
   int np_x = 0, np_w = 0;
+  bool fused = false;  // one contraction (no per-pair int32 tensors)
   int64_t n_in = 0, wrow = 0, M = 0, mk = 0;
   int64_t xs = 0, ws = 0;                  // bytes per input / weight plane (256-aligned)
   int64_t off_w = 0, off_cs = 0, off_acc = 0, total = 0;
@@ -626,6 +627,14 @@ int wide_weight_planes(int wl, int sign) {
     if (qmin >= -128 * m && qmax <= 127 * m) return n;
   }
   return 5;
+}
+
+// Bits bounding the exact contraction of a wide C-Block: each plane pair's
+// int32 sum (< 2^31) times 256^(p+q), summed over the pairs.
+int wide_sum_bits(int np_x, int np_w) {
+  const int pairs = np_x * np_w;
+  const int lg = pairs <= 1 ? 0 : 32 - __builtin_clz((unsigned)(pairs - 1));  // ceil(log2 pairs)
+  return 31 + 8 * (np_x + np_w - 2) + lg;
 }
 
 bool wide_layout(const fxpq_conv_desc* d, int wl_x, int sign_x, int wl_w, int sign_w,
@@ -650,7 +659,12 @@ bool wide_layout(const fxpq_conv_desc* d, int wl_x, int sign_x, int wl_w, int si
   L->off_w = L->np_x * L->xs;
   L->off_cs = L->off_w + L->np_w * L->ws;
   L->off_acc = L->off_cs + align256((int64_t)L->np_w * d->k * 4);
-  L->total = L->off_acc + (int64_t)L->np_x * L->np_w * L->mk * 4;
+  // the fused contraction sums up to min(np_x, np_w) plane pairs of one
+  // shift in int32: |sum| <= pairs * padded depth * 2^14 < 2^31
+  const int64_t kpad = (L->wrow + 63) / 64 * 64;
+  const int gp = L->np_x < L->np_w ? L->np_x : L->np_w;
+  L->fused = (int64_t)gp * kpad < ((int64_t)1 << 17);
+  L->total = L->fused ? L->off_acc : L->off_acc + (int64_t)L->np_x * L->np_w * L->mk * 4;
   return true;
 }
 
@@ -697,6 +711,29 @@ fxpq_status fxpq_qconv_wide(fxpq_handle h, const fxpq_conv_desc* d, const int32_
     err = launch_wide_split_w(c, w, (int64_t)d->k * L.wrow, L.np_w, sign_w, L.ws, pw);
   for (int q = 0; q < L.np_w && err == hipSuccess; ++q)
     err = launch_colsum(c, pw + q * L.ws, d->k, L.wrow, cs + (int64_t)q * d->k);
+  if (L.fused && err == hipSuccess) {
+    WideFusedArgs fa{};
+    fa.px = px;
+    fa.xs = L.xs;
+    fa.pw = pw;
+    fa.ws = L.ws;
+    fa.cs = cs;
+    fa.np_x = L.np_x;
+    fa.np_w = L.np_w;
+    fa.sign_x = sign_x;
+    fa.N = d->n; fa.H = d->h; fa.W = d->w; fa.C = d->c; fa.K = d->k; fa.R = d->r; fa.S = d->s;
+    fa.stride = d->stride; fa.pad = d->pad;
+    fa.Ho = (d->h + 2 * d->pad - d->r) / d->stride + 1;
+    fa.Wo = (d->w + 2 * d->pad - d->s) / d->stride + 1;
+    fa.M = (int)L.M;
+    fa.kdepth = d->r * d->s * d->c;
+    fa.wrow = (int)L.wrow;
+    fa.ep = e;
+    fa.v = v;
+    fa.d_scale = d_scale;
+    fa.flags = h->sc.flags;
+    return hip_status(launch_wide_fused(c, fa, wide_sum_bits(L.np_x, L.np_w) >= 62));
+  }
   for (int p = 0; p < L.np_x && err == hipSuccess; ++p) {
     const int t = (p < L.np_x - 1 || !sign_x) ? FXPQ_U8OFF : FXPQ_I8;
     for (int q = 0; q < L.np_w && err == hipSuccess; ++q)

@@ -83,14 +83,16 @@ def test_wide_workspace_layout_on_host(fx):
     """Plane counts and workspace bytes of fxpq_qconv_wide (host arithmetic):
     ceil(wl / 8) input planes; balanced base-256 digits for the weights'
     code range (16-bit signed needs 3: 32767 > 127 * 257); 256-byte aligned
-    regions for the input planes, weight planes, column sums and one int32
-    accumulator tensor per plane pair."""
+    regions for the input planes, weight planes and column sums, plus one
+    int32 accumulator tensor per plane pair when the contraction is too deep
+    for the fused path."""
     d = fx.ConvDesc(2, 8, 8, 16, 32, 3, 3, 1, 1)
 
     def want(px, pw):
+        # one fused contraction: planes and column sums only
         a = lambda b: (b + 255) // 256 * 256
-        n_in, wrow, mk = 2 * 8 * 8 * 16, 9 * 16, 2 * 8 * 8 * 32
-        return px * a(n_in) + pw * a(32 * wrow) + a(pw * 32 * 4) + px * pw * mk * 4
+        n_in, wrow = 2 * 8 * 8 * 16, 9 * 16
+        return px * a(n_in) + pw * a(32 * wrow) + a(pw * 32 * 4)
 
     for (wx, sx, ww, sw), (px, pw) in [((16, 1, 16, 1), (2, 3)), ((16, 1, 15, 1), (2, 2)),
                                        ((8, 1, 8, 1), (1, 1)), ((8, 0, 8, 0), (1, 2)),
@@ -102,8 +104,14 @@ def test_wide_workspace_layout_on_host(fx):
     d4 = fx.ConvDesc(1, 10, 10, 4, 64, 7, 7, 2, 3)
     ho = (10 + 6 - 7) // 2 + 1
     a = lambda b: (b + 255) // 256 * 256
-    assert fx.qconv_wide_workspace(d4, 16, 1, 8, 1) == (
-        2 * a(400) + a(64 * 256) + a(64 * 4) + 2 * ho * ho * 64 * 4)
+    assert fx.qconv_wide_workspace(d4, 16, 1, 8, 1) == 2 * a(400) + a(64 * 256) + a(64 * 4)
+    # a contraction too deep for the fused path's int32 group sums (pairs of
+    # one shift * padded depth * 2^14 must stay below 2^31): one int32
+    # accumulator tensor per plane pair as well
+    dd = fx.ConvDesc(1, 2, 2, 8192, 16, 3, 3, 1, 1)
+    depth = 9 * 8192
+    assert fx.qconv_wide_workspace(dd, 16, 1, 16, 1) == (
+        2 * a(4 * 8192) + 3 * a(16 * depth) + a(3 * 16 * 4) + 2 * 3 * 4 * 16 * 4)
     for bad in [(0, 1, 8, 1), (8, 2, 8, 1), (33, 1, 8, 1), (8, 1, 33, 0), (32, -1, 8, 1)]:
         with pytest.raises(fx.FxpqError):
             fx.qconv_wide_workspace(d, *bad)

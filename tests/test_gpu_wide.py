@@ -121,6 +121,41 @@ def test_wide_cblock_values(fx, h, orc, case):
     assert fx.sync_status(h) == 0
 
 
+@pytest.mark.parametrize("wx,sx,ww,sw,C,planes", [(32, 1, 32, 1, 32768, (4, 5)),
+                                                  (24, 0, 16, 1, 45056, (3, 3))])
+def test_wide_cblock_deep_unfused(fx, h, orc, wx, sx, ww, sw, C, planes):
+    """A contraction too deep for the fused path (pairs of one shift x padded
+    depth x 2^14 reaches 2^31): one int8 contraction per plane pair and the
+    exact combination pass, against the oracle.  Codes kept small enough for
+    the exact values to stay below 2^62."""
+    import torch
+    N, K = 2, 8
+    px, pw = planes
+    assert min(px, pw) * C >= 2 ** 17
+    lo_x = -(2 ** 11) if sx else 0
+    xc = synth.integers(61, "deep-x", (N, C, 1, 1), lo_x, 2 ** 11).astype(np.int64)
+    wc = synth.integers(61, "deep-w", (K, C, 1, 1), -(2 ** 13), 2 ** 13).astype(np.int64)
+    xc[:, 0] = (1 << wx) - 1 if not sx else -(1 << (wx - 1))  # every plane's extremes
+    wc[:, 1] = (1 << (ww - 1)) - 1
+    desc = fx.conv_desc(N, 1, 1, C, K, 1, 1, 1, 0)
+    nb = fx.qconv_wide_workspace(desc, wx, sx, ww, sw)
+    a = lambda b: (b + 255) // 256 * 256
+    assert nb == px * a(N * C) + pw * a(K * C) + a(pw * K * 4) + px * pw * N * K * 4
+    ws = empty((nb,), torch.uint8)
+    v = empty((N * K,), torch.int64)
+    sc = empty((1,), torch.int32)
+    fin = fmt_dev(wx, 3, sx)
+    ep = fx.epilogue(K, 2, fin, relu=False)
+    note("qconv_wide deep unfused", wx, sx, ww, sw)
+    fx.qconv_wide(h, desc, dev(xc.reshape(N, 1, 1, C).astype(np.int32)), wx, sx,
+                  dev(wc.reshape(K, C).astype(np.int32)), ww, sw, ep, v, sc, ws, nb)
+    acc = orc.conv2d(xc, wc, 1, 0)
+    want, s_out = orc.epilogue(acc, 3 + 2)
+    assert int(host(sc)[0]) == s_out
+    assert np.array_equal(host(v), np.transpose(want, (0, 2, 3, 1)).reshape(-1))
+    assert fx.sync_status(h) == 0
+
+
 def test_wide_cblock_fxp_qlayer(fx, h, orc):
     """The FxP-QLayer over a wide C-Block: fl search (8 bits) and codes."""
     import torch
