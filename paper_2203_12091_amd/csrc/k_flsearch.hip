@@ -127,6 +127,173 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
   }
 }
 
+// ---------------------------------------------------------------------------
+// Eltwise sources through a histogram.  Every sum of the window pass (per
+// candidate sum q^2 and sum W q, sum W^2, the clipping error) and the min /
+// max depend on the values only through how often each integer
+// W = relu(a 2^sa + b 2^sb) occurs.  With two 8-bit codes and shifts of at
+// most 5 the sum before ReLU takes at most 255 * 33 + 1 values, so a block
+// counts them in an LDS histogram while it streams the operands and writes
+// the codes of the predicted candidate (16-bit lanes, two values per
+// register), and derives its window sums from the counts at the end: a few
+// instructions per value instead of the fp64 sums of every value.  The sums
+// are the same exact integers as the per-value form (the code of a value
+// exactly at qmax + 1/2 of the unsaturated candidate is qmax here, qmax + 1
+// there: the same error term).
+// ---------------------------------------------------------------------------
+constexpr int kAddHistBins = 33 * 256;  // >= 255 * (2^5 + 1) + 1
+constexpr int kAddHistSets = 2;         // register sets of the histogram pass
+
+typedef short s2v __attribute__((ext_vector_type(2)));
+
+struct AddHist {
+  int ok;
+  int d0;          // sigma - b0, in [1, 14]; candidate 1 shifts by d0 - 1
+  int ma, mb;      // 2^sa, 2^sb (one is 1)
+  int k;           // the +128 of offset-stored codes, aligned: W = a ma + b mb + k
+  int wlo, nbins;  // histogram bin i counts the sums (before ReLU) wlo + i
+  int relu;
+  int qmin, qmax;
+  int cs;          // fl of the clipping bound less sigma (<= 1)
+};
+
+// The histogram form applies when the window has two candidates, both
+// shifts are at most 5, the codes are 8 bits wide and a block adds at most
+// 2^31 values (counts in 32 bits; every sum W q per thread below 2^53).
+__device__ inline AddHist add_hist_setup(const SrcDev& s, const FlsU& u, const WinSetup& ws,
+                                         int64_t per_thread) {
+  AddHist p{};
+  const int F = imax(s.fa->fl, s.fb->fl);
+  const int sa = F - s.fa->fl, sb = F - s.fb->fl;
+  const int d0 = u.sigma - ws.b0;
+  const int cs = ws.bce - u.sigma;
+  p.ok = ws.nc == 2 && u.sigma == F && sa <= 5 && sb <= 5 && d0 >= 1 && d0 <= 14 && cs <= 1 &&
+         u.qmax <= 255.0 && u.qmin >= -128.0 && per_thread * kThreads <= (1ll << 31);
+  if (!p.ok) return p;
+  p.d0 = d0;
+  p.ma = 1 << sa;
+  p.mb = 1 << sb;
+  // offset-stored codes hold u - 128 as a signed byte
+  p.k = (code_is_off(s.dtype, s.fa) ? 128 * p.ma : 0) + (code_is_off(s.dtype2, s.fb) ? 128 * p.mb : 0);
+  p.wlo = -128 * (p.ma + p.mb) + p.k;
+  p.nbins = 255 * (p.ma + p.mb) + 1;
+  p.relu = s.relu;
+  p.qmin = (int)u.qmin;
+  p.qmax = (int)u.qmax;
+  p.cs = cs;
+  return p;
+}
+
+// rne(W / 2^d) per 16-bit lane (1 <= d <= 14, |W| < 2^14: no overflow).
+__device__ inline s2v rne_shr(s2v W, s2v dv, s2v halfm1) {
+  const s2v bit = (W >> dv) & (s2v){1, 1};
+  return (W + halfm1 + bit) >> dv;
+}
+
+// rne(W / 2^d) of one value (d >= 1).
+__device__ inline int rne_shr1(int W, int d) {
+  return (W + (1 << (d - 1)) - 1 + ((W >> d) & 1)) >> d;
+}
+
+// Bytes 1 and 3 of w, sign-extended, as two 16-bit lanes (permute
+// selectors 8 and 9 replicate the sign bits of bytes 1 and 3).
+__device__ inline s2v sext_odd_bytes(unsigned w) {
+  return __builtin_bit_cast(s2v, __builtin_amdgcn_perm(0u, w, 0x09030801u));
+}
+
+// Streams the operands: counts every sum in hist and writes the codes of the
+// candidate 2^-dp (dp = 0: the sum itself) to y, XOR xorw.
+template <bool DZ>
+__device__ __forceinline__ void add_hist_stream(const SrcDev& s, int64_t n, const AddHist& ap, int dp,
+                                                int8_t* y, unsigned xorw, unsigned* hist) {
+  using PK = Pack<FXPQ_SRC_ADD, FXPQ_I8>;
+  ThreadVals<PK::V> tv;  // unused by the raw callback
+  const s2v ma = {(short)ap.ma, (short)ap.ma}, mb = {(short)ap.mb, (short)ap.mb};
+  const s2v kv = {(short)ap.k, (short)ap.k};
+  const short lo = ap.relu ? 0 : (short)ap.qmin;
+  const s2v lov = {lo, lo}, hiv = {(short)ap.qmax, (short)ap.qmax};
+  const short h = DZ ? 0 : (short)((1 << (dp - 1)) - 1);
+  const s2v dv = {(short)dp, (short)dp}, hm = {h, h};
+  unsigned* hb = hist - ap.wlo;  // hb[W] is bin W - wlo
+  auto code = [&](s2v W) {
+    s2v q = DZ ? W : rne_shr(W, dv, hm);
+    q = q > lov ? q : lov;
+    return q < hiv ? q : hiv;
+  };
+  stream_packets<FXPQ_SRC_ADD, FXPQ_I8, false, kAddHistSets, true, true>(
+      s, n, tv, [&](const Raw<FXPQ_SRC_ADD, FXPQ_I8>& r, int64_t i0, int) {
+        const unsigned wa[4] = {(unsigned)r.a.x, (unsigned)r.a.y, (unsigned)r.a.z, (unsigned)r.a.w};
+        const unsigned wb[4] = {(unsigned)r.b.x, (unsigned)r.b.y, (unsigned)r.b.z, (unsigned)r.b.w};
+        unsigned cw[4];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          // lanes: values 4k, 4k + 2 (even) and 4k + 1, 4k + 3 (odd)
+          const s2v We = sext_odd_bytes(wa[k] << 8) * ma + (sext_odd_bytes(wb[k] << 8) * mb + kv);
+          const s2v Wo = sext_odd_bytes(wa[k]) * ma + (sext_odd_bytes(wb[k]) * mb + kv);
+          atomicAdd(hb + We.x, 1u);
+          atomicAdd(hb + Wo.x, 1u);
+          atomicAdd(hb + We.y, 1u);
+          atomicAdd(hb + Wo.y, 1u);
+          const s2v qe = code(We), qo = code(Wo);
+          cw[k] = __builtin_amdgcn_perm(__builtin_bit_cast(unsigned, qo),
+                                        __builtin_bit_cast(unsigned, qe), 0x06020400u) ^ xorw;
+        }
+        *reinterpret_cast<uint4*>(y + i0) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+      });
+}
+
+// The histogram pass of a predicted eltwise FxP-QLayer block: zero the
+// histogram, stream (codes of candidate pj), add the tail, then derive this
+// thread's share of the window sums and of the min / max from the counts.
+__device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const AddHist& ap, int pj,
+                                             int8_t* y, unsigned xorw, unsigned* hist, WinAcc& acc,
+                                             double* mn, double* mx) {
+  for (int i = threadIdx.x; i < ap.nbins; i += kThreads) hist[i] = 0u;
+  __syncthreads();
+  const int dp = ap.d0 - pj;
+  if (dp == 0) add_hist_stream<true>(s, n, ap, dp, y, xorw, hist);
+  else add_hist_stream<false>(s, n, ap, dp, y, xorw, hist);
+  const int lo = ap.relu ? 0 : ap.qmin;
+  auto clampq = [&](int q, int l) { return q < l ? l : (q > ap.qmax ? ap.qmax : q); };
+  if ((int64_t)blockIdx.x * kThreads + threadIdx.x == 0) {
+    const int8_t* xa = static_cast<const int8_t*>(s.x);
+    const int8_t* xb = static_cast<const int8_t*>(s.x2);
+    for (int64_t i = n - n % 16; i < n; ++i) {
+      const int W = (int)xa[i] * ap.ma + (int)xb[i] * ap.mb + ap.k;
+      atomicAdd(hist + (W - ap.wlo), 1u);
+      const int q = clampq(dp == 0 ? W : rne_shr1(W, dp), lo);
+      y[i] = (int8_t)((q & 0xFF) ^ (int)(xorw & 0xFF));
+    }
+  }
+  __syncthreads();
+  win_acc_zero(acc);
+  const double cce = ldexp(1.0, ap.cs), qmx = ap.qmax, qmn = ap.qmin;
+  int wmin = 0x7fffffff, wmax = -0x7fffffff - 1;
+  for (int i = threadIdx.x; i < ap.nbins; i += kThreads) {
+    const unsigned c = hist[i];
+    if (c == 0u) continue;
+    int W = ap.wlo + i;
+    if (ap.relu) W = W > 0 ? W : 0;
+    wmin = W < wmin ? W : wmin;
+    wmax = W > wmax ? W : wmax;
+    const int q0 = clampq(rne_shr1(W, ap.d0), ap.qmin);
+    const int q1 = clampq(ap.d0 == 1 ? W : rne_shr1(W, ap.d0 - 1), ap.qmin);
+    const double cd = (double)c;
+    acc.A[0] = fma(cd, (double)(q0 * q0), acc.A[0]);
+    acc.PL[0] = fma(cd, (double)(W * q0), acc.PL[0]);
+    acc.A[1] = fma(cd, (double)(q1 * q1), acc.A[1]);
+    acc.PL[1] = fma(cd, (double)(W * q1), acc.PL[1]);
+    acc.V2 = fma(cd, (double)W * (double)W, acc.V2);
+    const double t = (double)W * cce;
+    const double e1 = max64z(t - qmx), e2 = min64z(t - qmn);
+    acc.CE[0] = fma(cd, e1 * e1 + e2 * e2, acc.CE[0]);
+  }
+  if (wmin <= wmax) {
+    *mn = (double)wmin;
+    *mx = (double)wmax;
+  }
+}
+
 // Which window candidate's codes go to the output buffer of a fused
 // FxP-QLayer: candidate 1 when the format found by the previous search into
 // the same format (still in `out`) is that candidate's, else candidate 0.
@@ -201,7 +368,22 @@ __global__ __launch_bounds__(kThreads) void k_qlayer_pred(
   const WinSetup ws = win_setup<KIND>(s, mm, wl, sign_req, fl_lo, fl_hi, MODE_SEARCH, per_thread);
   const FlsU& u = ws.u;
   double mn = INFINITY, mx = -INFINITY;
-  if (ws.verdict == 0) {
+  bool counted = false;
+  if constexpr (KIND == FXPQ_SRC_ADD && NB == 1) {
+    __shared__ unsigned hist[kAddHistBins];
+    if (ws.verdict == 0) {
+      const AddHist ap = add_hist_setup(s, u, ws, per_thread);
+      if (ap.ok) {  // uniform over the grid
+        WinAcc acc;
+        add_hist_run(s, n, ap, pred_pick(ws, *out), y, u.sign ? 0u : 0x80808080u, hist, acc, &mn,
+                     &mx);
+        win_write_partials_int(acc, NB, blockIdx.x, part_i, part_f, wsh);
+        counted = true;
+      }
+    }
+  }
+  if (counted) {
+  } else if (ws.verdict == 0) {
     WinCodes wcd{};
     const int pj = pred_pick(ws, *out);
     wcd.y[pj] = y;

@@ -277,3 +277,46 @@ def test_qlayer_predicted(fx, h, orc):
                               orc.quantize_i64(vn, s_out, wl, ofl, osign), bn, "acc")
     assert hits >= 8, hits
     check_flags(fx, h)
+
+
+# Eltwise sums of the forms the predicted FxP-QLayer takes in packed 16-bit
+# integer arithmetic (both shifts <= 5, 8-bit codes, 8-bit or narrower
+# outputs), at both edges of each condition, and forms just outside them:
+# (fl_a, a unsigned, fl_b, b unsigned, code range of a, code range of b, wl).
+PACKED_FORMS = [
+    (3, 0, 3, 0, (-125, 125), (-125, 125), 8),   # sigma - b0 = 1: bound at sigma + 1
+    (4, 0, 4, 1, (-128, 127), (0, 255), 8),      # sigma - b0 = 2 (1 with ReLU): bound at sigma
+    (8, 0, 3, 1, (-128, 127), (0, 255), 8),      # a shifted by 5: |W| up to 8415
+    (2, 1, 7, 0, (0, 255), (-128, 127), 4),      # b shifted by 5, 4-bit output
+    (0, 1, 0, 1, (0, 255), (0, 255), 8),         # both unsigned: non-negative sums
+    (9, 0, 3, 0, (-128, 127), (-128, 127), 8),   # shift 6: the fp64 form
+    (5, 0, 5, 0, (-3, 3), (-3, 3), 8),           # sigma - b0 = 0: the fp64 form
+]
+
+
+@pytest.mark.parametrize("form", PACKED_FORMS, ids=lambda f: f"fl{f[0]}u{f[1]}-fl{f[2]}u{f[3]}-wl{f[6]}")
+def test_qlayer_predicted_eltwise_forms(fx, h, orc, form):
+    """The predicted FxP-QLayer over eltwise sums of every form the packed
+    16-bit path covers, and of forms beside them, equal to the oracle: codes,
+    format, min / max, with and without ReLU, whole packets and a ragged
+    tail."""
+    fla, ua, flb, ub, ra, rb, wl = form
+    n = 40_000 + 9
+    a = synth.integers(95, f"pa{fla}{ua}", (n,), *ra)
+    b = synth.integers(95, f"pb{flb}{ub}", (n,), *rb)
+    ad = dev((a - 128 * ua).astype(np.int8))
+    bd = dev((b - 128 * ub).astype(np.int8))
+    hits = cases = 0
+    for relu in (True, False):
+        for m in (n, 16 * 500):
+            src = fx.src_add(ad, fx.C8, fmt_dev(8, fla, 1 - ua), bd, fx.C8, fmt_dev(8, flb, 1 - ub),
+                             relu)
+            v, s = orc.eltwise_add(a[:m], fla, b[:m], flb, relu)
+            ofl, osign, _ = orc.fl_search_i64(v, s, wl, fx.SIGN_AUTO, FL_LO, FL_HI)
+            bn = beta_nosat([fr(v.min(), s), fr(v.max(), s)], wl, osign)
+            hits += run_predicted(fx, h, src, m, wl, (float(v.min()), float(v.max())),
+                                  (wl, ofl, osign, 0), orc.quantize_i64(v, s, wl, ofl, osign), bn,
+                                  f"add-{form}-relu{int(relu)}-{m}")
+            cases += 1
+    assert hits >= cases // 2, (hits, cases)
+    check_flags(fx, h)
