@@ -390,8 +390,8 @@ fxpq_status fxpq_cblock(fxpq_handle h, const fxpq_conv_desc* d, const void* x, f
  * the next call's prediction; NaN in d_minmax predicts nothing (a miss).
  * d_minmax: device double[2], caller-owned, in units of 2^-s of the C-Block
  * value (as fxpq_qconv writes it); d_miss: device uint32, caller-owned.
- * Requirements: as fxpq_cblock (C % 16 == 0; the padded RGB layout is not
- * supported), K % 4 == 0, 2 <= wl <= 8, y_type FXPQ_C8, y 16-byte aligned.
+ * Requirements: as fxpq_qconv (C % 16 == 0, or the padded RGB layout C == 4),
+ * K % 4 == 0, 2 <= wl <= 8, y_type FXPQ_C8, y 16-byte aligned.
  */
 fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const void* x,
                                   fxpq_dtype x_type, const int8_t* w, const int32_t* w_colsum,

@@ -237,7 +237,9 @@ hipError_t launch_fls_general(const Ctx& c, const SrcDev& s, int64_t n, int wl, 
 hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                        const int8_t* w, const int32_t* colsum, const SrcDev* ep, int32_t* acc,
                        double* d_minmax);
-int conv_fused_blocks(const fxpq_conv_desc& d, int cus);  // -1 when the fused path does not apply
+// Blocks of the fused / predicted C-Block launch; -1 when it does not apply
+// (the padded RGB layout: the predicted C-Block only, rgb_ok).
+int conv_fused_blocks(const fxpq_conv_desc& d, int cus, bool rgb_ok = false);
 hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x, int x_type,
                             const int8_t* w, const int32_t* colsum, const SrcDev& ep, int wl,
                             int sign, int fl_lo, int fl_hi, fxpq_fmt* out, int8_t* y,

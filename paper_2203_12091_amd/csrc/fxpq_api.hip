@@ -567,8 +567,9 @@ fxpq_status fxpq_cblock_predicted(fxpq_handle h, const fxpq_conv_desc* d, const 
   if (wl < 2 || wl > 8) return wl == 1 ? FXPQ_ERR_UNSUPPORTED : FXPQ_ERR_INVALID_ARG;
   if (sign != 0 && sign != 1 && sign != FXPQ_SIGN_AUTO) return FXPQ_ERR_INVALID_ARG;
   if (fl_lo > fl_hi || fl_lo < -64 || fl_hi > 64) return FXPQ_ERR_INVALID_ARG;
-  if (d->c % 16 != 0 || d->k % 4 != 0) return FXPQ_ERR_UNSUPPORTED;
-  const int nb = conv_fused_blocks(*d, h->cus);
+  // channel multiples of 16, or the padded RGB layout (conv_check)
+  if (d->k % 4 != 0) return FXPQ_ERR_UNSUPPORTED;
+  const int nb = conv_fused_blocks(*d, h->cus, true);
   if (nb < 1 || nb > kMaxConvBlocks) return FXPQ_ERR_UNSUPPORTED;
   if (h->pred_defer && h->pred_n >= kMaxPredJobs) return FXPQ_ERR_UNSUPPORTED;
   SrcDev e;

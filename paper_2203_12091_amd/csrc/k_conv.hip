@@ -896,7 +896,7 @@ static void conv_dispatch_loader(int loader, dim3 grid, hipStream_t st, const Co
     k_qconv<BM, BN, TM, TN, MINW, LD_GEN16, EPI><<<grid, 256, 0, st>>>(a);
   else if (loader == LD_HALO4 || loader == LD_HALO8)
     return;  // halo tiles have their own configurations
-  else if constexpr (EPI == EPI_ACC && BN == 64)
+  else if constexpr ((EPI == EPI_ACC || EPI == EPI_PRED) && BN == 64)
     k_qconv<BM, BN, TM, TN, MINW, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
 }
 
@@ -1021,12 +1021,12 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   return hipGetLastError();
 }
 
-int conv_fused_blocks(const fxpq_conv_desc& d, int cus) {
+int conv_fused_blocks(const fxpq_conv_desc& d, int cus, bool rgb_ok) {
   ConvArgs a{};
   int loader;
   int cfg;
   const dim3 grid = conv_setup(d, nullptr, 0, nullptr, nullptr, nullptr, a, loader, cfg, cus);
-  if (loader == LD_RGB4) return -1;
+  if (loader == LD_RGB4 && !rgb_ok) return -1;
   return (int)(grid.x * grid.y);
 }
 

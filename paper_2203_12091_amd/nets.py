@@ -487,11 +487,12 @@ class CalibNet:
 
     def _predictable(self, op, n, p):
         """A C-Block followed by its FxP-QLayer whose contraction the
-        predicted C-Block takes (channels a multiple of 16)."""
+        predicted C-Block takes (channels a multiple of 16, or the padded
+        RGB layout of a first conv)."""
         if op not in ("conv", "fc") or n.last:
             return False
         cin = p["Cin"] if op == "conv" else p["wlen"]
-        return cin % 16 == 0
+        return cin % 16 == 0 or (op == "conv" and cin == 4)
 
     def _plan_predicted(self, calls):
         """The forward with every predictable C-Block as one

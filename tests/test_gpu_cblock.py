@@ -95,8 +95,17 @@ class Case:
         import torch
         N, Cin, H, W, K, R = self.N, self.Cin, self.H, self.W, self.K, self.R
         in_signed, relu = self.in_signed, self.relu
-        x_nhwc = np.transpose(self.xc, (0, 2, 3, 1)) - (0 if in_signed else 128)
+        x_nhwc = np.transpose(self.xc, (0, 2, 3, 1))
         w_krsc = np.transpose(self.wc, (0, 2, 3, 1)).reshape(K, -1)
+        cin_dev = Cin
+        if Cin == 3:  # padded RGB: a zero fourth channel, filter rows padded to 64 bytes
+            x_nhwc = np.concatenate([x_nhwc, np.zeros(x_nhwc.shape[:3] + (1,), np.int64)], axis=3)
+            w4 = np.concatenate([np.transpose(self.wc, (0, 2, 3, 1)), np.zeros((K, R, R, 1), np.int64)],
+                                axis=3).reshape(K, -1)
+            kp = (w4.shape[1] + 63) // 64 * 64
+            w_krsc = np.concatenate([w4, np.zeros((K, kp - w4.shape[1]), np.int64)], axis=1)
+            cin_dev = 4
+        x_nhwc = x_nhwc - (0 if in_signed else 128)
         self.xd = dev(x_nhwc.astype(np.int8))
         self.wd = dev(w_krsc.astype(np.int8))
         self.x_type = fx.I8 if in_signed else fx.U8OFF
@@ -107,7 +116,7 @@ class Case:
         self.ep = fx.epilogue(K, self.fl_w, self.fin, bias=self.bd, fl_bias=self.fl_b, relu=relu,
                               scale=self.a1d, fl_scale=self.fl_a1, shift=self.a2d,
                               fl_shift=self.fl_a2)
-        self.desc = fx.conv_desc(N, H, W, Cin, K, R, R, self.stride, self.pad)
+        self.desc = fx.conv_desc(N, H, W, cin_dev, K, R, R, self.stride, self.pad)
         return self
 
     def oracle_values(self, orc):
@@ -157,6 +166,12 @@ CASES = [
     (2, 32, 10, 10, 40, 3, 1, 1, False, True),     # 3x3, ragged channels (k = 40)
     (1, 128, 7, 7, 512, 1, 1, 0, False, False),    # wide output, one row tile
     (300, 16, 1, 1, 96, 1, 1, 0, True, False),     # FC-like rows
+]
+# the predicted C-Block also takes a first conv over padded RGB (signed and
+# unsigned input codes, 7x7 stride 2, ragged rows)
+PRED_CASES = CASES + [
+    (2, 3, 23, 21, 64, 7, 2, 3, True, True),
+    (1, 3, 19, 17, 64, 7, 2, 3, False, False),
 ]
 
 
@@ -252,7 +267,7 @@ def test_cblock_rejects_unsupported(fx, h):
                   out, y, fx.C8, acc, mm)
 
 
-@pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
+@pytest.mark.parametrize("case", PRED_CASES, ids=[str(i) for i in range(len(PRED_CASES))])
 def test_cblock_predicted_deferred(fx, h, orc, case):
     """Deferred decisions (fxpq_predicted_defer / fxpq_predicted_decide):
     several predicted calls, then one decision launch.  No prediction: a
@@ -262,7 +277,7 @@ def test_cblock_predicted_deferred(fx, h, orc, case):
     would have replaced, but the calls after it already used): a miss.
     Every call's min / max ends exact."""
     import torch
-    c = Case(*case, seed=71 + CASES.index(case)).upload(fx, h)
+    c = Case(*case, seed=71 + PRED_CASES.index(case)).upload(fx, h)
     v, s = c.oracle_values(orc)
     exact = (float(v.min()), float(v.max()))
     fx.predicted_defer(h, 1)
@@ -302,7 +317,7 @@ def test_cblock_predicted_deferred(fx, h, orc, case):
     assert fx.sync_status(h) == 0
 
 
-@pytest.mark.parametrize("case", CASES, ids=[str(i) for i in range(len(CASES))])
+@pytest.mark.parametrize("case", PRED_CASES, ids=[str(i) for i in range(len(PRED_CASES))])
 def test_cblock_predicted(fx, h, orc, case):
     """The predicted C-Block: with no prediction (NaN min / max) a miss that
     still leaves the exact min / max; with the previous call's min / max and
@@ -310,7 +325,7 @@ def test_cblock_predicted(fx, h, orc, case):
     oracle's, or a miss when the window cannot decide alone; with the other
     window candidate's format, or a min / max from other data, a miss."""
     import torch
-    c = Case(*case, seed=51 + CASES.index(case)).upload(fx, h)
+    c = Case(*case, seed=51 + PRED_CASES.index(case)).upload(fx, h)
     v, s = c.oracle_values(orc)
     hits = 0
     for wl in (8, 6, 4):
