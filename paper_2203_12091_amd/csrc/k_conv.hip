@@ -780,8 +780,13 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     if (win) wc = win_ctx(u, ws);
     WinAcc wa;
     win_acc_zero(wa);
+    // byte selectors of the two transpose steps (v_perm: bytes 0-3 this
+    // lane's dword, 4-7 the partner's): step 1 pairs lanes j, j ^ 1 (even
+    // lanes keep bytes 0 and 2 of both, odd lanes bytes 1 and 3), step 2
+    // lanes j, j ^ 2 (the low or high halves of both)
     const int qj = lane & 3;
-    const unsigned m1 = (qj & 1) ? 0xFFFFFFFFu : 0u, m2 = (qj & 2) ? 0xFFFFFFFFu : 0u;
+    const unsigned s1 = (qj & 1) ? 0x03070105u : 0x06020400u;
+    const unsigned s2 = (qj & 2) ? 0x03020706u : 0x05040100u;
     // min / max from the integer extremes of each column (the epilogue is
     // monotonic in the accumulator within a channel), as EPI_ACC does
     int lo[TN], hi[TN];
@@ -829,15 +834,11 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
               const unsigned p23 = __builtin_amdgcn_perm((unsigned)c[3], (unsigned)c[2], 0x0C0C0400u);
               unsigned w4 = __builtin_amdgcn_perm(p23, p01, 0x05040100u);
               // lane j of the quad holds rows 0..3 of column j: transpose
-              // (branch-free: every lane computes both forms and keeps one)
-              const unsigned x1 = (unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0xB1, 0xF, 0xF, false);
-              const unsigned o1 = ((x1 & 0xFF00FF00u) >> 8) | (w4 & 0xFF00FF00u);
-              const unsigned e1 = (w4 & 0x00FF00FFu) | ((x1 & 0x00FF00FFu) << 8);
-              w4 = e1 ^ ((o1 ^ e1) & m1);
-              const unsigned x2 = (unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0x4E, 0xF, 0xF, false);
-              const unsigned o2 = ((x2 & 0xFFFF0000u) >> 16) | (w4 & 0xFFFF0000u);
-              const unsigned e2 = (w4 & 0x0000FFFFu) | ((x2 & 0x0000FFFFu) << 16);
-              w4 = e2 ^ ((o2 ^ e2) & m2);
+              // with one partner exchange and one per-lane byte permute per step
+              w4 = __builtin_amdgcn_perm((unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0xB1, 0xF, 0xF, false),
+                                         w4, s1);
+              w4 = __builtin_amdgcn_perm((unsigned)__builtin_amdgcn_mov_dpp((int)w4, 0x4E, 0xF, 0xF, false),
+                                         w4, s2);
               const int srow = rbase + qj;
               if (FULL || (srow < a.M && scol < a.K))
                 *reinterpret_cast<unsigned*>(a.y + (int64_t)srow * a.K + scol) = w4 ^ xorw;
