@@ -145,21 +145,25 @@ constexpr int kAddHistBins = 33 * 256;  // >= 255 * (2^5 + 1) + 1
 constexpr int kAddHistSets = 2;         // register sets of the histogram pass
 
 typedef short s2v __attribute__((ext_vector_type(2)));
+typedef unsigned short u2v __attribute__((ext_vector_type(2)));
 
 struct AddHist {
   int ok;
-  int d0;          // sigma - b0, in [1, 14]; candidate 1 shifts by d0 - 1
+  int d0;          // sigma - b0, in [-8, 14]; candidate 1 shifts by d0 - 1 (left when negative)
   int ma, mb;      // 2^sa, 2^sb (one is 1)
   int k;           // the +128 of offset-stored codes, aligned: W = a ma + b mb + k
   int wlo, nbins;  // histogram bin i counts the sums (before ReLU) wlo + i
   int relu;
   int qmin, qmax;
-  int cs;          // fl of the clipping bound less sigma (<= 1)
+  int cs;          // fl of the clipping bound less sigma
 };
 
 // The histogram form applies when the window has two candidates, both
 // shifts are at most 5, the codes are 8 bits wide and a block adds at most
-// 2^31 values (counts in 32 bits; every sum W q per thread below 2^53).
+// 2^31 values (counts in 32 bits; every sum W q per thread below 2^53).  A
+// candidate at or above sigma (d <= 0) takes the values exactly, W 2^-d:
+// within the predicted range (no value saturates at b0) these stay below
+// 2^10 in magnitude for both candidates.
 __device__ inline AddHist add_hist_setup(const SrcDev& s, const FlsU& u, const WinSetup& ws,
                                          int64_t per_thread) {
   AddHist p{};
@@ -167,7 +171,7 @@ __device__ inline AddHist add_hist_setup(const SrcDev& s, const FlsU& u, const W
   const int sa = F - s.fa->fl, sb = F - s.fb->fl;
   const int d0 = u.sigma - ws.b0;
   const int cs = ws.bce - u.sigma;
-  p.ok = ws.nc == 2 && u.sigma == F && sa <= 5 && sb <= 5 && d0 >= 1 && d0 <= 14 && cs <= 1 &&
+  p.ok = ws.nc == 2 && u.sigma == F && sa <= 5 && sb <= 5 && d0 >= -8 && d0 <= 14 &&
          u.qmax <= 255.0 && u.qmin >= -128.0 && per_thread * kThreads <= (1ll << 31);
   if (!p.ok) return p;
   p.d0 = d0;
@@ -190,8 +194,9 @@ __device__ inline s2v rne_shr(s2v W, s2v dv, s2v halfm1) {
   return (W + halfm1 + bit) >> dv;
 }
 
-// rne(W / 2^d) of one value (d >= 1).
+// rne(W / 2^d) of one value (d >= 1), W 2^-d exactly for d <= 0.
 __device__ inline int rne_shr1(int W, int d) {
+  if (d <= 0) return (int)((unsigned)W << (-d));
   return (W + (1 << (d - 1)) - 1 + ((W >> d) & 1)) >> d;
 }
 
@@ -202,8 +207,8 @@ __device__ inline s2v sext_odd_bytes(unsigned w) {
 }
 
 // Streams the operands: counts every sum in hist and writes the codes of the
-// candidate 2^-dp (dp = 0: the sum itself) to y, XOR xorw.
-template <bool DZ>
+// candidate 2^-dp to y, XOR xorw.  EXACT: dp <= 0, the codes are W 2^-dp.
+template <bool EXACT>
 __device__ __forceinline__ void add_hist_stream(const SrcDev& s, int64_t n, const AddHist& ap, int dp,
                                                 int8_t* y, unsigned xorw, unsigned* hist) {
   using PK = Pack<FXPQ_SRC_ADD, FXPQ_I8>;
@@ -212,11 +217,12 @@ __device__ __forceinline__ void add_hist_stream(const SrcDev& s, int64_t n, cons
   const s2v kv = {(short)ap.k, (short)ap.k};
   const short lo = ap.relu ? 0 : (short)ap.qmin;
   const s2v lov = {lo, lo}, hiv = {(short)ap.qmax, (short)ap.qmax};
-  const short h = DZ ? 0 : (short)((1 << (dp - 1)) - 1);
+  const short h = EXACT ? 0 : (short)((1 << (dp - 1)) - 1);
   const s2v dv = {(short)dp, (short)dp}, hm = {h, h};
+  const u2v lsh = {(unsigned short)(EXACT ? -dp : 0), (unsigned short)(EXACT ? -dp : 0)};
   unsigned* hb = hist - ap.wlo;  // hb[W] is bin W - wlo
   auto code = [&](s2v W) {
-    s2v q = DZ ? W : rne_shr(W, dv, hm);
+    s2v q = EXACT ? __builtin_bit_cast(s2v, __builtin_bit_cast(u2v, W) << lsh) : rne_shr(W, dv, hm);
     q = q > lov ? q : lov;
     return q < hiv ? q : hiv;
   };
@@ -251,7 +257,7 @@ __device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const A
   for (int i = threadIdx.x; i < ap.nbins; i += kThreads) hist[i] = 0u;
   __syncthreads();
   const int dp = ap.d0 - pj;
-  if (dp == 0) add_hist_stream<true>(s, n, ap, dp, y, xorw, hist);
+  if (dp <= 0) add_hist_stream<true>(s, n, ap, dp, y, xorw, hist);
   else add_hist_stream<false>(s, n, ap, dp, y, xorw, hist);
   const int lo = ap.relu ? 0 : ap.qmin;
   auto clampq = [&](int q, int l) { return q < l ? l : (q > ap.qmax ? ap.qmax : q); };
@@ -261,7 +267,7 @@ __device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const A
     for (int64_t i = n - n % 16; i < n; ++i) {
       const int W = (int)xa[i] * ap.ma + (int)xb[i] * ap.mb + ap.k;
       atomicAdd(hist + (W - ap.wlo), 1u);
-      const int q = clampq(dp == 0 ? W : rne_shr1(W, dp), lo);
+      const int q = clampq(rne_shr1(W, dp), lo);
       y[i] = (int8_t)((q & 0xFF) ^ (int)(xorw & 0xFF));
     }
   }
@@ -277,7 +283,7 @@ __device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const A
     wmin = W < wmin ? W : wmin;
     wmax = W > wmax ? W : wmax;
     const int q0 = clampq(rne_shr1(W, ap.d0), ap.qmin);
-    const int q1 = clampq(ap.d0 == 1 ? W : rne_shr1(W, ap.d0 - 1), ap.qmin);
+    const int q1 = clampq(rne_shr1(W, ap.d0 - 1), ap.qmin);
     const double cd = (double)c;
     acc.A[0] = fma(cd, (double)(q0 * q0), acc.A[0]);
     acc.PL[0] = fma(cd, (double)(W * q0), acc.PL[0]);

@@ -290,7 +290,9 @@ PACKED_FORMS = [
     (2, 1, 7, 0, (0, 255), (-128, 127), 4),      # b shifted by 5, 4-bit output
     (0, 1, 0, 1, (0, 255), (0, 255), 8),         # both unsigned: non-negative sums
     (9, 0, 3, 0, (-128, 127), (-128, 127), 8),   # shift 6: the fp64 form
-    (5, 0, 5, 0, (-3, 3), (-3, 3), 8),           # sigma - b0 = 0: the fp64 form
+    (3, 0, 3, 0, (-60, 60), (-60, 60), 8),       # sigma - b0 = 0 (-1 with ReLU): exact codes
+    (3, 0, 3, 1, (-100, 100), (0, 120), 8),      # signed + unsigned, sigma - b0 = 0
+    (5, 0, 5, 0, (-3, 3), (-3, 3), 8),           # values far below the scale: sigma - b0 = -4
 ]
 
 
