@@ -780,6 +780,15 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     if (win) wc = win_ctx(u, ws);
     WinAcc wa;
     win_acc_zero(wa);
+    // The window sums are formed from x = W 2^(b0 - sigma), the value in
+    // units of the first candidate's step, straight from the accumulator
+    // (multiplier and addend scaled by that power of two): its code is
+    // rne(x), the second candidate's rne(2 x), the clipping bound's
+    // argument x 2^(bce - b0).  Sums of x q and x^2 are those of W q and W^2
+    // scaled by 2^(b0 - sigma) and its square, exactly (every term keeps its
+    // bits); they are scaled back before the block reduction.
+    const double xs = win ? wc.cj[0] : 1.0;      // 2^(b0 - sigma)
+    const double xce = win ? wc.cce / xs : 1.0;  // 2^(bce - b0)
     // byte selectors of the two transpose steps (v_perm: bytes 0-3 this
     // lane's dword, 4-7 the partner's): step 1 pairs lanes j, j ^ 1 (even
     // lanes keep bytes 0 and 2 of both, odd lanes bytes 1 and 3), step 2
@@ -804,6 +813,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
         const int col = n0 + wn * WCOLS + ni * 32 + (lane & 31);
         double Mc, Ac;
         epi_channel_raw(a.ep, eu, eraw[ni], Mc, Ac);
+        Mc *= xs;
+        Ac *= xs;
         const int scol = n0 + wn * WCOLS + ni * 32 + ((lane & 31) & ~3);
 #pragma unroll
         for (int mi = 0; mi < TM; ++mi) {
@@ -820,10 +831,28 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
               c[jj] = 0;
               if constexpr (WIN) {
                 if (ok) {
-                  const double W = max64s(fma((double)v, Mc, Ac), relo);
-                  double q[kWindow];
-                  win_consume<false, NN, C0>(wc, wa, W, q);
-                  c[jj] = (int)q[PJ];
+                  static_assert(kWindow == 2, "two window candidates");
+                  const double x = max64s(fma((double)v, Mc, Ac), relo);
+                  wa.V2 = fma(x, x, wa.V2);
+                  double q0 = rint(x);
+                  if (C0) {
+                    q0 = min64(q0, wc.qmax);
+                    if (!NN) q0 = max64(q0, wc.qmin);
+                  }
+                  wa.A[0] = fma(q0, q0, wa.A[0]);
+                  wa.PL[0] = fma(x, q0, wa.PL[0]);
+                  double q1 = min64(rint(x + x), wc.qmax);
+                  if (!NN) q1 = max64(q1, wc.qmin);
+                  wa.A[1] = fma(q1, q1, wa.A[1]);
+                  wa.PL[1] = fma(x, q1, wa.PL[1]);
+                  const double t = x * xce;
+                  const double d1 = max64z(t - wc.qmax);
+                  wa.CE[0] = fma(d1, d1, wa.CE[0]);
+                  if (!NN) {
+                    const double d2 = min64z(t - wc.qmin);
+                    wa.CE[0] = fma(d2, d2, wa.CE[0]);
+                  }
+                  c[jj] = (int)(PJ ? q1 : q0);
                   if (PJ == 0 && !C0) c[jj] = min(c[jj], qmax);
                 }
               }
@@ -864,6 +893,12 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
         default: FXPQ_PRED_TILE(T, T); break;
       }
 #undef FXPQ_PRED_TILE
+      // back to the units of W: sum W q = 2^(sigma - b0) sum x q, sum W^2 =
+      // 2^(2 (sigma - b0)) sum x^2 (exact powers of two)
+      const double up = 1.0 / xs;
+      wa.PL[0] *= up;
+      wa.PL[1] *= up;
+      wa.V2 *= up * up;
       win_write_partials_int(wa, 1, bid, a.part_i, a.part_f, wsh);
     }
     double mn = INFINITY, mx = -INFINITY;
