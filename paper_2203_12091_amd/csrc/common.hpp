@@ -46,7 +46,12 @@ struct Scratch {
   struct PredJob* pred_jobs;     // [kMaxPredJobs]
   long long* pred_slots_i;       // [kMaxPredJobs][kWinSlots][kWinPart]
   double* pred_slots_f;          // [kMaxPredJobs][kWinSlots][kWinPartF]
+  // first-layer filters re-laid with every filter row padded to 8 taps
+  // (kRgbWBytes; nullptr: not available, the packed RGB loader runs)
+  int8_t* rgb_w;
 };
+
+constexpr size_t kRgbWBytes = 1 << 16;
 
 // Pending decisions of predicted calls in deferred mode (at most this many
 // between two fxpq_predicted_decide calls).

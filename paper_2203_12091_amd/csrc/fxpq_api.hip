@@ -218,6 +218,7 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   size_t o_plan = take(256);
   size_t o_sink = take(64 * sizeof(int32_t));
   size_t o_jobs = take((size_t)kMaxPredJobs * sizeof(PredJob));
+  size_t o_rgbw = take(kRgbWBytes);
   if (hipMalloc(&h->scratch, off) != hipSuccess) {
     delete h;
     return FXPQ_ERR_ALLOC;
@@ -236,6 +237,7 @@ fxpq_status fxpq_create(fxpq_handle* out, int device) {
   h->sc.pred_jobs = reinterpret_cast<PredJob*>(base + o_jobs);
   h->sc.pred_slots_i = reinterpret_cast<long long*>(base + o_psi);
   h->sc.pred_slots_f = reinterpret_cast<double*>(base + o_psf);
+  h->sc.rgb_w = reinterpret_cast<int8_t*>(base + o_rgbw);
   if (hipMemset(h->scratch, 0, o_mmp) != hipSuccess || hipDeviceSynchronize() != hipSuccess) {
     (void)hipFree(h->scratch);
     delete h;

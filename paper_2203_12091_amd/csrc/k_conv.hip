@@ -41,6 +41,7 @@
 namespace fxpq {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v4i_a4 __attribute__((ext_vector_type(4), aligned(4)));  // dword-aligned 16 bytes
 typedef int v16i __attribute__((ext_vector_type(16)));
 
 constexpr int BK = 64;
@@ -65,7 +66,8 @@ __device__ inline int lds_off(int row, int chunk) {
 // HALO8: C % 64 == 0, tiles of whole output-image rows whose input patch
 // (up to 256 / 512 pixels per channel chunk) is loaded into LDS once and read
 // by every filter tap, weights through the DMA ring.
-enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2, LD_DMA64 = 3, LD_HALO4 = 4, LD_HALO8 = 5 };
+enum Loader { LD_FAST64 = 0, LD_GEN16 = 1, LD_RGB4 = 2, LD_DMA64 = 3, LD_HALO4 = 4, LD_HALO8 = 5,
+              LD_RGB8 = 6 };
 
 constexpr bool is_halo(int loader) { return loader == LD_HALO4 || loader == LD_HALO8; }
 
@@ -563,6 +565,31 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
           const v4i t = *reinterpret_cast<const v4i*>(p);
           regA[i] = ok ? t : padv;
         }
+      } else if constexpr (LOADER == LD_RGB8) {
+        // filters re-laid as [r][s < 8][c]: chunk q = 4 kt + kc is filter
+        // row q / 2, taps 4 (q % 2) .. + 3, i.e. four neighbouring pixels of
+        // one input row -- one 16-byte load away from the image borders
+        // (the taps past S have zero weights: their pixels only need to be
+        // readable).  Rows past R are zero filter rows.
+        const int q = kt * 4 + kc;
+        const int r = q >> 1, s0 = (q & 1) * 4;
+#pragma unroll
+        for (int i = 0; i < ACH; ++i) {
+          v4i v = padv;
+          const int ih = ih0[i] + r, iw = iw0[i] + s0;
+          if (aval[i] && r < a.R && ih >= 0 && ih < a.H) {
+            const int8_t* rowp = abase[i] + (int64_t)ih * a.W * 4;
+            if (iw >= 0 && iw + 3 < a.W) {
+              v = *reinterpret_cast<const v4i_a4*>(rowp + iw * 4);
+            } else {
+#pragma unroll
+              for (int j = 0; j < 4; ++j)
+                if (s0 + j < a.S && iw + j >= 0 && iw + j < a.W)
+                  v[j] = *reinterpret_cast<const int*>(rowp + (iw + j) * 4);
+            }
+          }
+          regA[i] = v;
+        }
       } else {  // LD_RGB4: four 4-byte pixels per 16-byte chunk
 #pragma unroll
         for (int i = 0; i < ACH; ++i) {
@@ -932,8 +959,38 @@ static void conv_dispatch_loader(int loader, dim3 grid, hipStream_t st, const Co
     k_qconv<BM, BN, TM, TN, MINW, LD_GEN16, EPI><<<grid, 256, 0, st>>>(a);
   else if (loader == LD_HALO4 || loader == LD_HALO8)
     return;  // halo tiles have their own configurations
-  else if constexpr ((EPI == EPI_ACC || EPI == EPI_PRED) && BN == 64)
-    k_qconv<BM, BN, TM, TN, MINW, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
+  else if constexpr ((EPI == EPI_ACC || EPI == EPI_PRED) && BN == 64) {
+    if (loader == LD_RGB8) k_qconv<BM, BN, TM, TN, MINW, LD_RGB8, EPI><<<grid, 256, 0, st>>>(a);
+    else k_qconv<BM, BN, TM, TN, MINW, LD_RGB4, EPI><<<grid, 256, 0, st>>>(a);
+  }
+}
+
+// First-layer filters [k][(r S + s) 4 + c] (rows of wrow bytes) re-laid as
+// [k][r][s < 8][c] (rows of wrow8 bytes, zeros past R, S).
+__global__ void k_rgb8_weights(const int8_t* w, int K, int R, int S, int wrow, int8_t* out,
+                               int wrow8) {
+  const int64_t n = (int64_t)K * wrow8;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int k = (int)(i / wrow8), b = (int)(i - (int64_t)k * wrow8);
+    const int r = b >> 5, s = (b >> 2) & 7, c = b & 3;
+    out[i] = (r < R && s < S) ? w[(int64_t)k * wrow + (r * S + s) * 4 + c] : (int8_t)0;
+  }
+}
+
+// The padded RGB layout with filter rows of at most 8 taps: re-lay the
+// filters into the handle's buffer and switch to the 16-byte pixel loader.
+static void rgb8_setup(const Ctx& c, const fxpq_conv_desc& d, ConvArgs& a, int& loader) {
+  if (loader != LD_RGB4 || d.s > 8 || !c.sc.rgb_w) return;
+  const int wrow8 = (d.r * 32 + 63) / 64 * 64;
+  if ((size_t)d.k * wrow8 > kRgbWBytes) return;
+  const int64_t n = (int64_t)d.k * wrow8;
+  k_rgb8_weights<<<(int)((n + 255) / 256), 256, 0, c.stream>>>(a.w, d.k, d.r, d.s, a.wrow, c.sc.rgb_w,
+                                                               wrow8);
+  a.w = c.sc.rgb_w;
+  a.wrow = wrow8;
+  a.kdepth = wrow8;
+  loader = LD_RGB8;
 }
 
 // Convolutions the halo tiles take: 3x3 filters (stride 1 or 2), 64-channel
@@ -1051,6 +1108,7 @@ hipError_t launch_conv(const Ctx& c, const fxpq_conv_desc& d, const void* x, int
   a.want_mm = (ep != nullptr && d_minmax != nullptr);
   a.mm_part = c.sc.minmax_part;
   bool timed = timer_begin(c, FXPQ_TIMER_QCONV);
+  rgb8_setup(c, d, a, loader);
   conv_run<EPI_ACC>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   if (a.want_mm) return launch_minmax_fin(c, a.mm_part, (int)(grid.x * grid.y), d_minmax);
@@ -1165,6 +1223,7 @@ hipError_t launch_conv_pred(const Ctx& c, const fxpq_conv_desc& d, const void* x
   a.y_type = FXPQ_C8;
   a.flags = c.sc.flags;
   bool timed = timer_begin(c, FXPQ_TIMER_CBLOCK_PRED);
+  rgb8_setup(c, d, a, loader);
   conv_run<EPI_PRED>(a, loader, cfg, grid, c.stream);
   timer_end(c, timed, 2.0 * (double)a.M * (double)d.k * (double)(d.r * d.s * d.c));
   hipError_t e = hipGetLastError();
