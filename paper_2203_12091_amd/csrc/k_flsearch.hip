@@ -206,31 +206,47 @@ __device__ inline s2v sext_odd_bytes(unsigned w) {
   return __builtin_bit_cast(s2v, __builtin_amdgcn_perm(0u, w, 0x09030801u));
 }
 
-// Streams the operands: counts every sum in hist and writes the codes of the
-// candidate 2^-dp to y, XOR xorw.  EXACT: dp <= 0, the codes are W 2^-dp.
-template <bool EXACT>
-__device__ __forceinline__ void add_hist_stream(const SrcDev& s, int64_t n, const AddHist& ap, int dp,
-                                                int8_t* y, unsigned xorw, unsigned* hist) {
+// Streams the operands: counts every sum in hist and writes the codes of
+// candidate 0 (2^-d0) to y0 and of candidate 1 (2^-(d0 - 1)) to y1, XOR xorw
+// (Y0, Y1: the buffers exist).  DM: both candidates round (d0 >= 2), only
+// candidate 0 rounds (d0 = 1), or both take the values exactly, W 2^-d
+// (d0 <= 0).
+enum { kHistBothRound = 2, kHistOneRounds = 1, kHistExact = 0 };
+
+template <int DM, bool Y0, bool Y1>
+__device__ __forceinline__ void add_hist_stream(const SrcDev& s, int64_t n, const AddHist& ap,
+                                                int8_t* y0, int8_t* y1, unsigned xorw,
+                                                unsigned* hist) {
   using PK = Pack<FXPQ_SRC_ADD, FXPQ_I8>;
   ThreadVals<PK::V> tv;  // unused by the raw callback
   const s2v ma = {(short)ap.ma, (short)ap.ma}, mb = {(short)ap.mb, (short)ap.mb};
   const s2v kv = {(short)ap.k, (short)ap.k};
-  const short lo = ap.relu ? 0 : (short)ap.qmin;
+  const short lo = ap.relu ? 0 : (short)ap.qmin;  // ReLU folds into the lower clamp
   const s2v lov = {lo, lo}, hiv = {(short)ap.qmax, (short)ap.qmax};
-  const short h = EXACT ? 0 : (short)((1 << (dp - 1)) - 1);
-  const s2v dv = {(short)dp, (short)dp}, hm = {h, h};
-  const u2v lsh = {(unsigned short)(EXACT ? -dp : 0), (unsigned short)(EXACT ? -dp : 0)};
+  const short d0 = (short)ap.d0, d1 = (short)(ap.d0 - 1);
+  const short h0 = DM >= kHistOneRounds ? (short)((1 << (d0 - 1)) - 1) : 0;
+  const short h1 = DM == kHistBothRound ? (short)((1 << (d1 - 1)) - 1) : 0;
+  const s2v dv0 = {d0, d0}, dv1 = {d1, d1}, hm0 = {h0, h0}, hm1 = {h1, h1};
+  const unsigned short l0 = DM == kHistExact ? (unsigned short)(-d0) : 0;
+  const unsigned short l1 = DM == kHistBothRound ? 0 : (unsigned short)(-d1);
+  const u2v lsh0 = {l0, l0}, lsh1 = {l1, l1};
   unsigned* hb = hist - ap.wlo;  // hb[W] is bin W - wlo
-  auto code = [&](s2v W) {
-    s2v q = EXACT ? __builtin_bit_cast(s2v, __builtin_bit_cast(u2v, W) << lsh) : rne_shr(W, dv, hm);
+  auto clampq = [&](s2v q) {
     q = q > lov ? q : lov;
     return q < hiv ? q : hiv;
+  };
+  auto shl = [](s2v W, u2v sh) { return __builtin_bit_cast(s2v, __builtin_bit_cast(u2v, W) << sh); };
+  auto code0 = [&](s2v W) { return clampq(DM >= kHistOneRounds ? rne_shr(W, dv0, hm0) : shl(W, lsh0)); };
+  auto code1 = [&](s2v W) { return clampq(DM == kHistBothRound ? rne_shr(W, dv1, hm1) : shl(W, lsh1)); };
+  auto pack = [&](s2v qe, s2v qo) {
+    return __builtin_amdgcn_perm(__builtin_bit_cast(unsigned, qo), __builtin_bit_cast(unsigned, qe),
+                                 0x06020400u) ^ xorw;
   };
   stream_packets<FXPQ_SRC_ADD, FXPQ_I8, false, kAddHistSets, true, true>(
       s, n, tv, [&](const Raw<FXPQ_SRC_ADD, FXPQ_I8>& r, int64_t i0, int) {
         const unsigned wa[4] = {(unsigned)r.a.x, (unsigned)r.a.y, (unsigned)r.a.z, (unsigned)r.a.w};
         const unsigned wb[4] = {(unsigned)r.b.x, (unsigned)r.b.y, (unsigned)r.b.z, (unsigned)r.b.w};
-        unsigned cw[4];
+        unsigned cw0[4], cw1[4];
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
           // lanes: values 4k, 4k + 2 (even) and 4k + 1, 4k + 3 (odd)
@@ -240,25 +256,35 @@ __device__ __forceinline__ void add_hist_stream(const SrcDev& s, int64_t n, cons
           atomicAdd(hb + Wo.x, 1u);
           atomicAdd(hb + We.y, 1u);
           atomicAdd(hb + Wo.y, 1u);
-          const s2v qe = code(We), qo = code(Wo);
-          cw[k] = __builtin_amdgcn_perm(__builtin_bit_cast(unsigned, qo),
-                                        __builtin_bit_cast(unsigned, qe), 0x06020400u) ^ xorw;
+          if (Y0) cw0[k] = pack(code0(We), code0(Wo));
+          if (Y1) cw1[k] = pack(code1(We), code1(Wo));
         }
-        *reinterpret_cast<uint4*>(y + i0) = make_uint4(cw[0], cw[1], cw[2], cw[3]);
+        if (Y0) *reinterpret_cast<uint4*>(y0 + i0) = make_uint4(cw0[0], cw0[1], cw0[2], cw0[3]);
+        if (Y1) *reinterpret_cast<uint4*>(y1 + i0) = make_uint4(cw1[0], cw1[1], cw1[2], cw1[3]);
       });
 }
 
-// The histogram pass of a predicted eltwise FxP-QLayer block: zero the
-// histogram, stream (codes of candidate pj), add the tail, then derive this
-// thread's share of the window sums and of the min / max from the counts.
-__device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const AddHist& ap, int pj,
-                                             int8_t* y, unsigned xorw, unsigned* hist, WinAcc& acc,
-                                             double* mn, double* mx) {
+// The histogram pass of an eltwise window (a block's share): zero the
+// histogram, stream (codes of candidate 0 to y0, of candidate 1 to y1, when
+// given), add the tail, then derive this thread's share of the window sums
+// (nb clipping bounds) and of the min / max from the counts.
+__device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const AddHist& ap, int nb,
+                                             int8_t* y0, int8_t* y1, unsigned xorw, unsigned* hist,
+                                             WinAcc& acc, double* mn, double* mx) {
   for (int i = threadIdx.x; i < ap.nbins; i += kThreads) hist[i] = 0u;
   __syncthreads();
-  const int dp = ap.d0 - pj;
-  if (dp <= 0) add_hist_stream<true>(s, n, ap, dp, y, xorw, hist);
-  else add_hist_stream<false>(s, n, ap, dp, y, xorw, hist);
+  const int dm = ap.d0 >= 2 ? kHistBothRound : (ap.d0 == 1 ? kHistOneRounds : kHistExact);
+#define FXPQ_AHS(DM)                                                          \
+  do {                                                                        \
+    if (y0 && y1) add_hist_stream<DM, true, true>(s, n, ap, y0, y1, xorw, hist);   \
+    else if (y0) add_hist_stream<DM, true, false>(s, n, ap, y0, y1, xorw, hist);   \
+    else if (y1) add_hist_stream<DM, false, true>(s, n, ap, y0, y1, xorw, hist);   \
+    else add_hist_stream<DM, false, false>(s, n, ap, y0, y1, xorw, hist);          \
+  } while (0)
+  if (dm == kHistBothRound) FXPQ_AHS(kHistBothRound);
+  else if (dm == kHistOneRounds) FXPQ_AHS(kHistOneRounds);
+  else FXPQ_AHS(kHistExact);
+#undef FXPQ_AHS
   const int lo = ap.relu ? 0 : ap.qmin;
   auto clampq = [&](int q, int l) { return q < l ? l : (q > ap.qmax ? ap.qmax : q); };
   if ((int64_t)blockIdx.x * kThreads + threadIdx.x == 0) {
@@ -267,8 +293,8 @@ __device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const A
     for (int64_t i = n - n % 16; i < n; ++i) {
       const int W = (int)xa[i] * ap.ma + (int)xb[i] * ap.mb + ap.k;
       atomicAdd(hist + (W - ap.wlo), 1u);
-      const int q = clampq(rne_shr1(W, dp), lo);
-      y[i] = (int8_t)((q & 0xFF) ^ (int)(xorw & 0xFF));
+      if (y0) y0[i] = (int8_t)((clampq(rne_shr1(W, ap.d0), lo) & 0xFF) ^ (int)(xorw & 0xFF));
+      if (y1) y1[i] = (int8_t)((clampq(rne_shr1(W, ap.d0 - 1), lo) & 0xFF) ^ (int)(xorw & 0xFF));
     }
   }
   __syncthreads();
@@ -290,9 +316,16 @@ __device__ __forceinline__ void add_hist_run(const SrcDev& s, int64_t n, const A
     acc.A[1] = fma(cd, (double)(q1 * q1), acc.A[1]);
     acc.PL[1] = fma(cd, (double)(W * q1), acc.PL[1]);
     acc.V2 = fma(cd, (double)W * (double)W, acc.V2);
-    const double t = (double)W * cce;
-    const double e1 = max64z(t - qmx), e2 = min64z(t - qmn);
-    acc.CE[0] = fma(cd, e1 * e1 + e2 * e2, acc.CE[0]);
+    // clipping errors at the first nb fl above the window: W 2^(fl - sigma)
+    // doubles (exactly) from one to the next
+    double t = (double)W * cce;
+#pragma unroll
+    for (int k = 0; k < kCeBounds; ++k) {
+      if (k >= nb) break;
+      if (k) t += t;
+      const double e1 = max64z(t - qmx), e2 = min64z(t - qmn);
+      acc.CE[k] = fma(cd, e1 * e1 + e2 * e2, acc.CE[k]);
+    }
   }
   if (wmin <= wmax) {
     *mn = (double)wmin;
@@ -348,6 +381,17 @@ __global__ __launch_bounds__(kThreads) void k_fls_window(
     wcd.xorw = u.sign ? 0u : 0x80808080u;
   }
   WinAcc acc;
+  if constexpr (KIND == FXPQ_SRC_ADD) {
+    // eltwise sums through the histogram when it applies (uniform)
+    __shared__ unsigned hist[kAddHistBins];
+    const AddHist ap = add_hist_setup(s, u, ws, per_thread);
+    if (ap.ok) {
+      double mn, mx;  // not needed: the search has the min / max
+      add_hist_run(s, n, ap, NB, wcd.y[0], wcd.y[1], wcd.xorw, hist, acc, &mn, &mx);
+      win_write_partials_int(acc, NB, blockIdx.x, part_i, part_f, wsh);
+      return;
+    }
+  }
   switch (win_variant(u, ws, mm)) {
     case 0: win_loop<KIND, DT, false, false, NB, CODES>(s, n, u, ws, wcd, acc); break;
     case 1: win_loop<KIND, DT, false, true, NB, CODES>(s, n, u, ws, wcd, acc); break;
@@ -375,14 +419,15 @@ __global__ __launch_bounds__(kThreads) void k_qlayer_pred(
   const FlsU& u = ws.u;
   double mn = INFINITY, mx = -INFINITY;
   bool counted = false;
-  if constexpr (KIND == FXPQ_SRC_ADD && NB == 1) {
+  if constexpr (KIND == FXPQ_SRC_ADD) {
     __shared__ unsigned hist[kAddHistBins];
     if (ws.verdict == 0) {
       const AddHist ap = add_hist_setup(s, u, ws, per_thread);
       if (ap.ok) {  // uniform over the grid
         WinAcc acc;
-        add_hist_run(s, n, ap, pred_pick(ws, *out), y, u.sign ? 0u : 0x80808080u, hist, acc, &mn,
-                     &mx);
+        const int pj = pred_pick(ws, *out);
+        add_hist_run(s, n, ap, NB, pj ? nullptr : y, pj ? y : nullptr, u.sign ? 0u : 0x80808080u,
+                     hist, acc, &mn, &mx);
         win_write_partials_int(acc, NB, blockIdx.x, part_i, part_f, wsh);
         counted = true;
       }
@@ -1003,6 +1048,7 @@ static hipError_t fl_search_passes(const Ctx& c, const SrcDev& s, int64_t n, int
   const int set = fls_begin(c);
   auto run = [&](auto kernel) {
     blocks = stream_grid(n, channels, kWinMaxPerThread, vec, resident_blocks(c, (const void*)kernel));
+    if (s.kind == FXPQ_SRC_ADD && blocks > 2 * c.cus) blocks = 2 * c.cus;  // as the predicted pass
     per_thread = window_per_thread(n, blocks, vec);
     bool timed = timer_begin(c, FXPQ_TIMER_FLS_WINDOW);
     kernel<<<blocks, kThreads, 0, c.stream>>>(s, n, wl, sign, fl_lo, fl_hi, mode, per_thread,
