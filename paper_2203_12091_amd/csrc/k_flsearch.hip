@@ -134,7 +134,7 @@ __device__ inline void win_loop(const SrcDev& s, int64_t n, const FlsU& u, const
 // W = relu(a 2^sa + b 2^sb) occurs.  With two 8-bit codes and shifts of at
 // most 5 the sum before ReLU takes at most 255 * 33 + 1 values, so a block
 // counts them in an LDS histogram while it streams the operands and writes
-// the codes of the predicted candidate (16-bit lanes, two values per
+// the codes of the wanted window candidate(s) (16-bit lanes, two values per
 // register), and derives its window sums from the counts at the end: a few
 // instructions per value instead of the fp64 sums of every value.  The sums
 // are the same exact integers as the per-value form (the code of a value
@@ -162,8 +162,10 @@ struct AddHist {
 // shifts are at most 5, the codes are 8 bits wide and a block adds at most
 // 2^31 values (counts in 32 bits; every sum W q per thread below 2^53).  A
 // candidate at or above sigma (d <= 0) takes the values exactly, W 2^-d:
-// within the predicted range (no value saturates at b0) these stay below
-// 2^10 in magnitude for both candidates.
+// within the range the window was set up for (no value saturates at b0)
+// these stay below 2^10 in magnitude for both candidates; beyond it (a
+// predicted range that turns out wrong: the call is a miss) they wrap in
+// their 16-bit lanes without effect on anything kept.
 __device__ inline AddHist add_hist_setup(const SrcDev& s, const FlsU& u, const WinSetup& ws,
                                          int64_t per_thread) {
   AddHist p{};
