@@ -859,7 +859,13 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
               if constexpr (WIN) {
                 if (ok) {
                   static_assert(kWindow == 2, "two window candidates");
-                  const double x = max64s(fma((double)v, Mc, Ac), relo);
+                  // a window with negative values (!NN) is never a ReLU
+                  // layer's (its values are >= 0, so is the previous call's
+                  // minimum): no max with the ReLU bound there; a prediction
+                  // that says otherwise is a miss anyway (its window's
+                  // variant differs from the actual one)
+                  double x = fma((double)v, Mc, Ac);
+                  if (NN) x = max64s(x, relo);
                   wa.V2 = fma(x, x, wa.V2);
                   double q0 = rint(x);
                   if (C0) {
