@@ -816,6 +816,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     // bits); they are scaled back before the block reduction.
     const double xs = win ? wc.cj[0] : 1.0;      // 2^(b0 - sigma)
     const double xce = win ? wc.cce / xs : 1.0;  // 2^(bce - b0)
+    const double xce_hi = win ? wc.qmax / xce : 0.0, xce_lo = win ? wc.qmin / xce : 0.0;
     // byte selectors of the two transpose steps (v_perm: bytes 0-3 this
     // lane's dword, 4-7 the partner's): step 1 pairs lanes j, j ^ 1 (even
     // lanes keep bytes 0 and 2 of both, odd lanes bytes 1 and 3), step 2
@@ -878,13 +879,14 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
                   if (!NN) q1 = max64(q1, wc.qmin);
                   wa.A[1] = fma(q1, q1, wa.A[1]);
                   wa.PL[1] = fma(x, q1, wa.PL[1]);
-                  const double t = x * xce;
-                  const double d1 = max64z(t - wc.qmax);
-                  wa.CE[0] = fma(d1, d1, wa.CE[0]);
-                  if (!NN) {
-                    const double d2 = min64z(t - wc.qmin);
-                    wa.CE[0] = fma(d2, d2, wa.CE[0]);
-                  }
+                  // clipping error at bce: (x - x clamped to [qmin, qmax]
+                  // 2^(b0 - bce))^2, in units scaled by 2^(2 (b0 - bce))
+                  // (exactly those of (t - qmax)^+ and (t - qmin)^- with
+                  // t = x 2^(bce - b0), scaled back below)
+                  double xcl = min64(x, xce_hi);
+                  if (!NN) xcl = max64(xcl, xce_lo);
+                  const double e = x - xcl;
+                  wa.CE[0] = fma(e, e, wa.CE[0]);
                   c[jj] = (int)(PJ ? q1 : q0);
                   if (PJ == 0 && !C0) c[jj] = min(c[jj], qmax);
                 }
@@ -932,6 +934,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       wa.PL[0] *= up;
       wa.PL[1] *= up;
       wa.V2 *= up * up;
+      wa.CE[0] *= xce * xce;
       win_write_partials_int(wa, 1, bid, a.part_i, a.part_f, wsh);
     }
     double mn = INFINITY, mx = -INFINITY;
