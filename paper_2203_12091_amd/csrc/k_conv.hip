@@ -801,7 +801,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     const FlsU& u = ws.u;
     const bool win = ws.verdict == 0;
     const int pj = pred_pick(ws, *a.fmt_win);
-    const int qmax = (int)u.qmax;
+    const int qmax = (int)u.qmax, qmin = (int)u.qmin;
     const unsigned xorw = u.sign ? 0u : 0x80808080u;
     WinCtx wc;
     if (win) wc = win_ctx(u, ws);
@@ -813,7 +813,12 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     // rne(x), the second candidate's rne(2 x), the clipping bound's
     // argument x 2^(bce - b0).  Sums of x q and x^2 are those of W q and W^2
     // scaled by 2^(b0 - sigma) and its square, exactly (every term keeps its
-    // bits); they are scaled back before the block reduction.
+    // bits); they are scaled back before the block reduction.  In windows
+    // with negative values the second candidate's code (and the first's when
+    // it can saturate) comes from the low bits of x plus a rounding constant,
+    // clamped as an integer by one median-of-three, then converted back (as
+    // measured, this form does not pay in the non-negative windows, whose
+    // clamps are one-sided).
     const double xs = win ? wc.cj[0] : 1.0;      // 2^(b0 - sigma)
     const double xce = win ? wc.cce / xs : 1.0;  // 2^(bce - b0)
     const double xce_hi = win ? wc.qmax / xce : 0.0, xce_lo = win ? wc.qmin / xce : 0.0;
@@ -860,35 +865,57 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
               if constexpr (WIN) {
                 if (ok) {
                   static_assert(kWindow == 2, "two window candidates");
-                  // a window with negative values (!NN) is never a ReLU
-                  // layer's (its values are >= 0, so is the previous call's
-                  // minimum): no max with the ReLU bound there; a prediction
-                  // that says otherwise is a miss anyway (its window's
-                  // variant differs from the actual one)
-                  double x = fma((double)v, Mc, Ac);
-                  if (NN) x = max64s(x, relo);
-                  wa.V2 = fma(x, x, wa.V2);
-                  double q0 = rint(x);
-                  if (C0) {
-                    q0 = min64(q0, wc.qmax);
-                    if (!NN) q0 = max64(q0, wc.qmin);
+                  if constexpr (NN) {
+                    double x = fma((double)v, Mc, Ac);
+                    x = max64s(x, relo);
+                    wa.V2 = fma(x, x, wa.V2);
+                    double q0 = rint(x);
+                    if (C0) q0 = min64(q0, wc.qmax);
+                    wa.A[0] = fma(q0, q0, wa.A[0]);
+                    wa.PL[0] = fma(x, q0, wa.PL[0]);
+                    const double q1 = min64(rint(x + x), wc.qmax);
+                    wa.A[1] = fma(q1, q1, wa.A[1]);
+                    wa.PL[1] = fma(x, q1, wa.PL[1]);
+                    // clipping error at bce: (x - x clamped to its range
+                    // [qmin, qmax] 2^(b0 - bce))^2, in units scaled by
+                    // 2^(2 (b0 - bce)) (exactly those of (t - qmax)^+ and
+                    // (t - qmin)^- with t = x 2^(bce - b0), scaled back
+                    // below); one-sided here
+                    const double e = x - min64(x, xce_hi);
+                    wa.CE[0] = fma(e, e, wa.CE[0]);
+                    int c0 = (int)q0;
+                    const int c1 = (int)q1;
+                    if (PJ == 0 && !C0) c0 = min(c0, qmax);
+                    c[jj] = PJ ? c1 : c0;
+                  } else {
+                    // a window with negative values is never a ReLU layer's
+                    // (its values are >= 0, so is the previous call's
+                    // minimum): no max with the ReLU bound here; a prediction
+                    // that says otherwise is a miss anyway (its window's
+                    // variant differs from the actual one)
+                    const double x = fma((double)v, Mc, Ac);
+                    wa.V2 = fma(x, x, wa.V2);
+                    double q0;
+                    int c0 = 0;
+                    if (C0) {
+                      c0 = med3i(rne_lo(x + kRne0), qmin, qmax);
+                      q0 = (double)c0;
+                    } else {
+                      q0 = rint(x);
+                      if (PJ == 0) c0 = min((int)q0, qmax);
+                    }
+                    wa.A[0] = fma(q0, q0, wa.A[0]);
+                    wa.PL[0] = fma(x, q0, wa.PL[0]);
+                    const int c1 = med3i(rne_lo(x + kRne1), qmin, qmax);
+                    const double q1 = (double)c1;
+                    wa.A[1] = fma(q1, q1, wa.A[1]);
+                    wa.PL[1] = fma(x, q1, wa.PL[1]);
+                    // clipping error at bce, two-sided
+                    const double xcl = max64(min64(x, xce_hi), xce_lo);
+                    const double e = x - xcl;
+                    wa.CE[0] = fma(e, e, wa.CE[0]);
+                    c[jj] = PJ ? c1 : c0;
                   }
-                  wa.A[0] = fma(q0, q0, wa.A[0]);
-                  wa.PL[0] = fma(x, q0, wa.PL[0]);
-                  double q1 = min64(rint(x + x), wc.qmax);
-                  if (!NN) q1 = max64(q1, wc.qmin);
-                  wa.A[1] = fma(q1, q1, wa.A[1]);
-                  wa.PL[1] = fma(x, q1, wa.PL[1]);
-                  // clipping error at bce: (x - x clamped to [qmin, qmax]
-                  // 2^(b0 - bce))^2, in units scaled by 2^(2 (b0 - bce))
-                  // (exactly those of (t - qmax)^+ and (t - qmin)^- with
-                  // t = x 2^(bce - b0), scaled back below)
-                  double xcl = min64(x, xce_hi);
-                  if (!NN) xcl = max64(xcl, xce_lo);
-                  const double e = x - xcl;
-                  wa.CE[0] = fma(e, e, wa.CE[0]);
-                  c[jj] = (int)(PJ ? q1 : q0);
-                  if (PJ == 0 && !C0) c[jj] = min(c[jj], qmax);
                 }
               }
             }

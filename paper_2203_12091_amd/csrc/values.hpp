@@ -46,6 +46,23 @@ __device__ inline double min64z(double a) {
   return r;
 }
 
+// Median of three (x clamped to [lo, hi] when lo <= hi) as one v_med3_i32.
+__device__ inline int med3i(int x, int lo, int hi) {
+  int r;
+  asm("v_med3_i32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(lo), "v"(hi));
+  return r;
+}
+
+// Rounding to nearest even by one addition: for |t| < 2^(51 - k),
+// t + 1.5 * 2^(52 - k) is rne(t 2^k) 2^-k + 1.5 * 2^(52 - k) exactly (the
+// sum's unit in the last place is 2^-k), and the low 32 bits of that double
+// are rne(t 2^k) as a two's-complement int when |rne(t 2^k)| < 2^31.
+__device__ inline int rne_lo(double t_plus_magic) {
+  return (int)(unsigned)__builtin_bit_cast(unsigned long long, t_plus_magic);
+}
+constexpr double kRne0 = 0x1.8p52;  // k = 0: rne(t)
+constexpr double kRne1 = 0x1.8p51;  // k = 1: rne(2 t)
+
 // Sticky device flags (vector atomic OR at device scope).
 __device__ inline void raise_flag(unsigned* flags, unsigned f) {
   __hip_atomic_fetch_or(flags, f, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
