@@ -172,6 +172,8 @@ CASES = [
 PRED_CASES = CASES + [
     (2, 3, 23, 21, 64, 7, 2, 3, True, True),
     (1, 3, 19, 17, 64, 7, 2, 3, False, False),
+    # ReLU (a non-negative window) over 128 x 128 tiles
+    (2, 64, 13, 11, 128, 1, 1, 0, True, True),
 ]
 
 
