@@ -532,7 +532,13 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       int cc = col < a.K ? col : a.K - 1;
       bptr[i] = a.w + (int64_t)cc * a.wrow;
     }
+    // Loads are unconditional (from a valid address when the element does
+    // not exist); the pad / zero value replaces them at the LDS store.  A
+    // select right after the load would let the compiler branch around the
+    // load and then wait at the join for the loads just issued, i.e. for
+    // the next slab before this slab's MFMAs.
     v4i regA[ACH], regB[BCH];
+    bool aok[ACH], bok[BCH];
     auto gload = [&](int kt) {
       // FAST64 walks the depth channel chunk by channel chunk with the filter
       // taps innermost, so that consecutive slabs read neighbouring pixels of
@@ -549,8 +555,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
           int ih = ih0[i] + r, iw = iw0[i] + s;
           bool ok = aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
           const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 + kc * 16 : 0);
-          const v4i t = *reinterpret_cast<const v4i*>(p);
-          regA[i] = ok ? t : padv;
+          regA[i] = *reinterpret_cast<const v4i*>(p);
+          aok[i] = ok;
         }
       } else if constexpr (LOADER == LD_GEN16) {
         int k = k0 + kc * 16;
@@ -562,8 +568,8 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
           int ih = ih0[i] + r, iw = iw0[i] + s;
           bool ok = kin && aval[i] && ih >= 0 && ih < a.H && iw >= 0 && iw < a.W;
           const int8_t* p = abase[i] + (ok ? ((int64_t)ih * a.W + iw) * a.C + c0 : 0);
-          const v4i t = *reinterpret_cast<const v4i*>(p);
-          regA[i] = ok ? t : padv;
+          regA[i] = *reinterpret_cast<const v4i*>(p);
+          aok[i] = ok;
         }
       } else if constexpr (LOADER == LD_RGB8) {
         // filters re-laid as [r][s < 8][c]: chunk q = 4 kt + kc is filter
@@ -589,6 +595,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
             }
           }
           regA[i] = v;
+          aok[i] = true;
         }
       } else {  // LD_RGB4: four 4-byte pixels per 16-byte chunk
 #pragma unroll
@@ -607,23 +614,25 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
             v[j] = word;
           }
           regA[i] = v;
+          aok[i] = true;
         }
       }
 #pragma unroll
       for (int i = 0; i < BCH; ++i) {
         const int k = k0 + kc * 16;
         const bool kin = LOADER != LD_GEN16 || k < a.kdepth;
-        const v4i t = *reinterpret_cast<const v4i*>(bptr[i] + (kin ? k : 0));
-        regB[i] = kin ? t : v4i{0, 0, 0, 0};
+        regB[i] = *reinterpret_cast<const v4i*>(bptr[i] + (kin ? k : 0));
+        bok[i] = kin;
       }
     };
     auto lstore = [&](int buf) {
 #pragma unroll
       for (int i = 0; i < ACH; ++i)
-        *reinterpret_cast<v4i*>(&As[buf][lds_off((tid >> 2) + 64 * i, kc)]) = regA[i];
+        *reinterpret_cast<v4i*>(&As[buf][lds_off((tid >> 2) + 64 * i, kc)]) = aok[i] ? regA[i] : padv;
 #pragma unroll
       for (int i = 0; i < BCH; ++i)
-        *reinterpret_cast<v4i*>(&Bs[buf][lds_off((tid >> 2) + 64 * i, kc)]) = regB[i];
+        *reinterpret_cast<v4i*>(&Bs[buf][lds_off((tid >> 2) + 64 * i, kc)]) =
+            bok[i] ? regB[i] : v4i{0, 0, 0, 0};
     };
     gload(0);
     epi_loads();
