@@ -539,6 +539,7 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     // the next slab before this slab's MFMAs.
     v4i regA[ACH], regB[BCH];
     bool aok[ACH], bok[BCH];
+    int rgb_d[ACH];  // LD_RGB8: dword shift of the loaded pixels (0 inside)
     auto gload = [&](int kt) {
       // FAST64 walks the depth channel chunk by channel chunk with the filter
       // taps innermost, so that consecutive slabs read neighbouring pixels of
@@ -574,27 +575,22 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
       } else if constexpr (LOADER == LD_RGB8) {
         // filters re-laid as [r][s < 8][c]: chunk q = 4 kt + kc is filter
         // row q / 2, taps 4 (q % 2) .. + 3, i.e. four neighbouring pixels of
-        // one input row -- one 16-byte load away from the image borders
-        // (the taps past S have zero weights: their pixels only need to be
-        // readable).  Rows past R are zero filter rows.
+        // one input row: one 16-byte load of the four pixels from column
+        // iw clamped to [0, W - 4] (W >= 4); at the image borders the LDS
+        // store shifts them by d = iw - that column and pads the pixels
+        // outside the row (the taps past S have zero weights: their pixels
+        // only need to be readable).  Rows past R are zero filter rows; a
+        // row outside the image is all padding (d = 8).
         const int q = kt * 4 + kc;
         const int r = q >> 1, s0 = (q & 1) * 4;
 #pragma unroll
         for (int i = 0; i < ACH; ++i) {
-          v4i v = padv;
           const int ih = ih0[i] + r, iw = iw0[i] + s0;
-          if (aval[i] && r < a.R && ih >= 0 && ih < a.H) {
-            const int8_t* rowp = abase[i] + (int64_t)ih * a.W * 4;
-            if (iw >= 0 && iw + 3 < a.W) {
-              v = *reinterpret_cast<const v4i_a4*>(rowp + iw * 4);
-            } else {
-#pragma unroll
-              for (int j = 0; j < 4; ++j)
-                if (s0 + j < a.S && iw + j >= 0 && iw + j < a.W)
-                  v[j] = *reinterpret_cast<const int*>(rowp + (iw + j) * 4);
-            }
-          }
-          regA[i] = v;
+          const bool rowok = aval[i] && r < a.R && ih >= 0 && ih < a.H;
+          const int iwc = min(max(iw, 0), a.W - 4);
+          const int64_t off = rowok ? ((int64_t)ih * a.W + iwc) * 4 : 0;
+          regA[i] = *reinterpret_cast<const v4i_a4*>(abase[i] + off);
+          rgb_d[i] = rowok ? iw - iwc : 8;
           aok[i] = true;
         }
       } else {  // LD_RGB4: four 4-byte pixels per 16-byte chunk
@@ -627,8 +623,23 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     };
     auto lstore = [&](int buf) {
 #pragma unroll
-      for (int i = 0; i < ACH; ++i)
-        *reinterpret_cast<v4i*>(&As[buf][lds_off((tid >> 2) + 64 * i, kc)]) = aok[i] ? regA[i] : padv;
+      for (int i = 0; i < ACH; ++i) {
+        v4i v = aok[i] ? regA[i] : padv;
+        if constexpr (LOADER == LD_RGB8) {
+          const int d = rgb_d[i];
+          if (d != 0) {  // image border or missing row (no loads in here)
+            v4i o;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              const int m = j + d;
+              const int pk = m <= 0 ? v[0] : (m == 1 ? v[1] : (m == 2 ? v[2] : v[3]));
+              o[j] = (m >= 0 && m < 4) ? pk : padw;
+            }
+            v = o;
+          }
+        }
+        *reinterpret_cast<v4i*>(&As[buf][lds_off((tid >> 2) + 64 * i, kc)]) = v;
+      }
 #pragma unroll
       for (int i = 0; i < BCH; ++i)
         *reinterpret_cast<v4i*>(&Bs[buf][lds_off((tid >> 2) + 64 * i, kc)]) =
@@ -1026,7 +1037,7 @@ __global__ void k_rgb8_weights(const int8_t* w, int K, int R, int S, int wrow, i
 // The padded RGB layout with filter rows of at most 8 taps: re-lay the
 // filters into the handle's buffer and switch to the 16-byte pixel loader.
 static void rgb8_setup(const Ctx& c, const fxpq_conv_desc& d, ConvArgs& a, int& loader) {
-  if (loader != LD_RGB4 || d.s > 8 || !c.sc.rgb_w) return;
+  if (loader != LD_RGB4 || d.s > 8 || d.w < 4 || !c.sc.rgb_w) return;
   const int wrow8 = (d.r * 32 + 63) / 64 * 64;
   if ((size_t)d.k * wrow8 > kRgbWBytes) return;
   const int64_t n = (int64_t)d.k * wrow8;
