@@ -834,11 +834,11 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
     // argument x 2^(bce - b0).  Sums of x q and x^2 are those of W q and W^2
     // scaled by 2^(b0 - sigma) and its square, exactly (every term keeps its
     // bits); they are scaled back before the block reduction.  In windows
-    // with negative values the second candidate's code (and the first's when
-    // it can saturate) comes from the low bits of x plus a rounding constant,
-    // clamped as an integer by one median-of-three, then converted back (as
-    // measured, this form does not pay in the non-negative windows, whose
-    // clamps are one-sided).
+    // with negative values whose first candidate cannot saturate, the second
+    // candidate's code comes from the low bits of x plus a rounding
+    // constant, clamped as an integer by one median-of-three, then converted
+    // back (as measured, this form does not pay in the non-negative windows,
+    // whose clamps are one-sided).
     const double xs = win ? wc.cj[0] : 1.0;      // 2^(b0 - sigma)
     const double xce = win ? wc.cce / xs : 1.0;  // 2^(bce - b0)
     const double xce_hi = win ? wc.qmax / xce : 0.0, xce_lo = win ? wc.qmin / xce : 0.0;
@@ -915,19 +915,26 @@ __global__ __launch_bounds__(256, MINW) void k_qconv(ConvArgs a) {
                     // variant differs from the actual one)
                     const double x = fma((double)v, Mc, Ac);
                     wa.V2 = fma(x, x, wa.V2);
-                    double q0;
-                    int c0 = 0;
+                    double q0, q1;
+                    int c0 = 0, c1;
                     if (C0) {
-                      c0 = med3i(rne_lo(x + kRne0), qmin, qmax);
-                      q0 = (double)c0;
+                      // the first candidate saturates: x is not bounded by
+                      // the codes' range (the rounding constant's int view
+                      // needs |2 x| < 2^31), so both codes are clamped in fp64
+                      q0 = max64(min64(rint(x), wc.qmax), wc.qmin);
+                      q1 = max64(min64(rint(x + x), wc.qmax), wc.qmin);
+                      c0 = (int)q0;
+                      c1 = (int)q1;
                     } else {
+                      // every value of a hit lies within [qmin - 1/2,
+                      // qmax + 1/2] at the first candidate's step
                       q0 = rint(x);
                       if (PJ == 0) c0 = min((int)q0, qmax);
+                      c1 = med3i(rne_lo(x + kRne1), qmin, qmax);
+                      q1 = (double)c1;
                     }
                     wa.A[0] = fma(q0, q0, wa.A[0]);
                     wa.PL[0] = fma(x, q0, wa.PL[0]);
-                    const int c1 = med3i(rne_lo(x + kRne1), qmin, qmax);
-                    const double q1 = (double)c1;
                     wa.A[1] = fma(q1, q1, wa.A[1]);
                     wa.PL[1] = fma(x, q1, wa.PL[1]);
                     // clipping error at bce, two-sided

@@ -60,7 +60,6 @@ __device__ inline int med3i(int x, int lo, int hi) {
 __device__ inline int rne_lo(double t_plus_magic) {
   return (int)(unsigned)__builtin_bit_cast(unsigned long long, t_plus_magic);
 }
-constexpr double kRne0 = 0x1.8p52;  // k = 0: rne(t)
 constexpr double kRne1 = 0x1.8p51;  // k = 1: rne(2 t)
 
 // Sticky device flags (vector atomic OR at device scope).

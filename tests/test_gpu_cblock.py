@@ -66,14 +66,14 @@ class Case:
     """Seeded conv + epilogue operands (host), uploaded on demand."""
 
     def __init__(self, N, Cin, H, W, K, R, stride, pad, in_signed, relu, seed,
-                 kind="normal", fl_scale=15):
+                 kind="normal", fl_scale=15, fl_in=5, fl_w=9):
         self.N, self.Cin, self.H, self.W = N, Cin, H, W
         self.K, self.R, self.stride, self.pad = K, R, stride, pad
         self.in_signed = in_signed
         lo, hi = (-128, 127) if in_signed else (0, 255)
         self.xc = synth.integers(seed, "cb-x", (N, Cin, H, W), lo, hi)
         self.wc = synth.integers(seed, "cb-w", (K, Cin, R, R), -128, 127)
-        self.fl_in, self.fl_w, self.fl_b, self.fl_a1, self.fl_a2 = 5, 9, 11, fl_scale, fl_scale
+        self.fl_in, self.fl_w, self.fl_b, self.fl_a1, self.fl_a2 = fl_in, fl_w, 11, fl_scale, fl_scale
         g = synth.rng_for(seed, "cb-epi")
         self.bias = g.integers(-2 ** 18, 2 ** 18, K).astype(np.int32)
         self.a1 = g.integers(2 ** 13, 2 ** 15, K).astype(np.int32)
@@ -363,4 +363,37 @@ def test_cblock_predicted(fx, h, orc, case):
         if max(FL_LO, beta_nosat(4 * v, s, wl, osg)) != b0:
             assert int(host(miss)[0]) == 1
     assert hits >= 1, "no case decided by the window alone"
+    assert fx.sync_status(h) == 0
+
+
+def test_cblock_predicted_saturating(fx, h, orc):
+    """A predicted window whose first candidate saturates (no fractional
+    length in [FL_LO, FL_HI] keeps the values unclipped; coarse input and
+    weight scales, one pixel aligned with filter 77's signs): values reach
+    2^30 at the first candidate's step.  With the exact min / max and the
+    oracle's format as the prediction, a hit gives the oracle's format and
+    codes; the min / max end exact."""
+    import torch
+    c = Case(1, 512, 6, 6, 128, 1, 1, 0, True, False, seed=91, kind="outlier", fl_scale=14,
+             fl_in=-8, fl_w=-8).upload(fx, h)
+    v, s = c.oracle_values(orc)
+    exact = (float(v.min()), float(v.max()))
+    assert max(abs(exact[0]), abs(exact[1])) * 2.0 ** (FL_LO - s) >= 2 ** 29
+    hits = 0
+    for wl in (8, 6):
+        note("cblock predicted saturating", wl)
+        ofl, osg, _ = orc.fl_search_i64(v, s, wl, orc.SIGN_AUTO, FL_LO, FL_HI)
+        assert beta_nosat(v, s, wl, osg) < FL_LO
+        mm = torch.tensor(list(exact), dtype=torch.float64, device=DEV)
+        miss = torch.zeros(1, dtype=torch.int32, device=DEV)
+        out = fmt_dev(wl, ofl, osg)
+        y = c.predicted(fx, h, wl, mm, out, miss)
+        m = int(host(miss)[0])
+        assert m in (0, 2), m
+        if m == 0:
+            hits += 1
+            assert fmt_host(out) == (wl, ofl, osg, 0)
+            assert np.array_equal(decode8(host(y), osg == 0), orc.quantize_i64(v, s, wl, ofl, osg))
+        assert tuple(host(mm)) == exact
+    assert hits >= 1
     assert fx.sync_status(h) == 0
