@@ -292,15 +292,27 @@ __global__ __launch_bounds__(kThreads) void k_layer_error(const float* ref, cons
   const int64_t gtid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   double sse = 0.0, mn = INFINITY, mx = -INFINITY, s1 = 0.0, s2 = 0.0;
-  for (int64_t i = gtid; i < n; i += stride) {
-    double r = ref[i];
-    double d = r - (code_at<CT>(codes, i) + off) * step;
+  auto add = [&](double r, double c) {
+    const double d = r - (c + off) * step;
     sse = fma(d, d, sse);
     mn = fmin(mn, r);
     mx = fmax(mx, r);
     s1 += r;
     s2 = fma(r, r, s2);
+  };
+  // four grid strides per iteration: their loads are issued together
+  int64_t i = gtid;
+  for (; i + 3 * stride < n; i += 4 * stride) {
+    double r[4], c[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      r[k] = ref[i + k * stride];
+      c[k] = code_at<CT>(codes, i + k * stride);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) add(r[k], c[k]);
   }
+  for (; i < n; i += stride) add(ref[i], code_at<CT>(codes, i));
   sse = block_reduce(sse, OpAddD(), sh);
   mn = block_reduce(mn, OpMin(), sh);
   mx = block_reduce(mx, OpMax(), sh);
@@ -362,6 +374,32 @@ __global__ __launch_bounds__(kThreads) void k_maxpool(const int8_t* x, int n, in
     } best;
 #pragma unroll
     for (int j = 0; j < 16; ++j) best.b[j] = -128;
+    if (VEC == 16 && ks == 3) {
+      // 3x3 windows: the nine loads issued together (a tap outside the image
+      // reads the window's clamped pixel and is then left out), so that the
+      // thread waits for one round trip instead of nine
+      int4 v[9];
+      unsigned okm = 0;
+#pragma unroll
+      for (int r = 0; r < 3; ++r) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q) {
+          const int ih = oh * stride - pad + r, iw = ow * stride - pad + q;
+          const bool ok = ih >= 0 && ih < h && iw >= 0 && iw < w;
+          const int ihc = min(max(ih, 0), h - 1), iwc = min(max(iw, 0), w - 1);
+          v[3 * r + q] = *reinterpret_cast<const int4*>(
+              x + (((int64_t)b * h + ihc) * w + iwc) * ch + (int64_t)g * VEC);
+          okm |= ok ? 1u << (3 * r + q) : 0u;
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < 9; ++k) {
+        if (!((okm >> k) & 1u)) continue;
+        const int8_t* pv = reinterpret_cast<const int8_t*>(&v[k]);
+#pragma unroll
+        for (int j = 0; j < 16; ++j) best.b[j] = pv[j] > best.b[j] ? pv[j] : best.b[j];
+      }
+    } else
     for (int r = 0; r < ks; ++r) {
       int ih = oh * stride - pad + r;
       if (ih < 0 || ih >= h) continue;
