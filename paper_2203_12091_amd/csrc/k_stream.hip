@@ -441,7 +441,17 @@ __global__ __launch_bounds__(kThreads) void k_avgpool(const int8_t* x, const fxp
     int64_t b = idx / ch;
     int64_t s = 0;
     const int8_t* p = x + b * hw * ch + c;
-    for (int q = 0; q < hw; ++q) s += (int64_t)p[(int64_t)q * ch] + off;
+    // seven pixels per step, their loads issued together (an exact integer
+    // sum: the order does not matter)
+    int q = 0;
+    for (; q + 7 <= hw; q += 7) {
+      int v[7];
+#pragma unroll
+      for (int k = 0; k < 7; ++k) v[k] = p[(int64_t)(q + k) * ch];
+#pragma unroll
+      for (int k = 0; k < 7; ++k) s += (int64_t)v[k] + off;
+    }
+    for (; q < hw; ++q) s += (int64_t)p[(int64_t)q * ch] + off;
     y[idx] = s * recip;
   }
 }
